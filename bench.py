@@ -1,0 +1,184 @@
+"""Throughput of the packed causal long convolution on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+
+A step is one pass of the whole hot path over one batch: the filter spectra of
+the batch's size classes (rubiconv_filter_spectrum) and the packed convolution
+(rubiconv_packed_conv), on inputs already resident in HBM.  The plan (document
+table, size classes, twiddles) is built once per batch and shared by every layer,
+so it is built before the timed region and timed separately.
+
+Prints one JSON line: value = B*N*D / seconds per step / 1e6 (Mtokens*channels/s),
+the roofline of the dominant kernel (its compulsory bytes per launch over its
+average duration, timed with HIP events on the stream it runs on) and the CPU
+oracle timed on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, published
+FP32_VALU_TFLOPS = 157.3
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2, help="workload index (2 = N=16384, D=1024)")
+    ap.add_argument("--n1", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def kernel_bytes(info, W, plan):
+    """Compulsory HBM bytes per launch of each kernel: its inputs read once and its
+    outputs written once.  Grids are complex fp32 with two channels per value (4 B
+    per grid point and channel); a spectrum point holds S and Df for a channel pair
+    (8 B per point and channel)."""
+    D, G, Gc, n1 = W.D, info["grid_points"], info["class_points"], info["n1"]
+    sx = 2 if W.x_dtype == "bf16" else 4
+    sy = 2 if W.y_dtype == "bf16" else 4
+    tok = W.B * W.N * D
+    ms = [int(m) for m in plan.doc_table()[:, 4]]
+    classes = sorted(set(ms))
+    taps = [min(W.L, (n1 * m + 1) // 2) for m in classes]
+    spec_docs = sum((n1 // 2 + 1) * m for m in ms)
+    spec_cls = sum((n1 // 2 + 1) * m for m in classes)
+    return {
+        "col_fwd": tok * sx + 4 * G * D,
+        "row_conv": 8 * G * D + 8 * spec_docs * D,
+        "col_inv": 4 * G * D + tok * sy,
+        "filter_transpose": 8 * D * max(taps),
+        "filter_col_fwd": 4 * D * sum(taps) + 4 * Gc * D,
+        "filter_row_spec": 4 * Gc * D + 8 * spec_cls * D,
+    }
+
+
+def cpu_baseline(W, target_s):
+    """The oracle's per-document FFT variant (the parity reference at this size) on a
+    sample of channels of the same batch."""
+    import oracle
+    threads = min(16, os.cpu_count() or 1)
+
+    def run(nch):
+        x = np.ascontiguousarray(W.x[:, :, :nch])
+        k = np.ascontiguousarray(W.filters[:nch])
+        t0 = time.perf_counter()
+        oracle.conv_fft(x, k, W.cu_seqlens, threads=threads)
+        return time.perf_counter() - t0
+
+    probe = min(8, W.D)
+    t_probe = run(probe)
+    nch = int(max(probe, min(W.D, round(probe * target_s / max(t_probe, 1e-3)))))
+    t = run(nch) if nch != probe else t_probe
+    return {"value": W.B * W.N * nch / t / 1e6, "unit": "Mtokens*channels/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"per-document radix-2 FFT variant (fp64), all {W.B} rows x {W.N} tokens, "
+                      f"{nch} of {W.D} channels, {t:.2f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the convolution shards over channels with no exchange; see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2605_08451_amd as rc
+    import workloads as wl
+
+    dev = torch.device("cuda:0")
+    W = wl.make_config(args.config)
+    if W.x_dtype == "bf16":
+        x = torch.from_numpy(W.x_bits.view(np.int16)).view(torch.bfloat16).to(dev)
+    else:
+        x = torch.from_numpy(W.x).to(dev)
+    k = torch.from_numpy(W.filters).to(dev)
+
+    t0 = time.perf_counter()
+    plan = rc.Plan(W.cu_seqlens, N=W.N, D=W.D, L=W.L, x_dtype=W.x_dtype, y_dtype=W.y_dtype,
+                   n1=args.n1)
+    plan_ms = (time.perf_counter() - t0) * 1e3
+    info = plan.info()
+    ws = plan.new_workspace(dev)
+    spec = plan.new_spectrum(dev)
+    y = torch.empty_like(x) if W.y_dtype == W.x_dtype else torch.empty(
+        x.shape, dtype=torch.float32 if W.y_dtype == "f32" else torch.bfloat16, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        rc.filter_spectrum(plan, k, spectrum=spec, workspace=ws, stream=stream)
+        rc.packed_conv(plan, x, spec, y=y, workspace=ws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms = e0.elapsed_time(e1) / args.steps
+
+    # per-kernel durations: HIP events the library records around each of its kernels
+    plan.profile_start(2 * args.steps)
+    for _ in range(args.steps):
+        step()
+    kt = plan.profile_read()
+    plan.profile_start(0)
+    kb = kernel_bytes(info, W, plan)
+    per_kernel = {n: {"launches": c, "avg_us": 1e3 * tot / c,
+                      "GBps": kb.get(n, 0) / (tot / c * 1e-3) / 1e9}
+                  for n, (c, tot) in kt.items()}
+    dom = max(kt, key=lambda n: kt[n][1])
+    dom_us = per_kernel[dom]["avg_us"]
+    achieved = kb[dom] / (dom_us * 1e-6) / 1e9
+
+    tok_ch = W.B * W.N * W.D
+    sx = 2 if W.x_dtype == "bf16" else 4
+    sy = 2 if W.y_dtype == "bf16" else 4
+    min_bytes = tok_ch * (sx + sy) + W.D * W.L * 8
+    value = tok_ch / (ms * 1e-3) / 1e6
+    out = {
+        "metric": "packed-conv Mtokens*channels/s at N=16384,D=1024; % HBM roofline",
+        "value": round(value, 1),
+        "unit": "Mtokens*channels/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": wl.CONFIG_NAMES[args.config], "B": W.B, "N": W.N, "D": W.D,
+                   "L": W.L, "x_dtype": W.x_dtype, "y_dtype": W.y_dtype, "n1": info["n1"],
+                   "docs": info["n_docs"], "size_classes": info["n_classes"],
+                   "cu_seqlens_sha256_16": W.cu_hash(), "parallelism": "none (1 GPU)"},
+        "hbm_roofline_frac_step": round(min_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "step_min_bytes": min_bytes,
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": None, "bytes_per_launch": kb[dom], "avg_us": round(dom_us, 2)},
+        "kernels": {n: {kk: round(vv, 2) for kk, vv in d.items()} for n, d in per_kernel.items()},
+        "plan_ms": round(plan_ms, 3),
+        "wall_s_timed": round(wall, 4),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(W, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

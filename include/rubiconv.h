@@ -1,0 +1,189 @@
+/*
+ * rubiconv.h -- C ABI of the MI355X (gfx950) boundary-respecting causal long
+ * convolution over packed sequences (RubiConv, arXiv 2605.08451).
+ *
+ * The operation (problem statement, Section 1; depthwise causal convolution of
+ * Section 4.1, "Benchmarking protocol"; block-diagonal Toeplitz form of
+ * Section 3.2): every row b of x[B][N][D] is a concatenation of documents given
+ * by cu_seqlens.  For each document [s0, s1) of row b and each channel d,
+ *
+ *     y[b][t][d] = sum_{tau = 0}^{min(t - s0, L - 1)} k[d][tau] * x[b][t - tau][d],
+ *                  s0 <= t < s1,
+ *
+ * so no output mixes values across a document boundary and nothing wraps from
+ * the end of a row to its start.  Lags tau >= L contribute nothing.
+ *
+ * How it is computed (Algorithm 1, Theorem 2.1, Appendix "Implementation
+ * details"): every document i gets its own transform size P_i = N1 * m_i with
+ * P_i >= L_i + min(L_i, L) - 1 (the causal zero padding of Algorithm 1; m_i is
+ * rounded up to a 2^a 3^b 5^c size, which gives the identical exact result).
+ * The document is laid out as an N1 x m_i grid in row-major order (time
+ * t = m_i*a + j), transformed by N1-point column DFTs, the per-document twiddle
+ * omega_{P_i}^{u*j}, and m_i-point row DFTs (the block-diagonal second DFT).
+ * Two real channels share one complex transform and are separated by conjugate
+ * symmetry (Appendix, "Optimizing dual real FFTs", Algorithm 3); the product
+ * with the filter spectrum is taken on the 2-D frequency grid; the inverse runs
+ * the same steps in reverse order, then the output is cut back to L_i.
+ *
+ * Conventions shared by every call:
+ *   - All device pointers are HIP device memory on the current device; host
+ *     pointers are ordinary process memory.  The caller owns every buffer it
+ *     passes; the library owns only the plan and the plan's device tables.
+ *   - Calls taking a stream enqueue work on it and return without waiting.
+ *     They never synchronise the device, never allocate device memory and
+ *     never print.  The plan may be used from several streams at once as long
+ *     as each call has its own workspace (and output).
+ *   - Every call returns a status; nothing is thrown across the ABI.  Argument
+ *     errors are detected on the host before anything is enqueued.
+ */
+#ifndef RUBICONV_H_
+#define RUBICONV_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct rubiconv_plan_s* rubiconv_plan_t; /* opaque, library-owned */
+
+typedef enum {
+    RUBICONV_F32 = 0,  /* IEEE float32 */
+    RUBICONV_BF16 = 1  /* bfloat16 (upper half of a float32); outputs rounded to nearest even */
+} rubiconv_dtype_t;
+
+typedef enum {
+    RUBICONV_OK = 0,
+    RUBICONV_ERR_ARG = 1,         /* null pointer, non-positive size, unknown dtype */
+    RUBICONV_ERR_SEQLENS = 2,     /* cu_seqlens row not 0 = c0 <= c1 <= ... <= c_max_docs = N */
+    RUBICONV_ERR_UNSUPPORTED = 3, /* valid request this build does not implement */
+    RUBICONV_ERR_ALLOC = 4,       /* host or device allocation for the plan failed */
+    RUBICONV_ERR_HIP = 5          /* a HIP call or kernel launch failed */
+} rubiconv_status_t;
+
+/*
+ * Build a plan from the document boundaries (Algorithm 1, the data-processing
+ * step, which depends only on the segment ids and is shared by every layer of a
+ * model; Appendix, "Precomputation of adaptive structures").
+ *
+ *   out             receives the plan handle (host pointer, not null).
+ *   B, N, D, L      rows, tokens per row, channels, filter taps (all >= 1).
+ *   max_docs        documents per row in cu_seqlens_host (>= 1).
+ *   cu_seqlens_host host int32 [B][max_docs + 1]: per row the prefix sums of the
+ *                   document lengths, c[0] = 0, non-decreasing, c[max_docs] = N.
+ *                   Equal neighbours are empty documents and are ignored, which
+ *                   lets rows with fewer documents be padded with N.
+ *   x_dtype,y_dtype element types of x and y for packed_conv.
+ *   n1              column size N1 of the grid (the paper's k): 0 picks the
+ *                   default (256); otherwise 64 or 256.
+ *
+ * The plan copies what it needs; cu_seqlens_host may be freed on return.  Plan
+ * creation allocates device memory and copies the document and twiddle tables
+ * synchronously (it is not a stream-ordered call).
+ * Errors: RUBICONV_ERR_ARG, RUBICONV_ERR_SEQLENS, RUBICONV_ERR_UNSUPPORTED
+ * (n1 not supported, or a document so long that its row DFT would exceed the
+ * largest supported size), RUBICONV_ERR_ALLOC, RUBICONV_ERR_HIP.
+ */
+rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L, int max_docs,
+                                const int32_t* cu_seqlens_host, rubiconv_dtype_t x_dtype,
+                                rubiconv_dtype_t y_dtype, int n1);
+
+/* Release a plan and its device tables (null is ignored).  Work already
+ * enqueued that uses the plan must have finished. */
+void rubiconv_plan_destroy(rubiconv_plan_t plan);
+
+/* Bytes of the device buffer that holds the filter spectra of a plan (one per
+ * distinct transform size of the plan). 0 for a null plan. */
+size_t rubiconv_spectrum_bytes(rubiconv_plan_t plan);
+
+/* Bytes of device scratch that filter_spectrum and packed_conv need.  A single
+ * buffer of this size serves both calls (not at the same time). */
+size_t rubiconv_workspace_bytes(rubiconv_plan_t plan);
+
+/*
+ * Transform the filters into the plan's spectra (the filter side of
+ * Algorithm 3: the filter is padded to each transform size, transformed with
+ * the same column/twiddle/row steps as the data and separated by conjugate
+ * symmetry; the 1/P_i scale of the inverse is folded in).
+ *
+ *   filters    device float32 [D][L], row-major (channel d's taps contiguous).
+ *   spectrum   device buffer of rubiconv_spectrum_bytes(plan), 256-byte aligned,
+ *              written completely; its layout is private to the library.
+ *   workspace  device buffer of rubiconv_workspace_bytes(plan), 256-byte aligned.
+ *   stream     HIP stream the work is enqueued on.
+ * Errors: RUBICONV_ERR_ARG (null plan or pointer, misaligned buffer),
+ * RUBICONV_ERR_HIP (launch failure).
+ */
+rubiconv_status_t rubiconv_filter_spectrum(rubiconv_plan_t plan, const float* filters,
+                                           void* spectrum, void* workspace, hipStream_t stream);
+
+/*
+ * The packed convolution y = conv(x, k) defined at the top of this file.
+ *
+ *   x          device [B][N][D] of the plan's x_dtype, channels last, row-major.
+ *   spectrum   device spectra written by rubiconv_filter_spectrum with this plan.
+ *   y          device [B][N][D] of the plan's y_dtype; every element is written.
+ *              y must not overlap x, spectrum or workspace.
+ *   workspace  device buffer of rubiconv_workspace_bytes(plan), 256-byte aligned.
+ *   stream     HIP stream the work is enqueued on.
+ * Errors: RUBICONV_ERR_ARG, RUBICONV_ERR_HIP.
+ */
+rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, const void* spectrum,
+                                       void* y, void* workspace, hipStream_t stream);
+
+/* Summary of a plan (host call, no device work). */
+typedef struct {
+    int B, N, D, L;
+    int n1;             /* column size N1 of the grid */
+    int n_docs;         /* non-empty documents */
+    int n_classes;      /* distinct transform sizes P = N1 * m */
+    int n_pair_blocks;  /* channel pairs are processed in blocks of 16 */
+    int64_t grid_points;    /* sum over documents of P_i */
+    int64_t class_points;   /* sum over classes of P */
+    int64_t tokens;         /* sum over documents of L_i (= B * N) */
+} rubiconv_plan_info_t;
+
+rubiconv_status_t rubiconv_plan_info(rubiconv_plan_t plan, rubiconv_plan_info_t* info);
+
+/*
+ * The plan's document table, in row order: out is host int32 [cap][6] receiving
+ * (row, index of the document in its row, start, length, m_i, P_i) for each
+ * non-empty document; *n_docs receives the count (rows beyond cap are not
+ * written).  Used by tests to check the segment indexing exactly.
+ */
+rubiconv_status_t rubiconv_plan_doc_table(rubiconv_plan_t plan, int32_t* out, int cap,
+                                          int* n_docs);
+
+/*
+ * Stage timing (tracing; not for production loops).  After
+ * rubiconv_profile_start(plan, max_calls), each of the next max_calls calls of
+ * rubiconv_filter_spectrum / rubiconv_packed_conv with this plan records a HIP
+ * event on its stream before its first kernel and after every kernel, so each
+ * kernel's duration is measured on the stream it runs on.  rubiconv_profile_read
+ * waits for the recorded events and returns, per kernel name, the number of
+ * launches and their total milliseconds (host array of cap entries; *n receives
+ * the number of distinct kernels).  Profiling state belongs to the plan: use one
+ * stream and one thread while it is active.  max_calls = 0 stops profiling.
+ * Errors: RUBICONV_ERR_ARG, RUBICONV_ERR_ALLOC (event creation), RUBICONV_ERR_HIP.
+ */
+typedef struct {
+    char name[32];   /* kernel name, e.g. "col_fwd" */
+    int launches;
+    double total_ms;
+} rubiconv_kernel_time_t;
+
+rubiconv_status_t rubiconv_profile_start(rubiconv_plan_t plan, int max_calls);
+rubiconv_status_t rubiconv_profile_read(rubiconv_plan_t plan, rubiconv_kernel_time_t* out, int cap,
+                                        int* n);
+
+/* Static, human-readable name of a status code. */
+const char* rubiconv_status_string(rubiconv_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RUBICONV_H_ */

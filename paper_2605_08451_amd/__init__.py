@@ -1,0 +1,277 @@
+"""RubiConv on MI355X: boundary-respecting causal long convolution over packed sequences.
+
+A thin ctypes binding of ``librubiconv.so`` (C ABI in ``include/rubiconv.h``).  It
+only marshals arguments: every step of the convolution runs in the library's HIP
+kernels.  PyTorch supplies device memory and the stream; it is imported before the
+library is loaded so that both share one HIP runtime.
+
+    plan = Plan(cu_seqlens, N=x.shape[1], D=x.shape[2], L=filters.shape[1],
+                x_dtype=x.dtype, y_dtype=torch.bfloat16)
+    spec = filter_spectrum(plan, filters)          # filters: cuda float32 [D, L]
+    y = packed_conv(plan, x, spec)                 # x: cuda [B, N, D]
+
+The library must be built first (``python -m paper_2605_08451_amd.build``); if it
+is missing, loading fails loudly -- there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+import torch
+
+__all__ = ["Plan", "RubiconvError", "filter_spectrum", "packed_conv", "conv", "library_path",
+           "load_library", "EXPORTED_SYMBOLS"]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "librubiconv.so")
+_LIB = None
+
+F32, BF16 = 0, 1
+_STATUS = {0: "ok", 1: "invalid argument", 2: "invalid cu_seqlens", 3: "unsupported configuration",
+           4: "allocation failed", 5: "HIP error or no device"}
+
+#: Every function ``include/rubiconv.h`` declares.
+EXPORTED_SYMBOLS = ("rubiconv_plan", "rubiconv_plan_destroy", "rubiconv_spectrum_bytes",
+                    "rubiconv_workspace_bytes", "rubiconv_filter_spectrum", "rubiconv_packed_conv",
+                    "rubiconv_plan_info", "rubiconv_plan_doc_table", "rubiconv_profile_start",
+                    "rubiconv_profile_read", "rubiconv_status_string")
+
+
+class RubiconvError(RuntimeError):
+    def __init__(self, what: str, status: int):
+        super().__init__(f"{what}: {_STATUS.get(status, status)} (status {status})")
+        self.status = status
+
+
+class _PlanInfo(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int), ("N", ctypes.c_int), ("D", ctypes.c_int), ("L", ctypes.c_int),
+                ("n1", ctypes.c_int), ("n_docs", ctypes.c_int), ("n_classes", ctypes.c_int),
+                ("n_pair_blocks", ctypes.c_int), ("grid_points", ctypes.c_int64),
+                ("class_points", ctypes.c_int64), ("tokens", ctypes.c_int64)]
+
+
+class _KernelTime(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32), ("launches", ctypes.c_int),
+                ("total_ms", ctypes.c_double)]
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load_library():
+    """Load the in-tree ``librubiconv.so`` (raises if it has not been built)."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(f"{_LIB_PATH} is missing: build it with "
+                           "`python -m paper_2605_08451_amd.build` (no fallback exists)")
+    lib = ctypes.CDLL(_LIB_PATH)
+    vp, i32p, c_int, sz = ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.c_int, ctypes.c_size_t
+    lib.rubiconv_plan.argtypes = [ctypes.POINTER(vp), c_int, c_int, c_int, c_int, c_int, i32p,
+                                  c_int, c_int, c_int]
+    lib.rubiconv_plan.restype = c_int
+    lib.rubiconv_plan_destroy.argtypes = [vp]
+    lib.rubiconv_plan_destroy.restype = None
+    lib.rubiconv_spectrum_bytes.argtypes = [vp]
+    lib.rubiconv_spectrum_bytes.restype = sz
+    lib.rubiconv_workspace_bytes.argtypes = [vp]
+    lib.rubiconv_workspace_bytes.restype = sz
+    lib.rubiconv_filter_spectrum.argtypes = [vp, vp, vp, vp, vp]
+    lib.rubiconv_filter_spectrum.restype = c_int
+    lib.rubiconv_packed_conv.argtypes = [vp, vp, vp, vp, vp, vp]
+    lib.rubiconv_packed_conv.restype = c_int
+    lib.rubiconv_plan_info.argtypes = [vp, ctypes.POINTER(_PlanInfo)]
+    lib.rubiconv_plan_info.restype = c_int
+    lib.rubiconv_plan_doc_table.argtypes = [vp, i32p, c_int, ctypes.POINTER(c_int)]
+    lib.rubiconv_plan_doc_table.restype = c_int
+    lib.rubiconv_profile_start.argtypes = [vp, c_int]
+    lib.rubiconv_profile_start.restype = c_int
+    lib.rubiconv_profile_read.argtypes = [vp, ctypes.POINTER(_KernelTime), c_int,
+                                          ctypes.POINTER(c_int)]
+    lib.rubiconv_profile_read.restype = c_int
+    lib.rubiconv_status_string.argtypes = [c_int]
+    lib.rubiconv_status_string.restype = ctypes.c_char_p
+    _LIB = lib
+    return lib
+
+
+def _dtype_code(dt) -> int:
+    if dt in (torch.float32, "f32", "float32", F32):
+        return F32
+    if dt in (torch.bfloat16, "bf16", "bfloat16", BF16):
+        return BF16
+    raise ValueError(f"unsupported dtype {dt!r} (float32 or bfloat16)")
+
+
+def _torch_dtype(code: int):
+    return torch.float32 if code == F32 else torch.bfloat16
+
+
+def _check(status: int, what: str):
+    if status != 0:
+        raise RubiconvError(what, status)
+
+
+def _stream_handle(device, stream) -> int:
+    s = torch.cuda.current_stream(device) if stream is None else stream
+    return s.cuda_stream
+
+
+class Plan:
+    """Document table, size classes and twiddles for one batch of boundaries
+    (Algorithm 1's data processing; shared by every layer that sees this batch)."""
+
+    def __init__(self, cu_seqlens, N: int, D: int, L: int, x_dtype=torch.bfloat16,
+                 y_dtype=None, n1: int = 0):
+        lib = load_library()
+        if isinstance(cu_seqlens, torch.Tensor):
+            cu_seqlens = cu_seqlens.detach().cpu().numpy()
+        cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+        if cu.ndim == 1:
+            cu = cu[None]
+        if cu.ndim != 2 or cu.shape[1] < 2:
+            raise ValueError("cu_seqlens must be [B, max_docs + 1]")
+        self.B, self.max_docs = int(cu.shape[0]), int(cu.shape[1] - 1)
+        self.N, self.D, self.L = int(N), int(D), int(L)
+        self.x_dtype = _dtype_code(x_dtype)
+        self.y_dtype = self.x_dtype if y_dtype is None else _dtype_code(y_dtype)
+        self._h = ctypes.c_void_p()
+        self._lib = lib
+        _check(lib.rubiconv_plan(ctypes.byref(self._h), self.B, self.N, self.D, self.L,
+                                 self.max_docs, cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                 self.x_dtype, self.y_dtype, int(n1)), "rubiconv_plan")
+        self.cu_seqlens = cu.copy()
+
+    @property
+    def handle(self):
+        if not self._h:
+            raise RuntimeError("plan already destroyed")
+        return self._h
+
+    @property
+    def spectrum_bytes(self) -> int:
+        return int(self._lib.rubiconv_spectrum_bytes(self.handle))
+
+    @property
+    def workspace_bytes(self) -> int:
+        return int(self._lib.rubiconv_workspace_bytes(self.handle))
+
+    def info(self) -> dict:
+        inf = _PlanInfo()
+        _check(self._lib.rubiconv_plan_info(self.handle, ctypes.byref(inf)), "rubiconv_plan_info")
+        return {name: getattr(inf, name) for name, _ in _PlanInfo._fields_}
+
+    def doc_table(self) -> np.ndarray:
+        """int32 [n_docs, 6]: row, index in row, start, length, m_i, P_i."""
+        n = ctypes.c_int(0)
+        _check(self._lib.rubiconv_plan_doc_table(self.handle, None, 0, ctypes.byref(n)),
+               "rubiconv_plan_doc_table")
+        out = np.zeros((max(n.value, 1), 6), dtype=np.int32)
+        _check(self._lib.rubiconv_plan_doc_table(
+            self.handle, out.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n.value,
+            ctypes.byref(n)), "rubiconv_plan_doc_table")
+        return out[:n.value].copy()
+
+    def profile_start(self, max_calls: int):
+        """Time every kernel of the next ``max_calls`` library calls with HIP events."""
+        _check(self._lib.rubiconv_profile_start(self.handle, int(max_calls)),
+               "rubiconv_profile_start")
+
+    def profile_read(self) -> dict:
+        """{kernel name: (launches, total milliseconds)} of the profiled calls (waits)."""
+        out = (_KernelTime * 16)()
+        n = ctypes.c_int(0)
+        _check(self._lib.rubiconv_profile_read(self.handle, out, 16, ctypes.byref(n)),
+               "rubiconv_profile_read")
+        return {out[i].name.decode(): (out[i].launches, out[i].total_ms) for i in range(n.value)}
+
+    def new_spectrum(self, device) -> torch.Tensor:
+        return torch.empty(self.spectrum_bytes, dtype=torch.uint8, device=device)
+
+    def new_workspace(self, device) -> torch.Tensor:
+        return torch.empty(self.workspace_bytes, dtype=torch.uint8, device=device)
+
+    def close(self):
+        if self._h:
+            self._lib.rubiconv_plan_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _cuda_contig(t: torch.Tensor, name: str):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a CUDA (HIP) tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def filter_spectrum(plan: Plan, filters: torch.Tensor, spectrum: Optional[torch.Tensor] = None,
+                    workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Spectra of ``filters`` (cuda float32 [D, L]) for every size class of ``plan``."""
+    _cuda_contig(filters, "filters")
+    if filters.dtype != torch.float32 or tuple(filters.shape) != (plan.D, plan.L):
+        raise ValueError(f"filters must be float32 [{plan.D}, {plan.L}]")
+    dev = filters.device
+    if spectrum is None:
+        spectrum = plan.new_spectrum(dev)
+    if workspace is None:
+        workspace = plan.new_workspace(dev)
+    if spectrum.numel() * spectrum.element_size() < plan.spectrum_bytes:
+        raise ValueError("spectrum buffer too small")
+    if workspace.numel() * workspace.element_size() < plan.workspace_bytes:
+        raise ValueError("workspace buffer too small")
+    with torch.cuda.device(dev):
+        _check(plan._lib.rubiconv_filter_spectrum(plan.handle, filters.data_ptr(),
+                                                  spectrum.data_ptr(), workspace.data_ptr(),
+                                                  _stream_handle(dev, stream)),
+               "rubiconv_filter_spectrum")
+    return spectrum
+
+
+def packed_conv(plan: Plan, x: torch.Tensor, spectrum: torch.Tensor,
+                y: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                stream=None) -> torch.Tensor:
+    """y[b, t, d] = sum over the lags inside t's document of k[d, tau] x[b, t - tau, d]."""
+    _cuda_contig(x, "x")
+    if tuple(x.shape) != (plan.B, plan.N, plan.D) or x.dtype != _torch_dtype(plan.x_dtype):
+        raise ValueError(f"x must be {_torch_dtype(plan.x_dtype)} [{plan.B}, {plan.N}, {plan.D}]")
+    dev = x.device
+    if y is None:
+        y = torch.empty((plan.B, plan.N, plan.D), dtype=_torch_dtype(plan.y_dtype), device=dev)
+    _cuda_contig(y, "y")
+    if tuple(y.shape) != (plan.B, plan.N, plan.D) or y.dtype != _torch_dtype(plan.y_dtype):
+        raise ValueError("y has the wrong shape or dtype")
+    if workspace is None:
+        workspace = plan.new_workspace(dev)
+    if workspace.numel() * workspace.element_size() < plan.workspace_bytes:
+        raise ValueError("workspace buffer too small")
+    if spectrum.numel() * spectrum.element_size() < plan.spectrum_bytes:
+        raise ValueError("spectrum buffer too small")
+    with torch.cuda.device(dev):
+        _check(plan._lib.rubiconv_packed_conv(plan.handle, x.data_ptr(), spectrum.data_ptr(),
+                                              y.data_ptr(), workspace.data_ptr(),
+                                              _stream_handle(dev, stream)),
+               "rubiconv_packed_conv")
+    return y
+
+
+def conv(x: torch.Tensor, filters: torch.Tensor, cu_seqlens, y_dtype=None, n1: int = 0):
+    """One-shot convenience: plan, filter spectrum and convolution (allocates)."""
+    plan = Plan(cu_seqlens, N=x.shape[1], D=x.shape[2], L=filters.shape[1], x_dtype=x.dtype,
+                y_dtype=y_dtype, n1=n1)
+    ws = plan.new_workspace(x.device)
+    spec = filter_spectrum(plan, filters, workspace=ws)
+    y = packed_conv(plan, x, spec, workspace=ws)
+    torch.cuda.current_stream(x.device).synchronize()
+    plan.close()
+    return y

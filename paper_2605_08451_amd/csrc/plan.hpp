@@ -1,0 +1,39 @@
+// plan.hpp -- the plan's tables, as seen by the host builder and the kernels.
+//
+// A "segment" is one independent transform on the N1 x m grid: either a
+// document of the packed input (Algorithm 1: one block of the block-diagonal
+// second DFT per document) or one filter size class (the filter padded to that
+// class's transform size).  Segments of the same kind are laid out back to back
+// in a grid buffer; the kernels find their segment from a per-column or
+// per-row-task table.
+#pragma once
+
+#include <cstdint>
+
+namespace rubiconv {
+
+constexpr int kPairsPerBlock = 16;  // channel pairs per block: 16 * 8 B = 128 B of complex fp32
+constexpr int kMaxFactors = 14;     // radices of m (m <= 2048 has at most 11)
+constexpr int kMaxM = 2048;         // largest row DFT
+constexpr int kRowLdsBytes = 65536; // two ping-pong buffers of two rows each
+
+struct Seg {
+    int32_t row;       // source row of x (documents) / 0 (filter classes)
+    int32_t start;     // first token in the row / 0
+    int32_t len;       // tokens that are read (document length / filter taps kept)
+    int32_t m;         // row DFT size; P = N1 * m
+    int32_t P;
+    int32_t cls;       // size class
+    int64_t grid_off;  // first grid point of this segment in its grid buffer
+    int32_t tw_off;    // class twiddles: [tw_off, +N1) = w_P^r, [tw_off+N1, +m) = w_m^h
+    int32_t spec_off;  // class spectrum: first of (N1/2 + 1) * m points
+    int32_t col0;      // first global column index of this segment
+    int32_t task0;     // first global row-task index of this segment
+    int32_t spb;       // pairs per row task (16, or fewer for long rows)
+    int32_t nfac;      // radices of m, applied in order
+    int8_t fac[kMaxFactors];
+    int8_t pad_[2];
+};
+static_assert(sizeof(Seg) % 8 == 0, "Seg must stay 8-byte aligned in arrays");
+
+}  // namespace rubiconv

@@ -1,0 +1,156 @@
+// plan_build.cpp -- the data-processing step of Algorithm 1 as host tables.
+//
+// For every document i of length L_i the causal padding rule of Algorithm 1
+// asks for a transform of at least L_i + min(L_i, L) - 1 points that N1
+// divides.  The row DFT size m_i is the smallest 2^a 3^b 5^c number with
+// N1 * m_i >= L_i + min(L_i, L) - 1: any such size gives the same exact
+// convolution on [0, L_i) because the circular wrap of the padded product lands
+// only on positions >= L_i.  Documents with equal m_i share a size class and
+// one filter spectrum; that spectrum keeps Lh = min(L, floor((P + 1) / 2)) taps,
+// which covers every lag min(L_i, L) - 1 a document of the class can use and
+// still cannot wrap onto an output position < L_i (both follow from
+// P >= L_i + min(L_i, L) - 1).
+#include "plan_build.hpp"
+
+#include <algorithm>
+#include <cmath>
+#include <map>
+
+namespace rubiconv {
+
+int smooth_ceil(int v) {
+    if (v < 1) v = 1;
+    for (int n = v;; ++n) {
+        int k = n;
+        while (k % 2 == 0) k /= 2;
+        while (k % 3 == 0) k /= 3;
+        while (k % 5 == 0) k /= 5;
+        if (k == 1) return n;
+    }
+}
+
+namespace {
+
+// Radices of m in the order the row DFT applies them: 4s, then 2, 3s, 5s.
+int factorize(int m, int8_t* fac) {
+    int n = 0;
+    while (m % 4 == 0) { fac[n++] = 4; m /= 4; }
+    while (m % 2 == 0) { fac[n++] = 2; m /= 2; }
+    while (m % 3 == 0) { fac[n++] = 3; m /= 3; }
+    while (m % 5 == 0) { fac[n++] = 5; m /= 5; }
+    return m == 1 ? n : -1;
+}
+
+// Pairs per row task: two ping-pong buffers of two rows of m * spb complex
+// floats must fit the row pass's LDS budget.
+int pairs_per_task(int m) {
+    int spb = kPairsPerBlock;
+    while (spb > 1 && 4 * m * spb * 8 > kRowLdsBytes) spb /= 2;
+    return spb;
+}
+
+void push_twiddles(std::vector<float>& tw, int64_t count, int64_t period) {
+    const double two_pi = 6.283185307179586476925286766559;
+    for (int64_t r = 0; r < count; ++r) {
+        // forward root w_period^r = exp(-2 pi i r / period), angle reduced exactly
+        double a = two_pi * static_cast<double>(r % period) / static_cast<double>(period);
+        tw.push_back(static_cast<float>(std::cos(a)));
+        tw.push_back(static_cast<float>(-std::sin(a)));
+    }
+}
+
+}  // namespace
+
+BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_docs,
+                           const int32_t* cu, int x_dtype, int y_dtype, int n1) {
+    if (!out || !cu || B < 1 || N < 1 || D < 1 || L < 1 || max_docs < 1) return BuildError::kArg;
+    if (x_dtype < 0 || x_dtype > 1 || y_dtype < 0 || y_dtype > 1) return BuildError::kArg;
+    if (n1 == 0) n1 = 256;
+    int r = 0;
+    if (n1 == 64) r = 8;
+    else if (n1 == 256) r = 16;
+    else return BuildError::kUnsupported;
+    // Element offsets are 64-bit; per-row token indices are 32-bit.
+    if (static_cast<int64_t>(N) * D > (int64_t(1) << 40)) return BuildError::kUnsupported;
+
+    for (int b = 0; b < B; ++b) {
+        const int32_t* c = cu + static_cast<int64_t>(b) * (max_docs + 1);
+        if (c[0] != 0 || c[max_docs] != N) return BuildError::kSeqlens;
+        for (int k = 0; k < max_docs; ++k)
+            if (c[k + 1] < c[k] || c[k + 1] > N) return BuildError::kSeqlens;
+    }
+
+    HostPlan p;
+    p.B = B; p.N = N; p.D = D; p.L = L; p.max_docs = max_docs; p.n1 = n1; p.r = r;
+    p.x_dtype = x_dtype; p.y_dtype = y_dtype;
+    p.npb = ((D + 1) / 2 + kPairsPerBlock - 1) / kPairsPerBlock;
+
+    // documents and their row DFT sizes
+    std::map<int, int> class_of_m;
+    for (int b = 0; b < B; ++b) {
+        const int32_t* c = cu + static_cast<int64_t>(b) * (max_docs + 1);
+        for (int k = 0; k < max_docs; ++k) {
+            int len = c[k + 1] - c[k];
+            if (len == 0) continue;
+            int64_t need = static_cast<int64_t>(len) + std::min(len, L) - 1;
+            int64_t mmin = (need + n1 - 1) / n1;
+            if (mmin > kMaxM) return BuildError::kUnsupported;
+            int m = smooth_ceil(static_cast<int>(mmin));
+            if (m > kMaxM) return BuildError::kUnsupported;
+            Seg s{};
+            s.row = b; s.start = c[k]; s.len = len; s.m = m; s.P = n1 * m;
+            p.docs.push_back(s);
+            p.doc_index.push_back(k);
+            class_of_m[m] = 0;
+        }
+    }
+
+    // size classes, ascending m: twiddles, spectrum offsets, filter taps
+    for (auto& kv : class_of_m) {
+        int m = kv.first;
+        kv.second = static_cast<int>(p.classes.size());
+        Seg s{};
+        s.m = m; s.P = n1 * m; s.cls = kv.second;
+        s.len = static_cast<int32_t>(std::min<int64_t>(L, (static_cast<int64_t>(s.P) + 1) / 2));
+        s.tw_off = static_cast<int32_t>(p.tw.size() / 2);
+        push_twiddles(p.tw, n1, s.P);   // w_P^r, r < N1
+        push_twiddles(p.tw, m, m);      // w_m^h = w_P^(N1 h), h < m
+        s.spec_off = static_cast<int32_t>(p.spec_points);
+        p.spec_points += static_cast<int64_t>(n1 / 2 + 1) * m;
+        s.spb = pairs_per_task(m);
+        s.nfac = factorize(m, s.fac);
+        p.taps_max = std::max(p.taps_max, s.len);
+        p.classes.push_back(s);
+    }
+
+    // documents: class data, grid offsets, column and row-task tables
+    for (auto& s : p.docs) {
+        const Seg& c = p.classes[class_of_m[s.m]];
+        s.cls = c.cls; s.tw_off = c.tw_off; s.spec_off = c.spec_off;
+        s.spb = c.spb; s.nfac = c.nfac;
+        std::copy(c.fac, c.fac + kMaxFactors, s.fac);
+        s.grid_off = p.grid_points;
+        p.grid_points += s.P;
+        s.col0 = static_cast<int32_t>(p.doc_col_seg.size());
+        s.task0 = static_cast<int32_t>(p.doc_task_seg.size());
+        int idx = static_cast<int>(&s - p.docs.data());
+        p.doc_col_seg.insert(p.doc_col_seg.end(), s.m, idx);
+        p.doc_task_seg.insert(p.doc_task_seg.end(), (n1 / 2 + 1) * (kPairsPerBlock / s.spb), idx);
+        p.row_lds_docs = std::max(p.row_lds_docs, 4 * s.m * s.spb * 8);
+    }
+    for (auto& s : p.classes) {
+        s.grid_off = p.class_points;
+        p.class_points += s.P;
+        s.col0 = static_cast<int32_t>(p.cls_col_seg.size());
+        s.task0 = static_cast<int32_t>(p.cls_task_seg.size());
+        int idx = static_cast<int>(&s - p.classes.data());
+        p.cls_col_seg.insert(p.cls_col_seg.end(), s.m, idx);
+        p.cls_task_seg.insert(p.cls_task_seg.end(), (n1 / 2 + 1) * (kPairsPerBlock / s.spb), idx);
+        p.row_lds_classes = std::max(p.row_lds_classes, 4 * s.m * s.spb * 8);
+    }
+    push_twiddles(p.tw_n1, n1, n1);
+    *out = std::move(p);
+    return BuildError::kOk;
+}
+
+}  // namespace rubiconv

@@ -1,0 +1,41 @@
+// plan_build.hpp -- host-side construction of a plan's tables (no HIP calls).
+#pragma once
+
+#include <cstdint>
+#include <vector>
+
+#include "plan.hpp"
+
+namespace rubiconv {
+
+enum class BuildError { kOk, kArg, kSeqlens, kUnsupported };
+
+struct HostPlan {
+    int B = 0, N = 0, D = 0, L = 0, max_docs = 0, n1 = 0, r = 0;  // n1 = r * r
+    int x_dtype = 0, y_dtype = 0;
+    int npb = 0;                        // channel-pair blocks of kPairsPerBlock pairs
+    std::vector<Seg> docs;              // one per non-empty document, row order
+    std::vector<int32_t> doc_index;     // index of each document inside its row
+    std::vector<Seg> classes;           // one per distinct m, ascending m
+    std::vector<int32_t> doc_col_seg;   // global column -> document
+    std::vector<int32_t> doc_task_seg;  // global row task -> document
+    std::vector<int32_t> cls_col_seg;   // global column -> class
+    std::vector<int32_t> cls_task_seg;  // global row task -> class
+    std::vector<float> tw;              // complex pairs (re, im), per class: N1 then m entries
+    std::vector<float> tw_n1;           // complex pairs, w_N1^s for s < N1
+    int64_t grid_points = 0;            // sum over documents of P_i
+    int64_t class_points = 0;           // sum over classes of P
+    int64_t spec_points = 0;            // sum over classes of (N1/2 + 1) * m
+    int32_t taps_max = 0;               // largest number of filter taps any class keeps
+    int32_t row_lds_docs = 0;           // dynamic LDS bytes of the row pass (documents)
+    int32_t row_lds_classes = 0;        // same for the filter classes
+};
+
+// Smallest 2^a 3^b 5^c >= v (v >= 1).
+int smooth_ceil(int v);
+
+// Validates cu_seqlens and fills every table of *out.
+BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_docs,
+                           const int32_t* cu_seqlens, int x_dtype, int y_dtype, int n1);
+
+}  // namespace rubiconv

@@ -1,0 +1,326 @@
+// rubiconv.cpp -- the C ABI declared in include/rubiconv.h.
+//
+// rubiconv_plan validates the document boundaries and builds every table on the
+// host (plan_build.cpp), then uploads them in one device allocation.  The two
+// stream calls only enqueue kernels (kernels.hip) on the caller's stream.
+#include "rubiconv.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+
+#include "kernels.hpp"
+#include "plan_build.hpp"
+
+using rubiconv::BuildError;
+using rubiconv::HostPlan;
+using rubiconv::kPairsPerBlock;
+using rubiconv::LaunchTables;
+using rubiconv::Seg;
+
+struct rubiconv_plan_s {
+    HostPlan h;
+    void* dev = nullptr;  // all device tables, one allocation
+    bool device_ready = false;
+    LaunchTables doc_t{};
+    LaunchTables cls_t{};
+    int64_t grid_pb_stride = 0;  // float2 elements per pair block, document grid
+    int64_t cls_pb_stride = 0;   // same, filter-class grid
+    int64_t spec_pb_stride = 0;  // float2 elements per pair block, spectrum
+    size_t taps_bytes = 0;       // transposed filter taps (workspace head, filter call)
+    size_t spec_bytes = 0;
+    size_t ws_bytes = 0;
+    // stage timing (rubiconv_profile_start / _read)
+    static constexpr int kEventsPerCall = 4;  // before the first kernel + after each of <= 3
+    int prof_max = 0, prof_used = 0;
+    std::vector<hipEvent_t> prof_events;           // prof_max * kEventsPerCall
+    std::vector<std::vector<const char*>> prof_names;
+};
+
+namespace {
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) % kAlign) == 0; }
+
+rubiconv_status_t upload(rubiconv_plan_s* pl) {
+    const HostPlan& h = pl->h;
+    const size_t n_segs = h.docs.size() + h.classes.size();
+    size_t off = 0;
+    const size_t o_segs = off;       off = align_up(off + n_segs * sizeof(Seg));
+    const size_t o_dcol = off;       off = align_up(off + h.doc_col_seg.size() * 4);
+    const size_t o_dtask = off;      off = align_up(off + h.doc_task_seg.size() * 4);
+    const size_t o_ccol = off;       off = align_up(off + h.cls_col_seg.size() * 4);
+    const size_t o_ctask = off;      off = align_up(off + h.cls_task_seg.size() * 4);
+    const size_t o_tw = off;         off = align_up(off + h.tw.size() * 4);
+    const size_t o_twn = off;        off = align_up(off + h.tw_n1.size() * 4);
+    const size_t total = off;
+
+    std::vector<unsigned char> img(total, 0);
+    std::vector<Seg> segs(h.docs);
+    segs.insert(segs.end(), h.classes.begin(), h.classes.end());
+    std::memcpy(img.data() + o_segs, segs.data(), n_segs * sizeof(Seg));
+    std::memcpy(img.data() + o_dcol, h.doc_col_seg.data(), h.doc_col_seg.size() * 4);
+    std::memcpy(img.data() + o_dtask, h.doc_task_seg.data(), h.doc_task_seg.size() * 4);
+    std::memcpy(img.data() + o_ccol, h.cls_col_seg.data(), h.cls_col_seg.size() * 4);
+    std::memcpy(img.data() + o_ctask, h.cls_task_seg.data(), h.cls_task_seg.size() * 4);
+    std::memcpy(img.data() + o_tw, h.tw.data(), h.tw.size() * 4);
+    std::memcpy(img.data() + o_twn, h.tw_n1.data(), h.tw_n1.size() * 4);
+
+    int count = 0;
+    hipError_t e = hipGetDeviceCount(&count);
+    if (e == hipErrorNoDevice || (e == hipSuccess && count == 0)) {
+        (void)hipGetLastError();
+        return RUBICONV_OK;  // host-only plan: tables exist, stream calls report ERR_HIP
+    }
+    if (e != hipSuccess) return RUBICONV_ERR_HIP;
+    void* d = nullptr;
+    e = hipMalloc(&d, total);
+    if (e == hipErrorOutOfMemory) return RUBICONV_ERR_ALLOC;
+    if (e != hipSuccess) return RUBICONV_ERR_HIP;
+    e = hipMemcpy(d, img.data(), total, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(d);
+        return RUBICONV_ERR_HIP;
+    }
+    pl->dev = d;
+    unsigned char* base = static_cast<unsigned char*>(d);
+    const Seg* dsegs = reinterpret_cast<const Seg*>(base + o_segs);
+    const float2* tw = reinterpret_cast<const float2*>(base + o_tw);
+    const float2* twn = reinterpret_cast<const float2*>(base + o_twn);
+    pl->doc_t = LaunchTables{dsegs, reinterpret_cast<const int32_t*>(base + o_dcol),
+                             reinterpret_cast<const int32_t*>(base + o_dtask), tw, twn};
+    pl->cls_t = LaunchTables{dsegs + h.docs.size(), reinterpret_cast<const int32_t*>(base + o_ccol),
+                             reinterpret_cast<const int32_t*>(base + o_ctask), tw, twn};
+    pl->device_ready = true;
+    return RUBICONV_OK;
+}
+
+void destroy_events(rubiconv_plan_s* pl) {
+    for (hipEvent_t e : pl->prof_events) (void)hipEventDestroy(e);
+    pl->prof_events.clear();
+    pl->prof_names.clear();
+    pl->prof_max = pl->prof_used = 0;
+}
+
+// Records an event before a call's first kernel and after each kernel while
+// profiling slots remain; otherwise does nothing.
+struct StageRecorder {
+    rubiconv_plan_s* pl;
+    hipStream_t stream;
+    int slot = -1;
+    int k = 0;
+    StageRecorder(rubiconv_plan_s* p, hipStream_t s) : pl(p), stream(s) {
+        if (pl->prof_used < pl->prof_max) {
+            slot = pl->prof_used++;
+            pl->prof_names[slot].clear();
+            (void)hipEventRecord(pl->prof_events[slot * rubiconv_plan_s::kEventsPerCall], stream);
+        }
+    }
+    void mark(const char* name) {
+        if (slot < 0 || k + 1 >= rubiconv_plan_s::kEventsPerCall) return;
+        ++k;
+        (void)hipEventRecord(pl->prof_events[slot * rubiconv_plan_s::kEventsPerCall + k], stream);
+        pl->prof_names[slot].push_back(name);
+    }
+};
+
+}  // namespace
+
+extern "C" {
+
+rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L, int max_docs,
+                                const int32_t* cu_seqlens_host, rubiconv_dtype_t x_dtype,
+                                rubiconv_dtype_t y_dtype, int n1) {
+    if (!out) return RUBICONV_ERR_ARG;
+    *out = nullptr;
+    rubiconv_plan_s* pl = new (std::nothrow) rubiconv_plan_s();
+    if (!pl) return RUBICONV_ERR_ALLOC;
+    BuildError be = rubiconv::build_host_plan(&pl->h, B, N, D, L, max_docs, cu_seqlens_host,
+                                              static_cast<int>(x_dtype), static_cast<int>(y_dtype),
+                                              n1);
+    if (be != BuildError::kOk) {
+        delete pl;
+        if (be == BuildError::kArg) return RUBICONV_ERR_ARG;
+        if (be == BuildError::kSeqlens) return RUBICONV_ERR_SEQLENS;
+        return RUBICONV_ERR_UNSUPPORTED;
+    }
+    const HostPlan& h = pl->h;
+    pl->grid_pb_stride = h.grid_points * kPairsPerBlock;
+    pl->cls_pb_stride = h.class_points * kPairsPerBlock;
+    pl->spec_pb_stride = h.spec_points * 2 * kPairsPerBlock;
+    pl->spec_bytes = align_up(static_cast<size_t>(h.npb) * pl->spec_pb_stride * 8);
+    pl->taps_bytes = align_up(static_cast<size_t>(h.taps_max) * h.D * 4);
+    const size_t conv_ws = align_up(static_cast<size_t>(h.npb) * pl->grid_pb_stride * 8);
+    const size_t filt_ws = pl->taps_bytes + align_up(static_cast<size_t>(h.npb) * pl->cls_pb_stride * 8);
+    pl->ws_bytes = std::max(conv_ws, filt_ws);
+    rubiconv_status_t st = upload(pl);
+    if (st != RUBICONV_OK) {
+        delete pl;
+        return st;
+    }
+    *out = pl;
+    return RUBICONV_OK;
+}
+
+void rubiconv_plan_destroy(rubiconv_plan_t plan) {
+    if (!plan) return;
+    destroy_events(plan);
+    if (plan->dev) (void)hipFree(plan->dev);
+    delete plan;
+}
+
+size_t rubiconv_spectrum_bytes(rubiconv_plan_t plan) { return plan ? plan->spec_bytes : 0; }
+
+size_t rubiconv_workspace_bytes(rubiconv_plan_t plan) { return plan ? plan->ws_bytes : 0; }
+
+rubiconv_status_t rubiconv_filter_spectrum(rubiconv_plan_t plan, const float* filters,
+                                           void* spectrum, void* workspace, hipStream_t stream) {
+    if (!plan || !filters || !spectrum || !workspace) return RUBICONV_ERR_ARG;
+    if (!aligned(spectrum) || !aligned(workspace) || (reinterpret_cast<uintptr_t>(filters) % 4))
+        return RUBICONV_ERR_ARG;
+    if (!plan->device_ready) return RUBICONV_ERR_HIP;
+    const HostPlan& h = plan->h;
+    float* taps = static_cast<float*>(workspace);  // [taps_max][D]
+    float2* cgrid = reinterpret_cast<float2*>(static_cast<unsigned char*>(workspace) + plan->taps_bytes);
+    float2* spec = static_cast<float2*>(spectrum);
+    StageRecorder rec(plan, stream);
+    hipError_t e = rubiconv::launch_transpose(filters, h.D, h.taps_max, h.L, taps, h.D, stream);
+    rec.mark("filter_transpose");
+    if (e == hipSuccess)
+        e = rubiconv::launch_col_fwd(h.r, 0, taps, 0, h.D, cgrid, plan->cls_pb_stride, plan->cls_t,
+                                     static_cast<int>(h.cls_col_seg.size()), h.npb, stream);
+    rec.mark("filter_col_fwd");
+    if (e == hipSuccess)
+        e = rubiconv::launch_row_spec(h.n1, cgrid, plan->cls_pb_stride, spec, plan->spec_pb_stride,
+                                      plan->cls_t, static_cast<int>(h.cls_task_seg.size()), h.npb,
+                                      h.row_lds_classes, stream);
+    rec.mark("filter_row_spec");
+    return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
+}
+
+rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, const void* spectrum,
+                                       void* y, void* workspace, hipStream_t stream) {
+    if (!plan || !x || !spectrum || !y || !workspace) return RUBICONV_ERR_ARG;
+    if (!aligned(spectrum) || !aligned(workspace)) return RUBICONV_ERR_ARG;
+    const size_t esz = plan->h.x_dtype == RUBICONV_F32 ? 4 : 2;
+    const size_t ysz = plan->h.y_dtype == RUBICONV_F32 ? 4 : 2;
+    if (reinterpret_cast<uintptr_t>(x) % esz || reinterpret_cast<uintptr_t>(y) % ysz)
+        return RUBICONV_ERR_ARG;
+    if (!plan->device_ready) return RUBICONV_ERR_HIP;
+    const HostPlan& h = plan->h;
+    float2* grid = static_cast<float2*>(workspace);
+    const int n_cols = static_cast<int>(h.doc_col_seg.size());
+    const int64_t rs = static_cast<int64_t>(h.N) * h.D;
+    StageRecorder rec(plan, stream);
+    hipError_t e = rubiconv::launch_col_fwd(h.r, h.x_dtype, x, rs, h.D, grid, plan->grid_pb_stride,
+                                            plan->doc_t, n_cols, h.npb, stream);
+    rec.mark("col_fwd");
+    if (e == hipSuccess)
+        e = rubiconv::launch_row_conv(h.n1, grid, plan->grid_pb_stride,
+                                      static_cast<const float2*>(spectrum), plan->spec_pb_stride,
+                                      plan->doc_t, static_cast<int>(h.doc_task_seg.size()), h.npb,
+                                      h.row_lds_docs, stream);
+    rec.mark("row_conv");
+    if (e == hipSuccess)
+        e = rubiconv::launch_col_inv(h.r, h.y_dtype, grid, plan->grid_pb_stride, y, rs, h.D,
+                                     plan->doc_t, n_cols, h.npb, stream);
+    rec.mark("col_inv");
+    return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
+}
+
+rubiconv_status_t rubiconv_plan_info(rubiconv_plan_t plan, rubiconv_plan_info_t* info) {
+    if (!plan || !info) return RUBICONV_ERR_ARG;
+    const HostPlan& h = plan->h;
+    info->B = h.B; info->N = h.N; info->D = h.D; info->L = h.L;
+    info->n1 = h.n1;
+    info->n_docs = static_cast<int>(h.docs.size());
+    info->n_classes = static_cast<int>(h.classes.size());
+    info->n_pair_blocks = h.npb;
+    info->grid_points = h.grid_points;
+    info->class_points = h.class_points;
+    int64_t tok = 0;
+    for (const Seg& s : h.docs) tok += s.len;
+    info->tokens = tok;
+    return RUBICONV_OK;
+}
+
+rubiconv_status_t rubiconv_plan_doc_table(rubiconv_plan_t plan, int32_t* out, int cap,
+                                          int* n_docs) {
+    if (!plan || !n_docs || cap < 0 || (cap > 0 && !out)) return RUBICONV_ERR_ARG;
+    const HostPlan& h = plan->h;
+    const int n = static_cast<int>(h.docs.size());
+    *n_docs = n;
+    for (int i = 0; i < n && i < cap; ++i) {
+        const Seg& s = h.docs[i];
+        int32_t* o = out + 6 * static_cast<int64_t>(i);
+        o[0] = s.row; o[1] = h.doc_index[i]; o[2] = s.start; o[3] = s.len; o[4] = s.m; o[5] = s.P;
+    }
+    return RUBICONV_OK;
+}
+
+rubiconv_status_t rubiconv_profile_start(rubiconv_plan_t plan, int max_calls) {
+    if (!plan || max_calls < 0) return RUBICONV_ERR_ARG;
+    destroy_events(plan);
+    if (max_calls == 0) return RUBICONV_OK;
+    if (!plan->device_ready) return RUBICONV_ERR_HIP;
+    const int n = max_calls * rubiconv_plan_s::kEventsPerCall;
+    plan->prof_events.reserve(n);
+    for (int i = 0; i < n; ++i) {
+        hipEvent_t ev;
+        if (hipEventCreate(&ev) != hipSuccess) {
+            destroy_events(plan);
+            return RUBICONV_ERR_ALLOC;
+        }
+        plan->prof_events.push_back(ev);
+    }
+    plan->prof_names.assign(max_calls, {});
+    plan->prof_max = max_calls;
+    return RUBICONV_OK;
+}
+
+rubiconv_status_t rubiconv_profile_read(rubiconv_plan_t plan, rubiconv_kernel_time_t* out, int cap,
+                                        int* n) {
+    if (!plan || !n || cap < 0 || (cap > 0 && !out)) return RUBICONV_ERR_ARG;
+    std::vector<rubiconv_kernel_time_t> acc;
+    for (int slot = 0; slot < plan->prof_used; ++slot) {
+        const auto& names = plan->prof_names[slot];
+        hipEvent_t* ev = plan->prof_events.data() + slot * rubiconv_plan_s::kEventsPerCall;
+        if (!names.empty() && hipEventSynchronize(ev[names.size()]) != hipSuccess)
+            return RUBICONV_ERR_HIP;
+        for (size_t k = 0; k < names.size(); ++k) {
+            float ms = 0.0f;
+            if (hipEventElapsedTime(&ms, ev[k], ev[k + 1]) != hipSuccess) return RUBICONV_ERR_HIP;
+            auto it = std::find_if(acc.begin(), acc.end(), [&](const rubiconv_kernel_time_t& a) {
+                return std::strcmp(a.name, names[k]) == 0;
+            });
+            if (it == acc.end()) {
+                rubiconv_kernel_time_t t{};
+                std::strncpy(t.name, names[k], sizeof(t.name) - 1);
+                acc.push_back(t);
+                it = acc.end() - 1;
+            }
+            it->launches += 1;
+            it->total_ms += ms;
+        }
+    }
+    *n = static_cast<int>(acc.size());
+    for (int i = 0; i < *n && i < cap; ++i) out[i] = acc[i];
+    return RUBICONV_OK;
+}
+
+const char* rubiconv_status_string(rubiconv_status_t status) {
+    switch (status) {
+        case RUBICONV_OK: return "ok";
+        case RUBICONV_ERR_ARG: return "invalid argument";
+        case RUBICONV_ERR_SEQLENS: return "invalid cu_seqlens";
+        case RUBICONV_ERR_UNSUPPORTED: return "unsupported configuration";
+        case RUBICONV_ERR_ALLOC: return "allocation failed";
+        case RUBICONV_ERR_HIP: return "HIP error or no device";
+    }
+    return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,145 @@
+"""The C-ABI library on the host (no GPU needed): symbols, plan tables, errors.
+
+The document table must match the oracle's segment derivation exactly, and every
+transform size must satisfy the causal padding rule of Algorithm 1
+(P_i >= L_i + min(L_i, L) - 1, N1 divides P_i) with m_i the smallest 2^a 3^b 5^c
+size that does.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2605_08451_amd as rc
+import workloads as wl
+from tests.conftest import gpu_available
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                      "rubiconv.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rubiconv_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    lib = rc.load_library()
+    declared = header_functions()
+    assert declared, "no declarations parsed"
+    for name in declared:
+        assert hasattr(lib, name), f"{name} declared in rubiconv.h but not exported"
+    assert sorted(rc.EXPORTED_SYMBOLS) == declared
+
+
+def test_library_file_is_in_tree():
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    assert os.path.realpath(rc.library_path()).startswith(os.path.realpath(root))
+
+
+def _smooth(n):
+    for p in (2, 3, 5):
+        while n % p == 0:
+            n //= p
+    return n == 1
+
+
+@pytest.mark.parametrize("i", range(5))
+@pytest.mark.parametrize("n1", [0, 64])
+def test_doc_table_matches_oracle_segments(i, n1):
+    cu = wl.config_cu_seqlens(i)
+    D, L, dt = wl.CONFIG_SHAPES[i]
+    N = int(cu[0, -1])
+    k = 256 if n1 == 0 else n1
+    ref = oracle.doc_table(cu, N, L, k)
+    try:
+        plan = rc.Plan(cu, N=N, D=D, L=L, x_dtype=dt, n1=n1)
+    except rc.RubiconvError as e:   # N1 = 64 cannot reach the longest documents of config 4
+        assert i == 4 and n1 == 64 and e.status == 3
+        return
+    t = plan.doc_table()
+    np.testing.assert_array_equal(t[:, :4], ref[:, :4])   # row, index, start, length: exact
+    m, P = t[:, 4].astype(np.int64), t[:, 5].astype(np.int64)
+    np.testing.assert_array_equal(P, k * m)
+    assert np.all(P >= ref[:, 4]), "transform shorter than the causal padding rule allows"
+    for mi, minimal in zip(m, ref[:, 4] // k):
+        assert _smooth(int(mi))
+        assert all(not _smooth(c) for c in range(int(minimal), int(mi))), (mi, minimal)
+    info = plan.info()
+    assert info["n_docs"] == len(ref) and info["tokens"] == cu.shape[0] * N
+    assert info["grid_points"] == int(P.sum())
+    assert info["n_classes"] == len(set(m.tolist()))
+
+
+def test_empty_documents_are_skipped():
+    cu = np.array([[0, 0, 3, 3, 3, 10], [0, 10, 10, 10, 10, 10]], dtype=np.int32)
+    t = rc.Plan(cu, N=10, D=2, L=4, x_dtype="f32").doc_table()
+    np.testing.assert_array_equal(t[:, :4], [[0, 1, 0, 3], [0, 4, 3, 7], [1, 0, 0, 10]])
+
+
+@pytest.mark.parametrize("cu,N", [
+    ([[1, 5, 10]], 10),          # does not start at 0
+    ([[0, 5, 9]], 10),           # does not end at N
+    ([[0, 6, 5, 10]], 10),       # decreasing
+    ([[0, 11, 10]], 10),         # beyond N
+    ([[0, -1, 10]], 10),         # negative
+])
+def test_bad_seqlens_status(cu, N):
+    with pytest.raises(rc.RubiconvError) as e:
+        rc.Plan(np.array(cu, dtype=np.int32), N=N, D=4, L=3)
+    assert e.value.status == 2
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(N=0), 1), (dict(D=0), 1), (dict(L=0), 1), (dict(n1=100), 3), (dict(n1=512), 3),
+])
+def test_bad_arguments_status(kw, status):
+    args = dict(N=8, D=4, L=3, n1=0)
+    args.update(kw)
+    with pytest.raises(rc.RubiconvError) as e:
+        rc.Plan(np.array([[0, max(args["N"], 0)]], dtype=np.int32), **args)
+    assert e.value.status == status
+
+
+def test_too_long_document_is_unsupported():
+    N = 600000   # one document: P >= 2N - 1 needs m > 2048 at N1 = 256
+    with pytest.raises(rc.RubiconvError) as e:
+        rc.Plan(np.array([[0, N]], dtype=np.int32), N=N, D=2, L=N)
+    assert e.value.status == 3
+
+
+def test_null_arguments_rejected_before_any_device_work():
+    lib = rc.load_library()
+    plan = rc.Plan(np.array([[0, 8]], dtype=np.int32), N=8, D=2, L=3, x_dtype="f32")
+    assert lib.rubiconv_packed_conv(None, None, None, None, None, None) == 1
+    assert lib.rubiconv_packed_conv(plan.handle, None, None, None, None, None) == 1
+    assert lib.rubiconv_filter_spectrum(plan.handle, None, None, None, None) == 1
+    assert lib.rubiconv_filter_spectrum(plan.handle, 256, 512, 768 + 1, None) == 1  # misaligned
+    assert lib.rubiconv_plan(None, 1, 8, 2, 3, 1, None, 0, 0, 0) == 1
+    assert lib.rubiconv_spectrum_bytes(None) == 0 and lib.rubiconv_workspace_bytes(None) == 0
+    assert lib.rubiconv_status_string(2) == b"invalid cu_seqlens"
+    lib.rubiconv_plan_destroy(None)
+
+
+@pytest.mark.skipif(gpu_available(), reason="checks the host-only plan of a machine without a GPU")
+def test_stream_calls_without_device_report_hip_error():
+    lib = rc.load_library()
+    plan = rc.Plan(np.array([[0, 8]], dtype=np.int32), N=8, D=2, L=3, x_dtype="f32")
+    fake = 1 << 20   # never dereferenced: the call returns before launching
+    assert lib.rubiconv_packed_conv(plan.handle, fake, fake, fake, fake, None) == 5
+    assert lib.rubiconv_filter_spectrum(plan.handle, fake, fake, fake, None) == 5
+
+
+def test_buffer_sizes_cover_the_layouts():
+    cu = wl.config_cu_seqlens(3)
+    plan = rc.Plan(cu, N=8192, D=512, L=8192, x_dtype="f32")
+    info = plan.info()
+    npb = info["n_pair_blocks"]
+    assert npb == 16
+    # workspace holds at least the complex fp32 document grid of every pair block
+    assert plan.workspace_bytes >= npb * 16 * 8 * info["grid_points"]
+    assert plan.workspace_bytes % 256 == 0 and plan.spectrum_bytes % 256 == 0

@@ -1,0 +1,167 @@
+"""The HIP path against the oracle on the same seeded inputs (needs an MI355X).
+
+Bars: relative L2 <= 1e-4 for fp32 workloads and <= 2e-2 for bf16 inputs with
+fp32 accumulation, both over the whole output and over every document; zero
+cross-document leakage.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from tests.common import (ORACLE_THREADS, TOL, assert_parity, parity_report, reference,
+                          run_gpu)
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ------------------------------------------------------------------ the five workloads
+@pytest.mark.parametrize("i,method", [(0, "direct"), (1, "direct"), (3, "direct"), (2, "fft"),
+                                      (4, "fft")])
+def test_config_parity(device, i, method):
+    _say(f"[parity] config {i} ({wl.CONFIG_NAMES[i]}), oracle {method}")
+    W = wl.make_config(i)
+    y, plan = run_gpu(W, device)
+    ref = reference(W, method)
+    g, d = assert_parity(y, ref, W.cu_seqlens, W.x_dtype, f"config {i}")
+    _say(f"[parity] config {i}: global {g:.2e}, worst document {d:.2e}, docs {W.n_docs}")
+
+
+@pytest.mark.parametrize("i", [2, 4])
+def test_full_size_sampled_direct_sums(device, i):
+    """The bench workloads at full size, sampled entries against the defining sum."""
+    W = wl.make_config(i)
+    y, _ = run_gpu(W, device)
+    rng = np.random.default_rng(100 + i)
+    n = 4000
+    btd = np.stack([rng.integers(0, W.B, n), rng.integers(0, W.N, n), rng.integers(0, W.D, n)], 1)
+    # include the first and last token of every document
+    extra = []
+    for b, row in enumerate(W.cu_seqlens):
+        for s0, s1 in zip(row[:-1], row[1:]):
+            if s1 > s0:
+                extra += [(b, s0, rng.integers(W.D)), (b, s1 - 1, rng.integers(W.D))]
+    btd = np.concatenate([btd, np.array(extra, dtype=np.int64)])
+    ref = oracle.conv_at(W.x, W.filters, W.cu_seqlens, btd, threads=ORACLE_THREADS)
+    got = y[btd[:, 0], btd[:, 1], btd[:, 2]]
+    err = np.linalg.norm(got - ref) / np.linalg.norm(ref)
+    assert err <= TOL[W.x_dtype], err
+
+
+# ------------------------------------------------------------------ edge cases
+N1_EDGE = [1, 255, 256, 257, 511, 512, 513]
+
+
+@pytest.mark.parametrize("n1", [256, 64])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_ragged_edges(device, n1, dtype):
+    """Documents of length 1, N1 - 1, N1, N1 + 1, whole rows; L shorter and longer than them."""
+    rng = np.random.default_rng(7)
+    N = 2048
+    rows = [[N],
+            [1] * 5 + [n1 - 1, n1, n1 + 1] + [N - 5 - 3 * n1],
+            wl.random_rows(rng, 1, N, 300, p_short=0.5)[0],
+            [N - 1, 1]]
+    for L in (1, 7, 300, N, 3 * N):
+        W = wl.make_case(rows, D=6, L=L, x_dtype=dtype, seed=L)
+        y, _ = run_gpu(W, device, n1=n1)
+        assert_parity(y, reference(W), W.cu_seqlens, dtype, f"L={L}")
+
+
+@pytest.mark.parametrize("D", [1, 2, 3, 31, 33, 64])
+def test_channel_counts(device, D):
+    """Odd D (a lone last channel), D below and above one pair block of 32 channels."""
+    rng = np.random.default_rng(D)
+    rows = wl.random_rows(rng, 2, 1000, 400)
+    for dtype in ("f32", "bf16"):
+        W = wl.make_case(rows, D=D, L=500, x_dtype=dtype, seed=D)
+        y, _ = run_gpu(W, device)
+        assert_parity(y, reference(W), W.cu_seqlens, dtype, f"D={D} {dtype}")
+
+
+@pytest.mark.parametrize("N", [1, 2, 5, 100, 4096])
+def test_short_rows(device, N):
+    rng = np.random.default_rng(N)
+    rows = wl.random_rows(rng, 3, N, max(1, N // 3))
+    W = wl.make_case(rows, D=4, L=N + 3, seed=N)
+    y, _ = run_gpu(W, device)
+    assert_parity(y, reference(W), W.cu_seqlens, "f32", f"N={N}")
+
+
+def test_mixed_dtypes(device):
+    """bf16 input with fp32 output, and fp32 input with bf16 output."""
+    rng = np.random.default_rng(3)
+    rows = wl.random_rows(rng, 2, 3000, 1500)
+    W = wl.make_case(rows, D=8, L=3000, x_dtype="bf16", seed=3)
+    y, _ = run_gpu(W, device, y_dtype="f32")
+    assert_parity(y, reference(W), W.cu_seqlens, "f32", "bf16 -> f32")
+    W = wl.make_case(rows, D=8, L=3000, x_dtype="f32", seed=4)
+    y, _ = run_gpu(W, device, y_dtype="bf16")
+    assert_parity(y, reference(W), W.cu_seqlens, "bf16", "f32 -> bf16")
+
+
+def test_leakage_impulses(device):
+    """An impulse in document j, with an undecayed filter as long as the row, leaves every
+    other document and row below 1e-6 of the impulse document's peak."""
+    N, D = 4096, 4
+    rng = np.random.default_rng(11)
+    rows = [[1, 255, 256, 257, 1000, N - 1769], [N]]
+    cu = wl.cu_from_rows(rows, N)
+    k = rng.standard_normal((D, N)).astype(np.float32)   # no decay: long lags are live
+    docs = [(b, int(s0), int(s1)) for b, r in enumerate(cu) for s0, s1 in zip(r[:-1], r[1:])
+            if s1 > s0] + [(0, N - 1, N)]
+    for (b, s0, s1) in docs:
+        W = wl.make_case(rows, D=D, L=N, seed=0, filters=k)
+        W.x[:] = 0.0
+        t = s0 + int(rng.integers(0, s1 - s0))
+        W.x[b, t, :] = rng.standard_normal(D)
+        y, _ = run_gpu(W, device)
+        inside = np.zeros(y.shape, dtype=bool)
+        e = [(bb, a, z) for (bb, a, z) in docs[:-1] if bb == b and a <= t < z][0]
+        inside[b, e[1]:e[2]] = True
+        peak = np.abs(y[inside]).max()
+        assert peak > 0
+        assert np.abs(y[~inside]).max() <= 1e-6 * peak, (b, s0, s1)
+        np.testing.assert_array_equal(y[b, e[1]:t], 0.0)   # causal: nothing before the impulse
+
+
+def test_delta_filter_is_identity(device):
+    rng = np.random.default_rng(5)
+    rows = wl.random_rows(rng, 2, 3000, 1200)
+    D = 16
+    k = np.zeros((D, 50), dtype=np.float32)
+    k[:, 0] = 1.0
+    W = wl.make_case(rows, D=D, L=50, seed=5, filters=k)
+    y, _ = run_gpu(W, device)
+    assert np.abs(y - W.x).max() <= 1e-5 * np.abs(W.x).max()
+
+
+def test_deterministic(device):
+    W = wl.make_case(wl.random_rows(np.random.default_rng(2), 2, 5000, 3000), D=40, L=5000,
+                     x_dtype="bf16", seed=2)
+    ys, _ = run_gpu(W, device, repeats=3)
+    for y in ys[1:]:
+        np.testing.assert_array_equal(y, ys[0])
+
+
+def test_plan_reused_with_two_filters(device):
+    import torch
+    import paper_2605_08451_amd as rc
+    from tests.common import to_device
+    rows = wl.random_rows(np.random.default_rng(9), 2, 2500, 900)
+    W1 = wl.make_case(rows, D=10, L=2500, seed=1)
+    W2 = wl.make_case(rows, D=10, L=2500, seed=2)
+    plan = rc.Plan(W1.cu_seqlens, N=W1.N, D=W1.D, L=W1.L, x_dtype="f32")
+    ws = plan.new_workspace(device)
+    for W in (W1, W2, W1):
+        x, k = to_device(W, device)
+        spec = rc.filter_spectrum(plan, k, workspace=ws)
+        y = rc.packed_conv(plan, x, spec, workspace=ws)
+        torch.cuda.synchronize()
+        assert_parity(y.cpu().numpy().astype(np.float64), reference(W), W.cu_seqlens, "f32")
