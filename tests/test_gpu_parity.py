@@ -128,7 +128,8 @@ def test_leakage_impulses(device):
         peak = np.abs(y[inside]).max()
         assert peak > 0
         assert np.abs(y[~inside]).max() <= 1e-6 * peak, (b, s0, s1)
-        np.testing.assert_array_equal(y[b, e[1]:t], 0.0)   # causal: nothing before the impulse
+        # causal: before the impulse only transform rounding remains (zero in exact arithmetic)
+        assert np.abs(y[b, e[1]:t]).max(initial=0.0) <= 1e-6 * peak, (b, s0, s1)
 
 
 def test_delta_filter_is_identity(device):
