@@ -2,7 +2,7 @@
 //
 // dft<R, S>(v) replaces v[0..R) by its R-point DFT with kernel
 // exp(S * 2 pi i n k / R) (S = -1 forward, +1 inverse, unnormalised), natural
-// order in and out.  Sizes 2, 3, 4, 5 are written out; 8 and 16 are split
+// order in and out.  Sizes 2, 3, 4, 5 are written out; 6, 8, 9, 10, 12, 15, 16 are split
 // R = A * B by decimation in time with compile-time twiddles, so after
 // unrolling every index is a constant and the values stay in VGPRs.
 #pragma once
@@ -169,6 +169,26 @@ struct DftSplit {
     }
 };
 
+template <int S>
+struct Dft<6, S> {
+    __device__ __forceinline__ static void run(float2 (&v)[6]) { DftSplit<2, 3, S>::run(v); }
+};
+template <int S>
+struct Dft<9, S> {
+    __device__ __forceinline__ static void run(float2 (&v)[9]) { DftSplit<3, 3, S>::run(v); }
+};
+template <int S>
+struct Dft<10, S> {
+    __device__ __forceinline__ static void run(float2 (&v)[10]) { DftSplit<2, 5, S>::run(v); }
+};
+template <int S>
+struct Dft<12, S> {
+    __device__ __forceinline__ static void run(float2 (&v)[12]) { DftSplit<4, 3, S>::run(v); }
+};
+template <int S>
+struct Dft<15, S> {
+    __device__ __forceinline__ static void run(float2 (&v)[15]) { DftSplit<3, 5, S>::run(v); }
+};
 template <int S>
 struct Dft<8, S> {
     __device__ __forceinline__ static void run(float2 (&v)[8]) { DftSplit<2, 4, S>::run(v); }

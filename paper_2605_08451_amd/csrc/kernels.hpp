@@ -32,6 +32,7 @@ struct LaunchTables {
     const int32_t* task_seg;
     const float2* tw;      // per-class twiddles
     const float2* tw_n1;   // w_N1^s
+    const int32_t* list;   // documents grouped by class / class identity list
 };
 
 hipError_t launch_col_fwd(int r, int x_dtype, const void* src, int64_t src_row_stride, int D,
@@ -49,6 +50,13 @@ hipError_t launch_row_conv(int n1, float2* grid, int64_t grid_pb_stride, const f
 hipError_t launch_row_spec(int n1, const float2* grid, int64_t grid_pb_stride, float2* spec,
                            int64_t spec_pb_stride, const LaunchTables& t, int n_tasks, int npb,
                            int lds_bytes, hipStream_t stream);
+
+// Register-resident row pass for a listed row size m (row_sizes.hpp) over the
+// nlist segments list[0..nlist) of that size; spec_mode selects the filter side.
+hipError_t launch_row_fast(int m, bool spec_mode, float2* grid, int64_t grid_pb_stride,
+                           float2* spec, int64_t spec_pb_stride, const Seg* segs,
+                           const int32_t* list, int nlist, const float2* tw, int n1, int npb,
+                           hipStream_t stream);
 
 hipError_t launch_transpose(const float* in, int rows, int cols, int in_ld, float* out,
                             int out_ld, hipStream_t stream);

@@ -28,8 +28,10 @@ struct Seg {
     int32_t tw_off;    // class twiddles: [tw_off, +N1) = w_P^r, [tw_off+N1, +m) = w_m^h
     int32_t spec_off;  // class spectrum: first of (N1/2 + 1) * m points
     int32_t col0;      // first global column index of this segment
-    int32_t task0;     // first global row-task index of this segment
+    int32_t task0;     // first global row-task index of this segment (generic row kernel)
     int32_t spb;       // pairs per row task (16, or fewer for long rows)
+    int32_t list0;     // classes: first entry of this class in the class-ordered document list
+    int32_t nlist;     // classes: number of documents in the class
     int32_t nfac;      // radices of m, applied in order
     int8_t fac[kMaxFactors];
     int8_t pad_[2];

@@ -12,6 +12,8 @@
 // P >= L_i + min(L_i, L) - 1).
 #include "plan_build.hpp"
 
+#include "row_sizes.hpp"
+
 #include <algorithm>
 #include <cmath>
 #include <map>
@@ -45,6 +47,7 @@ int factorize(int m, int8_t* fac) {
 // floats must fit the row pass's LDS budget.
 int pairs_per_task(int m) {
     int spb = kPairsPerBlock;
+    if (m <= kMaxFastM) return spb;  // register-resident kernel: 32 lines of m values in LDS
     while (spb > 1 && 4 * m * spb * 8 > kRowLdsBytes) spb /= 2;
     return spb;
 }
@@ -95,7 +98,9 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
             int64_t need = static_cast<int64_t>(len) + std::min(len, L) - 1;
             int64_t mmin = (need + n1 - 1) / n1;
             if (mmin > kMaxM) return BuildError::kUnsupported;
-            int m = smooth_ceil(static_cast<int>(mmin));
+            // listed sizes have register-resident row kernels; longer rows are 5-smooth
+            int m = fast_row_size(static_cast<int>(mmin));
+            if (m == 0) m = smooth_ceil(static_cast<int>(mmin));
             if (m > kMaxM) return BuildError::kUnsupported;
             Seg s{};
             s.row = b; s.start = c[k]; s.len = len; s.m = m; s.P = n1 * m;
@@ -135,8 +140,10 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
         s.task0 = static_cast<int32_t>(p.doc_task_seg.size());
         int idx = static_cast<int>(&s - p.docs.data());
         p.doc_col_seg.insert(p.doc_col_seg.end(), s.m, idx);
-        p.doc_task_seg.insert(p.doc_task_seg.end(), (n1 / 2 + 1) * (kPairsPerBlock / s.spb), idx);
-        p.row_lds_docs = std::max(p.row_lds_docs, 4 * s.m * s.spb * 8);
+        if (s.m > kMaxFastM) {
+            p.doc_task_seg.insert(p.doc_task_seg.end(), (n1 / 2 + 1) * (kPairsPerBlock / s.spb), idx);
+            p.row_lds_docs = std::max(p.row_lds_docs, 4 * s.m * s.spb * 8);
+        }
     }
     for (auto& s : p.classes) {
         s.grid_off = p.class_points;
@@ -145,8 +152,16 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
         s.task0 = static_cast<int32_t>(p.cls_task_seg.size());
         int idx = static_cast<int>(&s - p.classes.data());
         p.cls_col_seg.insert(p.cls_col_seg.end(), s.m, idx);
-        p.cls_task_seg.insert(p.cls_task_seg.end(), (n1 / 2 + 1) * (kPairsPerBlock / s.spb), idx);
-        p.row_lds_classes = std::max(p.row_lds_classes, 4 * s.m * s.spb * 8);
+        if (s.m > kMaxFastM) {
+            p.cls_task_seg.insert(p.cls_task_seg.end(), (n1 / 2 + 1) * (kPairsPerBlock / s.spb), idx);
+            p.row_lds_classes = std::max(p.row_lds_classes, 4 * s.m * s.spb * 8);
+        }
+        // documents of this class, in document order
+        s.list0 = static_cast<int32_t>(p.class_docs.size());
+        for (size_t i = 0; i < p.docs.size(); ++i)
+            if (p.docs[i].cls == s.cls) p.class_docs.push_back(static_cast<int32_t>(i));
+        s.nlist = static_cast<int32_t>(p.class_docs.size()) - s.list0;
+        p.class_ident.push_back(s.cls);
     }
     push_twiddles(p.tw_n1, n1, n1);
     *out = std::move(p);

@@ -21,6 +21,8 @@ struct HostPlan {
     std::vector<int32_t> doc_task_seg;  // global row task -> document
     std::vector<int32_t> cls_col_seg;   // global column -> class
     std::vector<int32_t> cls_task_seg;  // global row task -> class
+    std::vector<int32_t> class_docs;    // documents grouped by class (class order)
+    std::vector<int32_t> class_ident;   // 0, 1, ..., n_classes - 1
     std::vector<float> tw;              // complex pairs (re, im), per class: N1 then m entries
     std::vector<float> tw_n1;           // complex pairs, w_N1^s for s < N1
     int64_t grid_points = 0;            // sum over documents of P_i

@@ -13,6 +13,7 @@
 
 #include "kernels.hpp"
 #include "plan_build.hpp"
+#include "row_sizes.hpp"
 
 using rubiconv::BuildError;
 using rubiconv::HostPlan;
@@ -56,6 +57,8 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     const size_t o_ctask = off;      off = align_up(off + h.cls_task_seg.size() * 4);
     const size_t o_tw = off;         off = align_up(off + h.tw.size() * 4);
     const size_t o_twn = off;        off = align_up(off + h.tw_n1.size() * 4);
+    const size_t o_cdoc = off;       off = align_up(off + h.class_docs.size() * 4);
+    const size_t o_cid = off;        off = align_up(off + h.class_ident.size() * 4);
     const size_t total = off;
 
     std::vector<unsigned char> img(total, 0);
@@ -68,6 +71,8 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     std::memcpy(img.data() + o_ctask, h.cls_task_seg.data(), h.cls_task_seg.size() * 4);
     std::memcpy(img.data() + o_tw, h.tw.data(), h.tw.size() * 4);
     std::memcpy(img.data() + o_twn, h.tw_n1.data(), h.tw_n1.size() * 4);
+    std::memcpy(img.data() + o_cdoc, h.class_docs.data(), h.class_docs.size() * 4);
+    std::memcpy(img.data() + o_cid, h.class_ident.data(), h.class_ident.size() * 4);
 
     int count = 0;
     hipError_t e = hipGetDeviceCount(&count);
@@ -91,9 +96,11 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     const float2* tw = reinterpret_cast<const float2*>(base + o_tw);
     const float2* twn = reinterpret_cast<const float2*>(base + o_twn);
     pl->doc_t = LaunchTables{dsegs, reinterpret_cast<const int32_t*>(base + o_dcol),
-                             reinterpret_cast<const int32_t*>(base + o_dtask), tw, twn};
+                             reinterpret_cast<const int32_t*>(base + o_dtask), tw, twn,
+                             reinterpret_cast<const int32_t*>(base + o_cdoc)};
     pl->cls_t = LaunchTables{dsegs + h.docs.size(), reinterpret_cast<const int32_t*>(base + o_ccol),
-                             reinterpret_cast<const int32_t*>(base + o_ctask), tw, twn};
+                             reinterpret_cast<const int32_t*>(base + o_ctask), tw, twn,
+                             reinterpret_cast<const int32_t*>(base + o_cid)};
     pl->device_ready = true;
     return RUBICONV_OK;
 }
@@ -197,6 +204,12 @@ rubiconv_status_t rubiconv_filter_spectrum(rubiconv_plan_t plan, const float* fi
         e = rubiconv::launch_row_spec(h.n1, cgrid, plan->cls_pb_stride, spec, plan->spec_pb_stride,
                                       plan->cls_t, static_cast<int>(h.cls_task_seg.size()), h.npb,
                                       h.row_lds_classes, stream);
+    for (size_t c = 0; c < h.classes.size() && e == hipSuccess; ++c) {
+        if (h.classes[c].m > rubiconv::kMaxFastM) continue;
+        e = rubiconv::launch_row_fast(h.classes[c].m, true, cgrid, plan->cls_pb_stride, spec,
+                                      plan->spec_pb_stride, plan->cls_t.segs,
+                                      plan->cls_t.list + c, 1, plan->cls_t.tw, h.n1, h.npb, stream);
+    }
     rec.mark("filter_row_spec");
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }
@@ -223,6 +236,15 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
                                       static_cast<const float2*>(spectrum), plan->spec_pb_stride,
                                       plan->doc_t, static_cast<int>(h.doc_task_seg.size()), h.npb,
                                       h.row_lds_docs, stream);
+    for (size_t c = 0; c < h.classes.size() && e == hipSuccess; ++c) {
+        const Seg& cs = h.classes[c];
+        if (cs.m > rubiconv::kMaxFastM) continue;
+        e = rubiconv::launch_row_fast(cs.m, false, grid, plan->grid_pb_stride,
+                                      const_cast<float2*>(static_cast<const float2*>(spectrum)),
+                                      plan->spec_pb_stride, plan->doc_t.segs,
+                                      plan->doc_t.list + cs.list0, cs.nlist, plan->doc_t.tw, h.n1,
+                                      h.npb, stream);
+    }
     rec.mark("row_conv");
     if (e == hipSuccess)
         e = rubiconv::launch_col_inv(h.r, h.y_dtype, grid, plan->grid_pb_stride, y, rs, h.D,

@@ -41,6 +41,19 @@ def test_library_file_is_in_tree():
     assert os.path.realpath(rc.library_path()).startswith(os.path.realpath(root))
 
 
+ROW_SIZES = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                         "paper_2605_08451_amd", "csrc", "row_sizes.hpp")
+
+
+def listed_row_sizes():
+    """Row sizes with a register-resident kernel (the X(m, M1, M2) list)."""
+    text = open(ROW_SIZES).read()
+    sizes = [(int(m), int(a), int(b)) for m, a, b in
+             re.findall(r"X\((\d+),\s*(\d+),\s*(\d+)\)", text)]
+    assert sizes and all(m == a * b and a >= b for m, a, b in sizes)
+    return sorted(m for m, _, _ in sizes)
+
+
 def _smooth(n):
     for p in (2, 3, 5):
         while n % p == 0:
@@ -66,9 +79,13 @@ def test_doc_table_matches_oracle_segments(i, n1):
     m, P = t[:, 4].astype(np.int64), t[:, 5].astype(np.int64)
     np.testing.assert_array_equal(P, k * m)
     assert np.all(P >= ref[:, 4]), "transform shorter than the causal padding rule allows"
+    listed = listed_row_sizes()
     for mi, minimal in zip(m, ref[:, 4] // k):
         assert _smooth(int(mi))
-        assert all(not _smooth(c) for c in range(int(minimal), int(mi))), (mi, minimal)
+        if minimal <= listed[-1]:   # the smallest listed size that is large enough
+            assert mi == min(s for s in listed if s >= minimal), (mi, minimal)
+        else:                       # the smallest 2^a 3^b 5^c size that is large enough
+            assert all(not _smooth(c) for c in range(int(minimal), int(mi))), (mi, minimal)
     info = plan.info()
     assert info["n_docs"] == len(ref) and info["tokens"] == cu.shape[0] * N
     assert info["grid_points"] == int(P.sum())
