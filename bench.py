@@ -42,27 +42,27 @@ def parse():
 
 
 def kernel_bytes(info, W, plan):
-    """Compulsory HBM bytes per launch of each kernel: its inputs read once and its
-    outputs written once.  Grids are complex fp32 with two channels per value (4 B
-    per grid point and channel); a spectrum point holds S and Df for a channel pair
-    (8 B per point and channel)."""
+    """Compulsory HBM bytes of each launch: its inputs read once and its outputs written
+    once.  Grid elements hold two channels (complex fp32 for fp32 inputs, complex fp16
+    for bf16 inputs: esz / 2 bytes per grid point and channel)."""
     D, G, Gc, n1 = W.D, info["grid_points"], info["class_points"], info["n1"]
     sx = 2 if W.x_dtype == "bf16" else 4
     sy = 2 if W.y_dtype == "bf16" else 4
+    esz = 4 if W.x_dtype == "bf16" else 8
     tok = W.B * W.N * D
     ms = [int(m) for m in plan.doc_table()[:, 4]]
     classes = sorted(set(ms))
-    taps = [min(W.L, (n1 * m + 1) // 2) for m in classes]
-    spec_docs = sum((n1 // 2 + 1) * m for m in ms)
-    spec_cls = sum((n1 // 2 + 1) * m for m in classes)
-    return {
-        "col_fwd": tok * sx + 4 * G * D,
-        "row_conv": 8 * G * D + 8 * spec_docs * D,
-        "col_inv": 4 * G * D + tok * sy,
-        "filter_transpose": 8 * D * max(taps),
-        "filter_col_fwd": 4 * D * sum(taps) + 4 * Gc * D,
-        "filter_row_spec": 4 * Gc * D + 8 * spec_cls * D,
+    taps = {m: min(W.L, (n1 * m + 1) // 2) for m in classes}
+    out = {
+        "col_fwd": tok * sx + G * D * esz // 2,
+        "col_inv": G * D * esz // 2 + tok * sy,
+        "filter_transpose": 8 * D * max(taps.values()),
+        "filter_col_fwd": 4 * D * sum(taps.values()) + Gc * D * esz // 2,
     }
+    for m in classes:   # document grids read + written, the class's filter grid read per document
+        nd = ms.count(m)
+        out[f"row_conv_m{m}"] = nd * (n1 * m * D * esz + n1 * m * D * esz // 2)
+    return out
 
 
 def cpu_baseline(W, target_s):
@@ -145,7 +145,11 @@ def main():
     per_kernel = {n: {"launches": c, "avg_us": 1e3 * tot / c,
                       "GBps": kb.get(n, 0) / (tot / c * 1e-3) / 1e9}
                   for n, (c, tot) in kt.items()}
-    dom = max(kt, key=lambda n: kt[n][1])
+    stages = {}
+    for n, (c, tot) in kt.items():   # per-stage totals: the row passes are one launch per class
+        st = n.split("_m")[0] if "row_" in n else n
+        stages[st] = stages.get(st, 0.0) + 1e3 * tot / c
+    dom = max(kt, key=lambda n: kt[n][1])   # the single launch with the most time
     dom_us = per_kernel[dom]["avg_us"]
     achieved = kb[dom] / (dom_us * 1e-6) / 1e9
 
@@ -171,6 +175,7 @@ def main():
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": None, "bytes_per_launch": kb[dom], "avg_us": round(dom_us, 2)},
+        "stages_us": {n: round(v, 1) for n, v in stages.items()},
         "kernels": {n: {kk: round(vv, 2) for kk, vv in d.items()} for n, d in per_kernel.items()},
         "plan_ms": round(plan_ms, 3),
         "wall_s_timed": round(wall, 4),

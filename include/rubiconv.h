@@ -95,19 +95,23 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
  * enqueued that uses the plan must have finished. */
 void rubiconv_plan_destroy(rubiconv_plan_t plan);
 
-/* Bytes of the device buffer that holds the filter spectra of a plan (one per
- * distinct transform size of the plan). 0 for a null plan. */
+/* Bytes of the device buffer that holds the transformed filters of a plan (one
+ * grid per distinct transform size of the plan). 0 for a null plan. */
 size_t rubiconv_spectrum_bytes(rubiconv_plan_t plan);
 
 /* Bytes of device scratch that filter_spectrum and packed_conv need.  A single
- * buffer of this size serves both calls (not at the same time). */
+ * buffer of this size serves both calls (not at the same time).  Grids are
+ * complex fp32 for fp32 inputs and complex fp16 for bf16 inputs. */
 size_t rubiconv_workspace_bytes(rubiconv_plan_t plan);
 
 /*
- * Transform the filters into the plan's spectra (the filter side of
- * Algorithm 3: the filter is padded to each transform size, transformed with
- * the same column/twiddle/row steps as the data and separated by conjugate
- * symmetry; the 1/P_i scale of the inverse is folded in).
+ * Transform the filters for the plan's size classes (the filter side of
+ * Algorithm 3).  For every distinct transform size P = N1 * m of the plan, the
+ * first min(L, floor((P+1)/2)) taps of each channel (enough for every document
+ * of that size) are padded to P and taken through the column DFTs and the
+ * per-size twiddle, two channels per complex value.  rubiconv_packed_conv
+ * applies the row DFTs and the conjugate-symmetry separation together with the
+ * data's, so the buffer holds the filters' half-transformed grids.
  *
  *   filters    device float32 [D][L], row-major (channel d's taps contiguous).
  *   spectrum   device buffer of rubiconv_spectrum_bytes(plan), 256-byte aligned,

@@ -184,11 +184,15 @@ class Plan:
 
     def profile_read(self) -> dict:
         """{kernel name: (launches, total milliseconds)} of the profiled calls (waits)."""
-        out = (_KernelTime * 16)()
         n = ctypes.c_int(0)
-        _check(self._lib.rubiconv_profile_read(self.handle, out, 16, ctypes.byref(n)),
+        _check(self._lib.rubiconv_profile_read(self.handle, None, 0, ctypes.byref(n)),
                "rubiconv_profile_read")
-        return {out[i].name.decode(): (out[i].launches, out[i].total_ms) for i in range(n.value)}
+        cap = max(n.value, 1)
+        out = (_KernelTime * cap)()
+        _check(self._lib.rubiconv_profile_read(self.handle, out, cap, ctypes.byref(n)),
+               "rubiconv_profile_read")
+        return {out[i].name.decode(): (out[i].launches, out[i].total_ms)
+                for i in range(min(n.value, cap))}
 
     def new_spectrum(self, device) -> torch.Tensor:
         return torch.empty(self.spectrum_bytes, dtype=torch.uint8, device=device)

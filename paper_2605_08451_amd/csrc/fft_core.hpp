@@ -198,4 +198,25 @@ struct Dft<16, S> {
     __device__ __forceinline__ static void run(float2 (&v)[16]) { DftSplit<4, 4, S>::run(v); }
 };
 
+// ---------------------------------------------------------------- spectral product
+// Conjugate-symmetry separation (Appendix, dual real FFTs; Algorithm 3) fused with
+// the product.  a is the pair transform at f = (u, v) with u <= N1/2, b at the
+// frequency -f.  For the filter pair h_d + i h_{d+1}:
+//     H_d = (a + conj b) / 2,   H_{d+1} = (a - conj b) / (2i),
+// kept as S = c (H_d + H_{d+1}) and Df = c (H_d - H_{d+1}).  For the data pair the
+// transform of y_d + i y_{d+1} is then
+//     W(f)  = a S + conj(b) Df,   W(-f) = conj(conj(b) S + a Df).
+__device__ __forceinline__ void filter_sdf(float2 a, float2 b, float c, float2& s, float2& df) {
+    const float2 hd = make_float2(0.5f * (a.x + b.x), 0.5f * (a.y - b.y));
+    const float2 hd1 = make_float2(0.5f * (a.y + b.y), 0.5f * (b.x - a.x));
+    s = cscale(cadd(hd, hd1), c);
+    df = cscale(csub(hd, hd1), c);
+}
+__device__ __forceinline__ float2 product_f(float2 a, float2 b, float2 s, float2 df) {
+    return cadd(cmul(a, s), cmul(cconj(b), df));
+}
+__device__ __forceinline__ float2 product_neg_f(float2 a, float2 b, float2 s, float2 df) {
+    return cconj(cadd(cmul(cconj(b), s), cmul(a, df)));
+}
+
 }  // namespace rubiconv

@@ -10,7 +10,11 @@
 // as one complex value (Appendix, dual real FFTs).
 #include <hip/hip_runtime.h>
 
+#include <hip/hip_bf16.h>
+#include <hip/hip_fp16.h>
+
 #include <cstdint>
+#include <type_traits>
 
 #include "fft_core.hpp"
 #include "kernels.hpp"
@@ -20,11 +24,11 @@ namespace rubiconv {
 // ---------------------------------------------------------------- element I/O
 __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
 
-__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;  // NaN stays a (quiet) NaN
-    u += 0x7fffu + ((u >> 16) & 1u);                                 // round to nearest, ties to even
-    return u >> 16;
+// Two floats rounded to bf16 (nearest, ties to even; one v_cvt_pk_bf16_f32 on gfx950),
+// low half = v.x.
+__device__ __forceinline__ uint32_t pack_bf16x2(float2 v) {
+    const __hip_bfloat162 h = __float22bfloat162_rn(v);
+    return *reinterpret_cast<const uint32_t*>(&h);
 }
 
 // Channels ch (real part) and ch + 1 (imaginary part) of one token; idx is the
@@ -66,55 +70,114 @@ __device__ __forceinline__ void store_pair<F32>(void* base, int64_t idx, float2 
 template <>
 __device__ __forceinline__ void store_pair<BF16>(void* base, int64_t idx, float2 v, bool both, bool even_d) {
     uint16_t* p = static_cast<uint16_t*>(base) + idx;
+    const uint32_t w = pack_bf16x2(v);
     if (even_d) {
-        *reinterpret_cast<uint32_t*>(p) = f32_to_bf16(v.x) | (f32_to_bf16(v.y) << 16);
+        *reinterpret_cast<uint32_t*>(p) = w;
         return;
     }
-    p[0] = static_cast<uint16_t>(f32_to_bf16(v.x));
-    if (both) p[1] = static_cast<uint16_t>(f32_to_bf16(v.y));
+    p[0] = static_cast<uint16_t>(w & 0xffffu);
+    if (both) p[1] = static_cast<uint16_t>(w >> 16);
 }
 
-// w_P^r for 0 <= r < P from the class table: w_P^(N1 hi + lo) = w_m^hi * w_P^lo.
-template <int N1>
-__device__ __forceinline__ float2 seg_root(const float2* tw_cls, int r) {
-    return cmul(tw_cls[N1 + r / N1], tw_cls[r % N1]);
+// Grid and spectrum elements: complex fp32 (float2) or complex fp16 (__half2),
+// always computed in fp32.
+__device__ __forceinline__ float2 gload(const float2* p) { return *p; }
+__device__ __forceinline__ float2 gload(const __half2* p) { return __half22float2(*p); }
+__device__ __forceinline__ void gstore(float2* p, float2 v) { *p = v; }
+__device__ __forceinline__ void gstore(__half2* p, float2 v) { *p = __float22half2_rn(v); }
+
+// Buffer resource over one document's tokens: accesses at byte offsets outside
+// [0, bytes) read as zero and are dropped on store, which implements the zero
+// padding beyond the document (and its cut-off) without branches.
+constexpr int kBufferWord3 = 0x00020000;  // gfx9 raw buffer: 32-bit data format
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t doc_buffer(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes),
+                                             kBufferWord3);
 }
+
+// Column-pass modes: channel count D a multiple of 32 (every lane live), D even,
+// or D odd (the last pair has a single channel).
+enum ColMode { kFull = 0, kEven = 1, kOdd = 2 };
+
+template <class T, int MODE>
+__device__ __forceinline__ float2 col_load(__amdgpu_buffer_rsrc_t rs, const void* doc, uint32_t off,
+                                           int64_t idx, bool live, bool in_doc, bool both) {
+    if constexpr (MODE == kOdd) {
+        if (!(live && in_doc)) return make_float2(0.0f, 0.0f);
+        return load_pair<T>(doc, idx, both, false);
+    } else {
+        float2 v;
+        if constexpr (sizeof(T) == sizeof(F32) && std::is_same<T, F32>::value) {
+            const auto w = __builtin_amdgcn_raw_buffer_load_b64(rs, static_cast<int>(off), 0, 0);
+            v = make_float2(__uint_as_float(w[0]), __uint_as_float(w[1]));
+        } else {
+            const uint32_t w = __builtin_amdgcn_raw_buffer_load_b32(rs, static_cast<int>(off), 0, 0);
+            v = make_float2(bf16_to_f32(w & 0xffffu), bf16_to_f32(w >> 16));
+        }
+        if constexpr (MODE == kEven) {
+            if (!live) v = make_float2(0.0f, 0.0f);
+        }
+        return v;
+    }
+}
+
+template <class T, int MODE>
+__device__ __forceinline__ void col_store(__amdgpu_buffer_rsrc_t rs, void* doc, uint32_t off,
+                                          int64_t idx, float2 v, bool in_doc, bool both) {
+    if constexpr (MODE == kOdd) {
+        if (in_doc) store_pair<T>(doc, idx, v, both, false);
+    } else if constexpr (std::is_same<T, F32>::value) {
+        __builtin_amdgcn_raw_buffer_store_b64(
+            __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(rs, 0, 0, 0)), v), rs,
+            static_cast<int>(off), 0, 0);
+    } else {
+        __builtin_amdgcn_raw_buffer_store_b32(pack_bf16x2(v), rs, static_cast<int>(off), 0, 0);
+    }
+}
+
+template <class T>
+constexpr int elem_bytes() { return std::is_same<T, F32>::value ? 4 : 2; }
 
 // ---------------------------------------------------------------- column passes
 // One workgroup = one grid column j of one segment x one block of 16 channel
-// pairs; 16 * R threads, thread (p, q) = (tid % 16, tid / 16).  N1 = R * R is
-// split as a = R n1 + n2, u = k1 + R k2:
+// pairs (1-D grid, pair block fastest, so that neighbouring workgroups touch the
+// two halves of each 128-byte line of x and y together); 16 * R threads,
+// thread (p, q) = (tid % 16, tid / 16).  N1 = R * R is split as a = R n1 + n2,
+// u = k1 + R k2:
 //   stage 1 (thread q = n2): R-point DFT over n1 -> k1, times w_N1^(n2 k1);
 //   exchange through LDS;
 //   stage 2 (thread q = k1): R-point DFT over n2 -> k2.
 // LDS holds [k1][n2][16 pairs] with a padded k1 stride so that both access
-// patterns are free of bank conflicts.
-template <int R, class TX>
+// patterns are free of bank conflicts.  The per-document twiddle w_P^(u j)
+// (scaled by 1/sqrt(N1)) comes from the class's full root table.
+template <int R, class TX, class G, int MODE>
 __global__ __launch_bounds__(16 * R) void col_fwd_kernel(const void* __restrict__ src,
                                                          int64_t src_row_stride, int D,
-                                                         float2* __restrict__ grid,
-                                                         int64_t grid_pb_stride, LaunchTables t) {
-    constexpr int N1 = R * R;
+                                                         G* __restrict__ grid,
+                                                         int64_t grid_pb_stride, LaunchTables t,
+                                                         int npb) {
     constexpr int LD = R * 16 + 16;
+    constexpr int ES = elem_bytes<TX>();
     __shared__ float2 lds[R * LD];
     const int tid = threadIdx.x;
     const int p = tid & 15, q = tid >> 4;
-    const int col = blockIdx.x, pb = blockIdx.y;
+    const int col = blockIdx.x / npb, pb = blockIdx.x - col * npb;
     const Seg* sg = t.segs + t.col_seg[col];
     const int j = col - sg->col0, m = sg->m, len = sg->len;
     const int ch = 2 * (pb * kPairsPerBlock + p);
-    const bool even_d = (D & 1) == 0;
-    const bool live = ch < D;
+    const bool live = MODE == kFull || ch < D;
 
+    const char* doc = static_cast<const char*>(src) +
+                      (static_cast<int64_t>(sg->row) * src_row_stride +
+                       static_cast<int64_t>(sg->start) * D) * ES;
+    const __amdgpu_buffer_rsrc_t rs = doc_buffer(doc, static_cast<uint32_t>(len) * D * ES);
     float2 v[R];
-    const int64_t base = static_cast<int64_t>(sg->row) * src_row_stride +
-                         static_cast<int64_t>(sg->start) * D + ch;
 #pragma unroll
     for (int n1 = 0; n1 < R; ++n1) {
         const int tt = m * (R * n1 + q) + j;
-        v[n1] = (live && tt < len) ? load_pair<TX>(src, base + static_cast<int64_t>(tt) * D,
-                                                   ch + 1 < D, even_d)
-                                   : make_float2(0.0f, 0.0f);
+        v[n1] = col_load<TX, MODE>(rs, doc, (static_cast<uint32_t>(tt) * D + ch) * ES,
+                                   static_cast<int64_t>(tt) * D + ch, live, tt < len, ch + 1 < D);
     }
     Dft<R, -1>::run(v);
 #pragma unroll
@@ -126,40 +189,38 @@ __global__ __launch_bounds__(16 * R) void col_fwd_kernel(const void* __restrict_
     for (int n2 = 0; n2 < R; ++n2) v[n2] = lds[q * LD + n2 * 16 + p];
     Dft<R, -1>::run(v);
 
-    const float2* twc = t.tw + sg->tw_off;
-    float2* out = grid + pb * grid_pb_stride + (sg->grid_off + j) * kPairsPerBlock + p;
+    const float2* twf = t.tw + sg->twf_off;
+    G* out = grid + pb * grid_pb_stride + (sg->grid_off + j) * kPairsPerBlock + p;
 #pragma unroll
     for (int k2 = 0; k2 < R; ++k2) {
         const int u = q + R * k2;
-        out[static_cast<int64_t>(u) * m * kPairsPerBlock] = cmul(v[k2], seg_root<N1>(twc, u * j));
+        gstore(out + static_cast<int64_t>(u) * m * kPairsPerBlock, cmul(v[k2], twf[u * j]));
     }
 }
 
-template <int R, class TY>
-__global__ __launch_bounds__(16 * R) void col_inv_kernel(const float2* __restrict__ grid,
+template <int R, class TY, class G, int MODE>
+__global__ __launch_bounds__(16 * R) void col_inv_kernel(const G* __restrict__ grid,
                                                          int64_t grid_pb_stride,
                                                          void* __restrict__ dst,
                                                          int64_t dst_row_stride, int D,
-                                                         LaunchTables t) {
-    constexpr int N1 = R * R;
+                                                         LaunchTables t, int npb) {
     constexpr int LD = R * 16 + 16;
+    constexpr int ES = elem_bytes<TY>();
     __shared__ float2 lds[R * LD];
     const int tid = threadIdx.x;
     const int p = tid & 15, q = tid >> 4;
-    const int col = blockIdx.x, pb = blockIdx.y;
+    const int col = blockIdx.x / npb, pb = blockIdx.x - col * npb;
     const Seg* sg = t.segs + t.col_seg[col];
     const int j = col - sg->col0, m = sg->m, len = sg->len;
     const int ch = 2 * (pb * kPairsPerBlock + p);
-    const bool even_d = (D & 1) == 0;
 
-    const float2* twc = t.tw + sg->tw_off;
-    const float2* in = grid + pb * grid_pb_stride + (sg->grid_off + j) * kPairsPerBlock + p;
+    const float2* twf = t.tw + sg->twf_off;
+    const G* in = grid + pb * grid_pb_stride + (sg->grid_off + j) * kPairsPerBlock + p;
     float2 v[R];
 #pragma unroll
     for (int k2 = 0; k2 < R; ++k2) {
         const int u = q + R * k2;  // thread q holds k1 = q
-        v[k2] = cmul(in[static_cast<int64_t>(u) * m * kPairsPerBlock],
-                     cconj(seg_root<N1>(twc, u * j)));
+        v[k2] = cmul(gload(in + static_cast<int64_t>(u) * m * kPairsPerBlock), cconj(twf[u * j]));
     }
     Dft<R, 1>::run(v);  // over k2 -> n2
 #pragma unroll
@@ -171,14 +232,15 @@ __global__ __launch_bounds__(16 * R) void col_inv_kernel(const float2* __restric
     for (int k1 = 0; k1 < R; ++k1) v[k1] = lds[k1 * LD + q * 16 + p];  // thread q holds n2 = q
     Dft<R, 1>::run(v);  // over k1 -> n1
 
-    if (ch >= D) return;
-    const int64_t base = static_cast<int64_t>(sg->row) * dst_row_stride +
-                         static_cast<int64_t>(sg->start) * D + ch;
+    if (MODE != kFull && ch >= D) return;
+    char* doc = static_cast<char*>(dst) + (static_cast<int64_t>(sg->row) * dst_row_stride +
+                                           static_cast<int64_t>(sg->start) * D) * ES;
+    const __amdgpu_buffer_rsrc_t rs = doc_buffer(doc, static_cast<uint32_t>(len) * D * ES);
 #pragma unroll
     for (int n1 = 0; n1 < R; ++n1) {
         const int tt = m * (R * n1 + q) + j;
-        if (tt < len)
-            store_pair<TY>(dst, base + static_cast<int64_t>(tt) * D, v[n1], ch + 1 < D, even_d);
+        col_store<TY, MODE>(rs, doc, (static_cast<uint32_t>(tt) * D + ch) * ES,
+                            static_cast<int64_t>(tt) * D + ch, v[n1], tt < len, ch + 1 < D);
     }
 }
 
@@ -268,51 +330,69 @@ __device__ __forceinline__ int partner_col(int u, int v, int m) {
     return u == 0 ? (v == 0 ? 0 : m - v) : m - 1 - v;
 }
 
-__device__ __forceinline__ void load_rows(float2* lds, const float2* g, const RowTask& r) {
+template <class G>
+__device__ __forceinline__ void load_rows(float2* lds, const G* g, const RowTask& r) {
     const int rowlen = r.m * r.spb;
     for (int e = threadIdx.x; e < r.nrows * rowlen; e += blockDim.x) {
         const int pp = e & (r.spb - 1);
         const int jj = (e >> r.spb_log2) % r.m;
         const int uu = e < rowlen ? r.u : r.ub;
-        lds[e] = g[(static_cast<int64_t>(uu) * r.m + jj) * kPairsPerBlock + pp];
+        lds[e] = gload(g + (static_cast<int64_t>(uu) * r.m + jj) * kPairsPerBlock + pp);
     }
 }
 
-__global__ __launch_bounds__(256) void row_conv_kernel(float2* __restrict__ grid,
+// Generic row pass (long rows): the filter class rows go through the row DFT
+// first; their conjugate-symmetry separation leaves S and Df for every row-u
+// frequency in the third LDS buffer ([0][v] = S, [1][v] = Df).  Then the
+// document rows go through the same DFT, the product, the inverse row DFT and
+// back to the grid.  LDS: three buffers of two rows of m * spb values.
+template <class G>
+__global__ __launch_bounds__(256) void row_conv_kernel(G* __restrict__ grid,
                                                        int64_t grid_pb_stride,
-                                                       const float2* __restrict__ spec,
-                                                       int64_t spec_pb_stride, LaunchTables t,
+                                                       const G* __restrict__ fgrid,
+                                                       int64_t fgrid_pb_stride, LaunchTables t,
                                                        int n1) {
     extern __shared__ float2 sm[];
     const RowTask r = row_task(t, n1);
     const int pb = blockIdx.y;
     const int rowlen = r.m * r.spb;
-    float2* bufa = sm;
-    float2* bufb = sm + 2 * rowlen;
-    float2* g = grid + pb * grid_pb_stride + r.sg->grid_off * kPairsPerBlock + r.s * r.spb;
-    load_rows(bufa, g, r);
+    float2* b0 = sm;
+    float2* b1 = sm + 2 * rowlen;
+    float2* sdf = sm + 4 * rowlen;
+    const float2* twm = t.tw + r.sg->tw_off;
+
+    const G* fg = fgrid + pb * fgrid_pb_stride + static_cast<int64_t>(r.sg->spec_off) * kPairsPerBlock +
+                  r.s * r.spb;
+    load_rows(b0, fg, r);
+    __syncthreads();
+    const float2* zh = row_dft<-1>(b0, b1, r.nrows, r.m, r.spb, r.spb_log2, r.sg, twm);
+    const float c = 0.5f * sqrtf(static_cast<float>(n1)) / static_cast<float>(r.m);
+    for (int e = threadIdx.x; e < rowlen; e += blockDim.x) {
+        const int pp = e & (r.spb - 1);
+        const int v = e >> r.spb_log2;
+        const int vb = partner_col(r.u, v, r.m);
+        float2 s, df;
+        filter_sdf(zh[e], zh[((r.nrows - 1) * r.m + vb) * r.spb + pp], c, s, df);
+        sdf[e] = s;
+        sdf[rowlen + e] = df;
+    }
     __syncthreads();
 
-    const float2* twm = t.tw + r.sg->tw_off + n1;
-    float2* z = row_dft<-1>(bufa, bufb, r.nrows, r.m, r.spb, r.spb_log2, r.sg, twm);
-    float2* w = (z == bufa) ? bufb : bufa;
-
-    // W(f) = Z(f) S(f) + conj(Z(-f)) Df(f) and W(-f) = conj(conj(Z(-f)) S(f) + Z(f) Df(f)):
-    // the spectrum of y_d + i y_{d+1} (Algorithm 3, separation and product fused).
-    const float2* sp = spec + pb * spec_pb_stride +
-                       (static_cast<int64_t>(r.sg->spec_off) + static_cast<int64_t>(r.u) * r.m) *
-                           (2 * kPairsPerBlock) +
-                       2 * r.s * r.spb;
+    G* g = grid + pb * grid_pb_stride + r.sg->grid_off * kPairsPerBlock + r.s * r.spb;
+    load_rows(b0, g, r);
+    __syncthreads();
+    float2* z = row_dft<-1>(b0, b1, r.nrows, r.m, r.spb, r.spb_log2, r.sg, twm);
+    float2* w = (z == b0) ? b1 : b0;
     for (int e = threadIdx.x; e < rowlen; e += blockDim.x) {
         const int pp = e & (r.spb - 1);
         const int v = e >> r.spb_log2;
         const int vb = partner_col(r.u, v, r.m);
         const float2 a = z[e];
-        const float2 b = z[((r.nrows - 1) * r.m + vb) * r.spb + pp];
-        const float2 s = sp[(v * kPairsPerBlock + pp) * 2];
-        const float2 df = sp[(v * kPairsPerBlock + pp) * 2 + 1];
-        w[e] = cadd(cmul(a, s), cmul(cconj(b), df));
-        if (r.nrows == 2) w[(r.m + vb) * r.spb + pp] = cconj(cadd(cmul(cconj(b), s), cmul(a, df)));
+        const int eb = ((r.nrows - 1) * r.m + vb) * r.spb + pp;
+        const float2 b = z[eb];
+        const float2 s = sdf[e], df = sdf[rowlen + e];
+        w[e] = product_f(a, b, s, df);
+        if (r.nrows == 2) w[eb] = product_neg_f(a, b, s, df);
     }
     __syncthreads();
 
@@ -321,46 +401,7 @@ __global__ __launch_bounds__(256) void row_conv_kernel(float2* __restrict__ grid
         const int pp = e & (r.spb - 1);
         const int jj = (e >> r.spb_log2) % r.m;
         const int uu = e < rowlen ? r.u : r.ub;
-        g[(static_cast<int64_t>(uu) * r.m + jj) * kPairsPerBlock + pp] = y[e];
-    }
-}
-
-// Filter side: forward row DFT of the filter pair h_d + i h_{d+1}, then
-// H_d = (Z(f) + conj Z(-f)) / 2, H_{d+1} = (Z(f) - conj Z(-f)) / (2i) and the
-// stored combinations S = (H_d + H_{d+1}) / (2P), Df = (H_d - H_{d+1}) / (2P).
-__global__ __launch_bounds__(256) void row_spec_kernel(const float2* __restrict__ grid,
-                                                       int64_t grid_pb_stride,
-                                                       float2* __restrict__ spec,
-                                                       int64_t spec_pb_stride, LaunchTables t,
-                                                       int n1) {
-    extern __shared__ float2 sm[];
-    const RowTask r = row_task(t, n1);
-    const int pb = blockIdx.y;
-    const int rowlen = r.m * r.spb;
-    float2* bufa = sm;
-    float2* bufb = sm + 2 * rowlen;
-    const float2* g = grid + pb * grid_pb_stride + r.sg->grid_off * kPairsPerBlock + r.s * r.spb;
-    load_rows(bufa, g, r);
-    __syncthreads();
-
-    const float2* twm = t.tw + r.sg->tw_off + n1;
-    const float2* z = row_dft<-1>(bufa, bufb, r.nrows, r.m, r.spb, r.spb_log2, r.sg, twm);
-
-    const float c = 0.5f / static_cast<float>(r.sg->P);
-    float2* sp = spec + pb * spec_pb_stride +
-                 (static_cast<int64_t>(r.sg->spec_off) + static_cast<int64_t>(r.u) * r.m) *
-                     (2 * kPairsPerBlock) +
-                 2 * r.s * r.spb;
-    for (int e = threadIdx.x; e < rowlen; e += blockDim.x) {
-        const int pp = e & (r.spb - 1);
-        const int v = e >> r.spb_log2;
-        const int vb = partner_col(r.u, v, r.m);
-        const float2 a = z[e];
-        const float2 b = z[((r.nrows - 1) * r.m + vb) * r.spb + pp];
-        const float2 hd = make_float2(0.5f * (a.x + b.x), 0.5f * (a.y - b.y));
-        const float2 hd1 = make_float2(0.5f * (a.y + b.y), 0.5f * (b.x - a.x));
-        sp[(v * kPairsPerBlock + pp) * 2] = cscale(cadd(hd, hd1), c);
-        sp[(v * kPairsPerBlock + pp) * 2 + 1] = cscale(csub(hd, hd1), c);
+        gstore(g + (static_cast<int64_t>(uu) * r.m + jj) * kPairsPerBlock + pp, y[e]);
     }
 }
 
@@ -384,67 +425,111 @@ __global__ __launch_bounds__(256) void transpose_kernel(const float* __restrict_
 }
 
 // ---------------------------------------------------------------- launchers
-template <int R>
-static hipError_t col_fwd_r(int x_dtype, const void* src, int64_t rs, int D, float2* grid,
-                            int64_t gs, const LaunchTables& t, int n_cols, int npb,
-                            hipStream_t stream) {
-    dim3 g(n_cols, npb), b(16 * R);
+static int col_mode(int D) { return D % 32 == 0 ? kFull : (D % 2 == 0 ? kEven : kOdd); }
+
+template <int R, class G, int MODE>
+static hipError_t col_fwd_rgm(int x_dtype, const void* src, int64_t rs, int D, void* grid,
+                              int64_t gs, const LaunchTables& t, int n_cols, int npb,
+                              hipStream_t stream) {
+    const dim3 g(static_cast<unsigned>(n_cols) * npb), b(16 * R);
+    G* gp = static_cast<G*>(grid);
     if (x_dtype == 0)
-        hipLaunchKernelGGL((col_fwd_kernel<R, F32>), g, b, 0, stream, src, rs, D, grid, gs, t);
+        hipLaunchKernelGGL((col_fwd_kernel<R, F32, G, MODE>), g, b, 0, stream, src, rs, D, gp, gs,
+                           t, npb);
     else
-        hipLaunchKernelGGL((col_fwd_kernel<R, BF16>), g, b, 0, stream, src, rs, D, grid, gs, t);
+        hipLaunchKernelGGL((col_fwd_kernel<R, BF16, G, MODE>), g, b, 0, stream, src, rs, D, gp, gs,
+                           t, npb);
     return hipGetLastError();
 }
 
-hipError_t launch_col_fwd(int r, int x_dtype, const void* src, int64_t src_row_stride, int D,
-                          float2* grid, int64_t grid_pb_stride, const LaunchTables& t,
+template <int R, class G>
+static hipError_t col_fwd_rg(int x_dtype, const void* src, int64_t rs, int D, void* grid,
+                             int64_t gs, const LaunchTables& t, int n_cols, int npb,
+                             hipStream_t stream) {
+    switch (col_mode(D)) {
+        case kFull: return col_fwd_rgm<R, G, kFull>(x_dtype, src, rs, D, grid, gs, t, n_cols, npb, stream);
+        case kEven: return col_fwd_rgm<R, G, kEven>(x_dtype, src, rs, D, grid, gs, t, n_cols, npb, stream);
+        default: return col_fwd_rgm<R, G, kOdd>(x_dtype, src, rs, D, grid, gs, t, n_cols, npb, stream);
+    }
+}
+
+hipError_t launch_col_fwd(int r, bool half, int x_dtype, const void* src, int64_t src_row_stride,
+                          int D, void* grid, int64_t grid_pb_stride, const LaunchTables& t,
                           int n_cols, int npb, hipStream_t stream) {
     if (n_cols == 0) return hipSuccess;
     if (r == 16)
-        return col_fwd_r<16>(x_dtype, src, src_row_stride, D, grid, grid_pb_stride, t, n_cols, npb,
-                             stream);
-    return col_fwd_r<8>(x_dtype, src, src_row_stride, D, grid, grid_pb_stride, t, n_cols, npb,
-                        stream);
+        return half ? col_fwd_rg<16, __half2>(x_dtype, src, src_row_stride, D, grid, grid_pb_stride,
+                                              t, n_cols, npb, stream)
+                    : col_fwd_rg<16, float2>(x_dtype, src, src_row_stride, D, grid, grid_pb_stride,
+                                             t, n_cols, npb, stream);
+    return half ? col_fwd_rg<8, __half2>(x_dtype, src, src_row_stride, D, grid, grid_pb_stride, t,
+                                         n_cols, npb, stream)
+                : col_fwd_rg<8, float2>(x_dtype, src, src_row_stride, D, grid, grid_pb_stride, t,
+                                        n_cols, npb, stream);
 }
 
-template <int R>
-static hipError_t col_inv_r(int y_dtype, const float2* grid, int64_t gs, void* dst, int64_t rs,
-                            int D, const LaunchTables& t, int n_cols, int npb,
-                            hipStream_t stream) {
-    dim3 g(n_cols, npb), b(16 * R);
+template <int R, class G, int MODE>
+static hipError_t col_inv_rgm(int y_dtype, const void* grid, int64_t gs, void* dst, int64_t rs,
+                              int D, const LaunchTables& t, int n_cols, int npb,
+                              hipStream_t stream) {
+    const dim3 g(static_cast<unsigned>(n_cols) * npb), b(16 * R);
+    const G* gp = static_cast<const G*>(grid);
     if (y_dtype == 0)
-        hipLaunchKernelGGL((col_inv_kernel<R, F32>), g, b, 0, stream, grid, gs, dst, rs, D, t);
+        hipLaunchKernelGGL((col_inv_kernel<R, F32, G, MODE>), g, b, 0, stream, gp, gs, dst, rs, D,
+                           t, npb);
     else
-        hipLaunchKernelGGL((col_inv_kernel<R, BF16>), g, b, 0, stream, grid, gs, dst, rs, D, t);
+        hipLaunchKernelGGL((col_inv_kernel<R, BF16, G, MODE>), g, b, 0, stream, gp, gs, dst, rs, D,
+                           t, npb);
     return hipGetLastError();
 }
 
-hipError_t launch_col_inv(int r, int y_dtype, const float2* grid, int64_t grid_pb_stride,
+template <int R, class G>
+static hipError_t col_inv_rg(int y_dtype, const void* grid, int64_t gs, void* dst, int64_t rs,
+                             int D, const LaunchTables& t, int n_cols, int npb,
+                             hipStream_t stream) {
+    switch (col_mode(D)) {
+        case kFull: return col_inv_rgm<R, G, kFull>(y_dtype, grid, gs, dst, rs, D, t, n_cols, npb, stream);
+        case kEven: return col_inv_rgm<R, G, kEven>(y_dtype, grid, gs, dst, rs, D, t, n_cols, npb, stream);
+        default: return col_inv_rgm<R, G, kOdd>(y_dtype, grid, gs, dst, rs, D, t, n_cols, npb, stream);
+    }
+}
+
+hipError_t launch_col_inv(int r, bool half, int y_dtype, const void* grid, int64_t grid_pb_stride,
                           void* dst, int64_t dst_row_stride, int D, const LaunchTables& t,
                           int n_cols, int npb, hipStream_t stream) {
     if (n_cols == 0) return hipSuccess;
     if (r == 16)
-        return col_inv_r<16>(y_dtype, grid, grid_pb_stride, dst, dst_row_stride, D, t, n_cols, npb,
-                             stream);
-    return col_inv_r<8>(y_dtype, grid, grid_pb_stride, dst, dst_row_stride, D, t, n_cols, npb,
-                        stream);
+        return half ? col_inv_rg<16, __half2>(y_dtype, grid, grid_pb_stride, dst, dst_row_stride, D,
+                                              t, n_cols, npb, stream)
+                    : col_inv_rg<16, float2>(y_dtype, grid, grid_pb_stride, dst, dst_row_stride, D,
+                                             t, n_cols, npb, stream);
+    return half ? col_inv_rg<8, __half2>(y_dtype, grid, grid_pb_stride, dst, dst_row_stride, D, t,
+                                         n_cols, npb, stream)
+                : col_inv_rg<8, float2>(y_dtype, grid, grid_pb_stride, dst, dst_row_stride, D, t,
+                                        n_cols, npb, stream);
 }
 
-hipError_t launch_row_conv(int n1, float2* grid, int64_t grid_pb_stride, const float2* spec,
-                           int64_t spec_pb_stride, const LaunchTables& t, int n_tasks, int npb,
-                           int lds_bytes, hipStream_t stream) {
+hipError_t launch_row_conv(int n1, bool half, void* grid, int64_t grid_pb_stride,
+                           const void* fgrid, int64_t fgrid_pb_stride, const LaunchTables& t,
+                           int n_tasks, int npb, int lds_bytes, hipStream_t stream) {
     if (n_tasks == 0) return hipSuccess;
-    hipLaunchKernelGGL(row_conv_kernel, dim3(n_tasks, npb), dim3(256), lds_bytes, stream, grid,
-                       grid_pb_stride, spec, spec_pb_stride, t, n1);
-    return hipGetLastError();
-}
-
-hipError_t launch_row_spec(int n1, const float2* grid, int64_t grid_pb_stride, float2* spec,
-                           int64_t spec_pb_stride, const LaunchTables& t, int n_tasks, int npb,
-                           int lds_bytes, hipStream_t stream) {
-    if (n_tasks == 0) return hipSuccess;
-    hipLaunchKernelGGL(row_spec_kernel, dim3(n_tasks, npb), dim3(256), lds_bytes, stream, grid,
-                       grid_pb_stride, spec, spec_pb_stride, t, n1);
+    const dim3 g(n_tasks, npb), b(256);
+    hipError_t e;
+    if (half) {
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&row_conv_kernel<__half2>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(row_conv_kernel<__half2>, g, b, lds_bytes, stream,
+                           static_cast<__half2*>(grid), grid_pb_stride,
+                           static_cast<const __half2*>(fgrid), fgrid_pb_stride, t, n1);
+    } else {
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&row_conv_kernel<float2>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(row_conv_kernel<float2>, g, b, lds_bytes, stream,
+                           static_cast<float2*>(grid), grid_pb_stride,
+                           static_cast<const float2*>(fgrid), fgrid_pb_stride, t, n1);
+    }
     return hipGetLastError();
 }
 

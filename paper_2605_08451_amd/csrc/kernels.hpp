@@ -3,17 +3,20 @@
 //   col_fwd : N1-point column DFTs of every document column (the left DFT of
 //             Algorithm 1) and the per-document twiddle w_P^(u j);
 //   row     : m-point row DFTs inside each document only (the block-diagonal
-//             right DFT), then either the spectral product with conjugate-
-//             symmetry separation and the inverse row DFT (convolution), or
-//             the separation into the two filters' spectra (filter side);
+//             right DFT) of the document rows and of the same rows of the
+//             filter class grid, the conjugate-symmetry separation of the
+//             filter pair, the spectral product and the inverse row DFT;
 //   col_inv : the conjugate twiddle and the inverse N1-point column DFT, the
 //             store of positions t < L_i.
 //
-// Grid buffer layout (complex fp32): [pair block][segment grid point][16 pairs],
+// Grid buffer layout (complex fp32, or complex fp16 for bf16 inputs):
+// [pair block][segment grid point][16 pairs],
 // grid point of (u, j) in a segment = grid_off + u * m + j.
-// Spectrum layout: [pair block][class spectrum point][16 pairs][2], spectrum
-// point of (u, v), u <= N1/2, = spec_off + u * m + v; entry 0 is S = (H_d +
-// H_{d+1}) / (2P), entry 1 is Df = (H_d - H_{d+1}) / (2P).
+// The filter "spectrum" is the filter pairs' class grids after the column stage,
+// same layout, class grid point of (u, j) = spec_off + u * m + j.  The stored
+// grids are the DFTs scaled by 1 / sqrt(N1) (folded into the w_P^r table); the
+// row pass scales the filter spectra by sqrt(N1) / (2 m), so that
+// 1/sqrt(N1) * 1/m * 1/sqrt(N1) = 1/P overall and fp16 values stay O(|x|).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -35,28 +38,26 @@ struct LaunchTables {
     const int32_t* list;   // documents grouped by class / class identity list
 };
 
-hipError_t launch_col_fwd(int r, int x_dtype, const void* src, int64_t src_row_stride, int D,
-                          float2* grid, int64_t grid_pb_stride, const LaunchTables& t,
+// `half` selects complex fp16 grid and spectrum elements (complex fp32 otherwise).
+hipError_t launch_col_fwd(int r, bool half, int x_dtype, const void* src, int64_t src_row_stride,
+                          int D, void* grid, int64_t grid_pb_stride, const LaunchTables& t,
                           int n_cols, int npb, hipStream_t stream);
 
-hipError_t launch_col_inv(int r, int y_dtype, const float2* grid, int64_t grid_pb_stride,
+hipError_t launch_col_inv(int r, bool half, int y_dtype, const void* grid, int64_t grid_pb_stride,
                           void* dst, int64_t dst_row_stride, int D, const LaunchTables& t,
                           int n_cols, int npb, hipStream_t stream);
 
-hipError_t launch_row_conv(int n1, float2* grid, int64_t grid_pb_stride, const float2* spec,
-                           int64_t spec_pb_stride, const LaunchTables& t, int n_tasks, int npb,
-                           int lds_bytes, hipStream_t stream);
-
-hipError_t launch_row_spec(int n1, const float2* grid, int64_t grid_pb_stride, float2* spec,
-                           int64_t spec_pb_stride, const LaunchTables& t, int n_tasks, int npb,
-                           int lds_bytes, hipStream_t stream);
+// Row pass: row DFTs of the filter class rows and the document rows, the
+// separation and product, the inverse row DFT (generic kernel: long rows).
+hipError_t launch_row_conv(int n1, bool half, void* grid, int64_t grid_pb_stride,
+                           const void* fgrid, int64_t fgrid_pb_stride, const LaunchTables& t,
+                           int n_tasks, int npb, int lds_bytes, hipStream_t stream);
 
 // Register-resident row pass for a listed row size m (row_sizes.hpp) over the
-// nlist segments list[0..nlist) of that size; spec_mode selects the filter side.
-hipError_t launch_row_fast(int m, bool spec_mode, float2* grid, int64_t grid_pb_stride,
-                           float2* spec, int64_t spec_pb_stride, const Seg* segs,
-                           const int32_t* list, int nlist, const float2* tw, int n1, int npb,
-                           hipStream_t stream);
+// nlist documents list[0..nlist) of that size.
+hipError_t launch_row_fast(int m, bool half, void* grid, int64_t grid_pb_stride, const void* fgrid,
+                           int64_t fgrid_pb_stride, const Seg* segs, const int32_t* list,
+                           int nlist, const float2* tw, int n1, int npb, hipStream_t stream);
 
 hipError_t launch_transpose(const float* in, int rows, int cols, int in_ld, float* out,
                             int out_ld, hipStream_t stream);

@@ -15,7 +15,7 @@ namespace rubiconv {
 constexpr int kPairsPerBlock = 16;  // channel pairs per block: 16 * 8 B = 128 B of complex fp32
 constexpr int kMaxFactors = 14;     // radices of m (m <= 2048 has at most 11)
 constexpr int kMaxM = 2048;         // largest row DFT
-constexpr int kRowLdsBytes = 65536; // two ping-pong buffers of two rows each
+constexpr int kRowLdsBytes = 98304; // generic row kernel: three buffers of two rows each
 
 struct Seg {
     int32_t row;       // source row of x (documents) / 0 (filter classes)
@@ -25,8 +25,9 @@ struct Seg {
     int32_t P;
     int32_t cls;       // size class
     int64_t grid_off;  // first grid point of this segment in its grid buffer
-    int32_t tw_off;    // class twiddles: [tw_off, +N1) = w_P^r, [tw_off+N1, +m) = w_m^h
-    int32_t spec_off;  // class spectrum: first of (N1/2 + 1) * m points
+    int32_t tw_off;    // class roots w_m^h, h < m, at [tw_off, tw_off + m) (complex)
+    int32_t twf_off;   // class roots w_P^r / sqrt(N1), r < P, at [twf_off, twf_off + P)
+    int32_t spec_off;  // first grid point of the class's filter grid (the "spectrum" buffer)
     int32_t col0;      // first global column index of this segment
     int32_t task0;     // first global row-task index of this segment (generic row kernel)
     int32_t spb;       // pairs per row task (16, or fewer for long rows)
@@ -34,7 +35,7 @@ struct Seg {
     int32_t nlist;     // classes: number of documents in the class
     int32_t nfac;      // radices of m, applied in order
     int8_t fac[kMaxFactors];
-    int8_t pad_[2];
+    int8_t pad_[6];
 };
 static_assert(sizeof(Seg) % 8 == 0, "Seg must stay 8-byte aligned in arrays");
 

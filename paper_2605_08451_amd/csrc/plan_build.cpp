@@ -2,7 +2,8 @@
 //
 // For every document i of length L_i the causal padding rule of Algorithm 1
 // asks for a transform of at least L_i + min(L_i, L) - 1 points that N1
-// divides.  The row DFT size m_i is the smallest 2^a 3^b 5^c number with
+// divides.  The row DFT size m_i is the smallest size of row_sizes.hpp's list
+// (longer rows: the smallest 2^a 3^b 5^c number) with
 // N1 * m_i >= L_i + min(L_i, L) - 1: any such size gives the same exact
 // convolution on [0, L_i) because the circular wrap of the padded product lands
 // only on positions >= L_i.  Documents with equal m_i share a size class and
@@ -43,22 +44,22 @@ int factorize(int m, int8_t* fac) {
     return m == 1 ? n : -1;
 }
 
-// Pairs per row task: two ping-pong buffers of two rows of m * spb complex
-// floats must fit the row pass's LDS budget.
+// Pairs per row task of the generic row kernel: three LDS buffers of two rows
+// of m * spb complex floats must fit its LDS budget.
 int pairs_per_task(int m) {
     int spb = kPairsPerBlock;
     if (m <= kMaxFastM) return spb;  // register-resident kernel: 32 lines of m values in LDS
-    while (spb > 1 && 4 * m * spb * 8 > kRowLdsBytes) spb /= 2;
+    while (spb > 1 && 6 * m * spb * 8 > kRowLdsBytes) spb /= 2;
     return spb;
 }
 
-void push_twiddles(std::vector<float>& tw, int64_t count, int64_t period) {
+void push_twiddles(std::vector<float>& tw, int64_t count, int64_t period, double scale = 1.0) {
     const double two_pi = 6.283185307179586476925286766559;
     for (int64_t r = 0; r < count; ++r) {
         // forward root w_period^r = exp(-2 pi i r / period), angle reduced exactly
         double a = two_pi * static_cast<double>(r % period) / static_cast<double>(period);
-        tw.push_back(static_cast<float>(std::cos(a)));
-        tw.push_back(static_cast<float>(-std::sin(a)));
+        tw.push_back(static_cast<float>(scale * std::cos(a)));
+        tw.push_back(static_cast<float>(-scale * std::sin(a)));
     }
 }
 
@@ -86,6 +87,7 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
     HostPlan p;
     p.B = B; p.N = N; p.D = D; p.L = L; p.max_docs = max_docs; p.n1 = n1; p.r = r;
     p.x_dtype = x_dtype; p.y_dtype = y_dtype;
+    p.grid_half = x_dtype == 1;  // bf16 inputs: complex fp16 grids and spectra
     p.npb = ((D + 1) / 2 + kPairsPerBlock - 1) / kPairsPerBlock;
 
     // documents and their row DFT sizes
@@ -98,6 +100,8 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
             int64_t need = static_cast<int64_t>(len) + std::min(len, L) - 1;
             int64_t mmin = (need + n1 - 1) / n1;
             if (mmin > kMaxM) return BuildError::kUnsupported;
+            // column passes address a document with 32-bit buffer offsets
+            if (static_cast<int64_t>(n1) * mmin * D * 4 > (int64_t(1) << 30)) return BuildError::kUnsupported;
             // listed sizes have register-resident row kernels; longer rows are 5-smooth
             int m = fast_row_size(static_cast<int>(mmin));
             if (m == 0) m = smooth_ceil(static_cast<int>(mmin));
@@ -118,10 +122,11 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
         s.m = m; s.P = n1 * m; s.cls = kv.second;
         s.len = static_cast<int32_t>(std::min<int64_t>(L, (static_cast<int64_t>(s.P) + 1) / 2));
         s.tw_off = static_cast<int32_t>(p.tw.size() / 2);
-        push_twiddles(p.tw, n1, s.P);   // w_P^r, r < N1
-        push_twiddles(p.tw, m, m);      // w_m^h = w_P^(N1 h), h < m
-        s.spec_off = static_cast<int32_t>(p.spec_points);
-        p.spec_points += static_cast<int64_t>(n1 / 2 + 1) * m;
+        push_twiddles(p.tw, m, m);             // w_m^h, h < m (row DFTs)
+        s.twf_off = static_cast<int32_t>(p.tw.size() / 2);
+        // w_P^r / sqrt(N1), r < P: the per-document twiddle of the column passes, which
+        // also scale by 1/sqrt(N1) (a power of two, exact)
+        push_twiddles(p.tw, s.P, s.P, 1.0 / r);
         s.spb = pairs_per_task(m);
         s.nfac = factorize(m, s.fac);
         p.taps_max = std::max(p.taps_max, s.len);
@@ -131,7 +136,7 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
     // documents: class data, grid offsets, column and row-task tables
     for (auto& s : p.docs) {
         const Seg& c = p.classes[class_of_m[s.m]];
-        s.cls = c.cls; s.tw_off = c.tw_off; s.spec_off = c.spec_off;
+        s.cls = c.cls; s.tw_off = c.tw_off; s.twf_off = c.twf_off;
         s.spb = c.spb; s.nfac = c.nfac;
         std::copy(c.fac, c.fac + kMaxFactors, s.fac);
         s.grid_off = p.grid_points;
@@ -142,20 +147,16 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
         p.doc_col_seg.insert(p.doc_col_seg.end(), s.m, idx);
         if (s.m > kMaxFastM) {
             p.doc_task_seg.insert(p.doc_task_seg.end(), (n1 / 2 + 1) * (kPairsPerBlock / s.spb), idx);
-            p.row_lds_docs = std::max(p.row_lds_docs, 4 * s.m * s.spb * 8);
+            p.row_lds_docs = std::max(p.row_lds_docs, 6 * s.m * s.spb * 8);
         }
     }
     for (auto& s : p.classes) {
         s.grid_off = p.class_points;
+        s.spec_off = static_cast<int32_t>(s.grid_off);  // a class's own filter grid
         p.class_points += s.P;
         s.col0 = static_cast<int32_t>(p.cls_col_seg.size());
-        s.task0 = static_cast<int32_t>(p.cls_task_seg.size());
         int idx = static_cast<int>(&s - p.classes.data());
         p.cls_col_seg.insert(p.cls_col_seg.end(), s.m, idx);
-        if (s.m > kMaxFastM) {
-            p.cls_task_seg.insert(p.cls_task_seg.end(), (n1 / 2 + 1) * (kPairsPerBlock / s.spb), idx);
-            p.row_lds_classes = std::max(p.row_lds_classes, 4 * s.m * s.spb * 8);
-        }
         // documents of this class, in document order
         s.list0 = static_cast<int32_t>(p.class_docs.size());
         for (size_t i = 0; i < p.docs.size(); ++i)
@@ -163,6 +164,8 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
         s.nlist = static_cast<int32_t>(p.class_docs.size()) - s.list0;
         p.class_ident.push_back(s.cls);
     }
+    for (auto& s : p.docs) s.spec_off = p.classes[s.cls].spec_off;  // its class's filter grid
+    if (p.class_points > (int64_t(1) << 31) - 1) return BuildError::kUnsupported;
     push_twiddles(p.tw_n1, n1, n1);
     *out = std::move(p);
     return BuildError::kOk;

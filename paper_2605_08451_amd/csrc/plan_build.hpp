@@ -13,6 +13,7 @@ enum class BuildError { kOk, kArg, kSeqlens, kUnsupported };
 struct HostPlan {
     int B = 0, N = 0, D = 0, L = 0, max_docs = 0, n1 = 0, r = 0;  // n1 = r * r
     int x_dtype = 0, y_dtype = 0;
+    bool grid_half = false;             // complex fp16 grids and spectra (else complex fp32)
     int npb = 0;                        // channel-pair blocks of kPairsPerBlock pairs
     std::vector<Seg> docs;              // one per non-empty document, row order
     std::vector<int32_t> doc_index;     // index of each document inside its row
@@ -20,17 +21,14 @@ struct HostPlan {
     std::vector<int32_t> doc_col_seg;   // global column -> document
     std::vector<int32_t> doc_task_seg;  // global row task -> document
     std::vector<int32_t> cls_col_seg;   // global column -> class
-    std::vector<int32_t> cls_task_seg;  // global row task -> class
     std::vector<int32_t> class_docs;    // documents grouped by class (class order)
     std::vector<int32_t> class_ident;   // 0, 1, ..., n_classes - 1
     std::vector<float> tw;              // complex pairs (re, im), per class: N1 then m entries
     std::vector<float> tw_n1;           // complex pairs, w_N1^s for s < N1
     int64_t grid_points = 0;            // sum over documents of P_i
     int64_t class_points = 0;           // sum over classes of P
-    int64_t spec_points = 0;            // sum over classes of (N1/2 + 1) * m
     int32_t taps_max = 0;               // largest number of filter taps any class keeps
-    int32_t row_lds_docs = 0;           // dynamic LDS bytes of the row pass (documents)
-    int32_t row_lds_classes = 0;        // same for the filter classes
+    int32_t row_lds_docs = 0;           // dynamic LDS bytes of the generic row kernel
 };
 
 // Smallest 2^a 3^b 5^c >= v (v >= 1).

@@ -7,8 +7,8 @@
 #pragma once
 
 #define RUBICONV_ROW_SIZES(X)                                                                  \
-    X(1, 1, 1) X(2, 2, 1) X(3, 3, 1) X(4, 4, 1) X(5, 5, 1) X(6, 6, 1) X(8, 8, 1) X(9, 9, 1)    \
-    X(10, 10, 1) X(12, 12, 1) X(15, 15, 1) X(16, 16, 1) X(18, 6, 3) X(20, 5, 4) X(24, 6, 4)    \
+    X(1, 1, 1) X(2, 2, 1) X(3, 3, 1) X(4, 2, 2) X(5, 5, 1) X(6, 3, 2) X(8, 4, 2) X(9, 3, 3)    \
+    X(10, 5, 2) X(12, 4, 3) X(15, 5, 3) X(16, 4, 4) X(18, 6, 3) X(20, 5, 4) X(24, 6, 4)        \
     X(25, 5, 5) X(27, 9, 3) X(30, 6, 5) X(32, 8, 4) X(36, 6, 6) X(40, 8, 5) X(45, 9, 5)        \
     X(48, 8, 6) X(50, 10, 5) X(54, 9, 6) X(60, 10, 6) X(64, 8, 8) X(72, 9, 8) X(75, 15, 5)     \
     X(80, 10, 8) X(81, 9, 9) X(90, 10, 9) X(96, 12, 8) X(100, 10, 10) X(108, 12, 9)            \

