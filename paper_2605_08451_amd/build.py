@@ -3,7 +3,8 @@
     python -m paper_2605_08451_amd.build        # always rebuilds
 
 Each source is compiled to an object under ``_build/`` in parallel, then linked.
-Packed fp32 VALU instructions are disabled for every device compilation.
+Packed fp32 VALU instructions are disabled for every device compilation, and
+MFMA results are kept in ordinary VGPRs.
 """
 import concurrent.futures
 import os
@@ -17,7 +18,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "librubiconv.so")
 BUILD = os.path.join(ROOT, "_build")
-SOURCES = ["kernels.hip", "row_fast.hip", "plan_build.cpp", "rubiconv.cpp"]
+SOURCES = ["kernels.hip", "row_fast.hip", "col_mfma.hip", "plan_build.cpp", "rubiconv.cpp"]
 ARCH = "gfx950"
 
 
@@ -30,8 +31,10 @@ def hipcc() -> str:
 
 
 def _flags():
+    # MFMA results go straight to VGPRs (no accumulator-register copies)
     return ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+            "-mllvm", "-amdgpu-mfma-vgpr-form=1",
             "-Wall", "-Wno-unused-result", "-I", INCLUDE, "-I", CSRC]
 
 

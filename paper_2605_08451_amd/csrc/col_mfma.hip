@@ -1,0 +1,348 @@
+// col_mfma.hip -- column passes on the matrix cores (N1 = 256, complex fp16 grids).
+//
+// The N1 = 256-point column DFT of Algorithm 1 (the shared left DFT M1 = F_k) is
+// applied as two dense 16 x 16 complex DFT stages on v_mfma_f32_16x16x32, the
+// small DFT matrices being genuine dense contractions over a batch of 16
+// channel pairs.  A complex 16 x 16 matrix M acts on [re; im] as the real
+// 16 x 32 operands A_re = [Re M | -Im M] and A_im = [Im M | Re M], with the K
+// index interleaving (re, im) per input, so the bf16/fp16 pair of a channel
+// pair is one operand element pair as loaded.
+//
+// One wave = one grid column j of one document x one block of 16 channel pairs
+// (lane l: pair p = l % 16, lane group h = l / 16).  With a = 16 n1 + n2 and
+// u = k1 + 16 k2:
+//   stage 1: for each n2, D[k1][p] = sum_n1 w16^(k1 n1) X[16 n1 + n2][p]
+//            (lane group h holds n1 = h, h+4, h+8, h+12 on input, k1 = 4h..4h+3 on
+//            output);
+//   4 x 4 lane-group transposes (v_permlane32/16_swap) so that lane group h holds
+//            n2 = 4h..4h+3 for every k1;
+//   stage 2: for each k1, Y[k1 + 16 k2][p] = sum_n2 w16^(n2 k2) w256^(n2 k1) D[k1][n2][p]
+//            (the inner twiddle is folded into one matrix per k1; lane group h
+//            produces k2 = h, h+4, h+8, h+12);
+//   the per-document twiddle w_P^(u j) / sqrt(N1) on the fp32 result, stored as fp16.
+// The inverse runs the mirror image (conjugate twiddle on the fp16 input, inner
+// twiddle folded per n2, output rounded to y's type).  Stage-1 matrices of the
+// bf16 input are split hi + lo in bf16 so that the coefficients keep ~16 bits.
+#include <hip/hip_bf16.h>
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <type_traits>
+
+#include "fft_core.hpp"
+#include "kernels.hpp"
+
+namespace rubiconv {
+
+namespace {
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef __bf16 b8 __attribute__((ext_vector_type(8)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t pack_h2(float re, float im) {
+    const __half2 h = __float22half2_rn(make_float2(re, im));
+    return __builtin_bit_cast(uint32_t, h);
+}
+__device__ __forceinline__ float2 unpack_h2(uint32_t w) {
+    return __half22float2(__builtin_bit_cast(__half2, w));
+}
+__device__ __forceinline__ uint32_t pack_bf2(float re, float im) {
+    const __hip_bfloat162 h = __float22bfloat162_rn(make_float2(re, im));
+    uint32_t w;
+    __builtin_memcpy(&w, &h, 4);
+    return w;
+}
+
+__device__ __forceinline__ f4 mma_f16(u4 a, u4 b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8, a), __builtin_bit_cast(h8, b),
+                                                  c, 0, 0, 0);
+}
+__device__ __forceinline__ f4 mma_bf16(u4 a, u4 b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(b8, a),
+                                                   __builtin_bit_cast(b8, b), c, 0, 0, 0);
+}
+
+// 4 x 4 transpose of (register, lane group): afterwards r_g in lane group h holds
+// what r_h held in lane group g.
+__device__ __forceinline__ void lanegroup_transpose(uint32_t& r0, uint32_t& r1, uint32_t& r2,
+                                                    uint32_t& r3) {
+    const auto s02 = __builtin_amdgcn_permlane32_swap(r0, r2, false, false);
+    const auto s13 = __builtin_amdgcn_permlane32_swap(r1, r3, false, false);
+    const auto t01 = __builtin_amdgcn_permlane16_swap(s02[0], s13[0], false, false);
+    const auto t23 = __builtin_amdgcn_permlane16_swap(s02[1], s13[1], false, false);
+    r0 = t01[0];
+    r1 = t01[1];
+    r2 = t23[0];
+    r3 = t23[1];
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t doc_buffer(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes),
+                                             0x00020000);
+}
+
+constexpr int kF32In = 0;   // fp32 input pairs (filter taps): converted to fp16
+constexpr int kBf16In = 1;  // bf16 input pairs: used as bf16 operands as loaded
+
+template <int IN>
+__global__ __launch_bounds__(256) void col_fwd_mfma_kernel(const void* __restrict__ src,
+                                                           int64_t src_row_stride, int D,
+                                                           uint32_t* __restrict__ grid,
+                                                           int64_t grid_pb_stride, LaunchTables t,
+                                                           const u4* __restrict__ mt, int npb,
+                                                           int ntasks) {
+    const int lane = threadIdx.x & 63;
+    // wave-uniform task index: keeps the document's buffer resource in SGPRs
+    const int task = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (task >= ntasks) return;  // whole wave; the kernel has no barriers
+    const int col = task / npb, pb = task - col * npb;
+    const Seg* sg = t.segs + t.col_seg[col];
+    const int j = col - sg->col0, m = sg->m, len = sg->len;
+    const int p = lane & 15, h = lane >> 4;
+    const int ch = 2 * (pb * kPairsPerBlock + p);
+    constexpr int ES = IN == kBf16In ? 2 : 4;
+
+    const char* doc = static_cast<const char*>(src) +
+                      (static_cast<int64_t>(sg->row) * src_row_stride +
+                       static_cast<int64_t>(sg->start) * D) * ES;
+    const __amdgpu_buffer_rsrc_t rs = doc_buffer(doc, static_cast<uint32_t>(len) * D * ES);
+
+    // stage 1: one MFMA tile per n2 (bf16: hi and lo matrix halves accumulate).
+    // Token t = m (16 n1 + n2) + j with n1 = 4i + h (operand slot 4h + i; the
+    // matrix tables use the same interleaving): a lane part and a wave-uniform part.
+    // All loads are issued before the first MFMA so that the wave waits once.
+    u4 xb[16];
+    {
+        uint32_t lane_off[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            lane_off[i] = (static_cast<uint32_t>(m) * 16u * (4 * i + h) * D + ch) * ES;
+#pragma unroll
+        for (int n2 = 0; n2 < 16; ++n2) {
+            const uint32_t wave_off = static_cast<uint32_t>(m * n2 + j) * D * ES;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int off = static_cast<int>(lane_off[i] + wave_off);
+                if constexpr (IN == kBf16In) {
+                    xb[n2][i] = __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
+                } else {
+                    const auto w = __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0);
+                    xb[n2][i] = pack_h2(__uint_as_float(w[0]), __uint_as_float(w[1]));
+                }
+            }
+        }
+    }
+    // per-document twiddle w_P^(u j) = w_P^(k1 j) * w_P^(16 k2 j), u = k1 + 16 k2: the first
+    // factor is wave-uniform, the second has four values per lane (k2 = 4 r2 + h)
+    const __amdgpu_buffer_rsrc_t rt = doc_buffer(t.tw + sg->twf_off, static_cast<uint32_t>(sg->P) * 8);
+    float2 tw_lane[4];
+#pragma unroll
+    for (int r2 = 0; r2 < 4; ++r2) {
+        const auto w = __builtin_amdgcn_raw_buffer_load_b64(
+            rt, static_cast<int>(16u * (4 * r2 + h) * j * 8), 0, 0);
+        tw_lane[r2] = make_float2(__uint_as_float(w[0]), __uint_as_float(w[1]));
+    }
+    u4 a[4];
+    if constexpr (IN == kBf16In) {
+#pragma unroll
+        for (int o = 0; o < 4; ++o) a[o] = mt[kMtFwd1Bf16 + o * 64 + lane];
+    } else {
+#pragma unroll
+        for (int o = 0; o < 2; ++o) a[o] = mt[kMtFwd1F16 + o * 64 + lane];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    uint32_t y[16][4];
+#pragma unroll
+    for (int n2 = 0; n2 < 16; ++n2) {
+        const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+        f4 dre, dim;
+        if constexpr (IN == kBf16In) {
+            dre = mma_bf16(a[1], xb[n2], mma_bf16(a[0], xb[n2], zero));
+            dim = mma_bf16(a[3], xb[n2], mma_bf16(a[2], xb[n2], zero));
+        } else {
+            dre = mma_f16(a[0], xb[n2], zero);
+            dim = mma_f16(a[1], xb[n2], zero);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) y[n2][r] = pack_h2(dre[r], dim[r]);
+    }
+    // y[n2][r] = D[k1 = 4h + r][n2]; regroup so that lane group h holds n2 = 4h + r'
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int rp = 0; rp < 4; ++rp)
+            lanegroup_transpose(y[rp][r], y[4 + rp][r], y[8 + rp][r], y[12 + rp][r]);
+
+    // stage 2 per k1 = 4g + r, then the per-document twiddle and the fp16 store
+    const float2* twf = t.tw + sg->twf_off;
+    const __amdgpu_buffer_rsrc_t rg =
+        doc_buffer(grid + pb * grid_pb_stride + sg->grid_off * kPairsPerBlock,
+                   static_cast<uint32_t>(sg->P) * kPairsPerBlock * 4);
+    const uint32_t g_lane = (static_cast<uint32_t>(j) * kPairsPerBlock + p) * 4;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int k1 = 4 * g + r;
+            const u4 b = {y[4 * g][r], y[4 * g + 1][r], y[4 * g + 2][r], y[4 * g + 3][r]};
+            const u4 are = mt[kMtFwd2 + (2 * k1) * 64 + lane];
+            const u4 aim = mt[kMtFwd2 + (2 * k1 + 1) * 64 + lane];
+            const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+            const f4 dre = mma_f16(are, b, zero);
+            const f4 dim = mma_f16(aim, b, zero);
+            // both table factors carry 1/sqrt(N1): undo one (x 16, exact)
+            const float2 tk = cscale(twf[k1 * j], 16.0f);  // wave-uniform
+#pragma unroll
+            for (int r2 = 0; r2 < 4; ++r2) {
+                const uint32_t u = static_cast<uint32_t>(k1 + 16 * (4 * r2 + h));  // k2 = 4 r2 + h
+                const float2 z = cmul(cmul(make_float2(dre[r2], dim[r2]), tk), tw_lane[r2]);
+                __builtin_amdgcn_raw_buffer_store_b32(
+                    pack_h2(z.x, z.y), rg, static_cast<int>(u * m * (kPairsPerBlock * 4) + g_lane), 0, 0);
+            }
+        }
+    }
+}
+
+template <class TY>
+__global__ __launch_bounds__(256) void col_inv_mfma_kernel(const uint32_t* __restrict__ grid,
+                                                           int64_t grid_pb_stride,
+                                                           void* __restrict__ dst,
+                                                           int64_t dst_row_stride, int D,
+                                                           LaunchTables t,
+                                                           const u4* __restrict__ mt, int npb,
+                                                           int ntasks) {
+    const int lane = threadIdx.x & 63;
+    const int task = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (task >= ntasks) return;
+    const int col = task / npb, pb = task - col * npb;
+    const Seg* sg = t.segs + t.col_seg[col];
+    const int j = col - sg->col0, m = sg->m, len = sg->len;
+    const int p = lane & 15, h = lane >> 4;
+    const int ch = 2 * (pb * kPairsPerBlock + p);
+
+    // stage 1 per k1: conjugate twiddle on the input, DFT over k2 -> n2.  All grid
+    // loads are issued first; w_P^(u j) = w_P^(k1 j) * w_P^(16 k2 j) with k2 = 4i + h.
+    const __amdgpu_buffer_rsrc_t rt = doc_buffer(t.tw + sg->twf_off, static_cast<uint32_t>(sg->P) * 8);
+    const __amdgpu_buffer_rsrc_t rg =
+        doc_buffer(grid + pb * grid_pb_stride + sg->grid_off * kPairsPerBlock,
+                   static_cast<uint32_t>(sg->P) * kPairsPerBlock * 4);
+    const uint32_t g_lane = (static_cast<uint32_t>(j) * kPairsPerBlock + p) * 4;
+    u4 yg[16];
+#pragma unroll
+    for (int k1 = 0; k1 < 16; ++k1)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t u = static_cast<uint32_t>(k1 + 16 * (4 * i + h));
+            yg[k1][i] = __builtin_amdgcn_raw_buffer_load_b32(
+                rg, static_cast<int>(u * m * (kPairsPerBlock * 4) + g_lane), 0, 0);
+        }
+    float2 tw_lane[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const auto w = __builtin_amdgcn_raw_buffer_load_b64(
+            rt, static_cast<int>(16u * (4 * i + h) * j * 8), 0, 0);
+        tw_lane[i] = make_float2(__uint_as_float(w[0]), -__uint_as_float(w[1]));  // conjugate
+    }
+    const u4 are1 = mt[kMtInv1 + lane];
+    const u4 aim1 = mt[kMtInv1 + 64 + lane];
+    const float2* twf = t.tw + sg->twf_off;
+    __builtin_amdgcn_sched_barrier(0);
+
+    uint32_t z[16][4];
+#pragma unroll
+    for (int k1 = 0; k1 < 16; ++k1) {
+        const float2 tk = cscale(cconj(twf[k1 * j]), 16.0f);  // wave-uniform
+        u4 b;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float2 v = cmul(cmul(unpack_h2(yg[k1][i]), tk), tw_lane[i]);
+            b[i] = pack_h2(v.x, v.y);
+        }
+        const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+        const f4 dre = mma_f16(are1, b, zero);
+        const f4 dim = mma_f16(aim1, b, zero);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) z[k1][r] = pack_h2(dre[r], dim[r]);
+    }
+    // z[k1][r] = Z[k1][n2 = 4h + r]; regroup so that lane group h holds k1 = 4h + r'
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int rp = 0; rp < 4; ++rp)
+            lanegroup_transpose(z[rp][r], z[4 + rp][r], z[8 + rp][r], z[12 + rp][r]);
+
+    constexpr int ES = std::is_same<TY, F32>::value ? 4 : 2;
+    char* doc = static_cast<char*>(dst) + (static_cast<int64_t>(sg->row) * dst_row_stride +
+                                           static_cast<int64_t>(sg->start) * D) * ES;
+    const __amdgpu_buffer_rsrc_t rs = doc_buffer(doc, static_cast<uint32_t>(len) * D * ES);
+    uint32_t lane_off[4];  // token t = m (16 n1 + n2) + j, n1 = 4 r2 + h
+#pragma unroll
+    for (int r2 = 0; r2 < 4; ++r2)
+        lane_off[r2] = (static_cast<uint32_t>(m) * 16u * (4 * r2 + h) * D + ch) * ES;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int n2 = 4 * g + r;
+            const u4 b = {z[4 * g][r], z[4 * g + 1][r], z[4 * g + 2][r], z[4 * g + 3][r]};
+            const u4 are = mt[kMtInv2 + (2 * n2) * 64 + lane];
+            const u4 aim = mt[kMtInv2 + (2 * n2 + 1) * 64 + lane];
+            const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+            const f4 dre = mma_f16(are, b, zero);
+            const f4 dim = mma_f16(aim, b, zero);
+#pragma unroll
+            for (int r2 = 0; r2 < 4; ++r2) {
+                const int off = static_cast<int>(lane_off[r2] + static_cast<uint32_t>(m * n2 + j) * D * ES);
+                if constexpr (std::is_same<TY, F32>::value) {
+                    const u2 w = {__float_as_uint(dre[r2]), __float_as_uint(dim[r2])};
+                    __builtin_amdgcn_raw_buffer_store_b64(w, rs, off, 0, 0);
+                } else {
+                    __builtin_amdgcn_raw_buffer_store_b32(pack_bf2(dre[r2], dim[r2]), rs, off, 0, 0);
+                }
+            }
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_col_fwd_mfma(int x_dtype, const void* src, int64_t src_row_stride, int D,
+                               void* grid, int64_t grid_pb_stride, const LaunchTables& t,
+                               const void* mtab, int n_cols, int npb, hipStream_t stream) {
+    if (n_cols == 0) return hipSuccess;
+    const int ntasks = n_cols * npb;
+    const dim3 g((ntasks + 3) / 4), b(256);
+    const u4* mt = static_cast<const u4*>(mtab);
+    uint32_t* gp = static_cast<uint32_t*>(grid);
+    if (x_dtype == 1)
+        hipLaunchKernelGGL(col_fwd_mfma_kernel<kBf16In>, g, b, 0, stream, src, src_row_stride, D, gp,
+                           grid_pb_stride, t, mt, npb, ntasks);
+    else
+        hipLaunchKernelGGL(col_fwd_mfma_kernel<kF32In>, g, b, 0, stream, src, src_row_stride, D, gp,
+                           grid_pb_stride, t, mt, npb, ntasks);
+    return hipGetLastError();
+}
+
+hipError_t launch_col_inv_mfma(int y_dtype, const void* grid, int64_t grid_pb_stride, void* dst,
+                               int64_t dst_row_stride, int D, const LaunchTables& t,
+                               const void* mtab, int n_cols, int npb, hipStream_t stream) {
+    if (n_cols == 0) return hipSuccess;
+    const int ntasks = n_cols * npb;
+    const dim3 g((ntasks + 3) / 4), b(256);
+    const u4* mt = static_cast<const u4*>(mtab);
+    const uint32_t* gp = static_cast<const uint32_t*>(grid);
+    if (y_dtype == 1)
+        hipLaunchKernelGGL(col_inv_mfma_kernel<BF16>, g, b, 0, stream, gp, grid_pb_stride, dst,
+                           dst_row_stride, D, t, mt, npb, ntasks);
+    else
+        hipLaunchKernelGGL(col_inv_mfma_kernel<F32>, g, b, 0, stream, gp, grid_pb_stride, dst,
+                           dst_row_stride, D, t, mt, npb, ntasks);
+    return hipGetLastError();
+}
+
+}  // namespace rubiconv

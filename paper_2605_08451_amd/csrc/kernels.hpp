@@ -59,6 +59,24 @@ hipError_t launch_row_fast(int m, bool half, void* grid, int64_t grid_pb_stride,
                            int64_t fgrid_pb_stride, const Seg* segs, const int32_t* list,
                            int nlist, const float2* tw, int n1, int npb, hipStream_t stream);
 
+// Matrix-core column passes (N1 = 256, complex fp16 grids, D a multiple of 32).
+// `mtab` holds the MFMA operand tables in lane order (16-byte entries, offsets
+// below; see build_mfma_tables).
+constexpr int kMtFwd1Bf16 = 0;     // forward stage 1, bf16 hi/lo: re_hi, re_lo, im_hi, im_lo
+constexpr int kMtFwd1F16 = 256;    // forward stage 1, fp16: re, im
+constexpr int kMtFwd2 = 384;       // forward stage 2 per k1: re, im
+constexpr int kMtInv1 = 2432;      // inverse stage 1: re, im
+constexpr int kMtInv2 = 2560;      // inverse stage 2 per n2: re, im
+constexpr int kMtEntries = 4608;
+
+hipError_t launch_col_fwd_mfma(int x_dtype, const void* src, int64_t src_row_stride, int D,
+                               void* grid, int64_t grid_pb_stride, const LaunchTables& t,
+                               const void* mtab, int n_cols, int npb, hipStream_t stream);
+
+hipError_t launch_col_inv_mfma(int y_dtype, const void* grid, int64_t grid_pb_stride, void* dst,
+                               int64_t dst_row_stride, int D, const LaunchTables& t,
+                               const void* mtab, int n_cols, int npb, hipStream_t stream);
+
 hipError_t launch_transpose(const float* in, int rows, int cols, int in_ld, float* out,
                             int out_ld, hipStream_t stream);
 

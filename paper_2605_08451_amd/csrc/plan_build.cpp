@@ -17,6 +17,8 @@
 
 #include <algorithm>
 #include <cmath>
+#include <complex>
+#include <cstring>
 #include <map>
 
 namespace rubiconv {
@@ -63,7 +65,91 @@ void push_twiddles(std::vector<float>& tw, int64_t count, int64_t period, double
     }
 }
 
+uint16_t to_f16_bits(double v) {
+    const _Float16 h = static_cast<_Float16>(static_cast<float>(v));  // round to nearest even
+    uint16_t b;
+    std::memcpy(&b, &h, 2);
+    return b;
+}
+
+uint16_t to_bf16_bits(float f) {
+    uint32_t u;
+    std::memcpy(&u, &f, 4);
+    u += 0x7fffu + ((u >> 16) & 1u);  // finite inputs only
+    return static_cast<uint16_t>(u >> 16);
+}
+
+float bf16_value(uint16_t b) {
+    const uint32_t u = static_cast<uint32_t>(b) << 16;
+    float f;
+    std::memcpy(&f, &u, 4);
+    return f;
+}
+
+// One 16 x 16 complex matrix M (row = output, column = input) as the two real
+// 16 x 32 MFMA A-operands A_re = [Re M | -Im M], A_im = [Im M | Re M] with the
+// K index interleaving (re, im) of each input; lane l holds row l % 16 and
+// K = 8 (l / 16) .. + 7.  kind: 0 = fp16, 1 = bf16 high part, 2 = bf16 low part.
+template <class F>
+void push_operands(std::vector<uint32_t>* out, F entry, int kind) {
+    for (int part = 0; part < 2; ++part) {  // 0: output real part, 1: output imaginary part
+        for (int lane = 0; lane < 64; ++lane) {
+            uint16_t hv[8];
+            for (int i = 0; i < 8; ++i) {
+                const int row = lane % 16, kk = 8 * (lane / 16) + i, n = kk / 2, c = kk % 2;
+                const std::complex<double> mv = entry(row, n);
+                double v = part == 0 ? (c == 0 ? mv.real() : -mv.imag())
+                                     : (c == 0 ? mv.imag() : mv.real());
+                if (kind == 0) {
+                    hv[i] = to_f16_bits(v);
+                } else {
+                    const uint16_t hi = to_bf16_bits(static_cast<float>(v));
+                    hv[i] = kind == 1 ? hi : to_bf16_bits(static_cast<float>(v - bf16_value(hi)));
+                }
+            }
+            for (int w = 0; w < 4; ++w) out->push_back(hv[2 * w] | (static_cast<uint32_t>(hv[2 * w + 1]) << 16));
+        }
+    }
+}
+
+// Index assigned to operand slot s = 4h + i (lane group h, slot i): 4i + h, so
+// that the four lane groups of one load or store instruction touch neighbouring
+// grid rows (an involution).
+int interleave(int s) { return 4 * (s % 4) + s / 4; }
+
+std::complex<double> root(double num, double den) {  // exp(2 pi i num / den)
+    const double a = 6.283185307179586476925286766559 * num / den;
+    return {std::cos(a), std::sin(a)};
+}
+
 }  // namespace
+
+void build_mfma_tables(std::vector<uint32_t>* out) {
+    out->clear();
+    // stage 1 contracts over the interleaved input slot; stage 2 produces the
+    // interleaved output slot (kernels address rows accordingly)
+    auto fwd1 = [](int k1, int s) { return root(-static_cast<double>(k1 * interleave(s)), 16); };
+    // forward stage 1 in bf16 hi/lo: (re_hi, re_lo, im_hi, im_lo)
+    std::vector<uint32_t> hi, lo;
+    push_operands(&hi, fwd1, 1);
+    push_operands(&lo, fwd1, 2);
+    out->insert(out->end(), hi.begin(), hi.begin() + 256);          // re_hi
+    out->insert(out->end(), lo.begin(), lo.begin() + 256);          // re_lo
+    out->insert(out->end(), hi.begin() + 256, hi.end());            // im_hi
+    out->insert(out->end(), lo.begin() + 256, lo.end());            // im_lo
+    push_operands(out, fwd1, 0);                                    // forward stage 1, fp16
+    for (int k1 = 0; k1 < 16; ++k1)                                 // stage 2, twiddle folded
+        push_operands(out, [k1](int s, int n2) {
+            const int k2 = interleave(s);
+            return root(-static_cast<double>(n2 * k2), 16) * root(-static_cast<double>(n2 * k1), 256);
+        }, 0);
+    push_operands(out, [](int n2, int s) { return root(static_cast<double>(n2 * interleave(s)), 16); }, 0);
+    for (int n2 = 0; n2 < 16; ++n2)
+        push_operands(out, [n2](int s, int k1) {
+            const int n1 = interleave(s);
+            return root(static_cast<double>(n1 * k1), 16) * root(static_cast<double>(n2 * k1), 256);
+        }, 0);
+}
 
 BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_docs,
                            const int32_t* cu, int x_dtype, int y_dtype, int n1) {
@@ -167,6 +253,9 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
     for (auto& s : p.docs) s.spec_off = p.classes[s.cls].spec_off;  // its class's filter grid
     if (p.class_points > (int64_t(1) << 31) - 1) return BuildError::kUnsupported;
     push_twiddles(p.tw_n1, n1, n1);
+    // bf16 inputs, N1 = 256 and whole 32-channel blocks: column passes on the matrix cores
+    p.col_mfma = p.grid_half && n1 == 256 && D % 32 == 0;
+    if (p.col_mfma) build_mfma_tables(&p.mfma_tab);
     *out = std::move(p);
     return BuildError::kOk;
 }

@@ -25,6 +25,8 @@ struct HostPlan {
     std::vector<int32_t> class_ident;   // 0, 1, ..., n_classes - 1
     std::vector<float> tw;              // complex pairs (re, im), per class: N1 then m entries
     std::vector<float> tw_n1;           // complex pairs, w_N1^s for s < N1
+    std::vector<uint32_t> mfma_tab;     // matrix-core operand tables (N1 = 256 only)
+    bool col_mfma = false;              // column passes on the matrix cores
     int64_t grid_points = 0;            // sum over documents of P_i
     int64_t class_points = 0;           // sum over classes of P
     int32_t taps_max = 0;               // largest number of filter taps any class keeps
@@ -33,6 +35,10 @@ struct HostPlan {
 
 // Smallest 2^a 3^b 5^c >= v (v >= 1).
 int smooth_ceil(int v);
+
+// MFMA operand tables of the N1 = 256 matrix-core column passes (kMtEntries
+// 16-byte entries, 4 x uint32 each, in the order of kernels.hpp's kMt* offsets).
+void build_mfma_tables(std::vector<uint32_t>* out);
 
 // Validates cu_seqlens and fills every table of *out.
 BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_docs,

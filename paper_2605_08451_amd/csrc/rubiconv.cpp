@@ -26,6 +26,7 @@ using rubiconv::Seg;
 struct rubiconv_plan_s {
     HostPlan h;
     void* dev = nullptr;  // all device tables, one allocation
+    const void* mfma_tab = nullptr;  // matrix-core operand tables (inside dev)
     bool device_ready = false;
     LaunchTables doc_t{};
     LaunchTables cls_t{};
@@ -59,6 +60,7 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     const size_t o_twn = off;        off = align_up(off + h.tw_n1.size() * 4);
     const size_t o_cdoc = off;       off = align_up(off + h.class_docs.size() * 4);
     const size_t o_cid = off;        off = align_up(off + h.class_ident.size() * 4);
+    const size_t o_mt = off;         off = align_up(off + h.mfma_tab.size() * 4);
     const size_t total = off;
 
     std::vector<unsigned char> img(total, 0);
@@ -72,6 +74,7 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     std::memcpy(img.data() + o_twn, h.tw_n1.data(), h.tw_n1.size() * 4);
     std::memcpy(img.data() + o_cdoc, h.class_docs.data(), h.class_docs.size() * 4);
     std::memcpy(img.data() + o_cid, h.class_ident.data(), h.class_ident.size() * 4);
+    if (!h.mfma_tab.empty()) std::memcpy(img.data() + o_mt, h.mfma_tab.data(), h.mfma_tab.size() * 4);
 
     int count = 0;
     hipError_t e = hipGetDeviceCount(&count);
@@ -100,6 +103,7 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     pl->cls_t = LaunchTables{dsegs + h.docs.size(), reinterpret_cast<const int32_t*>(base + o_ccol),
                              nullptr, tw, twn,
                              reinterpret_cast<const int32_t*>(base + o_cid)};
+    pl->mfma_tab = base + o_mt;
     pl->device_ready = true;
     return RUBICONV_OK;
 }
@@ -194,9 +198,13 @@ rubiconv_status_t rubiconv_filter_spectrum(rubiconv_plan_t plan, const float* fi
     hipError_t e = rubiconv::launch_transpose(filters, h.D, h.taps_max, h.L, taps, h.D, stream);
     rec.mark("filter_transpose");
     if (e == hipSuccess)
-        e = rubiconv::launch_col_fwd(h.r, h.grid_half, 0, taps, 0, h.D, spectrum,
-                                     plan->cls_pb_stride, plan->cls_t,
-                                     static_cast<int>(h.cls_col_seg.size()), h.npb, stream);
+        e = h.col_mfma
+                ? rubiconv::launch_col_fwd_mfma(0, taps, 0, h.D, spectrum, plan->cls_pb_stride,
+                                                plan->cls_t, plan->mfma_tab,
+                                                static_cast<int>(h.cls_col_seg.size()), h.npb, stream)
+                : rubiconv::launch_col_fwd(h.r, h.grid_half, 0, taps, 0, h.D, spectrum,
+                                           plan->cls_pb_stride, plan->cls_t,
+                                           static_cast<int>(h.cls_col_seg.size()), h.npb, stream);
     rec.mark("filter_col_fwd");
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }
@@ -215,9 +223,13 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
     const int64_t rs = static_cast<int64_t>(h.N) * h.D;
     StageRecorder rec(plan, stream);
     const bool half = h.grid_half;
-    hipError_t e = rubiconv::launch_col_fwd(h.r, half, h.x_dtype, x, rs, h.D, workspace,
-                                            plan->grid_pb_stride, plan->doc_t, n_cols, h.npb,
-                                            stream);
+    hipError_t e = h.col_mfma
+                       ? rubiconv::launch_col_fwd_mfma(h.x_dtype, x, rs, h.D, workspace,
+                                                       plan->grid_pb_stride, plan->doc_t,
+                                                       plan->mfma_tab, n_cols, h.npb, stream)
+                       : rubiconv::launch_col_fwd(h.r, half, h.x_dtype, x, rs, h.D, workspace,
+                                                  plan->grid_pb_stride, plan->doc_t, n_cols, h.npb,
+                                                  stream);
     rec.mark("col_fwd");
     if (e == hipSuccess && !h.doc_task_seg.empty()) {
         e = rubiconv::launch_row_conv(h.n1, half, workspace, plan->grid_pb_stride, spectrum,
@@ -236,8 +248,12 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
         rec.mark("row_conv_m" + std::to_string(cs.m));
     }
     if (e == hipSuccess)
-        e = rubiconv::launch_col_inv(h.r, half, h.y_dtype, workspace, plan->grid_pb_stride, y, rs,
-                                     h.D, plan->doc_t, n_cols, h.npb, stream);
+        e = h.col_mfma ? rubiconv::launch_col_inv_mfma(h.y_dtype, workspace, plan->grid_pb_stride, y,
+                                                       rs, h.D, plan->doc_t, plan->mfma_tab, n_cols,
+                                                       h.npb, stream)
+                       : rubiconv::launch_col_inv(h.r, half, h.y_dtype, workspace,
+                                                  plan->grid_pb_stride, y, rs, h.D, plan->doc_t,
+                                                  n_cols, h.npb, stream);
     rec.mark("col_inv");
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }

@@ -166,3 +166,17 @@ def test_plan_reused_with_two_filters(device):
         y = rc.packed_conv(plan, x, spec, workspace=ws)
         torch.cuda.synchronize()
         assert_parity(y.cpu().numpy().astype(np.float64), reference(W), W.cu_seqlens, "f32")
+
+
+@pytest.mark.parametrize("D", [32, 96])
+@pytest.mark.parametrize("y_dtype", ["bf16", "f32"])
+def test_matrix_core_column_path(device, D, y_dtype):
+    """bf16 inputs with whole 32-channel blocks take the matrix-core column passes:
+    documents of length 1, N1 - 1, N1, N1 + 1, whole rows, short and long filters."""
+    rng = np.random.default_rng(D)
+    N = 3000
+    rows = [[N], [1, 255, 256, 257, 1, 2230], wl.random_rows(rng, 1, N, 700, p_short=0.4)[0]]
+    for L in (5, 600, N):
+        W = wl.make_case(rows, D=D, L=L, x_dtype="bf16", seed=L + D)
+        y, _ = run_gpu(W, device, y_dtype=y_dtype)
+        assert_parity(y, reference(W), W.cu_seqlens, "bf16", f"D={D} L={L} y={y_dtype}")
