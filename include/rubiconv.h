@@ -31,8 +31,11 @@
  *     passes; the library owns only the plan and the plan's device tables.
  *   - Calls taking a stream enqueue work on it and return without waiting.
  *     They never synchronise the device, never allocate device memory and
- *     never print.  The plan may be used from several streams at once as long
- *     as each call has its own workspace (and output).
+ *     never print.  The plan may be used from several streams and host threads
+ *     at once as long as each call has its own workspace (and output).
+ *     rubiconv_packed_conv forks independent launches onto side streams owned
+ *     by the plan and joins them back into the caller's stream with events, so
+ *     the call remains ordered on the caller's stream (and capturable).
  *   - Every call returns a status; nothing is thrown across the ABI.  Argument
  *     errors are detected on the host before anything is enqueued.
  */

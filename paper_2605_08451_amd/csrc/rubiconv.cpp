@@ -9,6 +9,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -35,6 +36,14 @@ struct rubiconv_plan_s {
     size_t taps_bytes = 0;       // transposed filter taps (workspace of the filter call)
     size_t spec_bytes = 0;
     size_t ws_bytes = 0;
+    // The row pass runs its size classes (independent launches) on side streams
+    // forked from and joined back into the caller's stream with events; the mutex
+    // keeps one call's record/wait sequence from interleaving with another's.
+    static constexpr int kSideStreams = 4;
+    hipStream_t side[kSideStreams] = {};
+    hipEvent_t fork = nullptr;
+    hipEvent_t join[kSideStreams] = {};
+    std::mutex launch_mu;
     // stage timing (rubiconv_profile_start / _read)
     static constexpr int kEventsPerCall = 64;  // before the first kernel + after each launch
     int prof_max = 0, prof_used = 0;
@@ -104,8 +113,25 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
                              nullptr, tw, twn,
                              reinterpret_cast<const int32_t*>(base + o_cid)};
     pl->mfma_tab = base + o_mt;
+    if (hipEventCreateWithFlags(&pl->fork, hipEventDisableTiming) != hipSuccess) return RUBICONV_ERR_HIP;
+    for (int k = 0; k < rubiconv_plan_s::kSideStreams; ++k) {
+        if (hipStreamCreateWithFlags(&pl->side[k], hipStreamNonBlocking) != hipSuccess ||
+            hipEventCreateWithFlags(&pl->join[k], hipEventDisableTiming) != hipSuccess)
+            return RUBICONV_ERR_HIP;
+    }
     pl->device_ready = true;
     return RUBICONV_OK;
+}
+
+void destroy_side_streams(rubiconv_plan_s* pl) {
+    for (int k = 0; k < rubiconv_plan_s::kSideStreams; ++k) {
+        if (pl->side[k]) (void)hipStreamDestroy(pl->side[k]);
+        if (pl->join[k]) (void)hipEventDestroy(pl->join[k]);
+        pl->side[k] = nullptr;
+        pl->join[k] = nullptr;
+    }
+    if (pl->fork) (void)hipEventDestroy(pl->fork);
+    pl->fork = nullptr;
 }
 
 void destroy_events(rubiconv_plan_s* pl) {
@@ -168,6 +194,8 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
     pl->ws_bytes = std::max(conv_ws, filt_ws);
     rubiconv_status_t st = upload(pl);
     if (st != RUBICONV_OK) {
+        destroy_side_streams(pl);
+        if (pl->dev) (void)hipFree(pl->dev);
         delete pl;
         return st;
     }
@@ -178,6 +206,7 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
 void rubiconv_plan_destroy(rubiconv_plan_t plan) {
     if (!plan) return;
     destroy_events(plan);
+    destroy_side_streams(plan);
     if (plan->dev) (void)hipFree(plan->dev);
     delete plan;
 }
@@ -221,6 +250,7 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
     const HostPlan& h = plan->h;
     const int n_cols = static_cast<int>(h.doc_col_seg.size());
     const int64_t rs = static_cast<int64_t>(h.N) * h.D;
+    std::lock_guard<std::mutex> lock(plan->launch_mu);
     StageRecorder rec(plan, stream);
     const bool half = h.grid_half;
     hipError_t e = h.col_mfma
@@ -231,22 +261,51 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
                                                   plan->grid_pb_stride, plan->doc_t, n_cols, h.npb,
                                                   stream);
     rec.mark("col_fwd");
-    if (e == hipSuccess && !h.doc_task_seg.empty()) {
-        e = rubiconv::launch_row_conv(h.n1, half, workspace, plan->grid_pb_stride, spectrum,
-                                      plan->cls_pb_stride, plan->doc_t,
-                                      static_cast<int>(h.doc_task_seg.size()), h.npb,
-                                      h.row_lds_docs, stream);
-        rec.mark("row_conv_generic");
+    // row pass: the generic kernel (long rows) and one launch per listed size
+    // class, spread over the side streams (largest work first, least-loaded stream)
+    struct Launch {
+        int cls;       // -1: generic kernel
+        double work;
+    };
+    std::vector<Launch> launches;
+    if (!h.doc_task_seg.empty()) launches.push_back({-1, 1e30});
+    for (size_t c = 0; c < h.classes.size(); ++c)
+        if (h.classes[c].m <= rubiconv::kMaxFastM)
+            launches.push_back({static_cast<int>(c), static_cast<double>(h.classes[c].m) * h.classes[c].nlist});
+    std::sort(launches.begin(), launches.end(),
+              [](const Launch& a, const Launch& b) { return a.work > b.work; });
+    const int nside = std::min<int>(rubiconv_plan_s::kSideStreams, static_cast<int>(launches.size()));
+    auto launch_one = [&](const Launch& L, hipStream_t s) -> hipError_t {
+        if (L.cls < 0)
+            return rubiconv::launch_row_conv(h.n1, half, workspace, plan->grid_pb_stride, spectrum,
+                                             plan->cls_pb_stride, plan->doc_t,
+                                             static_cast<int>(h.doc_task_seg.size()), h.npb,
+                                             h.row_lds_docs, s);
+        const Seg& cs = h.classes[L.cls];
+        return rubiconv::launch_row_fast(cs.m, half, workspace, plan->grid_pb_stride, spectrum,
+                                         plan->cls_pb_stride, plan->doc_t.segs,
+                                         plan->doc_t.list + cs.list0, cs.nlist, plan->doc_t.tw,
+                                         h.n1, h.npb, s);
+    };
+    if (nside <= 1) {
+        for (const Launch& L : launches)
+            if (e == hipSuccess) e = launch_one(L, stream);
+    } else if (e == hipSuccess) {
+        e = hipEventRecord(plan->fork, stream);
+        for (int k = 0; k < nside && e == hipSuccess; ++k) e = hipStreamWaitEvent(plan->side[k], plan->fork, 0);
+        std::vector<double> load(nside, 0.0);
+        for (const Launch& L : launches) {
+            if (e != hipSuccess) break;
+            const int k = static_cast<int>(std::min_element(load.begin(), load.end()) - load.begin());
+            load[k] += L.work;
+            e = launch_one(L, plan->side[k]);
+        }
+        for (int k = 0; k < nside && e == hipSuccess; ++k) {
+            e = hipEventRecord(plan->join[k], plan->side[k]);
+            if (e == hipSuccess) e = hipStreamWaitEvent(stream, plan->join[k], 0);
+        }
     }
-    for (size_t c = 0; c < h.classes.size() && e == hipSuccess; ++c) {
-        const Seg& cs = h.classes[c];
-        if (cs.m > rubiconv::kMaxFastM) continue;
-        e = rubiconv::launch_row_fast(cs.m, half, workspace, plan->grid_pb_stride, spectrum,
-                                      plan->cls_pb_stride, plan->doc_t.segs,
-                                      plan->doc_t.list + cs.list0, cs.nlist, plan->doc_t.tw, h.n1,
-                                      h.npb, stream);
-        rec.mark("row_conv_m" + std::to_string(cs.m));
-    }
+    rec.mark("row_conv");
     if (e == hipSuccess)
         e = h.col_mfma ? rubiconv::launch_col_inv_mfma(h.y_dtype, workspace, plan->grid_pb_stride, y,
                                                        rs, h.D, plan->doc_t, plan->mfma_tab, n_cols,
