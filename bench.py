@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true",
                     help="launch every step from Python instead of replaying a captured HIP graph")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="after the run, copy a buffer of this many MiB three times (a plain copy "
+                         "kernel of known size, the scale for the hardware byte counters)")
     return ap.parse_args()
 
 
@@ -66,6 +69,35 @@ def kernel_bytes(info, W, plan):
         "filter_col_fwd": 4 * D * sum(taps.values()) + Gc * D * esz // 2,
     }
     return out
+
+
+def sources_digest():
+    """SHA-256 over the library's kernel and runtime sources (name + bytes, sorted)."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2605_08451_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".cpp", ".hpp")):
+            h.update(name.encode())
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(stage, workload):
+    """HBM bytes per launch of `stage` from the committed counter summary of this workload
+    (rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a plain copy of known size), or None
+    when there is none or the library sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        if line.strip().startswith("traffic {"):
+            rec = json.loads(line.strip()[len("traffic "):])
+            if rec.get("sources_sha256") != sources_digest():
+                return None
+            return rec["stages"].get(stage)
+    return None
 
 
 def cpu_baseline(W, target_s):
@@ -192,7 +224,8 @@ def main():
         "step_min_bytes": min_bytes,
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": None, "bytes_per_launch": kb[dom], "avg_us": round(dom_us, 2)},
+                     "traffic": recorded_traffic(dom, wl.CONFIG_SLUGS[args.config]),
+                     "bytes_per_launch": kb[dom], "avg_us": round(dom_us, 2)},
         "stages_us": {n: round(v, 1) for n, v in stages.items()},
         "kernels": {n: {kk: round(vv, 2) for kk, vv in d.items()} for n, d in per_kernel.items()},
         "plan_ms": round(plan_ms, 3),
@@ -202,6 +235,13 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(W, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+    if args.copy_probe_mib > 0:
+        # an elementwise kernel that reads and writes copy_probe_mib MiB once each
+        src = torch.zeros((args.copy_probe_mib << 20) // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
 
 
 if __name__ == "__main__":

@@ -175,6 +175,8 @@ CONFIG_NAMES = {
     3: "boundary-stress-fp32 B4xN8192xD512 L8192",
     4: "long-context-bf16 B1xN262144xD256 L262144 (lognormal 16384, s1.5)",
 }
+CONFIG_SLUGS = {0: "tiny_fp32", 1: "lm_packing_bf16", 2: "mid_length_bf16",
+                3: "boundary_stress_fp32", 4: "long_context_bf16"}
 
 
 def config_rows(i: int, rng: np.random.Generator, n1: int = DEFAULT_N1) -> List[List[int]]:
