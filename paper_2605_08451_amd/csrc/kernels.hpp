@@ -59,6 +59,13 @@ hipError_t launch_row_fast(int m, bool half, void* grid, int64_t grid_pb_stride,
                            int64_t fgrid_pb_stride, const Seg* segs, const int32_t* list,
                            int nlist, const float2* tw, int n1, int npb, hipStream_t stream);
 
+// Matrix-core row pass (complex fp16 grids): the documents of `list` all have
+// ceil(m / 16) == nb (1 <= nb <= kMaxDenseBlocks); tabs = the plan's dense operand
+// tables, addressed through each document's Seg::dense_off.
+hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const void* fgrid,
+                            int64_t fgrid_pb_stride, const Seg* segs, const int32_t* list,
+                            int nlist, const void* tabs, int n1, int npb, hipStream_t stream);
+
 // Matrix-core column passes (N1 = 256, complex fp16 grids, D a multiple of 32).
 // `mtab` holds the MFMA operand tables in lane order (16-byte entries, offsets
 // below; see build_mfma_tables).

@@ -16,6 +16,7 @@ constexpr int kPairsPerBlock = 16;  // channel pairs per block: 16 * 8 B = 128 B
 constexpr int kMaxFactors = 14;     // radices of m (m <= 2048 has at most 11)
 constexpr int kMaxM = 2048;         // largest row DFT
 constexpr int kRowLdsBytes = 98304; // generic row kernel: three buffers of two rows each
+constexpr int kMaxDenseBlocks = 8;  // matrix-core row pass: m <= 16 * kMaxDenseBlocks
 
 struct Seg {
     int32_t row;       // source row of x (documents) / 0 (filter classes)
@@ -35,7 +36,8 @@ struct Seg {
     int32_t nlist;     // classes: number of documents in the class
     int32_t nfac;      // radices of m, applied in order
     int8_t fac[kMaxFactors];
-    int8_t pad_[6];
+    int8_t pad_[2];
+    int32_t dense_off; // matrix-core row pass: first 16-byte entry of the class's DFT operands
 };
 static_assert(sizeof(Seg) % 8 == 0, "Seg must stay 8-byte aligned in arrays");
 

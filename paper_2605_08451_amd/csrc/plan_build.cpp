@@ -151,6 +151,25 @@ void build_mfma_tables(std::vector<uint32_t>* out) {
         }, 0);
 }
 
+void build_dense_tables(int m, int n1, std::vector<uint32_t>* out) {
+    const int nb = (m + 15) / 16;
+    const double fwd_scale = 1.0 / std::sqrt(static_cast<double>(m));
+    const double inv_scale = std::sqrt(static_cast<double>(n1)) / 4.0;
+    // time-domain points are interleaved within a block (slot s <-> point interleave(s)),
+    // so that one load or store instruction covers four neighbouring points; frequencies
+    // keep their natural order
+    for (int dir = 0; dir < 2; ++dir)
+        for (int kb = 0; kb < nb; ++kb)
+            for (int jb = 0; jb < nb; ++jb)
+                push_operands(out, [=](int row, int n) {
+                    const int k = dir == 0 ? 16 * kb + row : 16 * jb + n;              // frequency
+                    const int j = dir == 0 ? 16 * jb + interleave(n) : 16 * kb + interleave(row);  // time
+                    if (k >= m || j >= m) return std::complex<double>(0.0, 0.0);
+                    const double e = static_cast<double>((static_cast<int64_t>(k) * j) % m);
+                    return dir == 0 ? root(-e, m) * fwd_scale : root(e, m) * inv_scale;
+                }, 0);
+}
+
 BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_docs,
                            const int32_t* cu, int x_dtype, int y_dtype, int n1) {
     if (!out || !cu || B < 1 || N < 1 || D < 1 || L < 1 || max_docs < 1) return BuildError::kArg;
@@ -256,6 +275,22 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
     // bf16 inputs, N1 = 256 and whole 32-channel blocks: column passes on the matrix cores
     p.col_mfma = p.grid_half && n1 == 256 && D % 32 == 0;
     if (p.col_mfma) build_mfma_tables(&p.mfma_tab);
+    // complex fp16 grids: rows of up to 16 * kMaxDenseBlocks points on the matrix cores
+    p.row_dense = p.grid_half;
+    if (p.row_dense) {
+        for (auto& c : p.classes) {
+            if (c.m > 16 * kMaxDenseBlocks) continue;
+            c.dense_off = static_cast<int32_t>(p.dense_tab.size() / 4);
+            build_dense_tables(c.m, n1, &p.dense_tab);
+        }
+        for (auto& s : p.docs) s.dense_off = p.classes[s.cls].dense_off;
+        for (int nb = 1; nb <= kMaxDenseBlocks; ++nb) {
+            p.dense_list0[nb] = static_cast<int32_t>(p.dense_docs.size());
+            for (int32_t d : p.class_docs)
+                if ((p.docs[d].m + 15) / 16 == nb) p.dense_docs.push_back(d);
+            p.dense_count[nb] = static_cast<int32_t>(p.dense_docs.size()) - p.dense_list0[nb];
+        }
+    }
     *out = std::move(p);
     return BuildError::kOk;
 }

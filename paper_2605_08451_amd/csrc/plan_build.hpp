@@ -27,6 +27,11 @@ struct HostPlan {
     std::vector<float> tw_n1;           // complex pairs, w_N1^s for s < N1
     std::vector<uint32_t> mfma_tab;     // matrix-core operand tables (N1 = 256 only)
     bool col_mfma = false;              // column passes on the matrix cores
+    bool row_dense = false;             // row pass on the matrix cores for m <= 16 * kMaxDenseBlocks
+    std::vector<uint32_t> dense_tab;    // per class: forward then inverse row DFT operands
+    std::vector<int32_t> dense_docs;    // documents grouped by 16-point block count nb = ceil(m / 16)
+    int32_t dense_list0[kMaxDenseBlocks + 1] = {};  // first entry of block count nb in dense_docs
+    int32_t dense_count[kMaxDenseBlocks + 1] = {};  // documents with block count nb
     int64_t grid_points = 0;            // sum over documents of P_i
     int64_t class_points = 0;           // sum over classes of P
     int32_t taps_max = 0;               // largest number of filter taps any class keeps
@@ -39,6 +44,12 @@ int smooth_ceil(int v);
 // MFMA operand tables of the N1 = 256 matrix-core column passes (kMtEntries
 // 16-byte entries, 4 x uint32 each, in the order of kernels.hpp's kMt* offsets).
 void build_mfma_tables(std::vector<uint32_t>* out);
+
+// Operands of the matrix-core row pass for one size class (m <= 16 * kMaxDenseBlocks,
+// nb = ceil(m / 16)): the forward m-point DFT with entries w_m^(-k j) / sqrt(m) and the
+// inverse with entries (sqrt(n1) / 4) w_m^(k j), zero outside k, j < m, each as nb x nb
+// blocks (output block major) of the two 16 x 32 real operands; 4 * nb^2 * 64 entries.
+void build_dense_tables(int m, int n1, std::vector<uint32_t>* out);
 
 // Validates cu_seqlens and fills every table of *out.
 BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_docs,

@@ -1,0 +1,327 @@
+// row_dense.hip -- row pass on the matrix cores for complex fp16 grids, m <= 128.
+//
+// Algorithm 1's block-diagonal second DFT applies an m-point DFT to every grid
+// row of a document.  For m <= 16 * NB this kernel applies it as one dense
+// complex matrix product on v_mfma_f32_16x16x32_f16: NB x NB blocks of 16 x 16,
+// each block the two real 16 x 32 operands [Re | -Im] and [Im | Re] against
+// the row's 16 channel pairs (K interleaves real and imaginary parts).  The
+// output layout of a product (lane group h holds rows 4h..4h+3 of a block) is
+// the input layout of the next (lane group h holds K = 8h..8h+7, i.e. slots
+// 4h..4h+3), so the forward transform, the spectral product and the inverse
+// transform chain without any lane exchange.  Frequencies keep their natural
+// order in the slots; time points are interleaved (slot 4h + t holds point
+// 4t + h, folded into the operand tables) so that each load and store
+// instruction covers four neighbouring grid points.
+//
+// One wave handles grid row u (0 <= u <= N1/2) of one document and its
+// conjugate partner row ub = (N1 - u) mod N1, for one block of 16 pairs: the
+// filter-class rows and the data rows of both are transformed, row ub's two
+// spectra go to LDS, and for each frequency f of row u the wave forms, from
+// a = Z(f), b = Z(-f), A = F(f), Bf = F(-f) (Z data pair, F filter pair), the
+// separated product of Algorithm 3 for both f and -f:
+//   s = a + conj b, d = a - conj b, U = s - i d, V = s + i d,
+//   4 W(f) = A U + conj(Bf) V,   4 W(-f) = conj(conj(Bf) U + A V),
+// where W = X_d H_d + i X_(d+1) H_(d+1) is the spectrum of the output pair.  The
+// frequency -f of f = u + N1 v sits in row ub at column (-v - [u > 0]) mod m.
+// W(-f) replaces Z(-f) in LDS and feeds row ub's inverse transform; the
+// inverse of both rows is written back over the grid rows.
+//
+// Scaling: the forward operands carry 1 / sqrt(m), so the product carries the
+// 1 / m of the inverse row DFT; the inverse operands carry sqrt(N1) / 4 (the
+// 1/4 of the two separations, and the sqrt(N1) that undoes the filter grid's
+// 1 / sqrt(N1) column scaling), leaving the inverse column pass's 1 / sqrt(N1).
+//
+// Rows are read and written through buffer resources that cover exactly one
+// row: the padded points of the last block read zeros and write nothing.  Row
+// data is touched once, so it is loaded and stored non-temporally (cache policy
+// nt) and leaves the vector cache to the operand tables, which every wave of a
+// size class rereads.
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "kernels.hpp"
+
+namespace rubiconv {
+
+namespace {
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWaves = 4;   // row tasks per workgroup, one per wave
+constexpr int kPad = 16;    // LDS slots in front of a row: partner reads of padded points
+
+__device__ __forceinline__ f4 mma(u4 a, u4 b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8, a),
+                                                  __builtin_bit_cast(h8, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ uint32_t pack_h2(float re, float im) {
+    return __builtin_bit_cast(uint32_t, __float22half2_rn(make_float2(re, im)));
+}
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_buffer(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes),
+                                             0x00020000);
+}
+
+// Complex fp16 pairs (low half real, high half imaginary) on the packed-half ALU.
+// op_sel picks the source halves of the low result, op_sel_hi those of the high
+// result; neg_lo / neg_hi negate a source in the low / high result.
+__device__ __forceinline__ uint32_t pk_add_conj(uint32_t a, uint32_t b) {  // a + conj b
+    uint32_t r;
+    asm("v_pk_add_f16 %0, %1, %2 neg_hi:[0,1]" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+__device__ __forceinline__ uint32_t pk_swap_add_conj(uint32_t a, uint32_t b) {
+    // (a.im + b.im, a.re - b.re)
+    uint32_t r;
+    asm("v_pk_add_f16 %0, %1, %2 op_sel:[1,1] op_sel_hi:[0,0] neg_hi:[0,1]" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+__device__ __forceinline__ uint32_t pk_add_neg_hi(uint32_t a, uint32_t b) {  // (a.x + b.x, a.y - b.y)
+    uint32_t r;
+    asm("v_pk_add_f16 %0, %1, %2 neg_hi:[0,1]" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+__device__ __forceinline__ uint32_t pk_add_neg_lo(uint32_t a, uint32_t b) {  // (a.x - b.x, a.y + b.y)
+    uint32_t r;
+    asm("v_pk_add_f16 %0, %1, %2 neg_lo:[0,1]" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
+
+// 4 W(f) = A U + conj(Bf) V
+__device__ __forceinline__ uint32_t w_pos(uint32_t A, uint32_t Bf, uint32_t U, uint32_t V) {
+    uint32_t t;
+    asm("v_pk_mul_f16 %0, %1, %2 op_sel_hi:[0,1]" : "=v"(t) : "v"(A), "v"(U));
+    asm("v_pk_fma_f16 %0, %1, %2, %0 op_sel:[1,1,0] op_sel_hi:[1,0,1] neg_lo:[1,0,0]"
+        : "+v"(t) : "v"(A), "v"(U));
+    asm("v_pk_fma_f16 %0, %1, %2, %0 op_sel_hi:[0,1,1]" : "+v"(t) : "v"(Bf), "v"(V));
+    asm("v_pk_fma_f16 %0, %1, %2, %0 op_sel:[1,1,0] op_sel_hi:[1,0,1] neg_hi:[1,0,0]"
+        : "+v"(t) : "v"(Bf), "v"(V));
+    return t;
+}
+// 4 W(-f) = conj(conj(Bf) U + A V)
+__device__ __forceinline__ uint32_t w_neg(uint32_t A, uint32_t Bf, uint32_t U, uint32_t V) {
+    uint32_t t;
+    asm("v_pk_mul_f16 %0, %1, %2 op_sel_hi:[0,1] neg_hi:[1,0]" : "=v"(t) : "v"(Bf), "v"(U));
+    asm("v_pk_fma_f16 %0, %1, %2, %0 op_sel:[1,1,0] op_sel_hi:[1,0,1]" : "+v"(t) : "v"(Bf), "v"(U));
+    asm("v_pk_fma_f16 %0, %1, %2, %0 op_sel_hi:[0,1,1] neg_hi:[1,0,0]" : "+v"(t) : "v"(A), "v"(V));
+    asm("v_pk_fma_f16 %0, %1, %2, %0 op_sel:[1,1,0] op_sel_hi:[1,0,1] neg_lo:[1,0,0] neg_hi:[1,0,0]"
+        : "+v"(t) : "v"(A), "v"(V));
+    return t;
+}
+
+template <int NB>
+__global__ __launch_bounds__(64 * kWaves) void row_dense_kernel(uint32_t* __restrict__ grid,
+                                                               int64_t grid_pb_stride,
+                                                               const uint32_t* __restrict__ fgrid,
+                                                               int64_t fgrid_pb_stride,
+                                                               const Seg* __restrict__ segs,
+                                                               const int32_t* __restrict__ list,
+                                                               int nlist,
+                                                               const u4* __restrict__ tabs, int n1) {
+    constexpr int S = 16 * NB;              // points per row, padded to whole blocks
+    constexpr int RS = (kPad + S) * 16;     // u32 per LDS row: slots x 16 pairs
+    // the data rows' loads are issued with the filter rows' while registers allow
+    constexpr bool kPrefetch = NB <= 4;
+    __shared__ uint32_t lds_all[kWaves][2][RS];  // [wave][data, filter] row ub's spectra
+
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+    const int lane = threadIdx.x & 63;
+    const int p = lane & 15, h = lane >> 4;
+    const int nu = n1 / 2 + 1;
+    const int task = blockIdx.x * kWaves + wave;
+    if (task >= nlist * nu) return;  // no workgroup barrier follows
+    const Seg* sg = segs + list[task / nu];
+    const int u = task % nu;
+    const int ub = (n1 - u) & (n1 - 1);
+    const int m = sg->m;
+    const int pb = blockIdx.y;
+    // row u = 0 pairs v with (m - v) mod m instead of m - 1 - v: its partner-row
+    // spectra are stored one slot lower, so one read pattern serves every row
+    const int shift = u == 0 ? 1 : 0;
+    uint32_t* xlds = lds_all[wave][0] + kPad * 16 + p;  // slot s of the data row at xlds[16 s]
+    uint32_t* flds = lds_all[wave][1] + kPad * 16 + p;
+
+    const uint32_t row_bytes = static_cast<uint32_t>(m) * 64;
+    uint32_t* drow = grid + pb * grid_pb_stride + sg->grid_off * 16;
+    const uint32_t* frow = fgrid + pb * fgrid_pb_stride + static_cast<int64_t>(sg->spec_off) * 16;
+    const __amdgpu_buffer_rsrc_t rdu = row_buffer(drow + static_cast<int64_t>(u) * m * 16, row_bytes);
+    const __amdgpu_buffer_rsrc_t rdb = row_buffer(drow + static_cast<int64_t>(ub) * m * 16, row_bytes);
+    const __amdgpu_buffer_rsrc_t rfu = row_buffer(frow + static_cast<int64_t>(u) * m * 16, row_bytes);
+    const __amdgpu_buffer_rsrc_t rfb = row_buffer(frow + static_cast<int64_t>(ub) * m * 16, row_bytes);
+
+    // inputs: register t of lane (p, h) holds point 16 jb + 4 t + h of pair p (the
+    // operand tables interleave the time points accordingly), so the four lane groups
+    // of one load cover four neighbouring points, 256 contiguous bytes
+    const int lane_off = (h * 16 + p) * 4;
+    u4 fu[NB], fb[NB], xu[NB], xb[NB];
+#pragma unroll
+    for (int jb = 0; jb < NB; ++jb)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int off = lane_off + (16 * jb + 4 * t) * 64;
+            fu[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rfu, off, 0, 2);
+            fb[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rfb, off, 0, 2);
+        }
+    if constexpr (kPrefetch) {
+#pragma unroll
+        for (int jb = 0; jb < NB; ++jb)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const int off = lane_off + (16 * jb + 4 * t) * 64;
+                xu[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rdu, off, 0, 2);
+                xb[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rdb, off, 0, 2);
+            }
+    }
+    // zero the slots in front of both LDS rows (read by the padded points)
+#pragma unroll
+    for (int i = 0; i < kPad / 4; ++i) {
+        xlds[16 * (4 * i + h - kPad)] = 0u;
+        flds[16 * (4 * i + h - kPad)] = 0u;
+    }
+
+    const u4* fwd = tabs + sg->dense_off;   // [kb][jb][re, im][64 lanes]
+    const u4* inv = fwd + 2 * NB * NB * 64;
+
+    // forward DFT of the filter rows, then of the data rows: row u's spectra stay in
+    // registers (frequency v = 16 kb + 4 h + r in register r), row ub's go to LDS
+    uint32_t au[NB][4], fa[NB][4];
+    uint32_t keep_x = 0u, keep_f = 0u;
+#pragma unroll
+    for (int phase = 0; phase < 2; ++phase) {
+        if (phase == 1 && !kPrefetch) {
+#pragma unroll
+            for (int jb = 0; jb < NB; ++jb)
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const int off = lane_off + (16 * jb + 4 * t) * 64;
+                    xu[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rdu, off, 0, 2);
+                    xb[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rdb, off, 0, 2);
+                }
+        }
+        const u4* in_u = phase == 0 ? fu : xu;
+        const u4* in_b = phase == 0 ? fb : xb;
+        uint32_t(*own)[4] = phase == 0 ? fa : au;
+        uint32_t* dst = phase == 0 ? flds : xlds;
+#pragma unroll
+        for (int kb = 0; kb < NB; ++kb) {
+            f4 acc[2][2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int jb = 0; jb < NB; ++jb) {
+                const u4 are = fwd[((kb * NB + jb) * 2) * 64 + lane];
+                const u4 aim = fwd[((kb * NB + jb) * 2 + 1) * 64 + lane];
+                acc[0][0] = mma(are, in_u[jb], acc[0][0]);
+                acc[0][1] = mma(aim, in_u[jb], acc[0][1]);
+                acc[1][0] = mma(are, in_b[jb], acc[1][0]);
+                acc[1][1] = mma(aim, in_b[jb], acc[1][1]);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                own[kb][r] = pack_h2(acc[0][0][r], acc[0][1][r]);
+                const uint32_t bv = pack_h2(acc[1][0][r], acc[1][1][r]);
+                dst[16 * (16 * kb + 4 * h + r - shift)] = bv;
+                if (kb == 0 && r == 0) (phase == 0 ? keep_f : keep_x) = bv;
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    if (shift && h == 0) {  // row 0: point 0 is also its own partner's slot m - 1
+        flds[16 * (m - 1)] = keep_f;
+        xlds[16 * (m - 1)] = keep_x;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    // separated products: W(f) stays in registers for row u, W(-f) replaces Z(-f)
+    uint32_t wu[NB][4];
+    const int rbase = m - 1 - 4 * h;  // partner slot of v = 16 kb + 4 h + r: rbase - 16 kb - r
+#pragma unroll
+    for (int kb = 0; kb < NB; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int slot = rbase - 16 * kb - r;  // >= -15: inside the zeroed front slots
+            const uint32_t b = xlds[16 * slot];
+            const uint32_t bf = flds[16 * slot];
+            const uint32_t a = au[kb][r];
+            const uint32_t A = fa[kb][r];
+            const uint32_t e1 = pk_add_conj(a, b);       // s
+            const uint32_t e2 = pk_swap_add_conj(a, b);  // (Im d, Re d)
+            const uint32_t U = pk_add_neg_hi(e1, e2);    // s - i d
+            const uint32_t V = pk_add_neg_lo(e1, e2);    // s + i d
+            wu[kb][r] = w_pos(A, bf, U, V);
+            xlds[16 * slot] = w_neg(A, bf, U, V);
+        }
+    if (shift && h == 0) xlds[-16] = xlds[16 * (m - 1)];  // row 0: W at point 0 back to slot -1
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    u4 wb[NB];  // row ub's product spectrum in input layout
+#pragma unroll
+    for (int jb = 0; jb < NB; ++jb)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) wb[jb][t] = xlds[16 * (16 * jb + 4 * h + t - shift)];
+
+    // inverse DFT of both rows, written back over the grid rows
+#pragma unroll
+    for (int kb = 0; kb < NB; ++kb) {
+        f4 acc[2][2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int jb = 0; jb < NB; ++jb) {
+            const u4 are = inv[((kb * NB + jb) * 2) * 64 + lane];
+            const u4 aim = inv[((kb * NB + jb) * 2 + 1) * 64 + lane];
+            const u4 win = {wu[jb][0], wu[jb][1], wu[jb][2], wu[jb][3]};
+            acc[0][0] = mma(are, win, acc[0][0]);
+            acc[0][1] = mma(aim, win, acc[0][1]);
+            acc[1][0] = mma(are, wb[jb], acc[1][0]);
+            acc[1][1] = mma(aim, wb[jb], acc[1][1]);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {  // output register r: time point 16 kb + 4 r + h
+            const int off = lane_off + (16 * kb + 4 * r) * 64;
+            __builtin_amdgcn_raw_buffer_store_b32(pack_h2(acc[0][0][r], acc[0][1][r]), rdu, off, 0, 2);
+            __builtin_amdgcn_raw_buffer_store_b32(pack_h2(acc[1][0][r], acc[1][1][r]), rdb, off, 0, 2);
+        }
+    }
+}
+
+template <int NB>
+hipError_t launch_nb(void* grid, int64_t gs, const void* fgrid, int64_t fs, const Seg* segs,
+                     const int32_t* list, int nlist, const void* tabs, int n1, int npb,
+                     hipStream_t stream) {
+    const int tasks = nlist * (n1 / 2 + 1);
+    const dim3 g((tasks + kWaves - 1) / kWaves, npb), b(64 * kWaves);
+    hipLaunchKernelGGL((row_dense_kernel<NB>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
+                       static_cast<const uint32_t*>(fgrid), fs, segs, list, nlist,
+                       static_cast<const u4*>(tabs), n1);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const void* fgrid,
+                            int64_t fgrid_pb_stride, const Seg* segs, const int32_t* list,
+                            int nlist, const void* tabs, int n1, int npb, hipStream_t stream) {
+    if (nlist == 0) return hipSuccess;
+    switch (nb) {
+        case 1: return launch_nb<1>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        case 2: return launch_nb<2>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        case 3: return launch_nb<3>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        case 4: return launch_nb<4>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        case 5: return launch_nb<5>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        case 6: return launch_nb<6>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        case 7: return launch_nb<7>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        case 8: return launch_nb<8>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace rubiconv

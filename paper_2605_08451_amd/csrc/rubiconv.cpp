@@ -28,6 +28,8 @@ struct rubiconv_plan_s {
     HostPlan h;
     void* dev = nullptr;  // all device tables, one allocation
     const void* mfma_tab = nullptr;  // matrix-core operand tables (inside dev)
+    const void* dense_tab = nullptr; // matrix-core row pass operands (inside dev)
+    const int32_t* dense_docs = nullptr;  // documents by 16-point block count (inside dev)
     bool device_ready = false;
     LaunchTables doc_t{};
     LaunchTables cls_t{};
@@ -70,6 +72,8 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     const size_t o_cdoc = off;       off = align_up(off + h.class_docs.size() * 4);
     const size_t o_cid = off;        off = align_up(off + h.class_ident.size() * 4);
     const size_t o_mt = off;         off = align_up(off + h.mfma_tab.size() * 4);
+    const size_t o_dt = off;         off = align_up(off + h.dense_tab.size() * 4);
+    const size_t o_dd = off;         off = align_up(off + h.dense_docs.size() * 4);
     const size_t total = off;
 
     std::vector<unsigned char> img(total, 0);
@@ -84,6 +88,8 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     std::memcpy(img.data() + o_cdoc, h.class_docs.data(), h.class_docs.size() * 4);
     std::memcpy(img.data() + o_cid, h.class_ident.data(), h.class_ident.size() * 4);
     if (!h.mfma_tab.empty()) std::memcpy(img.data() + o_mt, h.mfma_tab.data(), h.mfma_tab.size() * 4);
+    if (!h.dense_tab.empty()) std::memcpy(img.data() + o_dt, h.dense_tab.data(), h.dense_tab.size() * 4);
+    if (!h.dense_docs.empty()) std::memcpy(img.data() + o_dd, h.dense_docs.data(), h.dense_docs.size() * 4);
 
     int count = 0;
     hipError_t e = hipGetDeviceCount(&count);
@@ -113,6 +119,8 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
                              nullptr, tw, twn,
                              reinterpret_cast<const int32_t*>(base + o_cid)};
     pl->mfma_tab = base + o_mt;
+    pl->dense_tab = base + o_dt;
+    pl->dense_docs = reinterpret_cast<const int32_t*>(base + o_dd);
     if (hipEventCreateWithFlags(&pl->fork, hipEventDisableTiming) != hipSuccess) return RUBICONV_ERR_HIP;
     for (int k = 0; k < rubiconv_plan_s::kSideStreams; ++k) {
         if (hipStreamCreateWithFlags(&pl->side[k], hipStreamNonBlocking) != hipSuccess ||
@@ -264,18 +272,33 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
     // row pass: the generic kernel (long rows) and one launch per listed size
     // class, spread over the side streams (largest work first, least-loaded stream)
     struct Launch {
-        int cls;       // -1: generic kernel
+        int cls;       // -1: generic kernel; >= 0: register-resident kernel of that class
+        int nb;        // > 0: matrix-core kernel for the documents of that block count
         double work;
     };
     std::vector<Launch> launches;
-    if (!h.doc_task_seg.empty()) launches.push_back({-1, 1e30});
-    for (size_t c = 0; c < h.classes.size(); ++c)
-        if (h.classes[c].m <= rubiconv::kMaxFastM)
-            launches.push_back({static_cast<int>(c), static_cast<double>(h.classes[c].m) * h.classes[c].nlist});
+    if (!h.doc_task_seg.empty()) launches.push_back({-1, 0, 1e30});
+    for (size_t c = 0; c < h.classes.size(); ++c) {
+        const int m = h.classes[c].m;
+        if (m > rubiconv::kMaxFastM || (h.row_dense && m <= 16 * rubiconv::kMaxDenseBlocks)) continue;
+        launches.push_back({static_cast<int>(c), 0, static_cast<double>(m) * h.classes[c].nlist});
+    }
+    if (h.row_dense)
+        for (int nb = 1; nb <= rubiconv::kMaxDenseBlocks; ++nb) {
+            if (h.dense_count[nb] == 0) continue;
+            double w = 0;
+            for (int k = 0; k < h.dense_count[nb]; ++k) w += h.docs[h.dense_docs[h.dense_list0[nb] + k]].m;
+            launches.push_back({-1, nb, w});
+        }
     std::sort(launches.begin(), launches.end(),
               [](const Launch& a, const Launch& b) { return a.work > b.work; });
     const int nside = std::min<int>(rubiconv_plan_s::kSideStreams, static_cast<int>(launches.size()));
     auto launch_one = [&](const Launch& L, hipStream_t s) -> hipError_t {
+        if (L.nb > 0)
+            return rubiconv::launch_row_dense(L.nb, workspace, plan->grid_pb_stride, spectrum,
+                                              plan->cls_pb_stride, plan->doc_t.segs,
+                                              plan->dense_docs + h.dense_list0[L.nb],
+                                              h.dense_count[L.nb], plan->dense_tab, h.n1, h.npb, s);
         if (L.cls < 0)
             return rubiconv::launch_row_conv(h.n1, half, workspace, plan->grid_pb_stride, spectrum,
                                              plan->cls_pb_stride, plan->doc_t,

@@ -180,3 +180,21 @@ def test_matrix_core_column_path(device, D, y_dtype):
         W = wl.make_case(rows, D=D, L=L, x_dtype="bf16", seed=L + D)
         y, _ = run_gpu(W, device, y_dtype=y_dtype)
         assert_parity(y, reference(W), W.cu_seqlens, "bf16", f"D={D} L={L} y={y_dtype}")
+
+
+@pytest.mark.parametrize("D", [32, 40])
+def test_row_pass_every_block_count(device, D):
+    """bf16 inputs (complex fp16 grids): documents whose row DFT sizes cover every
+    matrix-core block count (m <= 16, 17..32, ..., 113..128, at and next to the block
+    edges) and the register-resident sizes above it (135, 160, 256).  A length of
+    128 m needs exactly m grid columns at N1 = 256."""
+    rows = [[32768],
+            [20480, 12288],
+            [17280, 12800, 2304, 384],
+            [16384, 10368, 4608, 1408],
+            [9216, 8192, 6400, 4096, 2048, 1920, 896]]
+    W = wl.make_case(rows, D=D, L=32768, x_dtype="bf16", seed=D)
+    y, plan = run_gpu(W, device)
+    ms = sorted(set(int(m) for m in plan.doc_table()[:, 4]))
+    assert ms == [3, 8, 12, 15, 16, 18, 32, 36, 50, 64, 72, 81, 96, 100, 128, 135, 160, 256], ms
+    assert_parity(y, reference(W, "fft"), W.cu_seqlens, "bf16", f"D={D}")
