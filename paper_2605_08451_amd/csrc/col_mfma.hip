@@ -32,6 +32,7 @@
 
 #include "fft_core.hpp"
 #include "kernels.hpp"
+#include "pk_half.hpp"
 
 namespace rubiconv {
 
@@ -84,12 +85,21 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t doc_buffer(const void* base, u
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes),
                                              0x00020000);
 }
+// The part [off, bytes) of a buffer of `bytes` bytes as a buffer of its own (empty
+// when off >= bytes).  With wave-uniform arguments it costs scalar instructions
+// only, and keeps the range check of every access exact: a lane offset v into it
+// is in range exactly when off + v is in range of the whole buffer.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t sub_buffer(const void* base, int64_t bytes,
+                                                             int64_t off) {
+    const int64_t rest = bytes > off ? bytes - off : 0;
+    return doc_buffer(static_cast<const char*>(base) + off, static_cast<uint32_t>(rest));
+}
 
-constexpr int kF32In = 0;   // fp32 input pairs (filter taps): converted to fp16
-constexpr int kBf16In = 1;  // bf16 input pairs: used as bf16 operands as loaded
+constexpr int kF16In = 0;   // fp16 channel pairs (filter taps, packed by the pair transpose)
+constexpr int kBf16In = 1;  // bf16 channel pairs (x): used as bf16 operands as loaded
 
 template <int IN>
-__global__ __launch_bounds__(256) void col_fwd_mfma_kernel(const void* __restrict__ src,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void col_fwd_mfma_kernel(const void* __restrict__ src,
                                                            int64_t src_row_stride, int D,
                                                            uint32_t* __restrict__ grid,
                                                            int64_t grid_pb_stride, LaunchTables t,
@@ -104,12 +114,12 @@ __global__ __launch_bounds__(256) void col_fwd_mfma_kernel(const void* __restric
     const int j = col - sg->col0, m = sg->m, len = sg->len;
     const int p = lane & 15, h = lane >> 4;
     const int ch = 2 * (pb * kPairsPerBlock + p);
-    constexpr int ES = IN == kBf16In ? 2 : 4;
+    constexpr int ES = 2;  // bytes per channel
 
     const char* doc = static_cast<const char*>(src) +
                       (static_cast<int64_t>(sg->row) * src_row_stride +
                        static_cast<int64_t>(sg->start) * D) * ES;
-    const __amdgpu_buffer_rsrc_t rs = doc_buffer(doc, static_cast<uint32_t>(len) * D * ES);
+    const int64_t doc_bytes = static_cast<int64_t>(len) * D * ES;
 
     // stage 1: one MFMA tile per n2 (bf16: hi and lo matrix halves accumulate).
     // Token t = m (16 n1 + n2) + j with n1 = 4i + h (operand slot 4h + i; the
@@ -123,28 +133,24 @@ __global__ __launch_bounds__(256) void col_fwd_mfma_kernel(const void* __restric
             lane_off[i] = (static_cast<uint32_t>(m) * 16u * (4 * i + h) * D + ch) * ES;
 #pragma unroll
         for (int n2 = 0; n2 < 16; ++n2) {
-            const uint32_t wave_off = static_cast<uint32_t>(m * n2 + j) * D * ES;
+            const __amdgpu_buffer_rsrc_t rs =
+                sub_buffer(doc, doc_bytes, static_cast<int64_t>(m * n2 + j) * D * ES);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int off = static_cast<int>(lane_off[i] + wave_off);
-                if constexpr (IN == kBf16In) {
-                    xb[n2][i] = __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
-                } else {
-                    const auto w = __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0);
-                    xb[n2][i] = pack_h2(__uint_as_float(w[0]), __uint_as_float(w[1]));
-                }
+                const int off = static_cast<int>(lane_off[i]);
+                xb[n2][i] = __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
             }
         }
     }
     // per-document twiddle w_P^(u j) = w_P^(k1 j) * w_P^(16 k2 j), u = k1 + 16 k2: the first
     // factor is wave-uniform, the second has four values per lane (k2 = 4 r2 + h)
     const __amdgpu_buffer_rsrc_t rt = doc_buffer(t.tw + sg->twf_off, static_cast<uint32_t>(sg->P) * 8);
-    float2 tw_lane[4];
+    uint32_t tw_lane[4];  // complex fp16
 #pragma unroll
     for (int r2 = 0; r2 < 4; ++r2) {
         const auto w = __builtin_amdgcn_raw_buffer_load_b64(
             rt, static_cast<int>(16u * (4 * r2 + h) * j * 8), 0, 0);
-        tw_lane[r2] = make_float2(__uint_as_float(w[0]), __uint_as_float(w[1]));
+        tw_lane[r2] = h2_bits(__uint_as_float(w[0]), __uint_as_float(w[1]));
     }
     u4 a[4];
     if constexpr (IN == kBf16In) {
@@ -180,10 +186,13 @@ __global__ __launch_bounds__(256) void col_fwd_mfma_kernel(const void* __restric
 
     // stage 2 per k1 = 4g + r, then the per-document twiddle and the fp16 store
     const float2* twf = t.tw + sg->twf_off;
-    const __amdgpu_buffer_rsrc_t rg =
-        doc_buffer(grid + pb * grid_pb_stride + sg->grid_off * kPairsPerBlock,
-                   static_cast<uint32_t>(sg->P) * kPairsPerBlock * 4);
+    const uint32_t* gdoc = grid + pb * grid_pb_stride + sg->grid_off * kPairsPerBlock;
+    const int64_t grid_bytes = static_cast<int64_t>(sg->P) * kPairsPerBlock * 4;
     const uint32_t g_lane = (static_cast<uint32_t>(j) * kPairsPerBlock + p) * 4;
+    uint32_t st_lane[4];  // grid row u = k1 + 16 k2, k2 = 4 r2 + h: lane part of 16 k2
+#pragma unroll
+    for (int r2 = 0; r2 < 4; ++r2)
+        st_lane[r2] = static_cast<uint32_t>(16 * (4 * r2 + h)) * m * (kPairsPerBlock * 4) + g_lane;
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
 #pragma unroll
@@ -196,20 +205,21 @@ __global__ __launch_bounds__(256) void col_fwd_mfma_kernel(const void* __restric
             const f4 dre = mma_f16(are, b, zero);
             const f4 dim = mma_f16(aim, b, zero);
             // both table factors carry 1/sqrt(N1): undo one (x 16, exact)
-            const float2 tk = cscale(twf[k1 * j], 16.0f);  // wave-uniform
+            const float2 tkf = cscale(twf[k1 * j], 16.0f);  // wave-uniform
+            const uint32_t tk = h2_bits(tkf.x, tkf.y);
+            const __amdgpu_buffer_rsrc_t rg =
+                sub_buffer(gdoc, grid_bytes, static_cast<int64_t>(k1) * m * (kPairsPerBlock * 4));
 #pragma unroll
             for (int r2 = 0; r2 < 4; ++r2) {
-                const uint32_t u = static_cast<uint32_t>(k1 + 16 * (4 * r2 + h));  // k2 = 4 r2 + h
-                const float2 z = cmul(cmul(make_float2(dre[r2], dim[r2]), tk), tw_lane[r2]);
-                __builtin_amdgcn_raw_buffer_store_b32(
-                    pack_h2(z.x, z.y), rg, static_cast<int>(u * m * (kPairsPerBlock * 4) + g_lane), 0, 0);
+                const uint32_t z = cmul_h2(cmul_h2(h2_bits(dre[r2], dim[r2]), tk), tw_lane[r2]);
+                __builtin_amdgcn_raw_buffer_store_b32(z, rg, static_cast<int>(st_lane[r2]), 0, 0);
             }
         }
     }
 }
 
 template <class TY>
-__global__ __launch_bounds__(256) void col_inv_mfma_kernel(const uint32_t* __restrict__ grid,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void col_inv_mfma_kernel(const uint32_t* __restrict__ grid,
                                                            int64_t grid_pb_stride,
                                                            void* __restrict__ dst,
                                                            int64_t dst_row_stride, int D,
@@ -228,25 +238,28 @@ __global__ __launch_bounds__(256) void col_inv_mfma_kernel(const uint32_t* __res
     // stage 1 per k1: conjugate twiddle on the input, DFT over k2 -> n2.  All grid
     // loads are issued first; w_P^(u j) = w_P^(k1 j) * w_P^(16 k2 j) with k2 = 4i + h.
     const __amdgpu_buffer_rsrc_t rt = doc_buffer(t.tw + sg->twf_off, static_cast<uint32_t>(sg->P) * 8);
-    const __amdgpu_buffer_rsrc_t rg =
-        doc_buffer(grid + pb * grid_pb_stride + sg->grid_off * kPairsPerBlock,
-                   static_cast<uint32_t>(sg->P) * kPairsPerBlock * 4);
+    const uint32_t* gdoc = grid + pb * grid_pb_stride + sg->grid_off * kPairsPerBlock;
+    const int64_t grid_bytes = static_cast<int64_t>(sg->P) * kPairsPerBlock * 4;
     const uint32_t g_lane = (static_cast<uint32_t>(j) * kPairsPerBlock + p) * 4;
+    uint32_t ld_lane[4];  // grid row u = k1 + 16 k2, k2 = 4 i + h: lane part of 16 k2
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        ld_lane[i] = static_cast<uint32_t>(16 * (4 * i + h)) * m * (kPairsPerBlock * 4) + g_lane;
     u4 yg[16];
 #pragma unroll
-    for (int k1 = 0; k1 < 16; ++k1)
+    for (int k1 = 0; k1 < 16; ++k1) {
+        const __amdgpu_buffer_rsrc_t rg =
+            sub_buffer(gdoc, grid_bytes, static_cast<int64_t>(k1) * m * (kPairsPerBlock * 4));
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const uint32_t u = static_cast<uint32_t>(k1 + 16 * (4 * i + h));
-            yg[k1][i] = __builtin_amdgcn_raw_buffer_load_b32(
-                rg, static_cast<int>(u * m * (kPairsPerBlock * 4) + g_lane), 0, 0);
-        }
-    float2 tw_lane[4];
+        for (int i = 0; i < 4; ++i)
+            yg[k1][i] = __builtin_amdgcn_raw_buffer_load_b32(rg, static_cast<int>(ld_lane[i]), 0, 0);
+    }
+    uint32_t tw_lane[4];  // complex fp16, conjugated
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const auto w = __builtin_amdgcn_raw_buffer_load_b64(
             rt, static_cast<int>(16u * (4 * i + h) * j * 8), 0, 0);
-        tw_lane[i] = make_float2(__uint_as_float(w[0]), -__uint_as_float(w[1]));  // conjugate
+        tw_lane[i] = h2_bits(__uint_as_float(w[0]), -__uint_as_float(w[1]));
     }
     const u4 are1 = mt[kMtInv1 + lane];
     const u4 aim1 = mt[kMtInv1 + 64 + lane];
@@ -256,13 +269,11 @@ __global__ __launch_bounds__(256) void col_inv_mfma_kernel(const uint32_t* __res
     uint32_t z[16][4];
 #pragma unroll
     for (int k1 = 0; k1 < 16; ++k1) {
-        const float2 tk = cscale(cconj(twf[k1 * j]), 16.0f);  // wave-uniform
+        const float2 tkf = cscale(cconj(twf[k1 * j]), 16.0f);  // wave-uniform
+        const uint32_t tk = h2_bits(tkf.x, tkf.y);
         u4 b;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float2 v = cmul(cmul(unpack_h2(yg[k1][i]), tk), tw_lane[i]);
-            b[i] = pack_h2(v.x, v.y);
-        }
+        for (int i = 0; i < 4; ++i) b[i] = cmul_h2(cmul_h2(yg[k1][i], tk), tw_lane[i]);
         const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
         const f4 dre = mma_f16(are1, b, zero);
         const f4 dim = mma_f16(aim1, b, zero);
@@ -279,7 +290,7 @@ __global__ __launch_bounds__(256) void col_inv_mfma_kernel(const uint32_t* __res
     constexpr int ES = std::is_same<TY, F32>::value ? 4 : 2;
     char* doc = static_cast<char*>(dst) + (static_cast<int64_t>(sg->row) * dst_row_stride +
                                            static_cast<int64_t>(sg->start) * D) * ES;
-    const __amdgpu_buffer_rsrc_t rs = doc_buffer(doc, static_cast<uint32_t>(len) * D * ES);
+    const int64_t doc_bytes = static_cast<int64_t>(len) * D * ES;
     uint32_t lane_off[4];  // token t = m (16 n1 + n2) + j, n1 = 4 r2 + h
 #pragma unroll
     for (int r2 = 0; r2 < 4; ++r2)
@@ -295,9 +306,11 @@ __global__ __launch_bounds__(256) void col_inv_mfma_kernel(const uint32_t* __res
             const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
             const f4 dre = mma_f16(are, b, zero);
             const f4 dim = mma_f16(aim, b, zero);
+            const __amdgpu_buffer_rsrc_t rs =
+                sub_buffer(doc, doc_bytes, static_cast<int64_t>(m * n2 + j) * D * ES);
 #pragma unroll
             for (int r2 = 0; r2 < 4; ++r2) {
-                const int off = static_cast<int>(lane_off[r2] + static_cast<uint32_t>(m * n2 + j) * D * ES);
+                const int off = static_cast<int>(lane_off[r2]);
                 if constexpr (std::is_same<TY, F32>::value) {
                     const u2 w = {__float_as_uint(dre[r2]), __float_as_uint(dim[r2])};
                     __builtin_amdgcn_raw_buffer_store_b64(w, rs, off, 0, 0);
@@ -311,7 +324,7 @@ __global__ __launch_bounds__(256) void col_inv_mfma_kernel(const uint32_t* __res
 
 }  // namespace
 
-hipError_t launch_col_fwd_mfma(int x_dtype, const void* src, int64_t src_row_stride, int D,
+hipError_t launch_col_fwd_mfma(int src_dtype, const void* src, int64_t src_row_stride, int D,
                                void* grid, int64_t grid_pb_stride, const LaunchTables& t,
                                const void* mtab, int n_cols, int npb, hipStream_t stream) {
     if (n_cols == 0) return hipSuccess;
@@ -319,11 +332,11 @@ hipError_t launch_col_fwd_mfma(int x_dtype, const void* src, int64_t src_row_str
     const dim3 g((ntasks + 3) / 4), b(256);
     const u4* mt = static_cast<const u4*>(mtab);
     uint32_t* gp = static_cast<uint32_t*>(grid);
-    if (x_dtype == 1)
+    if (src_dtype == 1)
         hipLaunchKernelGGL(col_fwd_mfma_kernel<kBf16In>, g, b, 0, stream, src, src_row_stride, D, gp,
                            grid_pb_stride, t, mt, npb, ntasks);
     else
-        hipLaunchKernelGGL(col_fwd_mfma_kernel<kF32In>, g, b, 0, stream, src, src_row_stride, D, gp,
+        hipLaunchKernelGGL(col_fwd_mfma_kernel<kF16In>, g, b, 0, stream, src, src_row_stride, D, gp,
                            grid_pb_stride, t, mt, npb, ntasks);
     return hipGetLastError();
 }

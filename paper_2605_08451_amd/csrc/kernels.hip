@@ -424,6 +424,30 @@ __global__ __launch_bounds__(256) void transpose_kernel(const float* __restrict_
     }
 }
 
+// Filter taps [D][in_ld] fp32 -> [taps][D / 2] complex fp16 channel pairs (2q, 2q + 1),
+// the input of the matrix-core column pass (which computes in fp16).  Tiles of 64
+// channels x 32 taps through LDS: coalesced reads along taps, writes along pairs.
+__global__ __launch_bounds__(256) void transpose_pairs_kernel(const float* __restrict__ in, int D,
+                                                              int taps, int in_ld,
+                                                              uint32_t* __restrict__ out) {
+    __shared__ float tile[64][33];
+    const int t0 = blockIdx.x * 32, c0 = blockIdx.y * 64;
+    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+    for (int k = ty; k < 64; k += 8) {
+        const int c = c0 + k, t = t0 + tx;
+        tile[k][tx] = (c < D && t < taps) ? in[static_cast<int64_t>(c) * in_ld + t] : 0.0f;
+    }
+    __syncthreads();
+    const int half_d = D / 2;
+    for (int k = ty; k < 32; k += 8) {
+        const int t = t0 + k, q = c0 / 2 + tx;
+        if (t < taps && q < half_d) {
+            const __half2 v = __float22half2_rn(make_float2(tile[2 * tx][k], tile[2 * tx + 1][k]));
+            out[static_cast<int64_t>(t) * half_d + q] = __builtin_bit_cast(uint32_t, v);
+        }
+    }
+}
+
 // ---------------------------------------------------------------- launchers
 static int col_mode(int D) { return D % 32 == 0 ? kFull : (D % 2 == 0 ? kEven : kOdd); }
 
@@ -530,6 +554,15 @@ hipError_t launch_row_conv(int n1, bool half, void* grid, int64_t grid_pb_stride
                            static_cast<float2*>(grid), grid_pb_stride,
                            static_cast<const float2*>(fgrid), fgrid_pb_stride, t, n1);
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_transpose_pairs(const float* in, int D, int taps, int in_ld, void* out,
+                                  hipStream_t stream) {
+    if (D <= 0 || taps <= 0) return hipSuccess;
+    const dim3 g((taps + 31) / 32, (D + 63) / 64);
+    hipLaunchKernelGGL(transpose_pairs_kernel, g, dim3(256), 0, stream, in, D, taps, in_ld,
+                       static_cast<uint32_t*>(out));
     return hipGetLastError();
 }
 

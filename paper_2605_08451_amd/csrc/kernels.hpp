@@ -76,13 +76,19 @@ constexpr int kMtInv1 = 2432;      // inverse stage 1: re, im
 constexpr int kMtInv2 = 2560;      // inverse stage 2 per n2: re, im
 constexpr int kMtEntries = 4608;
 
-hipError_t launch_col_fwd_mfma(int x_dtype, const void* src, int64_t src_row_stride, int D,
+// src_dtype 1: bf16 channels [rows][N][D] (x); 0: fp16 channel pairs [taps][D / 2] from
+// launch_transpose_pairs (filter taps).
+hipError_t launch_col_fwd_mfma(int src_dtype, const void* src, int64_t src_row_stride, int D,
                                void* grid, int64_t grid_pb_stride, const LaunchTables& t,
                                const void* mtab, int n_cols, int npb, hipStream_t stream);
 
 hipError_t launch_col_inv_mfma(int y_dtype, const void* grid, int64_t grid_pb_stride, void* dst,
                                int64_t dst_row_stride, int D, const LaunchTables& t,
                                const void* mtab, int n_cols, int npb, hipStream_t stream);
+
+// Filter taps [D][in_ld] fp32 -> [taps][D / 2] complex fp16 channel pairs (D even).
+hipError_t launch_transpose_pairs(const float* in, int D, int taps, int in_ld, void* out,
+                                  hipStream_t stream);
 
 hipError_t launch_transpose(const float* in, int rows, int cols, int in_ld, float* out,
                             int out_ld, hipStream_t stream);

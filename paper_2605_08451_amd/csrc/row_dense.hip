@@ -113,8 +113,15 @@ __device__ __forceinline__ uint32_t w_neg(uint32_t A, uint32_t Bf, uint32_t U, u
     return t;
 }
 
+// Waves per SIMD the register allocation leaves room for: the kernel is bound by
+// how many row tasks are in flight, so the cap is as high as the rows allow
+// without spilling.
 template <int NB>
-__global__ __launch_bounds__(64 * kWaves) void row_dense_kernel(uint32_t* __restrict__ grid,
+constexpr int kMinWaves = NB <= 1 ? 8 : NB == 2 ? 5 : NB == 3 ? 4 : NB == 4 ? 3 : NB <= 6 ? 2 : 1;
+
+template <int NB>
+__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(kMinWaves<NB>, 8)))
+void row_dense_kernel(uint32_t* __restrict__ grid,
                                                                int64_t grid_pb_stride,
                                                                const uint32_t* __restrict__ fgrid,
                                                                int64_t fgrid_pb_stride,
@@ -124,8 +131,9 @@ __global__ __launch_bounds__(64 * kWaves) void row_dense_kernel(uint32_t* __rest
                                                                const u4* __restrict__ tabs, int n1) {
     constexpr int S = 16 * NB;              // points per row, padded to whole blocks
     constexpr int RS = (kPad + S) * 16;     // u32 per LDS row: slots x 16 pairs
-    // the data rows' loads are issued with the filter rows' while registers allow
-    constexpr bool kPrefetch = NB <= 4;
+    // the data rows' loads are issued with the filter rows' for single-block rows;
+    // longer rows keep the registers for occupancy instead
+    constexpr bool kPrefetch = NB <= 1;
     __shared__ uint32_t lds_all[kWaves][2][RS];  // [wave][data, filter] row ub's spectra
 
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);

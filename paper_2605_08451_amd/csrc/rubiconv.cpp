@@ -230,9 +230,13 @@ rubiconv_status_t rubiconv_filter_spectrum(rubiconv_plan_t plan, const float* fi
         return RUBICONV_ERR_ARG;
     if (!plan->device_ready) return RUBICONV_ERR_HIP;
     const HostPlan& h = plan->h;
-    float* taps = static_cast<float*>(workspace);  // [taps_max][D]
+    // taps as [taps_max][D] fp32, or as [taps_max][D / 2] fp16 channel pairs for the
+    // matrix-core column pass (which computes in fp16)
+    float* taps = static_cast<float*>(workspace);
     StageRecorder rec(plan, stream);
-    hipError_t e = rubiconv::launch_transpose(filters, h.D, h.taps_max, h.L, taps, h.D, stream);
+    hipError_t e = h.col_mfma
+                       ? rubiconv::launch_transpose_pairs(filters, h.D, h.taps_max, h.L, taps, stream)
+                       : rubiconv::launch_transpose(filters, h.D, h.taps_max, h.L, taps, h.D, stream);
     rec.mark("filter_transpose");
     if (e == hipSuccess)
         e = h.col_mfma
