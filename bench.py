@@ -61,12 +61,15 @@ def kernel_bytes(info, W, plan):
     row = 0
     for m in classes:   # document grids read + written, the class's filter grid read per document
         row += ms.count(m) * (n1 * m * D * esz + n1 * m * D * esz // 2)
+    # the matrix-core column passes (bf16 x, N1 = 256, whole 32-channel blocks) take the
+    # filter taps as fp16 channel pairs, the others as fp32
+    st = 2 if (W.x_dtype == "bf16" and n1 == 256 and D % 32 == 0) else 4
     out = {
         "row_conv": row,
         "col_fwd": tok * sx + G * D * esz // 2,
         "col_inv": G * D * esz // 2 + tok * sy,
-        "filter_transpose": 8 * D * max(taps.values()),
-        "filter_col_fwd": 4 * D * sum(taps.values()) + Gc * D * esz // 2,
+        "filter_transpose": (4 + st) * D * max(taps.values()),
+        "filter_col_fwd": st * D * sum(taps.values()) + Gc * D * esz // 2,
     }
     return out
 
