@@ -51,12 +51,7 @@ __device__ __forceinline__ uint32_t pack_h2(float re, float im) {
 __device__ __forceinline__ float2 unpack_h2(uint32_t w) {
     return __half22float2(__builtin_bit_cast(__half2, w));
 }
-__device__ __forceinline__ uint32_t pack_bf2(float re, float im) {
-    const __hip_bfloat162 h = __float22bfloat162_rn(make_float2(re, im));
-    uint32_t w;
-    __builtin_memcpy(&w, &h, 4);
-    return w;
-}
+__device__ __forceinline__ uint32_t pack_bf2(float re, float im) { return bf2_bits(re, im); }
 
 __device__ __forceinline__ f4 mma_f16(u4 a, u4 b, f4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8, a), __builtin_bit_cast(h8, b),
@@ -95,6 +90,23 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t sub_buffer(const void* base, i
     return doc_buffer(static_cast<const char*>(base) + off, static_cast<uint32_t>(rest));
 }
 
+// Copies `chunks` 1 KB pieces of src into LDS, 16 bytes per lane, spread over the
+// workgroup's four waves (buffer loads with the lds modifier: no registers).
+__device__ __forceinline__ void copy_to_lds(const u4* src, u4* lds, int chunks, int wave, int lane) {
+    const __amdgpu_buffer_rsrc_t rs = doc_buffer(src, static_cast<uint32_t>(chunks) * 1024);
+    for (int c = wave; c < chunks; c += 4)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rs, (__attribute__((address_space(3))) void*)(lds + c * 64), 16, c * 1024 + lane * 16, 0, 0, 0);
+}
+
+__device__ __forceinline__ void wave_lds_fence() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+constexpr int kTab2 = 16 * 2 * 64;  // stage-2 operands: 16 matrices x (re, im) x 64 lanes
+
 constexpr int kF16In = 0;   // fp16 channel pairs (filter taps, packed by the pair transpose)
 constexpr int kBf16In = 1;  // bf16 channel pairs (x): used as bf16 operands as loaded
 
@@ -105,16 +117,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                                                            int64_t grid_pb_stride, LaunchTables t,
                                                            const u4* __restrict__ mt, int npb,
                                                            int ntasks) {
+    // stage-2 operands, shared by the workgroup's four column tasks
+    __shared__ u4 tab2[kTab2];
+    // per wave: one output row group (16 grid rows x 16 pairs) on its way to 16-byte stores
+    __shared__ uint32_t ring_all[4][256];
     const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+    copy_to_lds(mt + kMtFwd2, tab2, kTab2 / 64, wave, lane);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();  // the only workgroup barrier
     // wave-uniform task index: keeps the document's buffer resource in SGPRs
-    const int task = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    if (task >= ntasks) return;  // whole wave; the kernel has no barriers
+    const int task = blockIdx.x * 4 + wave;
+    if (task >= ntasks) return;  // whole wave
     const int col = task / npb, pb = task - col * npb;
     const Seg* sg = t.segs + t.col_seg[col];
     const int j = col - sg->col0, m = sg->m, len = sg->len;
     const int p = lane & 15, h = lane >> 4;
     const int ch = 2 * (pb * kPairsPerBlock + p);
     constexpr int ES = 2;  // bytes per channel
+    uint32_t* ring = ring_all[wave];
 
     const char* doc = static_cast<const char*>(src) +
                       (static_cast<int64_t>(sg->row) * src_row_stride +
@@ -189,31 +210,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     const uint32_t* gdoc = grid + pb * grid_pb_stride + sg->grid_off * kPairsPerBlock;
     const int64_t grid_bytes = static_cast<int64_t>(sg->P) * kPairsPerBlock * 4;
     const uint32_t g_lane = (static_cast<uint32_t>(j) * kPairsPerBlock + p) * 4;
-    uint32_t st_lane[4];  // grid row u = k1 + 16 k2, k2 = 4 r2 + h: lane part of 16 k2
-#pragma unroll
-    for (int r2 = 0; r2 < 4; ++r2)
-        st_lane[r2] = static_cast<uint32_t>(16 * (4 * r2 + h)) * m * (kPairsPerBlock * 4) + g_lane;
+    // 16-byte stores: lane l writes pairs 4 (l % 4) .. + 3 of grid row u = k1 + 16 (l / 4)
+    const uint32_t st_lane = (static_cast<uint32_t>(16 * (lane >> 2)) * m + j) * (kPairsPerBlock * 4) +
+                             (lane & 3) * 16;
+    (void)g_lane;
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int k1 = 4 * g + r;
             const u4 b = {y[4 * g][r], y[4 * g + 1][r], y[4 * g + 2][r], y[4 * g + 3][r]};
-            const u4 are = mt[kMtFwd2 + (2 * k1) * 64 + lane];
-            const u4 aim = mt[kMtFwd2 + (2 * k1 + 1) * 64 + lane];
+            const u4 are = tab2[(2 * k1) * 64 + lane];
+            const u4 aim = tab2[(2 * k1 + 1) * 64 + lane];
             const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
             const f4 dre = mma_f16(are, b, zero);
             const f4 dim = mma_f16(aim, b, zero);
             // both table factors carry 1/sqrt(N1): undo one (x 16, exact)
             const float2 tkf = cscale(twf[k1 * j], 16.0f);  // wave-uniform
             const uint32_t tk = h2_bits(tkf.x, tkf.y);
+            // register r2 of lane (p, h) is grid row k1 + 16 (4 r2 + h), pair p
+#pragma unroll
+            for (int r2 = 0; r2 < 4; ++r2)
+                ring[(4 * r2 + h) * 16 + p] = cmul_h2(cmul_h2(h2_bits(dre[r2], dim[r2]), tk), tw_lane[r2]);
+            wave_lds_fence();
+            const u4 v = *reinterpret_cast<const u4*>(ring + lane * 4);
             const __amdgpu_buffer_rsrc_t rg =
                 sub_buffer(gdoc, grid_bytes, static_cast<int64_t>(k1) * m * (kPairsPerBlock * 4));
-#pragma unroll
-            for (int r2 = 0; r2 < 4; ++r2) {
-                const uint32_t z = cmul_h2(cmul_h2(h2_bits(dre[r2], dim[r2]), tk), tw_lane[r2]);
-                __builtin_amdgcn_raw_buffer_store_b32(z, rg, static_cast<int>(st_lane[r2]), 0, 0);
-            }
+            __builtin_amdgcn_raw_buffer_store_b128(v, rg, static_cast<int>(st_lane), 0, 0);
+            wave_lds_fence();  // the ring is rewritten for the next k1
         }
     }
 }
@@ -226,14 +250,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                                                            LaunchTables t,
                                                            const u4* __restrict__ mt, int npb,
                                                            int ntasks) {
+    constexpr int ES = std::is_same<TY, F32>::value ? 4 : 2;  // bytes per output channel
+    __shared__ u4 tab2[kTab2];
+    // per wave: one output group (16 tokens x 16 pairs) on its way to 16-byte stores
+    __shared__ uint32_t ring_all[4][128 * ES];
     const int lane = threadIdx.x & 63;
-    const int task = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+    copy_to_lds(mt + kMtInv2, tab2, kTab2 / 64, wave, lane);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();  // the only workgroup barrier
+    const int task = blockIdx.x * 4 + wave;
     if (task >= ntasks) return;
     const int col = task / npb, pb = task - col * npb;
     const Seg* sg = t.segs + t.col_seg[col];
     const int j = col - sg->col0, m = sg->m, len = sg->len;
     const int p = lane & 15, h = lane >> 4;
-    const int ch = 2 * (pb * kPairsPerBlock + p);
+    uint32_t* ring = ring_all[wave];
 
     // stage 1 per k1: conjugate twiddle on the input, DFT over k2 -> n2.  All grid
     // loads are issued first; w_P^(u j) = w_P^(k1 j) * w_P^(16 k2 j) with k2 = 4i + h.
@@ -287,37 +319,51 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         for (int rp = 0; rp < 4; ++rp)
             lanegroup_transpose(z[rp][r], z[4 + rp][r], z[8 + rp][r], z[12 + rp][r]);
 
-    constexpr int ES = std::is_same<TY, F32>::value ? 4 : 2;
     char* doc = static_cast<char*>(dst) + (static_cast<int64_t>(sg->row) * dst_row_stride +
                                            static_cast<int64_t>(sg->start) * D) * ES;
     const int64_t doc_bytes = static_cast<int64_t>(len) * D * ES;
-    uint32_t lane_off[4];  // token t = m (16 n1 + n2) + j, n1 = 4 r2 + h
+    // 16-byte stores of the group of 16 tokens m (16 n1 + n2) + j, n1 < 16: lane l writes
+    // token n1 = l / LPT (LPT lanes per token) at channel pair QPL (l % LPT) + ...
+    constexpr int LPT = 4 * ES / 2;         // lanes per token: 64 B (bf16) or 128 B (fp32)
+    constexpr int QPL = 16 / LPT;           // pairs per lane: 4 (bf16) or 2 (fp32)
+    constexpr int ROUNDS = ES / 2;          // 16 tokens x 16 pairs take 1 or 2 instructions
+    uint32_t st_lane[ROUNDS];
 #pragma unroll
-    for (int r2 = 0; r2 < 4; ++r2)
-        lane_off[r2] = (static_cast<uint32_t>(m) * 16u * (4 * r2 + h) * D + ch) * ES;
+    for (int q = 0; q < ROUNDS; ++q) {
+        const int n1 = (q * 64 + lane) / LPT;
+        st_lane[q] = (static_cast<uint32_t>(m) * 16u * n1 * D +
+                      2 * (pb * kPairsPerBlock + QPL * ((q * 64 + lane) % LPT))) * ES;
+    }
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int n2 = 4 * g + r;
             const u4 b = {z[4 * g][r], z[4 * g + 1][r], z[4 * g + 2][r], z[4 * g + 3][r]};
-            const u4 are = mt[kMtInv2 + (2 * n2) * 64 + lane];
-            const u4 aim = mt[kMtInv2 + (2 * n2 + 1) * 64 + lane];
+            const u4 are = tab2[(2 * n2) * 64 + lane];
+            const u4 aim = tab2[(2 * n2 + 1) * 64 + lane];
             const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
             const f4 dre = mma_f16(are, b, zero);
             const f4 dim = mma_f16(aim, b, zero);
+            // register r2 of lane (p, h) is token n1 = 4 r2 + h of this n2, pair p
+#pragma unroll
+            for (int r2 = 0; r2 < 4; ++r2) {
+                const int e = (4 * r2 + h) * 16 + p;  // [n1][pair]
+                if constexpr (std::is_same<TY, F32>::value) {
+                    *reinterpret_cast<u2*>(ring + 2 * e) = u2{__float_as_uint(dre[r2]), __float_as_uint(dim[r2])};
+                } else {
+                    ring[e] = pack_bf2(dre[r2], dim[r2]);
+                }
+            }
+            wave_lds_fence();
             const __amdgpu_buffer_rsrc_t rs =
                 sub_buffer(doc, doc_bytes, static_cast<int64_t>(m * n2 + j) * D * ES);
 #pragma unroll
-            for (int r2 = 0; r2 < 4; ++r2) {
-                const int off = static_cast<int>(lane_off[r2]);
-                if constexpr (std::is_same<TY, F32>::value) {
-                    const u2 w = {__float_as_uint(dre[r2]), __float_as_uint(dim[r2])};
-                    __builtin_amdgcn_raw_buffer_store_b64(w, rs, off, 0, 0);
-                } else {
-                    __builtin_amdgcn_raw_buffer_store_b32(pack_bf2(dre[r2], dim[r2]), rs, off, 0, 0);
-                }
+            for (int q = 0; q < ROUNDS; ++q) {
+                const u4 v = *reinterpret_cast<const u4*>(ring + (q * 64 + lane) * 4);
+                __builtin_amdgcn_raw_buffer_store_b128(v, rs, static_cast<int>(st_lane[q]), 0, 0);
             }
+            wave_lds_fence();  // the ring is rewritten for the next n2
         }
     }
 }

@@ -18,6 +18,7 @@
 
 #include "fft_core.hpp"
 #include "kernels.hpp"
+#include "pk_half.hpp"
 
 namespace rubiconv {
 
@@ -26,10 +27,7 @@ __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) { return __uint_as
 
 // Two floats rounded to bf16 (nearest, ties to even; one v_cvt_pk_bf16_f32 on gfx950),
 // low half = v.x.
-__device__ __forceinline__ uint32_t pack_bf16x2(float2 v) {
-    const __hip_bfloat162 h = __float22bfloat162_rn(v);
-    return *reinterpret_cast<const uint32_t*>(&h);
-}
+__device__ __forceinline__ uint32_t pack_bf16x2(float2 v) { return bf2_bits(v.x, v.y); }
 
 // Channels ch (real part) and ch + 1 (imaginary part) of one token; idx is the
 // element index of channel ch.  `both` is false when ch + 1 == D (odd D).

@@ -17,6 +17,20 @@ __device__ __forceinline__ uint32_t h2_bits(float re, float im) {  // round to n
     return __builtin_bit_cast(uint32_t, __float22half2_rn(make_float2(re, im)));
 }
 
+// bf16 of f rounded to nearest even (NaN stays a quiet NaN), in the low 16 bits.
+__device__ __forceinline__ uint32_t bf16_rne_bits(float f) {
+    const uint32_t u = __float_as_uint(f);
+    const uint32_t r = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+    return (u & 0x7fffffffu) > 0x7f800000u ? ((u >> 16) | 0x40u) : r;
+}
+
+// (bf16(lo), bf16(hi)) rounded to nearest even, in integer arithmetic.  The packed
+// conversion instruction gave wrong results here when its operands came straight
+// from matrix-core products, so every bf16 output goes through this form.
+__device__ __forceinline__ uint32_t bf2_bits(float lo, float hi) {
+    return bf16_rne_bits(lo) | (bf16_rne_bits(hi) << 16);
+}
+
 // a * b
 __device__ __forceinline__ uint32_t cmul_h2(uint32_t a, uint32_t b) {
     uint32_t t;

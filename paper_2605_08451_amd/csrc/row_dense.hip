@@ -301,6 +301,246 @@ void row_dense_kernel(uint32_t* __restrict__ grid,
     }
 }
 
+// ---------------------------------------------------------------------------
+// Variant for short rows (m <= 32): every memory access is 16 bytes per lane.
+// The time and frequency layouts, the products and the LDS exchange are those of
+// row_dense_kernel; what differs is how data reaches the matrix cores:
+//   - a workgroup's waves take consecutive rows u of one document, so the class's
+//     operand tables are copied into LDS once per workgroup;
+//   - the four input rows are copied straight into LDS (buffer loads with the lds
+//     modifier, 16 bytes per lane) and read from there in the operand layout;
+//   - the two output rows are staged in LDS and written with 16-byte stores.
+// The vector memory instructions per row pair drop from 16 NB + 8 NB (+ table
+// fragments) to 6 NB, which is what bounds the short-row launches.
+constexpr int kLdsWaves = 8;  // rows u of one document per workgroup
+
+template <int NB>
+struct RowInputs {  // one pair block's four rows in MFMA input layout
+    u4 fu[NB], fb[NB], xu[NB], xb[NB];
+};
+
+struct RowBuffers {  // buffer resources of one pair block's rows u and ub
+    __amdgpu_buffer_rsrc_t du, db, fu, fb;
+};
+
+__device__ __forceinline__ RowBuffers row_buffers(uint32_t* grid, int64_t grid_pb_stride,
+                                                  const uint32_t* fgrid, int64_t fgrid_pb_stride,
+                                                  const Seg* sg, int pb, int u, int ub) {
+    const int m = sg->m;
+    const uint32_t row_bytes = static_cast<uint32_t>(m) * 64;
+    uint32_t* drow = grid + pb * grid_pb_stride + sg->grid_off * 16;
+    const uint32_t* frow = fgrid + pb * fgrid_pb_stride + static_cast<int64_t>(sg->spec_off) * 16;
+    return {row_buffer(drow + static_cast<int64_t>(u) * m * 16, row_bytes),
+            row_buffer(drow + static_cast<int64_t>(ub) * m * 16, row_bytes),
+            row_buffer(frow + static_cast<int64_t>(u) * m * 16, row_bytes),
+            row_buffer(frow + static_cast<int64_t>(ub) * m * 16, row_bytes)};
+}
+
+__device__ __forceinline__ void wave_lds_fence() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// 16 bytes per lane from buffer offset voffset (lane part) to LDS at lds + 16 * lane
+__device__ __forceinline__ void lds_copy16(__amdgpu_buffer_rsrc_t rs, int voffset, void* lds) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(lds), 16,
+                                             voffset, 0, 0, 0);
+}
+
+template <int NB>
+__global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __restrict__ grid,
+                                                               int64_t grid_pb_stride,
+                                                               const uint32_t* __restrict__ fgrid,
+                                                               int64_t fgrid_pb_stride,
+                                                               const Seg* __restrict__ segs,
+                                                               const int32_t* __restrict__ list,
+                                                               const u4* __restrict__ tabs, int n1) {
+    constexpr int S = 16 * NB;                     // points per row, padded to whole blocks
+    constexpr int kTabU4 = 4 * NB * NB * 64;       // forward then inverse fragments
+    constexpr int kStage = 4 * S * 16;             // u32 per wave: four rows [point][16 pairs]
+    static_assert(kStage >= 2 * (kPad + S) * 16, "the exchange rows reuse the staging area");
+    __shared__ u4 tab[kTabU4];
+    __shared__ uint32_t stage_all[kLdsWaves][kStage];
+
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+    const int lane = threadIdx.x & 63;
+    const int p = lane & 15, h = lane >> 4;
+    const int nu = n1 / 2 + 1;
+    const int ug = (nu + kLdsWaves - 1) / kLdsWaves;
+    const Seg* sg = segs + list[blockIdx.x / ug];
+    const int u = (blockIdx.x % ug) * kLdsWaves + wave;
+    const bool active = u < nu;  // wave-uniform
+    const int m = sg->m;
+    const int pb = blockIdx.y;
+    uint32_t* stage = stage_all[wave];
+
+    // the class's operand tables, 1 KB per wave instruction
+    {
+        const __amdgpu_buffer_rsrc_t rt = row_buffer(tabs + sg->dense_off, kTabU4 * 16);
+        for (int c = wave; c < kTabU4 / 64; c += kLdsWaves) lds_copy16(rt, c * 1024 + lane * 16, &tab[c * 64]);
+    }
+    const int ub = (n1 - u) & (n1 - 1);
+    const RowBuffers rb = row_buffers(grid, grid_pb_stride, fgrid, fgrid_pb_stride, sg, pb, u, ub);
+    // the four rows [fu, fb, xu, xb] as [point][16 pairs], 16 points per instruction
+    if (active) {
+#pragma unroll
+        for (int jb = 0; jb < NB; ++jb) {
+            const int off = jb * 1024 + lane * 16;
+            lds_copy16(rb.fu, off, stage + 0 * S * 16 + jb * 256);
+            lds_copy16(rb.fb, off, stage + 1 * S * 16 + jb * 256);
+            lds_copy16(rb.du, off, stage + 2 * S * 16 + jb * 256);
+            lds_copy16(rb.db, off, stage + 3 * S * 16 + jb * 256);
+        }
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // the copies above have landed in LDS
+    if (active && (NB - 1) * 16 * 64 + lane * 16 >= m * 64) {
+        // the copy of points >= m was out of range: make the padding zero
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            *reinterpret_cast<u4*>(stage + r * S * 16 + (NB - 1) * 256 + lane * 4) = u4{0u, 0u, 0u, 0u};
+    }
+    __syncthreads();  // tables visible to every wave; the only workgroup barrier
+    if (!active) return;
+
+    // operand layout: register t of lane (p, h) holds point 16 jb + 4 t + h of pair p
+    RowInputs<NB> in;
+#pragma unroll
+    for (int jb = 0; jb < NB; ++jb)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int e = (16 * jb + 4 * t + h) * 16 + p;
+            in.fu[jb][t] = stage[0 * S * 16 + e];
+            in.fb[jb][t] = stage[1 * S * 16 + e];
+            in.xu[jb][t] = stage[2 * S * 16 + e];
+            in.xb[jb][t] = stage[3 * S * 16 + e];
+        }
+    wave_lds_fence();
+
+    // the staging area now holds the two exchange rows (row ub's spectra)
+    const int shift = u == 0 ? 1 : 0;
+    uint32_t* xlds = stage + kPad * 16 + p;
+    uint32_t* flds = stage + (2 * kPad + S) * 16 + p;
+#pragma unroll
+    for (int i = 0; i < kPad / 4; ++i) {
+        xlds[16 * (4 * i + h - kPad)] = 0u;
+        flds[16 * (4 * i + h - kPad)] = 0u;
+    }
+    const u4* fwd = tab;
+    const u4* inv = tab + 2 * NB * NB * 64;
+
+    uint32_t au[NB][4], fa[NB][4];
+    uint32_t keep_x = 0u, keep_f = 0u;
+#pragma unroll
+    for (int phase = 0; phase < 2; ++phase) {
+        const u4* in_u = phase == 0 ? in.fu : in.xu;
+        const u4* in_b = phase == 0 ? in.fb : in.xb;
+        uint32_t(*own)[4] = phase == 0 ? fa : au;
+        uint32_t* dst = phase == 0 ? flds : xlds;
+#pragma unroll
+        for (int kb = 0; kb < NB; ++kb) {
+            f4 acc[2][2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int jb = 0; jb < NB; ++jb) {
+                const u4 are = fwd[((kb * NB + jb) * 2) * 64 + lane];
+                const u4 aim = fwd[((kb * NB + jb) * 2 + 1) * 64 + lane];
+                acc[0][0] = mma(are, in_u[jb], acc[0][0]);
+                acc[0][1] = mma(aim, in_u[jb], acc[0][1]);
+                acc[1][0] = mma(are, in_b[jb], acc[1][0]);
+                acc[1][1] = mma(aim, in_b[jb], acc[1][1]);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                own[kb][r] = pack_h2(acc[0][0][r], acc[0][1][r]);
+                const uint32_t bv = pack_h2(acc[1][0][r], acc[1][1][r]);
+                dst[16 * (16 * kb + 4 * h + r - shift)] = bv;
+                if (kb == 0 && r == 0) (phase == 0 ? keep_f : keep_x) = bv;
+            }
+        }
+    }
+    if (shift && h == 0) {  // row 0: point 0 is also its own partner's slot m - 1
+        flds[16 * (m - 1)] = keep_f;
+        xlds[16 * (m - 1)] = keep_x;
+    }
+    wave_lds_fence();
+
+    uint32_t wu[NB][4];
+    const int rbase = m - 1 - 4 * h;
+#pragma unroll
+    for (int kb = 0; kb < NB; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int slot = rbase - 16 * kb - r;  // >= -15: inside the zeroed front slots
+            const uint32_t b = xlds[16 * slot];
+            const uint32_t bf = flds[16 * slot];
+            const uint32_t a = au[kb][r];
+            const uint32_t A = fa[kb][r];
+            const uint32_t e1 = pk_add_conj(a, b);
+            const uint32_t e2 = pk_swap_add_conj(a, b);
+            const uint32_t U = pk_add_neg_hi(e1, e2);
+            const uint32_t V = pk_add_neg_lo(e1, e2);
+            wu[kb][r] = w_pos(A, bf, U, V);
+            xlds[16 * slot] = w_neg(A, bf, U, V);
+        }
+    if (shift && h == 0) xlds[-16] = xlds[16 * (m - 1)];
+    wave_lds_fence();
+
+    u4 wb[NB];
+#pragma unroll
+    for (int jb = 0; jb < NB; ++jb)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) wb[jb][t] = xlds[16 * (16 * jb + 4 * h + t - shift)];
+    wave_lds_fence();
+
+    // inverse DFT of both rows into LDS as [row][point][16 pairs], then 16-byte stores
+    uint32_t* out = stage;
+#pragma unroll
+    for (int kb = 0; kb < NB; ++kb) {
+        f4 acc[2][2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int jb = 0; jb < NB; ++jb) {
+            const u4 are = inv[((kb * NB + jb) * 2) * 64 + lane];
+            const u4 aim = inv[((kb * NB + jb) * 2 + 1) * 64 + lane];
+            const u4 win = {wu[jb][0], wu[jb][1], wu[jb][2], wu[jb][3]};
+            acc[0][0] = mma(are, win, acc[0][0]);
+            acc[0][1] = mma(aim, win, acc[0][1]);
+            acc[1][0] = mma(are, wb[jb], acc[1][0]);
+            acc[1][1] = mma(aim, wb[jb], acc[1][1]);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {  // output register r: time point 16 kb + 4 r + h
+            const int e = (16 * kb + 4 * r + h) * 16 + p;
+            out[e] = pack_h2(acc[0][0][r], acc[0][1][r]);
+            out[S * 16 + e] = pack_h2(acc[1][0][r], acc[1][1][r]);
+        }
+    }
+    wave_lds_fence();
+#pragma unroll
+    for (int jb = 0; jb < NB; ++jb) {
+        const int off = jb * 1024 + lane * 16;
+        const u4 vu = *reinterpret_cast<const u4*>(out + jb * 256 + lane * 4);
+        const u4 vb = *reinterpret_cast<const u4*>(out + S * 16 + jb * 256 + lane * 4);
+        __builtin_amdgcn_raw_buffer_store_b128(vu, rb.du, off, 0, 2);
+        __builtin_amdgcn_raw_buffer_store_b128(vb, rb.db, off, 0, 2);
+    }
+}
+
+template <int NB>
+hipError_t launch_lds_nb(void* grid, int64_t gs, const void* fgrid, int64_t fs, const Seg* segs,
+                         const int32_t* list, int nlist, const void* tabs, int n1, int npb,
+                         hipStream_t stream) {
+    const int ug = (n1 / 2 + 1 + kLdsWaves - 1) / kLdsWaves;
+    const dim3 g(nlist * ug, npb), b(64 * kLdsWaves);
+    hipLaunchKernelGGL((row_lds_kernel<NB>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
+                       static_cast<const uint32_t*>(fgrid), fs, segs, list,
+                       static_cast<const u4*>(tabs), n1);
+    return hipGetLastError();
+}
+
 template <int NB>
 hipError_t launch_nb(void* grid, int64_t gs, const void* fgrid, int64_t fs, const Seg* segs,
                      const int32_t* list, int nlist, const void* tabs, int n1, int npb,
@@ -320,8 +560,8 @@ hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const vo
                             int nlist, const void* tabs, int n1, int npb, hipStream_t stream) {
     if (nlist == 0) return hipSuccess;
     switch (nb) {
-        case 1: return launch_nb<1>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
-        case 2: return launch_nb<2>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        case 1: return launch_lds_nb<1>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        case 2: return launch_lds_nb<2>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
         case 3: return launch_nb<3>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
         case 4: return launch_nb<4>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
         case 5: return launch_nb<5>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
