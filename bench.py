@@ -197,14 +197,19 @@ def main():
     kt = plan.profile_read()
     plan.profile_start(0)
     kb = kernel_bytes(info, W, plan)
-    per_kernel = {n: {"launches": c, "avg_us": 1e3 * tot / c,
-                      "GBps": kb.get(n, 0) / (tot / c * 1e-3) / 1e9}
+    # a stage that runs once per channel chunk has several launches per step: its
+    # bytes per launch are the step's bytes over that count
+    lps = {n: c / args.steps for n, (c, tot) in kt.items()}
+    kbl = {n: kb.get(n, 0) / lps[n] for n in kt}
+    per_kernel = {n: {"launches_per_step": lps[n], "avg_us": 1e3 * tot / c,
+                      "us_per_step": 1e3 * tot / args.steps,
+                      "GBps": kbl[n] / (tot / c * 1e-3) / 1e9}
                   for n, (c, tot) in kt.items()}
-    stages = {n: 1e3 * tot / c for n, (c, tot) in kt.items()}
+    stages = {n: 1e3 * tot / args.steps for n, (c, tot) in kt.items()}
     # the dominant single kernel (the row stage is several concurrent launches)
     dom = max((n for n in kt if n != "row_conv"), key=lambda n: kt[n][1])
     dom_us = per_kernel[dom]["avg_us"]
-    achieved = kb[dom] / (dom_us * 1e-6) / 1e9
+    achieved = kbl[dom] / (dom_us * 1e-6) / 1e9
 
     tok_ch = W.B * W.N * W.D
     sx = 2 if W.x_dtype == "bf16" else 4
@@ -228,7 +233,7 @@ def main():
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": recorded_traffic(dom, wl.CONFIG_SLUGS[args.config]),
-                     "bytes_per_launch": kb[dom], "avg_us": round(dom_us, 2)},
+                     "bytes_per_launch": round(kbl[dom]), "avg_us": round(dom_us, 2)},
         "stages_us": {n: round(v, 1) for n, v in stages.items()},
         "kernels": {n: {kk: round(vv, 2) for kk, vv in d.items()} for n, d in per_kernel.items()},
         "plan_ms": round(plan_ms, 3),
