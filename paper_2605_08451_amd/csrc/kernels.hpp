@@ -62,6 +62,11 @@ hipError_t launch_row_fast(int m, bool half, void* grid, int64_t grid_pb_stride,
 // Matrix-core row pass (complex fp16 grids): the documents of `list` all have
 // ceil(m / 16) == nb (1 <= nb <= kMaxDenseBlocks); tabs = the plan's dense operand
 // tables, addressed through each document's Seg::dense_off.
+// 16-byte entries of one class's tables for the rows of 3 to 8 blocks: per direction
+// nb * nb real operands of 64 lanes, then 16 nb complex fp16 twiddles w^(-j) and
+// 16 nb complex fp32 twiddles w^j (w = exp(-2 pi i / m)), padded to whole 1 KB chunks.
+constexpr int partner_tab_u4(int nb) { return (2 * nb * nb * 64 + 12 * nb + 63) / 64 * 64; }
+
 hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const void* fgrid,
                             int64_t fgrid_pb_stride, const Seg* segs, const int32_t* list,
                             int nlist, const void* tabs, int n1, int npb, hipStream_t stream);

@@ -170,6 +170,51 @@ void build_dense_tables(int m, int n1, std::vector<uint32_t>* out) {
                 }, 0);
 }
 
+void build_partner_tables(int m, int n1, std::vector<uint32_t>* out) {
+    const int nb = (m + 15) / 16, S = 16 * nb;
+    const double fwd_scale = 1.0 / std::sqrt(static_cast<double>(m));
+    const double inv_scale = std::sqrt(static_cast<double>(n1)) / 4.0;
+    const size_t start = out->size();
+    // one real operand per 16 x 16 block: lane (row, q) holds entries (row, 4 q + c) as
+    // (Re, -Im) pairs, c = 0..3; the imaginary output part comes from the same operand
+    // applied to -i times the input
+    auto push_re = [out](auto entry) {
+        for (int lane = 0; lane < 64; ++lane)
+            for (int c = 0; c < 4; ++c) {
+                const std::complex<double> v = entry(lane % 16, 4 * (lane / 16) + c);
+                out->push_back(to_f16_bits(v.real()) |
+                               (static_cast<uint32_t>(to_f16_bits(-v.imag())) << 16));
+            }
+    };
+    for (int dir = 0; dir < 2; ++dir)
+        for (int kb = 0; kb < nb; ++kb)
+            for (int jb = 0; jb < nb; ++jb)
+                push_re([=](int row, int n) {
+                    const int k = dir == 0 ? 16 * kb + row : 16 * jb + n;              // frequency
+                    const int j = dir == 0 ? 16 * jb + interleave(n) : 16 * kb + interleave(row);  // time
+                    if (k >= m || j >= m) return std::complex<double>(0.0, 0.0);
+                    const double e = static_cast<double>((static_cast<int64_t>(k) * j) % m);
+                    return dir == 0 ? root(-e, m) * fwd_scale : root(e, m) * inv_scale;
+                });
+    // partner-row twiddles: exp(+2 pi i j / m) as complex fp16, then exp(-2 pi i j / m)
+    // as complex fp32, for time points j < S (zero past m)
+    for (int j = 0; j < S; ++j) {
+        const std::complex<double> w = j < m ? root(j, m) : std::complex<double>(0.0, 0.0);
+        out->push_back(to_f16_bits(w.real()) | (static_cast<uint32_t>(to_f16_bits(w.imag())) << 16));
+    }
+    for (int j = 0; j < S; ++j) {
+        const std::complex<double> w = j < m ? root(-j, m) : std::complex<double>(0.0, 0.0);
+        const float re = static_cast<float>(w.real()), im = static_cast<float>(w.imag());
+        uint32_t b[2];
+        std::memcpy(&b[0], &re, 4);
+        std::memcpy(&b[1], &im, 4);
+        out->push_back(b[0]);
+        out->push_back(b[1]);
+    }
+    // whole 1 KB chunks, as the kernel copies them
+    while ((out->size() - start) % 256) out->push_back(0u);
+}
+
 BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_docs,
                            const int32_t* cu, int x_dtype, int y_dtype, int n1) {
     if (!out || !cu || B < 1 || N < 1 || D < 1 || L < 1 || max_docs < 1) return BuildError::kArg;
@@ -281,7 +326,10 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
         for (auto& c : p.classes) {
             if (c.m > 16 * kMaxDenseBlocks) continue;
             c.dense_off = static_cast<int32_t>(p.dense_tab.size() / 4);
-            build_dense_tables(c.m, n1, &p.dense_tab);
+            if (c.m <= 32)
+                build_dense_tables(c.m, n1, &p.dense_tab);
+            else
+                build_partner_tables(c.m, n1, &p.dense_tab);
         }
         for (auto& s : p.docs) s.dense_off = p.classes[s.cls].dense_off;
         for (int nb = 1; nb <= kMaxDenseBlocks; ++nb) {

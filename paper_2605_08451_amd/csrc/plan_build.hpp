@@ -50,6 +50,9 @@ void build_mfma_tables(std::vector<uint32_t>* out);
 // inverse with entries (sqrt(n1) / 4) w_m^(k j), zero outside k, j < m, each as nb x nb
 // blocks (output block major) of the two 16 x 32 real operands; 4 * nb^2 * 64 entries.
 void build_dense_tables(int m, int n1, std::vector<uint32_t>* out);
+// Matrix-core row pass for 32 < m <= 16 * kMaxDenseBlocks: one real operand per block
+// and direction, then the partner-row twiddles (kernels.hpp: kPartnerTabU4).
+void build_partner_tables(int m, int n1, std::vector<uint32_t>* out);
 
 // Validates cu_seqlens and fills every table of *out.
 BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_docs,

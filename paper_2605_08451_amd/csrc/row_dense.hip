@@ -16,15 +16,17 @@
 // One wave handles grid row u (0 <= u <= N1/2) of one document and its
 // conjugate partner row ub = (N1 - u) mod N1, for one block of 16 pairs: the
 // filter-class rows and the data rows of both are transformed, row ub's two
-// spectra go to LDS, and for each frequency f of row u the wave forms, from
+// spectra are brought to the lanes of the matching frequencies of row u (through
+// LDS for rows of up to 32 points, by the transform itself for longer rows, see
+// row_partner_kernel), and for each frequency f of row u the wave forms, from
 // a = Z(f), b = Z(-f), A = F(f), Bf = F(-f) (Z data pair, F filter pair), the
 // separated product of Algorithm 3 for both f and -f:
 //   s = a + conj b, d = a - conj b, U = s - i d, V = s + i d,
 //   4 W(f) = A U + conj(Bf) V,   4 W(-f) = conj(conj(Bf) U + A V),
 // where W = X_d H_d + i X_(d+1) H_(d+1) is the spectrum of the output pair.  The
 // frequency -f of f = u + N1 v sits in row ub at column (-v - [u > 0]) mod m.
-// W(-f) replaces Z(-f) in LDS and feeds row ub's inverse transform; the
-// inverse of both rows is written back over the grid rows.
+// W(-f) feeds row ub's inverse transform; the inverse of both rows is written
+// back over the grid rows.
 //
 // Scaling: the forward operands carry 1 / sqrt(m), so the product carries the
 // 1 / m of the inverse row DFT; the inverse operands carry sqrt(N1) / 4 (the
@@ -34,14 +36,15 @@
 // Rows are read and written through buffer resources that cover exactly one
 // row: the padded points of the last block read zeros and write nothing.  Row
 // data is touched once, so it is loaded and stored non-temporally (cache policy
-// nt) and leaves the vector cache to the operand tables, which every wave of a
-// size class rereads.
+// nt).  The operand tables of a size class go to LDS once per workgroup, whose
+// waves take consecutive rows of one document.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
 
 #include "kernels.hpp"
+#include "pk_half.hpp"
 
 namespace rubiconv {
 
@@ -51,7 +54,6 @@ typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = 4;   // row tasks per workgroup, one per wave
 constexpr int kPad = 16;    // LDS slots in front of a row: partner reads of padded points
 
 __device__ __forceinline__ f4 mma(u4 a, u4 b, f4 c) {
@@ -111,194 +113,6 @@ __device__ __forceinline__ uint32_t w_neg(uint32_t A, uint32_t Bf, uint32_t U, u
     asm("v_pk_fma_f16 %0, %1, %2, %0 op_sel:[1,1,0] op_sel_hi:[1,0,1] neg_lo:[1,0,0] neg_hi:[1,0,0]"
         : "+v"(t) : "v"(A), "v"(V));
     return t;
-}
-
-// Waves per SIMD the register allocation leaves room for: the kernel is bound by
-// how many row tasks are in flight, so the cap is as high as the rows allow
-// without spilling.
-template <int NB>
-constexpr int kMinWaves = NB <= 1 ? 8 : NB == 2 ? 5 : NB == 3 ? 4 : NB == 4 ? 3 : NB <= 6 ? 2 : 1;
-
-template <int NB>
-__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(kMinWaves<NB>, 8)))
-void row_dense_kernel(uint32_t* __restrict__ grid,
-                                                               int64_t grid_pb_stride,
-                                                               const uint32_t* __restrict__ fgrid,
-                                                               int64_t fgrid_pb_stride,
-                                                               const Seg* __restrict__ segs,
-                                                               const int32_t* __restrict__ list,
-                                                               int nlist,
-                                                               const u4* __restrict__ tabs, int n1) {
-    constexpr int S = 16 * NB;              // points per row, padded to whole blocks
-    constexpr int RS = (kPad + S) * 16;     // u32 per LDS row: slots x 16 pairs
-    // the data rows' loads are issued with the filter rows' for single-block rows;
-    // longer rows keep the registers for occupancy instead
-    constexpr bool kPrefetch = NB <= 1;
-    __shared__ uint32_t lds_all[kWaves][2][RS];  // [wave][data, filter] row ub's spectra
-
-    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
-    const int lane = threadIdx.x & 63;
-    const int p = lane & 15, h = lane >> 4;
-    const int nu = n1 / 2 + 1;
-    const int task = blockIdx.x * kWaves + wave;
-    if (task >= nlist * nu) return;  // no workgroup barrier follows
-    const Seg* sg = segs + list[task / nu];
-    const int u = task % nu;
-    const int ub = (n1 - u) & (n1 - 1);
-    const int m = sg->m;
-    const int pb = blockIdx.y;
-    // row u = 0 pairs v with (m - v) mod m instead of m - 1 - v: its partner-row
-    // spectra are stored one slot lower, so one read pattern serves every row
-    const int shift = u == 0 ? 1 : 0;
-    uint32_t* xlds = lds_all[wave][0] + kPad * 16 + p;  // slot s of the data row at xlds[16 s]
-    uint32_t* flds = lds_all[wave][1] + kPad * 16 + p;
-
-    const uint32_t row_bytes = static_cast<uint32_t>(m) * 64;
-    uint32_t* drow = grid + pb * grid_pb_stride + sg->grid_off * 16;
-    const uint32_t* frow = fgrid + pb * fgrid_pb_stride + static_cast<int64_t>(sg->spec_off) * 16;
-    const __amdgpu_buffer_rsrc_t rdu = row_buffer(drow + static_cast<int64_t>(u) * m * 16, row_bytes);
-    const __amdgpu_buffer_rsrc_t rdb = row_buffer(drow + static_cast<int64_t>(ub) * m * 16, row_bytes);
-    const __amdgpu_buffer_rsrc_t rfu = row_buffer(frow + static_cast<int64_t>(u) * m * 16, row_bytes);
-    const __amdgpu_buffer_rsrc_t rfb = row_buffer(frow + static_cast<int64_t>(ub) * m * 16, row_bytes);
-
-    // inputs: register t of lane (p, h) holds point 16 jb + 4 t + h of pair p (the
-    // operand tables interleave the time points accordingly), so the four lane groups
-    // of one load cover four neighbouring points, 256 contiguous bytes
-    const int lane_off = (h * 16 + p) * 4;
-    u4 fu[NB], fb[NB], xu[NB], xb[NB];
-#pragma unroll
-    for (int jb = 0; jb < NB; ++jb)
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            const int off = lane_off + (16 * jb + 4 * t) * 64;
-            fu[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rfu, off, 0, 2);
-            fb[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rfb, off, 0, 2);
-        }
-    if constexpr (kPrefetch) {
-#pragma unroll
-        for (int jb = 0; jb < NB; ++jb)
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                const int off = lane_off + (16 * jb + 4 * t) * 64;
-                xu[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rdu, off, 0, 2);
-                xb[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rdb, off, 0, 2);
-            }
-    }
-    // zero the slots in front of both LDS rows (read by the padded points)
-#pragma unroll
-    for (int i = 0; i < kPad / 4; ++i) {
-        xlds[16 * (4 * i + h - kPad)] = 0u;
-        flds[16 * (4 * i + h - kPad)] = 0u;
-    }
-
-    const u4* fwd = tabs + sg->dense_off;   // [kb][jb][re, im][64 lanes]
-    const u4* inv = fwd + 2 * NB * NB * 64;
-
-    // forward DFT of the filter rows, then of the data rows: row u's spectra stay in
-    // registers (frequency v = 16 kb + 4 h + r in register r), row ub's go to LDS
-    uint32_t au[NB][4], fa[NB][4];
-    uint32_t keep_x = 0u, keep_f = 0u;
-#pragma unroll
-    for (int phase = 0; phase < 2; ++phase) {
-        if (phase == 1 && !kPrefetch) {
-#pragma unroll
-            for (int jb = 0; jb < NB; ++jb)
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const int off = lane_off + (16 * jb + 4 * t) * 64;
-                    xu[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rdu, off, 0, 2);
-                    xb[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rdb, off, 0, 2);
-                }
-        }
-        const u4* in_u = phase == 0 ? fu : xu;
-        const u4* in_b = phase == 0 ? fb : xb;
-        uint32_t(*own)[4] = phase == 0 ? fa : au;
-        uint32_t* dst = phase == 0 ? flds : xlds;
-#pragma unroll
-        for (int kb = 0; kb < NB; ++kb) {
-            f4 acc[2][2];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-            for (int jb = 0; jb < NB; ++jb) {
-                const u4 are = fwd[((kb * NB + jb) * 2) * 64 + lane];
-                const u4 aim = fwd[((kb * NB + jb) * 2 + 1) * 64 + lane];
-                acc[0][0] = mma(are, in_u[jb], acc[0][0]);
-                acc[0][1] = mma(aim, in_u[jb], acc[0][1]);
-                acc[1][0] = mma(are, in_b[jb], acc[1][0]);
-                acc[1][1] = mma(aim, in_b[jb], acc[1][1]);
-            }
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                own[kb][r] = pack_h2(acc[0][0][r], acc[0][1][r]);
-                const uint32_t bv = pack_h2(acc[1][0][r], acc[1][1][r]);
-                dst[16 * (16 * kb + 4 * h + r - shift)] = bv;
-                if (kb == 0 && r == 0) (phase == 0 ? keep_f : keep_x) = bv;
-            }
-        }
-        __builtin_amdgcn_sched_barrier(0);
-    }
-    if (shift && h == 0) {  // row 0: point 0 is also its own partner's slot m - 1
-        flds[16 * (m - 1)] = keep_f;
-        xlds[16 * (m - 1)] = keep_x;
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-    // separated products: W(f) stays in registers for row u, W(-f) replaces Z(-f)
-    uint32_t wu[NB][4];
-    const int rbase = m - 1 - 4 * h;  // partner slot of v = 16 kb + 4 h + r: rbase - 16 kb - r
-#pragma unroll
-    for (int kb = 0; kb < NB; ++kb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int slot = rbase - 16 * kb - r;  // >= -15: inside the zeroed front slots
-            const uint32_t b = xlds[16 * slot];
-            const uint32_t bf = flds[16 * slot];
-            const uint32_t a = au[kb][r];
-            const uint32_t A = fa[kb][r];
-            const uint32_t e1 = pk_add_conj(a, b);       // s
-            const uint32_t e2 = pk_swap_add_conj(a, b);  // (Im d, Re d)
-            const uint32_t U = pk_add_neg_hi(e1, e2);    // s - i d
-            const uint32_t V = pk_add_neg_lo(e1, e2);    // s + i d
-            wu[kb][r] = w_pos(A, bf, U, V);
-            xlds[16 * slot] = w_neg(A, bf, U, V);
-        }
-    if (shift && h == 0) xlds[-16] = xlds[16 * (m - 1)];  // row 0: W at point 0 back to slot -1
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-    u4 wb[NB];  // row ub's product spectrum in input layout
-#pragma unroll
-    for (int jb = 0; jb < NB; ++jb)
-#pragma unroll
-        for (int t = 0; t < 4; ++t) wb[jb][t] = xlds[16 * (16 * jb + 4 * h + t - shift)];
-
-    // inverse DFT of both rows, written back over the grid rows
-#pragma unroll
-    for (int kb = 0; kb < NB; ++kb) {
-        f4 acc[2][2];
-#pragma unroll
-        for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int jb = 0; jb < NB; ++jb) {
-            const u4 are = inv[((kb * NB + jb) * 2) * 64 + lane];
-            const u4 aim = inv[((kb * NB + jb) * 2 + 1) * 64 + lane];
-            const u4 win = {wu[jb][0], wu[jb][1], wu[jb][2], wu[jb][3]};
-            acc[0][0] = mma(are, win, acc[0][0]);
-            acc[0][1] = mma(aim, win, acc[0][1]);
-            acc[1][0] = mma(are, wb[jb], acc[1][0]);
-            acc[1][1] = mma(aim, wb[jb], acc[1][1]);
-        }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {  // output register r: time point 16 kb + 4 r + h
-            const int off = lane_off + (16 * kb + 4 * r) * 64;
-            __builtin_amdgcn_raw_buffer_store_b32(pack_h2(acc[0][0][r], acc[0][1][r]), rdu, off, 0, 2);
-            __builtin_amdgcn_raw_buffer_store_b32(pack_h2(acc[1][0][r], acc[1][1][r]), rdb, off, 0, 2);
-        }
-    }
 }
 
 // ---------------------------------------------------------------------------
@@ -529,6 +343,192 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
     }
 }
 
+// ---------------------------------------------------------------------------
+// Rows of 33..128 points (3 to 8 blocks).  Their operand tables are too large to
+// stream from the vector cache for every row, and the two LDS exchange rows of the
+// short-row kernels would leave room for few waves beside the tables.  So this
+// kernel keeps one real operand per block and direction in LDS and produces the
+// partner row's spectra directly in the order the separated product needs them:
+//   - the imaginary output part is the same operand applied to -i times the input
+//     (A_re = [Re | -Im] against (Im x, -Re x) gives Im(a x)), halving the tables;
+//   - with w = exp(-2 pi i / m) and T the forward table, row ub's spectrum at the
+//     partner column of v is Z(m - 1 - v) = conj(T conj(z(j) w^(-j)))(v) for u > 0,
+//     and Z((m - v) mod m) = conj(T conj(z))(v) for row 0, so it lands in the
+//     registers of frequency v of row u;
+//   - W(-f) of row ub then sits at the slot of v, frequency m - 1 - v, and the row's
+//     inverse is y(j) = w^j conj(T_inv conj(G))(j) with G(v) = W(m - 1 - v).
+// The products and inverses need no lane exchange, so the only LDS is the tables
+// and the kernel runs as many waves as its registers allow.  Rows 0 and N1/2 are
+// their own partners: their partner spectra come from their own data and only the
+// row itself is transformed back and stored.
+constexpr int kPartnerWaves = 4;  // rows u of one document per workgroup
+
+template <int NB>
+constexpr int kPartnerMinWaves = NB <= 3 ? 4 : NB == 4 ? 3 : NB <= 6 ? 2 : 1;
+
+// -i a = (Im a, -Re a)
+__device__ __forceinline__ uint32_t mul_neg_i(uint32_t a) {
+    return __builtin_amdgcn_alignbit(a, a, 16) ^ 0x80000000u;
+}
+__device__ __forceinline__ u4 mul_neg_i4(u4 a) {
+    return u4{mul_neg_i(a[0]), mul_neg_i(a[1]), mul_neg_i(a[2]), mul_neg_i(a[3])};
+}
+
+template <int NB>
+__global__ __launch_bounds__(64 * kPartnerWaves) __attribute__((amdgpu_waves_per_eu(kPartnerMinWaves<NB>, 8)))
+void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
+                        const uint32_t* __restrict__ fgrid, int64_t fgrid_pb_stride,
+                        const Seg* __restrict__ segs, const int32_t* __restrict__ list,
+                        const u4* __restrict__ tabs, int n1) {
+    constexpr int S = 16 * NB;
+    constexpr int kFrag = NB * NB * 64;            // u4 per direction
+    constexpr int kTab = partner_tab_u4(NB);
+    constexpr bool kPrefetch = NB <= 4;            // data rows loaded with the filter rows
+    __shared__ u4 tab[kTab];
+
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+    const int lane = threadIdx.x & 63;
+    const int p = lane & 15, h = lane >> 4;
+    const int nu = n1 / 2 + 1;
+    const int ug = (nu + kPartnerWaves - 1) / kPartnerWaves;
+    const Seg* sg = segs + list[blockIdx.x / ug];
+    const int u = (blockIdx.x % ug) * kPartnerWaves + wave;
+    const bool active = u < nu;                    // wave-uniform
+    const bool self = u == 0 || 2 * u == n1;       // its own partner row
+    const int ub = self ? u : n1 - u;
+    const int pb = blockIdx.y;
+    const RowBuffers rb = row_buffers(grid, grid_pb_stride, fgrid, fgrid_pb_stride, sg, pb, u, ub);
+
+    // register t of lane (p, h) holds point 16 jb + 4 t + h of pair p: one load covers
+    // four neighbouring points, 256 contiguous bytes
+    const int lane_off = (h * 16 + p) * 4;
+    u4 fu[NB], fb[NB], xu[NB], xb[NB];
+    if (active) {
+#pragma unroll
+        for (int jb = 0; jb < NB; ++jb)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const int off = lane_off + (16 * jb + 4 * t) * 64;
+                fu[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rb.fu, off, 0, 2);
+                fb[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rb.fb, off, 0, 2);
+                if constexpr (kPrefetch) {
+                    xu[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rb.du, off, 0, 2);
+                    xb[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rb.db, off, 0, 2);
+                }
+            }
+    }
+    {  // the class's tables, 1 KB per wave instruction
+        const __amdgpu_buffer_rsrc_t rt = row_buffer(tabs + sg->dense_off, kTab * 16);
+        for (int c = wave; c < kTab / 64; c += kPartnerWaves) lds_copy16(rt, c * 1024 + lane * 16, &tab[c * 64]);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();  // tables visible to every wave; the only workgroup barrier
+    if (!active) return;
+
+    const uint32_t* tw_pre = reinterpret_cast<const uint32_t*>(tab + 2 * kFrag);  // w^(-j), fp16
+    const float2* tw_post = reinterpret_cast<const float2*>(tab + 2 * kFrag + S / 4);  // w^j
+    // rows u > 0 pair v with m - 1 - v and take the twiddle, row 0 pairs v with (m - v) mod m
+    const int pre_mask = u != 0 ? -1 : 0;
+
+    // forward DFT of the filter rows, then of the data rows: own[kb][r] and par[kb][r]
+    // hold frequency v = 16 kb + 4 h + r of row u and the partner value of row ub
+    uint32_t fa[NB][4], fp[NB][4], au[NB][4], ap[NB][4];
+#pragma unroll
+    for (int phase = 0; phase < 2; ++phase) {
+        if (phase == 1 && !kPrefetch) {
+#pragma unroll
+            for (int jb = 0; jb < NB; ++jb)
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const int off = lane_off + (16 * jb + 4 * t) * 64;
+                    xu[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rb.du, off, 0, 2);
+                    xb[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rb.db, off, 0, 2);
+                }
+        }
+        u4* in_u = phase == 0 ? fu : xu;
+        u4* in_b = phase == 0 ? fb : xb;
+        uint32_t(*own)[4] = phase == 0 ? fa : au;
+        uint32_t(*par)[4] = phase == 0 ? fp : ap;
+        // partner input conj(z(j) w^(-j)); row 0 reads entry 0, w^0 = 1, for every j
+#pragma unroll
+        for (int jb = 0; jb < NB; ++jb)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const uint32_t tw = tw_pre[(16 * jb + 4 * t + h) & pre_mask];
+                in_b[jb][t] = cmul_h2(in_b[jb][t], tw) ^ 0x80000000u;
+            }
+#pragma unroll
+        for (int kb = 0; kb < NB; ++kb) {
+            f4 acc[4];  // own re, own im, partner re, partner im
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[i] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int jb = 0; jb < NB; ++jb) {
+                const u4 a = tab[(kb * NB + jb) * 64 + lane];
+                acc[0] = mma(a, in_u[jb], acc[0]);
+                acc[1] = mma(a, mul_neg_i4(in_u[jb]), acc[1]);
+                acc[2] = mma(a, in_b[jb], acc[2]);
+                acc[3] = mma(a, mul_neg_i4(in_b[jb]), acc[3]);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                own[kb][r] = pack_h2(acc[0][r], acc[1][r]);
+                par[kb][r] = pack_h2(acc[2][r], -acc[3][r]);
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+
+    // separated products: W(f) for row u, W(-f) for row ub at the slot of f
+    uint32_t wu[NB][4], wp[NB][4];
+#pragma unroll
+    for (int kb = 0; kb < NB; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const uint32_t a = au[kb][r], b = ap[kb][r];
+            const uint32_t A = fa[kb][r], Bf = fp[kb][r];
+            const uint32_t e1 = pk_add_conj(a, b);       // s
+            const uint32_t e2 = pk_swap_add_conj(a, b);  // (Im d, Re d)
+            const uint32_t U = pk_add_neg_hi(e1, e2);    // s - i d
+            const uint32_t V = pk_add_neg_lo(e1, e2);    // s + i d
+            wu[kb][r] = w_pos(A, Bf, U, V);
+            wp[kb][r] = w_neg(A, Bf, U, V) ^ 0x80000000u;  // conj(G), the inverse's input
+        }
+
+    // inverse DFT of row u and of row ub.  A row that is its own partner stores only
+    // the first: the second goes through a buffer resource of no bytes.  The code
+    // has no branch between the matrix products and the reads of their results, so
+    // the compiler's wait states after the products hold on every path.
+    const u4* inv = tab + kFrag;
+    const __amdgpu_buffer_rsrc_t rdb = self ? row_buffer(nullptr, 0) : rb.db;
+#pragma unroll
+    for (int kb = 0; kb < NB; ++kb) {
+        f4 acc[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[i] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int jb = 0; jb < NB; ++jb) {
+            const u4 a = inv[(kb * NB + jb) * 64 + lane];
+            const u4 bu = {wu[jb][0], wu[jb][1], wu[jb][2], wu[jb][3]};
+            const u4 bp = {wp[jb][0], wp[jb][1], wp[jb][2], wp[jb][3]};
+            acc[0] = mma(a, bu, acc[0]);
+            acc[1] = mma(a, mul_neg_i4(bu), acc[1]);
+            acc[2] = mma(a, bp, acc[2]);
+            acc[3] = mma(a, mul_neg_i4(bp), acc[3]);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {  // output register r: time point j = 16 kb + 4 r + h
+            const int off = lane_off + (16 * kb + 4 * r) * 64;
+            __builtin_amdgcn_raw_buffer_store_b32(pack_h2(acc[0][r], acc[1][r]), rb.du, off, 0, 2);
+            // w^j conj(R + i I) with w^j = (c, s): (R c + I s, R s - I c)
+            const float2 w = tw_post[16 * kb + 4 * r + h];
+            const float re = acc[2][r] * w.x + acc[3][r] * w.y;
+            const float im = acc[2][r] * w.y - acc[3][r] * w.x;
+            __builtin_amdgcn_raw_buffer_store_b32(pack_h2(re, im), rdb, off, 0, 2);
+        }
+    }
+}
+
 template <int NB>
 hipError_t launch_lds_nb(void* grid, int64_t gs, const void* fgrid, int64_t fs, const Seg* segs,
                          const int32_t* list, int nlist, const void* tabs, int n1, int npb,
@@ -542,13 +542,13 @@ hipError_t launch_lds_nb(void* grid, int64_t gs, const void* fgrid, int64_t fs, 
 }
 
 template <int NB>
-hipError_t launch_nb(void* grid, int64_t gs, const void* fgrid, int64_t fs, const Seg* segs,
-                     const int32_t* list, int nlist, const void* tabs, int n1, int npb,
-                     hipStream_t stream) {
-    const int tasks = nlist * (n1 / 2 + 1);
-    const dim3 g((tasks + kWaves - 1) / kWaves, npb), b(64 * kWaves);
-    hipLaunchKernelGGL((row_dense_kernel<NB>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
-                       static_cast<const uint32_t*>(fgrid), fs, segs, list, nlist,
+hipError_t launch_partner_nb(void* grid, int64_t gs, const void* fgrid, int64_t fs, const Seg* segs,
+                             const int32_t* list, int nlist, const void* tabs, int n1, int npb,
+                             hipStream_t stream) {
+    const int ug = (n1 / 2 + 1 + kPartnerWaves - 1) / kPartnerWaves;
+    const dim3 g(nlist * ug, npb), b(64 * kPartnerWaves);
+    hipLaunchKernelGGL((row_partner_kernel<NB>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
+                       static_cast<const uint32_t*>(fgrid), fs, segs, list,
                        static_cast<const u4*>(tabs), n1);
     return hipGetLastError();
 }
@@ -562,12 +562,12 @@ hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const vo
     switch (nb) {
         case 1: return launch_lds_nb<1>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
         case 2: return launch_lds_nb<2>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
-        case 3: return launch_nb<3>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
-        case 4: return launch_nb<4>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
-        case 5: return launch_nb<5>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
-        case 6: return launch_nb<6>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
-        case 7: return launch_nb<7>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
-        case 8: return launch_nb<8>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        case 3: return launch_partner_nb<3>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        case 4: return launch_partner_nb<4>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        case 5: return launch_partner_nb<5>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        case 6: return launch_partner_nb<6>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        case 7: return launch_partner_nb<7>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        case 8: return launch_partner_nb<8>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
         default: return hipErrorInvalidValue;
     }
 }

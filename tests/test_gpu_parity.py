@@ -198,3 +198,25 @@ def test_row_pass_every_block_count(device, D):
     ms = sorted(set(int(m) for m in plan.doc_table()[:, 4]))
     assert ms == [3, 8, 12, 15, 16, 18, 32, 36, 50, 64, 72, 81, 96, 100, 128, 135, 160, 256], ms
     assert_parity(y, reference(W, "fft"), W.cu_seqlens, "bf16", f"D={D}")
+
+
+@pytest.mark.parametrize("n1", [64, 256])
+def test_long_row_sizes_precision(device, n1):
+    """Row sizes 33..128 (the partner-row matrix-core kernel), including the rows that
+    are their own partners (u = 0 and u = N1 / 2), at a bar tighter than the parity
+    tolerance: a wrong value in one grid row of a document shows up as an error of a
+    few percent on a few positions, which the 2e-2 bar alone could miss.  Healthy
+    errors here are about 2e-3 (bf16 output rounding plus fp16 grids)."""
+    ks = (34, 40, 45, 54, 64, 90, 126)
+    for short_filter in (True, False):
+        # P >= len + min(len, L) - 1: about len for a 7-tap filter, 2 len for a full one
+        lens = [n1 * (k - 1) + 3 if short_filter else n1 * k // 2 + 3 for k in ks]
+        N = max(lens)
+        L = 7 if short_filter else N
+        rows = [[ln, N - ln] if ln < N else [ln] for ln in lens]
+        W = wl.make_case(rows, D=6, L=L, x_dtype="bf16", seed=L)
+        y, plan = run_gpu(W, device, n1=n1)
+        ms = sorted(set(int(m) for m in plan.doc_table()[:, 4]))
+        assert max(ms) > 100 and sum(33 <= m <= 128 for m in ms) >= 5, ms
+        g, d = assert_parity(y, reference(W, "fft"), W.cu_seqlens, "bf16", f"n1={n1} L={L}")
+        assert d <= 5e-3, (n1, L, d)
