@@ -16,13 +16,23 @@ padding of Algorithm 1; ``conv_at`` evaluates the sum at sampled positions;
 ``doc_table`` returns the document table and the minimal padded sizes
 ``L_i' = k * ceil((L_i + min(L_i, L) - 1) / k)`` of Algorithm 1.
 
+Gradients (the method targets training pipelines, Section 1): the map is linear in
+x and in k, so for an upstream gradient ``dy`` the gradients are the adjoints of
+the two maps.  ``grad_x`` is the anti-causal correlation inside every document,
+``dx[s] = sum_{tau <= min(s1 - 1 - s, L - 1)} k[d, tau] dy[s + tau]``; ``grad_k``
+sums ``dy[t] x[t - tau]`` over the tokens of every document of every row for each
+lag ``tau < L``; ``grad_k_at`` evaluates single entries.
+
 Pins (tests/test_oracle.py, tests/golden/): brute-force block-diagonal Toeplitz
 matrices, single documents against library convolutions (numpy.convolve,
 scipy.signal.lfilter, numpy.fft), delta inputs and delta filters, bilinearity,
 zero leakage across documents and row ends, closed forms (prefix sums,
 geometric-filter recurrences with a reset at each document start), document
 permutation and packing invariance, direct versus FFT agreement, and hand-worked
-examples.  No function here is "parity unpinned".
+examples.  The gradients are pinned by the adjoint identities
+``<y(x), dy> = <x, grad_x>`` and ``<y(k), dy> = <k, grad_k>`` against the pinned
+forward sum, by the transposes of explicit block-diagonal Toeplitz matrices, and by
+delta filters and impulse inputs.  No function here is "parity unpinned".
 """
 import ctypes
 import os
@@ -54,6 +64,12 @@ def _lib():
                                            f64p, f64p, f64p, c_int]
         lib.rco_conv_at.argtypes = [c_int, c_int, c_int, c_int, c_int, i32p, f64p, f64p,
                                     c_long, i64p, f64p, c_int]
+        lib.rco_conv_grad_x.argtypes = [c_int, c_int, c_int, c_int, c_int, i32p, f64p, f64p,
+                                        f64p, c_int]
+        lib.rco_conv_grad_k.argtypes = [c_int, c_int, c_int, c_int, c_int, i32p, f64p, f64p,
+                                        f64p, c_int]
+        lib.rco_conv_grad_k_at.argtypes = [c_int, c_int, c_int, c_int, c_int, i32p, f64p, f64p,
+                                           c_long, i64p, f64p, c_int]
         lib.rco_default_threads.argtypes = []
         _LIB = lib
     return _LIB
@@ -113,6 +129,47 @@ def conv_at(x, k, cu_seqlens, btd, threads: int = 0) -> np.ndarray:
     _check(_lib().rco_conv_at(B, N, D, L, nd, _p(cu, ctypes.c_int32), _p(x, ctypes.c_double),
                               _p(k, ctypes.c_double), btd.shape[0], _p(btd, ctypes.c_int64),
                               _p(out, ctypes.c_double), threads), "conv_at")
+    return out
+
+
+def grad_x(k, dy, cu_seqlens, threads: int = 0) -> np.ndarray:
+    """Gradient of the convolution with respect to x for an upstream gradient dy:
+    the anti-causal correlation of dy with k inside every document, float64."""
+    dy, k, cu, B, N, D, L, nd = _prep(dy, k, cu_seqlens)
+    dx = np.zeros_like(dy)
+    _check(_lib().rco_conv_grad_x(B, N, D, L, nd, _p(cu, ctypes.c_int32), _p(k, ctypes.c_double),
+                                  _p(dy, ctypes.c_double), _p(dx, ctypes.c_double), threads),
+           "grad_x")
+    return dx
+
+
+def grad_k(x, dy, cu_seqlens, L: int, threads: int = 0) -> np.ndarray:
+    """Gradient with respect to the filters, [D, L] float64: per channel and lag, the
+    sum over all documents of dy[t] x[t - lag] inside the document."""
+    kshape = np.zeros((np.shape(x)[2], L))
+    x, _, cu, B, N, D, L, nd = _prep(x, kshape, cu_seqlens)
+    dy = np.ascontiguousarray(dy, dtype=np.float64)
+    if dy.shape != x.shape:
+        raise OracleError("dy must have x's shape")
+    dk = np.zeros((D, L), dtype=np.float64)
+    _check(_lib().rco_conv_grad_k(B, N, D, L, nd, _p(cu, ctypes.c_int32), _p(x, ctypes.c_double),
+                                  _p(dy, ctypes.c_double), _p(dk, ctypes.c_double), threads),
+           "grad_k")
+    return dk
+
+
+def grad_k_at(x, dy, cu_seqlens, L: int, dt, threads: int = 0) -> np.ndarray:
+    """grad_k at entries ``dt[n, 2] = (d, lag)``."""
+    kshape = np.zeros((np.shape(x)[2], L))
+    x, _, cu, B, N, D, L, nd = _prep(x, kshape, cu_seqlens)
+    dy = np.ascontiguousarray(dy, dtype=np.float64)
+    if dy.shape != x.shape:
+        raise OracleError("dy must have x's shape")
+    dt = np.ascontiguousarray(dt, dtype=np.int64).reshape(-1, 2)
+    out = np.zeros(dt.shape[0], dtype=np.float64)
+    _check(_lib().rco_conv_grad_k_at(B, N, D, L, nd, _p(cu, ctypes.c_int32), _p(x, ctypes.c_double),
+                                     _p(dy, ctypes.c_double), dt.shape[0], _p(dt, ctypes.c_int64),
+                                     _p(out, ctypes.c_double), threads), "grad_k_at")
     return out
 
 

@@ -315,3 +315,119 @@ int rco_conv_at(int B, int N, int D, int L, int max_docs, const int32_t *cu,
     at_ctx ctx = {N, D, L, max_docs, cu, x, k, btd, out};
     return run_parallel(n, nthreads, 0, at_item, &ctx);
 }
+
+/* ------------------------------------------------------------------ gradients
+ * The convolution is linear in x and in k, so its gradients are the adjoints of
+ * the two linear maps (the transpose of the block-diagonal Toeplitz matrix of
+ * Section 3.2, and of the map k -> y).  For an upstream gradient dy:
+ *
+ *     dx[b,s,d] = sum_{tau = 0}^{min(s1 - 1 - s, L - 1)} k[d,tau] * dy[b,s+tau,d],
+ *                 s0 <= s < s1   (anti-causal correlation inside the document);
+ *     dk[d,tau] = sum over documents [s0, s1) of every row of
+ *                 sum_{t = s0 + tau}^{s1 - 1} dy[b,t,d] * x[b,t-tau,d],   tau < L.
+ */
+typedef struct {
+    const rco_doc *docs;
+    int n_docs, N, D, L;
+    const double *x, *k, *dy;
+    double *dx, *dk;
+} grad_ctx;
+
+/* dx for one (document, channel), lags ascending. */
+static void grad_x_item(void *vctx, long item, void *scratch) {
+    (void)scratch;
+    const grad_ctx *c = (const grad_ctx *)vctx;
+    const rco_doc *doc = &c->docs[item / c->D];
+    int d = (int)(item % c->D);
+    const double *kd = c->k + (size_t)d * c->L;
+    const double *dyrow = c->dy + ((size_t)doc->b * c->N + doc->start) * c->D + d;
+    double *dxrow = c->dx + ((size_t)doc->b * c->N + doc->start) * c->D + d;
+    for (int s = 0; s < doc->len; ++s) {
+        int last = doc->len - 1 - s < c->L - 1 ? doc->len - 1 - s : c->L - 1;
+        double acc = 0.0;
+        for (int tau = 0; tau <= last; ++tau) acc += kd[tau] * dyrow[(size_t)(s + tau) * c->D];
+        dxrow[(size_t)s * c->D] = acc;
+    }
+}
+
+int rco_conv_grad_x(int B, int N, int D, int L, int max_docs, const int32_t *cu,
+                    const double *k, const double *dy, double *dx, int nthreads) {
+    if (D < 1 || L < 1 || !k || !dy || !dx) return RCO_EBADARG;
+    rco_doc *docs = NULL;
+    int n = collect_docs(B, N, max_docs, cu, &docs);
+    if (n < 0) return n;
+    grad_ctx ctx = {docs, n, N, D, L, NULL, k, dy, dx, NULL};
+    int rc = run_parallel((long)n * D, nthreads, 0, grad_x_item, &ctx);
+    free(docs);
+    return rc;
+}
+
+/* dk for one channel: every document of every row, lags ascending, tokens ascending. */
+static void grad_k_item(void *vctx, long d, void *scratch) {
+    (void)scratch;
+    const grad_ctx *c = (const grad_ctx *)vctx;
+    double *dkd = c->dk + (size_t)d * c->L;
+    for (int tau = 0; tau < c->L; ++tau) dkd[tau] = 0.0;
+    for (int i = 0; i < c->n_docs; ++i) {
+        const rco_doc *doc = &c->docs[i];
+        const double *xrow = c->x + ((size_t)doc->b * c->N + doc->start) * c->D + d;
+        const double *dyrow = c->dy + ((size_t)doc->b * c->N + doc->start) * c->D + d;
+        int lags = doc->len < c->L ? doc->len : c->L;
+        for (int tau = 0; tau < lags; ++tau) {
+            double acc = 0.0;
+            for (int t = tau; t < doc->len; ++t)
+                acc += dyrow[(size_t)t * c->D] * xrow[(size_t)(t - tau) * c->D];
+            dkd[tau] += acc;
+        }
+    }
+}
+
+int rco_conv_grad_k(int B, int N, int D, int L, int max_docs, const int32_t *cu,
+                    const double *x, const double *dy, double *dk, int nthreads) {
+    if (D < 1 || L < 1 || !x || !dy || !dk) return RCO_EBADARG;
+    rco_doc *docs = NULL;
+    int n = collect_docs(B, N, max_docs, cu, &docs);
+    if (n < 0) return n;
+    grad_ctx ctx = {docs, n, N, D, L, x, NULL, dy, NULL, dk};
+    int rc = run_parallel(D, nthreads, 0, grad_k_item, &ctx);
+    free(docs);
+    return rc;
+}
+
+/* dk at n sampled entries dt[n][2] = (d, tau). */
+typedef struct {
+    grad_ctx g;
+    const int64_t *dt;
+    double *out;
+} grad_k_at_ctx;
+
+static void grad_k_at_item(void *vctx, long i, void *scratch) {
+    (void)scratch;
+    const grad_k_at_ctx *c = (const grad_k_at_ctx *)vctx;
+    int64_t d = c->dt[2 * i], tau = c->dt[2 * i + 1];
+    double acc = 0.0;
+    for (int j = 0; j < c->g.n_docs; ++j) {
+        const rco_doc *doc = &c->g.docs[j];
+        const double *xrow = c->g.x + ((size_t)doc->b * c->g.N + doc->start) * c->g.D + d;
+        const double *dyrow = c->g.dy + ((size_t)doc->b * c->g.N + doc->start) * c->g.D + d;
+        for (int64_t t = tau; t < doc->len; ++t)
+            acc += dyrow[(size_t)t * c->g.D] * xrow[(size_t)(t - tau) * c->g.D];
+    }
+    c->out[i] = acc;
+}
+
+int rco_conv_grad_k_at(int B, int N, int D, int L, int max_docs, const int32_t *cu,
+                       const double *x, const double *dy, long n, const int64_t *dt,
+                       double *out, int nthreads) {
+    if (D < 1 || L < 1 || !x || !dy || (n > 0 && (!dt || !out))) return RCO_EBADARG;
+    for (long i = 0; i < n; ++i)
+        if (dt[2 * i] < 0 || dt[2 * i] >= D || dt[2 * i + 1] < 0 || dt[2 * i + 1] >= L)
+            return RCO_EBADARG;
+    rco_doc *docs = NULL;
+    int nd = collect_docs(B, N, max_docs, cu, &docs);
+    if (nd < 0) return nd;
+    grad_k_at_ctx ctx = {{docs, nd, N, D, L, x, NULL, dy, NULL, NULL}, dt, out};
+    int rc = run_parallel(n, nthreads, 0, grad_k_at_item, &ctx);
+    free(docs);
+    return rc;
+}
