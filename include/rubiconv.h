@@ -141,6 +141,60 @@ rubiconv_status_t rubiconv_filter_spectrum(rubiconv_plan_t plan, const float* fi
 rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, const void* spectrum,
                                        void* y, void* workspace, hipStream_t stream);
 
+/*
+ * Gradients for training (the method targets training pipelines, Section 1).
+ * The convolution is linear in x and in k, so for an upstream gradient dy of y
+ * the gradients are the adjoints of the two maps:
+ *
+ *     dx[b][s][d] = sum_{tau = 0}^{min(s1 - 1 - s, L - 1)} k[d][tau] * dy[b][s + tau][d],
+ *                   s0 <= s < s1   (anti-causal correlation inside the document);
+ *     dk[d][tau]  = sum over every document [s0, s1) of every row of
+ *                   sum_{t = s0 + tau}^{s1 - 1} dy[b][t][d] * x[b][t - tau][d],   tau < L.
+ *
+ * Both run the convolution's four-step passes on the same plan.  For dx the
+ * product takes the filter spectrum at -f, i.e. its conjugate for real taps
+ * (Appendix, conjugate symmetry of real transforms).  For dk each document's
+ * product is dy's spectrum times the conjugate of x's spectrum on the
+ * document's own grid, the inverse leaves the document's cross-correlation at
+ * lags 0..len-1, and the documents' correlations are summed per channel and lag.
+ */
+
+/*
+ * dx for an upstream gradient dy.
+ *
+ *   dy         device [B][N][D] of the plan's y_dtype, channels last.
+ *   spectrum   device spectra written by rubiconv_filter_spectrum with this plan
+ *              (the same buffer the forward call uses).
+ *   dx         device [B][N][D] of the plan's x_dtype; every element is written.
+ *              dx must not overlap dy, spectrum or workspace.
+ *   workspace  device buffer of rubiconv_workspace_bytes(plan), 256-byte aligned.
+ *   stream     HIP stream the work is enqueued on.
+ * Errors: RUBICONV_ERR_ARG, RUBICONV_ERR_HIP.
+ */
+rubiconv_status_t rubiconv_packed_conv_dx(rubiconv_plan_t plan, const void* dy, const void* spectrum,
+                                          void* dx, void* workspace, hipStream_t stream);
+
+/* Bytes of device scratch rubiconv_packed_conv_dk needs: two document grids and
+ * a float32 [B][N][D] buffer.  0 for a null plan. */
+size_t rubiconv_dk_workspace_bytes(rubiconv_plan_t plan);
+
+/*
+ * dk for an upstream gradient dy and the forward input x.
+ *
+ *   x          device [B][N][D] of the plan's x_dtype (the forward call's input).
+ *   dy         device [B][N][D] of the plan's y_dtype.
+ *   dk         device float32 [D][L], row-major; every element is written (lags
+ *              no document reaches are 0).
+ *   workspace  device buffer of rubiconv_dk_workspace_bytes(plan), 256-byte
+ *              aligned; dk must not overlap it.
+ *   stream     HIP stream the work is enqueued on.
+ * The sum over documents runs in document order, so results are deterministic.
+ * Errors: RUBICONV_ERR_ARG, RUBICONV_ERR_UNSUPPORTED (a plan of 2^31 grid points
+ * or more), RUBICONV_ERR_HIP.
+ */
+rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, const void* dy,
+                                          float* dk, void* workspace, hipStream_t stream);
+
 /* Summary of a plan (host call, no device work). */
 typedef struct {
     int B, N, D, L;
@@ -167,7 +221,8 @@ rubiconv_status_t rubiconv_plan_doc_table(rubiconv_plan_t plan, int32_t* out, in
 /*
  * Stage timing (tracing; not for production loops).  After
  * rubiconv_profile_start(plan, max_calls), each of the next max_calls calls of
- * rubiconv_filter_spectrum / rubiconv_packed_conv with this plan records a HIP
+ * rubiconv_filter_spectrum / rubiconv_packed_conv / rubiconv_packed_conv_dx /
+ * rubiconv_packed_conv_dk with this plan records a HIP
  * event on its stream before its first kernel and after every kernel, so each
  * kernel's duration is measured on the stream it runs on.  rubiconv_profile_read
  * waits for the recorded events and returns, per kernel name, the number of

@@ -21,7 +21,7 @@ x and in k, so for an upstream gradient ``dy`` the gradients are the adjoints of
 the two maps.  ``grad_x`` is the anti-causal correlation inside every document,
 ``dx[s] = sum_{tau <= min(s1 - 1 - s, L - 1)} k[d, tau] dy[s + tau]``; ``grad_k``
 sums ``dy[t] x[t - tau]`` over the tokens of every document of every row for each
-lag ``tau < L``; ``grad_k_at`` evaluates single entries.
+lag ``tau < L``; ``grad_x_at`` and ``grad_k_at`` evaluate single entries.
 
 Pins (tests/test_oracle.py, tests/golden/): brute-force block-diagonal Toeplitz
 matrices, single documents against library convolutions (numpy.convolve,
@@ -68,6 +68,8 @@ def _lib():
                                         f64p, c_int]
         lib.rco_conv_grad_k.argtypes = [c_int, c_int, c_int, c_int, c_int, i32p, f64p, f64p,
                                         f64p, c_int]
+        lib.rco_conv_grad_x_at.argtypes = [c_int, c_int, c_int, c_int, c_int, i32p, f64p, f64p,
+                                           c_long, i64p, f64p, c_int]
         lib.rco_conv_grad_k_at.argtypes = [c_int, c_int, c_int, c_int, c_int, i32p, f64p, f64p,
                                            c_long, i64p, f64p, c_int]
         lib.rco_default_threads.argtypes = []
@@ -141,6 +143,17 @@ def grad_x(k, dy, cu_seqlens, threads: int = 0) -> np.ndarray:
                                   _p(dy, ctypes.c_double), _p(dx, ctypes.c_double), threads),
            "grad_x")
     return dx
+
+
+def grad_x_at(k, dy, cu_seqlens, bsd, threads: int = 0) -> np.ndarray:
+    """grad_x at positions ``bsd[n, 3] = (b, s, d)``."""
+    dy, k, cu, B, N, D, L, nd = _prep(dy, k, cu_seqlens)
+    bsd = np.ascontiguousarray(bsd, dtype=np.int64).reshape(-1, 3)
+    out = np.zeros(bsd.shape[0], dtype=np.float64)
+    _check(_lib().rco_conv_grad_x_at(B, N, D, L, nd, _p(cu, ctypes.c_int32), _p(k, ctypes.c_double),
+                                     _p(dy, ctypes.c_double), bsd.shape[0], _p(bsd, ctypes.c_int64),
+                                     _p(out, ctypes.c_double), threads), "grad_x_at")
+    return out
 
 
 def grad_k(x, dy, cu_seqlens, L: int, threads: int = 0) -> np.ndarray:

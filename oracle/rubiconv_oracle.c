@@ -431,3 +431,41 @@ int rco_conv_grad_k_at(int B, int N, int D, int L, int max_docs, const int32_t *
     free(docs);
     return rc;
 }
+
+/* dx at n sampled positions bsd[n][3] = (b, s, d). */
+typedef struct {
+    int N, D, L, max_docs;
+    const int32_t *cu;
+    const double *k, *dy;
+    const int64_t *bsd;
+    double *out;
+} grad_x_at_ctx;
+
+static void grad_x_at_item(void *vctx, long i, void *scratch) {
+    (void)scratch;
+    const grad_x_at_ctx *c = (const grad_x_at_ctx *)vctx;
+    int64_t b = c->bsd[3 * i], s = c->bsd[3 * i + 1], d = c->bsd[3 * i + 2];
+    const int32_t *row = c->cu + (size_t)b * (c->max_docs + 1);
+    int64_t s1 = c->N;
+    for (int j = 0; j < c->max_docs; ++j)            /* the document holding s */
+        if (row[j] <= s && s < row[j + 1]) { s1 = row[j + 1]; break; }
+    int64_t last = s1 - 1 - s < c->L - 1 ? s1 - 1 - s : c->L - 1;
+    double acc = 0.0;
+    for (int64_t tau = 0; tau <= last; ++tau)
+        acc += c->k[d * c->L + tau] * c->dy[((size_t)b * c->N + (s + tau)) * c->D + d];
+    c->out[i] = acc;
+}
+
+int rco_conv_grad_x_at(int B, int N, int D, int L, int max_docs, const int32_t *cu,
+                       const double *k, const double *dy, long n, const int64_t *bsd,
+                       double *out, int nthreads) {
+    if (D < 1 || L < 1 || !k || !dy || (n > 0 && (!bsd || !out))) return RCO_EBADARG;
+    int rc = rco_validate(B, N, max_docs, cu);
+    if (rc) return rc;
+    for (long i = 0; i < n; ++i)
+        if (bsd[3 * i] < 0 || bsd[3 * i] >= B || bsd[3 * i + 1] < 0 || bsd[3 * i + 1] >= N ||
+            bsd[3 * i + 2] < 0 || bsd[3 * i + 2] >= D)
+            return RCO_EBADARG;
+    grad_x_at_ctx ctx = {N, D, L, max_docs, cu, k, dy, bsd, out};
+    return run_parallel(n, nthreads, 0, grad_x_at_item, &ctx);
+}

@@ -22,8 +22,8 @@ from typing import Optional
 import numpy as np
 import torch
 
-__all__ = ["Plan", "RubiconvError", "filter_spectrum", "packed_conv", "conv", "library_path",
-           "load_library", "EXPORTED_SYMBOLS"]
+__all__ = ["Plan", "RubiconvError", "filter_spectrum", "packed_conv", "packed_conv_dx",
+           "packed_conv_dk", "conv", "library_path", "load_library", "EXPORTED_SYMBOLS"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "librubiconv.so")
@@ -36,6 +36,7 @@ _STATUS = {0: "ok", 1: "invalid argument", 2: "invalid cu_seqlens", 3: "unsuppor
 #: Every function ``include/rubiconv.h`` declares.
 EXPORTED_SYMBOLS = ("rubiconv_plan", "rubiconv_plan_destroy", "rubiconv_spectrum_bytes",
                     "rubiconv_workspace_bytes", "rubiconv_filter_spectrum", "rubiconv_packed_conv",
+                    "rubiconv_packed_conv_dx", "rubiconv_dk_workspace_bytes", "rubiconv_packed_conv_dk",
                     "rubiconv_plan_info", "rubiconv_plan_doc_table", "rubiconv_profile_start",
                     "rubiconv_profile_read", "rubiconv_status_string")
 
@@ -85,6 +86,12 @@ def load_library():
     lib.rubiconv_filter_spectrum.restype = c_int
     lib.rubiconv_packed_conv.argtypes = [vp, vp, vp, vp, vp, vp]
     lib.rubiconv_packed_conv.restype = c_int
+    lib.rubiconv_packed_conv_dx.argtypes = [vp, vp, vp, vp, vp, vp]
+    lib.rubiconv_packed_conv_dx.restype = c_int
+    lib.rubiconv_dk_workspace_bytes.argtypes = [vp]
+    lib.rubiconv_dk_workspace_bytes.restype = sz
+    lib.rubiconv_packed_conv_dk.argtypes = [vp, vp, vp, vp, vp, vp]
+    lib.rubiconv_packed_conv_dk.restype = c_int
     lib.rubiconv_plan_info.argtypes = [vp, ctypes.POINTER(_PlanInfo)]
     lib.rubiconv_plan_info.restype = c_int
     lib.rubiconv_plan_doc_table.argtypes = [vp, i32p, c_int, ctypes.POINTER(c_int)]
@@ -200,6 +207,13 @@ class Plan:
     def new_workspace(self, device) -> torch.Tensor:
         return torch.empty(self.workspace_bytes, dtype=torch.uint8, device=device)
 
+    @property
+    def dk_workspace_bytes(self) -> int:
+        return int(self._lib.rubiconv_dk_workspace_bytes(self.handle))
+
+    def new_dk_workspace(self, device) -> torch.Tensor:
+        return torch.empty(self.dk_workspace_bytes, dtype=torch.uint8, device=device)
+
     def close(self):
         if self._h:
             self._lib.rubiconv_plan_destroy(self._h)
@@ -267,6 +281,60 @@ def packed_conv(plan: Plan, x: torch.Tensor, spectrum: torch.Tensor,
                                               _stream_handle(dev, stream)),
                "rubiconv_packed_conv")
     return y
+
+
+def _check_btd(t: torch.Tensor, plan: "Plan", code: int, name: str):
+    _cuda_contig(t, name)
+    if tuple(t.shape) != (plan.B, plan.N, plan.D) or t.dtype != _torch_dtype(code):
+        raise ValueError(f"{name} must be {_torch_dtype(code)} [{plan.B}, {plan.N}, {plan.D}]")
+
+
+def packed_conv_dx(plan: Plan, dy: torch.Tensor, spectrum: torch.Tensor,
+                   dx: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                   stream=None) -> torch.Tensor:
+    """dx[b, s, d] = sum over the lags that stay in s's document of k[d, tau] dy[b, s + tau, d]
+    (dy has the plan's y dtype, dx its x dtype)."""
+    _check_btd(dy, plan, plan.y_dtype, "dy")
+    dev = dy.device
+    if dx is None:
+        dx = torch.empty((plan.B, plan.N, plan.D), dtype=_torch_dtype(plan.x_dtype), device=dev)
+    _check_btd(dx, plan, plan.x_dtype, "dx")
+    if workspace is None:
+        workspace = plan.new_workspace(dev)
+    if workspace.numel() * workspace.element_size() < plan.workspace_bytes:
+        raise ValueError("workspace buffer too small")
+    if spectrum.numel() * spectrum.element_size() < plan.spectrum_bytes:
+        raise ValueError("spectrum buffer too small")
+    with torch.cuda.device(dev):
+        _check(plan._lib.rubiconv_packed_conv_dx(plan.handle, dy.data_ptr(), spectrum.data_ptr(),
+                                                 dx.data_ptr(), workspace.data_ptr(),
+                                                 _stream_handle(dev, stream)),
+               "rubiconv_packed_conv_dx")
+    return dx
+
+
+def packed_conv_dk(plan: Plan, x: torch.Tensor, dy: torch.Tensor,
+                   dk: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                   stream=None) -> torch.Tensor:
+    """dk[d, tau] = sum over every document of dy[b, t, d] x[b, t - tau, d], float32 [D, L]."""
+    _check_btd(x, plan, plan.x_dtype, "x")
+    _check_btd(dy, plan, plan.y_dtype, "dy")
+    dev = x.device
+    if dk is None:
+        dk = torch.empty((plan.D, plan.L), dtype=torch.float32, device=dev)
+    _cuda_contig(dk, "dk")
+    if tuple(dk.shape) != (plan.D, plan.L) or dk.dtype != torch.float32:
+        raise ValueError(f"dk must be float32 [{plan.D}, {plan.L}]")
+    if workspace is None:
+        workspace = plan.new_dk_workspace(dev)
+    if workspace.numel() * workspace.element_size() < plan.dk_workspace_bytes:
+        raise ValueError("workspace buffer too small")
+    with torch.cuda.device(dev):
+        _check(plan._lib.rubiconv_packed_conv_dk(plan.handle, x.data_ptr(), dy.data_ptr(),
+                                                 dk.data_ptr(), workspace.data_ptr(),
+                                                 _stream_handle(dev, stream)),
+               "rubiconv_packed_conv_dk")
+    return dk
 
 
 def conv(x: torch.Tensor, filters: torch.Tensor, cu_seqlens, y_dtype=None, n1: int = 0):

@@ -349,7 +349,7 @@ __global__ __launch_bounds__(256) void row_conv_kernel(G* __restrict__ grid,
                                                        int64_t grid_pb_stride,
                                                        const G* __restrict__ fgrid,
                                                        int64_t fgrid_pb_stride, LaunchTables t,
-                                                       int n1) {
+                                                       int n1, int corr) {
     extern __shared__ float2 sm[];
     const RowTask r = row_task(t, n1);
     const int pb = blockIdx.y;
@@ -370,7 +370,9 @@ __global__ __launch_bounds__(256) void row_conv_kernel(G* __restrict__ grid,
         const int v = e >> r.spb_log2;
         const int vb = partner_col(r.u, v, r.m);
         float2 s, df;
-        filter_sdf(zh[e], zh[((r.nrows - 1) * r.m + vb) * r.spb + pp], c, s, df);
+        // correlation: the filter spectrum read at -f (its conjugate for real taps)
+        const float2 fa = zh[e], fb = zh[((r.nrows - 1) * r.m + vb) * r.spb + pp];
+        filter_sdf(corr ? fb : fa, corr ? fa : fb, c, s, df);
         sdf[e] = s;
         sdf[rowlen + e] = df;
     }
@@ -443,6 +445,44 @@ __global__ __launch_bounds__(256) void transpose_pairs_kernel(const float* __res
             const __half2 v = __float22half2_rn(make_float2(tile[2 * tx][k], tile[2 * tx + 1][k]));
             out[static_cast<int64_t>(t) * half_d + q] = __builtin_bit_cast(uint32_t, v);
         }
+    }
+}
+
+// Filter gradient, last step: every document's cross-correlation r_i[tau] of dy
+// with x (lags 0 <= tau < min(len_i, L), written by the inverse passes at the
+// document's token positions s_i + tau of a [B][N][D] fp32 buffer) summed over the
+// documents into dk[D][L], documents in table order.  A workgroup owns 64 lags x 64
+// channels: lanes run along channels for the reads and along lags for the writes
+// (through LDS).
+__global__ __launch_bounds__(256) void lag_sum_kernel(const float* __restrict__ r,
+                                                      const Seg* __restrict__ segs, int n_docs,
+                                                      int N, int D, int L, float* __restrict__ dk) {
+    __shared__ float tile[64][65];
+    const int tau0 = blockIdx.x * 64, d0 = blockIdx.y * 64;
+    const int dl = threadIdx.x & 63, tq = threadIdx.x >> 6;  // channel lane, lag quarter
+    const int d = d0 + dl;
+    float acc[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
+    for (int k = 0; k < n_docs; ++k) {
+        const Seg sg = segs[k];
+        const int lags = sg.len < L ? sg.len : L;
+        if (lags <= tau0 || d >= D) continue;
+        const float* base = r + (static_cast<int64_t>(sg.row) * N + sg.start) * D + d;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int tau = tau0 + tq * 16 + i;
+            if (tau < lags) acc[i] += base[static_cast<int64_t>(tau) * D];
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) tile[tq * 16 + i][dl] = acc[i];
+    __syncthreads();
+    // write: lane along lags
+    const int tl = threadIdx.x & 63, dq = threadIdx.x >> 6;
+    for (int j = dq; j < 64; j += 4) {
+        const int dd = d0 + j, tau = tau0 + tl;
+        if (dd < D && tau < L) dk[static_cast<int64_t>(dd) * L + tau] = tile[tl][j];
     }
 }
 
@@ -533,7 +573,7 @@ hipError_t launch_col_inv(int r, bool half, int y_dtype, const void* grid, int64
 
 hipError_t launch_row_conv(int n1, bool half, void* grid, int64_t grid_pb_stride,
                            const void* fgrid, int64_t fgrid_pb_stride, const LaunchTables& t,
-                           int n_tasks, int npb, int lds_bytes, hipStream_t stream) {
+                           int n_tasks, int npb, int lds_bytes, int corr, hipStream_t stream) {
     if (n_tasks == 0) return hipSuccess;
     const dim3 g(n_tasks, npb), b(256);
     hipError_t e;
@@ -543,15 +583,23 @@ hipError_t launch_row_conv(int n1, bool half, void* grid, int64_t grid_pb_stride
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(row_conv_kernel<__half2>, g, b, lds_bytes, stream,
                            static_cast<__half2*>(grid), grid_pb_stride,
-                           static_cast<const __half2*>(fgrid), fgrid_pb_stride, t, n1);
+                           static_cast<const __half2*>(fgrid), fgrid_pb_stride, t, n1, corr);
     } else {
         e = hipFuncSetAttribute(reinterpret_cast<const void*>(&row_conv_kernel<float2>),
                                 hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(row_conv_kernel<float2>, g, b, lds_bytes, stream,
                            static_cast<float2*>(grid), grid_pb_stride,
-                           static_cast<const float2*>(fgrid), fgrid_pb_stride, t, n1);
+                           static_cast<const float2*>(fgrid), fgrid_pb_stride, t, n1, corr);
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_lag_sum(const float* r, const Seg* segs, int n_docs, int N, int D, int L,
+                          float* dk, hipStream_t stream) {
+    if (D <= 0 || L <= 0) return hipSuccess;
+    const dim3 g((L + 63) / 64, (D + 63) / 64), b(256);
+    hipLaunchKernelGGL(lag_sum_kernel, g, b, 0, stream, r, segs, n_docs, N, D, L, dk);
     return hipGetLastError();
 }
 

@@ -49,15 +49,18 @@ hipError_t launch_col_inv(int r, bool half, int y_dtype, const void* grid, int64
 
 // Row pass: row DFTs of the filter class rows and the document rows, the
 // separation and product, the inverse row DFT (generic kernel: long rows).
+// Every row launcher takes `corr`: 0 multiplies by the filter spectrum F(f)
+// (convolution), 1 by F(-f) = conj F(f) (correlation, the adjoint in x).
 hipError_t launch_row_conv(int n1, bool half, void* grid, int64_t grid_pb_stride,
                            const void* fgrid, int64_t fgrid_pb_stride, const LaunchTables& t,
-                           int n_tasks, int npb, int lds_bytes, hipStream_t stream);
+                           int n_tasks, int npb, int lds_bytes, int corr, hipStream_t stream);
 
 // Register-resident row pass for a listed row size m (row_sizes.hpp) over the
 // nlist documents list[0..nlist) of that size.
 hipError_t launch_row_fast(int m, bool half, void* grid, int64_t grid_pb_stride, const void* fgrid,
                            int64_t fgrid_pb_stride, const Seg* segs, const int32_t* list,
-                           int nlist, const float2* tw, int n1, int npb, hipStream_t stream);
+                           int nlist, const float2* tw, int n1, int npb, int corr,
+                           hipStream_t stream);
 
 // Matrix-core row pass (complex fp16 grids): the documents of `list` all have
 // ceil(m / 16) == nb (1 <= nb <= kMaxDenseBlocks); tabs = the plan's dense operand
@@ -69,7 +72,8 @@ constexpr int partner_tab_u4(int nb) { return (2 * nb * nb * 64 + 12 * nb + 63) 
 
 hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const void* fgrid,
                             int64_t fgrid_pb_stride, const Seg* segs, const int32_t* list,
-                            int nlist, const void* tabs, int n1, int npb, hipStream_t stream);
+                            int nlist, const void* tabs, int n1, int npb, int corr,
+                            hipStream_t stream);
 
 // Matrix-core column passes (N1 = 256, complex fp16 grids, D a multiple of 32).
 // `mtab` holds the MFMA operand tables in lane order (16-byte entries, offsets
@@ -90,6 +94,11 @@ hipError_t launch_col_fwd_mfma(int src_dtype, const void* src, int64_t src_row_s
 hipError_t launch_col_inv_mfma(int y_dtype, const void* grid, int64_t grid_pb_stride, void* dst,
                                int64_t dst_row_stride, int D, const LaunchTables& t,
                                const void* mtab, int n_cols, int npb, hipStream_t stream);
+
+// dk[d][tau] = sum over documents k < n_docs with tau < min(len_k, L) of
+// r[row_k][start_k + tau][d] (r fp32 [B][N][D]); dk [D][L] fp32, fully written.
+hipError_t launch_lag_sum(const float* r, const Seg* segs, int n_docs, int N, int D, int L,
+                          float* dk, hipStream_t stream);
 
 // Filter taps [D][in_ld] fp32 -> [taps][D / 2] complex fp16 channel pairs (D even).
 hipError_t launch_transpose_pairs(const float* in, int D, int taps, int in_ld, void* out,

@@ -169,7 +169,8 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
                                                                int64_t fgrid_pb_stride,
                                                                const Seg* __restrict__ segs,
                                                                const int32_t* __restrict__ list,
-                                                               const u4* __restrict__ tabs, int n1) {
+                                                               const u4* __restrict__ tabs, int n1,
+                                                               int corr) {
     constexpr int S = 16 * NB;                     // points per row, padded to whole blocks
     constexpr int kTabU4 = 4 * NB * NB * 64;       // forward then inverse fragments
     constexpr int kStage = 4 * S * 16;             // u32 per wave: four rows [point][16 pairs]
@@ -288,9 +289,11 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
         for (int r = 0; r < 4; ++r) {
             const int slot = rbase - 16 * kb - r;  // >= -15: inside the zeroed front slots
             const uint32_t b = xlds[16 * slot];
-            const uint32_t bf = flds[16 * slot];
             const uint32_t a = au[kb][r];
-            const uint32_t A = fa[kb][r];
+            // correlation: the filter spectrum read at -f (its conjugate for real taps)
+            const uint32_t fl = flds[16 * slot];
+            const uint32_t A = corr ? fl : fa[kb][r];
+            const uint32_t bf = corr ? fa[kb][r] : fl;
             const uint32_t e1 = pk_add_conj(a, b);
             const uint32_t e2 = pk_swap_add_conj(a, b);
             const uint32_t U = pk_add_neg_hi(e1, e2);
@@ -379,7 +382,7 @@ __global__ __launch_bounds__(64 * kPartnerWaves) __attribute__((amdgpu_waves_per
 void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
                         const uint32_t* __restrict__ fgrid, int64_t fgrid_pb_stride,
                         const Seg* __restrict__ segs, const int32_t* __restrict__ list,
-                        const u4* __restrict__ tabs, int n1) {
+                        const u4* __restrict__ tabs, int n1, int corr) {
     constexpr int S = 16 * NB;
     constexpr int kFrag = NB * NB * 64;            // u4 per direction
     constexpr int kTab = partner_tab_u4(NB);
@@ -486,7 +489,9 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const uint32_t a = au[kb][r], b = ap[kb][r];
-            const uint32_t A = fa[kb][r], Bf = fp[kb][r];
+            // correlation: the filter spectrum read at -f (its conjugate for real taps)
+            const uint32_t A = corr ? fp[kb][r] : fa[kb][r];
+            const uint32_t Bf = corr ? fa[kb][r] : fp[kb][r];
             const uint32_t e1 = pk_add_conj(a, b);       // s
             const uint32_t e2 = pk_swap_add_conj(a, b);  // (Im d, Re d)
             const uint32_t U = pk_add_neg_hi(e1, e2);    // s - i d
@@ -532,24 +537,24 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
 template <int NB>
 hipError_t launch_lds_nb(void* grid, int64_t gs, const void* fgrid, int64_t fs, const Seg* segs,
                          const int32_t* list, int nlist, const void* tabs, int n1, int npb,
-                         hipStream_t stream) {
+                         int corr, hipStream_t stream) {
     const int ug = (n1 / 2 + 1 + kLdsWaves - 1) / kLdsWaves;
     const dim3 g(nlist * ug, npb), b(64 * kLdsWaves);
     hipLaunchKernelGGL((row_lds_kernel<NB>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
                        static_cast<const uint32_t*>(fgrid), fs, segs, list,
-                       static_cast<const u4*>(tabs), n1);
+                       static_cast<const u4*>(tabs), n1, corr);
     return hipGetLastError();
 }
 
 template <int NB>
 hipError_t launch_partner_nb(void* grid, int64_t gs, const void* fgrid, int64_t fs, const Seg* segs,
                              const int32_t* list, int nlist, const void* tabs, int n1, int npb,
-                             hipStream_t stream) {
+                             int corr, hipStream_t stream) {
     const int ug = (n1 / 2 + 1 + kPartnerWaves - 1) / kPartnerWaves;
     const dim3 g(nlist * ug, npb), b(64 * kPartnerWaves);
     hipLaunchKernelGGL((row_partner_kernel<NB>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
                        static_cast<const uint32_t*>(fgrid), fs, segs, list,
-                       static_cast<const u4*>(tabs), n1);
+                       static_cast<const u4*>(tabs), n1, corr);
     return hipGetLastError();
 }
 
@@ -557,17 +562,18 @@ hipError_t launch_partner_nb(void* grid, int64_t gs, const void* fgrid, int64_t 
 
 hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const void* fgrid,
                             int64_t fgrid_pb_stride, const Seg* segs, const int32_t* list,
-                            int nlist, const void* tabs, int n1, int npb, hipStream_t stream) {
+                            int nlist, const void* tabs, int n1, int npb, int corr,
+                            hipStream_t stream) {
     if (nlist == 0) return hipSuccess;
     switch (nb) {
-        case 1: return launch_lds_nb<1>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
-        case 2: return launch_lds_nb<2>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
-        case 3: return launch_partner_nb<3>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
-        case 4: return launch_partner_nb<4>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
-        case 5: return launch_partner_nb<5>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
-        case 6: return launch_partner_nb<6>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
-        case 7: return launch_partner_nb<7>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
-        case 8: return launch_partner_nb<8>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, stream);
+        case 1: return launch_lds_nb<1>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, corr, stream);
+        case 2: return launch_lds_nb<2>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, corr, stream);
+        case 3: return launch_partner_nb<3>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, corr, stream);
+        case 4: return launch_partner_nb<4>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, corr, stream);
+        case 5: return launch_partner_nb<5>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, corr, stream);
+        case 6: return launch_partner_nb<6>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, corr, stream);
+        case 7: return launch_partner_nb<7>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, corr, stream);
+        case 8: return launch_partner_nb<8>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, corr, stream);
         default: return hipErrorInvalidValue;
     }
 }

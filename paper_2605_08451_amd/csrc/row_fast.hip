@@ -68,7 +68,8 @@ __global__ __launch_bounds__(32 * M1) void row_fast_kernel(G* __restrict__ grid,
                                                            int64_t fgrid_pb_stride,
                                                            const Seg* __restrict__ segs,
                                                            const int32_t* __restrict__ list,
-                                                           const float2* __restrict__ tw, int n1) {
+                                                           const float2* __restrict__ tw, int n1,
+                                                           int corr) {
     constexpr int M = M1 * M2;
     __shared__ float2 lds[M * 32];
     __shared__ float2 roots[M];  // w_m^h, h < m
@@ -115,10 +116,9 @@ __global__ __launch_bounds__(32 * M1) void row_fast_kernel(G* __restrict__ grid,
         for (int k2 = 0; k2 < M2; ++k2) {
             const int vv = q + M1 * k2;
             const float2 par = lds[partner_v(u, vv, M) * 32 + pline];
-            if (r == 0)
-                filter_sdf(w[k2], par, c, s[k2], df[k2]);
-            else
-                filter_sdf(par, w[k2], c, s[k2], df[k2]);
+            // correlation: the filter spectrum read at -f (its conjugate for real taps)
+            const bool own_first = (r == 0) != (corr != 0);
+            filter_sdf(own_first ? w[k2] : par, own_first ? par : w[k2], c, s[k2], df[k2]);
         }
     }
     __syncthreads();  // partner reads done before the data reuses LDS
@@ -156,10 +156,10 @@ __global__ __launch_bounds__(32 * M1) void row_fast_kernel(G* __restrict__ grid,
 template <int M1, int M2, class G>
 hipError_t launch_mg(void* grid, int64_t gs, const void* fgrid, int64_t fs, const Seg* segs,
                      const int32_t* list, int nlist, const float2* tw, int n1, int npb,
-                     hipStream_t stream) {
+                     int corr, hipStream_t stream) {
     const dim3 g(nlist * (n1 / 2 + 1), npb), b(32 * M1);
     hipLaunchKernelGGL((row_fast_kernel<M1, M2, G>), g, b, 0, stream, static_cast<G*>(grid), gs,
-                       static_cast<const G*>(fgrid), fs, segs, list, tw, n1);
+                       static_cast<const G*>(fgrid), fs, segs, list, tw, n1, corr);
     return hipGetLastError();
 }
 
@@ -167,15 +167,16 @@ hipError_t launch_mg(void* grid, int64_t gs, const void* fgrid, int64_t fs, cons
 
 hipError_t launch_row_fast(int m, bool half, void* grid, int64_t grid_pb_stride, const void* fgrid,
                            int64_t fgrid_pb_stride, const Seg* segs, const int32_t* list,
-                           int nlist, const float2* tw, int n1, int npb, hipStream_t stream) {
+                           int nlist, const float2* tw, int n1, int npb, int corr,
+                           hipStream_t stream) {
     if (nlist == 0) return hipSuccess;
     switch (m) {
 #define RUBICONV_CASE(mm, a, b)                                                                  \
     case mm:                                                                                     \
         return half ? launch_mg<a, b, __half2>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, \
-                                               list, nlist, tw, n1, npb, stream)                  \
+                                               list, nlist, tw, n1, npb, corr, stream)            \
                     : launch_mg<a, b, float2>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs,  \
-                                              list, nlist, tw, n1, npb, stream);
+                                              list, nlist, tw, n1, npb, corr, stream);
         RUBICONV_ROW_SIZES(RUBICONV_CASE)
 #undef RUBICONV_CASE
         default:

@@ -8,6 +8,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <climits>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -33,11 +34,14 @@ struct rubiconv_plan_s {
     bool device_ready = false;
     LaunchTables doc_t{};
     LaunchTables cls_t{};
+    LaunchTables grad_t{};       // doc_t with each document's "filter" rows at its own grid rows
     int64_t grid_pb_stride = 0;  // grid elements per pair block, document grid
     int64_t cls_pb_stride = 0;   // same, filter class grids (the spectrum buffer)
     size_t taps_bytes = 0;       // transposed filter taps (workspace of the filter call)
     size_t spec_bytes = 0;
     size_t ws_bytes = 0;
+    size_t grid_bytes = 0;       // one document grid (all pair blocks)
+    size_t dk_ws_bytes = 0;      // rubiconv_packed_conv_dk: two grids and an fp32 [B][N][D] buffer
     // The row pass runs its size classes (independent launches) on side streams
     // forked from and joined back into the caller's stream with events; the mutex
     // keeps one call's record/wait sequence from interleaving with another's.
@@ -64,6 +68,7 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     const size_t n_segs = h.docs.size() + h.classes.size();
     size_t off = 0;
     const size_t o_segs = off;       off = align_up(off + n_segs * sizeof(Seg));
+    const size_t o_gsegs = off;      off = align_up(off + h.docs.size() * sizeof(Seg));
     const size_t o_dcol = off;       off = align_up(off + h.doc_col_seg.size() * 4);
     const size_t o_dtask = off;      off = align_up(off + h.doc_task_seg.size() * 4);
     const size_t o_ccol = off;       off = align_up(off + h.cls_col_seg.size() * 4);
@@ -80,6 +85,11 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     std::vector<Seg> segs(h.docs);
     segs.insert(segs.end(), h.classes.begin(), h.classes.end());
     std::memcpy(img.data() + o_segs, segs.data(), n_segs * sizeof(Seg));
+    {  // filter gradient: the second operand of a document's row stage is its own x grid
+        std::vector<Seg> gsegs(h.docs);
+        for (Seg& g : gsegs) g.spec_off = static_cast<int32_t>(g.grid_off);
+        if (!gsegs.empty()) std::memcpy(img.data() + o_gsegs, gsegs.data(), gsegs.size() * sizeof(Seg));
+    }
     std::memcpy(img.data() + o_dcol, h.doc_col_seg.data(), h.doc_col_seg.size() * 4);
     std::memcpy(img.data() + o_dtask, h.doc_task_seg.data(), h.doc_task_seg.size() * 4);
     std::memcpy(img.data() + o_ccol, h.cls_col_seg.data(), h.cls_col_seg.size() * 4);
@@ -115,6 +125,8 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     pl->doc_t = LaunchTables{dsegs, reinterpret_cast<const int32_t*>(base + o_dcol),
                              reinterpret_cast<const int32_t*>(base + o_dtask), tw, twn,
                              reinterpret_cast<const int32_t*>(base + o_cdoc)};
+    pl->grad_t = pl->doc_t;
+    pl->grad_t.segs = reinterpret_cast<const Seg*>(base + o_gsegs);
     pl->cls_t = LaunchTables{dsegs + h.docs.size(), reinterpret_cast<const int32_t*>(base + o_ccol),
                              nullptr, tw, twn,
                              reinterpret_cast<const int32_t*>(base + o_cid)};
@@ -171,6 +183,102 @@ struct StageRecorder {
     }
 };
 
+// Stage names in the profile: the forward's plain, the gradients' prefixed.
+std::string stage(const char* tag, const char* name) { return std::string(tag) + name; }
+
+// The data passes shared by the convolution and its gradients: column DFTs of `in`
+// (dtype in_dtype, [B][N][D]) into `grid`; the row stage against the second grid
+// `fgrid`, whose rows for each document are located by the spec_off of the segment
+// table `t` (the filter class grids, or a document grid of the same plan); the
+// product with F(f) (corr = 0) or F(-f) (corr = 1); the inverse passes into `out`
+// (dtype out_dtype).  The caller holds the plan's launch mutex.
+hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, const void* fgrid,
+                        int64_t fgrid_pb_stride, const LaunchTables& t, void* out, int out_dtype,
+                        void* grid, int corr, const char* tag, hipStream_t stream,
+                        StageRecorder& rec) {
+    const HostPlan& h = plan->h;
+    const int n_cols = static_cast<int>(h.doc_col_seg.size());
+    const int64_t rs = static_cast<int64_t>(h.N) * h.D;
+    const bool half = h.grid_half;
+    hipError_t e = h.col_mfma && in_dtype == RUBICONV_BF16
+                       ? rubiconv::launch_col_fwd_mfma(in_dtype, in, rs, h.D, grid,
+                                                       plan->grid_pb_stride, plan->doc_t,
+                                                       plan->mfma_tab, n_cols, h.npb, stream)
+                       : rubiconv::launch_col_fwd(h.r, half, in_dtype, in, rs, h.D, grid,
+                                                  plan->grid_pb_stride, plan->doc_t, n_cols, h.npb,
+                                                  stream);
+    rec.mark(stage(tag, "col_fwd"));
+    // row pass: the generic kernel (long rows) and one launch per listed size
+    // class, spread over the side streams (largest work first, least-loaded stream)
+    struct Launch {
+        int cls;       // -1: generic kernel; >= 0: register-resident kernel of that class
+        int nb;        // > 0: matrix-core kernel for the documents of that block count
+        double work;
+    };
+    std::vector<Launch> launches;
+    if (!h.doc_task_seg.empty()) launches.push_back({-1, 0, 1e30});
+    for (size_t c = 0; c < h.classes.size(); ++c) {
+        const int m = h.classes[c].m;
+        if (m > rubiconv::kMaxFastM || (h.row_dense && m <= 16 * rubiconv::kMaxDenseBlocks)) continue;
+        launches.push_back({static_cast<int>(c), 0, static_cast<double>(m) * h.classes[c].nlist});
+    }
+    if (h.row_dense)
+        for (int nb = 1; nb <= rubiconv::kMaxDenseBlocks; ++nb) {
+            if (h.dense_count[nb] == 0) continue;
+            double w = 0;
+            for (int k = 0; k < h.dense_count[nb]; ++k) w += h.docs[h.dense_docs[h.dense_list0[nb] + k]].m;
+            launches.push_back({-1, nb, w});
+        }
+    std::sort(launches.begin(), launches.end(),
+              [](const Launch& a, const Launch& b) { return a.work > b.work; });
+    const int nside = std::min<int>(rubiconv_plan_s::kSideStreams, static_cast<int>(launches.size()));
+    auto launch_one = [&](const Launch& L, hipStream_t s) -> hipError_t {
+        if (L.nb > 0)
+            return rubiconv::launch_row_dense(L.nb, grid, plan->grid_pb_stride, fgrid,
+                                              fgrid_pb_stride, t.segs,
+                                              plan->dense_docs + h.dense_list0[L.nb],
+                                              h.dense_count[L.nb], plan->dense_tab, h.n1, h.npb,
+                                              corr, s);
+        if (L.cls < 0)
+            return rubiconv::launch_row_conv(h.n1, half, grid, plan->grid_pb_stride, fgrid,
+                                             fgrid_pb_stride, t,
+                                             static_cast<int>(h.doc_task_seg.size()), h.npb,
+                                             h.row_lds_docs, corr, s);
+        const Seg& cs = h.classes[L.cls];
+        return rubiconv::launch_row_fast(cs.m, half, grid, plan->grid_pb_stride, fgrid,
+                                         fgrid_pb_stride, t.segs, plan->doc_t.list + cs.list0,
+                                         cs.nlist, plan->doc_t.tw, h.n1, h.npb, corr, s);
+    };
+    if (nside <= 1) {
+        for (const Launch& L : launches)
+            if (e == hipSuccess) e = launch_one(L, stream);
+    } else if (e == hipSuccess) {
+        e = hipEventRecord(plan->fork, stream);
+        for (int k = 0; k < nside && e == hipSuccess; ++k) e = hipStreamWaitEvent(plan->side[k], plan->fork, 0);
+        std::vector<double> load(nside, 0.0);
+        for (const Launch& L : launches) {
+            if (e != hipSuccess) break;
+            const int k = static_cast<int>(std::min_element(load.begin(), load.end()) - load.begin());
+            load[k] += L.work;
+            e = launch_one(L, plan->side[k]);
+        }
+        for (int k = 0; k < nside && e == hipSuccess; ++k) {
+            e = hipEventRecord(plan->join[k], plan->side[k]);
+            if (e == hipSuccess) e = hipStreamWaitEvent(stream, plan->join[k], 0);
+        }
+    }
+    rec.mark(stage(tag, "row_conv"));
+    if (e == hipSuccess)
+        e = h.col_mfma ? rubiconv::launch_col_inv_mfma(out_dtype, grid, plan->grid_pb_stride, out,
+                                                       rs, h.D, plan->doc_t, plan->mfma_tab, n_cols,
+                                                       h.npb, stream)
+                       : rubiconv::launch_col_inv(h.r, half, out_dtype, grid,
+                                                  plan->grid_pb_stride, out, rs, h.D, plan->doc_t,
+                                                  n_cols, h.npb, stream);
+    rec.mark(stage(tag, "col_inv"));
+    return e;
+}
+
 }  // namespace
 
 extern "C" {
@@ -200,6 +308,8 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
     const size_t conv_ws = align_up(static_cast<size_t>(h.npb) * pl->grid_pb_stride * esz);
     const size_t filt_ws = pl->taps_bytes;
     pl->ws_bytes = std::max(conv_ws, filt_ws);
+    pl->grid_bytes = conv_ws;
+    pl->dk_ws_bytes = 2 * conv_ws + align_up(static_cast<size_t>(h.B) * h.N * h.D * 4);
     rubiconv_status_t st = upload(pl);
     if (st != RUBICONV_OK) {
         destroy_side_streams(pl);
@@ -259,88 +369,72 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
     if (reinterpret_cast<uintptr_t>(x) % esz || reinterpret_cast<uintptr_t>(y) % ysz)
         return RUBICONV_ERR_ARG;
     if (!plan->device_ready) return RUBICONV_ERR_HIP;
-    const HostPlan& h = plan->h;
-    const int n_cols = static_cast<int>(h.doc_col_seg.size());
-    const int64_t rs = static_cast<int64_t>(h.N) * h.D;
     std::lock_guard<std::mutex> lock(plan->launch_mu);
     StageRecorder rec(plan, stream);
-    const bool half = h.grid_half;
-    hipError_t e = h.col_mfma
-                       ? rubiconv::launch_col_fwd_mfma(h.x_dtype, x, rs, h.D, workspace,
+    const hipError_t e = enqueue_conv(plan, x, plan->h.x_dtype, spectrum, plan->cls_pb_stride,
+                                      plan->doc_t, y, plan->h.y_dtype, workspace, 0, "", stream, rec);
+    return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
+}
+
+rubiconv_status_t rubiconv_packed_conv_dx(rubiconv_plan_t plan, const void* dy, const void* spectrum,
+                                          void* dx, void* workspace, hipStream_t stream) {
+    if (!plan || !dy || !spectrum || !dx || !workspace) return RUBICONV_ERR_ARG;
+    if (!aligned(spectrum) || !aligned(workspace)) return RUBICONV_ERR_ARG;
+    const size_t xsz = plan->h.x_dtype == RUBICONV_F32 ? 4 : 2;
+    const size_t ysz = plan->h.y_dtype == RUBICONV_F32 ? 4 : 2;
+    if (reinterpret_cast<uintptr_t>(dy) % ysz || reinterpret_cast<uintptr_t>(dx) % xsz)
+        return RUBICONV_ERR_ARG;
+    if (!plan->device_ready) return RUBICONV_ERR_HIP;
+    std::lock_guard<std::mutex> lock(plan->launch_mu);
+    StageRecorder rec(plan, stream);
+    // dy has y's dtype and dx has x's: the correlation runs the convolution's passes
+    // with the roles of the two dtypes exchanged
+    const hipError_t e = enqueue_conv(plan, dy, plan->h.y_dtype, spectrum, plan->cls_pb_stride,
+                                      plan->doc_t, dx, plan->h.x_dtype, workspace, 1, "dx_", stream,
+                                      rec);
+    return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
+}
+
+size_t rubiconv_dk_workspace_bytes(rubiconv_plan_t plan) { return plan ? plan->dk_ws_bytes : 0; }
+
+rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, const void* dy,
+                                          float* dk, void* workspace, hipStream_t stream) {
+    if (!plan || !x || !dy || !dk || !workspace) return RUBICONV_ERR_ARG;
+    if (!aligned(workspace)) return RUBICONV_ERR_ARG;
+    const HostPlan& h = plan->h;
+    const size_t xsz = h.x_dtype == RUBICONV_F32 ? 4 : 2;
+    const size_t ysz = h.y_dtype == RUBICONV_F32 ? 4 : 2;
+    if (reinterpret_cast<uintptr_t>(x) % xsz || reinterpret_cast<uintptr_t>(dy) % ysz ||
+        reinterpret_cast<uintptr_t>(dk) % 4)
+        return RUBICONV_ERR_ARG;
+    // the x grid doubles as the "filter" grid: its offsets must fit the 32-bit field
+    if (h.grid_points > INT32_MAX) return RUBICONV_ERR_UNSUPPORTED;
+    if (!plan->device_ready) return RUBICONV_ERR_HIP;
+    std::lock_guard<std::mutex> lock(plan->launch_mu);
+    StageRecorder rec(plan, stream);
+    char* ws = static_cast<char*>(workspace);
+    void* xgrid = ws + plan->grid_bytes;
+    float* r = reinterpret_cast<float*>(ws + 2 * plan->grid_bytes);
+    const int n_cols = static_cast<int>(h.doc_col_seg.size());
+    const int64_t rs = static_cast<int64_t>(h.N) * h.D;
+    // x's column DFTs into the second grid, then dy's passes against it with the
+    // correlation product: document i's cross-correlation of dy with x lands at its
+    // own token positions (lag = offset in the document) of r
+    hipError_t e = h.col_mfma && h.x_dtype == RUBICONV_BF16
+                       ? rubiconv::launch_col_fwd_mfma(h.x_dtype, x, rs, h.D, xgrid,
                                                        plan->grid_pb_stride, plan->doc_t,
                                                        plan->mfma_tab, n_cols, h.npb, stream)
-                       : rubiconv::launch_col_fwd(h.r, half, h.x_dtype, x, rs, h.D, workspace,
+                       : rubiconv::launch_col_fwd(h.r, h.grid_half, h.x_dtype, x, rs, h.D, xgrid,
                                                   plan->grid_pb_stride, plan->doc_t, n_cols, h.npb,
                                                   stream);
-    rec.mark("col_fwd");
-    // row pass: the generic kernel (long rows) and one launch per listed size
-    // class, spread over the side streams (largest work first, least-loaded stream)
-    struct Launch {
-        int cls;       // -1: generic kernel; >= 0: register-resident kernel of that class
-        int nb;        // > 0: matrix-core kernel for the documents of that block count
-        double work;
-    };
-    std::vector<Launch> launches;
-    if (!h.doc_task_seg.empty()) launches.push_back({-1, 0, 1e30});
-    for (size_t c = 0; c < h.classes.size(); ++c) {
-        const int m = h.classes[c].m;
-        if (m > rubiconv::kMaxFastM || (h.row_dense && m <= 16 * rubiconv::kMaxDenseBlocks)) continue;
-        launches.push_back({static_cast<int>(c), 0, static_cast<double>(m) * h.classes[c].nlist});
-    }
-    if (h.row_dense)
-        for (int nb = 1; nb <= rubiconv::kMaxDenseBlocks; ++nb) {
-            if (h.dense_count[nb] == 0) continue;
-            double w = 0;
-            for (int k = 0; k < h.dense_count[nb]; ++k) w += h.docs[h.dense_docs[h.dense_list0[nb] + k]].m;
-            launches.push_back({-1, nb, w});
-        }
-    std::sort(launches.begin(), launches.end(),
-              [](const Launch& a, const Launch& b) { return a.work > b.work; });
-    const int nside = std::min<int>(rubiconv_plan_s::kSideStreams, static_cast<int>(launches.size()));
-    auto launch_one = [&](const Launch& L, hipStream_t s) -> hipError_t {
-        if (L.nb > 0)
-            return rubiconv::launch_row_dense(L.nb, workspace, plan->grid_pb_stride, spectrum,
-                                              plan->cls_pb_stride, plan->doc_t.segs,
-                                              plan->dense_docs + h.dense_list0[L.nb],
-                                              h.dense_count[L.nb], plan->dense_tab, h.n1, h.npb, s);
-        if (L.cls < 0)
-            return rubiconv::launch_row_conv(h.n1, half, workspace, plan->grid_pb_stride, spectrum,
-                                             plan->cls_pb_stride, plan->doc_t,
-                                             static_cast<int>(h.doc_task_seg.size()), h.npb,
-                                             h.row_lds_docs, s);
-        const Seg& cs = h.classes[L.cls];
-        return rubiconv::launch_row_fast(cs.m, half, workspace, plan->grid_pb_stride, spectrum,
-                                         plan->cls_pb_stride, plan->doc_t.segs,
-                                         plan->doc_t.list + cs.list0, cs.nlist, plan->doc_t.tw,
-                                         h.n1, h.npb, s);
-    };
-    if (nside <= 1) {
-        for (const Launch& L : launches)
-            if (e == hipSuccess) e = launch_one(L, stream);
-    } else if (e == hipSuccess) {
-        e = hipEventRecord(plan->fork, stream);
-        for (int k = 0; k < nside && e == hipSuccess; ++k) e = hipStreamWaitEvent(plan->side[k], plan->fork, 0);
-        std::vector<double> load(nside, 0.0);
-        for (const Launch& L : launches) {
-            if (e != hipSuccess) break;
-            const int k = static_cast<int>(std::min_element(load.begin(), load.end()) - load.begin());
-            load[k] += L.work;
-            e = launch_one(L, plan->side[k]);
-        }
-        for (int k = 0; k < nside && e == hipSuccess; ++k) {
-            e = hipEventRecord(plan->join[k], plan->side[k]);
-            if (e == hipSuccess) e = hipStreamWaitEvent(stream, plan->join[k], 0);
-        }
-    }
-    rec.mark("row_conv");
+    rec.mark("dk_col_fwd_x");
     if (e == hipSuccess)
-        e = h.col_mfma ? rubiconv::launch_col_inv_mfma(h.y_dtype, workspace, plan->grid_pb_stride, y,
-                                                       rs, h.D, plan->doc_t, plan->mfma_tab, n_cols,
-                                                       h.npb, stream)
-                       : rubiconv::launch_col_inv(h.r, half, h.y_dtype, workspace,
-                                                  plan->grid_pb_stride, y, rs, h.D, plan->doc_t,
-                                                  n_cols, h.npb, stream);
-    rec.mark("col_inv");
+        e = enqueue_conv(plan, dy, h.y_dtype, xgrid, plan->grid_pb_stride, plan->grad_t, r,
+                         RUBICONV_F32, workspace, 1, "dk_", stream, rec);
+    if (e == hipSuccess)
+        e = rubiconv::launch_lag_sum(r, plan->doc_t.segs, static_cast<int>(h.docs.size()), h.N, h.D,
+                                     h.L, dk, stream);
+    rec.mark("dk_lag_sum");
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }
 

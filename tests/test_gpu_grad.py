@@ -1,0 +1,161 @@
+"""Gradients on the GPU (rubiconv_packed_conv_dx / _dk through the C ABI) against the
+oracle's gradients on the same seeded inputs (needs an MI355X).
+
+Bars as for the forward: relative L2 <= 1e-4 for fp32 workloads and <= 2e-2 for bf16
+inputs with fp32 accumulation; dx also per document, dk also per channel.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from tests.common import ORACLE_THREADS, TOL, assert_parity, rel_l2, to_device
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _dy(W, seed):
+    """Upstream gradient of y's dtype: values (float64) and the device tensor."""
+    import torch
+    vals, bits = wl.draw_x(np.random.default_rng(seed), W.B, W.N, W.D, W.y_dtype)
+    if W.y_dtype == "bf16":
+        t = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(vals, dtype=np.float32))
+    return vals.astype(np.float64), t
+
+
+def _run(W, device, seed, n1=0, want_dk=True):
+    import torch
+    import paper_2605_08451_amd as rc
+    x, k = to_device(W, device)
+    dyv, dy = _dy(W, seed)
+    dy = dy.to(device)
+    plan = rc.Plan(W.cu_seqlens, N=W.N, D=W.D, L=W.L, x_dtype=W.x_dtype, y_dtype=W.y_dtype, n1=n1)
+    ws = plan.new_workspace(device)
+    spec = rc.filter_spectrum(plan, k, workspace=ws)
+    dx = rc.packed_conv_dx(plan, dy, spec, workspace=ws)
+    dk = rc.packed_conv_dk(plan, x, dy) if want_dk else None
+    torch.cuda.synchronize(device)
+    dxv = dx.float().cpu().numpy().astype(np.float64)
+    dkv = dk.cpu().numpy().astype(np.float64) if want_dk else None
+    return dyv, dxv, dkv, plan
+
+
+def _check_dk(dk, ref, dtype, label):
+    """Relative L2 over all of dk, and per channel once a channel has 64 lags or more.
+    With fewer lags the per-channel figure is the error of a few entries of a
+    correlation computed through fp16 transforms, whose rounding scales with the
+    whole correlation (every lag of every document), not with the lags kept."""
+    tol = TOL[dtype]
+    g = rel_l2(dk, ref)
+    worst = 0.0
+    if ref.shape[1] >= 64:
+        worst = max(rel_l2(dk[d], ref[d]) for d in range(ref.shape[0]) if np.any(ref[d]))
+    assert g <= tol and worst <= tol, f"{label}: dk global {g:.2e}, worst channel {worst:.2e}"
+    return g, worst
+
+
+@pytest.mark.parametrize("i", [0, 1, 3])
+def test_gradients_config(device, i):
+    _say(f"[grad] config {i} ({wl.CONFIG_NAMES[i]})")
+    W = wl.make_config(i)
+    dyv, dx, dk, _ = _run(W, device, seed=100 + i)
+    g, d = assert_parity(dx, oracle.grad_x(W.filters, dyv, W.cu_seqlens, threads=ORACLE_THREADS),
+                         W.cu_seqlens, W.x_dtype, f"dx config {i}")
+    gk, wk = _check_dk(dk, oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L, threads=ORACLE_THREADS),
+                       W.x_dtype, f"config {i}")
+    _say(f"[grad] config {i}: dx {g:.2e} / {d:.2e}, dk {gk:.2e} / {wk:.2e}")
+
+
+@pytest.mark.parametrize("i", [2, 4])
+def test_gradients_full_size_sampled(device, i):
+    """The bench workloads at full size: sampled dx and dk entries against the defining
+    sums (first and last token of every document included)."""
+    W = wl.make_config(i)
+    dyv, dx, dk, _ = _run(W, device, seed=100 + i)
+    rng = np.random.default_rng(200 + i)
+    n = 3000
+    bsd = np.stack([rng.integers(0, W.B, n), rng.integers(0, W.N, n), rng.integers(0, W.D, n)], 1)
+    extra = [(b, s, rng.integers(W.D)) for b, row in enumerate(W.cu_seqlens)
+             for s0, s1 in zip(row[:-1], row[1:]) if s1 > s0 for s in (s0, s1 - 1)]
+    bsd = np.concatenate([bsd, np.array(extra, dtype=np.int64)])
+    ref = oracle.grad_x_at(W.filters, dyv, W.cu_seqlens, bsd, threads=ORACLE_THREADS)
+    got = dx[bsd[:, 0], bsd[:, 1], bsd[:, 2]]
+    assert rel_l2(got, ref) <= TOL[W.x_dtype], rel_l2(got, ref)
+    m = 400
+    dt = np.stack([rng.integers(0, W.D, m), rng.integers(0, W.L, m)], 1)
+    dt[: m // 4, 1] = rng.integers(0, 64, m // 4)   # the short lags every document has
+    refk = oracle.grad_k_at(W.x, dyv, W.cu_seqlens, W.L, dt, threads=ORACLE_THREADS)
+    gotk = dk[dt[:, 0], dt[:, 1]]
+    assert rel_l2(gotk, refk) <= TOL[W.x_dtype], rel_l2(gotk, refk)
+
+
+@pytest.mark.parametrize("n1", [256, 64])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_gradient_edges(device, n1, dtype):
+    """Documents of length 1, N1 - 1, N1, N1 + 1, whole rows; L shorter and longer than
+    them; an odd channel count."""
+    rng = np.random.default_rng(17)
+    N = 2048
+    rows = [[N],
+            [1] * 5 + [n1 - 1, n1, n1 + 1] + [N - 5 - 3 * n1],
+            wl.random_rows(rng, 1, N, 300, p_short=0.5)[0],
+            [N - 1, 1]]
+    for L in (1, 7, 300, N, 3 * N):
+        W = wl.make_case(rows, D=5, L=L, x_dtype=dtype, seed=L)
+        dyv, dx, dk, _ = _run(W, device, seed=L + 1, n1=n1)
+        assert_parity(dx, oracle.grad_x(W.filters, dyv, W.cu_seqlens), W.cu_seqlens, dtype,
+                      f"dx n1={n1} L={L}")
+        _check_dk(dk, oracle.grad_k(W.x, dyv, W.cu_seqlens, L), dtype, f"n1={n1} L={L}")
+
+
+@pytest.mark.parametrize("D", [32, 96])
+def test_gradients_matrix_core_rows(device, D):
+    """bf16 inputs with whole 32-channel blocks (matrix-core column passes) and row sizes
+    across the short-row and partner-row kernels."""
+    rows = [[20480, 12288], [17280, 12800, 2304, 384], [9216, 8192, 6400, 4096, 2048, 1920, 896]]
+    W = wl.make_case(rows, D=D, L=32768, x_dtype="bf16", seed=D)
+    dyv, dx, dk, plan = _run(W, device, seed=D + 1)
+    ms = sorted(set(int(m) for m in plan.doc_table()[:, 4]))
+    assert min(ms) <= 16 and max(ms) > 100, ms
+    assert_parity(dx, oracle.grad_x(W.filters, dyv, W.cu_seqlens, threads=ORACLE_THREADS),
+                  W.cu_seqlens, "bf16", f"dx D={D}")
+    _check_dk(dk, oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L, threads=ORACLE_THREADS), "bf16",
+              f"D={D}")
+
+
+def test_dx_leakage(device):
+    """An impulse of dy in one document leaves dx of every other document below 1e-6 of
+    its peak; impulses at the first and last token of a row."""
+    import torch
+    import paper_2605_08451_amd as rc
+    N, D, L = 4096, 4, 4096
+    rows = [[1000, 1, 2000, 1095], [4096]]
+    W = wl.make_case(rows, D=D, L=L, x_dtype="f32", seed=3)
+    x, k = to_device(W, device)
+    plan = rc.Plan(W.cu_seqlens, N=N, D=D, L=L, x_dtype="f32")
+    spec = rc.filter_spectrum(plan, k)
+    for b, s0, s1 in [(0, 1000, 1001), (0, 1001, 3001), (0, 3001, 4096), (0, 0, 1000)]:
+        for t in (s0, s1 - 1):
+            dy = torch.zeros((2, N, D), dtype=torch.float32, device=device)
+            dy[b, t] = 1.0
+            dx = rc.packed_conv_dx(plan, dy, spec).cpu().numpy()
+            peak = np.abs(dx[b, s0:s1]).max()
+            outside = np.abs(np.concatenate([dx[b, :s0].ravel(), dx[b, s1:].ravel(), dx[1].ravel()]))
+            assert peak > 0 and outside.max() <= 1e-6 * peak, (b, s0, s1, t)
+
+
+def test_gradients_deterministic(device):
+    W = wl.make_case(wl.random_rows(np.random.default_rng(4), 2, 5000, 3000), D=40, L=5000,
+                     x_dtype="bf16", seed=4)
+    a = _run(W, device, seed=9)
+    b = _run(W, device, seed=9)
+    np.testing.assert_array_equal(a[1], b[1])
+    np.testing.assert_array_equal(a[2], b[2])

@@ -124,6 +124,14 @@ def test_grad_k_at_matches_grad_k():
                                    atol=1e-12 * (1 + np.abs(dk).max()))
 
 
+def test_grad_x_at_matches_grad_x():
+    for c, rows, cu, x, k, dy in _cases(26, n=3):
+        dx = oracle.grad_x(k, dy, cu)
+        bsd = np.array([(b, s, d) for b in range(dx.shape[0]) for s in range(dx.shape[1])
+                        for d in range(dx.shape[2])])
+        np.testing.assert_array_equal(oracle.grad_x_at(k, dy, cu, bsd), dx.reshape(-1))
+
+
 @pytest.mark.parametrize("bad", [np.array([[0, 3, 2]]), np.array([[1, 4]])])
 def test_gradients_reject_bad_seqlens(bad):
     x = np.zeros((1, 4, 1))
