@@ -40,10 +40,90 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true",
                     help="launch every step from Python instead of replaying a captured HIP graph")
+    ap.add_argument("--no-backward", action="store_true",
+                    help="skip the gradient measurement (dx and dk steps after the forward)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the run, copy a buffer of this many MiB three times (a plain copy "
                          "kernel of known size, the scale for the hardware byte counters)")
     return ap.parse_args()
+
+
+def time_step(launch, stream, steps, warmup, eager):
+    """Milliseconds per call of launch(stream): a captured HIP graph replayed steps times
+    (or eager launches), bracketed by events on the timing stream."""
+    import torch
+    dev = stream.device
+    graph = None
+    if not eager:
+        launch(stream)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            launch(torch.cuda.current_stream(dev))
+        torch.cuda.synchronize()
+
+    def step():
+        if graph is not None:
+            graph.replay()
+        else:
+            launch(stream)
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def backward_measurement(rc, plan, W, x, k, spec, ws, stream, args):
+    """The two gradient calls on the same batch: dx (rubiconv_packed_conv_dx) and dk
+    (rubiconv_packed_conv_dk) for a seeded upstream gradient of y's shape and dtype, each
+    timed as its own step, with per-kernel event times of the same calls."""
+    import torch
+    import workloads as wl
+    dev = x.device
+    vals, bits = wl.draw_x(np.random.default_rng(1000 + args.config), W.B, W.N, W.D, W.y_dtype)
+    if W.y_dtype == "bf16":
+        dy = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(dev)
+    else:
+        dy = torch.from_numpy(np.ascontiguousarray(vals, dtype=np.float32)).to(dev)
+    dx = torch.empty(x.shape, dtype=x.dtype, device=dev)
+    dk = torch.empty((W.D, W.L), dtype=torch.float32, device=dev)
+    dk_ws = plan.new_dk_workspace(dev)
+
+    def launch_dx(s):
+        rc.packed_conv_dx(plan, dy, spec, dx=dx, workspace=ws, stream=s)
+
+    def launch_dk(s):
+        rc.packed_conv_dk(plan, x, dy, dk=dk, workspace=dk_ws, stream=s)
+    dx_ms = time_step(launch_dx, stream, args.steps, args.warmup, args.eager)
+    dk_ms = time_step(launch_dk, stream, args.steps, args.warmup, args.eager)
+    plan.profile_start(2 * args.steps)
+    for _ in range(args.steps):
+        launch_dx(stream)
+        launch_dk(stream)
+    kt = plan.profile_read()
+    plan.profile_start(0)
+    tok_ch = W.B * W.N * W.D
+    sx = 2 if W.x_dtype == "bf16" else 4
+    sy = 2 if W.y_dtype == "bf16" else 4
+    # compulsory bytes: dx reads dy and the filter spectrum (D L 8, as for the forward)
+    # and writes dx; dk reads x and dy and writes dk (D L 4)
+    dx_min = tok_ch * (sx + sy) + W.D * W.L * 8
+    dk_min = tok_ch * (sx + sy) + W.D * W.L * 4
+    out = {"dx_ms": round(dx_ms, 4), "dk_ms": round(dk_ms, 4),
+           "dx_value": round(tok_ch / (dx_ms * 1e-3) / 1e6, 1),
+           "dk_value": round(tok_ch / (dk_ms * 1e-3) / 1e6, 1),
+           "unit": "Mtokens*channels/s",
+           "dx_hbm_roofline_frac_step": round(dx_min / (dx_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+           "dk_hbm_roofline_frac_step": round(dk_min / (dk_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+           "stages_us": {n: round(1e3 * tot / args.steps, 1) for n, (c, tot) in kt.items()}}
+    del dk_ws, dx, dk, dy
+    return out
 
 
 def kernel_bytes(info, W, plan):
@@ -240,6 +320,8 @@ def main():
         "execution": "eager launches" if graph is None else "HIP graph replay of one captured step",
         "wall_s_timed": round(wall, 4),
     }
+    if not args.no_backward:
+        out["backward"] = backward_measurement(rc, plan, W, x, k, spec, ws, stream, args)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(W, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -451,36 +451,58 @@ __global__ __launch_bounds__(256) void transpose_pairs_kernel(const float* __res
 // Filter gradient, last step: every document's cross-correlation r_i[tau] of dy
 // with x (lags 0 <= tau < min(len_i, L), written by the inverse passes at the
 // document's token positions s_i + tau of a [B][N][D] fp32 buffer) summed over the
-// documents into dk[D][L], documents in table order.  A workgroup owns 64 lags x 64
-// channels: lanes run along channels for the reads and along lags for the writes
-// (through LDS).
+// documents into dk[D][L], documents in table order.  A workgroup owns 32 lags x
+// 64 VEC channels: lanes run along channels for the reads (VEC channels per lane,
+// 8 lags per wave) and along lags for the writes, through LDS.  The loads of four
+// documents are issued together, so each wave waits once per four documents.
+template <int VEC>
 __global__ __launch_bounds__(256) void lag_sum_kernel(const float* __restrict__ r,
                                                       const Seg* __restrict__ segs, int n_docs,
                                                       int N, int D, int L, float* __restrict__ dk) {
-    __shared__ float tile[64][65];
-    const int tau0 = blockIdx.x * 64, d0 = blockIdx.y * 64;
-    const int dl = threadIdx.x & 63, tq = threadIdx.x >> 6;  // channel lane, lag quarter
-    const int d = d0 + dl;
-    float acc[16];
+    typedef float fv __attribute__((ext_vector_type(VEC)));
+    constexpr int C = 64 * VEC;                 // channels per workgroup
+    constexpr int T = 8;                        // lags per wave
+    constexpr int U = 4;                        // documents per round of loads
+    __shared__ float tile[4 * T][C + 1];
+    const int tau0 = blockIdx.x * (4 * T), d0 = blockIdx.y * C;
+    const int lane = threadIdx.x & 63, tq = threadIdx.x >> 6;  // channel group, lag group
+    const int d = d0 + VEC * lane;
+    const int t0 = tau0 + tq * T;
+    fv acc[T];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
-    for (int k = 0; k < n_docs; ++k) {
-        const Seg sg = segs[k];
-        const int lags = sg.len < L ? sg.len : L;
-        if (lags <= tau0 || d >= D) continue;
-        const float* base = r + (static_cast<int64_t>(sg.row) * N + sg.start) * D + d;
+    for (int i = 0; i < T; ++i) acc[i] = fv(0.0f);
+    if (d < D) {
+        for (int k = 0; k < n_docs; k += U) {
+            fv v[U][T];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int tau = tau0 + tq * 16 + i;
-            if (tau < lags) acc[i] += base[static_cast<int64_t>(tau) * D];
+            for (int u = 0; u < U; ++u) {
+                int lags = 0;
+                const float* base = r;
+                if (k + u < n_docs) {
+                    const Seg& sg = segs[k + u];
+                    lags = sg.len < L ? sg.len : L;
+                    base = r + (static_cast<int64_t>(sg.row) * N + sg.start) * D + d;
+                }
+#pragma unroll
+                for (int i = 0; i < T; ++i)
+                    v[u][i] = t0 + i < lags
+                                  ? *reinterpret_cast<const fv*>(base + static_cast<int64_t>(t0 + i) * D)
+                                  : fv(0.0f);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int i = 0; i < T; ++i) acc[i] += v[u][i];
         }
     }
 #pragma unroll
-    for (int i = 0; i < 16; ++i) tile[tq * 16 + i][dl] = acc[i];
+    for (int i = 0; i < T; ++i)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) tile[tq * T + i][VEC * lane + e] = acc[i][e];
     __syncthreads();
-    // write: lane along lags
-    const int tl = threadIdx.x & 63, dq = threadIdx.x >> 6;
-    for (int j = dq; j < 64; j += 4) {
+    // write: 32 lanes along lags, two channels per instruction
+    const int tl = threadIdx.x & 31, jq = threadIdx.x >> 5;
+    for (int j = jq; j < C; j += 8) {
         const int dd = d0 + j, tau = tau0 + tl;
         if (dd < D && tau < L) dk[static_cast<int64_t>(dd) * L + tau] = tile[tl][j];
     }
@@ -598,8 +620,13 @@ hipError_t launch_row_conv(int n1, bool half, void* grid, int64_t grid_pb_stride
 hipError_t launch_lag_sum(const float* r, const Seg* segs, int n_docs, int N, int D, int L,
                           float* dk, hipStream_t stream) {
     if (D <= 0 || L <= 0) return hipSuccess;
-    const dim3 g((L + 63) / 64, (D + 63) / 64), b(256);
-    hipLaunchKernelGGL(lag_sum_kernel, g, b, 0, stream, r, segs, n_docs, N, D, L, dk);
+    if (D % 4 == 0) {  // whole float4 groups: 16-byte loads (r is 256-byte aligned)
+        const dim3 g((L + 31) / 32, (D + 255) / 256), b(256);
+        hipLaunchKernelGGL(lag_sum_kernel<4>, g, b, 0, stream, r, segs, n_docs, N, D, L, dk);
+    } else {
+        const dim3 g((L + 31) / 32, (D + 63) / 64), b(256);
+        hipLaunchKernelGGL(lag_sum_kernel<1>, g, b, 0, stream, r, segs, n_docs, N, D, L, dk);
+    }
     return hipGetLastError();
 }
 
