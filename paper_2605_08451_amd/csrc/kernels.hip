@@ -508,6 +508,53 @@ __global__ __launch_bounds__(256) void lag_sum_kernel(const float* __restrict__ 
     }
 }
 
+// The same transpose for tap rows whose stride is a multiple of 4 floats (taps <= stride):
+// tiles of 128 channels x 64 taps, 16-byte loads along taps (256-byte runs per channel)
+// and 16-byte stores of four pairs along channels (256-byte runs per tap).
+__global__ __launch_bounds__(256) void transpose_pairs4_kernel(const float* __restrict__ in, int D,
+                                                               int taps, int in_ld,
+                                                               uint32_t* __restrict__ out) {
+    __shared__ float tile[128][65];
+    const int t0 = blockIdx.x * 64, c0 = blockIdx.y * 128;
+    const int tid = threadIdx.x;
+    {
+        const int tx = tid & 15, cy = tid >> 4;  // 4 taps per thread, 16 channel rows per pass
+        const int t = t0 + 4 * tx;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int c = c0 + cy + 16 * k;
+            float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            if (c < D && t < taps) {  // t + 3 < in_ld: in_ld is a multiple of 4, taps <= in_ld
+                v = *reinterpret_cast<const float4*>(in + static_cast<int64_t>(c) * in_ld + t);
+            }
+            float* row = &tile[cy + 16 * k][4 * tx];
+            row[0] = v.x; row[1] = v.y; row[2] = v.z; row[3] = v.w;
+        }
+    }
+    __syncthreads();
+    const int half_d = D / 2;
+    const int qx = tid & 15, ty = tid >> 4;  // 4 pairs per thread, 16 tap rows per pass
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int tt = ty + 16 * k, t = t0 + tt;
+        const int q0 = c0 / 2 + 4 * qx;
+        if (t < taps && q0 < half_d) {
+            uint32_t w[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int cl = 8 * qx + 2 * e;
+                w[e] = __builtin_bit_cast(uint32_t, __float22half2_rn(make_float2(tile[cl][tt], tile[cl + 1][tt])));
+            }
+            uint32_t* dst = out + static_cast<int64_t>(t) * half_d + q0;
+            if (q0 + 4 <= half_d) {
+                *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+            } else {
+                for (int e = 0; e < 4 && q0 + e < half_d; ++e) dst[e] = w[e];
+            }
+        }
+    }
+}
+
 // ---------------------------------------------------------------- launchers
 static int col_mode(int D) { return D % 32 == 0 ? kFull : (D % 2 == 0 ? kEven : kOdd); }
 
@@ -633,6 +680,14 @@ hipError_t launch_lag_sum(const float* r, const Seg* segs, int n_docs, int N, in
 hipError_t launch_transpose_pairs(const float* in, int D, int taps, int in_ld, void* out,
                                   hipStream_t stream) {
     if (D <= 0 || taps <= 0) return hipSuccess;
+    // 16-byte paths: whole float4 groups of taps (aligned rows) and of pairs (D / 2)
+    if (taps <= in_ld && in_ld % 4 == 0 && (D / 2) % 4 == 0 &&
+        reinterpret_cast<uintptr_t>(in) % 16 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0) {
+        const dim3 g((taps + 63) / 64, (D + 127) / 128);
+        hipLaunchKernelGGL(transpose_pairs4_kernel, g, dim3(256), 0, stream, in, D, taps, in_ld,
+                           static_cast<uint32_t*>(out));
+        return hipGetLastError();
+    }
     const dim3 g((taps + 31) / 32, (D + 63) / 64);
     hipLaunchKernelGGL(transpose_pairs_kernel, g, dim3(256), 0, stream, in, D, taps, in_ld,
                        static_cast<uint32_t*>(out));
