@@ -83,12 +83,20 @@ typedef enum {
  *   n1              column size N1 of the grid (the paper's k): 0 picks the
  *                   default (256); otherwise 64 or 256.
  *
+ * Documents of at most 64 tokens take the direct path when together they would
+ * fill at least 1/16 of the transform grid: they skip the transforms, and their
+ * outputs are the defining sums of the block-diagonal Toeplitz form (Section 3.2)
+ * evaluated directly, which avoids padding a short document to a whole N1-point
+ * column grid.  The environment variable RUBICONV_DIRECT_MAX = 0..128, read when
+ * the plan is made, sets the length limit and drops the share condition (0 turns
+ * the path off).
  * The plan copies what it needs; cu_seqlens_host may be freed on return.  Plan
  * creation allocates device memory and copies the document and twiddle tables
  * synchronously (it is not a stream-ordered call).
- * Errors: RUBICONV_ERR_ARG, RUBICONV_ERR_SEQLENS, RUBICONV_ERR_UNSUPPORTED
- * (n1 not supported, or a document so long that its row DFT would exceed the
- * largest supported size), RUBICONV_ERR_ALLOC, RUBICONV_ERR_HIP.
+ * Errors: RUBICONV_ERR_ARG (also for a malformed RUBICONV_DIRECT_MAX),
+ * RUBICONV_ERR_SEQLENS, RUBICONV_ERR_UNSUPPORTED (n1 not supported, or a document
+ * so long that its row DFT would exceed the largest supported size),
+ * RUBICONV_ERR_ALLOC, RUBICONV_ERR_HIP.
  */
 rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L, int max_docs,
                                 const int32_t* cu_seqlens_host, rubiconv_dtype_t x_dtype,
@@ -188,7 +196,8 @@ size_t rubiconv_dk_workspace_bytes(rubiconv_plan_t plan);
  *   workspace  device buffer of rubiconv_dk_workspace_bytes(plan), 256-byte
  *              aligned; dk must not overlap it.
  *   stream     HIP stream the work is enqueued on.
- * The sum over documents runs in document order, so results are deterministic.
+ * The sum over documents runs in a fixed order (longest document first, ties in
+ * table order), so results are deterministic.
  * Errors: RUBICONV_ERR_ARG, RUBICONV_ERR_UNSUPPORTED (a plan of 2^31 grid points
  * or more), RUBICONV_ERR_HIP.
  */
@@ -205,6 +214,8 @@ typedef struct {
     int64_t grid_points;    /* sum over documents of P_i */
     int64_t class_points;   /* sum over classes of P */
     int64_t tokens;         /* sum over documents of L_i (= B * N) */
+    int direct_max;         /* documents of at most this many tokens take the direct path */
+    int n_direct;           /* documents on the direct path */
 } rubiconv_plan_info_t;
 
 rubiconv_status_t rubiconv_plan_info(rubiconv_plan_t plan, rubiconv_plan_info_t* info);
@@ -213,7 +224,8 @@ rubiconv_status_t rubiconv_plan_info(rubiconv_plan_t plan, rubiconv_plan_info_t*
  * The plan's document table, in row order: out is host int32 [cap][6] receiving
  * (row, index of the document in its row, start, length, m_i, P_i) for each
  * non-empty document; *n_docs receives the count (rows beyond cap are not
- * written).  Used by tests to check the segment indexing exactly.
+ * written).  m_i = P_i = 0 marks a document of the direct path.  Used by tests to
+ * check the segment indexing exactly.
  */
 rubiconv_status_t rubiconv_plan_doc_table(rubiconv_plan_t plan, int32_t* out, int cap,
                                           int* n_docs);

@@ -51,7 +51,8 @@ class _PlanInfo(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int), ("N", ctypes.c_int), ("D", ctypes.c_int), ("L", ctypes.c_int),
                 ("n1", ctypes.c_int), ("n_docs", ctypes.c_int), ("n_classes", ctypes.c_int),
                 ("n_pair_blocks", ctypes.c_int), ("grid_points", ctypes.c_int64),
-                ("class_points", ctypes.c_int64), ("tokens", ctypes.c_int64)]
+                ("class_points", ctypes.c_int64), ("tokens", ctypes.c_int64),
+                ("direct_max", ctypes.c_int), ("n_direct", ctypes.c_int)]
 
 
 class _KernelTime(ctypes.Structure):
@@ -174,7 +175,8 @@ class Plan:
         return {name: getattr(inf, name) for name, _ in _PlanInfo._fields_}
 
     def doc_table(self) -> np.ndarray:
-        """int32 [n_docs, 6]: row, index in row, start, length, m_i, P_i."""
+        """int32 [n_docs, 6]: row, index in row, start, length, m_i, P_i (m_i = P_i = 0 for a
+        document the direct path computes)."""
         n = ctypes.c_int(0)
         _check(self._lib.rubiconv_plan_doc_table(self.handle, None, 0, ctypes.byref(n)),
                "rubiconv_plan_doc_table")

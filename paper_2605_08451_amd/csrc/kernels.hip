@@ -448,31 +448,143 @@ __global__ __launch_bounds__(256) void transpose_pairs_kernel(const float* __res
     }
 }
 
+// Short documents (at most kMaxDirect tokens) by their defining sums, one workgroup
+// per document and 64 channels, lanes along channels (coalesced rows of x), four
+// output positions in flight.  taps: the first T filter taps transposed, [T][D]
+// fp32 (T >= every lag a direct document uses).  Modes:
+//   kDirectConv:  out[t]   = sum_{tau <= min(t, L-1)} k[tau] a[t - tau]   (y from x)
+//   kDirectCorr:  out[s]   = sum_{tau <= min(len-1-s, L-1)} k[tau] a[s + tau]   (dx from dy)
+//   kDirectXcorr: out[tau] = sum_{t = tau}^{len-1} a[t] b[t - tau], tau < min(len, L)
+//                 (the filter gradient's per-document correlation of dy with x, fp32)
+// All sums run in fp32 in ascending lag (or token) order.
+constexpr int kDirectConv = 0;
+constexpr int kDirectCorr = 1;
+constexpr int kDirectXcorr = 2;
+
+template <class T>
+__device__ __forceinline__ float load_elem(const T* p, int64_t i);
+template <>
+__device__ __forceinline__ float load_elem<float>(const float* p, int64_t i) { return p[i]; }
+template <>
+__device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p, int64_t i) {
+    return __uint_as_float(static_cast<uint32_t>(p[i]) << 16);
+}
+__device__ __forceinline__ void store_elem(float* p, int64_t i, float v) { p[i] = v; }
+__device__ __forceinline__ void store_elem(uint16_t* p, int64_t i, float v) {
+    p[i] = static_cast<uint16_t>(bf16_rne_bits(v));
+}
+
+template <int MODE, int MAXLEN, class TA, class TB, class TO>
+__global__ __launch_bounds__(256) void direct_kernel(const TA* __restrict__ a, const TB* __restrict__ b,
+                                                     const float* __restrict__ taps,
+                                                     const Seg* __restrict__ docs, int N, int D,
+                                                     int L, TO* __restrict__ out) {
+    // the document's 64 channels of a, and of the taps (conv, corr) or b (xcorr), in LDS
+    __shared__ float sa[MAXLEN][65];
+    __shared__ float sb[MAXLEN][65];
+    const Seg sg = docs[blockIdx.x];
+    const int len = sg.len;
+    const int c = threadIdx.x & 63, tq = threadIdx.x >> 6;
+    const int d = blockIdx.y * 64 + c;
+    const bool live = d < D;
+    const int64_t base = (static_cast<int64_t>(sg.row) * N + sg.start) * D + d;
+    const int nb = MODE == kDirectXcorr ? len : (len < L ? len : L);  // rows of sb in use
+    for (int t = tq; t < len; t += 4) sa[t][c] = live ? load_elem(a, base + static_cast<int64_t>(t) * D) : 0.0f;
+    for (int t = tq; t < nb; t += 4) {
+        if constexpr (MODE == kDirectXcorr)
+            sb[t][c] = live ? load_elem(b, base + static_cast<int64_t>(t) * D) : 0.0f;
+        else
+            sb[t][c] = live ? taps[static_cast<int64_t>(t) * D + d] : 0.0f;
+    }
+    __syncthreads();  // the only barrier: every thread reaches it
+    if (!live) return;
+    // four consecutive outputs per thread share each operand load: a window of four
+    // values of the sliding operand moves by one element per step of the sum.  Values
+    // outside [0, len) and taps at or past L read as zero, which keeps every sum exact.
+    auto at = [&](float (*m)[65], int i, int lim) { return (i >= 0 && i < lim) ? m[i][c] : 0.0f; };
+    for (int t0 = 4 * tq; t0 < len; t0 += 16) {
+        float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        if constexpr (MODE == kDirectConv) {
+            // out[t0 + i] = sum_tau k[tau] a[t0 + i - tau], tau <= t0 + i, tau < L
+            const int kl = len < L ? len : L;
+            float w[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) w[i] = at(sa, t0 + i, len);  // a[t0 + i - tau], tau = 0
+            const int last = t0 + 3 < kl - 1 ? t0 + 3 : kl - 1;
+            for (int tau = 0; tau <= last; ++tau) {
+                const float kv = sb[tau][c];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[i] += kv * w[i];
+                w[3] = w[2]; w[2] = w[1]; w[1] = w[0];
+                w[0] = at(sa, t0 - tau - 1, len);
+            }
+        } else if constexpr (MODE == kDirectCorr) {
+            // out[t0 + i] = sum_tau k[tau] a[t0 + i + tau], t0 + i + tau < len, tau < L
+            const int kl = len < L ? len : L;
+            float w[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) w[i] = at(sa, t0 + i, len);
+            const int last = len - 1 - t0 < kl - 1 ? len - 1 - t0 : kl - 1;
+            for (int tau = 0; tau <= last; ++tau) {
+                const float kv = sb[tau][c];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[i] += kv * w[i];
+                w[0] = w[1]; w[1] = w[2]; w[2] = w[3];
+                w[3] = at(sa, t0 + tau + 4, len);
+            }
+        } else {
+            // out[t0 + i] = sum_{s >= t0 + i} a[s] b[s - t0 - i], lags t0 + i < min(len, L)
+            float w[4];  // b[s - t0 - i] for the current s
+#pragma unroll
+            for (int i = 0; i < 4; ++i) w[i] = at(sb, -i, len);  // s = t0
+            for (int s = t0; s < len; ++s) {
+                const float av = sa[s][c];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[i] += av * w[i];
+                w[3] = w[2]; w[2] = w[1]; w[1] = w[0];
+                w[0] = at(sb, s + 1 - t0, len);
+            }
+        }
+        const int lim = MODE == kDirectXcorr ? (len < L ? len : L) : len;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (t0 + i < lim) store_elem(out, base + static_cast<int64_t>(t0 + i) * D, acc[i]);
+    }
+}
+
 // Filter gradient, last step: every document's cross-correlation r_i[tau] of dy
 // with x (lags 0 <= tau < min(len_i, L), written by the inverse passes at the
-// document's token positions s_i + tau of a [B][N][D] fp32 buffer) summed over the
-// documents into dk[D][L], documents in table order.  A workgroup owns 32 lags x
-// 64 VEC channels: lanes run along channels for the reads (VEC channels per lane,
-// 8 lags per wave) and along lags for the writes, through LDS.  The loads of four
-// documents are issued together, so each wave waits once per four documents.
+// document's token positions s_i + tau of a [B][N][D] fp32 buffer; the direct path
+// writes its documents' correlations there too) summed over the documents into
+// dk[D][L].  A workgroup owns 8 lags x 64 VEC channels; its four waves split the
+// documents (rounds of four documents, round k to wave k mod 4) and their partial
+// sums are added in wave order through LDS, so the order of every sum is fixed.
+// segs lists the documents longest first: a wave stops at the first round whose
+// longest document ends before the workgroup's lags.  Lanes run along channels for
+// the reads (VEC channels per lane) and along lags for the writes.
 template <int VEC>
 __global__ __launch_bounds__(256) void lag_sum_kernel(const float* __restrict__ r,
                                                       const Seg* __restrict__ segs, int n_docs,
                                                       int N, int D, int L, float* __restrict__ dk) {
     typedef float fv __attribute__((ext_vector_type(VEC)));
     constexpr int C = 64 * VEC;                 // channels per workgroup
-    constexpr int T = 8;                        // lags per wave
+    constexpr int T = 8;                        // lags per workgroup
     constexpr int U = 4;                        // documents per round of loads
-    __shared__ float tile[4 * T][C + 1];
-    const int tau0 = blockIdx.x * (4 * T), d0 = blockIdx.y * C;
-    const int lane = threadIdx.x & 63, tq = threadIdx.x >> 6;  // channel group, lag group
+    __shared__ float part[4][T][C + 1];
+    // workgroup b runs on XCD b mod 8: the four lag tiles of one 128-byte row segment
+    // of dk go to workgroups 8 apart on one XCD, whose L2 joins their 32-byte writes
+    const int b = blockIdx.x;
+    const int tile = 4 * (8 * (b >> 5) + (b & 7)) + ((b >> 3) & 3);
+    const int tau0 = tile * T, d0 = blockIdx.y * C;
+    if (tau0 >= L) return;  // grid padding; no barrier has been reached
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int d = d0 + VEC * lane;
-    const int t0 = tau0 + tq * T;
     fv acc[T];
 #pragma unroll
     for (int i = 0; i < T; ++i) acc[i] = fv(0.0f);
     if (d < D) {
-        for (int k = 0; k < n_docs; k += U) {
+        for (int k = U * w; k < n_docs; k += 4 * U) {
+            if ((segs[k].len < L ? segs[k].len : L) <= tau0) break;
             fv v[U][T];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
@@ -485,8 +597,8 @@ __global__ __launch_bounds__(256) void lag_sum_kernel(const float* __restrict__ 
                 }
 #pragma unroll
                 for (int i = 0; i < T; ++i)
-                    v[u][i] = t0 + i < lags
-                                  ? *reinterpret_cast<const fv*>(base + static_cast<int64_t>(t0 + i) * D)
+                    v[u][i] = tau0 + i < lags
+                                  ? *reinterpret_cast<const fv*>(base + static_cast<int64_t>(tau0 + i) * D)
                                   : fv(0.0f);
             }
 #pragma unroll
@@ -498,13 +610,15 @@ __global__ __launch_bounds__(256) void lag_sum_kernel(const float* __restrict__ 
 #pragma unroll
     for (int i = 0; i < T; ++i)
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) tile[tq * T + i][VEC * lane + e] = acc[i][e];
+        for (int e = 0; e < VEC; ++e) part[w][i][VEC * lane + e] = acc[i][e];
     __syncthreads();
-    // write: 32 lanes along lags, two channels per instruction
-    const int tl = threadIdx.x & 31, jq = threadIdx.x >> 5;
-    for (int j = jq; j < C; j += 8) {
+    // write: 8 lanes along lags, 32 channels per instruction; waves added in order
+    const int tl = threadIdx.x & (T - 1), jq = threadIdx.x >> 3;
+    for (int j = jq; j < C; j += 256 / T) {
         const int dd = d0 + j, tau = tau0 + tl;
-        if (dd < D && tau < L) dk[static_cast<int64_t>(dd) * L + tau] = tile[tl][j];
+        if (dd < D && tau < L)
+            dk[static_cast<int64_t>(dd) * L + tau] =
+                ((part[0][tl][j] + part[1][tl][j]) + part[2][tl][j]) + part[3][tl][j];
     }
 }
 
@@ -664,14 +778,72 @@ hipError_t launch_row_conv(int n1, bool half, void* grid, int64_t grid_pb_stride
     return hipGetLastError();
 }
 
+template <int MAXLEN>
+hipError_t launch_direct_len(int mode, int a_dtype, const void* a, int b_dtype, const void* b,
+                             const float* taps, const Seg* docs, int n_docs, int N, int D, int L,
+                             int out_dtype, void* out, hipStream_t stream) {
+    const dim3 g(n_docs, (D + 63) / 64), blk(256);
+    using U = uint16_t;
+    if (mode == kDirectXcorr) {  // out fp32; a = dy, b = x
+        if (a_dtype == 1 && b_dtype == 1)
+            hipLaunchKernelGGL((direct_kernel<kDirectXcorr, MAXLEN, U, U, float>), g, blk, 0, stream,
+                               static_cast<const U*>(a), static_cast<const U*>(b), taps, docs, N, D, L,
+                               static_cast<float*>(out));
+        else if (a_dtype == 1)
+            hipLaunchKernelGGL((direct_kernel<kDirectXcorr, MAXLEN, U, float, float>), g, blk, 0, stream,
+                               static_cast<const U*>(a), static_cast<const float*>(b), taps, docs, N,
+                               D, L, static_cast<float*>(out));
+        else if (b_dtype == 1)
+            hipLaunchKernelGGL((direct_kernel<kDirectXcorr, MAXLEN, float, U, float>), g, blk, 0, stream,
+                               static_cast<const float*>(a), static_cast<const U*>(b), taps, docs, N,
+                               D, L, static_cast<float*>(out));
+        else
+            hipLaunchKernelGGL((direct_kernel<kDirectXcorr, MAXLEN, float, float, float>), g, blk, 0,
+                               stream, static_cast<const float*>(a), static_cast<const float*>(b), taps,
+                               docs, N, D, L, static_cast<float*>(out));
+        return hipGetLastError();
+    }
+#define RUBICONV_DIRECT(M, TA, TO)                                                              \
+    hipLaunchKernelGGL((direct_kernel<M, MAXLEN, TA, float, TO>), g, blk, 0, stream,           \
+                       static_cast<const TA*>(a), static_cast<const float*>(nullptr), taps, docs, \
+                       N, D, L, static_cast<TO*>(out))
+    if (mode == kDirectConv) {
+        if (a_dtype == 1) {
+            if (out_dtype == 1) RUBICONV_DIRECT(kDirectConv, U, U); else RUBICONV_DIRECT(kDirectConv, U, float);
+        } else {
+            if (out_dtype == 1) RUBICONV_DIRECT(kDirectConv, float, U); else RUBICONV_DIRECT(kDirectConv, float, float);
+        }
+    } else {
+        if (a_dtype == 1) {
+            if (out_dtype == 1) RUBICONV_DIRECT(kDirectCorr, U, U); else RUBICONV_DIRECT(kDirectCorr, U, float);
+        } else {
+            if (out_dtype == 1) RUBICONV_DIRECT(kDirectCorr, float, U); else RUBICONV_DIRECT(kDirectCorr, float, float);
+        }
+    }
+#undef RUBICONV_DIRECT
+    return hipGetLastError();
+}
+
+hipError_t launch_direct(int mode, int max_len, int a_dtype, const void* a, int b_dtype,
+                         const void* b, const float* taps, const Seg* docs, int n_docs, int N, int D,
+                         int L, int out_dtype, void* out, hipStream_t stream) {
+    if (n_docs == 0) return hipSuccess;
+    if (max_len > kMaxDirect) return hipErrorInvalidValue;
+    // LDS sized for the longest document the plan sends here
+    return max_len <= 64 ? launch_direct_len<64>(mode, a_dtype, a, b_dtype, b, taps, docs, n_docs, N,
+                                                 D, L, out_dtype, out, stream)
+                         : launch_direct_len<kMaxDirect>(mode, a_dtype, a, b_dtype, b, taps, docs,
+                                                         n_docs, N, D, L, out_dtype, out, stream);
+}
+
 hipError_t launch_lag_sum(const float* r, const Seg* segs, int n_docs, int N, int D, int L,
                           float* dk, hipStream_t stream) {
     if (D <= 0 || L <= 0) return hipSuccess;
     if (D % 4 == 0) {  // whole float4 groups: 16-byte loads (r is 256-byte aligned)
-        const dim3 g((L + 31) / 32, (D + 255) / 256), b(256);
+        const dim3 g((L + 255) / 256 * 32, (D + 255) / 256), b(256);
         hipLaunchKernelGGL(lag_sum_kernel<4>, g, b, 0, stream, r, segs, n_docs, N, D, L, dk);
     } else {
-        const dim3 g((L + 31) / 32, (D + 63) / 64), b(256);
+        const dim3 g((L + 255) / 256 * 32, (D + 63) / 64), b(256);
         hipLaunchKernelGGL(lag_sum_kernel<1>, g, b, 0, stream, r, segs, n_docs, N, D, L, dk);
     }
     return hipGetLastError();

@@ -95,8 +95,18 @@ hipError_t launch_col_inv_mfma(int y_dtype, const void* grid, int64_t grid_pb_st
                                int64_t dst_row_stride, int D, const LaunchTables& t,
                                const void* mtab, int n_cols, int npb, hipStream_t stream);
 
+// Documents computed by their defining sums (the direct path; kernels.hip):
+// mode 0 out = y from a = x, mode 1 out = dx from a = dy, mode 2 out = the
+// per-document correlation of a = dy with b = x at lags tau < min(len, L), written at
+// the document's tokens (fp32).  Dtype codes: 0 fp32, 1 bf16.  taps: [T][D] fp32.
+// max_len: no document in docs is longer (at most kMaxDirect).
+hipError_t launch_direct(int mode, int max_len, int a_dtype, const void* a, int b_dtype,
+                         const void* b, const float* taps, const Seg* docs, int n_docs, int N, int D,
+                         int L, int out_dtype, void* out, hipStream_t stream);
+
 // dk[d][tau] = sum over documents k < n_docs with tau < min(len_k, L) of
 // r[row_k][start_k + tau][d] (r fp32 [B][N][D]); dk [D][L] fp32, fully written.
+// segs must list the documents by non-increasing length.
 hipError_t launch_lag_sum(const float* r, const Seg* segs, int n_docs, int N, int D, int L,
                           float* dk, hipStream_t stream);
 

@@ -18,6 +18,14 @@ constexpr int kMaxM = 2048;         // largest row DFT
 constexpr int kRowLdsBytes = 98304; // generic row kernel: three buffers of two rows each
 constexpr int kMaxDenseBlocks = 8;  // matrix-core row pass: m <= 16 * kMaxDenseBlocks
 
+// Longest document the direct path may take (its per-output sums stay short).
+constexpr int kMaxDirect = 128;
+// Default: documents of at most this many tokens take the direct path, when together
+// they would hold at least 1/kDirectMinShare of the transform grid (measured: a few
+// short documents among long ones cost more on their own launch than they save).
+constexpr int kDefaultDirect = 64;
+constexpr int kDirectMinShare = 16;
+
 struct Seg {
     int32_t row;       // source row of x (documents) / 0 (filter classes)
     int32_t start;     // first token in the row / 0

@@ -216,7 +216,8 @@ void build_partner_tables(int m, int n1, std::vector<uint32_t>* out) {
 }
 
 BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_docs,
-                           const int32_t* cu, int x_dtype, int y_dtype, int n1) {
+                           const int32_t* cu, int x_dtype, int y_dtype, int n1, int direct_max,
+                           bool direct_by_share) {
     if (!out || !cu || B < 1 || N < 1 || D < 1 || L < 1 || max_docs < 1) return BuildError::kArg;
     if (x_dtype < 0 || x_dtype > 1 || y_dtype < 0 || y_dtype > 1) return BuildError::kArg;
     if (n1 == 0) n1 = 256;
@@ -234,8 +235,28 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
             if (c[k + 1] < c[k] || c[k + 1] > N) return BuildError::kSeqlens;
     }
 
+    if (direct_max < 0 || direct_max > kMaxDirect) return BuildError::kArg;
+    if (direct_by_share && direct_max > 0) {
+        // the direct path pays once its documents would hold a real share of the
+        // transform grid (each at least one whole N1-point column grid); a handful of
+        // short documents among long ones stays on the transform path
+        int64_t all = 0, shortp = 0;
+        for (int b = 0; b < B; ++b) {
+            const int32_t* c = cu + static_cast<int64_t>(b) * (max_docs + 1);
+            for (int k = 0; k < max_docs; ++k) {
+                const int len = c[k + 1] - c[k];
+                if (len == 0) continue;
+                const int64_t mmin = (static_cast<int64_t>(len) + std::min(len, L) - 1 + n1 - 1) / n1;
+                const int64_t P = n1 * mmin;
+                all += P;
+                if (len <= direct_max) shortp += P;
+            }
+        }
+        if (shortp * kDirectMinShare < all) direct_max = 0;
+    }
     HostPlan p;
     p.B = B; p.N = N; p.D = D; p.L = L; p.max_docs = max_docs; p.n1 = n1; p.r = r;
+    p.direct_max = direct_max;
     p.x_dtype = x_dtype; p.y_dtype = y_dtype;
     p.grid_half = x_dtype == 1;  // bf16 inputs: complex fp16 grids and spectra
     p.npb = ((D + 1) / 2 + kPairsPerBlock - 1) / kPairsPerBlock;
@@ -247,6 +268,15 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
         for (int k = 0; k < max_docs; ++k) {
             int len = c[k + 1] - c[k];
             if (len == 0) continue;
+            if (len <= direct_max) {
+                Seg s{};
+                s.row = b; s.start = c[k]; s.len = len;
+                p.direct_docs.push_back(s);
+                p.direct_index.push_back(k);
+                p.all_docs.push_back(s);
+                p.all_index.push_back(k);
+                continue;
+            }
             int64_t need = static_cast<int64_t>(len) + std::min(len, L) - 1;
             int64_t mmin = (need + n1 - 1) / n1;
             if (mmin > kMaxM) return BuildError::kUnsupported;
@@ -260,10 +290,13 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
             s.row = b; s.start = c[k]; s.len = len; s.m = m; s.P = n1 * m;
             p.docs.push_back(s);
             p.doc_index.push_back(k);
+            p.all_docs.push_back(s);
+            p.all_index.push_back(k);
             class_of_m[m] = 0;
         }
     }
 
+    if (!p.direct_docs.empty()) p.direct_taps = std::min(L, direct_max);
     // size classes, ascending m: twiddles, spectrum offsets, filter taps
     for (auto& kv : class_of_m) {
         int m = kv.first;

@@ -17,6 +17,16 @@ struct HostPlan {
     int npb = 0;                        // channel-pair blocks of kPairsPerBlock pairs
     std::vector<Seg> docs;              // one per non-empty document, row order
     std::vector<int32_t> doc_index;     // index of each document inside its row
+    // Documents of at most direct_max tokens skip the transforms: their outputs are the
+    // defining sums, computed directly (direct_docs: row, start, len; m = P = 0).
+    int direct_max = 0;
+    int direct_taps = 0;                // taps the direct path reads: min(L, direct_max)
+    std::vector<Seg> direct_docs;
+    std::vector<int32_t> direct_index;  // index of each direct document inside its row
+    // every non-empty document in row order (transformed ones with their m and P,
+    // direct ones with m = P = 0): the plan's document table
+    std::vector<Seg> all_docs;
+    std::vector<int32_t> all_index;
     std::vector<Seg> classes;           // one per distinct m, ascending m
     std::vector<int32_t> doc_col_seg;   // global column -> document
     std::vector<int32_t> doc_task_seg;  // global row task -> document
@@ -55,7 +65,11 @@ void build_dense_tables(int m, int n1, std::vector<uint32_t>* out);
 void build_partner_tables(int m, int n1, std::vector<uint32_t>* out);
 
 // Validates cu_seqlens and fills every table of *out.
+// direct_max: documents of at most this many tokens take the direct path (0: none);
+// with direct_by_share they do so only when they would hold at least 1/kDirectMinShare
+// of the transform grid (plan.hpp).
 BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_docs,
-                           const int32_t* cu_seqlens, int x_dtype, int y_dtype, int n1);
+                           const int32_t* cu_seqlens, int x_dtype, int y_dtype, int n1,
+                           int direct_max, bool direct_by_share);
 
 }  // namespace rubiconv

@@ -9,6 +9,7 @@
 
 #include <algorithm>
 #include <climits>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -35,6 +36,9 @@ struct rubiconv_plan_s {
     LaunchTables doc_t{};
     LaunchTables cls_t{};
     LaunchTables grad_t{};       // doc_t with each document's "filter" rows at its own grid rows
+    const Seg* direct_segs = nullptr;  // documents of the direct path
+    const Seg* all_segs = nullptr;     // every document, longest first (the filter gradient's sum)
+    size_t dtaps_off = 0;        // spectrum: the direct path's taps [direct_taps][D] fp32
     int64_t grid_pb_stride = 0;  // grid elements per pair block, document grid
     int64_t cls_pb_stride = 0;   // same, filter class grids (the spectrum buffer)
     size_t taps_bytes = 0;       // transposed filter taps (workspace of the filter call)
@@ -48,6 +52,7 @@ struct rubiconv_plan_s {
     static constexpr int kSideStreams = 4;
     hipStream_t side[kSideStreams] = {};
     hipEvent_t fork = nullptr;
+    hipEvent_t direct_done = nullptr;  // the direct path's launch on its side stream
     hipEvent_t join[kSideStreams] = {};
     std::mutex launch_mu;
     // stage timing (rubiconv_profile_start / _read)
@@ -69,6 +74,8 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     size_t off = 0;
     const size_t o_segs = off;       off = align_up(off + n_segs * sizeof(Seg));
     const size_t o_gsegs = off;      off = align_up(off + h.docs.size() * sizeof(Seg));
+    const size_t o_dsegs = off;      off = align_up(off + h.direct_docs.size() * sizeof(Seg));
+    const size_t o_asegs = off;      off = align_up(off + h.all_docs.size() * sizeof(Seg));
     const size_t o_dcol = off;       off = align_up(off + h.doc_col_seg.size() * 4);
     const size_t o_dtask = off;      off = align_up(off + h.doc_task_seg.size() * 4);
     const size_t o_ccol = off;       off = align_up(off + h.cls_col_seg.size() * 4);
@@ -85,6 +92,14 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     std::vector<Seg> segs(h.docs);
     segs.insert(segs.end(), h.classes.begin(), h.classes.end());
     std::memcpy(img.data() + o_segs, segs.data(), n_segs * sizeof(Seg));
+    if (!h.direct_docs.empty())
+        std::memcpy(img.data() + o_dsegs, h.direct_docs.data(), h.direct_docs.size() * sizeof(Seg));
+    if (!h.all_docs.empty()) {  // longest first, ties in table order (the lag sum's order)
+        std::vector<Seg> by_len(h.all_docs);
+        std::stable_sort(by_len.begin(), by_len.end(),
+                         [](const Seg& a, const Seg& b) { return a.len > b.len; });
+        std::memcpy(img.data() + o_asegs, by_len.data(), by_len.size() * sizeof(Seg));
+    }
     {  // filter gradient: the second operand of a document's row stage is its own x grid
         std::vector<Seg> gsegs(h.docs);
         for (Seg& g : gsegs) g.spec_off = static_cast<int32_t>(g.grid_off);
@@ -125,6 +140,8 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     pl->doc_t = LaunchTables{dsegs, reinterpret_cast<const int32_t*>(base + o_dcol),
                              reinterpret_cast<const int32_t*>(base + o_dtask), tw, twn,
                              reinterpret_cast<const int32_t*>(base + o_cdoc)};
+    pl->direct_segs = reinterpret_cast<const Seg*>(base + o_dsegs);
+    pl->all_segs = reinterpret_cast<const Seg*>(base + o_asegs);
     pl->grad_t = pl->doc_t;
     pl->grad_t.segs = reinterpret_cast<const Seg*>(base + o_gsegs);
     pl->cls_t = LaunchTables{dsegs + h.docs.size(), reinterpret_cast<const int32_t*>(base + o_ccol),
@@ -133,7 +150,9 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     pl->mfma_tab = base + o_mt;
     pl->dense_tab = base + o_dt;
     pl->dense_docs = reinterpret_cast<const int32_t*>(base + o_dd);
-    if (hipEventCreateWithFlags(&pl->fork, hipEventDisableTiming) != hipSuccess) return RUBICONV_ERR_HIP;
+    if (hipEventCreateWithFlags(&pl->fork, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&pl->direct_done, hipEventDisableTiming) != hipSuccess)
+        return RUBICONV_ERR_HIP;
     for (int k = 0; k < rubiconv_plan_s::kSideStreams; ++k) {
         if (hipStreamCreateWithFlags(&pl->side[k], hipStreamNonBlocking) != hipSuccess ||
             hipEventCreateWithFlags(&pl->join[k], hipEventDisableTiming) != hipSuccess)
@@ -152,6 +171,8 @@ void destroy_side_streams(rubiconv_plan_s* pl) {
     }
     if (pl->fork) (void)hipEventDestroy(pl->fork);
     pl->fork = nullptr;
+    if (pl->direct_done) (void)hipEventDestroy(pl->direct_done);
+    pl->direct_done = nullptr;
 }
 
 void destroy_events(rubiconv_plan_s* pl) {
@@ -175,6 +196,7 @@ struct StageRecorder {
             (void)hipEventRecord(pl->prof_events[slot * rubiconv_plan_s::kEventsPerCall], stream);
         }
     }
+    bool active() const { return slot >= 0; }
     void mark(const std::string& name) {
         if (slot < 0 || k + 1 >= rubiconv_plan_s::kEventsPerCall) return;
         ++k;
@@ -182,6 +204,35 @@ struct StageRecorder {
         pl->prof_names[slot].push_back(name);
     }
 };
+
+// Starts the direct path's launch: on the last side stream, forked from `stream`, so
+// that it runs beside the transforms; the caller joins with join_direct before the
+// direct outputs are used or the call returns.  While stage timing records this call,
+// the launch stays on `stream` so that its events time it.
+template <class F>
+hipError_t fork_direct(rubiconv_plan_s* plan, hipStream_t stream, StageRecorder& rec,
+                       const char* name, F launch) {
+    if (rec.active()) {
+        const hipError_t e = launch(stream);
+        rec.mark(name);
+        return e;
+    }
+    hipStream_t side = plan->side[rubiconv_plan_s::kSideStreams - 1];
+    hipError_t e = hipEventRecord(plan->fork, stream);
+    if (e == hipSuccess) e = hipStreamWaitEvent(side, plan->fork, 0);
+    if (e == hipSuccess) e = launch(side);
+    if (e == hipSuccess) e = hipEventRecord(plan->direct_done, side);
+    return e;
+}
+
+hipError_t join_direct(rubiconv_plan_s* plan, hipStream_t stream, const StageRecorder& rec) {
+    return rec.active() ? hipSuccess : hipStreamWaitEvent(stream, plan->direct_done, 0);
+}
+
+// The direct path's taps inside a spectrum buffer.
+const float* direct_taps(const rubiconv_plan_s* plan, const void* spectrum) {
+    return reinterpret_cast<const float*>(static_cast<const char*>(spectrum) + plan->dtaps_off);
+}
 
 // Stage names in the profile: the forward's plain, the gradients' prefixed.
 std::string stage(const char* tag, const char* name) { return std::string(tag) + name; }
@@ -290,9 +341,22 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
     *out = nullptr;
     rubiconv_plan_s* pl = new (std::nothrow) rubiconv_plan_s();
     if (!pl) return RUBICONV_ERR_ALLOC;
+    // RUBICONV_DIRECT_MAX (0 .. kMaxDirect) overrides the direct path's length limit
+    int direct_max = rubiconv::kDefaultDirect;
+    bool direct_by_share = true;  // an explicit limit applies as given
+    if (const char* v = std::getenv("RUBICONV_DIRECT_MAX")) {
+        direct_by_share = false;
+        char* end = nullptr;
+        const long n = std::strtol(v, &end, 10);
+        if (end == v || *end != '\0' || n < 0 || n > rubiconv::kMaxDirect) {
+            delete pl;
+            return RUBICONV_ERR_ARG;
+        }
+        direct_max = static_cast<int>(n);
+    }
     BuildError be = rubiconv::build_host_plan(&pl->h, B, N, D, L, max_docs, cu_seqlens_host,
                                               static_cast<int>(x_dtype), static_cast<int>(y_dtype),
-                                              n1);
+                                              n1, direct_max, direct_by_share);
     if (be != BuildError::kOk) {
         delete pl;
         if (be == BuildError::kArg) return RUBICONV_ERR_ARG;
@@ -304,12 +368,18 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
     pl->cls_pb_stride = h.class_points * kPairsPerBlock;
     const size_t esz = h.grid_half ? 4 : 8;  // complex fp16 / complex fp32 grid element
     pl->spec_bytes = align_up(static_cast<size_t>(h.npb) * pl->cls_pb_stride * esz);
+    pl->dtaps_off = pl->spec_bytes;
+    pl->spec_bytes += align_up(static_cast<size_t>(h.direct_taps) * h.D * 4);
     pl->taps_bytes = align_up(static_cast<size_t>(h.taps_max) * h.D * 4);
     const size_t conv_ws = align_up(static_cast<size_t>(h.npb) * pl->grid_pb_stride * esz);
     const size_t filt_ws = pl->taps_bytes;
     pl->ws_bytes = std::max(conv_ws, filt_ws);
     pl->grid_bytes = conv_ws;
     pl->dk_ws_bytes = 2 * conv_ws + align_up(static_cast<size_t>(h.B) * h.N * h.D * 4);
+    // never empty: a plan whose documents all take the direct path still hands out
+    // buffers callers can allocate and pass
+    pl->ws_bytes = std::max(pl->ws_bytes, kAlign);
+    pl->spec_bytes = std::max(pl->spec_bytes, kAlign);
     rubiconv_status_t st = upload(pl);
     if (st != RUBICONV_OK) {
         destroy_side_streams(pl);
@@ -357,6 +427,12 @@ rubiconv_status_t rubiconv_filter_spectrum(rubiconv_plan_t plan, const float* fi
                                            plan->cls_pb_stride, plan->cls_t,
                                            static_cast<int>(h.cls_col_seg.size()), h.npb, stream);
     rec.mark("filter_col_fwd");
+    if (e == hipSuccess && h.direct_taps > 0) {  // the direct path's taps, [T][D] fp32
+        e = rubiconv::launch_transpose(filters, h.D, h.direct_taps, h.L,
+                                       reinterpret_cast<float*>(static_cast<char*>(spectrum) + plan->dtaps_off),
+                                       h.D, stream);
+        rec.mark("filter_direct_taps");
+    }
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }
 
@@ -371,8 +447,19 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
     if (!plan->device_ready) return RUBICONV_ERR_HIP;
     std::lock_guard<std::mutex> lock(plan->launch_mu);
     StageRecorder rec(plan, stream);
-    const hipError_t e = enqueue_conv(plan, x, plan->h.x_dtype, spectrum, plan->cls_pb_stride,
-                                      plan->doc_t, y, plan->h.y_dtype, workspace, 0, "", stream, rec);
+    const HostPlan& h = plan->h;
+    const bool direct = !h.direct_docs.empty();
+    hipError_t e = hipSuccess;
+    if (direct)
+        e = fork_direct(plan, stream, rec, "direct", [&](hipStream_t s) {
+            return rubiconv::launch_direct(0, h.direct_max, h.x_dtype, x, 0, nullptr, direct_taps(plan, spectrum),
+                                           plan->direct_segs, static_cast<int>(h.direct_docs.size()),
+                                           h.N, h.D, h.L, h.y_dtype, y, s);
+        });
+    if (e == hipSuccess)
+        e = enqueue_conv(plan, x, h.x_dtype, spectrum, plan->cls_pb_stride, plan->doc_t, y, h.y_dtype,
+                         workspace, 0, "", stream, rec);
+    if (e == hipSuccess && direct) e = join_direct(plan, stream, rec);
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }
 
@@ -389,9 +476,19 @@ rubiconv_status_t rubiconv_packed_conv_dx(rubiconv_plan_t plan, const void* dy, 
     StageRecorder rec(plan, stream);
     // dy has y's dtype and dx has x's: the correlation runs the convolution's passes
     // with the roles of the two dtypes exchanged
-    const hipError_t e = enqueue_conv(plan, dy, plan->h.y_dtype, spectrum, plan->cls_pb_stride,
-                                      plan->doc_t, dx, plan->h.x_dtype, workspace, 1, "dx_", stream,
-                                      rec);
+    const HostPlan& h = plan->h;
+    const bool direct = !h.direct_docs.empty();
+    hipError_t e = hipSuccess;
+    if (direct)
+        e = fork_direct(plan, stream, rec, "dx_direct", [&](hipStream_t s) {
+            return rubiconv::launch_direct(1, h.direct_max, h.y_dtype, dy, 0, nullptr, direct_taps(plan, spectrum),
+                                           plan->direct_segs, static_cast<int>(h.direct_docs.size()),
+                                           h.N, h.D, h.L, h.x_dtype, dx, s);
+        });
+    if (e == hipSuccess)
+        e = enqueue_conv(plan, dy, h.y_dtype, spectrum, plan->cls_pb_stride, plan->doc_t, dx,
+                         h.x_dtype, workspace, 1, "dx_", stream, rec);
+    if (e == hipSuccess && direct) e = join_direct(plan, stream, rec);
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }
 
@@ -417,10 +514,20 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
     float* r = reinterpret_cast<float*>(ws + 2 * plan->grid_bytes);
     const int n_cols = static_cast<int>(h.doc_col_seg.size());
     const int64_t rs = static_cast<int64_t>(h.N) * h.D;
+    // direct documents: their correlations straight into r, beside the transforms
+    const bool direct = !h.direct_docs.empty();
+    hipError_t e = hipSuccess;
+    if (direct)
+        e = fork_direct(plan, stream, rec, "dk_direct", [&](hipStream_t s) {
+            return rubiconv::launch_direct(2, h.direct_max, h.y_dtype, dy, h.x_dtype, x, nullptr, plan->direct_segs,
+                                           static_cast<int>(h.direct_docs.size()), h.N, h.D, h.L, 0,
+                                           r, s);
+        });
     // x's column DFTs into the second grid, then dy's passes against it with the
     // correlation product: document i's cross-correlation of dy with x lands at its
     // own token positions (lag = offset in the document) of r
-    hipError_t e = h.col_mfma && h.x_dtype == RUBICONV_BF16
+    if (e == hipSuccess)
+        e = h.col_mfma && h.x_dtype == RUBICONV_BF16
                        ? rubiconv::launch_col_fwd_mfma(h.x_dtype, x, rs, h.D, xgrid,
                                                        plan->grid_pb_stride, plan->doc_t,
                                                        plan->mfma_tab, n_cols, h.npb, stream)
@@ -431,8 +538,9 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
     if (e == hipSuccess)
         e = enqueue_conv(plan, dy, h.y_dtype, xgrid, plan->grid_pb_stride, plan->grad_t, r,
                          RUBICONV_F32, workspace, 1, "dk_", stream, rec);
+    if (e == hipSuccess && direct) e = join_direct(plan, stream, rec);
     if (e == hipSuccess)
-        e = rubiconv::launch_lag_sum(r, plan->doc_t.segs, static_cast<int>(h.docs.size()), h.N, h.D,
+        e = rubiconv::launch_lag_sum(r, plan->all_segs, static_cast<int>(h.all_docs.size()), h.N, h.D,
                                      h.L, dk, stream);
     rec.mark("dk_lag_sum");
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
@@ -443,14 +551,16 @@ rubiconv_status_t rubiconv_plan_info(rubiconv_plan_t plan, rubiconv_plan_info_t*
     const HostPlan& h = plan->h;
     info->B = h.B; info->N = h.N; info->D = h.D; info->L = h.L;
     info->n1 = h.n1;
-    info->n_docs = static_cast<int>(h.docs.size());
+    info->n_docs = static_cast<int>(h.all_docs.size());
     info->n_classes = static_cast<int>(h.classes.size());
     info->n_pair_blocks = h.npb;
     info->grid_points = h.grid_points;
     info->class_points = h.class_points;
     int64_t tok = 0;
-    for (const Seg& s : h.docs) tok += s.len;
+    for (const Seg& s : h.all_docs) tok += s.len;
     info->tokens = tok;
+    info->direct_max = h.direct_max;
+    info->n_direct = static_cast<int>(h.direct_docs.size());
     return RUBICONV_OK;
 }
 
@@ -458,12 +568,12 @@ rubiconv_status_t rubiconv_plan_doc_table(rubiconv_plan_t plan, int32_t* out, in
                                           int* n_docs) {
     if (!plan || !n_docs || cap < 0 || (cap > 0 && !out)) return RUBICONV_ERR_ARG;
     const HostPlan& h = plan->h;
-    const int n = static_cast<int>(h.docs.size());
+    const int n = static_cast<int>(h.all_docs.size());
     *n_docs = n;
     for (int i = 0; i < n && i < cap; ++i) {
-        const Seg& s = h.docs[i];
+        const Seg& s = h.all_docs[i];
         int32_t* o = out + 6 * static_cast<int64_t>(i);
-        o[0] = s.row; o[1] = h.doc_index[i]; o[2] = s.start; o[3] = s.len; o[4] = s.m; o[5] = s.P;
+        o[0] = s.row; o[1] = h.all_index[i]; o[2] = s.start; o[3] = s.len; o[4] = s.m; o[5] = s.P;
     }
     return RUBICONV_OK;
 }

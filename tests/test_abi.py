@@ -78,9 +78,15 @@ def test_doc_table_matches_oracle_segments(i, n1):
     np.testing.assert_array_equal(t[:, :4], ref[:, :4])   # row, index, start, length: exact
     m, P = t[:, 4].astype(np.int64), t[:, 5].astype(np.int64)
     np.testing.assert_array_equal(P, k * m)
-    assert np.all(P >= ref[:, 4]), "transform shorter than the causal padding rule allows"
+    # documents of at most DIRECT_MAX tokens take the direct path (m = P = 0), all others
+    # a transform
+    direct = P == 0
+    np.testing.assert_array_equal(direct, t[:, 3] <= plan.info()["direct_max"])
+    assert plan.info()["n_direct"] == int(direct.sum())
+    P, m, refP = P[~direct], m[~direct], ref[~direct, 4]
+    assert np.all(P >= refP), "transform shorter than the causal padding rule allows"
     listed = listed_row_sizes()
-    for mi, minimal in zip(m, ref[:, 4] // k):
+    for mi, minimal in zip(m, refP // k):
         assert _smooth(int(mi))
         if minimal <= listed[-1]:   # the smallest listed size that is large enough
             assert mi == min(s for s in listed if s >= minimal), (mi, minimal)

@@ -220,3 +220,30 @@ def test_long_row_sizes_precision(device, n1):
         assert max(ms) > 100 and sum(33 <= m <= 128 for m in ms) >= 5, ms
         g, d = assert_parity(y, reference(W, "fft"), W.cu_seqlens, "bf16", f"n1={n1} L={L}")
         assert d <= 5e-3, (n1, L, d)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_direct_path_limits(device, monkeypatch, dtype):
+    """Short documents by their defining sums (the direct path) at several length limits,
+    including rows made only of short documents and a limit above every document: the
+    forward and both gradients meet the oracle bar at each limit."""
+    import tests.test_gpu_grad as tg
+    rng = np.random.default_rng(31)
+    N = 1024
+    rows = [[1] * 8 + [64, 65, 63, 128, 129] + [N - 8 - 449],
+            [int(v) for v in rng.integers(1, 40, 40)],
+            [N]]
+    rows[1].append(N - sum(rows[1]))
+    W = wl.make_case(rows, D=40, L=700, x_dtype=dtype, seed=31)
+    ref = reference(W)
+    for limit in (0, 16, 64, 128):
+        monkeypatch.setenv("RUBICONV_DIRECT_MAX", str(limit))
+        y, plan = run_gpu(W, device)
+        info = plan.info()
+        assert info["direct_max"] == limit
+        assert info["n_direct"] == sum(1 for r in rows for n in r if 0 < n <= limit)
+        assert_parity(y, ref, W.cu_seqlens, dtype, f"limit {limit}")
+        dyv, dx, dk, _ = tg._run(W, device, seed=limit + 5)
+        assert_parity(dx, oracle.grad_x(W.filters, dyv, W.cu_seqlens), W.cu_seqlens, dtype,
+                      f"dx limit {limit}")
+        tg._check_dk(dk, oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L), dtype, f"limit {limit}")
