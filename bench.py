@@ -40,6 +40,11 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true",
                     help="launch every step from Python instead of replaying a captured HIP graph")
+    ap.add_argument("--layers", type=int, default=4,
+                    help="layers of the stacked measurement (one plan, one filter bank per layer)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the benchmark line: the forward step over channel counts D and "
+                         "filter lengths L on the same document structure, one JSON line each")
     ap.add_argument("--no-backward", action="store_true",
                     help="skip the gradient measurement (dx and dk steps after the forward)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -124,6 +129,80 @@ def backward_measurement(rc, plan, W, x, k, spec, ws, stream, args):
            "stages_us": {n: round(1e3 * tot / args.steps, 1) for n, (c, tot) in kt.items()}}
     del dk_ws, dx, dk, dy
     return out
+
+
+def stacked_measurement(rc, plan, W, x, stream, plan_ms, args):
+    """One plan shared by a stack of layers (the plan depends only on the document
+    boundaries): each layer transforms its own filter bank and convolves the previous
+    layer's output.  Reports the per-layer cost and the per-layer cost with the plan
+    amortised over the stack."""
+    import torch
+    import workloads as wl
+    dev = x.device
+    rng = np.random.default_rng(2000 + args.config)
+    banks = [torch.from_numpy(wl.decaying_filters(rng, W.D, W.L)).to(dev) for _ in range(args.layers)]
+    chain = W.x_dtype == W.y_dtype
+    ydt = x.dtype if chain else (torch.float32 if W.y_dtype == "f32" else torch.bfloat16)
+    outs = [torch.empty(x.shape, dtype=ydt, device=dev) for _ in range(args.layers)]
+    ws = plan.new_workspace(dev)
+    specs = [plan.new_spectrum(dev) for _ in range(args.layers)]
+
+    def launch(s):
+        inp = x
+        for i in range(args.layers):
+            rc.filter_spectrum(plan, banks[i], spectrum=specs[i], workspace=ws, stream=s)
+            rc.packed_conv(plan, inp, specs[i], y=outs[i], workspace=ws, stream=s)
+            if chain:
+                inp = outs[i]
+    ms = time_step(launch, stream, args.steps, args.warmup, args.eager)
+    per_layer = ms / args.layers
+    del banks, outs, specs, ws
+    # a new batch's plan once the process has built one (operand tables cached)
+    t0 = time.perf_counter()
+    plan2 = rc.Plan(W.cu_seqlens, N=W.N, D=W.D, L=W.L, x_dtype=W.x_dtype, y_dtype=W.y_dtype,
+                    n1=args.n1)
+    warm_ms = (time.perf_counter() - t0) * 1e3
+    plan2.close()
+    return {"layers": args.layers, "ms_per_stack": round(ms, 4),
+            "ms_per_layer": round(per_layer, 4),
+            "ms_per_layer_with_plan": round((ms + warm_ms) / args.layers, 4),
+            "plan_ms_first": round(plan_ms, 3), "plan_ms": round(warm_ms, 3), "chained": chain}
+
+
+def sweep(args):
+    """Forward step (filter spectra + convolution, graph replay) over D and L on the
+    document structure of the chosen workload."""
+    import torch
+    import paper_2605_08451_amd as rc
+    import workloads as wl
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    base = wl.make_config(args.config)
+    rows = wl.rows_from_cu(base.cu_seqlens)
+    for D in (256, 512, 1024, 2048):
+        for L in (1024, 4096, 16384):
+            W = wl.make_case(rows, D=D, L=min(L, 4 * base.N), x_dtype=base.x_dtype, seed=D + L)
+            if W.x_dtype == "bf16":
+                x = torch.from_numpy(W.x_bits.view(np.int16)).view(torch.bfloat16).to(dev)
+            else:
+                x = torch.from_numpy(W.x).to(dev)
+            k = torch.from_numpy(W.filters).to(dev)
+            plan = rc.Plan(W.cu_seqlens, N=W.N, D=W.D, L=W.L, x_dtype=W.x_dtype, y_dtype=W.y_dtype)
+            ws, spec = plan.new_workspace(dev), plan.new_spectrum(dev)
+            y = torch.empty(x.shape, dtype=x.dtype if W.y_dtype == W.x_dtype else torch.float32,
+                            device=dev)
+
+            def launch(s):
+                rc.filter_spectrum(plan, k, spectrum=spec, workspace=ws, stream=s)
+                rc.packed_conv(plan, x, spec, y=y, workspace=ws, stream=s)
+            ms = time_step(launch, stream, args.steps, args.warmup, args.eager)
+            tok_ch = W.B * W.N * W.D
+            print(json.dumps({"sweep": wl.CONFIG_NAMES[args.config], "D": D, "L": W.L,
+                              "ms_per_step": round(ms, 4),
+                              "value": round(tok_ch / (ms * 1e-3) / 1e6, 1),
+                              "unit": "Mtokens*channels/s"}), flush=True)
+            del x, k, plan, ws, spec, y
+            torch.cuda.empty_cache()
 
 
 def kernel_bytes(info, W, plan):
@@ -217,6 +296,9 @@ def main():
     import paper_2605_08451_amd as rc
     import workloads as wl
 
+    if args.sweep:
+        sweep(args)
+        return
     dev = torch.device("cuda:0")
     W = wl.make_config(args.config)
     if W.x_dtype == "bf16":
@@ -322,6 +404,8 @@ def main():
     }
     if not args.no_backward:
         out["backward"] = backward_measurement(rc, plan, W, x, k, spec, ws, stream, args)
+    if args.layers > 0:
+        out["stacked"] = stacked_measurement(rc, plan, W, x, stream, plan_ms, args)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(W, args.cpu_seconds)
     print(json.dumps(out), flush=True)

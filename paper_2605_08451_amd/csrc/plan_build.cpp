@@ -20,6 +20,8 @@
 #include <complex>
 #include <cstring>
 #include <map>
+#include <mutex>
+#include <tuple>
 
 namespace rubiconv {
 
@@ -55,13 +57,55 @@ int pairs_per_task(int m) {
     return spb;
 }
 
-void push_twiddles(std::vector<float>& tw, int64_t count, int64_t period, double scale = 1.0) {
+// z[r] = exp(-2 pi i r / period), r < period.  Only the first eighth of the circle is
+// evaluated (cos and sin of 2 pi r / period); the rest follows from the exact
+// symmetries of the circle, so the table costs period / 8 evaluations.
+std::vector<std::complex<double>> unit_circle(int64_t period) {
+    std::vector<std::complex<double>> z(static_cast<size_t>(period));
     const double two_pi = 6.283185307179586476925286766559;
+    auto direct = [&](int64_t r) {
+        const double a = two_pi * static_cast<double>(r) / static_cast<double>(period);
+        return std::complex<double>(std::cos(a), -std::sin(a));
+    };
+    if (period % 8 != 0) {
+        for (int64_t r = 0; r < period; ++r) z[r] = direct(r);
+        return z;
+    }
+    const int64_t q = period / 4, e = period / 8;
+    std::vector<double> c(q + 1), sn(q + 1);  // cos, sin of 2 pi r / period, r <= period / 4
+    for (int64_t r = 0; r <= e; ++r) {
+        const double a = two_pi * static_cast<double>(r) / static_cast<double>(period);
+        c[r] = std::cos(a);
+        sn[r] = std::sin(a);
+    }
+    for (int64_t r = e + 1; r <= q; ++r) {  // cos(pi/2 - x) = sin x
+        c[r] = sn[q - r];
+        sn[r] = c[q - r];
+    }
+    for (int64_t r = 0; r < period; ++r) {
+        const int64_t quad = r / q, t = r % q;
+        double cr, sr;  // cos, sin of 2 pi r / period
+        switch (quad) {
+            case 0: cr = c[t]; sr = sn[t]; break;
+            case 1: cr = -sn[t]; sr = c[t]; break;
+            case 2: cr = -c[t]; sr = -sn[t]; break;
+            default: cr = sn[t]; sr = -c[t]; break;
+        }
+        z[r] = std::complex<double>(cr, -sr);
+    }
+    return z;
+}
+
+void push_twiddles(std::vector<float>& tw, int64_t count, int64_t period, double scale = 1.0) {
+    // forward roots w_period^r = exp(-2 pi i r / period)
+    const std::vector<std::complex<double>> z = unit_circle(period);
+    const size_t base = tw.size();
+    tw.resize(base + 2 * static_cast<size_t>(count));
+    float* out = tw.data() + base;
     for (int64_t r = 0; r < count; ++r) {
-        // forward root w_period^r = exp(-2 pi i r / period), angle reduced exactly
-        double a = two_pi * static_cast<double>(r % period) / static_cast<double>(period);
-        tw.push_back(static_cast<float>(scale * std::cos(a)));
-        tw.push_back(static_cast<float>(-scale * std::sin(a)));
+        const std::complex<double>& w = z[r % period];
+        out[2 * r] = static_cast<float>(scale * w.real());
+        out[2 * r + 1] = static_cast<float>(scale * w.imag());
     }
 }
 
@@ -117,18 +161,20 @@ void push_operands(std::vector<uint32_t>* out, F entry, int kind) {
 // grid rows (an involution).
 int interleave(int s) { return 4 * (s % 4) + s / 4; }
 
-std::complex<double> root(double num, double den) {  // exp(2 pi i num / den)
-    const double a = 6.283185307179586476925286766559 * num / den;
-    return {std::cos(a), std::sin(a)};
+// exp(2 pi i e / 256) for any integer e (the column stages' roots, all 256th roots of
+// unity), from one table
+std::complex<double> root256(int64_t e) {
+    static const std::vector<std::complex<double>> z = unit_circle(256);  // exp(-2 pi i r / 256)
+    return std::conj(z[static_cast<size_t>(((e % 256) + 256) % 256)]);
 }
 
 }  // namespace
 
-void build_mfma_tables(std::vector<uint32_t>* out) {
-    out->clear();
+namespace {
+void make_mfma_tables(std::vector<uint32_t>* out) {
     // stage 1 contracts over the interleaved input slot; stage 2 produces the
     // interleaved output slot (kernels address rows accordingly)
-    auto fwd1 = [](int k1, int s) { return root(-static_cast<double>(k1 * interleave(s)), 16); };
+    auto fwd1 = [](int k1, int s) { return root256(-16 * k1 * interleave(s)); };
     // forward stage 1 in bf16 hi/lo: (re_hi, re_lo, im_hi, im_lo)
     std::vector<uint32_t> hi, lo;
     push_operands(&hi, fwd1, 1);
@@ -141,20 +187,21 @@ void build_mfma_tables(std::vector<uint32_t>* out) {
     for (int k1 = 0; k1 < 16; ++k1)                                 // stage 2, twiddle folded
         push_operands(out, [k1](int s, int n2) {
             const int k2 = interleave(s);
-            return root(-static_cast<double>(n2 * k2), 16) * root(-static_cast<double>(n2 * k1), 256);
+            return root256(-16 * n2 * k2 - n2 * k1);
         }, 0);
-    push_operands(out, [](int n2, int s) { return root(static_cast<double>(n2 * interleave(s)), 16); }, 0);
+    push_operands(out, [](int n2, int s) { return root256(16 * n2 * interleave(s)); }, 0);
     for (int n2 = 0; n2 < 16; ++n2)
         push_operands(out, [n2](int s, int k1) {
             const int n1 = interleave(s);
-            return root(static_cast<double>(n1 * k1), 16) * root(static_cast<double>(n2 * k1), 256);
+            return root256(16 * n1 * k1 + n2 * k1);
         }, 0);
 }
 
-void build_dense_tables(int m, int n1, std::vector<uint32_t>* out) {
+void make_dense_tables(int m, int n1, std::vector<uint32_t>* out) {
     const int nb = (m + 15) / 16;
     const double fwd_scale = 1.0 / std::sqrt(static_cast<double>(m));
     const double inv_scale = std::sqrt(static_cast<double>(n1)) / 4.0;
+    const std::vector<std::complex<double>> z = unit_circle(m);  // exp(-2 pi i e / m)
     // time-domain points are interleaved within a block (slot s <-> point interleave(s)),
     // so that one load or store instruction covers four neighbouring points; frequencies
     // keep their natural order
@@ -165,15 +212,16 @@ void build_dense_tables(int m, int n1, std::vector<uint32_t>* out) {
                     const int k = dir == 0 ? 16 * kb + row : 16 * jb + n;              // frequency
                     const int j = dir == 0 ? 16 * jb + interleave(n) : 16 * kb + interleave(row);  // time
                     if (k >= m || j >= m) return std::complex<double>(0.0, 0.0);
-                    const double e = static_cast<double>((static_cast<int64_t>(k) * j) % m);
-                    return dir == 0 ? root(-e, m) * fwd_scale : root(e, m) * inv_scale;
+                    const std::complex<double> w = z[(static_cast<int64_t>(k) * j) % m];
+                    return dir == 0 ? w * fwd_scale : std::conj(w) * inv_scale;
                 }, 0);
 }
 
-void build_partner_tables(int m, int n1, std::vector<uint32_t>* out) {
+void make_partner_tables(int m, int n1, std::vector<uint32_t>* out) {
     const int nb = (m + 15) / 16, S = 16 * nb;
     const double fwd_scale = 1.0 / std::sqrt(static_cast<double>(m));
     const double inv_scale = std::sqrt(static_cast<double>(n1)) / 4.0;
+    const std::vector<std::complex<double>> z = unit_circle(m);  // exp(-2 pi i e / m)
     const size_t start = out->size();
     // one real operand per 16 x 16 block: lane (row, q) holds entries (row, 4 q + c) as
     // (Re, -Im) pairs, c = 0..3; the imaginary output part comes from the same operand
@@ -193,17 +241,17 @@ void build_partner_tables(int m, int n1, std::vector<uint32_t>* out) {
                     const int k = dir == 0 ? 16 * kb + row : 16 * jb + n;              // frequency
                     const int j = dir == 0 ? 16 * jb + interleave(n) : 16 * kb + interleave(row);  // time
                     if (k >= m || j >= m) return std::complex<double>(0.0, 0.0);
-                    const double e = static_cast<double>((static_cast<int64_t>(k) * j) % m);
-                    return dir == 0 ? root(-e, m) * fwd_scale : root(e, m) * inv_scale;
+                    const std::complex<double> w = z[(static_cast<int64_t>(k) * j) % m];
+                    return dir == 0 ? w * fwd_scale : std::conj(w) * inv_scale;
                 });
     // partner-row twiddles: exp(+2 pi i j / m) as complex fp16, then exp(-2 pi i j / m)
     // as complex fp32, for time points j < S (zero past m)
     for (int j = 0; j < S; ++j) {
-        const std::complex<double> w = j < m ? root(j, m) : std::complex<double>(0.0, 0.0);
+        const std::complex<double> w = j < m ? std::conj(z[j]) : std::complex<double>(0.0, 0.0);
         out->push_back(to_f16_bits(w.real()) | (static_cast<uint32_t>(to_f16_bits(w.imag())) << 16));
     }
     for (int j = 0; j < S; ++j) {
-        const std::complex<double> w = j < m ? root(-j, m) : std::complex<double>(0.0, 0.0);
+        const std::complex<double> w = j < m ? z[j] : std::complex<double>(0.0, 0.0);
         const float re = static_cast<float>(w.real()), im = static_cast<float>(w.imag());
         uint32_t b[2];
         std::memcpy(&b[0], &re, 4);
@@ -213,6 +261,36 @@ void build_partner_tables(int m, int n1, std::vector<uint32_t>* out) {
     }
     // whole 1 KB chunks, as the kernel copies them
     while ((out->size() - start) % 256) out->push_back(0u);
+}
+
+// Operand tables depend only on (kind, m, N1): each is computed once per process and
+// copied into every plan that needs it.
+const std::vector<uint32_t>& cached_tables(int kind, int m, int n1) {
+    static std::mutex mu;
+    static std::map<std::tuple<int, int, int>, std::vector<uint32_t>> cache;
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = cache.find({kind, m, n1});
+    if (it == cache.end()) {
+        std::vector<uint32_t> t;
+        if (kind == 0) make_mfma_tables(&t);
+        else if (kind == 1) make_dense_tables(m, n1, &t);
+        else make_partner_tables(m, n1, &t);
+        it = cache.emplace(std::make_tuple(kind, m, n1), std::move(t)).first;
+    }
+    return it->second;
+}
+}  // namespace
+
+void build_mfma_tables(std::vector<uint32_t>* out) { *out = cached_tables(0, 0, 0); }
+
+void build_dense_tables(int m, int n1, std::vector<uint32_t>* out) {
+    const std::vector<uint32_t>& t = cached_tables(1, m, n1);
+    out->insert(out->end(), t.begin(), t.end());
+}
+
+void build_partner_tables(int m, int n1, std::vector<uint32_t>* out) {
+    const std::vector<uint32_t>& t = cached_tables(2, m, n1);
+    out->insert(out->end(), t.begin(), t.end());
 }
 
 BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_docs,
@@ -298,6 +376,11 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
 
     if (!p.direct_docs.empty()) p.direct_taps = std::min(L, direct_max);
     // size classes, ascending m: twiddles, spectrum offsets, filter taps
+    {
+        size_t tw_floats = 0;
+        for (const auto& kv : class_of_m) tw_floats += 2 * (static_cast<size_t>(kv.first) + static_cast<size_t>(n1) * kv.first);
+        p.tw.reserve(tw_floats);
+    }
     for (auto& kv : class_of_m) {
         int m = kv.first;
         kv.second = static_cast<int>(p.classes.size());
