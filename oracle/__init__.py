@@ -23,6 +23,10 @@ the two maps.  ``grad_x`` is the anti-causal correlation inside every document,
 sums ``dy[t] x[t - tau]`` over the tokens of every document of every row for each
 lag ``tau < L``; ``grad_x_at`` and ``grad_k_at`` evaluate single entries.
 
+``oracle.masked_fft`` holds the boundary-respecting Cooley-Tukey transform of
+Algorithm 2 (masked radix-2 stages over the packed array) and the convolution
+built on it, pinned separately (tests/test_oracle_ct.py).
+
 Pins (tests/test_oracle.py, tests/golden/): brute-force block-diagonal Toeplitz
 matrices, single documents against library convolutions (numpy.convolve,
 scipy.signal.lfilter, numpy.fft), delta inputs and delta filters, bilinearity,
