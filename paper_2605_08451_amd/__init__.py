@@ -23,7 +23,8 @@ import numpy as np
 import torch
 
 __all__ = ["Plan", "RubiconvError", "filter_spectrum", "packed_conv", "packed_conv_dx",
-           "packed_conv_dk", "conv", "library_path", "load_library", "EXPORTED_SYMBOLS"]
+           "packed_conv_dk", "conv", "CTPlan", "ct_filter_spectrum", "ct_packed_conv",
+           "library_path", "load_library", "EXPORTED_SYMBOLS"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "librubiconv.so")
@@ -33,12 +34,15 @@ F32, BF16 = 0, 1
 _STATUS = {0: "ok", 1: "invalid argument", 2: "invalid cu_seqlens", 3: "unsupported configuration",
            4: "allocation failed", 5: "HIP error or no device"}
 
-#: Every function ``include/rubiconv.h`` declares.
+#: Every function ``include/rubiconv.h`` and ``include/rubiconv_ct.h`` declare.
 EXPORTED_SYMBOLS = ("rubiconv_plan", "rubiconv_plan_destroy", "rubiconv_spectrum_bytes",
                     "rubiconv_workspace_bytes", "rubiconv_filter_spectrum", "rubiconv_packed_conv",
                     "rubiconv_packed_conv_dx", "rubiconv_dk_workspace_bytes", "rubiconv_packed_conv_dk",
                     "rubiconv_plan_info", "rubiconv_plan_doc_table", "rubiconv_profile_start",
-                    "rubiconv_profile_read", "rubiconv_status_string")
+                    "rubiconv_profile_read", "rubiconv_status_string",
+                    "rubiconv_ct_plan", "rubiconv_ct_plan_destroy", "rubiconv_ct_spectrum_bytes",
+                    "rubiconv_ct_workspace_bytes", "rubiconv_ct_filter_spectrum",
+                    "rubiconv_ct_packed_conv", "rubiconv_ct_plan_doc_table")
 
 
 class RubiconvError(RuntimeError):
@@ -104,6 +108,21 @@ def load_library():
     lib.rubiconv_profile_read.restype = c_int
     lib.rubiconv_status_string.argtypes = [c_int]
     lib.rubiconv_status_string.restype = ctypes.c_char_p
+    lib.rubiconv_ct_plan.argtypes = [ctypes.POINTER(vp), c_int, c_int, c_int, c_int, c_int, i32p,
+                                     c_int, c_int]
+    lib.rubiconv_ct_plan.restype = c_int
+    lib.rubiconv_ct_plan_destroy.argtypes = [vp]
+    lib.rubiconv_ct_plan_destroy.restype = None
+    lib.rubiconv_ct_spectrum_bytes.argtypes = [vp]
+    lib.rubiconv_ct_spectrum_bytes.restype = sz
+    lib.rubiconv_ct_workspace_bytes.argtypes = [vp]
+    lib.rubiconv_ct_workspace_bytes.restype = sz
+    lib.rubiconv_ct_filter_spectrum.argtypes = [vp, vp, vp, vp, vp]
+    lib.rubiconv_ct_filter_spectrum.restype = c_int
+    lib.rubiconv_ct_packed_conv.argtypes = [vp, vp, vp, vp, vp, vp]
+    lib.rubiconv_ct_packed_conv.restype = c_int
+    lib.rubiconv_ct_plan_doc_table.argtypes = [vp, i32p, c_int, ctypes.POINTER(c_int)]
+    lib.rubiconv_ct_plan_doc_table.restype = c_int
     _LIB = lib
     return lib
 
@@ -130,6 +149,17 @@ def _stream_handle(device, stream) -> int:
     return s.cuda_stream
 
 
+def _cu_array(cu_seqlens) -> np.ndarray:
+    if isinstance(cu_seqlens, torch.Tensor):
+        cu_seqlens = cu_seqlens.detach().cpu().numpy()
+    cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+    if cu.ndim == 1:
+        cu = cu[None]
+    if cu.ndim != 2 or cu.shape[1] < 2:
+        raise ValueError("cu_seqlens must be [B, max_docs + 1]")
+    return cu
+
+
 class Plan:
     """Document table, size classes and twiddles for one batch of boundaries
     (Algorithm 1's data processing; shared by every layer that sees this batch)."""
@@ -137,13 +167,7 @@ class Plan:
     def __init__(self, cu_seqlens, N: int, D: int, L: int, x_dtype=torch.bfloat16,
                  y_dtype=None, n1: int = 0):
         lib = load_library()
-        if isinstance(cu_seqlens, torch.Tensor):
-            cu_seqlens = cu_seqlens.detach().cpu().numpy()
-        cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
-        if cu.ndim == 1:
-            cu = cu[None]
-        if cu.ndim != 2 or cu.shape[1] < 2:
-            raise ValueError("cu_seqlens must be [B, max_docs + 1]")
+        cu = _cu_array(cu_seqlens)
         self.B, self.max_docs = int(cu.shape[0]), int(cu.shape[1] - 1)
         self.N, self.D, self.L = int(N), int(D), int(L)
         self.x_dtype = _dtype_code(x_dtype)
@@ -348,4 +372,112 @@ def conv(x: torch.Tensor, filters: torch.Tensor, cu_seqlens, y_dtype=None, n1: i
     y = packed_conv(plan, x, spec, workspace=ws)
     torch.cuda.current_stream(x.device).synchronize()
     plan.close()
+    return y
+
+
+# ----------------------------------------------------------------- masked Cooley-Tukey
+class CTPlan:
+    """Plan of the masked Cooley-Tukey variant (Algorithm 2, ``include/rubiconv_ct.h``):
+    power-of-two document sizes and the packed layout its masked stages run on."""
+
+    def __init__(self, cu_seqlens, N: int, D: int, L: int, x_dtype=torch.bfloat16, y_dtype=None):
+        lib = load_library()
+        cu = _cu_array(cu_seqlens)
+        self.B, self.max_docs = int(cu.shape[0]), int(cu.shape[1] - 1)
+        self.N, self.D, self.L = int(N), int(D), int(L)
+        self.x_dtype = _dtype_code(x_dtype)
+        self.y_dtype = self.x_dtype if y_dtype is None else _dtype_code(y_dtype)
+        self._h = ctypes.c_void_p()
+        self._lib = lib
+        _check(lib.rubiconv_ct_plan(ctypes.byref(self._h), self.B, self.N, self.D, self.L,
+                                    self.max_docs, cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                    self.x_dtype, self.y_dtype), "rubiconv_ct_plan")
+        self.cu_seqlens = cu.copy()
+
+    @property
+    def handle(self):
+        if not self._h:
+            raise RuntimeError("plan already destroyed")
+        return self._h
+
+    @property
+    def spectrum_bytes(self) -> int:
+        return int(self._lib.rubiconv_ct_spectrum_bytes(self.handle))
+
+    @property
+    def workspace_bytes(self) -> int:
+        return int(self._lib.rubiconv_ct_workspace_bytes(self.handle))
+
+    def doc_table(self) -> np.ndarray:
+        """int32 [n_docs, 6]: row, index in row, start, length, P_i, offset in the packed array."""
+        n = ctypes.c_int(0)
+        _check(self._lib.rubiconv_ct_plan_doc_table(self.handle, None, 0, ctypes.byref(n)),
+               "rubiconv_ct_plan_doc_table")
+        out = np.zeros((max(n.value, 1), 6), dtype=np.int32)
+        _check(self._lib.rubiconv_ct_plan_doc_table(
+            self.handle, out.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n.value,
+            ctypes.byref(n)), "rubiconv_ct_plan_doc_table")
+        return out[:n.value].copy()
+
+    def new_spectrum(self, device) -> torch.Tensor:
+        return torch.empty(self.spectrum_bytes, dtype=torch.uint8, device=device)
+
+    def new_workspace(self, device) -> torch.Tensor:
+        return torch.empty(self.workspace_bytes, dtype=torch.uint8, device=device)
+
+    def close(self):
+        if self._h:
+            self._lib.rubiconv_ct_plan_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def ct_filter_spectrum(plan: CTPlan, filters: torch.Tensor, spectrum: Optional[torch.Tensor] = None,
+                       workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Spectra of ``filters`` (cuda float32 [D, L]) for every power-of-two size of ``plan``."""
+    _cuda_contig(filters, "filters")
+    if filters.dtype != torch.float32 or tuple(filters.shape) != (plan.D, plan.L):
+        raise ValueError(f"filters must be float32 [{plan.D}, {plan.L}]")
+    dev = filters.device
+    if spectrum is None:
+        spectrum = plan.new_spectrum(dev)
+    if workspace is None:
+        workspace = plan.new_workspace(dev)
+    if spectrum.numel() * spectrum.element_size() < plan.spectrum_bytes:
+        raise ValueError("spectrum buffer too small")
+    if workspace.numel() * workspace.element_size() < plan.workspace_bytes:
+        raise ValueError("workspace buffer too small")
+    with torch.cuda.device(dev):
+        _check(plan._lib.rubiconv_ct_filter_spectrum(plan.handle, filters.data_ptr(),
+                                                     spectrum.data_ptr(), workspace.data_ptr(),
+                                                     _stream_handle(dev, stream)),
+               "rubiconv_ct_filter_spectrum")
+    return spectrum
+
+
+def ct_packed_conv(plan: CTPlan, x: torch.Tensor, spectrum: torch.Tensor,
+                   y: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                   stream=None) -> torch.Tensor:
+    """The packed causal convolution through the masked Cooley-Tukey transform."""
+    _check_btd(x, plan, plan.x_dtype, "x")
+    dev = x.device
+    if y is None:
+        y = torch.empty((plan.B, plan.N, plan.D), dtype=_torch_dtype(plan.y_dtype), device=dev)
+    _check_btd(y, plan, plan.y_dtype, "y")
+    if workspace is None:
+        workspace = plan.new_workspace(dev)
+    if workspace.numel() * workspace.element_size() < plan.workspace_bytes:
+        raise ValueError("workspace buffer too small")
+    if spectrum.numel() * spectrum.element_size() < plan.spectrum_bytes:
+        raise ValueError("spectrum buffer too small")
+    with torch.cuda.device(dev):
+        _check(plan._lib.rubiconv_ct_packed_conv(plan.handle, x.data_ptr(), spectrum.data_ptr(),
+                                                 y.data_ptr(), workspace.data_ptr(),
+                                                 _stream_handle(dev, stream)),
+               "rubiconv_ct_packed_conv")
     return y

@@ -1,0 +1,638 @@
+// ct_kernels.hip -- the masked Cooley-Tukey convolution (Algorithm 2) on gfx950.
+//
+// Algorithm 2 runs the radix-2 decimation-in-time stages over the whole packed
+// array and masks them: at stage s (butterflies of size m = 2^s) an element whose
+// document is shorter than m keeps its value, every other element takes the
+// standard butterfly at its position inside its own document.  Here the same
+// stages run on a flat array holding the documents longest first (ct_plan.hpp), so
+// every document starts at a multiple of its size and the standard twiddle of an
+// element depends on its flat position alone; only the mask needs the document.
+//
+// Stages are fused three at a time in registers (a radix-8 group holds the 8
+// elements that three consecutive radix-2 stages combine), and a workgroup keeps a
+// tile of kTile points x kPairs channel pairs in LDS:
+//   * short documents (P <= kTile): one kernel takes a tile of whole documents from
+//     x through the forward stages, the spectral product, the inverse stages and
+//     into y;
+//   * long documents (P = kTile * M, M <= 64): the first kLogTile stages run on
+//     each tile (front), the last log2 M stages on the columns l = c + kTile * j
+//     (column pass, which also takes the product), and the inverse repeats the
+//     split in reverse (column pass, then back).
+// The inverse uses decimation-in-frequency stages (the same butterflies with the
+// conjugate twiddles, in reverse order), which take the spectrum in natural order
+// and leave the time samples in bit-reversed order: the forward transform's load
+// and the inverse's store use the same bit-reversed positions, and no separate
+// reordering pass is needed.  Channels d and d + 1 share one complex transform;
+// the filter spectrum separates them (ct_kernels.hpp).
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "ct_kernels.hpp"
+#include "fft_core.hpp"
+#include "pk_half.hpp"
+
+namespace rubiconv::ct {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kSlots = kThreads / kPairs;      // 16 element slots per channel-pair lane
+constexpr int kTileGroups = kTile / 8;         // radix-8 groups of one tile
+constexpr int kMaxCols = 1 << kMaxLogCols;
+
+__device__ __forceinline__ int bitrev(int v, int bits) {
+    return bits == 0 ? 0 : static_cast<int>(__builtin_bitreverse32(static_cast<uint32_t>(v)) >> (32 - bits));
+}
+
+__device__ __forceinline__ float2 sel(bool c, float2 a, float2 b) {
+    return make_float2(c ? a.x : b.x, c ? a.y : b.y);
+}
+
+__device__ __forceinline__ float2 mul_conj(float2 a, float2 b) {  // a * conj(b)
+    return make_float2(a.x * b.x + a.y * b.y, a.y * b.x - a.x * b.y);
+}
+
+__device__ __forceinline__ Doc load_doc(const Doc* docs, int i) {
+    const int4* p = reinterpret_cast<const int4*>(docs + i);
+    const int4 a = p[0], b = p[1];
+    return Doc{a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+}
+
+// ---------------------------------------------------------------- element I/O
+// Channel pair p of token `tok` of row `row` as one complex value (zero past D).
+template <int TA>
+__device__ __forceinline__ float2 load_pair(const void* a, int row, int tok, int N, int D, int p) {
+    if (2 * p >= D) return make_float2(0.f, 0.f);
+    const int64_t i = (static_cast<int64_t>(row) * N + tok) * D + 2 * p;
+    if constexpr (TA == 0) {
+        return *reinterpret_cast<const float2*>(static_cast<const float*>(a) + i);
+    } else {
+        const uint32_t u = *reinterpret_cast<const uint32_t*>(static_cast<const uint16_t*>(a) + i);
+        return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xffff0000u));
+    }
+}
+
+template <int TO>
+__device__ __forceinline__ void store_pair(void* o, int row, int tok, int N, int D, int p, float2 v) {
+    if (2 * p >= D) return;
+    const int64_t i = (static_cast<int64_t>(row) * N + tok) * D + 2 * p;
+    if constexpr (TO == 0) {
+        *reinterpret_cast<float2*>(static_cast<float*>(o) + i) = v;
+    } else {
+        *reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(o) + i) = bf2_bits(v.x, v.y);
+    }
+}
+
+template <bool HALF>
+__device__ __forceinline__ float2 grid_load(const void* g, int64_t i) {
+    if constexpr (HALF) {
+        const uint32_t u = static_cast<const uint32_t*>(g)[i];
+        return __half22float2(__builtin_bit_cast(__half2, u));
+    } else {
+        return static_cast<const float2*>(g)[i];
+    }
+}
+
+template <bool HALF>
+__device__ __forceinline__ void grid_store(void* g, int64_t i, float2 v) {
+    if constexpr (HALF) static_cast<uint32_t*>(g)[i] = h2_bits(v.x, v.y);
+    else static_cast<float2*>(g)[i] = v;
+}
+
+// ---------------------------------------------------------------- stage groups
+// A group holds the 2^K elements l_i = base + i * h0 (h0 = 2^(sigma0 - 1), b0 = base
+// mod h0).  Stage sigma = sigma0 + k pairs elements i and i + 2^k (bit k of i clear)
+// with the twiddle w_{2^sigma}^r, r = b0 + (i mod 2^k) * h0 (the element's position
+// inside its butterfly).  on(i, sigma) is the element's mask: its document holds at
+// least 2^sigma points.
+template <int K, class Tw, class On>
+__device__ __forceinline__ void dit_group(float2 (&v)[1 << K], int b0, int h0, int sigma0, Tw tw, On on) {
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        const int sigma = sigma0 + k;
+#pragma unroll
+        for (int i = 0; i < (1 << K); ++i) {
+            if (i & (1 << k)) continue;
+            const int j = i | (1 << k);
+            const float2 t = cmul(tw(b0 + (i & ((1 << k) - 1)) * h0, sigma), v[j]);
+            const bool a = on(i, sigma);
+            const float2 top = cadd(v[i], t), bot = csub(v[i], t);
+            v[i] = sel(a, top, v[i]);
+            v[j] = sel(a, bot, v[j]);
+        }
+    }
+}
+
+// The inverse (decimation in frequency): stages sigma0 + K - 1 down to sigma0, each
+// (a, b) -> (a + b, (a - b) conj(w)) with the same pairs and twiddles.
+template <int K, class Tw, class On>
+__device__ __forceinline__ void dif_group(float2 (&v)[1 << K], int b0, int h0, int sigma0, Tw tw, On on) {
+#pragma unroll
+    for (int k = K - 1; k >= 0; --k) {
+        const int sigma = sigma0 + k;
+#pragma unroll
+        for (int i = 0; i < (1 << K); ++i) {
+            if (i & (1 << k)) continue;
+            const int j = i | (1 << k);
+            const bool a = on(i, sigma);
+            const float2 top = cadd(v[i], v[j]);
+            const float2 bot = mul_conj(csub(v[i], v[j]), tw(b0 + (i & ((1 << k) - 1)) * h0, sigma));
+            v[i] = sel(a, top, v[i]);
+            v[j] = sel(a, bot, v[j]);
+        }
+    }
+}
+
+// Group g of a radix-8 pass with element stride h0 over a tile: base and b0.
+__device__ __forceinline__ int group_base(int g, int lg_h0) {
+    return (g & ((1 << lg_h0) - 1)) + ((g >> lg_h0) << (lg_h0 + 3));
+}
+
+struct TileTw {  // w_{2^sigma}^r for sigma <= kLogTile, from w_kTile^k in LDS
+    const float2* s;
+    __device__ float2 operator()(int r, int sigma) const { return s[r << (kLogTile - sigma)]; }
+};
+
+struct GlobalTw {  // w_{2^sigma}^r for sigma <= kMaxLogP
+    const float2* g;
+    __device__ float2 operator()(int r, int sigma) const { return g[r << (kMaxLogP - sigma)]; }
+};
+
+struct AllOn {
+    __device__ bool operator()(int, int) const { return true; }
+};
+
+__device__ __forceinline__ void load_tile_twiddles(float2* s_tw, const float2* tw) {
+    for (int k = threadIdx.x; k < kTile / 2; k += kThreads) s_tw[k] = tw[k << (kMaxLogP - kLogTile)];
+}
+
+// One radix-8 pass over the LDS tile (forward or inverse), stride 2^lg_h0.
+template <bool INV>
+__device__ __forceinline__ void tile_pass(float2 (*s_z)[kPairs], const uint8_t* s_lp, TileTw tw,
+                                          int lg_h0, int q, int slot) {
+    const int h0 = 1 << lg_h0;
+    for (int g = slot; g < kTileGroups; g += kSlots) {
+        const int base = group_base(g, lg_h0);
+        float2 v[8];
+        int lp[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            v[i] = s_z[base + i * h0][q];
+            lp[i] = s_lp ? s_lp[base + i * h0] : kMaxLogP;
+        }
+        auto on = [&](int i, int sigma) { return lp[i] >= sigma; };
+        if constexpr (INV) dif_group<3>(v, base & (h0 - 1), h0, lg_h0 + 1, tw, on);
+        else dit_group<3>(v, base & (h0 - 1), h0, lg_h0 + 1, tw, on);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s_z[base + i * h0][q] = v[i];
+    }
+}
+
+// ---------------------------------------------------------------- short documents
+// W(f) for element f of a document of 2^lg points: Z(f) U(f) + conj(Z(-f)) V(f).
+__device__ __forceinline__ float2 spectral_product(float2 z, float2 zn, const float4* spec, int64_t e,
+                                                   bool upper) {
+    const float4 s = spec[e];
+    float2 u = make_float2(s.x, s.y), w = make_float2(s.z, s.w);
+    if (upper) {
+        u = cconj(u);
+        w = cconj(w);
+    }
+    return cadd(cmul(z, u), cmul(cconj(zn), w));
+}
+
+// U and V of the spectrum from the transform Zk of the taps pair (k_d + i k_{d+1}).
+__device__ __forceinline__ float4 spectrum_entry(float2 z, float2 zn, float inv2p) {
+    const float2 c = cconj(zn);
+    const float2 hd = cscale(cadd(z, c), 0.5f);                   // H_d
+    const float2 dd = csub(z, c);
+    const float2 hd1 = make_float2(0.5f * dd.y, -0.5f * dd.x);     // H_{d+1} = (z - conj zn) / (2i)
+    const float2 u = cscale(cadd(hd, hd1), inv2p), v = cscale(csub(hd, hd1), inv2p);
+    return make_float4(u.x, u.y, v.x, v.y);
+}
+
+template <int MODE, int TA, int TO>
+__global__ __launch_bounds__(kThreads, 2) void short_kernel(
+    const Doc* __restrict__ docs, const int32_t* __restrict__ tile_docs, int64_t region_off,
+    const void* __restrict__ a, int N, int D, float4* __restrict__ spec, void* __restrict__ out,
+    const float2* __restrict__ tw) {
+    __shared__ float2 s_z[kTile][kPairs];
+    __shared__ float2 s_tw[kTile / 2];
+    __shared__ uint8_t s_lp[kTile];   // log2 of the point's document size (0: none)
+    __shared__ int16_t s_doc[kTile];  // the point's document relative to d0 (-1: none)
+    const int tile = blockIdx.x, pb = blockIdx.y;
+    const int q = threadIdx.x & (kPairs - 1), slot = threadIdx.x / kPairs;
+    const int p = pb * kPairs + q;
+    const int d0 = tile_docs[2 * tile], d1 = tile_docs[2 * tile + 1];
+    const int64_t base = region_off + static_cast<int64_t>(tile) * kTile;
+    load_tile_twiddles(s_tw, tw);
+    for (int u = threadIdx.x; u < kTile; u += kThreads) {
+        int lp = 0, rel = -1;
+        const int64_t pos = base + u;
+        if (d1 > d0 && docs[d0].off <= pos) {
+            int lo = d0, hi = d1;  // docs[lo].off <= pos < docs[hi].off
+            while (hi - lo > 1) {
+                const int mid = (lo + hi) >> 1;
+                if (docs[mid].off <= pos) lo = mid;
+                else hi = mid;
+            }
+            if (pos < static_cast<int64_t>(docs[lo].off) + (int64_t(1) << docs[lo].logp)) {
+                lp = docs[lo].logp;
+                rel = lo - d0;
+            }
+        }
+        s_lp[u] = static_cast<uint8_t>(lp);
+        s_doc[u] = static_cast<int16_t>(rel);
+    }
+    __syncthreads();
+    const TileTw ttw{s_tw};
+    // forward stages 1-3, loading the bit-reversed samples straight from global memory
+    for (int g = slot; g < kTileGroups; g += kSlots) {
+        float2 v[8];
+        int lp[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int u = 8 * g + i;
+            const int rel = s_doc[u];
+            lp[i] = s_lp[u];
+            v[i] = make_float2(0.f, 0.f);
+            if (rel >= 0) {
+                const Doc d = load_doc(docs, d0 + rel);
+                const int t = bitrev(static_cast<int>(base + u - d.off), d.logp);
+                if (t < d.len) v[i] = load_pair<TA>(a, d.row, d.start + t, N, D, p);
+            }
+        }
+        auto on = [&](int i, int sigma) { return lp[i] >= sigma; };
+        dit_group<3>(v, 0, 1, 1, ttw, on);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s_z[8 * g + i][q] = v[i];
+    }
+    __syncthreads();
+    tile_pass<false>(s_z, s_lp, ttw, 3, q, slot);
+    __syncthreads();
+    tile_pass<false>(s_z, s_lp, ttw, 6, q, slot);
+    __syncthreads();
+    constexpr int kPer = kTile / kSlots;  // points per thread
+    if constexpr (MODE == 1) {
+        // spectrum entries f <= P/2 of every size class in the tile
+        for (int k = 0; k < kPer; ++k) {
+            const int u = slot + kSlots * k;
+            const int rel = s_doc[u];
+            if (rel < 0) continue;
+            const Doc d = load_doc(docs, d0 + rel);
+            const int P = 1 << d.logp;
+            const int f = static_cast<int>(base + u - d.off);
+            if (2 * f > P) continue;
+            const int nf = (P - f) & (P - 1);
+            const float4 e = spectrum_entry(s_z[u][q], s_z[u - f + nf][q], 0.5f / P);
+            spec[d.spec + (static_cast<int64_t>(pb) * (P / 2 + 1) + f) * kPairs + q] = e;
+        }
+        return;
+    } else {
+        float2 w[kPer];
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int u = slot + kSlots * k;
+            const int rel = s_doc[u];
+            w[k] = make_float2(0.f, 0.f);
+            if (rel >= 0) {
+                const Doc d = load_doc(docs, d0 + rel);
+                const int P = 1 << d.logp;
+                const int f = static_cast<int>(base + u - d.off);
+                const int nf = (P - f) & (P - 1);
+                const bool upper = 2 * f > P;
+                const int fi = upper ? P - f : f;
+                w[k] = spectral_product(s_z[u][q], s_z[u - f + nf][q], spec,
+                                        d.spec + (static_cast<int64_t>(pb) * (P / 2 + 1) + fi) * kPairs + q,
+                                        upper);
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) s_z[slot + kSlots * k][q] = w[k];
+        __syncthreads();
+        tile_pass<true>(s_z, s_lp, ttw, 6, q, slot);
+        __syncthreads();
+        tile_pass<true>(s_z, s_lp, ttw, 3, q, slot);
+        __syncthreads();
+        // inverse stages 3-1, then every sample to its bit-reversed time in y
+        for (int g = slot; g < kTileGroups; g += kSlots) {
+            float2 v[8];
+            int lp[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                v[i] = s_z[8 * g + i][q];
+                lp[i] = s_lp[8 * g + i];
+            }
+            auto on = [&](int i, int sigma) { return lp[i] >= sigma; };
+            dif_group<3>(v, 0, 1, 1, ttw, on);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int u = 8 * g + i;
+                const int rel = s_doc[u];
+                if (rel < 0) continue;
+                const Doc d = load_doc(docs, d0 + rel);
+                const int t = bitrev(static_cast<int>(base + u - d.off), d.logp);
+                if (t < d.len) store_pair<TO>(out, d.row, d.start + t, N, D, p, v[i]);
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- long documents
+// Tile k of document d holds, at point u, time c + M * bitrev(u) (forward input and
+// inverse output alike), with M = P / kTile and c = bitrev(k) over log2 M bits.
+template <int TA, bool HALF>
+__global__ __launch_bounds__(kThreads, 2) void front_kernel(
+    const Doc* __restrict__ docs, const int32_t* __restrict__ tile_doc, const void* __restrict__ a,
+    int N, int D, void* __restrict__ grid, int64_t long_points, const float2* __restrict__ tw) {
+    __shared__ float2 s_z[kTile][kPairs];
+    __shared__ float2 s_tw[kTile / 2];
+    const int tile = blockIdx.x, pb = blockIdx.y;
+    const int q = threadIdx.x & (kPairs - 1), slot = threadIdx.x / kPairs;
+    const int p = pb * kPairs + q;
+    const Doc d = load_doc(docs, tile_doc[tile]);
+    const int lg_m = d.logp - kLogTile;
+    const int c = bitrev(static_cast<int>((static_cast<int64_t>(tile) * kTile - d.off) >> kLogTile), lg_m);
+    load_tile_twiddles(s_tw, tw);
+    __syncthreads();
+    const TileTw ttw{s_tw};
+    for (int g = slot; g < kTileGroups; g += kSlots) {
+        float2 v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int t = c + (bitrev(8 * g + i, kLogTile) << lg_m);
+            v[i] = t < d.len ? load_pair<TA>(a, d.row, d.start + t, N, D, p) : make_float2(0.f, 0.f);
+        }
+        dit_group<3>(v, 0, 1, 1, ttw, AllOn{});
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s_z[8 * g + i][q] = v[i];
+    }
+    __syncthreads();
+    tile_pass<false>(s_z, nullptr, ttw, 3, q, slot);
+    __syncthreads();
+    const int64_t row0 = static_cast<int64_t>(pb) * long_points + static_cast<int64_t>(tile) * kTile;
+    for (int g = slot; g < kTileGroups; g += kSlots) {  // stages 7-9, stride 64, to the grid
+        float2 v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = s_z[g + 64 * i][q];
+        dit_group<3>(v, g, 64, 7, ttw, AllOn{});
+#pragma unroll
+        for (int i = 0; i < 8; ++i) grid_store<HALF>(grid, (row0 + g + 64 * i) * kPairs + q, v[i]);
+    }
+}
+
+template <int TO, bool HALF>
+__global__ __launch_bounds__(kThreads, 2) void back_kernel(
+    const Doc* __restrict__ docs, const int32_t* __restrict__ tile_doc, const void* __restrict__ grid,
+    int64_t long_points, void* __restrict__ out, int N, int D, const float2* __restrict__ tw) {
+    __shared__ float2 s_z[kTile][kPairs];
+    __shared__ float2 s_tw[kTile / 2];
+    const int tile = blockIdx.x, pb = blockIdx.y;
+    const int q = threadIdx.x & (kPairs - 1), slot = threadIdx.x / kPairs;
+    const int p = pb * kPairs + q;
+    const Doc d = load_doc(docs, tile_doc[tile]);
+    const int lg_m = d.logp - kLogTile;
+    const int c = bitrev(static_cast<int>((static_cast<int64_t>(tile) * kTile - d.off) >> kLogTile), lg_m);
+    load_tile_twiddles(s_tw, tw);
+    __syncthreads();
+    const TileTw ttw{s_tw};
+    const int64_t row0 = static_cast<int64_t>(pb) * long_points + static_cast<int64_t>(tile) * kTile;
+    for (int g = slot; g < kTileGroups; g += kSlots) {  // inverse stages 9-7 from the grid
+        float2 v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = grid_load<HALF>(grid, (row0 + g + 64 * i) * kPairs + q);
+        dif_group<3>(v, g, 64, 7, ttw, AllOn{});
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s_z[g + 64 * i][q] = v[i];
+    }
+    __syncthreads();
+    tile_pass<true>(s_z, nullptr, ttw, 3, q, slot);
+    __syncthreads();
+    for (int g = slot; g < kTileGroups; g += kSlots) {  // inverse stages 3-1, to y
+        float2 v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = s_z[8 * g + i][q];
+        dif_group<3>(v, 0, 1, 1, ttw, AllOn{});
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int t = c + (bitrev(8 * g + i, kLogTile) << lg_m);
+            if (t < d.len) store_pair<TO>(out, d.row, d.start + t, N, D, p, v[i]);
+        }
+    }
+}
+
+// Column pass over the columns l = c + kTile * j (j < M) of one long document: a
+// work item takes kColGroup low columns c = g * kColGroup + s and their partners
+// (kTile - c) mod kTile, which hold the frequencies -f of the low columns'
+// frequencies f = c + kTile * j; the last item takes column kTile / 2 alone.
+template <int K, bool INV>
+__device__ __forceinline__ void col_pass(float2 (*s_c)[kMaxCols][kPairs], const int* cols, int lg_m,
+                                         int sigma0, GlobalTw tw, int q, int slot) {
+    // stages sigma0 .. sigma0 + K - 1 (> kLogTile): element stride over j is 2^(sigma0 - kLogTile - 1)
+    const int lg_hj = sigma0 - kLogTile - 1;
+    const int hj = 1 << lg_hj;
+    const int per_col = (1 << lg_m) >> K;  // groups per column
+    for (int e = slot; e < 2 * kColGroup * per_col; e += kSlots) {
+        const int s = e / per_col, g = e - s * per_col;
+        if (cols[s] < 0) continue;
+        const int jb = (g & (hj - 1)) + ((g >> lg_hj) << (lg_hj + K));
+        float2 v[1 << K];
+#pragma unroll
+        for (int i = 0; i < (1 << K); ++i) v[i] = s_c[s][jb + i * hj][q];
+        const int b0 = cols[s] + kTile * (jb & (hj - 1));
+        if constexpr (INV) dif_group<K>(v, b0, kTile * hj, sigma0, tw, AllOn{});
+        else dit_group<K>(v, b0, kTile * hj, sigma0, tw, AllOn{});
+#pragma unroll
+        for (int i = 0; i < (1 << K); ++i) s_c[s][jb + i * hj][q] = v[i];
+    }
+}
+
+// All stages of the column pass in one direction: passes of 3, then the remainder.
+template <bool INV>
+__device__ __forceinline__ void col_stages(float2 (*s_c)[kMaxCols][kPairs], const int* cols, int lg_m,
+                                           GlobalTw tw, int q, int slot) {
+    // forward order: stages kLogTile+1 ..; a pass of 3 at the low end, 3 next, remainder last
+    const int n3 = lg_m / 3, rem = lg_m - 3 * n3;
+    int sig[3], kk[3], n = 0;
+    int s0 = kLogTile + 1;
+    for (int i = 0; i < n3; ++i) { sig[n] = s0; kk[n] = 3; ++n; s0 += 3; }
+    if (rem) { sig[n] = s0; kk[n] = rem; ++n; }
+    for (int t = 0; t < n; ++t) {
+        const int i = INV ? n - 1 - t : t;
+        if (kk[i] == 3) col_pass<3, INV>(s_c, cols, lg_m, sig[i], tw, q, slot);
+        else if (kk[i] == 2) col_pass<2, INV>(s_c, cols, lg_m, sig[i], tw, q, slot);
+        else col_pass<1, INV>(s_c, cols, lg_m, sig[i], tw, q, slot);
+        __syncthreads();
+    }
+}
+
+template <int MODE, bool HALF>
+__global__ __launch_bounds__(kThreads, 2) void col_kernel(
+    const Doc* __restrict__ docs, const int32_t* __restrict__ items, void* __restrict__ grid,
+    int64_t long_points, float4* __restrict__ spec, const float2* __restrict__ tw) {
+    __shared__ float2 s_c[2 * kColGroup][kMaxCols][kPairs];
+    __shared__ int s_cols[2 * kColGroup];
+    const int item = items[blockIdx.x], pb = blockIdx.y;
+    const int q = threadIdx.x & (kPairs - 1), slot = threadIdx.x / kPairs;
+    const Doc d = load_doc(docs, item / kColItems);
+    const int grp = item % kColItems;
+    const int lg_m = d.logp - kLogTile, M = 1 << lg_m, P = 1 << d.logp;
+    if (threadIdx.x < 2 * kColGroup) {
+        const int s = threadIdx.x % kColGroup;
+        const bool last = grp == kColItems - 1;
+        const int lo = last ? (s == 0 ? kTile / 2 : -1) : grp * kColGroup + s;
+        s_cols[threadIdx.x] = threadIdx.x < kColGroup ? lo : (lo < 0 ? -1 : (kTile - lo) & (kTile - 1));
+    }
+    __syncthreads();
+    const int64_t row0 = static_cast<int64_t>(pb) * long_points + d.off;
+    const int n_el = 2 * kColGroup * M;
+    for (int e = slot; e < n_el; e += kSlots) {  // e = j * 2R + s: adjacent columns adjacent
+        const int s = e % (2 * kColGroup), j = e / (2 * kColGroup);
+        const int c = s_cols[s];
+        s_c[s][j][q] = c < 0 ? make_float2(0.f, 0.f)
+                             : grid_load<HALF>(grid, (row0 + c + static_cast<int64_t>(kTile) * j) * kPairs + q);
+    }
+    __syncthreads();
+    const GlobalTw gtw{tw};
+    col_stages<false>(s_c, s_cols, lg_m, gtw, q, slot);
+    if constexpr (MODE == 1) {
+        for (int e = slot; e < n_el; e += kSlots) {
+            const int s = e % (2 * kColGroup), j = e / (2 * kColGroup);
+            const int c = s_cols[s];
+            if (c < 0 || (s >= kColGroup && c == s_cols[s - kColGroup])) continue;
+            const int f = c + kTile * j;
+            if (2 * f > P) continue;
+            const int sn = s < kColGroup ? s + kColGroup : s - kColGroup;
+            const int jn = c == 0 ? (M - j) & (M - 1) : M - 1 - j;
+            const float4 v = spectrum_entry(s_c[s][j][q], s_c[sn][jn][q], 0.5f / P);
+            spec[d.spec + (static_cast<int64_t>(pb) * (P / 2 + 1) + f) * kPairs + q] = v;
+        }
+        return;
+    } else {
+        constexpr int kPer = 2 * kColGroup * kMaxCols / kSlots;
+        float2 w[kPer];
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int e = slot + kSlots * k;
+            w[k] = make_float2(0.f, 0.f);
+            if (e >= n_el) continue;
+            const int s = e % (2 * kColGroup), j = e / (2 * kColGroup);
+            const int c = s_cols[s];
+            if (c < 0) continue;
+            const int f = c + kTile * j;
+            const int sn = s < kColGroup ? s + kColGroup : s - kColGroup;
+            const int jn = c == 0 ? (M - j) & (M - 1) : M - 1 - j;
+            const bool upper = 2 * f > P;
+            const int fi = upper ? P - f : f;
+            w[k] = spectral_product(s_c[s][j][q], s_c[sn][jn][q], spec,
+                                    d.spec + (static_cast<int64_t>(pb) * (P / 2 + 1) + fi) * kPairs + q,
+                                    upper);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int e = slot + kSlots * k;
+            if (e < n_el) s_c[e % (2 * kColGroup)][e / (2 * kColGroup)][q] = w[k];
+        }
+        __syncthreads();
+        col_stages<true>(s_c, s_cols, lg_m, gtw, q, slot);
+        for (int e = slot; e < n_el; e += kSlots) {
+            const int s = e % (2 * kColGroup), j = e / (2 * kColGroup);
+            const int c = s_cols[s];
+            if (c < 0 || (s >= kColGroup && c == s_cols[s - kColGroup])) continue;
+            grid_store<HALF>(grid, (row0 + c + static_cast<int64_t>(kTile) * j) * kPairs + q, s_c[s][j][q]);
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_short(int mode, const Doc* docs, const int32_t* tile_docs, int n_tiles,
+                        int64_t region_off, int a_dtype, const void* a, int N, int D, int npb,
+                        void* spec, int out_dtype, void* out, const float2* tw, hipStream_t stream) {
+    if (n_tiles == 0) return hipSuccess;
+    const dim3 grid(n_tiles, npb);
+    float4* sp = static_cast<float4*>(spec);
+    if (mode == 1) {
+        hipLaunchKernelGGL((short_kernel<1, 0, 0>), grid, dim3(kThreads), 0, stream, docs, tile_docs,
+                           region_off, a, N, D, sp, nullptr, tw);
+    } else if (a_dtype == 0 && out_dtype == 0) {
+        hipLaunchKernelGGL((short_kernel<0, 0, 0>), grid, dim3(kThreads), 0, stream, docs, tile_docs,
+                           region_off, a, N, D, sp, out, tw);
+    } else if (a_dtype == 1 && out_dtype == 1) {
+        hipLaunchKernelGGL((short_kernel<0, 1, 1>), grid, dim3(kThreads), 0, stream, docs, tile_docs,
+                           region_off, a, N, D, sp, out, tw);
+    } else if (a_dtype == 0) {
+        hipLaunchKernelGGL((short_kernel<0, 0, 1>), grid, dim3(kThreads), 0, stream, docs, tile_docs,
+                           region_off, a, N, D, sp, out, tw);
+    } else {
+        hipLaunchKernelGGL((short_kernel<0, 1, 0>), grid, dim3(kThreads), 0, stream, docs, tile_docs,
+                           region_off, a, N, D, sp, out, tw);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_front(const Doc* docs, const int32_t* tile_doc, int n_tiles, int a_dtype,
+                        const void* a, int N, int D, int npb, bool half, void* grid,
+                        int64_t long_points, const float2* tw, hipStream_t stream) {
+    if (n_tiles == 0) return hipSuccess;
+    const dim3 g(n_tiles, npb);
+    if (a_dtype == 0 && !half)
+        hipLaunchKernelGGL((front_kernel<0, false>), g, dim3(kThreads), 0, stream, docs, tile_doc, a, N, D,
+                           grid, long_points, tw);
+    else if (a_dtype == 0)
+        hipLaunchKernelGGL((front_kernel<0, true>), g, dim3(kThreads), 0, stream, docs, tile_doc, a, N, D,
+                           grid, long_points, tw);
+    else if (!half)
+        hipLaunchKernelGGL((front_kernel<1, false>), g, dim3(kThreads), 0, stream, docs, tile_doc, a, N, D,
+                           grid, long_points, tw);
+    else
+        hipLaunchKernelGGL((front_kernel<1, true>), g, dim3(kThreads), 0, stream, docs, tile_doc, a, N, D,
+                           grid, long_points, tw);
+    return hipGetLastError();
+}
+
+hipError_t launch_col(int mode, const Doc* docs, const int32_t* items, int n_items, bool half,
+                      void* grid, int64_t long_points, int npb, void* spec, const float2* tw,
+                      hipStream_t stream) {
+    if (n_items == 0) return hipSuccess;
+    const dim3 g(n_items, npb);
+    float4* sp = static_cast<float4*>(spec);
+    if (mode == 1 && !half)
+        hipLaunchKernelGGL((col_kernel<1, false>), g, dim3(kThreads), 0, stream, docs, items, grid,
+                           long_points, sp, tw);
+    else if (mode == 1)
+        hipLaunchKernelGGL((col_kernel<1, true>), g, dim3(kThreads), 0, stream, docs, items, grid,
+                           long_points, sp, tw);
+    else if (!half)
+        hipLaunchKernelGGL((col_kernel<0, false>), g, dim3(kThreads), 0, stream, docs, items, grid,
+                           long_points, sp, tw);
+    else
+        hipLaunchKernelGGL((col_kernel<0, true>), g, dim3(kThreads), 0, stream, docs, items, grid,
+                           long_points, sp, tw);
+    return hipGetLastError();
+}
+
+hipError_t launch_back(const Doc* docs, const int32_t* tile_doc, int n_tiles, bool half,
+                       const void* grid, int64_t long_points, int npb, int out_dtype, void* out,
+                       int N, int D, const float2* tw, hipStream_t stream) {
+    if (n_tiles == 0) return hipSuccess;
+    const dim3 g(n_tiles, npb);
+    if (out_dtype == 0 && !half)
+        hipLaunchKernelGGL((back_kernel<0, false>), g, dim3(kThreads), 0, stream, docs, tile_doc, grid,
+                           long_points, out, N, D, tw);
+    else if (out_dtype == 0)
+        hipLaunchKernelGGL((back_kernel<0, true>), g, dim3(kThreads), 0, stream, docs, tile_doc, grid,
+                           long_points, out, N, D, tw);
+    else if (!half)
+        hipLaunchKernelGGL((back_kernel<1, false>), g, dim3(kThreads), 0, stream, docs, tile_doc, grid,
+                           long_points, out, N, D, tw);
+    else
+        hipLaunchKernelGGL((back_kernel<1, true>), g, dim3(kThreads), 0, stream, docs, tile_doc, grid,
+                           long_points, out, N, D, tw);
+    return hipGetLastError();
+}
+
+}  // namespace rubiconv::ct
