@@ -45,6 +45,8 @@ def parse():
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the benchmark line: the forward step over channel counts D and "
                          "filter lengths L on the same document structure, one JSON line each")
+    ap.add_argument("--no-ct", action="store_true",
+                    help="skip the masked Cooley-Tukey variant's measurement")
     ap.add_argument("--no-backward", action="store_true",
                     help="skip the gradient measurement (dx and dk steps after the forward)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -128,6 +130,44 @@ def backward_measurement(rc, plan, W, x, k, spec, ws, stream, args):
            "dk_hbm_roofline_frac_step": round(dk_min / (dk_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
            "stages_us": {n: round(1e3 * tot / args.steps, 1) for n, (c, tot) in kt.items()}}
     del dk_ws, dx, dk, dy
+    return out
+
+
+def ct_measurement(rc, W, x, k, y, stream, four_step_ms, args):
+    """The masked Cooley-Tukey variant (Algorithm 2) on the same batch: its own plan,
+    then a step of the same scope (filter spectra + convolution), and the convolution
+    alone, with the padded transform size the power-of-two rule gives."""
+    import torch
+    dev = x.device
+    t0 = time.perf_counter()
+    try:
+        plan = rc.CTPlan(W.cu_seqlens, N=W.N, D=W.D, L=W.L, x_dtype=W.x_dtype, y_dtype=W.y_dtype)
+    except rc.RubiconvError as e:
+        return {"skipped": str(e)}
+    plan_ms = (time.perf_counter() - t0) * 1e3
+    ws = plan.new_workspace(dev)
+    spec = plan.new_spectrum(dev)
+    yc = torch.empty_like(y)
+
+    def launch(s):
+        rc.ct_filter_spectrum(plan, k, spectrum=spec, workspace=ws, stream=s)
+        rc.ct_packed_conv(plan, x, spec, y=yc, workspace=ws, stream=s)
+
+    def launch_conv(s):
+        rc.ct_packed_conv(plan, x, spec, y=yc, workspace=ws, stream=s)
+    ms = time_step(launch, stream, args.steps, args.warmup, args.eager)
+    conv_ms = time_step(launch_conv, stream, args.steps, args.warmup, args.eager)
+    t = plan.doc_table()
+    padded = int(t[:, 4].astype(np.int64).sum())
+    tok_ch = W.B * W.N * W.D
+    out = {"ms_per_step": round(ms, 4), "conv_ms": round(conv_ms, 4),
+           "value": round(tok_ch / (ms * 1e-3) / 1e6, 1), "unit": "Mtokens*channels/s",
+           "four_step_speedup": round(ms / four_step_ms, 3),
+           "padded_points_per_token": round(padded / (W.B * W.N), 3),
+           "spectrum_MB": round(plan.spectrum_bytes / 1e6, 1),
+           "workspace_MB": round(plan.workspace_bytes / 1e6, 1), "plan_ms": round(plan_ms, 3)}
+    plan.close()
+    del ws, spec, yc
     return out
 
 
@@ -404,6 +444,8 @@ def main():
     }
     if not args.no_backward:
         out["backward"] = backward_measurement(rc, plan, W, x, k, spec, ws, stream, args)
+    if not args.no_ct:
+        out["cooley_tukey"] = ct_measurement(rc, W, x, k, y, stream, ms, args)
     if args.layers > 0:
         out["stacked"] = stacked_measurement(rc, plan, W, x, stream, plan_ms, args)
     if not args.no_cpu_baseline:

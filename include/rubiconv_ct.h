@@ -54,7 +54,8 @@ rubiconv_status_t rubiconv_ct_plan(rubiconv_ct_plan_t* out, int B, int N, int D,
 void rubiconv_ct_plan_destroy(rubiconv_ct_plan_t plan);
 
 /* Bytes of the filter spectrum buffer: per power-of-two size present, the
- * non-negative half of the spectrum of every channel pair (complex fp32). */
+ * non-negative half of the spectrum of every channel pair (complex fp16 for
+ * bf16 x, complex fp32 otherwise). */
 size_t rubiconv_ct_spectrum_bytes(rubiconv_ct_plan_t plan);
 
 /* Bytes of device scratch rubiconv_ct_filter_spectrum and rubiconv_ct_packed_conv

@@ -138,7 +138,7 @@ rubiconv_status_t rubiconv_ct_plan(rubiconv_ct_plan_t* out, int B, int N, int D,
     }
     const CtHostPlan& h = pl->h;
     const size_t esz = h.grid_half ? 4 : 8;
-    pl->spec_bytes = std::max(kAlign, align_up(static_cast<size_t>(h.spec_entries) * 16));
+    pl->spec_bytes = std::max(kAlign, align_up(static_cast<size_t>(h.spec_entries) * (h.grid_half ? 8 : 16)));
     const size_t conv_ws = align_up(static_cast<size_t>(h.npb) * h.data.long_points * kPairs * esz);
     pl->taps_bytes = align_up(static_cast<size_t>(h.taps_max) * h.D * 4);
     const size_t filt_ws = pl->taps_bytes + align_up(static_cast<size_t>(h.npb) * h.filt.long_points * kPairs * 8);
@@ -179,10 +179,11 @@ rubiconv_status_t rubiconv_ct_filter_spectrum(rubiconv_ct_plan_t plan, const flo
                                        false, fgrid, h.filt.long_points, plan->tw, stream);
     if (e == hipSuccess)
         e = rubiconv::ct::launch_col(1, f.docs, f.col_items, f.n_items, false, fgrid, h.filt.long_points,
-                                     h.npb, spectrum, plan->tw, stream);
+                                     h.npb, h.grid_half, spectrum, plan->tw, stream);
     if (e == hipSuccess)
         e = rubiconv::ct::launch_short(1, f.docs, f.short_tile_docs, f.n_short_tiles, h.filt.long_points, 0,
-                                       taps, 0, h.D, h.npb, spectrum, 0, nullptr, plan->tw, stream);
+                                       taps, 0, h.D, h.npb, h.grid_half, spectrum, 0, nullptr, plan->tw,
+                                       stream);
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }
 
@@ -199,14 +200,14 @@ rubiconv_status_t rubiconv_ct_packed_conv(rubiconv_ct_plan_t plan, const void* x
     const DevLayout& d = plan->data;
     void* spec = const_cast<void*>(spectrum);  // read only by the convolution's kernels
     hipError_t e = rubiconv::ct::launch_short(0, d.docs, d.short_tile_docs, d.n_short_tiles,
-                                              h.data.long_points, h.x_dtype, x, h.N, h.D, h.npb, spec,
-                                              h.y_dtype, y, plan->tw, stream);
+                                              h.data.long_points, h.x_dtype, x, h.N, h.D, h.npb,
+                                              h.grid_half, spec, h.y_dtype, y, plan->tw, stream);
     if (e == hipSuccess)
         e = rubiconv::ct::launch_front(d.docs, d.long_tile_doc, d.n_long_tiles, h.x_dtype, x, h.N, h.D,
                                        h.npb, h.grid_half, workspace, h.data.long_points, plan->tw, stream);
     if (e == hipSuccess)
         e = rubiconv::ct::launch_col(0, d.docs, d.col_items, d.n_items, h.grid_half, workspace,
-                                     h.data.long_points, h.npb, spec, plan->tw, stream);
+                                     h.data.long_points, h.npb, h.grid_half, spec, plan->tw, stream);
     if (e == hipSuccess)
         e = rubiconv::ct::launch_back(d.docs, d.long_tile_doc, d.n_long_tiles, h.grid_half, workspace,
                                       h.data.long_points, h.npb, h.y_dtype, y, h.N, h.D, plan->tw, stream);

@@ -28,6 +28,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 #include "ct_kernels.hpp"
 #include "fft_core.hpp"
@@ -40,6 +41,7 @@ constexpr int kThreads = 256;
 constexpr int kSlots = kThreads / kPairs;      // 16 element slots per channel-pair lane
 constexpr int kTileGroups = kTile / 8;         // radix-8 groups of one tile
 constexpr int kMaxCols = 1 << kMaxLogCols;
+static_assert(kMaxCols <= kTile / 4, "a column work item needs at least one low column pair");
 
 __device__ __forceinline__ int bitrev(int v, int bits) {
     return bits == 0 ? 0 : static_cast<int>(__builtin_bitreverse32(static_cast<uint32_t>(v)) >> (32 - bits));
@@ -172,6 +174,7 @@ template <bool INV>
 __device__ __forceinline__ void tile_pass(float2 (*s_z)[kPairs], const uint8_t* s_lp, TileTw tw,
                                           int lg_h0, int q, int slot) {
     const int h0 = 1 << lg_h0;
+    #pragma unroll
     for (int g = slot; g < kTileGroups; g += kSlots) {
         const int base = group_base(g, lg_h0);
         float2 v[8];
@@ -190,38 +193,62 @@ __device__ __forceinline__ void tile_pass(float2 (*s_z)[kPairs], const uint8_t* 
 }
 
 // ---------------------------------------------------------------- short documents
-// W(f) for element f of a document of 2^lg points: Z(f) U(f) + conj(Z(-f)) V(f).
-__device__ __forceinline__ float2 spectral_product(float2 z, float2 zn, const float4* spec, int64_t e,
-                                                   bool upper) {
-    const float4 s = spec[e];
-    float2 u = make_float2(s.x, s.y), w = make_float2(s.z, s.w);
+// Spectrum entry e: (U, V) of one channel pair at one frequency, complex fp16 pairs
+// (8 bytes) or complex fp32 (16 bytes).  The entries hold (H_d + H_{d+1}) / 2 and
+// (H_d - H_{d+1}) / 2; the product applies the inverse transform's 1/P.
+template <bool SH>
+__device__ __forceinline__ void spec_load(const void* spec, int64_t e, float2& u, float2& v) {
+    if constexpr (SH) {
+        const uint2 w = static_cast<const uint2*>(spec)[e];
+        u = __half22float2(__builtin_bit_cast(__half2, w.x));
+        v = __half22float2(__builtin_bit_cast(__half2, w.y));
+    } else {
+        const float4 w = static_cast<const float4*>(spec)[e];
+        u = make_float2(w.x, w.y);
+        v = make_float2(w.z, w.w);
+    }
+}
+
+template <bool SH>
+__device__ __forceinline__ void spec_store(void* spec, int64_t e, float2 u, float2 v) {
+    if constexpr (SH) static_cast<uint2*>(spec)[e] = make_uint2(h2_bits(u.x, u.y), h2_bits(v.x, v.y));
+    else static_cast<float4*>(spec)[e] = make_float4(u.x, u.y, v.x, v.y);
+}
+
+// W(f) / P for element f: (Z(f) U(f) + conj(Z(-f)) V(f)) / P; entries above P/2 are
+// the conjugates of the stored entries at P - f (real filters).
+template <bool SH>
+__device__ __forceinline__ float2 spectral_product(float2 z, float2 zn, const void* spec, int64_t e,
+                                                   bool upper, float inv_p) {
+    float2 u, w;
+    spec_load<SH>(spec, e, u, w);
     if (upper) {
         u = cconj(u);
         w = cconj(w);
     }
-    return cadd(cmul(z, u), cmul(cconj(zn), w));
+    return cscale(cadd(cmul(z, u), cmul(cconj(zn), w)), inv_p);
 }
 
 // U and V of the spectrum from the transform Zk of the taps pair (k_d + i k_{d+1}).
-__device__ __forceinline__ float4 spectrum_entry(float2 z, float2 zn, float inv2p) {
+template <bool SH>
+__device__ __forceinline__ void spectrum_entry(void* spec, int64_t e, float2 z, float2 zn) {
     const float2 c = cconj(zn);
     const float2 hd = cscale(cadd(z, c), 0.5f);                   // H_d
     const float2 dd = csub(z, c);
     const float2 hd1 = make_float2(0.5f * dd.y, -0.5f * dd.x);     // H_{d+1} = (z - conj zn) / (2i)
-    const float2 u = cscale(cadd(hd, hd1), inv2p), v = cscale(csub(hd, hd1), inv2p);
-    return make_float4(u.x, u.y, v.x, v.y);
+    spec_store<SH>(spec, e, cscale(cadd(hd, hd1), 0.5f), cscale(csub(hd, hd1), 0.5f));
 }
 
-template <int MODE, int TA, int TO>
+template <int MODE, int TA, int TO, bool SH>
 __global__ __launch_bounds__(kThreads, 2) void short_kernel(
     const Doc* __restrict__ docs, const int32_t* __restrict__ tile_docs, int64_t region_off,
-    const void* __restrict__ a, int N, int D, float4* __restrict__ spec, void* __restrict__ out,
+    const void* __restrict__ a, int N, int D, void* __restrict__ spec, void* __restrict__ out,
     const float2* __restrict__ tw) {
     __shared__ float2 s_z[kTile][kPairs];
     __shared__ float2 s_tw[kTile / 2];
     __shared__ uint8_t s_lp[kTile];   // log2 of the point's document size (0: none)
     __shared__ int16_t s_doc[kTile];  // the point's document relative to d0 (-1: none)
-    const int tile = blockIdx.x, pb = blockIdx.y;
+    const int tile = blockIdx.y, pb = blockIdx.x;
     const int q = threadIdx.x & (kPairs - 1), slot = threadIdx.x / kPairs;
     const int p = pb * kPairs + q;
     const int d0 = tile_docs[2 * tile], d1 = tile_docs[2 * tile + 1];
@@ -248,6 +275,7 @@ __global__ __launch_bounds__(kThreads, 2) void short_kernel(
     __syncthreads();
     const TileTw ttw{s_tw};
     // forward stages 1-3, loading the bit-reversed samples straight from global memory
+    #pragma unroll
     for (int g = slot; g < kTileGroups; g += kSlots) {
         float2 v[8];
         int lp[8];
@@ -285,8 +313,8 @@ __global__ __launch_bounds__(kThreads, 2) void short_kernel(
             const int f = static_cast<int>(base + u - d.off);
             if (2 * f > P) continue;
             const int nf = (P - f) & (P - 1);
-            const float4 e = spectrum_entry(s_z[u][q], s_z[u - f + nf][q], 0.5f / P);
-            spec[d.spec + (static_cast<int64_t>(pb) * (P / 2 + 1) + f) * kPairs + q] = e;
+            spectrum_entry<SH>(spec, d.spec + (static_cast<int64_t>(pb) * (P / 2 + 1) + f) * kPairs + q,
+                               s_z[u][q], s_z[u - f + nf][q]);
         }
         return;
     } else {
@@ -303,9 +331,9 @@ __global__ __launch_bounds__(kThreads, 2) void short_kernel(
                 const int nf = (P - f) & (P - 1);
                 const bool upper = 2 * f > P;
                 const int fi = upper ? P - f : f;
-                w[k] = spectral_product(s_z[u][q], s_z[u - f + nf][q], spec,
-                                        d.spec + (static_cast<int64_t>(pb) * (P / 2 + 1) + fi) * kPairs + q,
-                                        upper);
+                w[k] = spectral_product<SH>(s_z[u][q], s_z[u - f + nf][q], spec,
+                                            d.spec + (static_cast<int64_t>(pb) * (P / 2 + 1) + fi) * kPairs + q,
+                                            upper, 1.0f / P);
             }
         }
         __syncthreads();
@@ -317,7 +345,8 @@ __global__ __launch_bounds__(kThreads, 2) void short_kernel(
         tile_pass<true>(s_z, s_lp, ttw, 3, q, slot);
         __syncthreads();
         // inverse stages 3-1, then every sample to its bit-reversed time in y
-        for (int g = slot; g < kTileGroups; g += kSlots) {
+        #pragma unroll
+    for (int g = slot; g < kTileGroups; g += kSlots) {
             float2 v[8];
             int lp[8];
 #pragma unroll
@@ -349,7 +378,7 @@ __global__ __launch_bounds__(kThreads, 2) void front_kernel(
     int N, int D, void* __restrict__ grid, int64_t long_points, const float2* __restrict__ tw) {
     __shared__ float2 s_z[kTile][kPairs];
     __shared__ float2 s_tw[kTile / 2];
-    const int tile = blockIdx.x, pb = blockIdx.y;
+    const int tile = blockIdx.y, pb = blockIdx.x;
     const int q = threadIdx.x & (kPairs - 1), slot = threadIdx.x / kPairs;
     const int p = pb * kPairs + q;
     const Doc d = load_doc(docs, tile_doc[tile]);
@@ -358,6 +387,7 @@ __global__ __launch_bounds__(kThreads, 2) void front_kernel(
     load_tile_twiddles(s_tw, tw);
     __syncthreads();
     const TileTw ttw{s_tw};
+    #pragma unroll
     for (int g = slot; g < kTileGroups; g += kSlots) {
         float2 v[8];
 #pragma unroll
@@ -373,6 +403,7 @@ __global__ __launch_bounds__(kThreads, 2) void front_kernel(
     tile_pass<false>(s_z, nullptr, ttw, 3, q, slot);
     __syncthreads();
     const int64_t row0 = static_cast<int64_t>(pb) * long_points + static_cast<int64_t>(tile) * kTile;
+    #pragma unroll
     for (int g = slot; g < kTileGroups; g += kSlots) {  // stages 7-9, stride 64, to the grid
         float2 v[8];
 #pragma unroll
@@ -389,7 +420,7 @@ __global__ __launch_bounds__(kThreads, 2) void back_kernel(
     int64_t long_points, void* __restrict__ out, int N, int D, const float2* __restrict__ tw) {
     __shared__ float2 s_z[kTile][kPairs];
     __shared__ float2 s_tw[kTile / 2];
-    const int tile = blockIdx.x, pb = blockIdx.y;
+    const int tile = blockIdx.y, pb = blockIdx.x;
     const int q = threadIdx.x & (kPairs - 1), slot = threadIdx.x / kPairs;
     const int p = pb * kPairs + q;
     const Doc d = load_doc(docs, tile_doc[tile]);
@@ -399,6 +430,7 @@ __global__ __launch_bounds__(kThreads, 2) void back_kernel(
     __syncthreads();
     const TileTw ttw{s_tw};
     const int64_t row0 = static_cast<int64_t>(pb) * long_points + static_cast<int64_t>(tile) * kTile;
+    #pragma unroll
     for (int g = slot; g < kTileGroups; g += kSlots) {  // inverse stages 9-7 from the grid
         float2 v[8];
 #pragma unroll
@@ -410,6 +442,7 @@ __global__ __launch_bounds__(kThreads, 2) void back_kernel(
     __syncthreads();
     tile_pass<true>(s_z, nullptr, ttw, 3, q, slot);
     __syncthreads();
+    #pragma unroll
     for (int g = slot; g < kTileGroups; g += kSlots) {  // inverse stages 3-1, to y
         float2 v[8];
 #pragma unroll
@@ -423,37 +456,39 @@ __global__ __launch_bounds__(kThreads, 2) void back_kernel(
     }
 }
 
-// Column pass over the columns l = c + kTile * j (j < M) of one long document: a
-// work item takes kColGroup low columns c = g * kColGroup + s and their partners
-// (kTile - c) mod kTile, which hold the frequencies -f of the low columns'
-// frequencies f = c + kTile * j; the last item takes column kTile / 2 alone.
+// Column pass over the columns l = c + kTile * j (j < M) of one long document.  A work
+// item holds kTile points of every pair lane: G = kTile / (2M) low columns
+// c = g * G + s (s < G) and, in the high slots, their partners kTile - c, which hold
+// the frequencies -f of the low columns' frequencies f = c + kTile * j.  Column 0 is
+// its own partner, so the high slot that would repeat it holds column kTile / 2,
+// also its own partner.  A document of M points per column has M work items.
+// LDS row of (slot, j): slot * M + j.
 template <int K, bool INV>
-__device__ __forceinline__ void col_pass(float2 (*s_c)[kMaxCols][kPairs], const int* cols, int lg_m,
-                                         int sigma0, GlobalTw tw, int q, int slot) {
+__device__ __forceinline__ void col_pass(float2 (*s_c)[kPairs], const int* cols, int lg_m, int sigma0,
+                                         GlobalTw tw, int q, int slot) {
     // stages sigma0 .. sigma0 + K - 1 (> kLogTile): element stride over j is 2^(sigma0 - kLogTile - 1)
     const int lg_hj = sigma0 - kLogTile - 1;
     const int hj = 1 << lg_hj;
-    const int per_col = (1 << lg_m) >> K;  // groups per column
-    for (int e = slot; e < 2 * kColGroup * per_col; e += kSlots) {
-        const int s = e / per_col, g = e - s * per_col;
-        if (cols[s] < 0) continue;
+    const int lg_per = lg_m - K;  // groups per column: M / 2^K
+    for (int e = slot; e < (kTile >> K); e += kSlots) {
+        const int s = e >> lg_per, g = e & ((1 << lg_per) - 1);
         const int jb = (g & (hj - 1)) + ((g >> lg_hj) << (lg_hj + K));
+        const int row = (s << lg_m) + jb;
         float2 v[1 << K];
 #pragma unroll
-        for (int i = 0; i < (1 << K); ++i) v[i] = s_c[s][jb + i * hj][q];
+        for (int i = 0; i < (1 << K); ++i) v[i] = s_c[row + i * hj][q];
         const int b0 = cols[s] + kTile * (jb & (hj - 1));
         if constexpr (INV) dif_group<K>(v, b0, kTile * hj, sigma0, tw, AllOn{});
         else dit_group<K>(v, b0, kTile * hj, sigma0, tw, AllOn{});
 #pragma unroll
-        for (int i = 0; i < (1 << K); ++i) s_c[s][jb + i * hj][q] = v[i];
+        for (int i = 0; i < (1 << K); ++i) s_c[row + i * hj][q] = v[i];
     }
 }
 
 // All stages of the column pass in one direction: passes of 3, then the remainder.
 template <bool INV>
-__device__ __forceinline__ void col_stages(float2 (*s_c)[kMaxCols][kPairs], const int* cols, int lg_m,
-                                           GlobalTw tw, int q, int slot) {
-    // forward order: stages kLogTile+1 ..; a pass of 3 at the low end, 3 next, remainder last
+__device__ __forceinline__ void col_stages(float2 (*s_c)[kPairs], const int* cols, int lg_m, GlobalTw tw,
+                                           int q, int slot) {
     const int n3 = lg_m / 3, rem = lg_m - 3 * n3;
     int sig[3], kk[3], n = 0;
     int s0 = kLogTile + 1;
@@ -468,109 +503,125 @@ __device__ __forceinline__ void col_stages(float2 (*s_c)[kMaxCols][kPairs], cons
     }
 }
 
-template <int MODE, bool HALF>
+template <int MODE, bool HALF, bool SH>
 __global__ __launch_bounds__(kThreads, 2) void col_kernel(
     const Doc* __restrict__ docs, const int32_t* __restrict__ items, void* __restrict__ grid,
-    int64_t long_points, float4* __restrict__ spec, const float2* __restrict__ tw) {
-    __shared__ float2 s_c[2 * kColGroup][kMaxCols][kPairs];
-    __shared__ int s_cols[2 * kColGroup];
-    const int item = items[blockIdx.x], pb = blockIdx.y;
+    int64_t long_points, void* __restrict__ spec, const float2* __restrict__ tw) {
+    __shared__ float2 s_c[kTile][kPairs];
+    __shared__ int s_cols[kTile / 2];  // column of each slot (2G <= kTile / 2 slots)
+    __shared__ int s_part[kTile / 2];  // slot holding the partner column
+    const int item = items[blockIdx.y], pb = blockIdx.x;
     const int q = threadIdx.x & (kPairs - 1), slot = threadIdx.x / kPairs;
-    const Doc d = load_doc(docs, item / kColItems);
-    const int grp = item % kColItems;
+    const Doc d = load_doc(docs, item >> kMaxLogCols);
+    const int grp = item & (kMaxCols - 1);
     const int lg_m = d.logp - kLogTile, M = 1 << lg_m, P = 1 << d.logp;
-    if (threadIdx.x < 2 * kColGroup) {
-        const int s = threadIdx.x % kColGroup;
-        const bool last = grp == kColItems - 1;
-        const int lo = last ? (s == 0 ? kTile / 2 : -1) : grp * kColGroup + s;
-        s_cols[threadIdx.x] = threadIdx.x < kColGroup ? lo : (lo < 0 ? -1 : (kTile - lo) & (kTile - 1));
+    const int lg_g = kLogTile - 1 - lg_m;  // G = kTile / (2M) low columns
+    const int G = 1 << lg_g;
+    if (threadIdx.x < 2 * G) {
+        const int s = threadIdx.x & (G - 1);
+        const int lo = grp * G + s;
+        const bool high = threadIdx.x >= G;
+        const int c = !high ? lo : (lo == 0 ? kTile / 2 : kTile - lo);
+        s_cols[threadIdx.x] = c;
+        s_part[threadIdx.x] = (c == 0 || c == kTile / 2) ? threadIdx.x : (high ? s : G + s);
     }
     __syncthreads();
     const int64_t row0 = static_cast<int64_t>(pb) * long_points + d.off;
-    const int n_el = 2 * kColGroup * M;
-    for (int e = slot; e < n_el; e += kSlots) {  // e = j * 2R + s: adjacent columns adjacent
-        const int s = e % (2 * kColGroup), j = e / (2 * kColGroup);
-        const int c = s_cols[s];
-        s_c[s][j][q] = c < 0 ? make_float2(0.f, 0.f)
-                             : grid_load<HALF>(grid, (row0 + c + static_cast<int64_t>(kTile) * j) * kPairs + q);
+    constexpr int kPer = kTile / kSlots;  // elements per thread
+    const int lg_2g = lg_g + 1;
+    {
+        float2 r[kPer];  // every load issued before the first LDS store
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {  // e = j * 2G + slot: adjacent columns adjacent
+            const int e = slot + kSlots * k;
+            const int s = e & ((2 << lg_g) - 1), j = e >> lg_2g;
+            r[k] = grid_load<HALF>(grid, (row0 + s_cols[s] + static_cast<int64_t>(kTile) * j) * kPairs + q);
+        }
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int e = slot + kSlots * k;
+            s_c[((e & ((2 << lg_g) - 1)) << lg_m) + (e >> lg_2g)][q] = r[k];
+        }
     }
     __syncthreads();
     const GlobalTw gtw{tw};
     col_stages<false>(s_c, s_cols, lg_m, gtw, q, slot);
     if constexpr (MODE == 1) {
-        for (int e = slot; e < n_el; e += kSlots) {
-            const int s = e % (2 * kColGroup), j = e / (2 * kColGroup);
+        for (int e = slot; e < kTile; e += kSlots) {
+            const int s = e & ((2 << lg_g) - 1), j = e >> lg_2g;
             const int c = s_cols[s];
-            if (c < 0 || (s >= kColGroup && c == s_cols[s - kColGroup])) continue;
             const int f = c + kTile * j;
             if (2 * f > P) continue;
-            const int sn = s < kColGroup ? s + kColGroup : s - kColGroup;
             const int jn = c == 0 ? (M - j) & (M - 1) : M - 1 - j;
-            const float4 v = spectrum_entry(s_c[s][j][q], s_c[sn][jn][q], 0.5f / P);
-            spec[d.spec + (static_cast<int64_t>(pb) * (P / 2 + 1) + f) * kPairs + q] = v;
+            spectrum_entry<SH>(spec, d.spec + (static_cast<int64_t>(pb) * (P / 2 + 1) + f) * kPairs + q,
+                               s_c[(s << lg_m) + j][q], s_c[(s_part[s] << lg_m) + jn][q]);
         }
         return;
     } else {
-        constexpr int kPer = 2 * kColGroup * kMaxCols / kSlots;
-        float2 w[kPer];
-#pragma unroll
-        for (int k = 0; k < kPer; ++k) {
-            const int e = slot + kSlots * k;
-            w[k] = make_float2(0.f, 0.f);
-            if (e >= n_el) continue;
-            const int s = e % (2 * kColGroup), j = e / (2 * kColGroup);
+        // each thread owns frequency pairs (f, -f) with f <= P/2: the elements j < M/2 of
+        // every slot, and f = P/2 in column 0; it reads both values and one spectrum entry
+        // and writes both products, so no other thread touches them
+        const float inv_p = 1.0f / P;
+        const int64_t sp0 = d.spec + static_cast<int64_t>(pb) * (P / 2 + 1) * kPairs + q;
+        auto product = [&](int s, int j) {
             const int c = s_cols[s];
-            if (c < 0) continue;
             const int f = c + kTile * j;
-            const int sn = s < kColGroup ? s + kColGroup : s - kColGroup;
             const int jn = c == 0 ? (M - j) & (M - 1) : M - 1 - j;
-            const bool upper = 2 * f > P;
-            const int fi = upper ? P - f : f;
-            w[k] = spectral_product(s_c[s][j][q], s_c[sn][jn][q], spec,
-                                    d.spec + (static_cast<int64_t>(pb) * (P / 2 + 1) + fi) * kPairs + q,
-                                    upper);
-        }
-        __syncthreads();
-#pragma unroll
-        for (int k = 0; k < kPer; ++k) {
-            const int e = slot + kSlots * k;
-            if (e < n_el) s_c[e % (2 * kColGroup)][e / (2 * kColGroup)][q] = w[k];
-        }
+            const int rf = (s << lg_m) + j, rn = (s_part[s] << lg_m) + jn;
+            float2 u, v;
+            spec_load<SH>(spec, sp0 + static_cast<int64_t>(f) * kPairs, u, v);
+            const float2 z = s_c[rf][q], zn = s_c[rn][q];
+            const float2 wn = cscale(cadd(cmul(zn, cconj(u)), cmul(cconj(z), cconj(v))), inv_p);
+            const float2 wf = cscale(cadd(cmul(z, u), cmul(cconj(zn), v)), inv_p);
+            s_c[rn][q] = wn;
+            s_c[rf][q] = wf;  // last: for f = -f both are the same element and value
+        };
+        for (int e = slot; e < kTile / 2; e += kSlots) product(e & ((2 << lg_g) - 1), e >> lg_2g);
+        if (grp == 0 && slot == 0) product(0, M / 2);
         __syncthreads();
         col_stages<true>(s_c, s_cols, lg_m, gtw, q, slot);
-        for (int e = slot; e < n_el; e += kSlots) {
-            const int s = e % (2 * kColGroup), j = e / (2 * kColGroup);
-            const int c = s_cols[s];
-            if (c < 0 || (s >= kColGroup && c == s_cols[s - kColGroup])) continue;
-            grid_store<HALF>(grid, (row0 + c + static_cast<int64_t>(kTile) * j) * kPairs + q, s_c[s][j][q]);
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int e = slot + kSlots * k;
+            const int s = e & ((2 << lg_g) - 1), j = e >> lg_2g;
+            grid_store<HALF>(grid, (row0 + s_cols[s] + static_cast<int64_t>(kTile) * j) * kPairs + q,
+                             s_c[(s << lg_m) + j][q]);
         }
     }
 }
 
 }  // namespace
 
+template <int V>
+using IC = std::integral_constant<int, V>;
+
+template <class F>
+void dispatch2(int v, F f) {  // v in {0, 1}
+    if (v) f(IC<1>{});
+    else f(IC<0>{});
+}
+
 hipError_t launch_short(int mode, const Doc* docs, const int32_t* tile_docs, int n_tiles,
                         int64_t region_off, int a_dtype, const void* a, int N, int D, int npb,
-                        void* spec, int out_dtype, void* out, const float2* tw, hipStream_t stream) {
+                        bool spec_half, void* spec, int out_dtype, void* out, const float2* tw,
+                        hipStream_t stream) {
     if (n_tiles == 0) return hipSuccess;
-    const dim3 grid(n_tiles, npb);
-    float4* sp = static_cast<float4*>(spec);
-    if (mode == 1) {
-        hipLaunchKernelGGL((short_kernel<1, 0, 0>), grid, dim3(kThreads), 0, stream, docs, tile_docs,
-                           region_off, a, N, D, sp, nullptr, tw);
-    } else if (a_dtype == 0 && out_dtype == 0) {
-        hipLaunchKernelGGL((short_kernel<0, 0, 0>), grid, dim3(kThreads), 0, stream, docs, tile_docs,
-                           region_off, a, N, D, sp, out, tw);
-    } else if (a_dtype == 1 && out_dtype == 1) {
-        hipLaunchKernelGGL((short_kernel<0, 1, 1>), grid, dim3(kThreads), 0, stream, docs, tile_docs,
-                           region_off, a, N, D, sp, out, tw);
-    } else if (a_dtype == 0) {
-        hipLaunchKernelGGL((short_kernel<0, 0, 1>), grid, dim3(kThreads), 0, stream, docs, tile_docs,
-                           region_off, a, N, D, sp, out, tw);
-    } else {
-        hipLaunchKernelGGL((short_kernel<0, 1, 0>), grid, dim3(kThreads), 0, stream, docs, tile_docs,
-                           region_off, a, N, D, sp, out, tw);
-    }
+    const dim3 grid(npb, n_tiles);  // pair blocks of one tile adjacent: whole token rows
+    dispatch2(spec_half, [&](auto sh) {
+        if (mode == 1) {
+            hipLaunchKernelGGL((short_kernel<1, 0, 0, decltype(sh)::value != 0>), grid, dim3(kThreads), 0,
+                               stream, docs, tile_docs, region_off, a, N, D, spec, nullptr, tw);
+            return;
+        }
+        dispatch2(a_dtype, [&](auto ta) {
+            dispatch2(out_dtype, [&](auto to) {
+                hipLaunchKernelGGL((short_kernel<0, decltype(ta)::value, decltype(to)::value,
+                                                 decltype(sh)::value != 0>),
+                                   grid, dim3(kThreads), 0, stream, docs, tile_docs, region_off, a, N, D,
+                                   spec, out, tw);
+            });
+        });
+    });
     return hipGetLastError();
 }
 
@@ -578,7 +629,7 @@ hipError_t launch_front(const Doc* docs, const int32_t* tile_doc, int n_tiles, i
                         const void* a, int N, int D, int npb, bool half, void* grid,
                         int64_t long_points, const float2* tw, hipStream_t stream) {
     if (n_tiles == 0) return hipSuccess;
-    const dim3 g(n_tiles, npb);
+    const dim3 g(npb, n_tiles);  // pair blocks of one tile adjacent: whole token rows
     if (a_dtype == 0 && !half)
         hipLaunchKernelGGL((front_kernel<0, false>), g, dim3(kThreads), 0, stream, docs, tile_doc, a, N, D,
                            grid, long_points, tw);
@@ -595,23 +646,19 @@ hipError_t launch_front(const Doc* docs, const int32_t* tile_doc, int n_tiles, i
 }
 
 hipError_t launch_col(int mode, const Doc* docs, const int32_t* items, int n_items, bool half,
-                      void* grid, int64_t long_points, int npb, void* spec, const float2* tw,
-                      hipStream_t stream) {
+                      void* grid, int64_t long_points, int npb, bool spec_half, void* spec,
+                      const float2* tw, hipStream_t stream) {
     if (n_items == 0) return hipSuccess;
-    const dim3 g(n_items, npb);
-    float4* sp = static_cast<float4*>(spec);
-    if (mode == 1 && !half)
-        hipLaunchKernelGGL((col_kernel<1, false>), g, dim3(kThreads), 0, stream, docs, items, grid,
-                           long_points, sp, tw);
-    else if (mode == 1)
-        hipLaunchKernelGGL((col_kernel<1, true>), g, dim3(kThreads), 0, stream, docs, items, grid,
-                           long_points, sp, tw);
-    else if (!half)
-        hipLaunchKernelGGL((col_kernel<0, false>), g, dim3(kThreads), 0, stream, docs, items, grid,
-                           long_points, sp, tw);
-    else
-        hipLaunchKernelGGL((col_kernel<0, true>), g, dim3(kThreads), 0, stream, docs, items, grid,
-                           long_points, sp, tw);
+    const dim3 g(npb, n_items);
+    dispatch2(mode, [&](auto md) {
+        dispatch2(half, [&](auto hf) {
+            dispatch2(spec_half, [&](auto sh) {
+                hipLaunchKernelGGL((col_kernel<decltype(md)::value, decltype(hf)::value != 0,
+                                               decltype(sh)::value != 0>),
+                                   g, dim3(kThreads), 0, stream, docs, items, grid, long_points, spec, tw);
+            });
+        });
+    });
     return hipGetLastError();
 }
 
@@ -619,7 +666,7 @@ hipError_t launch_back(const Doc* docs, const int32_t* tile_doc, int n_tiles, bo
                        const void* grid, int64_t long_points, int npb, int out_dtype, void* out,
                        int N, int D, const float2* tw, hipStream_t stream) {
     if (n_tiles == 0) return hipSuccess;
-    const dim3 g(n_tiles, npb);
+    const dim3 g(npb, n_tiles);  // pair blocks of one tile adjacent: whole token rows
     if (out_dtype == 0 && !half)
         hipLaunchKernelGGL((back_kernel<0, false>), g, dim3(kThreads), 0, stream, docs, tile_doc, grid,
                            long_points, out, N, D, tw);

@@ -38,14 +38,12 @@ void pack(std::vector<Doc> docs, const int64_t* class_spec, Layout* out) {
     for (int i = 0; i < out->n_long; ++i) {
         for (int64_t t = 0; t < (int64_t(1) << docs[i].logp) / kTile; ++t) out->long_tile_doc.push_back(i);
     }
-    // column items ordered group-major inside each size class, so that work items
-    // reading the same spectrum entries are dispatched together
-    for (int i = 0; i < out->n_long;) {
-        int j = i;
-        while (j < out->n_long && docs[j].logp == docs[i].logp) ++j;
-        for (int g = 0; g < kColItems; ++g)
-            for (int k = i; k < j; ++k) out->col_items.push_back(k * kColItems + g);
-        i = j;
+    // column items: M = P / kTile per document (each holds kTile points of every
+    // pair lane), document by document, so that the items reading adjacent columns
+    // of one document are dispatched together
+    for (int i = 0; i < out->n_long; ++i) {
+        const int M = 1 << (docs[i].logp - kLogTile);
+        for (int g = 0; g < M; ++g) out->col_items.push_back((i << kMaxLogCols) | g);
     }
     out->short_tile_docs.clear();
     const int64_t n_short_tiles = (out->points - out->long_points) / kTile;

@@ -19,15 +19,13 @@ constexpr int kTile = 1 << kLogTile;          // points one workgroup transforms
 constexpr int kMaxLogCols = 6;                // column pass: up to 64 points per column
 constexpr int kMaxLogP = kLogTile + kMaxLogCols;  // largest transform, 2^15 points
 constexpr int kPairs = 16;                    // channel pairs per block (32 channels)
-constexpr int kColGroup = 4;                  // column pass: low columns per work item
-constexpr int kColItems = kTile / (2 * kColGroup) + 1;  // column work items per long document
 
 // One transformed array of the flat layout: a document, or a filter size class.
 struct Doc {
     int32_t row, start, len;  // tokens [start, start + len) of row `row`
     int32_t logp;             // P = 2^logp
     int32_t off;              // first point in the flat layout (a multiple of P)
-    int32_t spec;             // first spectrum entry (16-byte units) of its size class
+    int32_t spec;             // first spectrum entry of its size class
     int32_t index;            // index inside its row (documents) / 0 (filter classes)
     int32_t pad;
 };
@@ -40,7 +38,7 @@ struct Layout {
     int64_t points = 0;                   // all points, the short region rounded up to a tile
     std::vector<int32_t> long_tile_doc;   // tile of the long region -> its document
     std::vector<int32_t> short_tile_docs; // tile of the short region -> first and end document
-    std::vector<int32_t> col_items;       // column work item -> document * kColItems + group
+    std::vector<int32_t> col_items;       // column work item -> document << kMaxLogCols | group
 };
 
 struct CtHostPlan {
