@@ -25,6 +25,12 @@ constexpr int kMaxDirect = 128;
 // short documents among long ones cost more on their own launch than they save).
 constexpr int kDefaultDirect = 64;
 constexpr int kDirectMinShare = 16;
+// Size-class merging: bytes moved per grid point and channel pair, in units of one
+// grid element.  A document's point costs five (column pass write, row pass read,
+// write and filter-class read, inverse column pass read); a filter class's point
+// costs one and a half (its column pass write and about half a point of taps read).
+constexpr int kDocPointCost = 10;
+constexpr int kClassPointCost = 3;
 
 struct Seg {
     int32_t row;       // source row of x (documents) / 0 (filter classes)

@@ -293,9 +293,45 @@ void build_partner_tables(int m, int n1, std::vector<uint32_t>* out) {
     out->insert(out->end(), t.begin(), t.end());
 }
 
+std::vector<int> merge_size_classes(const std::vector<int>& m0, int max_merge_m) {
+    std::map<int, int64_t> count;
+    for (int m : m0) ++count[m];
+    std::vector<int> u;
+    std::vector<int64_t> c;
+    for (const auto& kv : count) {
+        u.push_back(kv.first);
+        c.push_back(kv.second);
+    }
+    const int k = static_cast<int>(u.size());
+    // best[j]: cheapest cost of sizes u_0 .. u_{j-1}; first[j]: first size of the last group
+    std::vector<int64_t> best(k + 1, 0);
+    std::vector<int> first(k + 1, 0);
+    for (int j = 1; j <= k; ++j) {
+        const int64_t s = u[j - 1];
+        int64_t docs = 0;
+        best[j] = -1;
+        for (int i = j; i >= 1; --i) {
+            docs += c[i - 1];
+            if (i < j && s > max_merge_m) break;
+            const int64_t cost = best[i - 1] + kClassPointCost * s + kDocPointCost * s * docs;
+            if (best[j] < 0 || cost < best[j]) {
+                best[j] = cost;
+                first[j] = i;
+            }
+        }
+    }
+    std::map<int, int> to;
+    for (int j = k; j >= 1; j = first[j] - 1)
+        for (int i = first[j]; i <= j; ++i) to[u[i - 1]] = u[j - 1];
+    std::vector<int> out;
+    out.reserve(m0.size());
+    for (int m : m0) out.push_back(to[m]);
+    return out;
+}
+
 BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_docs,
                            const int32_t* cu, int x_dtype, int y_dtype, int n1, int direct_max,
-                           bool direct_by_share) {
+                           bool direct_by_share, bool merge_classes) {
     if (!out || !cu || B < 1 || N < 1 || D < 1 || L < 1 || max_docs < 1) return BuildError::kArg;
     if (x_dtype < 0 || x_dtype > 1 || y_dtype < 0 || y_dtype > 1) return BuildError::kArg;
     if (n1 == 0) n1 = 256;
@@ -370,9 +406,23 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
             p.doc_index.push_back(k);
             p.all_docs.push_back(s);
             p.all_index.push_back(k);
-            class_of_m[m] = 0;
         }
     }
+    if (merge_classes && p.docs.size() > 1) {
+        std::vector<int> m0;
+        for (const Seg& s : p.docs) m0.push_back(s.m);
+        // the column passes address a document with 32-bit offsets (as checked above)
+        const int max_merge_m = static_cast<int>(std::min<int64_t>(
+            kMaxM, (int64_t(1) << 30) / (static_cast<int64_t>(n1) * D * 4)));
+        const std::vector<int> m1 = merge_size_classes(m0, max_merge_m);
+        for (size_t i = 0; i < p.docs.size(); ++i) {
+            p.docs[i].m = m1[i];
+            p.docs[i].P = n1 * m1[i];
+        }
+        for (size_t i = 0, k = 0; i < p.all_docs.size(); ++i)
+            if (p.all_docs[i].P > 0) p.all_docs[i] = p.docs[k++];
+    }
+    for (const Seg& s : p.docs) class_of_m[s.m] = 0;
 
     if (!p.direct_docs.empty()) p.direct_taps = std::min(L, direct_max);
     // size classes, ascending m: twiddles, spectrum offsets, filter taps

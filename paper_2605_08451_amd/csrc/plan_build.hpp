@@ -68,8 +68,17 @@ void build_partner_tables(int m, int n1, std::vector<uint32_t>* out);
 // direct_max: documents of at most this many tokens take the direct path (0: none);
 // with direct_by_share they do so only when they would hold at least 1/kDirectMinShare
 // of the transform grid (plan.hpp).
+// merge_classes: documents may take a larger listed row size than their own when
+// that removes a filter class and saves bytes overall (merge_size_classes).
 BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_docs,
                            const int32_t* cu_seqlens, int x_dtype, int y_dtype, int n1,
-                           int direct_max, bool direct_by_share);
+                           int direct_max, bool direct_by_share, bool merge_classes);
+
+// Row sizes after class merging, one per entry of m0 (each a valid size for its
+// document).  Sizes u_1 < ... < u_k with document counts c_t; a class of size u_j
+// serving the sizes u_i..u_j costs kClassPointCost u_j + kDocPointCost u_j (c_i + ... + c_j),
+// and the cheapest split into consecutive groups is found by dynamic programming.
+// A size above max_merge_m never absorbs a smaller one.
+std::vector<int> merge_size_classes(const std::vector<int>& m0, int max_merge_m);
 
 }  // namespace rubiconv

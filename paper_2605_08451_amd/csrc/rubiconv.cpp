@@ -354,9 +354,18 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
         }
         direct_max = static_cast<int>(n);
     }
+    // RUBICONV_CLASS_MERGE = 0 keeps every document at its own smallest row size
+    bool merge = true;
+    if (const char* v = std::getenv("RUBICONV_CLASS_MERGE")) {
+        if (std::strcmp(v, "0") != 0 && std::strcmp(v, "1") != 0) {
+            delete pl;
+            return RUBICONV_ERR_ARG;
+        }
+        merge = v[0] == '1';
+    }
     BuildError be = rubiconv::build_host_plan(&pl->h, B, N, D, L, max_docs, cu_seqlens_host,
                                               static_cast<int>(x_dtype), static_cast<int>(y_dtype),
-                                              n1, direct_max, direct_by_share);
+                                              n1, direct_max, direct_by_share, merge);
     if (be != BuildError::kOk) {
         delete pl;
         if (be == BuildError::kArg) return RUBICONV_ERR_ARG;

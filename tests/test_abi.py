@@ -67,7 +67,8 @@ def _smooth(n):
 
 @pytest.mark.parametrize("i", range(5))
 @pytest.mark.parametrize("n1", [0, 64])
-def test_doc_table_matches_oracle_segments(i, n1):
+def test_doc_table_matches_oracle_segments(i, n1, monkeypatch):
+    monkeypatch.setenv("RUBICONV_CLASS_MERGE", "0")
     cu = wl.config_cu_seqlens(i)
     D, L, dt = wl.CONFIG_SHAPES[i]
     N = int(cu[0, -1])
@@ -100,6 +101,77 @@ def test_doc_table_matches_oracle_segments(i, n1):
     assert info["n_docs"] == len(ref) and info["tokens"] == cu.shape[0] * N
     assert info["grid_points"] == int(P.sum())
     assert info["n_classes"] == len(set(m.tolist()))
+
+
+def _own_sizes(plan_table, k):
+    """Each transform document's own row size (no class merging): the smallest listed
+    size (else 2^a 3^b 5^c number) whose N1 m reaches the causal padding."""
+    listed = listed_row_sizes()
+    out = []
+    for minimal in plan_table:
+        mm = -(-int(minimal) // k)
+        if mm <= listed[-1]:
+            out.append(min(s for s in listed if s >= mm))
+        else:
+            out.append(next(c for c in range(mm, 4 * mm) if _smooth(c)))
+    return out
+
+
+#: bytes per grid point and channel pair (in grid elements) of a document and of a
+#: filter class, the cost the plan's class merging minimises
+DOC_POINT, CLASS_POINT = 10, 3
+
+
+def _cost(ms):
+    return DOC_POINT * sum(ms) + CLASS_POINT * sum(set(ms))
+
+
+@pytest.mark.parametrize("i", range(5))
+def test_class_merging(i):
+    """With class merging (the default) every document keeps the segment of the oracle's
+    table, a transform at least as long as the causal padding asks, and a row size that
+    is some document's own size; the merged sizes cost no more than the unmerged ones, and
+    no other choice of classes costs less (every subset of the sizes, brute force)."""
+    import itertools
+    cu = wl.config_cu_seqlens(i)
+    D, L, dt = wl.CONFIG_SHAPES[i]
+    N = int(cu[0, -1])
+    ref = oracle.doc_table(cu, N, L, 256)
+    t = rc.Plan(cu, N=N, D=D, L=L, x_dtype=dt).doc_table()
+    np.testing.assert_array_equal(t[:, :4], ref[:, :4])
+    tr = t[:, 5] > 0
+    m = [int(v) for v in t[tr, 4]]
+    own = _own_sizes(ref[tr, 4], 256)
+    assert all(mi >= oi and mi in own for mi, oi in zip(m, own)), (m, own)
+    assert np.all(t[tr, 5] >= ref[tr, 4])
+    assert _cost(m) <= _cost(own)
+    sizes = sorted(set(own))
+    if len(sizes) <= 16:
+        best = None
+        for r in range(len(sizes)):
+            for sub in itertools.combinations(sizes[:-1], r):
+                cls = sorted(sub) + [sizes[-1]]
+                c = _cost([min(s for s in cls if s >= o) for o in own])
+                best = c if best is None else min(best, c)
+        assert _cost(m) == best
+
+
+def test_class_merging_switch(monkeypatch):
+    """RUBICONV_CLASS_MERGE = 0 keeps each document at its own size; anything but 0 or 1
+    is rejected when the plan is made."""
+    cu = wl.config_cu_seqlens(2)
+    D, L, dt = wl.CONFIG_SHAPES[2]
+    N = int(cu[0, -1])
+    ref = oracle.doc_table(cu, N, L, 256)
+    merged = rc.Plan(cu, N=N, D=D, L=L, x_dtype=dt).info()["n_classes"]
+    monkeypatch.setenv("RUBICONV_CLASS_MERGE", "0")
+    t = rc.Plan(cu, N=N, D=D, L=L, x_dtype=dt).doc_table()
+    assert [int(v) for v in t[:, 4]] == _own_sizes(ref[:, 4], 256)
+    assert merged < len(set(t[:, 4].tolist()))
+    monkeypatch.setenv("RUBICONV_CLASS_MERGE", "2")
+    with pytest.raises(rc.RubiconvError) as e:
+        rc.Plan(cu, N=N, D=D, L=L, x_dtype=dt)
+    assert e.value.status == 1
 
 
 def test_empty_documents_are_skipped():

@@ -183,7 +183,7 @@ def test_matrix_core_column_path(device, D, y_dtype):
 
 
 @pytest.mark.parametrize("D", [32, 40])
-def test_row_pass_every_block_count(device, D):
+def test_row_pass_every_block_count(device, D, monkeypatch):
     """bf16 inputs (complex fp16 grids): documents whose row DFT sizes cover every
     matrix-core block count (m <= 16, 17..32, ..., 113..128, at and next to the block
     edges) and the register-resident sizes above it (135, 160, 256).  A length of
@@ -194,6 +194,7 @@ def test_row_pass_every_block_count(device, D):
             [16384, 10368, 4608, 1408],
             [9216, 8192, 6400, 4096, 2048, 1920, 896]]
     W = wl.make_case(rows, D=D, L=32768, x_dtype="bf16", seed=D)
+    monkeypatch.setenv("RUBICONV_CLASS_MERGE", "0")   # every document at its own size
     y, plan = run_gpu(W, device)
     ms = sorted(set(int(m) for m in plan.doc_table()[:, 4]))
     assert ms == [3, 8, 12, 15, 16, 18, 32, 36, 50, 64, 72, 81, 96, 100, 128, 135, 160, 256], ms
@@ -201,13 +202,14 @@ def test_row_pass_every_block_count(device, D):
 
 
 @pytest.mark.parametrize("n1", [64, 256])
-def test_long_row_sizes_precision(device, n1):
+def test_long_row_sizes_precision(device, n1, monkeypatch):
     """Row sizes 33..128 (the partner-row matrix-core kernel), including the rows that
     are their own partners (u = 0 and u = N1 / 2), at a bar tighter than the parity
     tolerance: a wrong value in one grid row of a document shows up as an error of a
     few percent on a few positions, which the 2e-2 bar alone could miss.  Healthy
     errors here are about 2e-3 (bf16 output rounding plus fp16 grids)."""
     ks = (34, 40, 45, 54, 64, 90, 126)
+    monkeypatch.setenv("RUBICONV_CLASS_MERGE", "0")   # every document at its own size
     for short_filter in (True, False):
         # P >= len + min(len, L) - 1: about len for a 7-tap filter, 2 len for a full one
         lens = [n1 * (k - 1) + 3 if short_filter else n1 * k // 2 + 3 for k in ks]
