@@ -62,18 +62,20 @@ hipError_t launch_row_fast(int m, bool half, void* grid, int64_t grid_pb_stride,
                            int nlist, const float2* tw, int n1, int npb, int corr,
                            hipStream_t stream);
 
-// Matrix-core row pass (complex fp16 grids): the documents of `list` all have
-// ceil(m / 16) == nb (1 <= nb <= kMaxDenseBlocks); tabs = the plan's dense operand
-// tables, addressed through each document's Seg::dense_off.
+// Matrix-core row pass (complex fp16 grids) over `ngroups` groups, each a pair
+// (first, count) of consecutive entries of `docs` (indices into segs) that share one
+// size class and whose second-grid rows are those of the group's first document.
+// Every document has ceil(m / 16) == nb (1 <= nb <= kMaxDenseBlocks); tabs = the
+// plan's dense operand tables, addressed through Seg::dense_off.
 // 16-byte entries of one class's tables for the rows of 3 to 8 blocks: per direction
 // nb * nb real operands of 64 lanes, then 16 nb complex fp16 twiddles w^(-j) and
 // 16 nb complex fp32 twiddles w^j (w = exp(-2 pi i / m)), padded to whole 1 KB chunks.
 constexpr int partner_tab_u4(int nb) { return (2 * nb * nb * 64 + 12 * nb + 63) / 64 * 64; }
 
 hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const void* fgrid,
-                            int64_t fgrid_pb_stride, const Seg* segs, const int32_t* list,
-                            int nlist, const void* tabs, int n1, int npb, int corr,
-                            hipStream_t stream);
+                            int64_t fgrid_pb_stride, const Seg* segs, const int32_t* docs,
+                            const int32_t* groups, int ngroups, const void* tabs, int n1, int npb,
+                            int corr, hipStream_t stream);
 
 // Matrix-core column passes (N1 = 256, complex fp16 grids, D a multiple of 32).
 // `mtab` holds the MFMA operand tables in lane order (16-byte entries, offsets

@@ -31,6 +31,8 @@ constexpr int kDirectMinShare = 16;
 // costs one and a half (its column pass write and about half a point of taps read).
 constexpr int kDocPointCost = 10;
 constexpr int kClassPointCost = 3;
+// Documents of one size class that share a row task of the matrix-core row pass
+constexpr int kMaxGroupDocs = 4;
 
 struct Seg {
     int32_t row;       // source row of x (documents) / 0 (filter classes)

@@ -504,6 +504,33 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
                 if ((p.docs[d].m + 15) / 16 == nb) p.dense_docs.push_back(d);
             p.dense_count[nb] = static_cast<int32_t>(p.dense_docs.size()) - p.dense_list0[nb];
         }
+        // class groups: consecutive entries of one class (class_docs is in class order),
+        // split into near-equal groups of at most kMaxGroupDocs
+        for (int nb = 1; nb <= kMaxDenseBlocks; ++nb) {
+            p.dense_grp0[nb] = static_cast<int32_t>(p.dense_groups.size() / 2);
+            const int e0 = p.dense_list0[nb], e1 = e0 + p.dense_count[nb];
+            for (int a = e0; a < e1;) {
+                int b = a;
+                while (b < e1 && p.docs[p.dense_docs[b]].cls == p.docs[p.dense_docs[a]].cls) ++b;
+                const int n = b - a, ng = (n + kMaxGroupDocs - 1) / kMaxGroupDocs;
+                for (int g = 0, first = a; g < ng; ++g) {
+                    const int cnt = n / ng + (g < n % ng ? 1 : 0);
+                    p.dense_groups.push_back(first);
+                    p.dense_groups.push_back(cnt);
+                    first += cnt;
+                }
+                a = b;
+            }
+            p.dense_grp_n[nb] = static_cast<int32_t>(p.dense_groups.size() / 2) - p.dense_grp0[nb];
+        }
+        for (int nb = 1; nb <= kMaxDenseBlocks; ++nb) {
+            p.dense_dgrp0[nb] = static_cast<int32_t>(p.dense_groups.size() / 2);
+            for (int k = 0; k < p.dense_count[nb]; ++k) {
+                p.dense_groups.push_back(p.dense_list0[nb] + k);
+                p.dense_groups.push_back(1);
+            }
+            p.dense_dgrp_n[nb] = p.dense_count[nb];
+        }
     }
     *out = std::move(p);
     return BuildError::kOk;

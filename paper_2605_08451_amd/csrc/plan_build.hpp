@@ -42,6 +42,15 @@ struct HostPlan {
     std::vector<int32_t> dense_docs;    // documents grouped by 16-point block count nb = ceil(m / 16)
     int32_t dense_list0[kMaxDenseBlocks + 1] = {};  // first entry of block count nb in dense_docs
     int32_t dense_count[kMaxDenseBlocks + 1] = {};  // documents with block count nb
+    // row-task groups, pairs (first entry in dense_docs, documents): the documents of
+    // one size class, at most kMaxGroupDocs per group, share one load and transform of
+    // the class's filter rows; the one-document groups serve the filter gradient, whose
+    // second operand is each document's own grid
+    std::vector<int32_t> dense_groups;
+    int32_t dense_grp0[kMaxDenseBlocks + 1] = {};   // class groups of block count nb (pair index)
+    int32_t dense_grp_n[kMaxDenseBlocks + 1] = {};
+    int32_t dense_dgrp0[kMaxDenseBlocks + 1] = {};  // one-document groups of block count nb
+    int32_t dense_dgrp_n[kMaxDenseBlocks + 1] = {};
     int64_t grid_points = 0;            // sum over documents of P_i
     int64_t class_points = 0;           // sum over classes of P
     int32_t taps_max = 0;               // largest number of filter taps any class keeps

@@ -156,6 +156,10 @@ __device__ __forceinline__ void wave_lds_fence() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// s_waitcnt immediate that waits until at most n vector memory operations are
+// outstanding and leaves the other counters alone (vmcnt in bits 3:0 and 15:14)
+constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
 // 16 bytes per lane from buffer offset voffset (lane part) to LDS at lds + 16 * lane
 __device__ __forceinline__ void lds_copy16(__amdgpu_buffer_rsrc_t rs, int voffset, void* lds) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(lds), 16,
@@ -168,7 +172,8 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
                                                                const uint32_t* __restrict__ fgrid,
                                                                int64_t fgrid_pb_stride,
                                                                const Seg* __restrict__ segs,
-                                                               const int32_t* __restrict__ list,
+                                                               const int32_t* __restrict__ docs,
+                                                               const int2* __restrict__ groups,
                                                                const u4* __restrict__ tabs, int n1,
                                                                int corr) {
     constexpr int S = 16 * NB;                     // points per row, padded to whole blocks
@@ -183,12 +188,15 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
     const int p = lane & 15, h = lane >> 4;
     const int nu = n1 / 2 + 1;
     const int ug = (nu + kLdsWaves - 1) / kLdsWaves;
-    const Seg* sg = segs + list[blockIdx.x / ug];
+    // a group: documents of one size class, sharing the filter rows of the first
+    const int2 grp = groups[blockIdx.x / ug];
+    const Seg* sg = segs + docs[grp.x];
     const int u = (blockIdx.x % ug) * kLdsWaves + wave;
     const bool active = u < nu;  // wave-uniform
     const int m = sg->m;
     const int pb = blockIdx.y;
     uint32_t* stage = stage_all[wave];
+    const bool pad = (NB - 1) * 16 * 64 + lane * 16 >= m * 64;  // this lane's copy was out of range
 
     // the class's operand tables, 1 KB per wave instruction
     {
@@ -196,7 +204,7 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
         for (int c = wave; c < kTabU4 / 64; c += kLdsWaves) lds_copy16(rt, c * 1024 + lane * 16, &tab[c * 64]);
     }
     const int ub = (n1 - u) & (n1 - 1);
-    const RowBuffers rb = row_buffers(grid, grid_pb_stride, fgrid, fgrid_pb_stride, sg, pb, u, ub);
+    RowBuffers rb = row_buffers(grid, grid_pb_stride, fgrid, fgrid_pb_stride, sg, pb, u, ub);
     // the four rows [fu, fb, xu, xb] as [point][16 pairs], 16 points per instruction
     if (active) {
 #pragma unroll
@@ -209,7 +217,7 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
         }
     }
     __builtin_amdgcn_s_waitcnt(0);  // the copies above have landed in LDS
-    if (active && (NB - 1) * 16 * 64 + lane * 16 >= m * 64) {
+    if (active && pad) {
         // the copy of points >= m was out of range: make the padding zero
 #pragma unroll
         for (int r = 0; r < 4; ++r)
@@ -236,22 +244,17 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
     const int shift = u == 0 ? 1 : 0;
     uint32_t* xlds = stage + kPad * 16 + p;
     uint32_t* flds = stage + (2 * kPad + S) * 16 + p;
-#pragma unroll
-    for (int i = 0; i < kPad / 4; ++i) {
-        xlds[16 * (4 * i + h - kPad)] = 0u;
-        flds[16 * (4 * i + h - kPad)] = 0u;
-    }
     const u4* fwd = tab;
     const u4* inv = tab + 2 * NB * NB * 64;
+    const int rbase = m - 1 - 4 * h;
 
-    uint32_t au[NB][4], fa[NB][4];
-    uint32_t keep_x = 0u, keep_f = 0u;
+    // forward DFT of rows u and ub: own[kb][r] = frequency 16 kb + 4 h + r of row u;
+    // row ub's spectrum to the exchange row dst (slot 16 kb + 4 h + r - shift), and
+    // its frequency 0 returned for row 0's wrap
+    auto forward = [&](const u4* in_u, const u4* in_b, uint32_t(*own)[4], uint32_t* dst) {
 #pragma unroll
-    for (int phase = 0; phase < 2; ++phase) {
-        const u4* in_u = phase == 0 ? in.fu : in.xu;
-        const u4* in_b = phase == 0 ? in.fb : in.xb;
-        uint32_t(*own)[4] = phase == 0 ? fa : au;
-        uint32_t* dst = phase == 0 ? flds : xlds;
+        for (int i = 0; i < kPad / 4; ++i) dst[16 * (4 * i + h - kPad)] = 0u;
+        uint32_t keep = 0u;
 #pragma unroll
         for (int kb = 0; kb < NB; ++kb) {
             f4 acc[2][2];
@@ -271,78 +274,126 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
                 own[kb][r] = pack_h2(acc[0][0][r], acc[0][1][r]);
                 const uint32_t bv = pack_h2(acc[1][0][r], acc[1][1][r]);
                 dst[16 * (16 * kb + 4 * h + r - shift)] = bv;
-                if (kb == 0 && r == 0) (phase == 0 ? keep_f : keep_x) = bv;
+                if (kb == 0 && r == 0) keep = bv;
             }
         }
-    }
-    if (shift && h == 0) {  // row 0: point 0 is also its own partner's slot m - 1
-        flds[16 * (m - 1)] = keep_f;
-        xlds[16 * (m - 1)] = keep_x;
-    }
-    wave_lds_fence();
+        if (shift && h == 0) dst[16 * (m - 1)] = keep;  // row 0: point 0 is also slot m - 1
+        wave_lds_fence();
+    };
 
-    uint32_t wu[NB][4];
-    const int rbase = m - 1 - 4 * h;
+    // the filter rows, once per group: own spectrum in registers, and the partner
+    // values at the slots the product reads gathered from the exchange row
+    uint32_t fa[NB][4], fl[NB][4];
+    forward(in.fu, in.fb, fa, flds);
 #pragma unroll
     for (int kb = 0; kb < NB; ++kb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int slot = rbase - 16 * kb - r;  // >= -15: inside the zeroed front slots
-            const uint32_t b = xlds[16 * slot];
-            const uint32_t a = au[kb][r];
-            // correlation: the filter spectrum read at -f (its conjugate for real taps)
-            const uint32_t fl = flds[16 * slot];
-            const uint32_t A = corr ? fl : fa[kb][r];
-            const uint32_t bf = corr ? fa[kb][r] : fl;
-            const uint32_t e1 = pk_add_conj(a, b);
-            const uint32_t e2 = pk_swap_add_conj(a, b);
-            const uint32_t U = pk_add_neg_hi(e1, e2);
-            const uint32_t V = pk_add_neg_lo(e1, e2);
-            wu[kb][r] = w_pos(A, bf, U, V);
-            xlds[16 * slot] = w_neg(A, bf, U, V);
+        for (int r = 0; r < 4; ++r) fl[kb][r] = flds[16 * (rbase - 16 * kb - r)];
+    wave_lds_fence();  // the filter exchange row is free from here on
+
+    for (int k = 0;;) {
+        // the group's next document (if any): its two rows into LDS rows 2 and 3, which
+        // nothing else uses from here on, while this one is computed
+        {
+            const bool more = k + 1 < grp.y;
+            const RowBuffers nb_rb = row_buffers(grid, grid_pb_stride, fgrid, fgrid_pb_stride,
+                                                 segs + docs[grp.x + (more ? k + 1 : k)], pb, u, ub);
+            const __amdgpu_buffer_rsrc_t ndu = more ? nb_rb.du : row_buffer(nullptr, 0);
+            const __amdgpu_buffer_rsrc_t ndb = more ? nb_rb.db : row_buffer(nullptr, 0);
+#pragma unroll
+            for (int jb = 0; jb < NB; ++jb) {
+                const int off = jb * 1024 + lane * 16;
+                lds_copy16(ndu, off, stage + 2 * S * 16 + jb * 256);
+                lds_copy16(ndb, off, stage + 3 * S * 16 + jb * 256);
+            }
+            if (pad) {
+#pragma unroll
+                for (int r = 2; r < 4; ++r)
+                    *reinterpret_cast<u4*>(stage + r * S * 16 + (NB - 1) * 256 + lane * 4) = u4{0u, 0u, 0u, 0u};
+            }
+            __builtin_amdgcn_sched_barrier(0);  // the copies stay ahead of this document's stores
         }
-    if (shift && h == 0) xlds[-16] = xlds[16 * (m - 1)];
-    wave_lds_fence();
+        uint32_t au[NB][4];
+        forward(in.xu, in.xb, au, xlds);
 
-    u4 wb[NB];
+        uint32_t wu[NB][4];
 #pragma unroll
-    for (int jb = 0; jb < NB; ++jb)
+        for (int kb = 0; kb < NB; ++kb)
 #pragma unroll
-        for (int t = 0; t < 4; ++t) wb[jb][t] = xlds[16 * (16 * jb + 4 * h + t - shift)];
-    wave_lds_fence();
+            for (int r = 0; r < 4; ++r) {
+                const int slot = rbase - 16 * kb - r;  // >= -15: inside the zeroed front slots
+                const uint32_t b = xlds[16 * slot];
+                const uint32_t a = au[kb][r];
+                // correlation: the filter spectrum read at -f (its conjugate for real taps)
+                const uint32_t A = corr ? fl[kb][r] : fa[kb][r];
+                const uint32_t bf = corr ? fa[kb][r] : fl[kb][r];
+                const uint32_t e1 = pk_add_conj(a, b);
+                const uint32_t e2 = pk_swap_add_conj(a, b);
+                const uint32_t U = pk_add_neg_hi(e1, e2);
+                const uint32_t V = pk_add_neg_lo(e1, e2);
+                wu[kb][r] = w_pos(A, bf, U, V);
+                xlds[16 * slot] = w_neg(A, bf, U, V);
+            }
+        if (shift && h == 0) xlds[-16] = xlds[16 * (m - 1)];
+        wave_lds_fence();
 
-    // inverse DFT of both rows into LDS as [row][point][16 pairs], then 16-byte stores
-    uint32_t* out = stage;
+        u4 wb[NB];
 #pragma unroll
-    for (int kb = 0; kb < NB; ++kb) {
-        f4 acc[2][2];
+        for (int jb = 0; jb < NB; ++jb)
 #pragma unroll
-        for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+            for (int t = 0; t < 4; ++t) wb[jb][t] = xlds[16 * (16 * jb + 4 * h + t - shift)];
+        wave_lds_fence();
+
+        // inverse DFT of both rows into LDS rows 0 and 1 as [row][point][16 pairs],
+        // then 16-byte stores
+        uint32_t* out = stage;
+#pragma unroll
+        for (int kb = 0; kb < NB; ++kb) {
+            f4 acc[2][2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int jb = 0; jb < NB; ++jb) {
+                const u4 are = inv[((kb * NB + jb) * 2) * 64 + lane];
+                const u4 aim = inv[((kb * NB + jb) * 2 + 1) * 64 + lane];
+                const u4 win = {wu[jb][0], wu[jb][1], wu[jb][2], wu[jb][3]};
+                acc[0][0] = mma(are, win, acc[0][0]);
+                acc[0][1] = mma(aim, win, acc[0][1]);
+                acc[1][0] = mma(are, wb[jb], acc[1][0]);
+                acc[1][1] = mma(aim, wb[jb], acc[1][1]);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {  // output register r: time point 16 kb + 4 r + h
+                const int e = (16 * kb + 4 * r + h) * 16 + p;
+                out[e] = pack_h2(acc[0][0][r], acc[0][1][r]);
+                out[S * 16 + e] = pack_h2(acc[1][0][r], acc[1][1][r]);
+            }
+        }
+        wave_lds_fence();
 #pragma unroll
         for (int jb = 0; jb < NB; ++jb) {
-            const u4 are = inv[((kb * NB + jb) * 2) * 64 + lane];
-            const u4 aim = inv[((kb * NB + jb) * 2 + 1) * 64 + lane];
-            const u4 win = {wu[jb][0], wu[jb][1], wu[jb][2], wu[jb][3]};
-            acc[0][0] = mma(are, win, acc[0][0]);
-            acc[0][1] = mma(aim, win, acc[0][1]);
-            acc[1][0] = mma(are, wb[jb], acc[1][0]);
-            acc[1][1] = mma(aim, wb[jb], acc[1][1]);
+            const int off = jb * 1024 + lane * 16;
+            const u4 vu = *reinterpret_cast<const u4*>(out + jb * 256 + lane * 4);
+            const u4 vb = *reinterpret_cast<const u4*>(out + S * 16 + jb * 256 + lane * 4);
+            __builtin_amdgcn_raw_buffer_store_b128(vu, rb.du, off, 0, 2);
+            __builtin_amdgcn_raw_buffer_store_b128(vb, rb.db, off, 0, 2);
         }
+        if (++k == grp.y) break;
+
+        // the next document's rows: the copies were issued before this document's 2 NB
+        // stores, and the memory counter completes in order
+        rb = row_buffers(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs + docs[grp.x + k], pb, u, ub);
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * NB));
+        wave_lds_fence();
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {  // output register r: time point 16 kb + 4 r + h
-            const int e = (16 * kb + 4 * r + h) * 16 + p;
-            out[e] = pack_h2(acc[0][0][r], acc[0][1][r]);
-            out[S * 16 + e] = pack_h2(acc[1][0][r], acc[1][1][r]);
-        }
-    }
-    wave_lds_fence();
+        for (int jb = 0; jb < NB; ++jb)
 #pragma unroll
-    for (int jb = 0; jb < NB; ++jb) {
-        const int off = jb * 1024 + lane * 16;
-        const u4 vu = *reinterpret_cast<const u4*>(out + jb * 256 + lane * 4);
-        const u4 vb = *reinterpret_cast<const u4*>(out + S * 16 + jb * 256 + lane * 4);
-        __builtin_amdgcn_raw_buffer_store_b128(vu, rb.du, off, 0, 2);
-        __builtin_amdgcn_raw_buffer_store_b128(vb, rb.db, off, 0, 2);
+            for (int t = 0; t < 4; ++t) {
+                const int e = (16 * jb + 4 * t + h) * 16 + p;
+                in.xu[jb][t] = stage[2 * S * 16 + e];
+                in.xb[jb][t] = stage[3 * S * 16 + e];
+            }
+        wave_lds_fence();
     }
 }
 
@@ -367,7 +418,7 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
 constexpr int kPartnerWaves = 4;  // rows u of one document per workgroup
 
 template <int NB>
-constexpr int kPartnerMinWaves = NB <= 3 ? 4 : NB == 4 ? 3 : NB <= 6 ? 2 : 1;
+constexpr int kPartnerMinWaves = NB <= 2 ? 4 : NB <= 4 ? 3 : NB <= 6 ? 2 : 1;
 
 // -i a = (Im a, -Re a)
 __device__ __forceinline__ uint32_t mul_neg_i(uint32_t a) {
@@ -381,12 +432,13 @@ template <int NB>
 __global__ __launch_bounds__(64 * kPartnerWaves) __attribute__((amdgpu_waves_per_eu(kPartnerMinWaves<NB>, 8)))
 void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
                         const uint32_t* __restrict__ fgrid, int64_t fgrid_pb_stride,
-                        const Seg* __restrict__ segs, const int32_t* __restrict__ list,
-                        const u4* __restrict__ tabs, int n1, int corr) {
+                        const Seg* __restrict__ segs, const int32_t* __restrict__ docs,
+                        const int2* __restrict__ groups, const u4* __restrict__ tabs, int n1,
+                        int corr) {
     constexpr int S = 16 * NB;
     constexpr int kFrag = NB * NB * 64;            // u4 per direction
     constexpr int kTab = partner_tab_u4(NB);
-    constexpr bool kPrefetch = NB <= 4;            // data rows loaded with the filter rows
+    constexpr bool kPrefetch = NB <= 4;            // first data rows loaded with the filter rows
     __shared__ u4 tab[kTab];
 
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
@@ -394,31 +446,33 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
     const int p = lane & 15, h = lane >> 4;
     const int nu = n1 / 2 + 1;
     const int ug = (nu + kPartnerWaves - 1) / kPartnerWaves;
-    const Seg* sg = segs + list[blockIdx.x / ug];
+    // a group: documents of one size class, sharing the filter rows of the first
+    const int2 grp = groups[blockIdx.x / ug];
+    const Seg* sg = segs + docs[grp.x];
     const int u = (blockIdx.x % ug) * kPartnerWaves + wave;
     const bool active = u < nu;                    // wave-uniform
     const bool self = u == 0 || 2 * u == n1;       // its own partner row
     const int ub = self ? u : n1 - u;
     const int pb = blockIdx.y;
-    const RowBuffers rb = row_buffers(grid, grid_pb_stride, fgrid, fgrid_pb_stride, sg, pb, u, ub);
+    RowBuffers rb = row_buffers(grid, grid_pb_stride, fgrid, fgrid_pb_stride, sg, pb, u, ub);
 
     // register t of lane (p, h) holds point 16 jb + 4 t + h of pair p: one load covers
     // four neighbouring points, 256 contiguous bytes
     const int lane_off = (h * 16 + p) * 4;
     u4 fu[NB], fb[NB], xu[NB], xb[NB];
-    if (active) {
+    auto load_rows = [&](__amdgpu_buffer_rsrc_t ru, __amdgpu_buffer_rsrc_t rbb, u4* du, u4* db) {
 #pragma unroll
         for (int jb = 0; jb < NB; ++jb)
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
                 const int off = lane_off + (16 * jb + 4 * t) * 64;
-                fu[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rb.fu, off, 0, 2);
-                fb[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rb.fb, off, 0, 2);
-                if constexpr (kPrefetch) {
-                    xu[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rb.du, off, 0, 2);
-                    xb[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rb.db, off, 0, 2);
-                }
+                du[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(ru, off, 0, 2);
+                db[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rbb, off, 0, 2);
             }
+    };
+    if (active) {
+        load_rows(rb.fu, rb.fb, fu, fb);
+        if constexpr (kPrefetch) load_rows(rb.du, rb.db, xu, xb);
     }
     {  // the class's tables, 1 KB per wave instruction
         const __amdgpu_buffer_rsrc_t rt = row_buffer(tabs + sg->dense_off, kTab * 16);
@@ -433,31 +487,18 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
     // rows u > 0 pair v with m - 1 - v and take the twiddle, row 0 pairs v with (m - v) mod m
     const int pre_mask = u != 0 ? -1 : 0;
 
-    // forward DFT of the filter rows, then of the data rows: own[kb][r] and par[kb][r]
-    // hold frequency v = 16 kb + 4 h + r of row u and the partner value of row ub
-    uint32_t fa[NB][4], fp[NB][4], au[NB][4], ap[NB][4];
-#pragma unroll
-    for (int phase = 0; phase < 2; ++phase) {
-        if (phase == 1 && !kPrefetch) {
-#pragma unroll
-            for (int jb = 0; jb < NB; ++jb)
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const int off = lane_off + (16 * jb + 4 * t) * 64;
-                    xu[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rb.du, off, 0, 2);
-                    xb[jb][t] = __builtin_amdgcn_raw_buffer_load_b32(rb.db, off, 0, 2);
-                }
-        }
-        u4* in_u = phase == 0 ? fu : xu;
-        u4* in_b = phase == 0 ? fb : xb;
-        uint32_t(*own)[4] = phase == 0 ? fa : au;
-        uint32_t(*par)[4] = phase == 0 ? fp : ap;
+    // forward DFT of rows u and ub: own[kb][r] and par[kb][r] hold frequency
+    // v = 16 kb + 4 h + r of row u and the partner value of row ub
+    // lk: the lane index through an empty asm statement, so that table reads indexed by
+    // it are issued where they are used rather than hoisted out of the document loop
+    // (which would hold every operand fragment in registers across the loop)
+    auto forward = [&](u4* in_u, u4* in_b, uint32_t(*own)[4], uint32_t(*par)[4], int lk) {
         // partner input conj(z(j) w^(-j)); row 0 reads entry 0, w^0 = 1, for every j
 #pragma unroll
         for (int jb = 0; jb < NB; ++jb)
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
-                const uint32_t tw = tw_pre[(16 * jb + 4 * t + h) & pre_mask];
+                const uint32_t tw = tw_pre[(16 * jb + 4 * t + (lk >> 4)) & pre_mask];
                 in_b[jb][t] = cmul_h2(in_b[jb][t], tw) ^ 0x80000000u;
             }
 #pragma unroll
@@ -467,7 +508,7 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
             for (int i = 0; i < 4; ++i) acc[i] = f4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
             for (int jb = 0; jb < NB; ++jb) {
-                const u4 a = tab[(kb * NB + jb) * 64 + lane];
+                const u4 a = tab[(kb * NB + jb) * 64 + lk];
                 acc[0] = mma(a, in_u[jb], acc[0]);
                 acc[1] = mma(a, mul_neg_i4(in_u[jb]), acc[1]);
                 acc[2] = mma(a, in_b[jb], acc[2]);
@@ -480,102 +521,118 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
             }
         }
         __builtin_amdgcn_sched_barrier(0);
-    }
+    };
 
-    // separated products: W(f) for row u, W(-f) for row ub at the slot of f
-    uint32_t wu[NB][4], wp[NB][4];
-#pragma unroll
-    for (int kb = 0; kb < NB; ++kb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const uint32_t a = au[kb][r], b = ap[kb][r];
-            // correlation: the filter spectrum read at -f (its conjugate for real taps)
-            const uint32_t A = corr ? fp[kb][r] : fa[kb][r];
-            const uint32_t Bf = corr ? fa[kb][r] : fp[kb][r];
-            const uint32_t e1 = pk_add_conj(a, b);       // s
-            const uint32_t e2 = pk_swap_add_conj(a, b);  // (Im d, Re d)
-            const uint32_t U = pk_add_neg_hi(e1, e2);    // s - i d
-            const uint32_t V = pk_add_neg_lo(e1, e2);    // s + i d
-            wu[kb][r] = w_pos(A, Bf, U, V);
-            wp[kb][r] = w_neg(A, Bf, U, V) ^ 0x80000000u;  // conj(G), the inverse's input
-        }
+    // the filter rows, once per group
+    uint32_t fa[NB][4], fp[NB][4];
+    forward(fu, fb, fa, fp, lane);
 
-    // inverse DFT of row u and of row ub.  A row that is its own partner stores only
-    // the first: the second goes through a buffer resource of no bytes.  The code
-    // has no branch between the matrix products and the reads of their results, so
-    // the compiler's wait states after the products hold on every path.
     const u4* inv = tab + kFrag;
-    const __amdgpu_buffer_rsrc_t rdb = self ? row_buffer(nullptr, 0) : rb.db;
+    for (int k = 0;;) {
+        if (!kPrefetch || k > 0) load_rows(rb.du, rb.db, xu, xb);
+        int lk = lane;
+        asm volatile("" : "+v"(lk));
+        uint32_t au[NB][4], ap[NB][4];
+        forward(xu, xb, au, ap, lk);
+
+        // separated products: W(f) for row u, W(-f) for row ub at the slot of f
+        uint32_t wu[NB][4], wp[NB][4];
 #pragma unroll
-    for (int kb = 0; kb < NB; ++kb) {
-        f4 acc[4];
+        for (int kb = 0; kb < NB; ++kb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc[i] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+            for (int r = 0; r < 4; ++r) {
+                const uint32_t a = au[kb][r], b = ap[kb][r];
+                // correlation: the filter spectrum read at -f (its conjugate for real taps)
+                const uint32_t A = corr ? fp[kb][r] : fa[kb][r];
+                const uint32_t Bf = corr ? fa[kb][r] : fp[kb][r];
+                const uint32_t e1 = pk_add_conj(a, b);       // s
+                const uint32_t e2 = pk_swap_add_conj(a, b);  // (Im d, Re d)
+                const uint32_t U = pk_add_neg_hi(e1, e2);    // s - i d
+                const uint32_t V = pk_add_neg_lo(e1, e2);    // s + i d
+                wu[kb][r] = w_pos(A, Bf, U, V);
+                wp[kb][r] = w_neg(A, Bf, U, V) ^ 0x80000000u;  // conj(G), the inverse's input
+            }
+
+        // inverse DFT of row u and of row ub.  A row that is its own partner stores only
+        // the first: the second goes through a buffer resource of no bytes.  The code
+        // has no branch between the matrix products and the reads of their results, so
+        // the compiler's wait states after the products hold on every path.
+        const __amdgpu_buffer_rsrc_t rdb = self ? row_buffer(nullptr, 0) : rb.db;
 #pragma unroll
-        for (int jb = 0; jb < NB; ++jb) {
-            const u4 a = inv[(kb * NB + jb) * 64 + lane];
-            const u4 bu = {wu[jb][0], wu[jb][1], wu[jb][2], wu[jb][3]};
-            const u4 bp = {wp[jb][0], wp[jb][1], wp[jb][2], wp[jb][3]};
-            acc[0] = mma(a, bu, acc[0]);
-            acc[1] = mma(a, mul_neg_i4(bu), acc[1]);
-            acc[2] = mma(a, bp, acc[2]);
-            acc[3] = mma(a, mul_neg_i4(bp), acc[3]);
+        for (int kb = 0; kb < NB; ++kb) {
+            f4 acc[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[i] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int jb = 0; jb < NB; ++jb) {
+                const u4 a = inv[(kb * NB + jb) * 64 + lk];
+                const u4 bu = {wu[jb][0], wu[jb][1], wu[jb][2], wu[jb][3]};
+                const u4 bp = {wp[jb][0], wp[jb][1], wp[jb][2], wp[jb][3]};
+                acc[0] = mma(a, bu, acc[0]);
+                acc[1] = mma(a, mul_neg_i4(bu), acc[1]);
+                acc[2] = mma(a, bp, acc[2]);
+                acc[3] = mma(a, mul_neg_i4(bp), acc[3]);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {  // output register r: time point j = 16 kb + 4 r + h
+                const int off = lane_off + (16 * kb + 4 * r) * 64;
+                __builtin_amdgcn_raw_buffer_store_b32(pack_h2(acc[0][r], acc[1][r]), rb.du, off, 0, 2);
+                // w^j conj(R + i I) with w^j = (c, s): (R c + I s, R s - I c)
+                const float2 w = tw_post[16 * kb + 4 * r + (lk >> 4)];
+                const float re = acc[2][r] * w.x + acc[3][r] * w.y;
+                const float im = acc[2][r] * w.y - acc[3][r] * w.x;
+                __builtin_amdgcn_raw_buffer_store_b32(pack_h2(re, im), rdb, off, 0, 2);
+            }
         }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {  // output register r: time point j = 16 kb + 4 r + h
-            const int off = lane_off + (16 * kb + 4 * r) * 64;
-            __builtin_amdgcn_raw_buffer_store_b32(pack_h2(acc[0][r], acc[1][r]), rb.du, off, 0, 2);
-            // w^j conj(R + i I) with w^j = (c, s): (R c + I s, R s - I c)
-            const float2 w = tw_post[16 * kb + 4 * r + h];
-            const float re = acc[2][r] * w.x + acc[3][r] * w.y;
-            const float im = acc[2][r] * w.y - acc[3][r] * w.x;
-            __builtin_amdgcn_raw_buffer_store_b32(pack_h2(re, im), rdb, off, 0, 2);
-        }
+        if (++k == grp.y) break;
+        rb = row_buffers(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs + docs[grp.x + k], pb, u, ub);
     }
 }
 
 template <int NB>
 hipError_t launch_lds_nb(void* grid, int64_t gs, const void* fgrid, int64_t fs, const Seg* segs,
-                         const int32_t* list, int nlist, const void* tabs, int n1, int npb,
-                         int corr, hipStream_t stream) {
+                         const int32_t* docs, const int32_t* groups, int ngroups, const void* tabs,
+                         int n1, int npb, int corr, hipStream_t stream) {
     const int ug = (n1 / 2 + 1 + kLdsWaves - 1) / kLdsWaves;
-    const dim3 g(nlist * ug, npb), b(64 * kLdsWaves);
+    const dim3 g(ngroups * ug, npb), b(64 * kLdsWaves);
     hipLaunchKernelGGL((row_lds_kernel<NB>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
-                       static_cast<const uint32_t*>(fgrid), fs, segs, list,
-                       static_cast<const u4*>(tabs), n1, corr);
+                       static_cast<const uint32_t*>(fgrid), fs, segs, docs,
+                       reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr);
     return hipGetLastError();
 }
 
 template <int NB>
 hipError_t launch_partner_nb(void* grid, int64_t gs, const void* fgrid, int64_t fs, const Seg* segs,
-                             const int32_t* list, int nlist, const void* tabs, int n1, int npb,
-                             int corr, hipStream_t stream) {
+                             const int32_t* docs, const int32_t* groups, int ngroups,
+                             const void* tabs, int n1, int npb, int corr, hipStream_t stream) {
     const int ug = (n1 / 2 + 1 + kPartnerWaves - 1) / kPartnerWaves;
-    const dim3 g(nlist * ug, npb), b(64 * kPartnerWaves);
+    const dim3 g(ngroups * ug, npb), b(64 * kPartnerWaves);
     hipLaunchKernelGGL((row_partner_kernel<NB>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
-                       static_cast<const uint32_t*>(fgrid), fs, segs, list,
-                       static_cast<const u4*>(tabs), n1, corr);
+                       static_cast<const uint32_t*>(fgrid), fs, segs, docs,
+                       reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr);
     return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const void* fgrid,
-                            int64_t fgrid_pb_stride, const Seg* segs, const int32_t* list,
-                            int nlist, const void* tabs, int n1, int npb, int corr,
-                            hipStream_t stream) {
-    if (nlist == 0) return hipSuccess;
+                            int64_t fgrid_pb_stride, const Seg* segs, const int32_t* docs,
+                            const int32_t* groups, int ngroups, const void* tabs, int n1, int npb,
+                            int corr, hipStream_t stream) {
+    if (ngroups == 0) return hipSuccess;
+#define RUBICONV_ARGS grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, docs, groups, ngroups, tabs, n1, npb, corr, stream
     switch (nb) {
-        case 1: return launch_lds_nb<1>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, corr, stream);
-        case 2: return launch_lds_nb<2>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, corr, stream);
-        case 3: return launch_partner_nb<3>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, corr, stream);
-        case 4: return launch_partner_nb<4>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, corr, stream);
-        case 5: return launch_partner_nb<5>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, corr, stream);
-        case 6: return launch_partner_nb<6>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, corr, stream);
-        case 7: return launch_partner_nb<7>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, corr, stream);
-        case 8: return launch_partner_nb<8>(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, list, nlist, tabs, n1, npb, corr, stream);
+        case 1: return launch_lds_nb<1>(RUBICONV_ARGS);
+        case 2: return launch_lds_nb<2>(RUBICONV_ARGS);
+        case 3: return launch_partner_nb<3>(RUBICONV_ARGS);
+        case 4: return launch_partner_nb<4>(RUBICONV_ARGS);
+        case 5: return launch_partner_nb<5>(RUBICONV_ARGS);
+        case 6: return launch_partner_nb<6>(RUBICONV_ARGS);
+        case 7: return launch_partner_nb<7>(RUBICONV_ARGS);
+        case 8: return launch_partner_nb<8>(RUBICONV_ARGS);
         default: return hipErrorInvalidValue;
     }
+#undef RUBICONV_ARGS
 }
 
 }  // namespace rubiconv

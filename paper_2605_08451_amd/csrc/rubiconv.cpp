@@ -32,6 +32,7 @@ struct rubiconv_plan_s {
     const void* mfma_tab = nullptr;  // matrix-core operand tables (inside dev)
     const void* dense_tab = nullptr; // matrix-core row pass operands (inside dev)
     const int32_t* dense_docs = nullptr;  // documents by 16-point block count (inside dev)
+    const int32_t* dense_groups = nullptr;  // row-task groups of dense_docs (inside dev)
     bool device_ready = false;
     LaunchTables doc_t{};
     LaunchTables cls_t{};
@@ -86,6 +87,7 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     const size_t o_mt = off;         off = align_up(off + h.mfma_tab.size() * 4);
     const size_t o_dt = off;         off = align_up(off + h.dense_tab.size() * 4);
     const size_t o_dd = off;         off = align_up(off + h.dense_docs.size() * 4);
+    const size_t o_dg = off;         off = align_up(off + h.dense_groups.size() * 4);
     const size_t total = off;
 
     std::vector<unsigned char> img(total, 0);
@@ -115,6 +117,8 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     if (!h.mfma_tab.empty()) std::memcpy(img.data() + o_mt, h.mfma_tab.data(), h.mfma_tab.size() * 4);
     if (!h.dense_tab.empty()) std::memcpy(img.data() + o_dt, h.dense_tab.data(), h.dense_tab.size() * 4);
     if (!h.dense_docs.empty()) std::memcpy(img.data() + o_dd, h.dense_docs.data(), h.dense_docs.size() * 4);
+    if (!h.dense_groups.empty())
+        std::memcpy(img.data() + o_dg, h.dense_groups.data(), h.dense_groups.size() * 4);
 
     int count = 0;
     hipError_t e = hipGetDeviceCount(&count);
@@ -150,6 +154,7 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     pl->mfma_tab = base + o_mt;
     pl->dense_tab = base + o_dt;
     pl->dense_docs = reinterpret_cast<const int32_t*>(base + o_dd);
+    pl->dense_groups = reinterpret_cast<const int32_t*>(base + o_dg);
     if (hipEventCreateWithFlags(&pl->fork, hipEventDisableTiming) != hipSuccess ||
         hipEventCreateWithFlags(&pl->direct_done, hipEventDisableTiming) != hipSuccess)
         return RUBICONV_ERR_HIP;
@@ -242,10 +247,12 @@ std::string stage(const char* tag, const char* name) { return std::string(tag) +
 // `fgrid`, whose rows for each document are located by the spec_off of the segment
 // table `t` (the filter class grids, or a document grid of the same plan); the
 // product with F(f) (corr = 0) or F(-f) (corr = 1); the inverse passes into `out`
-// (dtype out_dtype).  The caller holds the plan's launch mutex.
+// (dtype out_dtype).  own_rows: every document's second grid rows are its own (the
+// filter gradient), so the matrix-core row pass takes one document per task instead
+// of groups of a size class.  The caller holds the plan's launch mutex.
 hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, const void* fgrid,
                         int64_t fgrid_pb_stride, const LaunchTables& t, void* out, int out_dtype,
-                        void* grid, int corr, const char* tag, hipStream_t stream,
+                        void* grid, int corr, bool own_rows, const char* tag, hipStream_t stream,
                         StageRecorder& rec) {
     const HostPlan& h = plan->h;
     const int n_cols = static_cast<int>(h.doc_col_seg.size());
@@ -285,11 +292,11 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
     const int nside = std::min<int>(rubiconv_plan_s::kSideStreams, static_cast<int>(launches.size()));
     auto launch_one = [&](const Launch& L, hipStream_t s) -> hipError_t {
         if (L.nb > 0)
-            return rubiconv::launch_row_dense(L.nb, grid, plan->grid_pb_stride, fgrid,
-                                              fgrid_pb_stride, t.segs,
-                                              plan->dense_docs + h.dense_list0[L.nb],
-                                              h.dense_count[L.nb], plan->dense_tab, h.n1, h.npb,
-                                              corr, s);
+            return rubiconv::launch_row_dense(
+                L.nb, grid, plan->grid_pb_stride, fgrid, fgrid_pb_stride, t.segs, plan->dense_docs,
+                plan->dense_groups + 2 * (own_rows ? h.dense_dgrp0[L.nb] : h.dense_grp0[L.nb]),
+                own_rows ? h.dense_dgrp_n[L.nb] : h.dense_grp_n[L.nb], plan->dense_tab, h.n1, h.npb,
+                corr, s);
         if (L.cls < 0)
             return rubiconv::launch_row_conv(h.n1, half, grid, plan->grid_pb_stride, fgrid,
                                              fgrid_pb_stride, t,
@@ -467,7 +474,7 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
         });
     if (e == hipSuccess)
         e = enqueue_conv(plan, x, h.x_dtype, spectrum, plan->cls_pb_stride, plan->doc_t, y, h.y_dtype,
-                         workspace, 0, "", stream, rec);
+                         workspace, 0, false, "", stream, rec);
     if (e == hipSuccess && direct) e = join_direct(plan, stream, rec);
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }
@@ -496,7 +503,7 @@ rubiconv_status_t rubiconv_packed_conv_dx(rubiconv_plan_t plan, const void* dy, 
         });
     if (e == hipSuccess)
         e = enqueue_conv(plan, dy, h.y_dtype, spectrum, plan->cls_pb_stride, plan->doc_t, dx,
-                         h.x_dtype, workspace, 1, "dx_", stream, rec);
+                         h.x_dtype, workspace, 1, false, "dx_", stream, rec);
     if (e == hipSuccess && direct) e = join_direct(plan, stream, rec);
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }
@@ -546,7 +553,7 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
     rec.mark("dk_col_fwd_x");
     if (e == hipSuccess)
         e = enqueue_conv(plan, dy, h.y_dtype, xgrid, plan->grid_pb_stride, plan->grad_t, r,
-                         RUBICONV_F32, workspace, 1, "dk_", stream, rec);
+                         RUBICONV_F32, workspace, 1, true, "dk_", stream, rec);
     if (e == hipSuccess && direct) e = join_direct(plan, stream, rec);
     if (e == hipSuccess)
         e = rubiconv::launch_lag_sum(r, plan->all_segs, static_cast<int>(h.all_docs.size()), h.N, h.D,
