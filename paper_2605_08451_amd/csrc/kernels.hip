@@ -308,9 +308,20 @@ struct RowTask {
     int m, spb, spb_log2, u, ub, nrows, s;
 };
 
-__device__ __forceinline__ RowTask row_task(const LaunchTables& t, int n1) {
+// Workgroups go to the eight XCDs in turn (workgroup b to XCD b % 8).  Task
+// numbers are dealt so that each XCD takes runs of kXcdRun consecutive tasks, i.e.
+// the sub-blocks of channel pairs of a grid row together: their 4- to 16-byte
+// pieces of each 64-byte grid point then meet in one XCD's L2 instead of being
+// fetched by several.  The launch covers a multiple of 8 kXcdRun workgroups;
+// numbers past the last task return at once.
+constexpr int kXcdRun = 16;
+__device__ __forceinline__ int xcd_task(int b) {
+    const int xcd = b & 7, k = b >> 3;
+    return (k % kXcdRun) + kXcdRun * (xcd + 8 * (k / kXcdRun));
+}
+
+__device__ __forceinline__ RowTask row_task(const LaunchTables& t, int n1, int task) {
     RowTask r;
-    const int task = blockIdx.x;
     r.sg = t.segs + t.task_seg[task];
     r.m = r.sg->m;
     r.spb = r.sg->spb;
@@ -349,9 +360,11 @@ __global__ __launch_bounds__(256) void row_conv_kernel(G* __restrict__ grid,
                                                        int64_t grid_pb_stride,
                                                        const G* __restrict__ fgrid,
                                                        int64_t fgrid_pb_stride, LaunchTables t,
-                                                       int n1, int corr) {
+                                                       int n1, int n_tasks, int corr) {
     extern __shared__ float2 sm[];
-    const RowTask r = row_task(t, n1);
+    const int task = xcd_task(static_cast<int>(blockIdx.x));
+    if (task >= n_tasks) return;  // whole workgroup
+    const RowTask r = row_task(t, n1, task);
     const int pb = blockIdx.y;
     const int rowlen = r.m * r.spb;
     float2* b0 = sm;
@@ -758,7 +771,8 @@ hipError_t launch_row_conv(int n1, bool half, void* grid, int64_t grid_pb_stride
                            const void* fgrid, int64_t fgrid_pb_stride, const LaunchTables& t,
                            int n_tasks, int npb, int lds_bytes, int corr, hipStream_t stream) {
     if (n_tasks == 0) return hipSuccess;
-    const dim3 g(n_tasks, npb), b(256);
+    const int run = 8 * kXcdRun;
+    const dim3 g((n_tasks + run - 1) / run * run, npb), b(256);
     hipError_t e;
     if (half) {
         e = hipFuncSetAttribute(reinterpret_cast<const void*>(&row_conv_kernel<__half2>),
@@ -766,14 +780,14 @@ hipError_t launch_row_conv(int n1, bool half, void* grid, int64_t grid_pb_stride
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(row_conv_kernel<__half2>, g, b, lds_bytes, stream,
                            static_cast<__half2*>(grid), grid_pb_stride,
-                           static_cast<const __half2*>(fgrid), fgrid_pb_stride, t, n1, corr);
+                           static_cast<const __half2*>(fgrid), fgrid_pb_stride, t, n1, n_tasks, corr);
     } else {
         e = hipFuncSetAttribute(reinterpret_cast<const void*>(&row_conv_kernel<float2>),
                                 hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(row_conv_kernel<float2>, g, b, lds_bytes, stream,
                            static_cast<float2*>(grid), grid_pb_stride,
-                           static_cast<const float2*>(fgrid), fgrid_pb_stride, t, n1, corr);
+                           static_cast<const float2*>(fgrid), fgrid_pb_stride, t, n1, n_tasks, corr);
     }
     return hipGetLastError();
 }

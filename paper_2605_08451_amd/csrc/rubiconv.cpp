@@ -289,7 +289,8 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
         }
     std::sort(launches.begin(), launches.end(),
               [](const Launch& a, const Launch& b) { return a.work > b.work; });
-    const int nside = std::min<int>(rubiconv_plan_s::kSideStreams, static_cast<int>(launches.size()));
+    // the largest launch runs on the calling stream itself, the others on side streams
+    const int nside = std::min<int>(rubiconv_plan_s::kSideStreams, static_cast<int>(launches.size()) - 1);
     auto launch_one = [&](const Launch& L, hipStream_t s) -> hipError_t {
         if (L.nb > 0)
             return rubiconv::launch_row_dense(
@@ -307,19 +308,20 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
                                          fgrid_pb_stride, t.segs, plan->doc_t.list + cs.list0,
                                          cs.nlist, plan->doc_t.tw, h.n1, h.npb, corr, s);
     };
-    if (nside <= 1) {
+    if (nside < 1) {
         for (const Launch& L : launches)
             if (e == hipSuccess) e = launch_one(L, stream);
     } else if (e == hipSuccess) {
         e = hipEventRecord(plan->fork, stream);
         for (int k = 0; k < nside && e == hipSuccess; ++k) e = hipStreamWaitEvent(plan->side[k], plan->fork, 0);
         std::vector<double> load(nside, 0.0);
-        for (const Launch& L : launches) {
-            if (e != hipSuccess) break;
+        for (size_t i = 1; i < launches.size() && e == hipSuccess; ++i) {
+            const Launch& L = launches[i];
             const int k = static_cast<int>(std::min_element(load.begin(), load.end()) - load.begin());
             load[k] += L.work;
             e = launch_one(L, plan->side[k]);
         }
+        if (e == hipSuccess) e = launch_one(launches[0], stream);
         for (int k = 0; k < nside && e == hipSuccess; ++k) {
             e = hipEventRecord(plan->join[k], plan->side[k]);
             if (e == hipSuccess) e = hipStreamWaitEvent(stream, plan->join[k], 0);
