@@ -425,7 +425,9 @@ def main():
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f32", "data": "synthetic",
+        # arithmetic type of the path: complex fp16 grids and matrix-core products with
+        # fp32 accumulation for bf16 inputs, fp32 throughout for fp32 inputs
+        "dtype": "f16" if W.x_dtype == "bf16" else "f32", "accumulate": "f32", "data": "synthetic",
         "config": {"workload": wl.CONFIG_NAMES[args.config], "B": W.B, "N": W.N, "D": W.D,
                    "L": W.L, "x_dtype": W.x_dtype, "y_dtype": W.y_dtype, "n1": info["n1"],
                    "docs": info["n_docs"], "size_classes": info["n_classes"],
