@@ -245,14 +245,14 @@ __global__ __launch_bounds__(16 * R) void col_inv_kernel(const G* __restrict__ g
 // ---------------------------------------------------------------- row pass
 // Stockham autosort stage of radix R on `lines` independent m-point rows held
 // in LDS as [row][j][spb pairs]; Ns = product of the radices already applied.
-template <int R, int S>
-__device__ __forceinline__ void stockham_butterfly(const float2* in, float2* out, int i, int mr,
+template <int R, int S, class E>
+__device__ __forceinline__ void stockham_butterfly(const E* in, E* out, int i, int mr,
                                                    int spb, int Ns, int m, const float2* twm) {
     const int k = i % Ns;
     const int step = (m / (Ns * R)) * k;
     float2 v[R];
 #pragma unroll
-    for (int qq = 0; qq < R; ++qq) v[qq] = in[(i + qq * mr) * spb];
+    for (int qq = 0; qq < R; ++qq) v[qq] = gload(in + (i + qq * mr) * spb);
 #pragma unroll
     for (int qq = 1; qq < R; ++qq) {
         const float2 w = twm[qq * step];
@@ -261,14 +261,15 @@ __device__ __forceinline__ void stockham_butterfly(const float2* in, float2* out
     Dft<R, S>::run(v);
     const int d = (i / Ns) * Ns * R + k;
 #pragma unroll
-    for (int qq = 0; qq < R; ++qq) out[(d + qq * Ns) * spb] = v[qq];
+    for (int qq = 0; qq < R; ++qq) gstore(out + (d + qq * Ns) * spb, v[qq]);
 }
 
-// m-point DFT (sign S) of nrows * spb lines; ping-pongs between a and b and
-// returns the buffer holding the natural-order result.
-template <int S>
-__device__ float2* row_dft(float2* a, float2* b, int nrows, int m, int spb, int spb_log2,
-                           const Seg* sg, const float2* twm) {
+// m-point DFT (sign S) of nrows * spb lines of LDS elements E (complex fp32, or
+// complex fp16 for fp16 grids: every stage computes in fp32 and rounds its outputs);
+// ping-pongs between a and b and returns the buffer holding the natural-order result.
+template <int S, class E>
+__device__ E* row_dft(E* a, E* b, int nrows, int m, int spb, int spb_log2,
+                      const Seg* sg, const float2* twm) {
     int Ns = 1;
     const int nfac = sg->nfac;
     for (int f = 0; f < nfac; ++f) {
@@ -280,8 +281,8 @@ __device__ float2* row_dft(float2* a, float2* b, int nrows, int m, int spb, int 
             const int rest = e >> spb_log2;
             const int i = rest % mr;
             const int row = rest / mr;
-            const float2* in = a + row * m * spb + pp;
-            float2* out = b + row * m * spb + pp;
+            const E* in = a + row * m * spb + pp;
+            E* out = b + row * m * spb + pp;
             switch (R) {
                 case 2: stockham_butterfly<2, S>(in, out, i, mr, spb, Ns, m, twm); break;
                 case 3: stockham_butterfly<3, S>(in, out, i, mr, spb, Ns, m, twm); break;
@@ -290,7 +291,7 @@ __device__ float2* row_dft(float2* a, float2* b, int nrows, int m, int spb, int 
             }
         }
         __syncthreads();
-        float2* tmp = a;
+        E* tmp = a;
         a = b;
         b = tmp;
         Ns *= R;
@@ -339,14 +340,15 @@ __device__ __forceinline__ int partner_col(int u, int v, int m) {
     return u == 0 ? (v == 0 ? 0 : m - v) : m - 1 - v;
 }
 
+// LDS holds the grid's own element type: rows are copied as they are
 template <class G>
-__device__ __forceinline__ void load_rows(float2* lds, const G* g, const RowTask& r) {
+__device__ __forceinline__ void load_rows(G* lds, const G* g, const RowTask& r) {
     const int rowlen = r.m * r.spb;
     for (int e = threadIdx.x; e < r.nrows * rowlen; e += blockDim.x) {
         const int pp = e & (r.spb - 1);
         const int jj = (e >> r.spb_log2) % r.m;
         const int uu = e < rowlen ? r.u : r.ub;
-        lds[e] = gload(g + (static_cast<int64_t>(uu) * r.m + jj) * kPairsPerBlock + pp);
+        lds[e] = g[(static_cast<int64_t>(uu) * r.m + jj) * kPairsPerBlock + pp];
     }
 }
 
@@ -354,29 +356,31 @@ __device__ __forceinline__ void load_rows(float2* lds, const G* g, const RowTask
 // first; their conjugate-symmetry separation leaves S and Df for every row-u
 // frequency in the third LDS buffer ([0][v] = S, [1][v] = Df).  Then the
 // document rows go through the same DFT, the product, the inverse row DFT and
-// back to the grid.  LDS: three buffers of two rows of m * spb values.
+// back to the grid.  LDS: three buffers of two rows of m * spb values of the
+// grid's element type.
 template <class G>
 __global__ __launch_bounds__(256) void row_conv_kernel(G* __restrict__ grid,
                                                        int64_t grid_pb_stride,
                                                        const G* __restrict__ fgrid,
                                                        int64_t fgrid_pb_stride, LaunchTables t,
                                                        int n1, int n_tasks, int corr) {
-    extern __shared__ float2 sm[];
+    extern __shared__ __align__(16) unsigned char row_smem[];
+    G* const sm = reinterpret_cast<G*>(row_smem);
     const int task = xcd_task(static_cast<int>(blockIdx.x));
     if (task >= n_tasks) return;  // whole workgroup
     const RowTask r = row_task(t, n1, task);
     const int pb = blockIdx.y;
     const int rowlen = r.m * r.spb;
-    float2* b0 = sm;
-    float2* b1 = sm + 2 * rowlen;
-    float2* sdf = sm + 4 * rowlen;
+    G* b0 = sm;
+    G* b1 = sm + 2 * rowlen;
+    G* sdf = sm + 4 * rowlen;
     const float2* twm = t.tw + r.sg->tw_off;
 
     const G* fg = fgrid + pb * fgrid_pb_stride + static_cast<int64_t>(r.sg->spec_off) * kPairsPerBlock +
                   r.s * r.spb;
     load_rows(b0, fg, r);
     __syncthreads();
-    const float2* zh = row_dft<-1>(b0, b1, r.nrows, r.m, r.spb, r.spb_log2, r.sg, twm);
+    const G* zh = row_dft<-1>(b0, b1, r.nrows, r.m, r.spb, r.spb_log2, r.sg, twm);
     const float c = 0.5f * sqrtf(static_cast<float>(n1)) / static_cast<float>(r.m);
     for (int e = threadIdx.x; e < rowlen; e += blockDim.x) {
         const int pp = e & (r.spb - 1);
@@ -384,37 +388,37 @@ __global__ __launch_bounds__(256) void row_conv_kernel(G* __restrict__ grid,
         const int vb = partner_col(r.u, v, r.m);
         float2 s, df;
         // correlation: the filter spectrum read at -f (its conjugate for real taps)
-        const float2 fa = zh[e], fb = zh[((r.nrows - 1) * r.m + vb) * r.spb + pp];
+        const float2 fa = gload(zh + e), fb = gload(zh + ((r.nrows - 1) * r.m + vb) * r.spb + pp);
         filter_sdf(corr ? fb : fa, corr ? fa : fb, c, s, df);
-        sdf[e] = s;
-        sdf[rowlen + e] = df;
+        gstore(sdf + e, s);
+        gstore(sdf + rowlen + e, df);
     }
     __syncthreads();
 
     G* g = grid + pb * grid_pb_stride + r.sg->grid_off * kPairsPerBlock + r.s * r.spb;
     load_rows(b0, g, r);
     __syncthreads();
-    float2* z = row_dft<-1>(b0, b1, r.nrows, r.m, r.spb, r.spb_log2, r.sg, twm);
-    float2* w = (z == b0) ? b1 : b0;
+    G* z = row_dft<-1>(b0, b1, r.nrows, r.m, r.spb, r.spb_log2, r.sg, twm);
+    G* w = (z == b0) ? b1 : b0;
     for (int e = threadIdx.x; e < rowlen; e += blockDim.x) {
         const int pp = e & (r.spb - 1);
         const int v = e >> r.spb_log2;
         const int vb = partner_col(r.u, v, r.m);
-        const float2 a = z[e];
+        const float2 a = gload(z + e);
         const int eb = ((r.nrows - 1) * r.m + vb) * r.spb + pp;
-        const float2 b = z[eb];
-        const float2 s = sdf[e], df = sdf[rowlen + e];
-        w[e] = product_f(a, b, s, df);
-        if (r.nrows == 2) w[eb] = product_neg_f(a, b, s, df);
+        const float2 b = gload(z + eb);
+        const float2 s = gload(sdf + e), df = gload(sdf + rowlen + e);
+        gstore(w + e, product_f(a, b, s, df));
+        if (r.nrows == 2) gstore(w + eb, product_neg_f(a, b, s, df));
     }
     __syncthreads();
 
-    float2* y = row_dft<1>(w, z, r.nrows, r.m, r.spb, r.spb_log2, r.sg, twm);
+    const G* y = row_dft<1>(w, z, r.nrows, r.m, r.spb, r.spb_log2, r.sg, twm);
     for (int e = threadIdx.x; e < r.nrows * rowlen; e += blockDim.x) {
         const int pp = e & (r.spb - 1);
         const int jj = (e >> r.spb_log2) % r.m;
         const int uu = e < rowlen ? r.u : r.ub;
-        gstore(g + (static_cast<int64_t>(uu) * r.m + jj) * kPairsPerBlock + pp, y[e]);
+        g[(static_cast<int64_t>(uu) * r.m + jj) * kPairsPerBlock + pp] = y[e];
     }
 }
 

@@ -48,12 +48,12 @@ int factorize(int m, int8_t* fac) {
     return m == 1 ? n : -1;
 }
 
-// Pairs per row task of the generic row kernel: three LDS buffers of two rows
-// of m * spb complex floats must fit its LDS budget.
-int pairs_per_task(int m) {
+// Pairs per row task of the generic row kernel: three LDS buffers of two rows of
+// m * spb complex values of esz bytes (the grid's element) must fit its LDS budget.
+int pairs_per_task(int m, int esz) {
     int spb = kPairsPerBlock;
     if (m <= kMaxFastM) return spb;  // register-resident kernel: 32 lines of m values in LDS
-    while (spb > 1 && 6 * m * spb * 8 > kRowLdsBytes) spb /= 2;
+    while (spb > 1 && 6 * m * spb * esz > kRowLdsBytes) spb /= 2;
     return spb;
 }
 
@@ -443,7 +443,7 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
         // w_P^r / sqrt(N1), r < P: the per-document twiddle of the column passes, which
         // also scale by 1/sqrt(N1) (a power of two, exact)
         push_twiddles(p.tw, s.P, s.P, 1.0 / r);
-        s.spb = pairs_per_task(m);
+        s.spb = pairs_per_task(m, p.grid_half ? 4 : 8);
         s.nfac = factorize(m, s.fac);
         p.taps_max = std::max(p.taps_max, s.len);
         p.classes.push_back(s);
@@ -463,7 +463,7 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
         p.doc_col_seg.insert(p.doc_col_seg.end(), s.m, idx);
         if (s.m > kMaxFastM) {
             p.doc_task_seg.insert(p.doc_task_seg.end(), (n1 / 2 + 1) * (kPairsPerBlock / s.spb), idx);
-            p.row_lds_docs = std::max(p.row_lds_docs, 6 * s.m * s.spb * 8);
+            p.row_lds_docs = std::max(p.row_lds_docs, 6 * s.m * s.spb * (p.grid_half ? 4 : 8));
         }
     }
     for (auto& s : p.classes) {
