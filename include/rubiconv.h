@@ -90,10 +90,17 @@ typedef enum {
  * column grid.  The environment variable RUBICONV_DIRECT_MAX = 0..128, read when
  * the plan is made, sets the length limit and drops the share condition (0 turns
  * the path off).
+ * Documents whose smallest transform sizes differ little may share one size class:
+ * a document then takes a larger transform than its own minimum (any transform
+ * holding the causal padding gives the same exact result, Theorem 2.1), when that
+ * removes a filter spectrum and moves fewer bytes overall.  The environment
+ * variable RUBICONV_CLASS_MERGE = 0 (read when the plan is made) keeps every
+ * document at its own smallest size; 1 or unset merges.
  * The plan copies what it needs; cu_seqlens_host may be freed on return.  Plan
  * creation allocates device memory and copies the document and twiddle tables
  * synchronously (it is not a stream-ordered call).
- * Errors: RUBICONV_ERR_ARG (also for a malformed RUBICONV_DIRECT_MAX),
+ * Errors: RUBICONV_ERR_ARG (also for a malformed RUBICONV_DIRECT_MAX or
+ * RUBICONV_CLASS_MERGE),
  * RUBICONV_ERR_SEQLENS, RUBICONV_ERR_UNSUPPORTED (n1 not supported, or a document
  * so long that its row DFT would exceed the largest supported size),
  * RUBICONV_ERR_ALLOC, RUBICONV_ERR_HIP.
