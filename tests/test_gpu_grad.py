@@ -159,3 +159,33 @@ def test_gradients_deterministic(device):
     b = _run(W, device, seed=9)
     np.testing.assert_array_equal(a[1], b[1])
     np.testing.assert_array_equal(a[2], b[2])
+
+
+def test_class_groups(device):
+    """Size classes holding one to ten documents: the matrix-core row kernels take a
+    class's documents in groups of at most four sharing one filter-row transform (ten
+    documents: groups of 4, 3 and 3), for short rows, 17-32-point rows and the partner
+    kernel; the forward, dx and dk (whose tasks keep one document each) meet the bar."""
+    import paper_2605_08451_amd as rc
+    import torch
+    N = 8192
+    rows = [[500] * 10 + [N - 5000], [1500] * 5 + [N - 7500], [3000, 3000, N - 6000], [6000, N - 6000]]
+    W = wl.make_case(rows, D=32, L=N, x_dtype="bf16", seed=77)
+    x, k = to_device(W, device)
+    dyv, dy = _dy(W, 78)
+    dy = dy.to(device)
+    plan = rc.Plan(W.cu_seqlens, N=W.N, D=W.D, L=W.L, x_dtype="bf16")
+    ms = [int(v) for v in plan.doc_table()[:, 4]]
+    assert max(ms.count(m) for m in set(ms)) >= 9 and max(ms) > 32, ms
+    ws = plan.new_workspace(device)
+    spec = rc.filter_spectrum(plan, k, workspace=ws)
+    y = rc.packed_conv(plan, x, spec, workspace=ws)
+    dx = rc.packed_conv_dx(plan, dy, spec, workspace=ws)
+    dk = rc.packed_conv_dk(plan, x, dy)
+    torch.cuda.synchronize(device)
+    f64 = lambda t: t.float().cpu().numpy().astype(np.float64)
+    assert_parity(f64(y), oracle.conv_direct(W.x, W.filters, W.cu_seqlens, threads=ORACLE_THREADS),
+                  W.cu_seqlens, "bf16", "y")
+    assert_parity(f64(dx), oracle.grad_x(W.filters, dyv, W.cu_seqlens, threads=ORACLE_THREADS),
+                  W.cu_seqlens, "bf16", "dx")
+    _check_dk(f64(dk), oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L, threads=ORACLE_THREADS), "bf16", "dk")
