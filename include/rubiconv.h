@@ -96,6 +96,9 @@ typedef enum {
  * removes a filter spectrum and moves fewer bytes overall.  The environment
  * variable RUBICONV_CLASS_MERGE = 0 (read when the plan is made) keeps every
  * document at its own smallest size; 1 or unset merges.
+ * Rows of at most 8 points (bf16 inputs) are transformed 16 / m documents at a time
+ * when such rows hold at least a quarter of the grid; RUBICONV_ROW_BATCH = 0 turns
+ * this off and 1..8 sets the largest batched row size regardless of the share.
  * The plan copies what it needs; cu_seqlens_host may be freed on return.  Plan
  * creation allocates device memory and copies the document and twiddle tables
  * synchronously (it is not a stream-ordered call).

@@ -77,6 +77,15 @@ hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const vo
                             const int32_t* groups, int ngroups, const void* tabs, int n1, int npb,
                             int corr, hipStream_t stream);
 
+// The same pass for rows of at most kMaxBatchM points, 16 / m documents of a group side
+// by side in one matrix-core block; each document's second-grid rows are its own
+// (Seg::spec_off), so the groups may also hold documents with different second grids.
+// The grid and the second grid of a pair block must each span less than 2^31 bytes.
+hipError_t launch_row_batch(void* grid, int64_t grid_pb_stride, const void* fgrid,
+                            int64_t fgrid_pb_stride, const Seg* segs, const int32_t* docs,
+                            const int32_t* groups, int ngroups, const void* tabs, int n1, int npb,
+                            int corr, hipStream_t stream);
+
 // Matrix-core column passes (N1 = 256, complex fp16 grids, D a multiple of 32).
 // `mtab` holds the MFMA operand tables in lane order (16-byte entries, offsets
 // below; see build_mfma_tables).

@@ -18,6 +18,7 @@
 #include <algorithm>
 #include <cmath>
 #include <complex>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <mutex>
@@ -197,7 +198,9 @@ void make_mfma_tables(std::vector<uint32_t>* out) {
         }, 0);
 }
 
-void make_dense_tables(int m, int n1, std::vector<uint32_t>* out) {
+// batch > 1 (m <= 8, one block): the block-diagonal form for `batch` rows side by side,
+// row r at slots r m .. r m + m - 1 in both time and frequency, zero elsewhere.
+void make_dense_tables(int m, int n1, std::vector<uint32_t>* out, int batch = 1) {
     const int nb = (m + 15) / 16;
     const double fwd_scale = 1.0 / std::sqrt(static_cast<double>(m));
     const double inv_scale = std::sqrt(static_cast<double>(n1)) / 4.0;
@@ -209,8 +212,13 @@ void make_dense_tables(int m, int n1, std::vector<uint32_t>* out) {
         for (int kb = 0; kb < nb; ++kb)
             for (int jb = 0; jb < nb; ++jb)
                 push_operands(out, [=](int row, int n) {
-                    const int k = dir == 0 ? 16 * kb + row : 16 * jb + n;              // frequency
-                    const int j = dir == 0 ? 16 * jb + interleave(n) : 16 * kb + interleave(row);  // time
+                    int k = dir == 0 ? 16 * kb + row : 16 * jb + n;              // frequency
+                    int j = dir == 0 ? 16 * jb + interleave(n) : 16 * kb + interleave(row);  // time
+                    if (batch > 1) {  // row k / m of the batch, and the same row for j
+                        if (k / m != j / m || k / m >= batch) return std::complex<double>(0.0, 0.0);
+                        k %= m;
+                        j %= m;
+                    }
                     if (k >= m || j >= m) return std::complex<double>(0.0, 0.0);
                     const std::complex<double> w = z[(static_cast<int64_t>(k) * j) % m];
                     return dir == 0 ? w * fwd_scale : std::conj(w) * inv_scale;
@@ -274,7 +282,8 @@ const std::vector<uint32_t>& cached_tables(int kind, int m, int n1) {
         std::vector<uint32_t> t;
         if (kind == 0) make_mfma_tables(&t);
         else if (kind == 1) make_dense_tables(m, n1, &t);
-        else make_partner_tables(m, n1, &t);
+        else if (kind == 2) make_partner_tables(m, n1, &t);
+        else make_dense_tables(m, n1, &t, 16 / m);
         it = cache.emplace(std::make_tuple(kind, m, n1), std::move(t)).first;
     }
     return it->second;
@@ -290,6 +299,11 @@ void build_dense_tables(int m, int n1, std::vector<uint32_t>* out) {
 
 void build_partner_tables(int m, int n1, std::vector<uint32_t>* out) {
     const std::vector<uint32_t>& t = cached_tables(2, m, n1);
+    out->insert(out->end(), t.begin(), t.end());
+}
+
+void build_batch_tables(int m, int n1, std::vector<uint32_t>* out) {
+    const std::vector<uint32_t>& t = cached_tables(3, m, n1);
     out->insert(out->end(), t.begin(), t.end());
 }
 
@@ -488,6 +502,22 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
     if (p.col_mfma) build_mfma_tables(&p.mfma_tab);
     // complex fp16 grids: rows of up to 16 * kMaxDenseBlocks points on the matrix cores
     p.row_dense = p.grid_half;
+    // the batched kernel addresses a pair block's grids with 32-bit byte offsets
+    int batch_m = p.grid_points * 64 < (int64_t(1) << 31) && p.class_points * 64 < (int64_t(1) << 31)
+                      ? kMaxBatchM : 0;
+    if (batch_m > 0) {
+        // the batched kernel is one more launch: worth it once its rows hold a real share
+        // of the grid (RUBICONV_ROW_BATCH = 0 turns it off, 1..8 sets the largest batched
+        // row size and drops the share condition)
+        const char* v = std::getenv("RUBICONV_ROW_BATCH");
+        if (v) {
+            batch_m = std::min(batch_m, std::max(0, std::atoi(v)));
+        } else {
+            int64_t pts = 0;
+            for (const Seg& d : p.docs) pts += d.m <= batch_m ? d.P : 0;
+            if (pts * kBatchMinShare < p.grid_points) batch_m = 0;
+        }
+    }
     if (p.row_dense) {
         for (auto& c : p.classes) {
             if (c.m > 16 * kMaxDenseBlocks) continue;
@@ -496,6 +526,8 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
                 build_dense_tables(c.m, n1, &p.dense_tab);
             else
                 build_partner_tables(c.m, n1, &p.dense_tab);
+            // rows of at most kMaxBatchM points: the block-diagonal tables follow the plain ones
+            if (c.m <= batch_m) build_batch_tables(c.m, n1, &p.dense_tab);
         }
         for (auto& s : p.docs) s.dense_off = p.classes[s.cls].dense_off;
         for (int nb = 1; nb <= kMaxDenseBlocks; ++nb) {
@@ -505,31 +537,48 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
             p.dense_count[nb] = static_cast<int32_t>(p.dense_docs.size()) - p.dense_list0[nb];
         }
         // class groups: consecutive entries of one class (class_docs is in class order),
-        // split into near-equal groups of at most kMaxGroupDocs
-        for (int nb = 1; nb <= kMaxDenseBlocks; ++nb) {
-            p.dense_grp0[nb] = static_cast<int32_t>(p.dense_groups.size() / 2);
+        // split into near-equal groups of at most `cap` documents.  Rows of at most
+        // kMaxBatchM points go to the batched kernel (pass 1), the others to the kernel
+        // of their block count (pass 0).
+        auto class_groups = [&](int nb, bool batched) {
             const int e0 = p.dense_list0[nb], e1 = e0 + p.dense_count[nb];
             for (int a = e0; a < e1;) {
                 int b = a;
                 while (b < e1 && p.docs[p.dense_docs[b]].cls == p.docs[p.dense_docs[a]].cls) ++b;
-                const int n = b - a, ng = (n + kMaxGroupDocs - 1) / kMaxGroupDocs;
-                for (int g = 0, first = a; g < ng; ++g) {
-                    const int cnt = n / ng + (g < n % ng ? 1 : 0);
-                    p.dense_groups.push_back(first);
-                    p.dense_groups.push_back(cnt);
-                    first += cnt;
+                const int m = p.docs[p.dense_docs[a]].m;
+                if ((m <= batch_m) == batched) {
+                    const int cap = batched ? kMaxGroupDocs * (16 / m) : kMaxGroupDocs;
+                    const int n = b - a, ng = (n + cap - 1) / cap;
+                    for (int g = 0, first = a; g < ng; ++g) {
+                        const int cnt = n / ng + (g < n % ng ? 1 : 0);
+                        p.dense_groups.push_back(first);
+                        p.dense_groups.push_back(cnt);
+                        first += cnt;
+                    }
                 }
                 a = b;
             }
+        };
+        for (int nb = 1; nb <= kMaxDenseBlocks; ++nb) {
+            p.dense_grp0[nb] = static_cast<int32_t>(p.dense_groups.size() / 2);
+            class_groups(nb, false);
             p.dense_grp_n[nb] = static_cast<int32_t>(p.dense_groups.size() / 2) - p.dense_grp0[nb];
         }
         for (int nb = 1; nb <= kMaxDenseBlocks; ++nb) {
             p.dense_dgrp0[nb] = static_cast<int32_t>(p.dense_groups.size() / 2);
             for (int k = 0; k < p.dense_count[nb]; ++k) {
+                if (p.docs[p.dense_docs[p.dense_list0[nb] + k]].m <= batch_m) continue;
                 p.dense_groups.push_back(p.dense_list0[nb] + k);
                 p.dense_groups.push_back(1);
             }
-            p.dense_dgrp_n[nb] = p.dense_count[nb];
+            p.dense_dgrp_n[nb] = static_cast<int32_t>(p.dense_groups.size() / 2) - p.dense_dgrp0[nb];
+        }
+        p.dense_bgrp0 = static_cast<int32_t>(p.dense_groups.size() / 2);
+        class_groups(1, true);
+        p.dense_bgrp_n = static_cast<int32_t>(p.dense_groups.size() / 2) - p.dense_bgrp0;
+        for (int k = 0; k < p.dense_count[1]; ++k) {
+            const Seg& d = p.docs[p.dense_docs[p.dense_list0[1] + k]];
+            if (d.m <= batch_m) p.dense_bwork += d.m;
         }
     }
     *out = std::move(p);

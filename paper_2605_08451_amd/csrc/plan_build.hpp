@@ -51,6 +51,11 @@ struct HostPlan {
     int32_t dense_grp_n[kMaxDenseBlocks + 1] = {};
     int32_t dense_dgrp0[kMaxDenseBlocks + 1] = {};  // one-document groups of block count nb
     int32_t dense_dgrp_n[kMaxDenseBlocks + 1] = {};
+    // rows of at most kMaxBatchM points: class groups of the batched kernel, which puts
+    // 16 / m documents side by side in one block (for the filter gradient as well, as it
+    // takes each document's second rows from that document)
+    int32_t dense_bgrp0 = 0, dense_bgrp_n = 0;
+    double dense_bwork = 0;                          // their summed row sizes
     int64_t grid_points = 0;            // sum over documents of P_i
     int64_t class_points = 0;           // sum over classes of P
     int32_t taps_max = 0;               // largest number of filter taps any class keeps
@@ -72,6 +77,9 @@ void build_dense_tables(int m, int n1, std::vector<uint32_t>* out);
 // Matrix-core row pass for 32 < m <= 16 * kMaxDenseBlocks: one real operand per block
 // and direction, then the partner-row twiddles (kernels.hpp: kPartnerTabU4).
 void build_partner_tables(int m, int n1, std::vector<uint32_t>* out);
+// Batched rows (m <= kMaxBatchM): the tables of build_dense_tables in block-diagonal form
+// for 16 / m rows side by side (row r at slots r m .. r m + m - 1).
+void build_batch_tables(int m, int n1, std::vector<uint32_t>* out);
 
 // Validates cu_seqlens and fills every table of *out.
 // direct_max: documents of at most this many tokens take the direct path (0: none);

@@ -589,6 +589,180 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
     }
 }
 
+// ---------------------------------------------------------------------------
+// Rows of at most kMaxBatchM points (one 16-point block): R = 16 / m documents of a
+// group sit side by side in the block, document r at slots r m .. r m + m - 1 of both
+// the time and the frequency axis, and block-diagonal tables transform them together;
+// the per-row work of the short-row kernel is then shared by R documents.  Each lane
+// register reads its point from the grids of its own document (4 bytes per lane: the
+// 16 lanes of a lane group cover one 64-byte grid point) and writes it back the same
+// way, and each document's second rows are its own (Seg::spec_off), so one group may
+// mix second grids (the filter gradient).  Row 0, whose partner columns wrap inside
+// the row, keeps one document per block and the plain tables; rows that are their own
+// partners store one row.
+constexpr int kBatchWaves = 8;
+
+__global__ __launch_bounds__(64 * kBatchWaves) void row_batch_kernel(uint32_t* __restrict__ grid,
+                                                                    int64_t grid_pb_stride,
+                                                                    const uint32_t* __restrict__ fgrid,
+                                                                    int64_t fgrid_pb_stride,
+                                                                    const Seg* __restrict__ segs,
+                                                                    const int32_t* __restrict__ docs,
+                                                                    const int2* __restrict__ groups,
+                                                                    const u4* __restrict__ tabs, int n1,
+                                                                    int corr) {
+    constexpr int kTabU4 = 4 * 64;                   // one table set: forward then inverse
+    constexpr uint32_t kNone = 0xffffffffu;          // an offset outside every buffer
+    __shared__ u4 tab[2 * kTabU4];                   // plain tables, then block-diagonal ones
+    __shared__ uint32_t xch_all[kBatchWaves][2 * (kPad + 16) * 16];
+
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+    const int lane = threadIdx.x & 63;
+    const int p = lane & 15, h = lane >> 4;
+    const int nu = n1 / 2 + 1;
+    const int ug = (nu + kBatchWaves - 1) / kBatchWaves;
+    const int2 grp = groups[blockIdx.x / ug];
+    const int m = segs[docs[grp.x]].m;
+    const int u = (blockIdx.x % ug) * kBatchWaves + wave;
+    const bool active = u < nu;  // wave-uniform
+    const int pb = blockIdx.y;
+    {
+        const __amdgpu_buffer_rsrc_t rt = row_buffer(tabs + segs[docs[grp.x]].dense_off, 2 * kTabU4 * 16);
+        for (int c = wave; c < 2 * kTabU4 / 64; c += kBatchWaves) lds_copy16(rt, c * 1024 + lane * 16, &tab[c * 64]);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();  // tables visible to every wave; the only workgroup barrier
+    if (!active) return;
+
+    const int ub = (n1 - u) & (n1 - 1);
+    const bool self = ub == u;
+    const int shift = u == 0 ? 1 : 0;
+    const int R = u == 0 ? 1 : 16 / m;  // documents per block
+    const u4* fwd = tab + (u == 0 ? 0 : kTabU4);
+    const u4* inv = fwd + 2 * 64;
+    const __amdgpu_buffer_rsrc_t rg =
+        row_buffer(grid + pb * grid_pb_stride, static_cast<uint32_t>(grid_pb_stride * 4));
+    const __amdgpu_buffer_rsrc_t rf =
+        row_buffer(fgrid + pb * fgrid_pb_stride, static_cast<uint32_t>(fgrid_pb_stride * 4));
+    uint32_t* stage = xch_all[wave];
+    uint32_t* xlds = stage + kPad * 16 + p;
+    uint32_t* flds = stage + (2 * kPad + 16) * 16 + p;
+
+    // forward DFT of rows u and ub: own[r] = frequency slot 4 h + r of row u; row ub's
+    // spectrum to the exchange row dst at slot 4 h + r - shift (row 0: its frequency 0
+    // also at slot m - 1)
+    auto forward = [&](u4 in_u, u4 in_b, uint32_t* own, uint32_t* dst) {
+#pragma unroll
+        for (int i = 0; i < kPad / 4; ++i) dst[16 * (4 * i + h - kPad)] = 0u;
+        f4 acc[2][2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        const u4 are = fwd[lane], aim = fwd[64 + lane];
+        acc[0][0] = mma(are, in_u, acc[0][0]);
+        acc[0][1] = mma(aim, in_u, acc[0][1]);
+        acc[1][0] = mma(are, in_b, acc[1][0]);
+        acc[1][1] = mma(aim, in_b, acc[1][1]);
+        uint32_t keep = 0u;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            own[r] = pack_h2(acc[0][0][r], acc[0][1][r]);
+            const uint32_t bv = pack_h2(acc[1][0][r], acc[1][1][r]);
+            dst[16 * (4 * h + r - shift)] = bv;
+            if (r == 0) keep = bv;
+        }
+        if (shift && h == 0) dst[16 * (m - 1)] = keep;
+        wave_lds_fence();
+    };
+
+    // frequency slot 4 h + r reads its partner at slot (2 q + 1) m - 1 - v, q its
+    // document (row 0: m - 1 - v, through the shifted exchange row).  Slots past the
+    // block's documents read the first front slot, which holds zero: their own slot may
+    // hold a stale value (row 0 leaves slot 15 unwritten), and a non-finite one would
+    // reach every output through the zero entries of the inverse table (0 * inf)
+    int pslot[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int v = 4 * h + r, q = v / m;
+        pslot[r] = q < R ? (2 * q + 1) * m - 1 - v : -kPad;
+    }
+
+    for (int k0 = 0; k0 < grp.y; k0 += R) {
+        const int nr = min(R, grp.y - k0);  // documents in this block
+        // register t holds time slot 4 t + h: point j of document q
+        uint32_t o_du[4], o_db[4], o_fu[4], o_fb[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int v = 4 * t + h, q = v / m, j = v - q * m;
+            o_du[t] = o_db[t] = o_fu[t] = o_fb[t] = kNone;
+            if (q < nr) {
+                const Seg& sg = segs[docs[grp.x + k0 + q]];
+                const uint32_t pbyte = static_cast<uint32_t>(p) * 4;
+                o_du[t] = static_cast<uint32_t>((sg.grid_off + static_cast<int64_t>(u) * m + j) * 64) + pbyte;
+                o_db[t] = static_cast<uint32_t>((sg.grid_off + static_cast<int64_t>(ub) * m + j) * 64) + pbyte;
+                o_fu[t] = static_cast<uint32_t>((static_cast<int64_t>(sg.spec_off) + static_cast<int64_t>(u) * m + j) * 64) + pbyte;
+                o_fb[t] = static_cast<uint32_t>((static_cast<int64_t>(sg.spec_off) + static_cast<int64_t>(ub) * m + j) * 64) + pbyte;
+            }
+        }
+        u4 fu, fb, xu, xb;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            fu[t] = __builtin_amdgcn_raw_buffer_load_b32(rf, static_cast<int>(o_fu[t]), 0, 2);
+            fb[t] = __builtin_amdgcn_raw_buffer_load_b32(rf, static_cast<int>(o_fb[t]), 0, 2);
+            xu[t] = __builtin_amdgcn_raw_buffer_load_b32(rg, static_cast<int>(o_du[t]), 0, 2);
+            xb[t] = __builtin_amdgcn_raw_buffer_load_b32(rg, static_cast<int>(o_db[t]), 0, 2);
+        }
+
+        uint32_t fa[4], fl[4], au[4], wu[4];
+        forward(fu, fb, fa, flds);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) fl[r] = flds[16 * pslot[r]];
+        forward(xu, xb, au, xlds);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const uint32_t b = xlds[16 * pslot[r]];
+            const uint32_t a = au[r];
+            // correlation: the filter spectrum read at -f (its conjugate for real taps)
+            const uint32_t A = corr ? fl[r] : fa[r];
+            const uint32_t bf = corr ? fa[r] : fl[r];
+            const uint32_t e1 = pk_add_conj(a, b);
+            const uint32_t e2 = pk_swap_add_conj(a, b);
+            const uint32_t U = pk_add_neg_hi(e1, e2);
+            const uint32_t V = pk_add_neg_lo(e1, e2);
+            wu[r] = w_pos(A, bf, U, V);
+            xlds[16 * pslot[r]] = w_neg(A, bf, U, V);
+        }
+        if (shift && h == 0) xlds[-16] = xlds[16 * (m - 1)];
+        wave_lds_fence();
+        u4 wb;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) wb[t] = xlds[16 * (4 * h + t - shift)];
+        wave_lds_fence();
+
+        // inverse of both rows: output register r is time slot 4 r + h, the slot that
+        // input register r came from
+        f4 acc[2][2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        const u4 are = inv[lane], aim = inv[64 + lane];
+        const u4 win = {wu[0], wu[1], wu[2], wu[3]};
+        acc[0][0] = mma(are, win, acc[0][0]);
+        acc[0][1] = mma(aim, win, acc[0][1]);
+        acc[1][0] = mma(are, wb, acc[1][0]);
+        acc[1][1] = mma(aim, wb, acc[1][1]);
+        uint32_t ou[4], ob[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            ou[r] = pack_h2(acc[0][0][r], acc[0][1][r]);
+            ob[r] = pack_h2(acc[1][0][r], acc[1][1][r]);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            __builtin_amdgcn_raw_buffer_store_b32(ou[r], rg, static_cast<int>(o_du[r]), 0, 2);
+            __builtin_amdgcn_raw_buffer_store_b32(ob[r], rg, static_cast<int>(self ? kNone : o_db[r]), 0, 2);
+        }
+    }
+}
+
 template <int NB>
 hipError_t launch_lds_nb(void* grid, int64_t gs, const void* fgrid, int64_t fs, const Seg* segs,
                          const int32_t* docs, const int32_t* groups, int ngroups, const void* tabs,
@@ -614,6 +788,19 @@ hipError_t launch_partner_nb(void* grid, int64_t gs, const void* fgrid, int64_t 
 }
 
 }  // namespace
+
+hipError_t launch_row_batch(void* grid, int64_t grid_pb_stride, const void* fgrid,
+                            int64_t fgrid_pb_stride, const Seg* segs, const int32_t* docs,
+                            const int32_t* groups, int ngroups, const void* tabs, int n1, int npb,
+                            int corr, hipStream_t stream) {
+    if (ngroups == 0) return hipSuccess;
+    const int ug = (n1 / 2 + 1 + kBatchWaves - 1) / kBatchWaves;
+    const dim3 g(ngroups * ug, npb), b(64 * kBatchWaves);
+    hipLaunchKernelGGL(row_batch_kernel, g, b, 0, stream, static_cast<uint32_t*>(grid), grid_pb_stride,
+                       static_cast<const uint32_t*>(fgrid), fgrid_pb_stride, segs, docs,
+                       reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr);
+    return hipGetLastError();
+}
 
 hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const void* fgrid,
                             int64_t fgrid_pb_stride, const Seg* segs, const int32_t* docs,

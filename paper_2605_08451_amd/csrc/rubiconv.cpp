@@ -272,26 +272,33 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
         int cls;       // -1: generic kernel; >= 0: register-resident kernel of that class
         int nb;        // > 0: matrix-core kernel for the documents of that block count
         double work;
+        bool batch;    // the batched matrix-core kernel (rows of at most kMaxBatchM points)
     };
     std::vector<Launch> launches;
-    if (!h.doc_task_seg.empty()) launches.push_back({-1, 0, 1e30});
+    if (!h.doc_task_seg.empty()) launches.push_back({-1, 0, 1e30, false});
     for (size_t c = 0; c < h.classes.size(); ++c) {
         const int m = h.classes[c].m;
         if (m > rubiconv::kMaxFastM || (h.row_dense && m <= 16 * rubiconv::kMaxDenseBlocks)) continue;
-        launches.push_back({static_cast<int>(c), 0, static_cast<double>(m) * h.classes[c].nlist});
+        launches.push_back({static_cast<int>(c), 0, static_cast<double>(m) * h.classes[c].nlist, false});
     }
     if (h.row_dense)
         for (int nb = 1; nb <= rubiconv::kMaxDenseBlocks; ++nb) {
             if (h.dense_count[nb] == 0) continue;
             double w = 0;
             for (int k = 0; k < h.dense_count[nb]; ++k) w += h.docs[h.dense_docs[h.dense_list0[nb] + k]].m;
-            launches.push_back({-1, nb, w});
+            if (nb == 1) w -= h.dense_bwork;
+            if ((own_rows ? h.dense_dgrp_n[nb] : h.dense_grp_n[nb]) > 0) launches.push_back({-1, nb, w, false});
         }
+    if (h.row_dense && h.dense_bgrp_n > 0) launches.push_back({-1, 1, h.dense_bwork, true});
     std::sort(launches.begin(), launches.end(),
               [](const Launch& a, const Launch& b) { return a.work > b.work; });
     // the largest launch runs on the calling stream itself, the others on side streams
     const int nside = std::min<int>(rubiconv_plan_s::kSideStreams, static_cast<int>(launches.size()) - 1);
     auto launch_one = [&](const Launch& L, hipStream_t s) -> hipError_t {
+        if (L.batch)
+            return rubiconv::launch_row_batch(grid, plan->grid_pb_stride, fgrid, fgrid_pb_stride, t.segs,
+                                              plan->dense_docs, plan->dense_groups + 2 * h.dense_bgrp0,
+                                              h.dense_bgrp_n, plan->dense_tab, h.n1, h.npb, corr, s);
         if (L.nb > 0)
             return rubiconv::launch_row_dense(
                 L.nb, grid, plan->grid_pb_stride, fgrid, fgrid_pb_stride, t.segs, plan->dense_docs,

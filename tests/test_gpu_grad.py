@@ -189,3 +189,24 @@ def test_class_groups(device):
     assert_parity(f64(dx), oracle.grad_x(W.filters, dyv, W.cu_seqlens, threads=ORACLE_THREADS),
                   W.cu_seqlens, "bf16", "dx")
     _check_dk(f64(dk), oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L, threads=ORACLE_THREADS), "bf16", "dk")
+
+
+@pytest.mark.parametrize("rows", [[[200] * 10 + [48]], [[200, 200, 1648]], [[200, 1848]],
+                                  [[600] * 3 + [248]], [[100] * 20 + [48]]])
+def test_batched_short_rows(device, rows, monkeypatch):
+    """Rows of at most 8 points go 16 / m documents to a matrix-core block: full and
+    partial blocks, a class of one document, rows of one point, and row 0 (one
+    document per block); forward, dx and dk.  Slots past a block's documents must
+    not read stale exchange values (a non-finite one would spread over its pair)."""
+    import paper_2605_08451_amd as rc
+    monkeypatch.setenv("RUBICONV_ROW_BATCH", "8")   # whatever share these rows hold
+    W = wl.make_case(rows, D=32, L=2048, x_dtype="bf16", seed=sum(rows[0]))
+    dyv, dx, dk, plan = _run(W, device, seed=5)
+    assert min(int(v) for v in plan.doc_table()[:, 4]) <= 2
+    x, k = to_device(W, device)
+    p2 = rc.Plan(W.cu_seqlens, N=W.N, D=W.D, L=W.L, x_dtype="bf16")
+    y = rc.packed_conv(p2, x, rc.filter_spectrum(p2, k)).float().cpu().numpy().astype(np.float64)
+    assert np.isfinite(y).all() and np.isfinite(dx).all() and np.isfinite(dk).all()
+    assert_parity(y, oracle.conv_direct(W.x, W.filters, W.cu_seqlens), W.cu_seqlens, "bf16", "y")
+    assert_parity(dx, oracle.grad_x(W.filters, dyv, W.cu_seqlens), W.cu_seqlens, "bf16", "dx")
+    _check_dk(dk, oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L), "bf16", "dk")
