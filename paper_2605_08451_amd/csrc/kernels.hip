@@ -245,11 +245,30 @@ __global__ __launch_bounds__(16 * R) void col_inv_kernel(const G* __restrict__ g
 // ---------------------------------------------------------------- row pass
 // Stockham autosort stage of radix R on `lines` independent m-point rows held
 // in LDS as [row][j][spb pairs]; Ns = product of the radices already applied.
+// Quotient and remainder of x / d for 0 <= x < 2^24 and a divisor shared by the
+// workgroup, through a float reciprocal and one correction step (the hardware has
+// no integer division, and its emulation costs tens of instructions).
+struct FastDiv {
+    int d;
+    float inv;
+    __device__ explicit FastDiv(int dv) : d(dv), inv(1.0f / static_cast<float>(dv)) {}
+    __device__ __forceinline__ int div(int x, int* rem) const {
+        int q = static_cast<int>(static_cast<float>(x) * inv);
+        int r = x - q * d;
+        if (r < 0) { --q; r += d; }
+        if (r >= d) { ++q; r -= d; }
+        *rem = r;
+        return q;
+    }
+};
+
 template <int R, int S, class E>
 __device__ __forceinline__ void stockham_butterfly(const E* in, E* out, int i, int mr,
-                                                   int spb, int Ns, int m, const float2* twm) {
-    const int k = i % Ns;
-    const int step = (m / (Ns * R)) * k;
+                                                   int spb, int Ns, const FastDiv& fns, int mstep,
+                                                   const float2* twm) {
+    int k;
+    const int iq = fns.div(i, &k);  // i / Ns, i % Ns
+    const int step = mstep * k;
     float2 v[R];
 #pragma unroll
     for (int qq = 0; qq < R; ++qq) v[qq] = gload(in + (i + qq * mr) * spb);
@@ -259,7 +278,7 @@ __device__ __forceinline__ void stockham_butterfly(const E* in, E* out, int i, i
         v[qq] = cmul(v[qq], S < 0 ? w : cconj(w));
     }
     Dft<R, S>::run(v);
-    const int d = (i / Ns) * Ns * R + k;
+    const int d = iq * Ns * R + k;
 #pragma unroll
     for (int qq = 0; qq < R; ++qq) gstore(out + (d + qq * Ns) * spb, v[qq]);
 }
@@ -276,18 +295,20 @@ __device__ E* row_dft(E* a, E* b, int nrows, int m, int spb, int spb_log2,
         const int R = sg->fac[f];
         const int mr = m / R;
         const int nbf = nrows * spb * mr;
+        const FastDiv fmr(mr), fns(Ns);
+        const int mstep = m / (Ns * R);
         for (int e = threadIdx.x; e < nbf; e += blockDim.x) {
             const int pp = e & (spb - 1);
             const int rest = e >> spb_log2;
-            const int i = rest % mr;
-            const int row = rest / mr;
+            int i;
+            const int row = fmr.div(rest, &i);  // rest / mr, rest % mr
             const E* in = a + row * m * spb + pp;
             E* out = b + row * m * spb + pp;
             switch (R) {
-                case 2: stockham_butterfly<2, S>(in, out, i, mr, spb, Ns, m, twm); break;
-                case 3: stockham_butterfly<3, S>(in, out, i, mr, spb, Ns, m, twm); break;
-                case 4: stockham_butterfly<4, S>(in, out, i, mr, spb, Ns, m, twm); break;
-                default: stockham_butterfly<5, S>(in, out, i, mr, spb, Ns, m, twm); break;
+                case 2: stockham_butterfly<2, S>(in, out, i, mr, spb, Ns, fns, mstep, twm); break;
+                case 3: stockham_butterfly<3, S>(in, out, i, mr, spb, Ns, fns, mstep, twm); break;
+                case 4: stockham_butterfly<4, S>(in, out, i, mr, spb, Ns, fns, mstep, twm); break;
+                default: stockham_butterfly<5, S>(in, out, i, mr, spb, Ns, fns, mstep, twm); break;
             }
         }
         __syncthreads();
@@ -344,9 +365,11 @@ __device__ __forceinline__ int partner_col(int u, int v, int m) {
 template <class G>
 __device__ __forceinline__ void load_rows(G* lds, const G* g, const RowTask& r) {
     const int rowlen = r.m * r.spb;
+    const FastDiv fm(r.m);
     for (int e = threadIdx.x; e < r.nrows * rowlen; e += blockDim.x) {
         const int pp = e & (r.spb - 1);
-        const int jj = (e >> r.spb_log2) % r.m;
+        int jj;
+        (void)fm.div(e >> r.spb_log2, &jj);
         const int uu = e < rowlen ? r.u : r.ub;
         lds[e] = g[(static_cast<int64_t>(uu) * r.m + jj) * kPairsPerBlock + pp];
     }
@@ -414,9 +437,11 @@ __global__ __launch_bounds__(256) void row_conv_kernel(G* __restrict__ grid,
     __syncthreads();
 
     const G* y = row_dft<1>(w, z, r.nrows, r.m, r.spb, r.spb_log2, r.sg, twm);
+    const FastDiv fm(r.m);
     for (int e = threadIdx.x; e < r.nrows * rowlen; e += blockDim.x) {
         const int pp = e & (r.spb - 1);
-        const int jj = (e >> r.spb_log2) % r.m;
+        int jj;
+        (void)fm.div(e >> r.spb_log2, &jj);
         const int uu = e < rowlen ? r.u : r.ub;
         g[(static_cast<int64_t>(uu) * r.m + jj) * kPairsPerBlock + pp] = y[e];
     }
