@@ -197,6 +197,26 @@ template <int S>
 struct Dft<16, S> {
     __device__ __forceinline__ static void run(float2 (&v)[16]) { DftSplit<4, 4, S>::run(v); }
 };
+template <int S>
+struct Dft<20, S> {
+    __device__ __forceinline__ static void run(float2 (&v)[20]) { DftSplit<4, 5, S>::run(v); }
+};
+template <int S>
+struct Dft<24, S> {
+    __device__ __forceinline__ static void run(float2 (&v)[24]) { DftSplit<8, 3, S>::run(v); }
+};
+template <int S>
+struct Dft<25, S> {
+    __device__ __forceinline__ static void run(float2 (&v)[25]) { DftSplit<5, 5, S>::run(v); }
+};
+template <int S>
+struct Dft<30, S> {
+    __device__ __forceinline__ static void run(float2 (&v)[30]) { DftSplit<6, 5, S>::run(v); }
+};
+template <int S>
+struct Dft<32, S> {
+    __device__ __forceinline__ static void run(float2 (&v)[32]) { DftSplit<8, 4, S>::run(v); }
+};
 
 // ---------------------------------------------------------------- spectral product
 // Conjugate-symmetry separation (Appendix, dual real FFTs; Algorithm 3) fused with

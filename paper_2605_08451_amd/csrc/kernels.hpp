@@ -77,6 +77,12 @@ hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const vo
                             const int32_t* groups, int ngroups, const void* tabs, int n1, int npb,
                             int corr, hipStream_t stream);
 
+// Long rows (fp16 grids): the first level of the row DFT of one document or class grid
+// (LrItem) for its n1 grid rows and npb pair blocks, into its sub-row region, or the
+// inverse from the region back (long_rows.hip).  grid_pb_stride in complex elements.
+hipError_t launch_lr_step(bool inverse, void* grid, int64_t grid_pb_stride, const LrItem& it,
+                          const float2* tw, int n1, int npb, hipStream_t stream);
+
 // The same pass for rows of at most kMaxBatchM points, 16 / m documents of a group side
 // by side in one matrix-core block; each document's second-grid rows are its own
 // (Seg::spec_off), so the groups may also hold documents with different second grids.

@@ -62,4 +62,19 @@ struct Seg {
 };
 static_assert(sizeof(Seg) % 8 == 0, "Seg must stay 8-byte aligned in arrays");
 
+// Rows longer than kMaxFastM points on fp16 grids take a second four-step level: a row of
+// m = m1 * m2 points (j = m2 j1 + j2) becomes m1 sub-rows of m2 points, sub-row k1 of
+// grid row u at sub-row index k1 N1 + u of a virtual document of N1 m1 rows, whose
+// partner rows and columns then follow the same rules as the grid's own rows.  The
+// sub-rows live in a region of the same grid buffer past the documents' grids.
+struct LrItem {
+    int64_t real_off;  // first grid point of the document (or class) grid
+    int64_t virt_off;  // first point of its sub-row region
+    int32_t m, m1, m2;
+    int32_t tw_off;    // w_m^h, h < m, in the plan's twiddles
+};
+static_assert(sizeof(LrItem) % 8 == 0, "LrItem must stay 8-byte aligned in arrays");
+// sub-row counts the first level may take (register-resident DFTs), smallest first
+constexpr int kLrRadices[] = {2, 3, 4, 5, 6, 8, 9, 10, 12, 15, 16, 20, 24, 25, 30, 32};
+
 }  // namespace rubiconv

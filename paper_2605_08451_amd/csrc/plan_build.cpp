@@ -445,8 +445,20 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
         for (const auto& kv : class_of_m) tw_floats += 2 * (static_cast<size_t>(kv.first) + static_cast<size_t>(n1) * kv.first);
         p.tw.reserve(tw_floats);
     }
+    // long rows on fp16 grids: the first-level size m1 of each class (0: the generic row
+    // kernel); sub-rows of at most 64 points if possible, else at most 128
+    std::vector<int> lr_m1;
+    const char* lr_env = std::getenv("RUBICONV_LONG_ROWS");
+    const bool lr_on = p.grid_half && !(lr_env && lr_env[0] == '0');
     for (auto& kv : class_of_m) {
         int m = kv.first;
+        int m1 = 0;
+        for (int cap : {64, 128}) {
+            if (!lr_on || m <= kMaxFastM || m1) break;
+            for (int r1 : kLrRadices)
+                if (m % r1 == 0 && m / r1 <= cap) { m1 = r1; break; }
+        }
+        lr_m1.push_back(m1);
         kv.second = static_cast<int>(p.classes.size());
         Seg s{};
         s.m = m; s.P = n1 * m; s.cls = kv.second;
@@ -475,7 +487,7 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
         s.task0 = static_cast<int32_t>(p.doc_task_seg.size());
         int idx = static_cast<int>(&s - p.docs.data());
         p.doc_col_seg.insert(p.doc_col_seg.end(), s.m, idx);
-        if (s.m > kMaxFastM) {
+        if (s.m > kMaxFastM && lr_m1[s.cls] == 0) {
             p.doc_task_seg.insert(p.doc_task_seg.end(), (n1 / 2 + 1) * (kPairsPerBlock / s.spb), idx);
             p.row_lds_docs = std::max(p.row_lds_docs, 6 * s.m * s.spb * (p.grid_half ? 4 : 8));
         }
@@ -503,7 +515,8 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
     // complex fp16 grids: rows of up to 16 * kMaxDenseBlocks points on the matrix cores
     p.row_dense = p.grid_half;
     // the batched kernel addresses a pair block's grids with 32-bit byte offsets
-    int batch_m = p.grid_points * 64 < (int64_t(1) << 31) && p.class_points * 64 < (int64_t(1) << 31)
+    // (twice the grids: the sub-row regions of long rows, added below, are at most as large)
+    int batch_m = 2 * p.grid_points * 64 < (int64_t(1) << 31) && 2 * p.class_points * 64 < (int64_t(1) << 31)
                       ? kMaxBatchM : 0;
     if (batch_m > 0) {
         // the batched kernel is one more launch: worth it once its rows hold a real share
@@ -581,6 +594,59 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
             if (d.m <= batch_m) p.dense_bwork += d.m;
         }
     }
+    // long rows: sub-row regions past the documents' and classes' grids, tables of m2
+    for (size_t c = 0; c < p.classes.size(); ++c) {
+        const int m1 = lr_m1[c];
+        if (m1 == 0) continue;
+        const Seg& cs = p.classes[c];
+        const int m2 = cs.m / m1;
+        const int64_t vcls = p.class_points + p.class_points_lr;
+        p.class_points_lr += cs.P;
+        const int32_t dense_off = static_cast<int32_t>(p.dense_tab.size() / 4);
+        if (m2 <= 32)
+            build_dense_tables(m2, n1, &p.dense_tab);
+        else
+            build_partner_tables(m2, n1, &p.dense_tab);
+        p.lr_cls_items.push_back(LrItem{cs.grid_off, vcls, cs.m, m1, m2, cs.tw_off});
+        HostPlan::LrLaunch L{m1, (m2 + 15) / 16, 0, 0, 0, 0, 0.0};
+        const int first = static_cast<int>(p.lr_idx.size());
+        for (const Seg& d : p.docs) {
+            if (d.cls != cs.cls) continue;
+            const int64_t vdoc = p.grid_points + p.grid_points_lr;
+            p.grid_points_lr += d.P;
+            p.lr_doc_items.push_back(LrItem{d.grid_off, vdoc, d.m, m1, m2, d.tw_off});
+            Seg v = d;
+            v.m = m2;
+            v.grid_off = vdoc;
+            v.spec_off = static_cast<int32_t>(vcls);
+            v.dense_off = dense_off;
+            p.lr_segs.push_back(v);
+            v.spec_off = static_cast<int32_t>(vdoc);  // the filter gradient's own rows
+            p.lr_gsegs.push_back(v);
+            p.lr_idx.push_back(static_cast<int32_t>(p.lr_segs.size()) - 1);
+            L.work += d.m;
+        }
+        const int n = static_cast<int>(p.lr_idx.size()) - first;
+        const int ng = (n + kMaxGroupDocs - 1) / kMaxGroupDocs;
+        L.grp0 = static_cast<int>(p.lr_groups.size() / 2);
+        for (int g = 0, f = first; g < ng; ++g) {
+            const int cnt = n / ng + (g < n % ng ? 1 : 0);
+            p.lr_groups.push_back(f);
+            p.lr_groups.push_back(cnt);
+            f += cnt;
+        }
+        L.grp_n = ng;
+        L.dgrp0 = static_cast<int>(p.lr_groups.size() / 2);
+        for (int k = 0; k < n; ++k) {
+            p.lr_groups.push_back(first + k);
+            p.lr_groups.push_back(1);
+        }
+        L.dgrp_n = n;
+        p.lr_launches.push_back(L);
+    }
+    if (p.class_points + p.class_points_lr > (int64_t(1) << 31) - 1 ||
+        p.grid_points + p.grid_points_lr > (int64_t(1) << 31) - 1)
+        return BuildError::kUnsupported;
     *out = std::move(p);
     return BuildError::kOk;
 }

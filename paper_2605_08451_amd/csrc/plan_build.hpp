@@ -56,6 +56,17 @@ struct HostPlan {
     // takes each document's second rows from that document)
     int32_t dense_bgrp0 = 0, dense_bgrp_n = 0;
     double dense_bwork = 0;                          // their summed row sizes
+    // long rows: the documents' and classes' first-level items, the virtual documents
+    // (m = m2, offsets into the sub-row regions; spec_off of lr_segs points at the
+    // class's sub-rows, of lr_gsegs at the document's own), identity indices, and per
+    // long class one row launch of N1 m1 rows with its class groups and one-document
+    // groups (pairs into lr_idx)
+    std::vector<LrItem> lr_doc_items, lr_cls_items;
+    std::vector<Seg> lr_segs, lr_gsegs;
+    std::vector<int32_t> lr_idx, lr_groups;
+    struct LrLaunch { int m1, nb, grp0, grp_n, dgrp0, dgrp_n; double work; };
+    std::vector<LrLaunch> lr_launches;
+    int64_t grid_points_lr = 0, class_points_lr = 0;  // the sub-row regions
     int64_t grid_points = 0;            // sum over documents of P_i
     int64_t class_points = 0;           // sum over classes of P
     int32_t taps_max = 0;               // largest number of filter taps any class keeps

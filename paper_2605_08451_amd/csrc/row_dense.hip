@@ -203,7 +203,7 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
         const __amdgpu_buffer_rsrc_t rt = row_buffer(tabs + sg->dense_off, kTabU4 * 16);
         for (int c = wave; c < kTabU4 / 64; c += kLdsWaves) lds_copy16(rt, c * 1024 + lane * 16, &tab[c * 64]);
     }
-    const int ub = (n1 - u) & (n1 - 1);
+    const int ub = u == 0 ? 0 : n1 - u;  // n1 need not be a power of two (sub-row documents)
     RowBuffers rb = row_buffers(grid, grid_pb_stride, fgrid, fgrid_pb_stride, sg, pb, u, ub);
     // the four rows [fu, fb, xu, xb] as [point][16 pairs], 16 points per instruction
     if (active) {
@@ -634,7 +634,7 @@ __global__ __launch_bounds__(64 * kBatchWaves) void row_batch_kernel(uint32_t* _
     __syncthreads();  // tables visible to every wave; the only workgroup barrier
     if (!active) return;
 
-    const int ub = (n1 - u) & (n1 - 1);
+    const int ub = u == 0 ? 0 : n1 - u;  // n1 need not be a power of two (sub-row documents)
     const bool self = ub == u;
     const int shift = u == 0 ? 1 : 0;
     const int R = u == 0 ? 1 : 16 / m;  // documents per block

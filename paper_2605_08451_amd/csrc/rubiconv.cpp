@@ -33,6 +33,10 @@ struct rubiconv_plan_s {
     const void* dense_tab = nullptr; // matrix-core row pass operands (inside dev)
     const int32_t* dense_docs = nullptr;  // documents by 16-point block count (inside dev)
     const int32_t* dense_groups = nullptr;  // row-task groups of dense_docs (inside dev)
+    const Seg* lr_segs = nullptr;           // long rows: sub-row documents (inside dev)
+    const Seg* lr_gsegs = nullptr;          //   the same, second rows their own (filter gradient)
+    const int32_t* lr_idx = nullptr;        //   identity indices
+    const int32_t* lr_groups = nullptr;     //   groups of the sub-row launches
     bool device_ready = false;
     LaunchTables doc_t{};
     LaunchTables cls_t{};
@@ -88,6 +92,10 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     const size_t o_dt = off;         off = align_up(off + h.dense_tab.size() * 4);
     const size_t o_dd = off;         off = align_up(off + h.dense_docs.size() * 4);
     const size_t o_dg = off;         off = align_up(off + h.dense_groups.size() * 4);
+    const size_t o_ls = off;         off = align_up(off + h.lr_segs.size() * sizeof(Seg));
+    const size_t o_lg = off;         off = align_up(off + h.lr_gsegs.size() * sizeof(Seg));
+    const size_t o_li = off;         off = align_up(off + h.lr_idx.size() * 4);
+    const size_t o_lq = off;         off = align_up(off + h.lr_groups.size() * 4);
     const size_t total = off;
 
     std::vector<unsigned char> img(total, 0);
@@ -119,6 +127,12 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     if (!h.dense_docs.empty()) std::memcpy(img.data() + o_dd, h.dense_docs.data(), h.dense_docs.size() * 4);
     if (!h.dense_groups.empty())
         std::memcpy(img.data() + o_dg, h.dense_groups.data(), h.dense_groups.size() * 4);
+    if (!h.lr_segs.empty()) {
+        std::memcpy(img.data() + o_ls, h.lr_segs.data(), h.lr_segs.size() * sizeof(Seg));
+        std::memcpy(img.data() + o_lg, h.lr_gsegs.data(), h.lr_gsegs.size() * sizeof(Seg));
+        std::memcpy(img.data() + o_li, h.lr_idx.data(), h.lr_idx.size() * 4);
+        std::memcpy(img.data() + o_lq, h.lr_groups.data(), h.lr_groups.size() * 4);
+    }
 
     int count = 0;
     hipError_t e = hipGetDeviceCount(&count);
@@ -155,6 +169,10 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     pl->dense_tab = base + o_dt;
     pl->dense_docs = reinterpret_cast<const int32_t*>(base + o_dd);
     pl->dense_groups = reinterpret_cast<const int32_t*>(base + o_dg);
+    pl->lr_segs = reinterpret_cast<const Seg*>(base + o_ls);
+    pl->lr_gsegs = reinterpret_cast<const Seg*>(base + o_lg);
+    pl->lr_idx = reinterpret_cast<const int32_t*>(base + o_li);
+    pl->lr_groups = reinterpret_cast<const int32_t*>(base + o_lq);
     if (hipEventCreateWithFlags(&pl->fork, hipEventDisableTiming) != hipSuccess ||
         hipEventCreateWithFlags(&pl->direct_done, hipEventDisableTiming) != hipSuccess)
         return RUBICONV_ERR_HIP;
@@ -266,6 +284,11 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
                                                   plan->grid_pb_stride, plan->doc_t, n_cols, h.npb,
                                                   stream);
     rec.mark(stage(tag, "col_fwd"));
+    // long rows: first level into the sub-row regions (both grids of the filter gradient)
+    for (const rubiconv::LrItem& it : h.lr_doc_items)
+        if (e == hipSuccess)
+            e = rubiconv::launch_lr_step(false, grid, plan->grid_pb_stride, it, plan->doc_t.tw, h.n1,
+                                         h.npb, stream);
     // row pass: the generic kernel (long rows) and one launch per listed size
     // class, spread over the side streams (largest work first, least-loaded stream)
     struct Launch {
@@ -273,6 +296,7 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
         int nb;        // > 0: matrix-core kernel for the documents of that block count
         double work;
         bool batch;    // the batched matrix-core kernel (rows of at most kMaxBatchM points)
+        int lr = -1;   // >= 0: sub-row documents of long-row class launch lr
     };
     std::vector<Launch> launches;
     if (!h.doc_task_seg.empty()) launches.push_back({-1, 0, 1e30, false});
@@ -290,11 +314,20 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
             if ((own_rows ? h.dense_dgrp_n[nb] : h.dense_grp_n[nb]) > 0) launches.push_back({-1, nb, w, false});
         }
     if (h.row_dense && h.dense_bgrp_n > 0) launches.push_back({-1, 1, h.dense_bwork, true});
+    for (size_t k = 0; k < h.lr_launches.size(); ++k)
+        launches.push_back({-1, h.lr_launches[k].nb, h.lr_launches[k].work, false, static_cast<int>(k)});
     std::sort(launches.begin(), launches.end(),
               [](const Launch& a, const Launch& b) { return a.work > b.work; });
     // the largest launch runs on the calling stream itself, the others on side streams
     const int nside = std::min<int>(rubiconv_plan_s::kSideStreams, static_cast<int>(launches.size()) - 1);
     auto launch_one = [&](const Launch& L, hipStream_t s) -> hipError_t {
+        if (L.lr >= 0) {
+            const HostPlan::LrLaunch& R = h.lr_launches[L.lr];
+            return rubiconv::launch_row_dense(
+                R.nb, grid, plan->grid_pb_stride, fgrid, fgrid_pb_stride, own_rows ? plan->lr_gsegs : plan->lr_segs,
+                plan->lr_idx, plan->lr_groups + 2 * (own_rows ? R.dgrp0 : R.grp0), own_rows ? R.dgrp_n : R.grp_n,
+                plan->dense_tab, h.n1 * R.m1, h.npb, corr, s);
+        }
         if (L.batch)
             return rubiconv::launch_row_batch(grid, plan->grid_pb_stride, fgrid, fgrid_pb_stride, t.segs,
                                               plan->dense_docs, plan->dense_groups + 2 * h.dense_bgrp0,
@@ -334,6 +367,10 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
             if (e == hipSuccess) e = hipStreamWaitEvent(stream, plan->join[k], 0);
         }
     }
+    for (const rubiconv::LrItem& it : h.lr_doc_items)
+        if (e == hipSuccess)
+            e = rubiconv::launch_lr_step(true, grid, plan->grid_pb_stride, it, plan->doc_t.tw, h.n1,
+                                         h.npb, stream);
     rec.mark(stage(tag, "row_conv"));
     if (e == hipSuccess)
         e = h.col_mfma ? rubiconv::launch_col_inv_mfma(out_dtype, grid, plan->grid_pb_stride, out,
@@ -389,8 +426,9 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
         return RUBICONV_ERR_UNSUPPORTED;
     }
     const HostPlan& h = pl->h;
-    pl->grid_pb_stride = h.grid_points * kPairsPerBlock;
-    pl->cls_pb_stride = h.class_points * kPairsPerBlock;
+    // the grids hold the documents' (classes') points, then the sub-row regions of long rows
+    pl->grid_pb_stride = (h.grid_points + h.grid_points_lr) * kPairsPerBlock;
+    pl->cls_pb_stride = (h.class_points + h.class_points_lr) * kPairsPerBlock;
     const size_t esz = h.grid_half ? 4 : 8;  // complex fp16 / complex fp32 grid element
     pl->spec_bytes = align_up(static_cast<size_t>(h.npb) * pl->cls_pb_stride * esz);
     pl->dtaps_off = pl->spec_bytes;
@@ -451,6 +489,10 @@ rubiconv_status_t rubiconv_filter_spectrum(rubiconv_plan_t plan, const float* fi
                 : rubiconv::launch_col_fwd(h.r, h.grid_half, 0, taps, 0, h.D, spectrum,
                                            plan->cls_pb_stride, plan->cls_t,
                                            static_cast<int>(h.cls_col_seg.size()), h.npb, stream);
+    for (const rubiconv::LrItem& it : h.lr_cls_items)
+        if (e == hipSuccess)
+            e = rubiconv::launch_lr_step(false, spectrum, plan->cls_pb_stride, it, plan->doc_t.tw, h.n1,
+                                         h.npb, stream);
     rec.mark("filter_col_fwd");
     if (e == hipSuccess && h.direct_taps > 0) {  // the direct path's taps, [T][D] fp32
         e = rubiconv::launch_transpose(filters, h.D, h.direct_taps, h.L,
@@ -530,7 +572,7 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
         reinterpret_cast<uintptr_t>(dk) % 4)
         return RUBICONV_ERR_ARG;
     // the x grid doubles as the "filter" grid: its offsets must fit the 32-bit field
-    if (h.grid_points > INT32_MAX) return RUBICONV_ERR_UNSUPPORTED;
+    if (h.grid_points + h.grid_points_lr > INT32_MAX) return RUBICONV_ERR_UNSUPPORTED;
     if (!plan->device_ready) return RUBICONV_ERR_HIP;
     std::lock_guard<std::mutex> lock(plan->launch_mu);
     StageRecorder rec(plan, stream);
@@ -559,6 +601,10 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
                        : rubiconv::launch_col_fwd(h.r, h.grid_half, h.x_dtype, x, rs, h.D, xgrid,
                                                   plan->grid_pb_stride, plan->doc_t, n_cols, h.npb,
                                                   stream);
+    for (const rubiconv::LrItem& it : h.lr_doc_items)
+        if (e == hipSuccess)
+            e = rubiconv::launch_lr_step(false, xgrid, plan->grid_pb_stride, it, plan->doc_t.tw, h.n1,
+                                         h.npb, stream);
     rec.mark("dk_col_fwd_x");
     if (e == hipSuccess)
         e = enqueue_conv(plan, dy, h.y_dtype, xgrid, plan->grid_pb_stride, plan->grad_t, r,

@@ -210,3 +210,32 @@ def test_batched_short_rows(device, rows, monkeypatch):
     assert_parity(y, oracle.conv_direct(W.x, W.filters, W.cu_seqlens), W.cu_seqlens, "bf16", "y")
     assert_parity(dx, oracle.grad_x(W.filters, dyv, W.cu_seqlens), W.cu_seqlens, "bf16", "dx")
     _check_dk(dk, oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L), "bf16", "dk")
+
+
+def test_long_rows(device, monkeypatch):
+    """Rows longer than 256 points on fp16 grids go through a second four-step level
+    (m = m1 m2 sub-rows of at most 64 points, run by the matrix-core row kernels with
+    N1 m1 rows): first-level sizes 5, 15, 16 and sub-rows of 25 to 64 points, the
+    forward against the full FFT oracle, dx and dk sampled against their sums.  (Sizes
+    here: 270 = 5 x 54, 360 = 6 x 60, 375 = 15 x 25, 400 = 8 x 50, 675 = 15 x 45,
+    1000 = 20 x 50, 1024 = 16 x 64.)"""
+    monkeypatch.setenv("RUBICONV_CLASS_MERGE", "0")   # every document at its own size
+    N = 130000
+    rows = [[N], [47000, N - 47000], [51000, 33920, N - 84920], [2000, N - 2000]]
+    W = wl.make_case(rows, D=32, L=N, x_dtype="bf16", seed=9)
+    dyv, dx, dk, plan = _run(W, device, seed=10)
+    ms = sorted(set(int(m) for m in plan.doc_table()[:, 4]))
+    assert sum(m > 256 for m in ms) >= 4 and 375 in ms and 1024 in ms, ms
+    import paper_2605_08451_amd as rc
+    x, k = to_device(W, device)
+    y = rc.packed_conv(plan, x, rc.filter_spectrum(plan, k)).float().cpu().numpy().astype(np.float64)
+    assert_parity(y, oracle.conv_fft(W.x, W.filters, W.cu_seqlens, threads=ORACLE_THREADS),
+                  W.cu_seqlens, "bf16", "y")
+    rng = np.random.default_rng(11)
+    n = 3000
+    bsd = np.stack([rng.integers(0, W.B, n), rng.integers(0, W.N, n), rng.integers(0, W.D, n)], 1)
+    ref = oracle.grad_x_at(W.filters, dyv, W.cu_seqlens, bsd, threads=ORACLE_THREADS)
+    assert rel_l2(dx[bsd[:, 0], bsd[:, 1], bsd[:, 2]], ref) <= TOL["bf16"]
+    dt = np.stack([rng.integers(0, W.D, 300), rng.integers(0, W.L, 300)], 1)
+    refk = oracle.grad_k_at(W.x, dyv, W.cu_seqlens, W.L, dt, threads=ORACLE_THREADS)
+    assert rel_l2(dk[dt[:, 0], dt[:, 1]], refk) <= TOL["bf16"]
