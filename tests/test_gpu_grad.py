@@ -229,8 +229,12 @@ def test_long_rows(device, monkeypatch):
     import paper_2605_08451_amd as rc
     x, k = to_device(W, device)
     y = rc.packed_conv(plan, x, rc.filter_spectrum(plan, k)).float().cpu().numpy().astype(np.float64)
-    assert_parity(y, oracle.conv_fft(W.x, W.filters, W.cu_seqlens, threads=ORACLE_THREADS),
-                  W.cu_seqlens, "bf16", "y")
+    g, d = assert_parity(y, oracle.conv_fft(W.x, W.filters, W.cu_seqlens, threads=ORACLE_THREADS),
+                         W.cu_seqlens, "bf16", "y")
+    print(f"[long rows] forward: global {g:.2e}, worst document {d:.2e}", file=sys.stderr, flush=True)
+    # one more fp16 rounding of the grid than ordinary rows: a wrong root or partner in
+    # one sub-row would show as a few percent on some positions, above this bar
+    assert d <= 5e-3, d
     rng = np.random.default_rng(11)
     n = 3000
     bsd = np.stack([rng.integers(0, W.B, n), rng.integers(0, W.N, n), rng.integers(0, W.D, n)], 1)
