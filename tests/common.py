@@ -10,7 +10,7 @@ import numpy as np
 import oracle
 import workloads as wl
 
-#: oracle threads: the GPU machine gives one GPU's share of its host cores (16)
+#: oracle threads: one GPU's share of a host's cores (16)
 ORACLE_THREADS = min(16, os.cpu_count() or 1)
 
 #: parity bars: relative L2 error, globally and per document
