@@ -99,6 +99,11 @@ typedef enum {
  * Rows of at most 8 points (bf16 inputs) are transformed 16 / m documents at a time
  * when such rows hold at least a quarter of the grid; RUBICONV_ROW_BATCH = 0 turns
  * this off and 1..8 sets the largest batched row size regardless of the share.
+ * Rows longer than 256 points (bf16 inputs) are split once more, m = m1 m2, into m1
+ * sub-rows of at most 64 (else 128) points each, transformed by the same matrix-core
+ * row kernels as short rows (Algorithm 1's four-step factorisation applied to
+ * the row DFT); RUBICONV_LONG_ROWS = 0 (read when the plan is made) keeps such rows
+ * whole in the generic row kernel instead.
  * The plan copies what it needs; cu_seqlens_host may be freed on return.  Plan
  * creation allocates device memory and copies the document and twiddle tables
  * synchronously (it is not a stream-ordered call).

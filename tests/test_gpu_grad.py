@@ -243,3 +243,30 @@ def test_long_rows(device, monkeypatch):
     dt = np.stack([rng.integers(0, W.D, 300), rng.integers(0, W.L, 300)], 1)
     refk = oracle.grad_k_at(W.x, dyv, W.cu_seqlens, W.L, dt, threads=ORACLE_THREADS)
     assert rel_l2(dk[dt[:, 0], dt[:, 1]], refk) <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_generic_long_rows(device, monkeypatch, dtype):
+    """Rows longer than 256 points in the generic (Stockham in LDS) row kernel: every
+    such row on fp32 grids, and on fp16 grids with the second four-step level off.
+    Forward against the full FFT oracle, dx sampled against its defining sums."""
+    monkeypatch.setenv("RUBICONV_CLASS_MERGE", "0")
+    if dtype == "bf16":
+        monkeypatch.setenv("RUBICONV_LONG_ROWS", "0")
+    N = 130000
+    rows = [[N], [51000, 33920, N - 84920]]
+    W = wl.make_case(rows, D=32, L=N, x_dtype=dtype, seed=19)
+    dyv, dx, _, plan = _run(W, device, seed=20, want_dk=False)
+    ms = sorted(set(int(m) for m in plan.doc_table()[:, 4]))
+    assert sum(m > 256 for m in ms) >= 2, ms
+    import paper_2605_08451_amd as rc
+    x, k = to_device(W, device)
+    y = rc.packed_conv(plan, x, rc.filter_spectrum(plan, k)).float().cpu().numpy().astype(np.float64)
+    g, d = assert_parity(y, oracle.conv_fft(W.x, W.filters, W.cu_seqlens, threads=ORACLE_THREADS),
+                         W.cu_seqlens, dtype, "y")
+    _say(f"[generic long rows] {dtype}: global {g:.2e}, worst document {d:.2e}, sizes {ms}")
+    rng = np.random.default_rng(21)
+    n = 2000
+    bsd = np.stack([rng.integers(0, W.B, n), rng.integers(0, W.N, n), rng.integers(0, W.D, n)], 1)
+    ref = oracle.grad_x_at(W.filters, dyv, W.cu_seqlens, bsd, threads=ORACLE_THREADS)
+    assert rel_l2(dx[bsd[:, 0], bsd[:, 1], bsd[:, 2]], ref) <= TOL[dtype]
