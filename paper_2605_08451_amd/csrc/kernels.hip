@@ -665,19 +665,20 @@ __global__ __launch_bounds__(256) void lag_sum_kernel(const float* __restrict__ 
 }
 
 // The same transpose for tap rows whose stride is a multiple of 4 floats (taps <= stride):
-// tiles of 128 channels x 64 taps, 16-byte loads along taps (256-byte runs per channel)
-// and 16-byte stores of four pairs along channels (256-byte runs per tap).
+// tiles of TC channels x 64 taps, 16-byte loads along taps (256-byte runs per channel)
+// and 16-byte stores of four pairs along channels (2 TC-byte runs per tap).
+template <int TC>
 __global__ __launch_bounds__(256) void transpose_pairs4_kernel(const float* __restrict__ in, int D,
                                                                int taps, int in_ld,
                                                                uint32_t* __restrict__ out) {
-    __shared__ float tile[128][65];
-    const int t0 = blockIdx.x * 64, c0 = blockIdx.y * 128;
+    __shared__ float tile[TC][65];
+    const int t0 = blockIdx.x * 64, c0 = blockIdx.y * TC;
     const int tid = threadIdx.x;
     {
         const int tx = tid & 15, cy = tid >> 4;  // 4 taps per thread, 16 channel rows per pass
         const int t = t0 + 4 * tx;
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
+        for (int k = 0; k < TC / 16; ++k) {
             const int c = c0 + cy + 16 * k;
             float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
             if (c < D && t < taps) {  // t + 3 < in_ld: in_ld is a multiple of 4, taps <= in_ld
@@ -689,10 +690,12 @@ __global__ __launch_bounds__(256) void transpose_pairs4_kernel(const float* __re
     }
     __syncthreads();
     const int half_d = D / 2;
-    const int qx = tid & 15, ty = tid >> 4;  // 4 pairs per thread, 16 tap rows per pass
+    constexpr int QT = TC / 8;         // threads per tap row, 4 pairs each
+    constexpr int RP = 256 / QT;       // tap rows per pass
+    const int qx = tid % QT, ty = tid / QT;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int tt = ty + 16 * k, t = t0 + tt;
+    for (int k = 0; k < 64 / RP; ++k) {
+        const int tt = ty + RP * k, t = t0 + tt;
         const int q0 = c0 / 2 + 4 * qx;
         if (t < taps && q0 < half_d) {
             uint32_t w[4];
@@ -898,8 +901,8 @@ hipError_t launch_transpose_pairs(const float* in, int D, int taps, int in_ld, v
     // 16-byte paths: whole float4 groups of taps (aligned rows) and of pairs (D / 2)
     if (taps <= in_ld && in_ld % 4 == 0 && (D / 2) % 4 == 0 &&
         reinterpret_cast<uintptr_t>(in) % 16 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0) {
-        const dim3 g((taps + 63) / 64, (D + 127) / 128);
-        hipLaunchKernelGGL(transpose_pairs4_kernel, g, dim3(256), 0, stream, in, D, taps, in_ld,
+        const dim3 g((taps + 63) / 64, (D + 63) / 64);
+        hipLaunchKernelGGL(transpose_pairs4_kernel<64>, g, dim3(256), 0, stream, in, D, taps, in_ld,
                            static_cast<uint32_t*>(out));
         return hipGetLastError();
     }
