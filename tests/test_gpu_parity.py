@@ -74,9 +74,10 @@ def test_ragged_edges(device, n1, dtype):
         assert_parity(y, reference(W), W.cu_seqlens, dtype, f"L={L}")
 
 
-@pytest.mark.parametrize("D", [1, 2, 3, 31, 33, 64])
+@pytest.mark.parametrize("D", [1, 2, 3, 8, 31, 33, 64, 96, 200])
 def test_channel_counts(device, D):
-    """Odd D (a lone last channel), D below and above one pair block of 32 channels."""
+    """Odd D (a lone last channel), D below and above one pair block of 32 channels, and
+    D % 8 = 0 with partial 64-channel tiles of the filter transpose (96, 200)."""
     rng = np.random.default_rng(D)
     rows = wl.random_rows(rng, 2, 1000, 400)
     for dtype in ("f32", "bf16"):
