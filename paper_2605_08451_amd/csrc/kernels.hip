@@ -664,6 +664,66 @@ __global__ __launch_bounds__(256) void lag_sum_kernel(const float* __restrict__ 
     }
 }
 
+// The same sum for plans with few documents (fewer than one round per wave above, so
+// most of those waves would idle): each wave owns 8 lags of the workgroup's 32 and sums
+// every document itself, longest first, in document order; the workgroup's 32 x 256
+// block of dk goes out through LDS with lanes along lags (128-byte runs per channel).
+__global__ __launch_bounds__(256) void lag_sum_few_kernel(const float* __restrict__ r,
+                                                         const Seg* __restrict__ segs, int n_docs,
+                                                         int N, int D, int L, float* __restrict__ dk) {
+    constexpr int C = 256;  // channels per workgroup, four per lane
+    constexpr int T = 8;    // lags per wave
+    constexpr int U = 4;    // documents per round of loads
+    __shared__ float part[4 * T][C + 1];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int tau0 = blockIdx.x * (4 * T) + w * T, d0 = blockIdx.y * C;
+    const int d = d0 + 4 * lane;
+    float4 acc[T];
+#pragma unroll
+    for (int i = 0; i < T; ++i) acc[i] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if (d < D && tau0 < L) {
+        for (int k = 0; k < n_docs; k += U) {
+            if ((segs[k].len < L ? segs[k].len : L) <= tau0) break;
+            float4 v[U][T];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                int lags = 0;
+                const float* base = r;
+                if (k + u < n_docs) {
+                    const Seg& sg = segs[k + u];
+                    lags = sg.len < L ? sg.len : L;
+                    base = r + (static_cast<int64_t>(sg.row) * N + sg.start) * D + d;
+                }
+#pragma unroll
+                for (int i = 0; i < T; ++i)
+                    v[u][i] = tau0 + i < lags
+                                  ? *reinterpret_cast<const float4*>(base + static_cast<int64_t>(tau0 + i) * D)
+                                  : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int i = 0; i < T; ++i) {
+                    acc[i].x += v[u][i].x; acc[i].y += v[u][i].y;
+                    acc[i].z += v[u][i].z; acc[i].w += v[u][i].w;
+                }
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < T; ++i) {
+        float* row = &part[w * T + i][4 * lane];
+        row[0] = acc[i].x; row[1] = acc[i].y; row[2] = acc[i].z; row[3] = acc[i].w;
+    }
+    __syncthreads();
+    // write: 32 lanes along lags, 8 channels per instruction
+    const int tl = threadIdx.x & 31, jq = threadIdx.x >> 5;
+    const int tau = blockIdx.x * (4 * T) + tl;
+    for (int j = jq; j < C; j += 8) {
+        const int dd = d0 + j;
+        if (dd < D && tau < L) dk[static_cast<int64_t>(dd) * L + tau] = part[tl][j];
+    }
+}
+
 // The same transpose for tap rows whose stride is a multiple of 4 floats (taps <= stride):
 // tiles of TC channels x 64 taps, 16-byte loads along taps (256-byte runs per channel)
 // and 16-byte stores of four pairs along channels (2 TC-byte runs per tap).
@@ -885,6 +945,11 @@ hipError_t launch_direct(int mode, int max_len, int a_dtype, const void* a, int 
 hipError_t launch_lag_sum(const float* r, const Seg* segs, int n_docs, int N, int D, int L,
                           float* dk, hipStream_t stream) {
     if (D <= 0 || L <= 0) return hipSuccess;
+    if (D % 4 == 0 && n_docs < 16) {  // fewer documents than the waves' rounds below
+        const dim3 g((L + 31) / 32, (D + 255) / 256), b(256);
+        hipLaunchKernelGGL(lag_sum_few_kernel, g, b, 0, stream, r, segs, n_docs, N, D, L, dk);
+        return hipGetLastError();
+    }
     if (D % 4 == 0) {  // whole float4 groups: 16-byte loads (r is 256-byte aligned)
         const dim3 g((L + 255) / 256 * 32, (D + 255) / 256), b(256);
         hipLaunchKernelGGL(lag_sum_kernel<4>, g, b, 0, stream, r, segs, n_docs, N, D, L, dk);
