@@ -115,6 +115,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                                                            int64_t src_row_stride, int D,
                                                            uint32_t* __restrict__ grid,
                                                            int64_t grid_pb_stride, LaunchTables t,
+                                                           GridScale sc,
                                                            const u4* __restrict__ mt, int npb,
                                                            int ntasks) {
     // stage-2 operands, shared by the workgroup's four column tasks
@@ -181,6 +182,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 #pragma unroll
         for (int o = 0; o < 2; ++o) a[o] = mt[kMtFwd1F16 + o * 64 + lane];
     }
+    // range scale of this lane's pair, applied to the fp32 products before fp16 rounding
+    const float in_mul = sc.pair[pb * kPairsPerBlock + p].x * sc.glob->x;
     __builtin_amdgcn_sched_barrier(0);
 
     uint32_t y[16][4];
@@ -196,7 +199,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             dim = mma_f16(a[1], xb[n2], zero);
         }
 #pragma unroll
-        for (int r = 0; r < 4; ++r) y[n2][r] = pack_h2(dre[r], dim[r]);
+        for (int r = 0; r < 4; ++r) y[n2][r] = pack_h2(dre[r] * in_mul, dim[r] * in_mul);
     }
     // y[n2][r] = D[k1 = 4h + r][n2]; regroup so that lane group h holds n2 = 4h + r'
 #pragma unroll
@@ -247,7 +250,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                                                            int64_t grid_pb_stride,
                                                            void* __restrict__ dst,
                                                            int64_t dst_row_stride, int D,
-                                                           LaunchTables t,
+                                                           LaunchTables t, GridScale sc,
                                                            const u4* __restrict__ mt, int npb,
                                                            int ntasks) {
     constexpr int ES = std::is_same<TY, F32>::value ? 4 : 2;  // bytes per output channel
@@ -296,6 +299,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     const u4 are1 = mt[kMtInv1 + lane];
     const u4 aim1 = mt[kMtInv1 + 64 + lane];
     const float2* twf = t.tw + sg->twf_off;
+    // undoes the range scales of this lane's pair on the fp32 outputs
+    const float out_mul = sc.pair[pb * kPairsPerBlock + p].y * sc.glob->y;
     __builtin_amdgcn_sched_barrier(0);
 
     uint32_t z[16][4];
@@ -334,6 +339,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         st_lane[q] = (static_cast<uint32_t>(m) * 16u * n1 * D +
                       2 * (pb * kPairsPerBlock + QPL * ((q * 64 + lane) % LPT))) * ES;
     }
+    // fp32 outputs: the scales of the QPL = 2 pairs a lane stores (the same in both rounds)
+    float st_mul[2] = {1.0f, 1.0f};
+    if constexpr (std::is_same<TY, F32>::value) {
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+            st_mul[c] = sc.pair[pb * kPairsPerBlock + QPL * (lane % LPT) + c].y * sc.glob->y;
+    }
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
 #pragma unroll
@@ -350,9 +362,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             for (int r2 = 0; r2 < 4; ++r2) {
                 const int e = (4 * r2 + h) * 16 + p;  // [n1][pair]
                 if constexpr (std::is_same<TY, F32>::value) {
+                    // fp32 outputs go to LDS as the products left them; the scale is applied
+                    // after the round trip (below): a multiply here, between the products and
+                    // the LDS stores, gave 4-5% errors on this variant (see the design notes)
                     *reinterpret_cast<u2*>(ring + 2 * e) = u2{__float_as_uint(dre[r2]), __float_as_uint(dim[r2])};
                 } else {
-                    ring[e] = pack_bf2(dre[r2], dim[r2]);
+                    ring[e] = pack_bf2(dre[r2] * out_mul, dim[r2] * out_mul);
                 }
             }
             wave_lds_fence();
@@ -360,7 +375,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                 sub_buffer(doc, doc_bytes, static_cast<int64_t>(m * n2 + j) * D * ES);
 #pragma unroll
             for (int q = 0; q < ROUNDS; ++q) {
-                const u4 v = *reinterpret_cast<const u4*>(ring + (q * 64 + lane) * 4);
+                u4 v = *reinterpret_cast<const u4*>(ring + (q * 64 + lane) * 4);
+                if constexpr (std::is_same<TY, F32>::value) {
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) v[c] = __float_as_uint(__uint_as_float(v[c]) * st_mul[c / 2]);
+                }
                 __builtin_amdgcn_raw_buffer_store_b128(v, rs, static_cast<int>(st_lane[q]), 0, 0);
             }
             wave_lds_fence();  // the ring is rewritten for the next n2
@@ -372,7 +391,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 
 hipError_t launch_col_fwd_mfma(int src_dtype, const void* src, int64_t src_row_stride, int D,
                                void* grid, int64_t grid_pb_stride, const LaunchTables& t,
-                               const void* mtab, int n_cols, int npb, hipStream_t stream) {
+                               GridScale sc, const void* mtab, int n_cols, int npb,
+                               hipStream_t stream) {
     if (n_cols == 0) return hipSuccess;
     const int ntasks = n_cols * npb;
     const dim3 g((ntasks + 3) / 4), b(256);
@@ -380,16 +400,17 @@ hipError_t launch_col_fwd_mfma(int src_dtype, const void* src, int64_t src_row_s
     uint32_t* gp = static_cast<uint32_t*>(grid);
     if (src_dtype == 1)
         hipLaunchKernelGGL(col_fwd_mfma_kernel<kBf16In>, g, b, 0, stream, src, src_row_stride, D, gp,
-                           grid_pb_stride, t, mt, npb, ntasks);
+                           grid_pb_stride, t, sc, mt, npb, ntasks);
     else
         hipLaunchKernelGGL(col_fwd_mfma_kernel<kF16In>, g, b, 0, stream, src, src_row_stride, D, gp,
-                           grid_pb_stride, t, mt, npb, ntasks);
+                           grid_pb_stride, t, sc, mt, npb, ntasks);
     return hipGetLastError();
 }
 
 hipError_t launch_col_inv_mfma(int y_dtype, const void* grid, int64_t grid_pb_stride, void* dst,
                                int64_t dst_row_stride, int D, const LaunchTables& t,
-                               const void* mtab, int n_cols, int npb, hipStream_t stream) {
+                               GridScale sc, const void* mtab, int n_cols, int npb,
+                               hipStream_t stream) {
     if (n_cols == 0) return hipSuccess;
     const int ntasks = n_cols * npb;
     const dim3 g((ntasks + 3) / 4), b(256);
@@ -397,10 +418,10 @@ hipError_t launch_col_inv_mfma(int y_dtype, const void* grid, int64_t grid_pb_st
     const uint32_t* gp = static_cast<const uint32_t*>(grid);
     if (y_dtype == 1)
         hipLaunchKernelGGL(col_inv_mfma_kernel<BF16>, g, b, 0, stream, gp, grid_pb_stride, dst,
-                           dst_row_stride, D, t, mt, npb, ntasks);
+                           dst_row_stride, D, t, sc, mt, npb, ntasks);
     else
         hipLaunchKernelGGL(col_inv_mfma_kernel<F32>, g, b, 0, stream, gp, grid_pb_stride, dst,
-                           dst_row_stride, D, t, mt, npb, ntasks);
+                           dst_row_stride, D, t, sc, mt, npb, ntasks);
     return hipGetLastError();
 }
 

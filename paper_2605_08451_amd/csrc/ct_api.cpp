@@ -173,7 +173,7 @@ rubiconv_status_t rubiconv_ct_filter_spectrum(rubiconv_ct_plan_t plan, const flo
     float* taps = static_cast<float*>(workspace);
     void* fgrid = static_cast<char*>(workspace) + plan->taps_bytes;
     const DevLayout& f = plan->filt;
-    hipError_t e = rubiconv::launch_transpose(filters, h.D, h.taps_max, h.L, taps, h.D, stream);
+    hipError_t e = rubiconv::launch_transpose(filters, h.D, h.taps_max, h.L, taps, h.D, nullptr, stream);
     if (e == hipSuccess)
         e = rubiconv::ct::launch_front(f.docs, f.long_tile_doc, f.n_long_tiles, 0, taps, 0, h.D, h.npb,
                                        false, fgrid, h.filt.long_points, plan->tw, stream);

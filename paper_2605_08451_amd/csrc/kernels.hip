@@ -154,7 +154,7 @@ __global__ __launch_bounds__(16 * R) void col_fwd_kernel(const void* __restrict_
                                                          int64_t src_row_stride, int D,
                                                          G* __restrict__ grid,
                                                          int64_t grid_pb_stride, LaunchTables t,
-                                                         int npb) {
+                                                         GridScale sc, int npb) {
     constexpr int LD = R * 16 + 16;
     constexpr int ES = elem_bytes<TX>();
     __shared__ float2 lds[R * LD];
@@ -189,10 +189,11 @@ __global__ __launch_bounds__(16 * R) void col_fwd_kernel(const void* __restrict_
 
     const float2* twf = t.tw + sg->twf_off;
     G* out = grid + pb * grid_pb_stride + (sg->grid_off + j) * kPairsPerBlock + p;
+    const float mul = sc.pair[pb * kPairsPerBlock + p].x * sc.glob->x;
 #pragma unroll
     for (int k2 = 0; k2 < R; ++k2) {
         const int u = q + R * k2;
-        gstore(out + static_cast<int64_t>(u) * m * kPairsPerBlock, cmul(v[k2], twf[u * j]));
+        gstore(out + static_cast<int64_t>(u) * m * kPairsPerBlock, cscale(cmul(v[k2], twf[u * j]), mul));
     }
 }
 
@@ -201,7 +202,7 @@ __global__ __launch_bounds__(16 * R) void col_inv_kernel(const G* __restrict__ g
                                                          int64_t grid_pb_stride,
                                                          void* __restrict__ dst,
                                                          int64_t dst_row_stride, int D,
-                                                         LaunchTables t, int npb) {
+                                                         LaunchTables t, GridScale sc, int npb) {
     constexpr int LD = R * 16 + 16;
     constexpr int ES = elem_bytes<TY>();
     __shared__ float2 lds[R * LD];
@@ -229,6 +230,9 @@ __global__ __launch_bounds__(16 * R) void col_inv_kernel(const G* __restrict__ g
 #pragma unroll
     for (int k1 = 0; k1 < R; ++k1) v[k1] = lds[k1 * LD + q * 16 + p];  // thread q holds n2 = q
     Dft<R, 1>::run(v);  // over k1 -> n1
+    const float mul = sc.pair[pb * kPairsPerBlock + p].y * sc.glob->y;
+#pragma unroll
+    for (int n1 = 0; n1 < R; ++n1) v[n1] = cscale(v[n1], mul);
 
     if (MODE != kFull && ch >= D) return;
     char* doc = static_cast<char*>(dst) + (static_cast<int64_t>(sg->row) * dst_row_stride +
@@ -449,17 +453,39 @@ __global__ __launch_bounds__(256) void row_conv_kernel(G* __restrict__ grid,
 
 // ---------------------------------------------------------------- transpose
 // out[c][r] = in[r][c] for r < rows, c < cols (32 x 32 tiles through LDS).
+// Sum of |tile[row][0 .. 31]| for the rows of a tile in LDS, in a fixed order (the same
+// result on every call): eight threads per row, four values each, then a butterfly over
+// the eight.  Thread `tid` of 256 covers row tid / 8; the result is in every thread of
+// the row's group.
+template <int LDW>
+__device__ __forceinline__ float tile_row_abs_sum32(const float (*tile)[LDW], int row_base, int tid) {
+    const int r = row_base + (tid >> 3), part = tid & 7;
+    float a = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) a += fabsf(tile[r][4 * part + i]);
+    a += __shfl_xor(a, 1);
+    a += __shfl_xor(a, 2);
+    a += __shfl_xor(a, 4);
+    return a;
+}
+
 __global__ __launch_bounds__(256) void transpose_kernel(const float* __restrict__ in, int rows,
                                                         int cols, int in_ld,
-                                                        float* __restrict__ out, int out_ld) {
+                                                        float* __restrict__ out, int out_ld,
+                                                        float* __restrict__ partials) {
     __shared__ float tile[32][33];
     const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
     const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
     for (int k = ty; k < 32; k += 8) {
         const int rr = r0 + k, cc = c0 + tx;
-        if (rr < rows && cc < cols) tile[k][tx] = in[static_cast<int64_t>(rr) * in_ld + cc];
+        tile[k][tx] = (rr < rows && cc < cols) ? in[static_cast<int64_t>(rr) * in_ld + cc] : 0.0f;
     }
     __syncthreads();
+    if (partials != nullptr) {  // per row (channel): sum of |k| over this tile's 32 columns (taps)
+        const float a = tile_row_abs_sum32<33>(tile, 0, threadIdx.x);
+        const int rr = r0 + (threadIdx.x >> 3);
+        if ((threadIdx.x & 7) == 0 && rr < rows) partials[static_cast<int64_t>(blockIdx.x) * rows + rr] = a;
+    }
     for (int k = ty; k < 32; k += 8) {
         const int cc = c0 + k, rr = r0 + tx;
         if (rr < rows && cc < cols) out[static_cast<int64_t>(cc) * out_ld + rr] = tile[tx][k];
@@ -471,7 +497,8 @@ __global__ __launch_bounds__(256) void transpose_kernel(const float* __restrict_
 // channels x 32 taps through LDS: coalesced reads along taps, writes along pairs.
 __global__ __launch_bounds__(256) void transpose_pairs_kernel(const float* __restrict__ in, int D,
                                                               int taps, int in_ld,
-                                                              uint32_t* __restrict__ out) {
+                                                              uint32_t* __restrict__ out,
+                                                              float* __restrict__ partials) {
     __shared__ float tile[64][33];
     const int t0 = blockIdx.x * 32, c0 = blockIdx.y * 64;
     const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
@@ -480,6 +507,14 @@ __global__ __launch_bounds__(256) void transpose_pairs_kernel(const float* __res
         tile[k][tx] = (c < D && t < taps) ? in[static_cast<int64_t>(c) * in_ld + t] : 0.0f;
     }
     __syncthreads();
+    if (partials != nullptr) {  // per channel: sum of |k| over this tile's 32 taps
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const float a = tile_row_abs_sum32<33>(tile, 32 * h, threadIdx.x);
+            const int c = c0 + 32 * h + (threadIdx.x >> 3);
+            if ((threadIdx.x & 7) == 0 && c < D) partials[static_cast<int64_t>(blockIdx.x) * D + c] = a;
+        }
+    }
     const int half_d = D / 2;
     for (int k = ty; k < 32; k += 8) {
         const int t = t0 + k, q = c0 / 2 + tx;
@@ -730,7 +765,8 @@ __global__ __launch_bounds__(256) void lag_sum_few_kernel(const float* __restric
 template <int TC>
 __global__ __launch_bounds__(256) void transpose_pairs4_kernel(const float* __restrict__ in, int D,
                                                                int taps, int in_ld,
-                                                               uint32_t* __restrict__ out) {
+                                                               uint32_t* __restrict__ out,
+                                                               float* __restrict__ partials) {
     __shared__ float tile[TC][65];
     const int t0 = blockIdx.x * 64, c0 = blockIdx.y * TC;
     const int tid = threadIdx.x;
@@ -749,6 +785,22 @@ __global__ __launch_bounds__(256) void transpose_pairs4_kernel(const float* __re
         }
     }
     __syncthreads();
+    if (partials != nullptr) {  // per channel: sum of |k| over each 32-tap half of the tile
+#pragma unroll
+        for (int rb = 0; rb < TC; rb += 32)
+#pragma unroll
+            for (int th = 0; th < 2; ++th) {
+                const int r = rb + (threadIdx.x >> 3), part = threadIdx.x & 7;
+                float a = 0.0f;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) a += fabsf(tile[r][32 * th + 4 * part + i]);
+                a += __shfl_xor(a, 1);
+                a += __shfl_xor(a, 2);
+                a += __shfl_xor(a, 4);
+                const int c = c0 + r;
+                if (part == 0 && c < D) partials[static_cast<int64_t>(2 * blockIdx.x + th) * D + c] = a;
+            }
+    }
     const int half_d = D / 2;
     constexpr int QT = TC / 8;         // threads per tap row, 4 pairs each
     constexpr int RP = 256 / QT;       // tap rows per pass
@@ -779,84 +831,84 @@ static int col_mode(int D) { return D % 32 == 0 ? kFull : (D % 2 == 0 ? kEven : 
 
 template <int R, class G, int MODE>
 static hipError_t col_fwd_rgm(int x_dtype, const void* src, int64_t rs, int D, void* grid,
-                              int64_t gs, const LaunchTables& t, int n_cols, int npb,
+                              int64_t gs, const LaunchTables& t, GridScale sc, int n_cols, int npb,
                               hipStream_t stream) {
     const dim3 g(static_cast<unsigned>(n_cols) * npb), b(16 * R);
     G* gp = static_cast<G*>(grid);
     if (x_dtype == 0)
         hipLaunchKernelGGL((col_fwd_kernel<R, F32, G, MODE>), g, b, 0, stream, src, rs, D, gp, gs,
-                           t, npb);
+                           t, sc, npb);
     else
         hipLaunchKernelGGL((col_fwd_kernel<R, BF16, G, MODE>), g, b, 0, stream, src, rs, D, gp, gs,
-                           t, npb);
+                           t, sc, npb);
     return hipGetLastError();
 }
 
 template <int R, class G>
 static hipError_t col_fwd_rg(int x_dtype, const void* src, int64_t rs, int D, void* grid,
-                             int64_t gs, const LaunchTables& t, int n_cols, int npb,
+                             int64_t gs, const LaunchTables& t, GridScale sc, int n_cols, int npb,
                              hipStream_t stream) {
     switch (col_mode(D)) {
-        case kFull: return col_fwd_rgm<R, G, kFull>(x_dtype, src, rs, D, grid, gs, t, n_cols, npb, stream);
-        case kEven: return col_fwd_rgm<R, G, kEven>(x_dtype, src, rs, D, grid, gs, t, n_cols, npb, stream);
-        default: return col_fwd_rgm<R, G, kOdd>(x_dtype, src, rs, D, grid, gs, t, n_cols, npb, stream);
+        case kFull: return col_fwd_rgm<R, G, kFull>(x_dtype, src, rs, D, grid, gs, t, sc, n_cols, npb, stream);
+        case kEven: return col_fwd_rgm<R, G, kEven>(x_dtype, src, rs, D, grid, gs, t, sc, n_cols, npb, stream);
+        default: return col_fwd_rgm<R, G, kOdd>(x_dtype, src, rs, D, grid, gs, t, sc, n_cols, npb, stream);
     }
 }
 
 hipError_t launch_col_fwd(int r, bool half, int x_dtype, const void* src, int64_t src_row_stride,
                           int D, void* grid, int64_t grid_pb_stride, const LaunchTables& t,
-                          int n_cols, int npb, hipStream_t stream) {
+                          GridScale sc, int n_cols, int npb, hipStream_t stream) {
     if (n_cols == 0) return hipSuccess;
     if (r == 16)
         return half ? col_fwd_rg<16, __half2>(x_dtype, src, src_row_stride, D, grid, grid_pb_stride,
-                                              t, n_cols, npb, stream)
+                                              t, sc, n_cols, npb, stream)
                     : col_fwd_rg<16, float2>(x_dtype, src, src_row_stride, D, grid, grid_pb_stride,
-                                             t, n_cols, npb, stream);
+                                             t, sc, n_cols, npb, stream);
     return half ? col_fwd_rg<8, __half2>(x_dtype, src, src_row_stride, D, grid, grid_pb_stride, t,
-                                         n_cols, npb, stream)
+                                         sc, n_cols, npb, stream)
                 : col_fwd_rg<8, float2>(x_dtype, src, src_row_stride, D, grid, grid_pb_stride, t,
-                                        n_cols, npb, stream);
+                                        sc, n_cols, npb, stream);
 }
 
 template <int R, class G, int MODE>
 static hipError_t col_inv_rgm(int y_dtype, const void* grid, int64_t gs, void* dst, int64_t rs,
-                              int D, const LaunchTables& t, int n_cols, int npb,
+                              int D, const LaunchTables& t, GridScale sc, int n_cols, int npb,
                               hipStream_t stream) {
     const dim3 g(static_cast<unsigned>(n_cols) * npb), b(16 * R);
     const G* gp = static_cast<const G*>(grid);
     if (y_dtype == 0)
         hipLaunchKernelGGL((col_inv_kernel<R, F32, G, MODE>), g, b, 0, stream, gp, gs, dst, rs, D,
-                           t, npb);
+                           t, sc, npb);
     else
         hipLaunchKernelGGL((col_inv_kernel<R, BF16, G, MODE>), g, b, 0, stream, gp, gs, dst, rs, D,
-                           t, npb);
+                           t, sc, npb);
     return hipGetLastError();
 }
 
 template <int R, class G>
 static hipError_t col_inv_rg(int y_dtype, const void* grid, int64_t gs, void* dst, int64_t rs,
-                             int D, const LaunchTables& t, int n_cols, int npb,
+                             int D, const LaunchTables& t, GridScale sc, int n_cols, int npb,
                              hipStream_t stream) {
     switch (col_mode(D)) {
-        case kFull: return col_inv_rgm<R, G, kFull>(y_dtype, grid, gs, dst, rs, D, t, n_cols, npb, stream);
-        case kEven: return col_inv_rgm<R, G, kEven>(y_dtype, grid, gs, dst, rs, D, t, n_cols, npb, stream);
-        default: return col_inv_rgm<R, G, kOdd>(y_dtype, grid, gs, dst, rs, D, t, n_cols, npb, stream);
+        case kFull: return col_inv_rgm<R, G, kFull>(y_dtype, grid, gs, dst, rs, D, t, sc, n_cols, npb, stream);
+        case kEven: return col_inv_rgm<R, G, kEven>(y_dtype, grid, gs, dst, rs, D, t, sc, n_cols, npb, stream);
+        default: return col_inv_rgm<R, G, kOdd>(y_dtype, grid, gs, dst, rs, D, t, sc, n_cols, npb, stream);
     }
 }
 
 hipError_t launch_col_inv(int r, bool half, int y_dtype, const void* grid, int64_t grid_pb_stride,
                           void* dst, int64_t dst_row_stride, int D, const LaunchTables& t,
-                          int n_cols, int npb, hipStream_t stream) {
+                          GridScale sc, int n_cols, int npb, hipStream_t stream) {
     if (n_cols == 0) return hipSuccess;
     if (r == 16)
         return half ? col_inv_rg<16, __half2>(y_dtype, grid, grid_pb_stride, dst, dst_row_stride, D,
-                                              t, n_cols, npb, stream)
+                                              t, sc, n_cols, npb, stream)
                     : col_inv_rg<16, float2>(y_dtype, grid, grid_pb_stride, dst, dst_row_stride, D,
-                                             t, n_cols, npb, stream);
+                                             t, sc, n_cols, npb, stream);
     return half ? col_inv_rg<8, __half2>(y_dtype, grid, grid_pb_stride, dst, dst_row_stride, D, t,
-                                         n_cols, npb, stream)
+                                         sc, n_cols, npb, stream)
                 : col_inv_rg<8, float2>(y_dtype, grid, grid_pb_stride, dst, dst_row_stride, D, t,
-                                        n_cols, npb, stream);
+                                        sc, n_cols, npb, stream);
 }
 
 hipError_t launch_row_conv(int n1, bool half, void* grid, int64_t grid_pb_stride,
@@ -961,28 +1013,189 @@ hipError_t launch_lag_sum(const float* r, const Seg* segs, int n_docs, int N, in
 }
 
 hipError_t launch_transpose_pairs(const float* in, int D, int taps, int in_ld, void* out,
-                                  hipStream_t stream) {
+                                  float* partials, int* ntiles, hipStream_t stream) {
+    *ntiles = 0;
     if (D <= 0 || taps <= 0) return hipSuccess;
-    // 16-byte paths: whole float4 groups of taps (aligned rows) and of pairs (D / 2)
+    // 16-byte paths: whole float4 groups of taps (aligned rows) and of pairs (D / 2).  Its
+    // 64-tap tiles write the partial sums of two 32-tap tiles (a last one without taps as
+    // zero): 2 ceil(taps / 64) tiles there, ceil(taps / 32) otherwise.
     if (taps <= in_ld && in_ld % 4 == 0 && (D / 2) % 4 == 0 &&
         reinterpret_cast<uintptr_t>(in) % 16 == 0 && reinterpret_cast<uintptr_t>(out) % 16 == 0) {
         const dim3 g((taps + 63) / 64, (D + 63) / 64);
+        *ntiles = 2 * static_cast<int>(g.x);
         hipLaunchKernelGGL(transpose_pairs4_kernel<64>, g, dim3(256), 0, stream, in, D, taps, in_ld,
-                           static_cast<uint32_t*>(out));
+                           static_cast<uint32_t*>(out), partials);
         return hipGetLastError();
     }
     const dim3 g((taps + 31) / 32, (D + 63) / 64);
+    *ntiles = static_cast<int>(g.x);
     hipLaunchKernelGGL(transpose_pairs_kernel, g, dim3(256), 0, stream, in, D, taps, in_ld,
-                       static_cast<uint32_t*>(out));
+                       static_cast<uint32_t*>(out), partials);
     return hipGetLastError();
 }
 
 hipError_t launch_transpose(const float* in, int rows, int cols, int in_ld, float* out,
-                            int out_ld, hipStream_t stream) {
-    if (rows == 0 || cols == 0) return hipSuccess;
+                            int out_ld, float* partials, hipStream_t stream) {
+    if (rows == 0 || cols == 0) return hipSuccess;  // partials: ceil(cols / 32) tiles
     dim3 g((cols + 31) / 32, (rows + 31) / 32);
     hipLaunchKernelGGL(transpose_kernel, g, dim3(256), 0, stream, in, rows, cols, in_ld, out,
-                       out_ld);
+                       out_ld, partials);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- range scales
+// 2^(target - e) for a finite positive value a < 2^e (frexp), else 1.
+__device__ __forceinline__ float pow2_scale(float a, int target) {
+    if (!(a > 0.0f) || !(a <= 3.0e38f)) return 1.0f;
+    int e;
+    (void)frexpf(a, &e);  // a = f 2^e, 0.5 <= f < 1
+    return ldexpf(1.0f, max(-126, min(127, target - e)));
+}
+
+// One workgroup per 8 channel pairs (16 channels): thread t sums the tiles t / 16,
+// t / 16 + 16, ... of channel t % 16 (16 channels x 4 bytes: 64-byte rows), then the 16
+// partial sums of each channel are added in a fixed order.
+__global__ __launch_bounds__(256) void filter_scale_kernel(const float* __restrict__ partials,
+                                                           int ntiles, int D, int npairs,
+                                                           float2* __restrict__ pair_scale) {
+    __shared__ float part[16][17];
+    const int c = threadIdx.x & 15, r = threadIdx.x >> 4;
+    const int d = blockIdx.x * 16 + c;
+    float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
+    if (d < D) {
+        int t = r;
+        for (; t + 48 < ntiles; t += 64) {  // four independent loads in flight
+            a0 += partials[static_cast<int64_t>(t) * D + d];
+            a1 += partials[static_cast<int64_t>(t + 16) * D + d];
+            a2 += partials[static_cast<int64_t>(t + 32) * D + d];
+            a3 += partials[static_cast<int64_t>(t + 48) * D + d];
+        }
+        for (; t < ntiles; t += 16) a0 += partials[static_cast<int64_t>(t) * D + d];
+    }
+    part[r][c] = (a0 + a1) + (a2 + a3);
+    __syncthreads();
+    if (threadIdx.x < 8) {
+        const int q = blockIdx.x * 8 + threadIdx.x;
+        float g = 0.0f;
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            float a = 0.0f;
+            for (int rr = 0; rr < 16; ++rr) a += part[rr][2 * threadIdx.x + k];
+            g = fmaxf(g, a);
+        }
+        if (q < npairs) {
+            const float sc = pow2_scale(g, kFilterGainExp);
+            pair_scale[q] = make_float2(sc, 1.0f / sc);
+        }
+    }
+}
+
+// |v| as the bits of a non-negative float, for bf16 pairs (dtype 1) or fp32 words
+__device__ __forceinline__ uint32_t abs_bits_max(uint32_t w, int dtype, uint32_t m) {
+    if (dtype == 1) {
+        m = max(m, w & 0x7fff0000u);
+        return max(m, (w << 16) & 0x7fff0000u);
+    }
+    return max(m, w & 0x7fffffffu);
+}
+
+// Stage 1: workgroup g reduces a grid-strided share of the words; one partial per group.
+// Each thread keeps four 16-byte loads in flight per round.
+__global__ __launch_bounds__(256) void amax_partial_kernel(const uint32_t* __restrict__ in, int64_t nwords,
+                                                           int dtype, uint32_t* __restrict__ parts) {
+    __shared__ uint32_t red[4];
+    uint32_t m = 0;
+    constexpr int kUnroll = 4;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * 256 * 4;  // words per round-robin step
+    const bool vec = (reinterpret_cast<uintptr_t>(in) & 15) == 0;
+    int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
+    if (vec) {
+        for (; i + (kUnroll - 1) * stride + 3 < nwords; i += kUnroll * stride) {
+            uint4 w[kUnroll];
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) w[u] = *reinterpret_cast<const uint4*>(in + i + u * stride);
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                m = abs_bits_max(w[u].x, dtype, m);
+                m = abs_bits_max(w[u].y, dtype, m);
+                m = abs_bits_max(w[u].z, dtype, m);
+                m = abs_bits_max(w[u].w, dtype, m);
+            }
+        }
+        for (; i + 3 < nwords; i += stride) {
+            const uint4 w = *reinterpret_cast<const uint4*>(in + i);
+            m = abs_bits_max(w.x, dtype, m);
+            m = abs_bits_max(w.y, dtype, m);
+            m = abs_bits_max(w.z, dtype, m);
+            m = abs_bits_max(w.w, dtype, m);
+        }
+        for (; i < nwords; ++i) m = abs_bits_max(in[i], dtype, m);  // the last partial group
+    } else {
+        for (; i < nwords; i += stride)
+            for (int k = 0; k < 4 && i + k < nwords; ++k) m = abs_bits_max(in[i + k], dtype, m);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), o)));
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) parts[blockIdx.x] = max(max(red[0], red[1]), max(red[2], red[3]));
+}
+
+// Stage 2: one workgroup combines the partials (and a last odd bf16 element) into the scale.
+__global__ __launch_bounds__(256) void amax_finish_kernel(const uint32_t* __restrict__ parts, int nparts,
+                                                          const uint16_t* __restrict__ head,
+                                                          const uint16_t* __restrict__ tail, float extra,
+                                                          const float2* __restrict__ prev,
+                                                          float2* __restrict__ out) {
+    __shared__ uint32_t red[4];
+    uint32_t m = 0;
+    for (int i = threadIdx.x; i < nparts; i += 256) m = max(m, parts[i]);
+    if (threadIdx.x == 0 && head != nullptr) m = max(m, (static_cast<uint32_t>(*head) << 16) & 0x7fff0000u);
+    if (threadIdx.x == 0 && tail != nullptr) m = max(m, (static_cast<uint32_t>(*tail) << 16) & 0x7fff0000u);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), o)));
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const float a = __uint_as_float(max(max(red[0], red[1]), max(red[2], red[3])));
+        const float s = pow2_scale(a, kDataAmaxExp) * extra;
+        out[0] = make_float2(s, (prev != nullptr ? prev->y : 1.0f) / s);
+    }
+}
+
+hipError_t launch_filter_scale(const float* partials, int ntiles, int D, int npairs,
+                               float2* pair_scale, hipStream_t stream) {
+    if (npairs <= 0) return hipSuccess;
+    hipLaunchKernelGGL(filter_scale_kernel, dim3((npairs + 7) / 8), dim3(256), 0, stream,
+                       partials, ntiles, D, npairs, pair_scale);
+    return hipGetLastError();
+}
+
+hipError_t launch_prescale(int dtype, const void* in, int64_t n, float extra, const float2* prev,
+                           float2* out, uint32_t* work, hipStream_t stream) {
+    // whole aligned 32-bit words; a bf16 element before the first word (a tensor that starts
+    // at an odd element) or after the last one goes to stage 2 on its own
+    const uint16_t* head = nullptr;
+    const uint16_t* tail = nullptr;
+    const uint32_t* words = static_cast<const uint32_t*>(in);
+    int64_t nwords = n;
+    if (dtype == 1) {
+        const uint16_t* e = static_cast<const uint16_t*>(in);
+        int64_t ne = n;
+        if (n > 0 && (reinterpret_cast<uintptr_t>(e) & 3) != 0) {
+            head = e;
+            ++e;
+            --ne;
+        }
+        if (ne & 1) tail = e + (ne - 1);
+        words = reinterpret_cast<const uint32_t*>(e);
+        nwords = ne / 2;
+    }
+    const int64_t groups = (nwords + 1023) / 1024;
+    const int nparts = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(kAmaxParts, groups)));
+    hipLaunchKernelGGL(amax_partial_kernel, dim3(nparts), dim3(256), 0, stream, words, nwords, dtype, work);
+    hipLaunchKernelGGL(amax_finish_kernel, dim3(1), dim3(256), 0, stream, work, nparts, head, tail, extra,
+                       prev, out);
     return hipGetLastError();
 }
 

@@ -29,6 +29,17 @@ namespace rubiconv {
 struct F32 {};
 struct BF16 {};
 
+// Power-of-two scales of the complex fp16 grids (device pointers, never null):
+// pair[q] = {s, 1 / s} per channel pair q (pair block * 16 + lane pair), glob = {s, m}.
+// A column pass into a grid multiplies its fp32 results by pair[q].x * glob->x before
+// they are rounded to the grid type; an inverse column pass multiplies its fp32
+// outputs by pair[q].y * glob->y.  The filter's per-pair normalisation and a
+// call's data prescale travel this way, so every fp16 value stays in range.
+struct GridScale {
+    const float2* pair;
+    const float2* glob;
+};
+
 struct LaunchTables {
     const Seg* segs;
     const int32_t* col_seg;
@@ -41,11 +52,11 @@ struct LaunchTables {
 // `half` selects complex fp16 grid and spectrum elements (complex fp32 otherwise).
 hipError_t launch_col_fwd(int r, bool half, int x_dtype, const void* src, int64_t src_row_stride,
                           int D, void* grid, int64_t grid_pb_stride, const LaunchTables& t,
-                          int n_cols, int npb, hipStream_t stream);
+                          GridScale sc, int n_cols, int npb, hipStream_t stream);
 
 hipError_t launch_col_inv(int r, bool half, int y_dtype, const void* grid, int64_t grid_pb_stride,
                           void* dst, int64_t dst_row_stride, int D, const LaunchTables& t,
-                          int n_cols, int npb, hipStream_t stream);
+                          GridScale sc, int n_cols, int npb, hipStream_t stream);
 
 // Row pass: row DFTs of the filter class rows and the document rows, the
 // separation and product, the inverse row DFT (generic kernel: long rows).
@@ -106,11 +117,13 @@ constexpr int kMtEntries = 4608;
 // launch_transpose_pairs (filter taps).
 hipError_t launch_col_fwd_mfma(int src_dtype, const void* src, int64_t src_row_stride, int D,
                                void* grid, int64_t grid_pb_stride, const LaunchTables& t,
-                               const void* mtab, int n_cols, int npb, hipStream_t stream);
+                               GridScale sc, const void* mtab, int n_cols, int npb,
+                               hipStream_t stream);
 
 hipError_t launch_col_inv_mfma(int y_dtype, const void* grid, int64_t grid_pb_stride, void* dst,
                                int64_t dst_row_stride, int D, const LaunchTables& t,
-                               const void* mtab, int n_cols, int npb, hipStream_t stream);
+                               GridScale sc, const void* mtab, int n_cols, int npb,
+                               hipStream_t stream);
 
 // Documents computed by their defining sums (the direct path; kernels.hip):
 // mode 0 out = y from a = x, mode 1 out = dx from a = dy, mode 2 out = the
@@ -128,10 +141,31 @@ hipError_t launch_lag_sum(const float* r, const Seg* segs, int n_docs, int N, in
                           float* dk, hipStream_t stream);
 
 // Filter taps [D][in_ld] fp32 -> [taps][D / 2] complex fp16 channel pairs (D even).
+// partials (may be null): float [*ntiles][D], the sum of |k| of each channel over each
+// tile of 32 taps (the input of launch_filter_scale); *ntiles <= tap_tile_rows(taps).
+constexpr int tap_tile_rows(int taps) { return 2 * ((taps + 63) / 64); }
 hipError_t launch_transpose_pairs(const float* in, int D, int taps, int in_ld, void* out,
-                                  hipStream_t stream);
+                                  float* partials, int* ntiles, hipStream_t stream);
 
+// out[c][r] = in[r][c] (r < rows, c < cols); partials as above with rows = channels and
+// cols = taps (may be null), ceil(cols / 32) tiles.
 hipError_t launch_transpose(const float* in, int rows, int cols, int in_ld, float* out,
-                            int out_ld, hipStream_t stream);
+                            int out_ld, float* partials, hipStream_t stream);
+
+// Per channel pair q < npairs: g = max over its channels of the summed partials (the
+// filter's absolute gain, sum over taps of |k|) and s = 2^(kFilterGainExp - e) with
+// g < 2^e (1 when g is zero or not finite); pair_scale[q] = {s, 1 / s}.
+constexpr int kFilterGainExp = 8;
+hipError_t launch_filter_scale(const float* partials, int ntiles, int D, int npairs,
+                               float2* pair_scale, hipStream_t stream);
+
+// Exact power-of-two prescale of a [n] bf16 (dtype 1) or fp32 (dtype 0) tensor:
+// a = max |v| (two passes, no atomics: a fixed result); s = 2^(kDataAmaxExp - e) with
+// a < 2^e (1 when a is zero or not finite), times `extra` (a power of two);
+// out = {s * extra, (prev ? prev->y : 1) / (s * extra)}.  work: kAmaxParts uint32.
+constexpr int kDataAmaxExp = 3;
+constexpr int kAmaxParts = 2048;
+hipError_t launch_prescale(int dtype, const void* in, int64_t n, float extra, const float2* prev,
+                           float2* out, uint32_t* work, hipStream_t stream);
 
 }  // namespace rubiconv

@@ -9,6 +9,7 @@
 
 #include <algorithm>
 #include <climits>
+#include <cmath>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
@@ -21,6 +22,7 @@
 #include "row_sizes.hpp"
 
 using rubiconv::BuildError;
+using rubiconv::GridScale;
 using rubiconv::HostPlan;
 using rubiconv::kPairsPerBlock;
 using rubiconv::LaunchTables;
@@ -37,13 +39,19 @@ struct rubiconv_plan_s {
     const Seg* lr_gsegs = nullptr;          //   the same, second rows their own (filter gradient)
     const int32_t* lr_idx = nullptr;        //   identity indices
     const int32_t* lr_groups = nullptr;     //   groups of the sub-row launches
+    const float2* ones = nullptr;           // {1, 1} per channel pair: the unit range scales
     bool device_ready = false;
+    bool prescale_fwd = true;    // the forward prescales x as the gradients do dy (and x)
     LaunchTables doc_t{};
     LaunchTables cls_t{};
     LaunchTables grad_t{};       // doc_t with each document's "filter" rows at its own grid rows
     const Seg* direct_segs = nullptr;  // documents of the direct path
     const Seg* all_segs = nullptr;     // every document, longest first (the filter gradient's sum)
     size_t dtaps_off = 0;        // spectrum: the direct path's taps [direct_taps][D] fp32
+    size_t sscale_off = 0;       // spectrum: the filter's range scales, float2 per channel pair
+    size_t partials_off = 0;     // filter call's workspace: |k| sums per tap tile and channel
+    size_t ws_hdr_off = 0;       // workspace: prescales of x and dy, then the amax partials
+    size_t dk_hdr_off = 0;       // the same in the filter gradient's workspace
     int64_t grid_pb_stride = 0;  // grid elements per pair block, document grid
     int64_t cls_pb_stride = 0;   // same, filter class grids (the spectrum buffer)
     size_t taps_bytes = 0;       // transposed filter taps (workspace of the filter call)
@@ -96,6 +104,8 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     const size_t o_lg = off;         off = align_up(off + h.lr_gsegs.size() * sizeof(Seg));
     const size_t o_li = off;         off = align_up(off + h.lr_idx.size() * 4);
     const size_t o_lq = off;         off = align_up(off + h.lr_groups.size() * 4);
+    const size_t n_ones = static_cast<size_t>(std::max(h.npb, 1)) * kPairsPerBlock;
+    const size_t o_one = off;        off = align_up(off + n_ones * sizeof(float2));
     const size_t total = off;
 
     std::vector<unsigned char> img(total, 0);
@@ -127,6 +137,10 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     if (!h.dense_docs.empty()) std::memcpy(img.data() + o_dd, h.dense_docs.data(), h.dense_docs.size() * 4);
     if (!h.dense_groups.empty())
         std::memcpy(img.data() + o_dg, h.dense_groups.data(), h.dense_groups.size() * 4);
+    {
+        std::vector<float> ones(2 * n_ones, 1.0f);
+        std::memcpy(img.data() + o_one, ones.data(), ones.size() * sizeof(float));
+    }
     if (!h.lr_segs.empty()) {
         std::memcpy(img.data() + o_ls, h.lr_segs.data(), h.lr_segs.size() * sizeof(Seg));
         std::memcpy(img.data() + o_lg, h.lr_gsegs.data(), h.lr_gsegs.size() * sizeof(Seg));
@@ -173,6 +187,7 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     pl->lr_gsegs = reinterpret_cast<const Seg*>(base + o_lg);
     pl->lr_idx = reinterpret_cast<const int32_t*>(base + o_li);
     pl->lr_groups = reinterpret_cast<const int32_t*>(base + o_lq);
+    pl->ones = reinterpret_cast<const float2*>(base + o_one);
     if (hipEventCreateWithFlags(&pl->fork, hipEventDisableTiming) != hipSuccess ||
         hipEventCreateWithFlags(&pl->direct_done, hipEventDisableTiming) != hipSuccess)
         return RUBICONV_ERR_HIP;
@@ -257,6 +272,28 @@ const float* direct_taps(const rubiconv_plan_s* plan, const void* spectrum) {
     return reinterpret_cast<const float*>(static_cast<const char*>(spectrum) + plan->dtaps_off);
 }
 
+// The filter's per-pair range scales inside a spectrum buffer (unit scales on fp32 grids).
+const float2* filter_scales(const rubiconv_plan_s* plan, const void* spectrum) {
+    if (!plan->h.grid_half) return plan->ones;
+    return reinterpret_cast<const float2*>(static_cast<const char*>(spectrum) + plan->sscale_off);
+}
+
+// The two prescale words (x, dy) and the amax partials of a workspace header.
+float2* prescale_words(void* workspace, size_t hdr_off) {
+    return reinterpret_cast<float2*>(static_cast<char*>(workspace) + hdr_off);
+}
+uint32_t* prescale_work(void* workspace, size_t hdr_off) {
+    return reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + hdr_off + kAlign);
+}
+
+// Prescale word of a [B][N][D] tensor (fp16 grids only; unit otherwise).
+hipError_t prescale(rubiconv_plan_s* plan, int dtype, const void* in, float extra, const float2* prev,
+                    float2* word, uint32_t* work, hipStream_t stream) {
+    const HostPlan& h = plan->h;
+    return rubiconv::launch_prescale(dtype, in, static_cast<int64_t>(h.B) * h.N * h.D, extra, prev, word,
+                                     work, stream);
+}
+
 // Stage names in the profile: the forward's plain, the gradients' prefixed.
 std::string stage(const char* tag, const char* name) { return std::string(tag) + name; }
 
@@ -270,19 +307,19 @@ std::string stage(const char* tag, const char* name) { return std::string(tag) +
 // of groups of a size class.  The caller holds the plan's launch mutex.
 hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, const void* fgrid,
                         int64_t fgrid_pb_stride, const LaunchTables& t, void* out, int out_dtype,
-                        void* grid, int corr, bool own_rows, const char* tag, hipStream_t stream,
-                        StageRecorder& rec) {
+                        void* grid, int corr, bool own_rows, GridScale in_sc, GridScale out_sc,
+                        const char* tag, hipStream_t stream, StageRecorder& rec) {
     const HostPlan& h = plan->h;
     const int n_cols = static_cast<int>(h.doc_col_seg.size());
     const int64_t rs = static_cast<int64_t>(h.N) * h.D;
     const bool half = h.grid_half;
     hipError_t e = h.col_mfma && in_dtype == RUBICONV_BF16
                        ? rubiconv::launch_col_fwd_mfma(in_dtype, in, rs, h.D, grid,
-                                                       plan->grid_pb_stride, plan->doc_t,
+                                                       plan->grid_pb_stride, plan->doc_t, in_sc,
                                                        plan->mfma_tab, n_cols, h.npb, stream)
                        : rubiconv::launch_col_fwd(h.r, half, in_dtype, in, rs, h.D, grid,
-                                                  plan->grid_pb_stride, plan->doc_t, n_cols, h.npb,
-                                                  stream);
+                                                  plan->grid_pb_stride, plan->doc_t, in_sc, n_cols,
+                                                  h.npb, stream);
     rec.mark(stage(tag, "col_fwd"));
     // long rows: first level into the sub-row regions (both grids of the filter gradient)
     for (const rubiconv::LrItem& it : h.lr_doc_items)
@@ -374,11 +411,11 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
     rec.mark(stage(tag, "row_conv"));
     if (e == hipSuccess)
         e = h.col_mfma ? rubiconv::launch_col_inv_mfma(out_dtype, grid, plan->grid_pb_stride, out,
-                                                       rs, h.D, plan->doc_t, plan->mfma_tab, n_cols,
-                                                       h.npb, stream)
+                                                       rs, h.D, plan->doc_t, out_sc, plan->mfma_tab,
+                                                       n_cols, h.npb, stream)
                        : rubiconv::launch_col_inv(h.r, half, out_dtype, grid,
                                                   plan->grid_pb_stride, out, rs, h.D, plan->doc_t,
-                                                  n_cols, h.npb, stream);
+                                                  out_sc, n_cols, h.npb, stream);
     rec.mark(stage(tag, "col_inv"));
     return e;
 }
@@ -433,16 +470,30 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
     pl->spec_bytes = align_up(static_cast<size_t>(h.npb) * pl->cls_pb_stride * esz);
     pl->dtaps_off = pl->spec_bytes;
     pl->spec_bytes += align_up(static_cast<size_t>(h.direct_taps) * h.D * 4);
+    pl->sscale_off = pl->spec_bytes;
+    pl->spec_bytes += align_up(static_cast<size_t>(std::max(h.npb, 1)) * kPairsPerBlock * sizeof(float2));
     pl->taps_bytes = align_up(static_cast<size_t>(h.taps_max) * h.D * 4);
+    pl->partials_off = pl->taps_bytes;
     const size_t conv_ws = align_up(static_cast<size_t>(h.npb) * pl->grid_pb_stride * esz);
-    const size_t filt_ws = pl->taps_bytes;
-    pl->ws_bytes = std::max(conv_ws, filt_ws);
+    const size_t filt_ws =
+        pl->taps_bytes + align_up(static_cast<size_t>(rubiconv::tap_tile_rows(std::max(h.taps_max, 1))) * h.D * 4);
+    const size_t hdr_bytes = kAlign + align_up(rubiconv::kAmaxParts * 4);
+    pl->ws_hdr_off = std::max(conv_ws, filt_ws);
+    pl->ws_bytes = pl->ws_hdr_off + hdr_bytes;
     pl->grid_bytes = conv_ws;
-    pl->dk_ws_bytes = 2 * conv_ws + align_up(static_cast<size_t>(h.B) * h.N * h.D * 4);
-    // never empty: a plan whose documents all take the direct path still hands out
-    // buffers callers can allocate and pass
-    pl->ws_bytes = std::max(pl->ws_bytes, kAlign);
+    pl->dk_hdr_off = 2 * conv_ws + align_up(static_cast<size_t>(h.B) * h.N * h.D * 4);
+    pl->dk_ws_bytes = pl->dk_hdr_off + hdr_bytes;
     pl->spec_bytes = std::max(pl->spec_bytes, kAlign);
+    // RUBICONV_PRESCALE = 0: the forward takes x as it is, without the power-of-two
+    // scale from its largest magnitude (which costs one extra read of x); the gradients
+    // always prescale dy (and x)
+    if (const char* v = std::getenv("RUBICONV_PRESCALE")) {
+        if (std::strcmp(v, "0") != 0 && std::strcmp(v, "1") != 0) {
+            delete pl;
+            return RUBICONV_ERR_ARG;
+        }
+        pl->prescale_fwd = v[0] == '1';
+    }
     rubiconv_status_t st = upload(pl);
     if (st != RUBICONV_OK) {
         destroy_side_streams(pl);
@@ -477,17 +528,30 @@ rubiconv_status_t rubiconv_filter_spectrum(rubiconv_plan_t plan, const float* fi
     // matrix-core column pass (which computes in fp16)
     float* taps = static_cast<float*>(workspace);
     StageRecorder rec(plan, stream);
+    // On fp16 grids the transpose also sums |k| per channel and tile of taps, and the
+    // filter's range scale per channel pair follows from those sums: the column pass
+    // normalises each pair's gain (sum of |k|) to 2^kFilterGainExp before fp16 rounding,
+    // and the inverse column pass of every later call undoes it.
+    float* partials = h.grid_half ? reinterpret_cast<float*>(static_cast<char*>(workspace) + plan->partials_off)
+                                  : nullptr;
+    float2* sscale = const_cast<float2*>(filter_scales(plan, spectrum));
+    int ntiles = (h.taps_max + 31) / 32;
     hipError_t e = h.col_mfma
-                       ? rubiconv::launch_transpose_pairs(filters, h.D, h.taps_max, h.L, taps, stream)
-                       : rubiconv::launch_transpose(filters, h.D, h.taps_max, h.L, taps, h.D, stream);
+                       ? rubiconv::launch_transpose_pairs(filters, h.D, h.taps_max, h.L, taps, partials,
+                                                          &ntiles, stream)
+                       : rubiconv::launch_transpose(filters, h.D, h.taps_max, h.L, taps, h.D, partials,
+                                                    stream);
+    if (e == hipSuccess && h.grid_half)
+        e = rubiconv::launch_filter_scale(partials, ntiles, h.D, h.npb * kPairsPerBlock, sscale, stream);
     rec.mark("filter_transpose");
+    const rubiconv::GridScale fsc{sscale, plan->ones};
     if (e == hipSuccess)
         e = h.col_mfma
                 ? rubiconv::launch_col_fwd_mfma(0, taps, 0, h.D, spectrum, plan->cls_pb_stride,
-                                                plan->cls_t, plan->mfma_tab,
+                                                plan->cls_t, fsc, plan->mfma_tab,
                                                 static_cast<int>(h.cls_col_seg.size()), h.npb, stream)
                 : rubiconv::launch_col_fwd(h.r, h.grid_half, 0, taps, 0, h.D, spectrum,
-                                           plan->cls_pb_stride, plan->cls_t,
+                                           plan->cls_pb_stride, plan->cls_t, fsc,
                                            static_cast<int>(h.cls_col_seg.size()), h.npb, stream);
     for (const rubiconv::LrItem& it : h.lr_cls_items)
         if (e == hipSuccess)
@@ -497,7 +561,7 @@ rubiconv_status_t rubiconv_filter_spectrum(rubiconv_plan_t plan, const float* fi
     if (e == hipSuccess && h.direct_taps > 0) {  // the direct path's taps, [T][D] fp32
         e = rubiconv::launch_transpose(filters, h.D, h.direct_taps, h.L,
                                        reinterpret_cast<float*>(static_cast<char*>(spectrum) + plan->dtaps_off),
-                                       h.D, stream);
+                                       h.D, nullptr, stream);
         rec.mark("filter_direct_taps");
     }
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
@@ -523,9 +587,18 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
                                            plan->direct_segs, static_cast<int>(h.direct_docs.size()),
                                            h.N, h.D, h.L, h.y_dtype, y, s);
         });
+    // range scales: the filter's per pair, and x's prescale when asked for
+    const float2* xs = plan->ones;
+    if (e == hipSuccess && h.grid_half && plan->prescale_fwd) {
+        float2* w = prescale_words(workspace, plan->ws_hdr_off);
+        e = prescale(plan, h.x_dtype, x, 1.0f, nullptr, w, prescale_work(workspace, plan->ws_hdr_off), stream);
+        rec.mark("prescale");
+        xs = w;
+    }
     if (e == hipSuccess)
         e = enqueue_conv(plan, x, h.x_dtype, spectrum, plan->cls_pb_stride, plan->doc_t, y, h.y_dtype,
-                         workspace, 0, false, "", stream, rec);
+                         workspace, 0, false, {plan->ones, xs}, {filter_scales(plan, spectrum), xs}, "",
+                         stream, rec);
     if (e == hipSuccess && direct) e = join_direct(plan, stream, rec);
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }
@@ -552,9 +625,19 @@ rubiconv_status_t rubiconv_packed_conv_dx(rubiconv_plan_t plan, const void* dy, 
                                            plan->direct_segs, static_cast<int>(h.direct_docs.size()),
                                            h.N, h.D, h.L, h.x_dtype, dx, s);
         });
+    // dy is prescaled by a power of two from its largest magnitude (upstream gradients are
+    // often far below 1), the filter by its per-pair scale
+    const float2* ds = plan->ones;
+    if (e == hipSuccess && h.grid_half) {
+        float2* w = prescale_words(workspace, plan->ws_hdr_off) + 1;
+        e = prescale(plan, h.y_dtype, dy, 1.0f, nullptr, w, prescale_work(workspace, plan->ws_hdr_off), stream);
+        rec.mark("dx_prescale");
+        ds = w;
+    }
     if (e == hipSuccess)
         e = enqueue_conv(plan, dy, h.y_dtype, spectrum, plan->cls_pb_stride, plan->doc_t, dx,
-                         h.x_dtype, workspace, 1, false, "dx_", stream, rec);
+                         h.x_dtype, workspace, 1, false, {plan->ones, ds}, {filter_scales(plan, spectrum), ds},
+                         "dx_", stream, rec);
     if (e == hipSuccess && direct) e = join_direct(plan, stream, rec);
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }
@@ -590,6 +673,25 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
                                            static_cast<int>(h.direct_docs.size()), h.N, h.D, h.L, 0,
                                            r, s);
         });
+    // range: x and dy prescaled by powers of two from their largest magnitudes, and
+    // together by 2^-ceil(log2 P_max) (half on each side), as a correlation sums up to P
+    // products; the inverse pass undoes all of it (the dy word's second half)
+    const float2* xs = plan->ones;
+    const float2* ds = plan->ones;
+    if (e == hipSuccess && h.grid_half) {
+        float2* w = prescale_words(workspace, plan->dk_hdr_off);
+        uint32_t* work = prescale_work(workspace, plan->dk_hdr_off);
+        int pmax = 1;
+        for (const Seg& d : h.docs) pmax = std::max(pmax, d.P);
+        int lg = 0;
+        while ((1 << lg) < pmax && lg < 30) ++lg;
+        e = prescale(plan, h.x_dtype, x, std::ldexp(1.0f, -(lg + 1) / 2), nullptr, w, work, stream);
+        if (e == hipSuccess)
+            e = prescale(plan, h.y_dtype, dy, std::ldexp(1.0f, -(lg / 2)), w, w + 1, work, stream);
+        rec.mark("dk_prescale");
+        xs = w;
+        ds = w + 1;
+    }
     // x's column DFTs into the second grid, then dy's passes against it with the
     // correlation product: document i's cross-correlation of dy with x lands at its
     // own token positions (lag = offset in the document) of r
@@ -597,10 +699,11 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
         e = h.col_mfma && h.x_dtype == RUBICONV_BF16
                        ? rubiconv::launch_col_fwd_mfma(h.x_dtype, x, rs, h.D, xgrid,
                                                        plan->grid_pb_stride, plan->doc_t,
-                                                       plan->mfma_tab, n_cols, h.npb, stream)
+                                                       {plan->ones, xs}, plan->mfma_tab, n_cols,
+                                                       h.npb, stream)
                        : rubiconv::launch_col_fwd(h.r, h.grid_half, h.x_dtype, x, rs, h.D, xgrid,
-                                                  plan->grid_pb_stride, plan->doc_t, n_cols, h.npb,
-                                                  stream);
+                                                  plan->grid_pb_stride, plan->doc_t, {plan->ones, xs},
+                                                  n_cols, h.npb, stream);
     for (const rubiconv::LrItem& it : h.lr_doc_items)
         if (e == hipSuccess)
             e = rubiconv::launch_lr_step(false, xgrid, plan->grid_pb_stride, it, plan->doc_t.tw, h.n1,
@@ -608,7 +711,8 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
     rec.mark("dk_col_fwd_x");
     if (e == hipSuccess)
         e = enqueue_conv(plan, dy, h.y_dtype, xgrid, plan->grid_pb_stride, plan->grad_t, r,
-                         RUBICONV_F32, workspace, 1, true, "dk_", stream, rec);
+                         RUBICONV_F32, workspace, 1, true, {plan->ones, ds}, {plan->ones, ds}, "dk_",
+                         stream, rec);
     if (e == hipSuccess && direct) e = join_direct(plan, stream, rec);
     if (e == hipSuccess)
         e = rubiconv::launch_lag_sum(r, plan->all_segs, static_cast<int>(h.all_docs.size()), h.N, h.D,

@@ -1,0 +1,127 @@
+"""Document isolation on the bf16 matrix-core path (needs an MI355X).
+
+The fp32 impulse tests take the VALU kernels.  bf16 inputs with whole 32-channel blocks
+take the matrix-core column passes and, depending on the row size m of each document,
+the batched short-row kernel (m <= 8), the LDS row kernel (m <= 32), the partner-row
+kernel (33..128), the VALU row kernel on fp16 grids (129..256) and the long-row split
+(m > 256).  An impulse in one document must leave every other document, and every other
+row, below 1e-6 of the impulse document's peak (problem statement, Section 1: no output
+mixes two documents).  The workspace and the spectrum buffer are filled with NaN before
+every call, so a kernel that reads memory this call did not write shows up as well.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+N = 40960
+ROWS = [[N],
+        [1, 2, 17, 300, 700, 1000, 5000, 9000, 12000, N - 28020],
+        [2000, 3000, 4000, N - 9000]]
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _docs(cu):
+    return [(b, int(s0), int(s1)) for b, r in enumerate(cu) for s0, s1 in zip(r[:-1], r[1:])
+            if s1 > s0]
+
+
+def _nan_fill(t):
+    import torch
+    t.view(torch.uint8).fill_(0xFF)   # 0xFFFF.. is a NaN in fp16, bf16 and fp32
+
+
+def _bf16(a):
+    import torch
+    return torch.from_numpy(wl.f32_to_bf16_bits(a).view(np.int16)).view(torch.bfloat16)
+
+
+class _Case:
+    """One plan, its buffers and the filter spectrum for the isolation runs."""
+
+    def __init__(self, device, D, L, seed):
+        import torch
+        import paper_2605_08451_amd as rc
+        self.rc, self.torch, self.device = rc, torch, device
+        self.cu = wl.cu_from_rows(ROWS, N)
+        self.D, self.L = D, L
+        rng = np.random.default_rng(seed)
+        k = rng.standard_normal((D, L)).astype(np.float32)   # undecayed: long lags are live
+        self.plan = rc.Plan(self.cu, N=N, D=D, L=L, x_dtype="bf16", y_dtype="bf16")
+        self.ws = self.plan.new_workspace(device)
+        self.spec = self.plan.new_spectrum(device)
+        _nan_fill(self.ws)
+        _nan_fill(self.spec)
+        rc.filter_spectrum(self.plan, torch.from_numpy(k).to(device), spectrum=self.spec,
+                           workspace=self.ws)
+        self.rng = rng
+
+    def forward(self, x):
+        _nan_fill(self.ws)
+        y = self.rc.packed_conv(self.plan, _bf16(x).to(self.device), self.spec, workspace=self.ws)
+        return y.float().cpu().numpy()
+
+    def dx(self, dy):
+        _nan_fill(self.ws)
+        d = self.rc.packed_conv_dx(self.plan, _bf16(dy).to(self.device), self.spec, workspace=self.ws)
+        return d.float().cpu().numpy()
+
+    def dk(self, x, dy):
+        wsk = self.plan.new_dk_workspace(self.device)
+        _nan_fill(wsk)
+        d = self.rc.packed_conv_dk(self.plan, _bf16(x).to(self.device), _bf16(dy).to(self.device),
+                                   workspace=wsk)
+        return d.cpu().numpy()
+
+
+def _row_sizes(plan):
+    return sorted(set(int(m) for m in plan.doc_table()[:, 4]))
+
+
+@pytest.mark.parametrize("D,L", [(32, N), (64, 300)])
+def test_impulse_isolation_forward_and_dx(device, monkeypatch, D, L):
+    monkeypatch.setenv("RUBICONV_ROW_BATCH", "8")   # rows of up to 8 points batched
+    c = _Case(device, D, L, seed=D)
+    ms = _row_sizes(c.plan)
+    _say(f"[isolation] D={D} L={L} row sizes {ms}")
+    assert min(ms) <= 8 and any(9 <= m <= 32 for m in ms) and any(33 <= m <= 128 for m in ms)
+    assert max(ms) > 128
+    docs = _docs(c.cu)
+    for (b, s0, s1) in docs:
+        for t in sorted({s0, (s0 + s1) // 2, s1 - 1}):
+            v = np.zeros((c.plan.B, N, D), dtype=np.float32)
+            v[b, t, :] = c.rng.standard_normal(D).astype(np.float32) + 2.0
+            inside = np.zeros(v.shape, dtype=bool)
+            inside[b, s0:s1] = True
+            for name, out in (("y", c.forward(v)), ("dx", c.dx(v))):
+                assert np.isfinite(out).all(), (name, b, s0, s1, t)
+                peak = np.abs(out[inside]).max()
+                assert peak > 0, (name, b, s0, s1, t)
+                leak = np.abs(out[~inside]).max()
+                assert leak <= 1e-6 * peak, (name, b, s0, s1, t, leak, peak)
+
+
+def test_dk_isolation(device, monkeypatch):
+    """x in one document only and dy in every other one: the filter gradient is exactly
+    zero (no document's correlation sees another's tokens); with dy everywhere it is not."""
+    monkeypatch.setenv("RUBICONV_ROW_BATCH", "8")
+    D = 32
+    c = _Case(device, D, N, seed=5)
+    for (b, s0, s1) in _docs(c.cu):
+        x = np.zeros((c.plan.B, N, D), dtype=np.float32)
+        x[b, s0:s1] = c.rng.standard_normal((s1 - s0, D)).astype(np.float32)
+        dy = c.rng.standard_normal((c.plan.B, N, D)).astype(np.float32)
+        full = c.dk(x, dy)
+        dy[b, s0:s1] = 0.0
+        other = c.dk(x, dy)
+        assert np.isfinite(full).all() and np.isfinite(other).all(), (b, s0, s1)
+        peak = np.abs(full).max()
+        assert peak > 0
+        assert np.abs(other).max() <= 1e-6 * peak, (b, s0, s1, np.abs(other).max(), peak)

@@ -1,0 +1,119 @@
+"""Value range of the bf16 path (needs an MI355X).
+
+bf16 inputs run on complex fp16 grids.  These cases leave the N(0, 1) inputs of the
+parity tests: a DC offset under an all-ones filter (the per-document prefix sum, whose
+outputs reach 8e4), wide activations, and the small upstream gradients of training.
+Each must meet the bf16 bar (2e-2 relative L2, globally and per document) against the
+oracle on the mid-length workload's document boundaries.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from tests.common import ORACLE_THREADS, assert_parity, to_device
+
+pytestmark = pytest.mark.gpu
+
+D = 32
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _workload(x, filters):
+    cu = wl.config_cu_seqlens(2)
+    B, N = cu.shape[0], int(cu[0, -1])
+    bits = wl.f32_to_bf16_bits(x).reshape(B, N, D)
+    xv = wl.bf16_bits_to_f32(bits).reshape(B, N, D)
+    return wl.Workload("range", B, N, D, filters.shape[1], "bf16", "bf16", cu, xv, bits,
+                       np.ascontiguousarray(filters, np.float32), 0)
+
+
+def _shape():
+    cu = wl.config_cu_seqlens(2)
+    return cu.shape[0], int(cu[0, -1])
+
+
+def _forward(W, device):
+    import torch
+    import paper_2605_08451_amd as rc
+    x, k = to_device(W, device)
+    plan = rc.Plan(W.cu_seqlens, N=W.N, D=W.D, L=W.L, x_dtype="bf16", y_dtype="bf16")
+    ws = plan.new_workspace(device)
+    spec = rc.filter_spectrum(plan, k, workspace=ws)
+    y = rc.packed_conv(plan, x, spec, workspace=ws)
+    torch.cuda.synchronize()
+    return y.float().cpu().numpy().astype(np.float64), plan, spec, ws
+
+
+def _case_inputs(case, B, N):
+    rng = np.random.default_rng(77)
+    if case == "dc5_all_ones":
+        x = 5.0 + rng.standard_normal((B, N, D), dtype=np.float32)
+        k = np.ones((D, N), dtype=np.float32)
+    elif case == "dc5_tiny_filter":      # the all-ones case with every tap 1e-6
+        x = 5.0 + rng.standard_normal((B, N, D), dtype=np.float32)
+        k = np.full((D, N), 1e-6, dtype=np.float32)
+    else:
+        scale = {"wide_300": 300.0, "small_1e-4": 1e-4, "tiny_1e-6": 1e-6, "huge_1e4": 1e4}[case]
+        x = scale * rng.standard_normal((B, N, D), dtype=np.float32)
+        k = wl.decaying_filters(rng, D, N)
+    return x, k
+
+
+@pytest.mark.parametrize("case", ["dc5_all_ones", "dc5_tiny_filter", "wide_300", "small_1e-4",
+                                  "tiny_1e-6", "huge_1e4"])
+def test_forward_range(device, case):
+    B, N = _shape()
+    W = _workload(*_case_inputs(case, B, N))
+    y, _, _, _ = _forward(W, device)
+    ref = oracle.conv_fft(W.x, W.filters, W.cu_seqlens, threads=ORACLE_THREADS)
+    assert np.isfinite(y).all(), case
+    g, d = assert_parity(y, ref, W.cu_seqlens, "bf16", case)
+    _say(f"[range] {case}: max |y| {np.abs(ref).max():.3g}, global {g:.2e}, worst document {d:.2e}")
+
+
+@pytest.mark.parametrize("case", ["dc5_all_ones", "wide_300", "small_1e-4"])
+def test_forward_range_without_prescale(device, monkeypatch, case):
+    """RUBICONV_PRESCALE=0 (x taken as it is): the range the forward then keeps, largest
+    coherent |x| of about 20 and rms(x) down to about 1e-4, still meets the bar."""
+    monkeypatch.setenv("RUBICONV_PRESCALE", "0")
+    B, N = _shape()
+    W = _workload(*_case_inputs(case, B, N))
+    y, _, _, _ = _forward(W, device)
+    ref = oracle.conv_fft(W.x, W.filters, W.cu_seqlens, threads=ORACLE_THREADS)
+    assert np.isfinite(y).all(), case
+    g, d = assert_parity(y, ref, W.cu_seqlens, "bf16", case)
+    _say(f"[range, no prescale] {case}: global {g:.2e}, worst document {d:.2e}")
+
+
+@pytest.mark.parametrize("scale", [1e-6, 1e3])
+def test_gradient_range(device, scale):
+    """Upstream gradients far from 1: dx and dk meet the bar."""
+    import torch
+    import paper_2605_08451_amd as rc
+    from tests.test_gpu_grad import _check_dk
+    B, N = _shape()
+    rng = np.random.default_rng(78)
+    x = rng.standard_normal((B, N, D), dtype=np.float32)
+    k = wl.decaying_filters(rng, D, N)
+    W = _workload(x, k)
+    dyv = wl.round_to_bf16(scale * rng.standard_normal((B, N, D), dtype=np.float32)).astype(np.float64)
+    dy = torch.from_numpy(wl.f32_to_bf16_bits(dyv.astype(np.float32)).view(np.int16)).view(
+        torch.bfloat16).to(device)
+    xd, kd = to_device(W, device)
+    plan = rc.Plan(W.cu_seqlens, N=W.N, D=W.D, L=W.L, x_dtype="bf16", y_dtype="bf16")
+    ws = plan.new_workspace(device)
+    spec = rc.filter_spectrum(plan, kd, workspace=ws)
+    dx = rc.packed_conv_dx(plan, dy, spec, workspace=ws).float().cpu().numpy().astype(np.float64)
+    dk = rc.packed_conv_dk(plan, xd, dy).cpu().numpy().astype(np.float64)
+    assert np.isfinite(dx).all() and np.isfinite(dk).all(), scale
+    g, d = assert_parity(dx, oracle.grad_x(W.filters, dyv, W.cu_seqlens, threads=ORACLE_THREADS),
+                         W.cu_seqlens, "bf16", f"dx scale {scale}")
+    gk, wk = _check_dk(dk, oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L, threads=ORACLE_THREADS),
+                       "bf16", f"dk scale {scale}")
+    _say(f"[range] dy scale {scale}: dx {g:.2e} / {d:.2e}, dk {gk:.2e} / {wk:.2e}")
