@@ -165,6 +165,25 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
                                        void* y, void* workspace, hipStream_t stream);
 
 /*
+ * The packed convolution for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).  It is
+ * rubiconv_packed_conv with the workspace taken from a scratch array that the library
+ * holds in device memory: RUBICONV_NOALLOC_SCRATCH_BYTES on every device that loads
+ * the library, kept until the process ends.  The call itself allocates nothing.
+ *
+ *   x, spectrum, y, stream   as for rubiconv_packed_conv (the caller still owns them).
+ * The scratch array of a device is shared by every call on that device and keeps the
+ * last call's contents; nothing in it needs to start at zero.  Calls that overlap in
+ * time on one device (other streams, other threads) race on it: order them.
+ * Errors: RUBICONV_ERR_ARG (null plan or pointer, misaligned buffer),
+ * RUBICONV_ERR_UNSUPPORTED (rubiconv_workspace_bytes(plan) exceeds
+ * RUBICONV_NOALLOC_SCRATCH_BYTES), RUBICONV_ERR_HIP.
+ */
+#define RUBICONV_NOALLOC_SCRATCH_BYTES ((size_t)320 << 20)
+rubiconv_status_t rubiconv_packed_conv_noalloc(rubiconv_plan_t plan, const void* x, const void* spectrum,
+                                               void* y, hipStream_t stream);
+
+/*
  * Gradients for training (the method targets training pipelines, Section 1).
  * The convolution is linear in x and in k, so for an upstream gradient dy of y
  * the gradients are the adjoints of the two maps:

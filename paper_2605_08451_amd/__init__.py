@@ -22,7 +22,8 @@ from typing import Optional
 import numpy as np
 import torch
 
-__all__ = ["Plan", "RubiconvError", "filter_spectrum", "packed_conv", "packed_conv_dx",
+__all__ = ["Plan", "RubiconvError", "filter_spectrum", "packed_conv", "packed_conv_noalloc",
+           "packed_conv_dx",
            "packed_conv_dk", "conv", "CTPlan", "ct_filter_spectrum", "ct_packed_conv",
            "library_path", "load_library", "EXPORTED_SYMBOLS"]
 
@@ -38,6 +39,7 @@ _STATUS = {0: "ok", 1: "invalid argument", 2: "invalid cu_seqlens", 3: "unsuppor
 EXPORTED_SYMBOLS = ("rubiconv_plan", "rubiconv_plan_destroy", "rubiconv_spectrum_bytes",
                     "rubiconv_workspace_bytes", "rubiconv_filter_spectrum", "rubiconv_packed_conv",
                     "rubiconv_packed_conv_dx", "rubiconv_dk_workspace_bytes", "rubiconv_packed_conv_dk",
+                    "rubiconv_packed_conv_noalloc",
                     "rubiconv_plan_info", "rubiconv_plan_doc_table", "rubiconv_profile_start",
                     "rubiconv_profile_read", "rubiconv_status_string",
                     "rubiconv_ct_plan", "rubiconv_ct_plan_destroy", "rubiconv_ct_spectrum_bytes",
@@ -91,6 +93,8 @@ def load_library():
     lib.rubiconv_filter_spectrum.restype = c_int
     lib.rubiconv_packed_conv.argtypes = [vp, vp, vp, vp, vp, vp]
     lib.rubiconv_packed_conv.restype = c_int
+    lib.rubiconv_packed_conv_noalloc.argtypes = [vp, vp, vp, vp, vp]
+    lib.rubiconv_packed_conv_noalloc.restype = c_int
     lib.rubiconv_packed_conv_dx.argtypes = [vp, vp, vp, vp, vp, vp]
     lib.rubiconv_packed_conv_dx.restype = c_int
     lib.rubiconv_dk_workspace_bytes.argtypes = [vp]
@@ -306,6 +310,25 @@ def packed_conv(plan: Plan, x: torch.Tensor, spectrum: torch.Tensor,
                                               y.data_ptr(), workspace.data_ptr(),
                                               _stream_handle(dev, stream)),
                "rubiconv_packed_conv")
+    return y
+
+
+#: Bytes of the library's per-device scratch array (RUBICONV_NOALLOC_SCRATCH_BYTES).
+NOALLOC_SCRATCH_BYTES = 320 << 20
+
+
+def packed_conv_noalloc(plan: Plan, x: torch.Tensor, spectrum: torch.Tensor, y: torch.Tensor,
+                        stream=None) -> torch.Tensor:
+    """packed_conv without a workspace: the library's per-device scratch array serves as
+    one (rubiconv_packed_conv_noalloc).  y must be given; nothing is allocated."""
+    _check_btd(x, plan, plan.x_dtype, "x")
+    _check_btd(y, plan, plan.y_dtype, "y")
+    if spectrum.numel() * spectrum.element_size() < plan.spectrum_bytes:
+        raise ValueError("spectrum buffer too small")
+    with torch.cuda.device(x.device):
+        _check(plan._lib.rubiconv_packed_conv_noalloc(plan.handle, x.data_ptr(), spectrum.data_ptr(),
+                                                      y.data_ptr(), _stream_handle(x.device, stream)),
+               "rubiconv_packed_conv_noalloc")
     return y
 
 

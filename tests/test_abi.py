@@ -224,6 +224,29 @@ def test_null_arguments_rejected_before_any_device_work():
     lib.rubiconv_plan_destroy(None)
 
 
+def test_noalloc_rejects_plans_beyond_its_scratch():
+    """rubiconv_packed_conv_noalloc refuses, before any device work, a plan whose
+    workspace exceeds the library's scratch array (the long-context workload needs
+    more), and null arguments."""
+    lib = rc.load_library()
+    cu = wl.config_cu_seqlens(4)
+    plan = rc.Plan(cu, N=int(cu[0, -1]), D=256, L=262144, x_dtype="bf16")
+    assert plan.workspace_bytes > rc.NOALLOC_SCRATCH_BYTES
+    fake = 1 << 20   # never dereferenced: the call returns before launching
+    assert lib.rubiconv_packed_conv_noalloc(plan.handle, fake, fake, fake, None) == 3
+    assert lib.rubiconv_packed_conv_noalloc(None, fake, fake, fake, None) == 1
+    assert lib.rubiconv_packed_conv_noalloc(plan.handle, None, fake, fake, None) == 1
+    small = rc.Plan(np.array([[0, 8]], dtype=np.int32), N=8, D=2, L=3, x_dtype="f32")
+    assert small.workspace_bytes <= rc.NOALLOC_SCRATCH_BYTES
+
+
+def test_noalloc_scratch_size_matches_header():
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    text = open(os.path.join(root, "include", "rubiconv.h")).read()
+    m = re.search(r"#define RUBICONV_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == rc.NOALLOC_SCRATCH_BYTES
+
+
 @pytest.mark.skipif(gpu_available(), reason="checks the host-only plan of a machine without a GPU")
 def test_stream_calls_without_device_report_hip_error():
     lib = rc.load_library()
