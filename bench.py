@@ -8,10 +8,18 @@ the batch's size classes (rubiconv_filter_spectrum) and the packed convolution
 table, size classes, twiddles) is built once per batch and shared by every layer,
 so it is built before the timed region and timed separately.
 
-Prints one JSON line: value = B*N*D / seconds per step / 1e6 (Mtokens*channels/s),
-the roofline of the dominant kernel (its compulsory bytes per launch over its
-average duration, timed with HIP events on the stream it runs on) and the CPU
-oracle timed on a bounded sample of the same workload.
+Prints one JSON line: value = B*N*D / seconds per step / 1e6 (Mtokens*channels/s) on
+the mid-length workload (B=4, N=16384, D=1024), then
+  - roofline: the step's algorithmic bytes (x + y + one complex fp32 half-spectrum
+    per channel, D*L*8) over the average duration of the dominant stage (the row
+    stage, timed from its fork to its join with HIP events on the calling stream),
+    against the 8 TB/s HBM peak; the stage's own compulsory bytes per launch are a
+    separate field;
+  - configs: every workload timed by the benchmarking protocol of Section 4.1 (warm-up
+    replays, then 20 trials; mean and 95% confidence interval), with the fractions of
+    the HBM roofline (peak and measured copy bandwidth) and of the FP32 VALU peak;
+  - cpu_baseline: the CPU oracle on bounded samples of every workload (1 warm-up and
+    3 timed runs each), with the host's CPU model and core count.
 """
 import argparse
 import json
@@ -35,8 +43,6 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=2, help="workload index (2 = N=16384, D=1024)")
     ap.add_argument("--n1", type=int, default=0)
-    ap.add_argument("--cpu-seconds", type=float, default=12.0,
-                    help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true",
                     help="launch every step from Python instead of replaying a captured HIP graph")
@@ -49,6 +55,8 @@ def parse():
                     help="skip the masked Cooley-Tukey variant's measurement")
     ap.add_argument("--no-backward", action="store_true",
                     help="skip the gradient measurement (dx and dk steps after the forward)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the protocol timing (and CPU oracle sample) of every workload")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the run, copy a buffer of this many MiB three times (a plain copy "
                          "kernel of known size, the scale for the hardware byte counters)")
@@ -269,6 +277,7 @@ def kernel_bytes(info, W, plan):
         "col_inv": G * D * esz // 2 + tok * sy,
         "filter_transpose": (4 + st) * D * max(taps.values()),
         "filter_col_fwd": st * D * sum(taps.values()) + Gc * D * esz // 2,
+        "prescale": tok * sx,
     }
     return out
 
@@ -302,27 +311,199 @@ def recorded_traffic(stage, workload):
     return None
 
 
-def cpu_baseline(W, target_s):
-    """The oracle's per-document FFT variant (the parity reference at this size) on a
-    sample of channels of the same batch."""
+def recorded_mfma(workload):
+    """Matrix-core counters of this workload's step from the committed summary
+    (profiles/mfma_<workload>.md), or None when there is none or the library sources
+    changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"mfma_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        if line.strip().startswith("mfma {"):
+            rec = json.loads(line.strip()[len("mfma "):])
+            if rec.get("sources_sha256") != sources_digest():
+                return None
+            rec.pop("sources_sha256", None)
+            return rec
+    return None
+
+
+def cpu_info():
+    """The host's CPU model and logical CPU count (as the OS reports them)."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return model, os.cpu_count() or 1
+
+
+ORACLE_THREADS = 16   # one GPU's share of the host's cores
+
+
+def cpu_baseline(W, target_s=1.0, variants=("fft",)):
+    """The CPU oracle on a bounded sample of workload W: all rows and tokens, the first
+    nch channels, nch chosen so that one run takes about target_s seconds; 1 warm-up and
+    3 timed runs per variant (per-document radix-2 FFT, and the defining sum where it is
+    the parity reference)."""
     import oracle
-    threads = min(16, os.cpu_count() or 1)
+    threads = min(ORACLE_THREADS, os.cpu_count() or 1)
+    fns = {"fft": oracle.conv_fft, "direct": oracle.conv_direct}
+    out = {}
+    for var in variants:
+        fn = fns[var]
 
-    def run(nch):
-        x = np.ascontiguousarray(W.x[:, :, :nch])
-        k = np.ascontiguousarray(W.filters[:nch])
-        t0 = time.perf_counter()
-        oracle.conv_fft(x, k, W.cu_seqlens, threads=threads)
-        return time.perf_counter() - t0
+        def run(nch):
+            x = np.ascontiguousarray(W.x[:, :, :nch])
+            k = np.ascontiguousarray(W.filters[:nch])
+            t0 = time.perf_counter()
+            fn(x, k, W.cu_seqlens, threads=threads)
+            return time.perf_counter() - t0
+        probe = min(W.D, 4)
+        t_probe = run(probe)
+        nch = int(max(1, min(W.D, round(probe * target_s / max(t_probe, 1e-4)))))
+        if nch > probe:   # one more sizing step from the larger sample (the probe's overheads weigh less)
+            nch = int(max(1, min(W.D, round(nch * target_s / max(run(nch), 1e-4)))))
+        run(nch)                                     # warm-up
+        ts = [run(nch) for _ in range(3)]
+        t = float(np.mean(ts))
+        out[var] = {"value": round(W.B * W.N * nch / t / 1e6, 3), "unit": "Mtokens*channels/s",
+                    "channels": nch, "of_channels": W.D, "run_s": [round(v, 4) for v in ts]}
+    return out, threads
 
-    probe = min(8, W.D)
-    t_probe = run(probe)
-    nch = int(max(probe, min(W.D, round(probe * target_s / max(t_probe, 1e-3)))))
-    t = run(nch) if nch != probe else t_probe
-    return {"value": W.B * W.N * nch / t / 1e6, "unit": "Mtokens*channels/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"per-document radix-2 FFT variant (fp64), all {W.B} rows x {W.N} tokens, "
-                      f"{nch} of {W.D} channels, {t:.2f} s"}
+
+def t_quantile_975(dof):
+    from scipy import stats
+    return float(stats.t.ppf(0.975, dof))
+
+
+def protocol_time(launch, stream, warmup=5, trials=20, target_ms=3.0):
+    """Section 4.1's protocol on one captured step: warm-up replays, then `trials` timed
+    trials of `reps` replays each (HIP events on the timing stream); mean and the 95%
+    confidence half-width of the per-step time over the trials, in ms."""
+    import torch
+    dev = stream.device
+    launch(stream)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        launch(torch.cuda.current_stream(dev))
+    torch.cuda.synchronize()
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    graph.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    reps = int(max(1, min(200, target_ms / max(e0.elapsed_time(e1), 1e-3))))
+    per = []
+    for _ in range(trials):
+        e0.record(stream)
+        for _ in range(reps):
+            graph.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        per.append(e0.elapsed_time(e1) / reps)
+    per = np.array(per)
+    mean = float(per.mean())
+    ci = float(t_quantile_975(trials - 1) * per.std(ddof=1) / np.sqrt(trials))
+    del graph
+    return mean, ci, reps
+
+
+def step_min_bytes(W):
+    """Algorithmic bytes of one step: x and y once each and one complex fp32
+    half-spectrum per channel (D * L * 8 bytes), whatever the implementation stores."""
+    sx = 2 if W.x_dtype == "bf16" else 4
+    sy = 2 if W.y_dtype == "bf16" else 4
+    return W.B * W.N * W.D * (sx + sy) + W.D * W.L * 8
+
+
+def alg_flops(W, n1=256):
+    """Algorithmic flops of one step: per document and channel one forward and one
+    inverse real transform at Algorithm 1's padded size P = n1 ceil((L_i + min(L_i, L)
+    - 1) / n1) (5 P log2 P per complex transform, half of it for a real one) and 3 P for
+    the product."""
+    tot = 0.0
+    for row in np.asarray(W.cu_seqlens):
+        for s0, s1 in zip(row[:-1], row[1:]):
+            n = int(s1 - s0)
+            if n <= 0:
+                continue
+            P = n1 * -(-(n + min(n, W.L) - 1) // n1)
+            tot += 5.0 * P * np.log2(P) + 3.0 * P
+    return tot * W.D
+
+
+def copy_bandwidth(dev, mib=1024):
+    """Read + write bytes per second of a plain device copy of `mib` MiB (GB/s)."""
+    import torch
+    src = torch.ones((mib << 20) // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(10):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    gbps = 2 * (mib << 20) / (e0.elapsed_time(e1) / 10 * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return gbps
+
+
+def configs_measurement(args, copy_gbps, cpu):
+    """Every workload: the step (filter spectra + convolution) by the protocol, its
+    throughput and roofline fractions, and (cpu) the oracle baseline on a sample."""
+    import torch
+    import paper_2605_08451_amd as rc
+    import workloads as wl
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    out, cpu_out, threads = {}, {}, None
+    for i in range(5):
+        W = wl.make_config(i)
+        if W.x_dtype == "bf16":
+            x = torch.from_numpy(W.x_bits.view(np.int16)).view(torch.bfloat16).to(dev)
+        else:
+            x = torch.from_numpy(W.x).to(dev)
+        k = torch.from_numpy(W.filters).to(dev)
+        plan = rc.Plan(W.cu_seqlens, N=W.N, D=W.D, L=W.L, x_dtype=W.x_dtype, y_dtype=W.y_dtype)
+        ws, spec = plan.new_workspace(dev), plan.new_spectrum(dev)
+        y = torch.empty_like(x)
+
+        def launch(s):
+            rc.filter_spectrum(plan, k, spectrum=spec, workspace=ws, stream=s)
+            rc.packed_conv(plan, x, spec, y=y, workspace=ws, stream=s)
+        mean, ci, reps = protocol_time(launch, stream, warmup=args.warmup, trials=20)
+        tok_ch = W.B * W.N * W.D
+        mb = step_min_bytes(W)
+        fl = alg_flops(W)
+        out[f"c{i}"] = {
+            "workload": wl.CONFIG_NAMES[i], "ms_mean": round(mean, 5), "ms_ci95": round(ci, 5),
+            "trials": 20, "replays_per_trial": reps,
+            "value": round(tok_ch / (mean * 1e-3) / 1e6, 1), "unit": "Mtokens*channels/s",
+            "min_bytes": mb, "hbm_frac_of_peak": round(mb / (mean * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "hbm_frac_of_copy": round(mb / (mean * 1e-3) / 1e9 / copy_gbps, 4),
+            "alg_flops": round(fl), "valu_frac_of_peak": round(fl / (mean * 1e-3) / 1e12 / FP32_VALU_TFLOPS, 4),
+            "docs": plan.info()["n_docs"], "cu_seqlens_sha256_16": W.cu_hash()}
+        print(f"[bench] c{i}: {mean:.4f} +- {ci:.4f} ms", file=sys.stderr, flush=True)
+        del x, k, plan, ws, spec, y
+        torch.cuda.empty_cache()
+        if cpu:
+            variants = ("fft", "direct") if i in (0, 1, 3) else ("fft",)
+            cpu_out[f"c{i}"], threads = cpu_baseline(W, target_s=1.0 if i == args.config else 0.5,
+                                                     variants=variants)
+            print(f"[bench] c{i} cpu oracle done", file=sys.stderr, flush=True)
+    return out, cpu_out, threads
 
 
 def main():
@@ -392,32 +573,29 @@ def main():
     wall = time.perf_counter() - w0
     ms = e0.elapsed_time(e1) / args.steps
 
-    # per-kernel durations: HIP events the library records around each of its kernels
+    # stage durations: HIP events the library records on the stream each stage runs on
+    # (a stage that forks to side streams is timed from before its fork to after its join)
     plan.profile_start(2 * args.steps)
     for _ in range(args.steps):
         launch(stream)
     kt = plan.profile_read()
     plan.profile_start(0)
     kb = kernel_bytes(info, W, plan)
-    # a stage that runs once per channel chunk has several launches per step: its
-    # bytes per launch are the step's bytes over that count
-    lps = {n: c / args.steps for n, (c, tot) in kt.items()}
-    kbl = {n: kb.get(n, 0) / lps[n] for n in kt}
-    per_kernel = {n: {"launches_per_step": lps[n], "avg_us": 1e3 * tot / c,
-                      "us_per_step": 1e3 * tot / args.steps,
-                      "GBps": kbl[n] / (tot / c * 1e-3) / 1e9}
-                  for n, (c, tot) in kt.items()}
-    stages = {n: 1e3 * tot / args.steps for n, (c, tot) in kt.items()}
-    # the dominant single kernel (the row stage is several concurrent launches)
-    dom = max((n for n in kt if n != "row_conv"), key=lambda n: kt[n][1])
-    dom_us = per_kernel[dom]["avg_us"]
-    achieved = kbl[dom] / (dom_us * 1e-6) / 1e9
+    stages = {n: {"launches_per_step": c / args.steps, "avg_us": 1e3 * tot / c,
+                  "us_per_step": 1e3 * tot / args.steps,
+                  "compulsory_bytes_per_launch": round(kb[n] * args.steps / c) if n in kb else None,
+                  "compulsory_GBps": (kb[n] * args.steps / c) / (tot / c * 1e-3) / 1e9 if n in kb else None}
+              for n, (c, tot) in kt.items()}
+    # the dominant stage: the longest one of a step
+    dom = max(stages, key=lambda n: stages[n]["us_per_step"])
+    dom_us = stages[dom]["avg_us"]
+    min_bytes = step_min_bytes(W)
+    achieved = min_bytes / (dom_us * 1e-6) / 1e9
+    copy_gbps = copy_bandwidth(dev)
 
     tok_ch = W.B * W.N * W.D
-    sx = 2 if W.x_dtype == "bf16" else 4
-    sy = 2 if W.y_dtype == "bf16" else 4
-    min_bytes = tok_ch * (sx + sy) + W.D * W.L * 8
     value = tok_ch / (ms * 1e-3) / 1e6
+    flops = alg_flops(W)
     out = {
         "metric": "packed-conv Mtokens*channels/s at N=16384,D=1024; % HBM roofline",
         "value": round(value, 1),
@@ -432,18 +610,27 @@ def main():
                    "L": W.L, "x_dtype": W.x_dtype, "y_dtype": W.y_dtype, "n1": info["n1"],
                    "docs": info["n_docs"], "size_classes": info["n_classes"],
                    "cu_seqlens_sha256_16": W.cu_hash(), "parallelism": "none (1 GPU)"},
-        "hbm_roofline_frac_step": round(min_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "step_min_bytes": min_bytes,
+        "hbm_roofline_frac_step": round(min_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "hbm_frac_of_copy_step": round(min_bytes / (ms * 1e-3) / 1e9 / copy_gbps, 4),
+        "valu_frac_step": round(flops / (ms * 1e-3) / 1e12 / FP32_VALU_TFLOPS, 4),
+        "copy_GBps": round(copy_gbps, 1),
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": recorded_traffic(dom, wl.CONFIG_SLUGS[args.config]),
-                     "bytes_per_launch": round(kbl[dom]), "avg_us": round(dom_us, 2)},
-        "stages_us": {n: round(v, 1) for n, v in stages.items()},
-        "kernels": {n: {kk: round(vv, 2) for kk, vv in d.items()} for n, d in per_kernel.items()},
+                     "bytes": min_bytes, "avg_us": round(dom_us, 2),
+                     "compulsory_bytes_per_launch": stages[dom]["compulsory_bytes_per_launch"]},
+        "stages": {n: {kk: (round(vv, 2) if isinstance(vv, float) else vv) for kk, vv in d.items()}
+                   for n, d in stages.items()},
+        "mfma": recorded_mfma(wl.CONFIG_SLUGS[args.config]),
         "plan_ms": round(plan_ms, 3),
         "execution": "eager launches" if graph is None else "HIP graph replay of one captured step",
         "wall_s_timed": round(wall, 4),
     }
+    del graph
+    cpu_cfg, threads = {}, None
+    if not args.no_configs:
+        out["configs"], cpu_cfg, threads = configs_measurement(args, copy_gbps, not args.no_cpu_baseline)
     if not args.no_backward:
         out["backward"] = backward_measurement(rc, plan, W, x, k, spec, ws, stream, args)
     if not args.no_ct:
@@ -451,7 +638,17 @@ def main():
     if args.layers > 0:
         out["stacked"] = stacked_measurement(rc, plan, W, x, stream, plan_ms, args)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(W, args.cpu_seconds)
+        model, ncpu = cpu_info()
+        key = f"c{args.config}"
+        if key not in cpu_cfg:
+            cpu_cfg[key], threads = cpu_baseline(W, target_s=1.0)
+        c = cpu_cfg[key]["fft"]
+        out["cpu_baseline"] = {
+            "value": c["value"], "unit": "Mtokens*channels/s", "cores": threads, "kind": "oracle",
+            "sample": f"per-document radix-2 FFT variant (fp64) on {W.B} rows x {W.N} tokens x "
+                      f"{c['channels']} of {W.D} channels of {wl.CONFIG_NAMES[args.config]}; "
+                      f"1 warm-up and 3 timed runs ({', '.join(str(v) for v in c['run_s'])} s)",
+            "cpu_model": model, "host_logical_cpus": ncpu, "configs": cpu_cfg}
     print(json.dumps(out), flush=True)
     if args.copy_probe_mib > 0:
         # an elementwise kernel that reads and writes copy_probe_mib MiB once each
