@@ -104,9 +104,14 @@ typedef enum {
  * row kernels as short rows (Algorithm 1's four-step factorisation applied to
  * the row DFT); RUBICONV_LONG_ROWS = 0 (read when the plan is made) keeps such rows
  * whole in the generic row kernel instead.
+ *   stream          HIP stream the upload of the plan's device tables is enqueued on
+ *                   (hipMemcpyAsync from a host copy the plan keeps): work that uses
+ *                   the plan on this stream is ordered after it; other streams must
+ *                   wait for it (or the device be synchronised) before using the plan.
  * The plan copies what it needs; cu_seqlens_host may be freed on return.  Plan
- * creation allocates device memory and copies the document and twiddle tables
- * synchronously (it is not a stream-ordered call).
+ * creation allocates the plan's device memory and creates its side streams and
+ * events (hipMalloc, hipStreamCreate, which HIP may order with other device work);
+ * it does not wait for the upload.
  * Errors: RUBICONV_ERR_ARG (also for a malformed RUBICONV_DIRECT_MAX or
  * RUBICONV_CLASS_MERGE),
  * RUBICONV_ERR_SEQLENS, RUBICONV_ERR_UNSUPPORTED (n1 not supported, or a document
@@ -115,7 +120,7 @@ typedef enum {
  */
 rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L, int max_docs,
                                 const int32_t* cu_seqlens_host, rubiconv_dtype_t x_dtype,
-                                rubiconv_dtype_t y_dtype, int n1);
+                                rubiconv_dtype_t y_dtype, int n1, hipStream_t stream);
 
 /* Release a plan and its device tables (null is ignored).  Work already
  * enqueued that uses the plan must have finished. */
@@ -152,6 +157,12 @@ rubiconv_status_t rubiconv_filter_spectrum(rubiconv_plan_t plan, const float* fi
 
 /*
  * The packed convolution y = conv(x, k) defined at the top of this file.
+ *
+ * Unlike a call that takes cu_seqlens and the filters directly, this one takes the
+ * plan (which consumed the segment ids once: the data-processing step depends only on
+ * them and is shared by every layer, Appendix, "Precomputation of adaptive
+ * structures") and the filter spectrum (rubiconv_filter_spectrum, the filter side of
+ * Algorithm 3, once per filter bank).  A step of the convolution is the two calls.
  *
  *   x          device [B][N][D] of the plan's x_dtype, channels last, row-major.
  *   spectrum   device spectra written by rubiconv_filter_spectrum with this plan.

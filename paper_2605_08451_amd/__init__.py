@@ -15,6 +15,7 @@ is missing, loading fails loudly -- there is no fallback implementation.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 from typing import Optional
@@ -81,7 +82,7 @@ def load_library():
     lib = ctypes.CDLL(_LIB_PATH)
     vp, i32p, c_int, sz = ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.c_int, ctypes.c_size_t
     lib.rubiconv_plan.argtypes = [ctypes.POINTER(vp), c_int, c_int, c_int, c_int, c_int, i32p,
-                                  c_int, c_int, c_int]
+                                  c_int, c_int, c_int, vp]
     lib.rubiconv_plan.restype = c_int
     lib.rubiconv_plan_destroy.argtypes = [vp]
     lib.rubiconv_plan_destroy.restype = None
@@ -148,6 +149,12 @@ def _check(status: int, what: str):
         raise RubiconvError(what, status)
 
 
+def _on_stream(stream):
+    """Context in which buffers the binding allocates for a call belong to the call's
+    stream: the caching allocator then reuses them only after that stream's work."""
+    return torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
+
+
 def _stream_handle(device, stream) -> int:
     s = torch.cuda.current_stream(device) if stream is None else stream
     return s.cuda_stream
@@ -169,7 +176,7 @@ class Plan:
     (Algorithm 1's data processing; shared by every layer that sees this batch)."""
 
     def __init__(self, cu_seqlens, N: int, D: int, L: int, x_dtype=torch.bfloat16,
-                 y_dtype=None, n1: int = 0):
+                 y_dtype=None, n1: int = 0, stream=None):
         lib = load_library()
         cu = _cu_array(cu_seqlens)
         self.B, self.max_docs = int(cu.shape[0]), int(cu.shape[1] - 1)
@@ -178,9 +185,14 @@ class Plan:
         self.y_dtype = self.x_dtype if y_dtype is None else _dtype_code(y_dtype)
         self._h = ctypes.c_void_p()
         self._lib = lib
+        # the device tables are uploaded on `stream` (the current stream by default);
+        # without a visible GPU the plan is host-only and no stream is touched
+        sh = None
+        if torch.cuda.is_available():
+            sh = (torch.cuda.current_stream() if stream is None else stream).cuda_stream
         _check(lib.rubiconv_plan(ctypes.byref(self._h), self.B, self.N, self.D, self.L,
                                  self.max_docs, cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
-                                 self.x_dtype, self.y_dtype, int(n1)), "rubiconv_plan")
+                                 self.x_dtype, self.y_dtype, int(n1), sh), "rubiconv_plan")
         self.cu_seqlens = cu.copy()
 
     @property
@@ -270,10 +282,11 @@ def filter_spectrum(plan: Plan, filters: torch.Tensor, spectrum: Optional[torch.
     if filters.dtype != torch.float32 or tuple(filters.shape) != (plan.D, plan.L):
         raise ValueError(f"filters must be float32 [{plan.D}, {plan.L}]")
     dev = filters.device
-    if spectrum is None:
-        spectrum = plan.new_spectrum(dev)
-    if workspace is None:
-        workspace = plan.new_workspace(dev)
+    with _on_stream(stream):
+        if spectrum is None:
+            spectrum = plan.new_spectrum(dev)
+        if workspace is None:
+            workspace = plan.new_workspace(dev)
     if spectrum.numel() * spectrum.element_size() < plan.spectrum_bytes:
         raise ValueError("spectrum buffer too small")
     if workspace.numel() * workspace.element_size() < plan.workspace_bytes:
@@ -294,13 +307,14 @@ def packed_conv(plan: Plan, x: torch.Tensor, spectrum: torch.Tensor,
     if tuple(x.shape) != (plan.B, plan.N, plan.D) or x.dtype != _torch_dtype(plan.x_dtype):
         raise ValueError(f"x must be {_torch_dtype(plan.x_dtype)} [{plan.B}, {plan.N}, {plan.D}]")
     dev = x.device
-    if y is None:
-        y = torch.empty((plan.B, plan.N, plan.D), dtype=_torch_dtype(plan.y_dtype), device=dev)
+    with _on_stream(stream):
+        if y is None:
+            y = torch.empty((plan.B, plan.N, plan.D), dtype=_torch_dtype(plan.y_dtype), device=dev)
+        if workspace is None:
+            workspace = plan.new_workspace(dev)
     _cuda_contig(y, "y")
     if tuple(y.shape) != (plan.B, plan.N, plan.D) or y.dtype != _torch_dtype(plan.y_dtype):
         raise ValueError("y has the wrong shape or dtype")
-    if workspace is None:
-        workspace = plan.new_workspace(dev)
     if workspace.numel() * workspace.element_size() < plan.workspace_bytes:
         raise ValueError("workspace buffer too small")
     if spectrum.numel() * spectrum.element_size() < plan.spectrum_bytes:
@@ -345,11 +359,12 @@ def packed_conv_dx(plan: Plan, dy: torch.Tensor, spectrum: torch.Tensor,
     (dy has the plan's y dtype, dx its x dtype)."""
     _check_btd(dy, plan, plan.y_dtype, "dy")
     dev = dy.device
-    if dx is None:
-        dx = torch.empty((plan.B, plan.N, plan.D), dtype=_torch_dtype(plan.x_dtype), device=dev)
+    with _on_stream(stream):
+        if dx is None:
+            dx = torch.empty((plan.B, plan.N, plan.D), dtype=_torch_dtype(plan.x_dtype), device=dev)
+        if workspace is None:
+            workspace = plan.new_workspace(dev)
     _check_btd(dx, plan, plan.x_dtype, "dx")
-    if workspace is None:
-        workspace = plan.new_workspace(dev)
     if workspace.numel() * workspace.element_size() < plan.workspace_bytes:
         raise ValueError("workspace buffer too small")
     if spectrum.numel() * spectrum.element_size() < plan.spectrum_bytes:
@@ -369,13 +384,14 @@ def packed_conv_dk(plan: Plan, x: torch.Tensor, dy: torch.Tensor,
     _check_btd(x, plan, plan.x_dtype, "x")
     _check_btd(dy, plan, plan.y_dtype, "dy")
     dev = x.device
-    if dk is None:
-        dk = torch.empty((plan.D, plan.L), dtype=torch.float32, device=dev)
+    with _on_stream(stream):
+        if dk is None:
+            dk = torch.empty((plan.D, plan.L), dtype=torch.float32, device=dev)
+        if workspace is None:
+            workspace = plan.new_dk_workspace(dev)
     _cuda_contig(dk, "dk")
     if tuple(dk.shape) != (plan.D, plan.L) or dk.dtype != torch.float32:
         raise ValueError(f"dk must be float32 [{plan.D}, {plan.L}]")
-    if workspace is None:
-        workspace = plan.new_dk_workspace(dev)
     if workspace.numel() * workspace.element_size() < plan.dk_workspace_bytes:
         raise ValueError("workspace buffer too small")
     with torch.cuda.device(dev):
@@ -467,10 +483,11 @@ def ct_filter_spectrum(plan: CTPlan, filters: torch.Tensor, spectrum: Optional[t
     if filters.dtype != torch.float32 or tuple(filters.shape) != (plan.D, plan.L):
         raise ValueError(f"filters must be float32 [{plan.D}, {plan.L}]")
     dev = filters.device
-    if spectrum is None:
-        spectrum = plan.new_spectrum(dev)
-    if workspace is None:
-        workspace = plan.new_workspace(dev)
+    with _on_stream(stream):
+        if spectrum is None:
+            spectrum = plan.new_spectrum(dev)
+        if workspace is None:
+            workspace = plan.new_workspace(dev)
     if spectrum.numel() * spectrum.element_size() < plan.spectrum_bytes:
         raise ValueError("spectrum buffer too small")
     if workspace.numel() * workspace.element_size() < plan.workspace_bytes:
@@ -489,11 +506,12 @@ def ct_packed_conv(plan: CTPlan, x: torch.Tensor, spectrum: torch.Tensor,
     """The packed causal convolution through the masked Cooley-Tukey transform."""
     _check_btd(x, plan, plan.x_dtype, "x")
     dev = x.device
-    if y is None:
-        y = torch.empty((plan.B, plan.N, plan.D), dtype=_torch_dtype(plan.y_dtype), device=dev)
+    with _on_stream(stream):
+        if y is None:
+            y = torch.empty((plan.B, plan.N, plan.D), dtype=_torch_dtype(plan.y_dtype), device=dev)
+        if workspace is None:
+            workspace = plan.new_workspace(dev)
     _check_btd(y, plan, plan.y_dtype, "y")
-    if workspace is None:
-        workspace = plan.new_workspace(dev)
     if workspace.numel() * workspace.element_size() < plan.workspace_bytes:
         raise ValueError("workspace buffer too small")
     if spectrum.numel() * spectrum.element_size() < plan.spectrum_bytes:

@@ -647,6 +647,18 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
     if (p.class_points + p.class_points_lr > (int64_t(1) << 31) - 1 ||
         p.grid_points + p.grid_points_lr > (int64_t(1) << 31) - 1)
         return BuildError::kUnsupported;
+    // 32-bit buffer offsets: the column passes address a document's tokens and grid
+    // points (and a size class's taps) with offsets below P D 4 bytes, after the final
+    // row sizes (rounding and class merging may have raised them); the row kernels
+    // address a pair block's grid (and second grid) with offsets below its byte size
+    const int64_t pb_point_bytes = p.grid_half ? 64 : 128;
+    for (const Seg& d : p.docs)
+        if (static_cast<int64_t>(d.P) * D * 4 > (int64_t(1) << 30)) return BuildError::kUnsupported;
+    for (const Seg& c : p.classes)
+        if (static_cast<int64_t>(c.P) * D * 4 > (int64_t(1) << 30)) return BuildError::kUnsupported;
+    if ((p.grid_points + p.grid_points_lr) * pb_point_bytes >= (int64_t(1) << 31) ||
+        (p.class_points + p.class_points_lr) * pb_point_bytes >= (int64_t(1) << 31))
+        return BuildError::kUnsupported;
     *out = std::move(p);
     return BuildError::kOk;
 }

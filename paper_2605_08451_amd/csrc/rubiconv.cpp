@@ -31,6 +31,8 @@ using rubiconv::Seg;
 struct rubiconv_plan_s {
     HostPlan h;
     void* dev = nullptr;  // all device tables, one allocation
+    std::vector<unsigned char> host_image;  // their host copy, the source of the upload
+    hipEvent_t uploaded = nullptr;          // recorded after the upload (destroy waits for it)
     const void* mfma_tab = nullptr;  // matrix-core operand tables (inside dev)
     const void* dense_tab = nullptr; // matrix-core row pass operands (inside dev)
     const int32_t* dense_docs = nullptr;  // documents by 16-point block count (inside dev)
@@ -81,7 +83,7 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) % kAlign) == 0; }
 
-rubiconv_status_t upload(rubiconv_plan_s* pl) {
+rubiconv_status_t upload(rubiconv_plan_s* pl, hipStream_t stream) {
     const HostPlan& h = pl->h;
     const size_t n_segs = h.docs.size() + h.classes.size();
     size_t off = 0;
@@ -108,7 +110,10 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     const size_t o_one = off;        off = align_up(off + n_ones * sizeof(float2));
     const size_t total = off;
 
-    std::vector<unsigned char> img(total, 0);
+    // the host image stays with the plan: the copy below is stream-ordered and may still
+    // be reading it when this call returns
+    std::vector<unsigned char>& img = pl->host_image;
+    img.assign(total, 0);
     std::vector<Seg> segs(h.docs);
     segs.insert(segs.end(), h.classes.begin(), h.classes.end());
     std::memcpy(img.data() + o_segs, segs.data(), n_segs * sizeof(Seg));
@@ -159,8 +164,11 @@ rubiconv_status_t upload(rubiconv_plan_s* pl) {
     e = hipMalloc(&d, total);
     if (e == hipErrorOutOfMemory) return RUBICONV_ERR_ALLOC;
     if (e != hipSuccess) return RUBICONV_ERR_HIP;
-    e = hipMemcpy(d, img.data(), total, hipMemcpyHostToDevice);
+    e = hipMemcpyAsync(d, img.data(), total, hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&pl->uploaded, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventRecord(pl->uploaded, stream);
     if (e != hipSuccess) {
+        (void)hipStreamSynchronize(stream);
         (void)hipFree(d);
         return RUBICONV_ERR_HIP;
     }
@@ -426,7 +434,7 @@ extern "C" {
 
 rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L, int max_docs,
                                 const int32_t* cu_seqlens_host, rubiconv_dtype_t x_dtype,
-                                rubiconv_dtype_t y_dtype, int n1) {
+                                rubiconv_dtype_t y_dtype, int n1, hipStream_t stream) {
     if (!out) return RUBICONV_ERR_ARG;
     *out = nullptr;
     rubiconv_plan_s* pl = new (std::nothrow) rubiconv_plan_s();
@@ -494,8 +502,12 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
         }
         pl->prescale_fwd = v[0] == '1';
     }
-    rubiconv_status_t st = upload(pl);
+    rubiconv_status_t st = upload(pl, stream);
     if (st != RUBICONV_OK) {
+        if (pl->uploaded) {
+            (void)hipEventSynchronize(pl->uploaded);
+            (void)hipEventDestroy(pl->uploaded);
+        }
         destroy_side_streams(pl);
         if (pl->dev) (void)hipFree(pl->dev);
         delete pl;
@@ -507,6 +519,10 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
 
 void rubiconv_plan_destroy(rubiconv_plan_t plan) {
     if (!plan) return;
+    if (plan->uploaded) {  // the upload reads the plan's host image until it completes
+        (void)hipEventSynchronize(plan->uploaded);
+        (void)hipEventDestroy(plan->uploaded);
+    }
     destroy_events(plan);
     destroy_side_streams(plan);
     if (plan->dev) (void)hipFree(plan->dev);

@@ -211,6 +211,20 @@ def test_too_long_document_is_unsupported():
     assert e.value.status == 3
 
 
+def test_32bit_offset_bound_is_unsupported():
+    """Column passes address a document with 32-bit buffer offsets (below P D 4 bytes):
+    a plan whose longest document would reach 2^30 bytes there is refused, the
+    long-context shape (P D 4 = 5.4e8) is not."""
+    N = 262144
+    cu = np.array([[0, N]], dtype=np.int32)
+    with pytest.raises(rc.RubiconvError) as e:
+        rc.Plan(cu, N=N, D=2048, L=N, x_dtype="bf16")
+    assert e.value.status == 3
+    p = rc.Plan(cu, N=N, D=256, L=N, x_dtype="bf16")
+    P = int(p.doc_table()[0, 5])
+    assert P * 256 * 4 <= 1 << 30 < P * 2048 * 4
+
+
 def test_null_arguments_rejected_before_any_device_work():
     lib = rc.load_library()
     plan = rc.Plan(np.array([[0, 8]], dtype=np.int32), N=8, D=2, L=3, x_dtype="f32")
@@ -218,7 +232,7 @@ def test_null_arguments_rejected_before_any_device_work():
     assert lib.rubiconv_packed_conv(plan.handle, None, None, None, None, None) == 1
     assert lib.rubiconv_filter_spectrum(plan.handle, None, None, None, None) == 1
     assert lib.rubiconv_filter_spectrum(plan.handle, 256, 512, 768 + 1, None) == 1  # misaligned
-    assert lib.rubiconv_plan(None, 1, 8, 2, 3, 1, None, 0, 0, 0) == 1
+    assert lib.rubiconv_plan(None, 1, 8, 2, 3, 1, None, 0, 0, 0, None) == 1
     assert lib.rubiconv_spectrum_bytes(None) == 0 and lib.rubiconv_workspace_bytes(None) == 0
     assert lib.rubiconv_status_string(2) == b"invalid cu_seqlens"
     lib.rubiconv_plan_destroy(None)
