@@ -496,6 +496,17 @@ def configs_measurement(args, copy_gbps, cpu):
             "alg_flops": round(fl), "valu_frac_of_peak": round(fl / (mean * 1e-3) / 1e12 / FP32_VALU_TFLOPS, 4),
             "docs": plan.info()["n_docs"], "cu_seqlens_sha256_16": W.cu_hash()}
         print(f"[bench] c{i}: {mean:.4f} +- {ci:.4f} ms", file=sys.stderr, flush=True)
+        if i == 4 and not args.no_ct:   # the masked Cooley-Tukey variant on the long documents
+            ctp = rc.CTPlan(W.cu_seqlens, N=W.N, D=W.D, L=W.L, x_dtype=W.x_dtype, y_dtype=W.y_dtype)
+            cws, cspec = ctp.new_workspace(dev), ctp.new_spectrum(dev)
+
+            def launch_ct(s):
+                rc.ct_filter_spectrum(ctp, k, spectrum=cspec, workspace=cws, stream=s)
+                rc.ct_packed_conv(ctp, x, cspec, y=y, workspace=cws, stream=s)
+            cm, cc, _ = protocol_time(launch_ct, stream, warmup=args.warmup, trials=20)
+            out[f"c{i}"]["cooley_tukey_ms_mean"] = round(cm, 5)
+            out[f"c{i}"]["cooley_tukey_ms_ci95"] = round(cc, 5)
+            del ctp, cws, cspec
         del x, k, plan, ws, spec, y
         torch.cuda.empty_cache()
         if cpu:

@@ -21,8 +21,10 @@
  * allocate, synchronise or print, and every call returns a status.
  *
  * Limits: D must be even, and no document may need a transform larger than
- * 2^15 points (L_i + min(L_i, L) - 1 <= 32768); other requests return
- * RUBICONV_ERR_UNSUPPORTED.
+ * 2^19 points (L_i + min(L_i, L) - 1 <= 524288); other requests return
+ * RUBICONV_ERR_UNSUPPORTED.  Documents above 2^15 points take one more pass over
+ * their transform grid in each direction (the stages between the tile and the
+ * column pass).
  */
 #ifndef RUBICONV_CT_H_
 #define RUBICONV_CT_H_

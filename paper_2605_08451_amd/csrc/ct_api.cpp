@@ -30,7 +30,8 @@ struct DevLayout {
     const int32_t* long_tile_doc = nullptr;
     const int32_t* short_tile_docs = nullptr;
     const int32_t* col_items = nullptr;
-    int n_long_tiles = 0, n_short_tiles = 0, n_items = 0;
+    const int32_t* mid_tiles = nullptr;
+    int n_long_tiles = 0, n_short_tiles = 0, n_items = 0, n_mid = 0;
 };
 
 }  // namespace
@@ -63,7 +64,7 @@ struct Blob {
 };
 
 struct LayoutOffsets {
-    size_t docs, ltd, std_, items;
+    size_t docs, ltd, std_, items, mid;
 };
 
 LayoutOffsets add_layout(Blob& b, const Layout& l) {
@@ -72,6 +73,7 @@ LayoutOffsets add_layout(Blob& b, const Layout& l) {
     o.ltd = b.add(l.long_tile_doc.data(), l.long_tile_doc.size() * 4);
     o.std_ = b.add(l.short_tile_docs.data(), l.short_tile_docs.size() * 4);
     o.items = b.add(l.col_items.data(), l.col_items.size() * 4);
+    o.mid = b.add(l.mid_tiles.data(), l.mid_tiles.size() * 4);
     return o;
 }
 
@@ -84,6 +86,8 @@ DevLayout dev_layout(const unsigned char* base, const LayoutOffsets& o, const La
     d.n_long_tiles = static_cast<int>(l.long_tile_doc.size());
     d.n_short_tiles = static_cast<int>(l.short_tile_docs.size() / 2);
     d.n_items = static_cast<int>(l.col_items.size());
+    d.mid_tiles = reinterpret_cast<const int32_t*>(base + o.mid);
+    d.n_mid = static_cast<int>(l.mid_tiles.size());
     return d;
 }
 
@@ -178,6 +182,9 @@ rubiconv_status_t rubiconv_ct_filter_spectrum(rubiconv_ct_plan_t plan, const flo
         e = rubiconv::ct::launch_front(f.docs, f.long_tile_doc, f.n_long_tiles, 0, taps, 0, h.D, h.npb,
                                        false, fgrid, h.filt.long_points, plan->tw, stream);
     if (e == hipSuccess)
+        e = rubiconv::ct::launch_mid(false, f.docs, f.mid_tiles, f.n_mid, false, fgrid, h.filt.long_points,
+                                     h.npb, plan->tw, stream);
+    if (e == hipSuccess)
         e = rubiconv::ct::launch_col(1, f.docs, f.col_items, f.n_items, false, fgrid, h.filt.long_points,
                                      h.npb, h.grid_half, spectrum, plan->tw, stream);
     if (e == hipSuccess)
@@ -206,8 +213,14 @@ rubiconv_status_t rubiconv_ct_packed_conv(rubiconv_ct_plan_t plan, const void* x
         e = rubiconv::ct::launch_front(d.docs, d.long_tile_doc, d.n_long_tiles, h.x_dtype, x, h.N, h.D,
                                        h.npb, h.grid_half, workspace, h.data.long_points, plan->tw, stream);
     if (e == hipSuccess)
+        e = rubiconv::ct::launch_mid(false, d.docs, d.mid_tiles, d.n_mid, h.grid_half, workspace,
+                                     h.data.long_points, h.npb, plan->tw, stream);
+    if (e == hipSuccess)
         e = rubiconv::ct::launch_col(0, d.docs, d.col_items, d.n_items, h.grid_half, workspace,
                                      h.data.long_points, h.npb, h.grid_half, spec, plan->tw, stream);
+    if (e == hipSuccess)
+        e = rubiconv::ct::launch_mid(true, d.docs, d.mid_tiles, d.n_mid, h.grid_half, workspace,
+                                     h.data.long_points, h.npb, plan->tw, stream);
     if (e == hipSuccess)
         e = rubiconv::ct::launch_back(d.docs, d.long_tile_doc, d.n_long_tiles, h.grid_half, workspace,
                                       h.data.long_points, h.npb, h.y_dtype, y, h.N, h.D, plan->tw, stream);

@@ -14,10 +14,12 @@
 //   * short documents (P <= kTile): one kernel takes a tile of whole documents from
 //     x through the forward stages, the spectral product, the inverse stages and
 //     into y;
-//   * long documents (P = kTile * M, M <= 64): the first kLogTile stages run on
-//     each tile (front), the last log2 M stages on the columns l = c + kTile * j
-//     (column pass, which also takes the product), and the inverse repeats the
-//     split in reverse (column pass, then back).
+//   * long documents (P = kTile * M, M <= 2^(kMaxLogMid + kMaxLogCols)): the first
+//     kLogTile stages run on each tile (front), for M > 64 the next log2 M - 6 stages
+//     on tiles of the column view (middle pass), the last stages (at most 6) on the
+//     columns l = c + S * j of a view of stride S (column pass, which also takes the
+//     product), and the inverse repeats the split in reverse (column pass, middle
+//     pass, then back).
 // The inverse uses decimation-in-frequency stages (the same butterflies with the
 // conjugate twiddles, in reverse order), which take the spectrum in natural order
 // and leave the time samples in bit-reversed order: the forward transform's load
@@ -42,6 +44,7 @@ constexpr int kSlots = kThreads / kPairs;      // 16 element slots per channel-p
 constexpr int kTileGroups = kTile / 8;         // radix-8 groups of one tile
 constexpr int kMaxCols = 1 << kMaxLogCols;
 static_assert(kMaxCols <= kTile / 4, "a column work item needs at least one low column pair");
+static_assert(kMaxLogMid < kLogTile, "a middle-pass tile needs at least one column");
 
 __device__ __forceinline__ int bitrev(int v, int bits) {
     return bits == 0 ? 0 : static_cast<int>(__builtin_bitreverse32(static_cast<uint32_t>(v)) >> (32 - bits));
@@ -456,30 +459,32 @@ __global__ __launch_bounds__(kThreads, 2) void back_kernel(
     }
 }
 
-// Column pass over the columns l = c + kTile * j (j < M) of one long document.  A work
-// item holds kTile points of every pair lane: G = kTile / (2M) low columns
-// c = g * G + s (s < G) and, in the high slots, their partners kTile - c, which hold
-// the frequencies -f of the low columns' frequencies f = c + kTile * j.  Column 0 is
-// its own partner, so the high slot that would repeat it holds column kTile / 2,
-// also its own partner.  A document of M points per column has M work items.
-// LDS row of (slot, j): slot * M + j.
+// Column pass over the columns l = c + S j (j < Mv) of one long document, S = kTile 2^A
+// and Mv = M / 2^A: A = max(0, log2 M - kMaxLogCols) middle stages run first
+// (mid_kernel), so that a column never holds more than 2^kMaxLogCols points.  A work
+// item holds kTile points of every pair lane: G = kTile / (2 Mv) low columns
+// c = g * G + s (s < G) and, in the high slots, their partners S - c, which hold the
+// frequencies -f of the low columns' frequencies f = c + S j.  Column 0 is its own
+// partner, so the high slot that would repeat it holds column S / 2, also its own
+// partner.  A document of M points per 512-point column has M work items.
+// LDS row of (slot, j): slot * Mv + j.
 template <int K, bool INV>
-__device__ __forceinline__ void col_pass(float2 (*s_c)[kPairs], const int* cols, int lg_m, int sigma0,
-                                         GlobalTw tw, int q, int slot) {
-    // stages sigma0 .. sigma0 + K - 1 (> kLogTile): element stride over j is 2^(sigma0 - kLogTile - 1)
-    const int lg_hj = sigma0 - kLogTile - 1;
+__device__ __forceinline__ void col_pass(float2 (*s_c)[kPairs], const int* cols, int lg_v, int lg_s,
+                                         int sigma0, GlobalTw tw, int q, int slot) {
+    // stages sigma0 .. sigma0 + K - 1 (> lg_s): element stride over j is 2^(sigma0 - lg_s - 1)
+    const int lg_hj = sigma0 - lg_s - 1;
     const int hj = 1 << lg_hj;
-    const int lg_per = lg_m - K;  // groups per column: M / 2^K
+    const int lg_per = lg_v - K;  // groups per column: Mv / 2^K
     for (int e = slot; e < (kTile >> K); e += kSlots) {
         const int s = e >> lg_per, g = e & ((1 << lg_per) - 1);
         const int jb = (g & (hj - 1)) + ((g >> lg_hj) << (lg_hj + K));
-        const int row = (s << lg_m) + jb;
+        const int row = (s << lg_v) + jb;
         float2 v[1 << K];
 #pragma unroll
         for (int i = 0; i < (1 << K); ++i) v[i] = s_c[row + i * hj][q];
-        const int b0 = cols[s] + kTile * (jb & (hj - 1));
-        if constexpr (INV) dif_group<K>(v, b0, kTile * hj, sigma0, tw, AllOn{});
-        else dit_group<K>(v, b0, kTile * hj, sigma0, tw, AllOn{});
+        const int b0 = cols[s] + ((jb & (hj - 1)) << lg_s);
+        if constexpr (INV) dif_group<K>(v, b0, hj << lg_s, sigma0, tw, AllOn{});
+        else dit_group<K>(v, b0, hj << lg_s, sigma0, tw, AllOn{});
 #pragma unroll
         for (int i = 0; i < (1 << K); ++i) s_c[row + i * hj][q] = v[i];
     }
@@ -487,19 +492,79 @@ __device__ __forceinline__ void col_pass(float2 (*s_c)[kPairs], const int* cols,
 
 // All stages of the column pass in one direction: passes of 3, then the remainder.
 template <bool INV>
-__device__ __forceinline__ void col_stages(float2 (*s_c)[kPairs], const int* cols, int lg_m, GlobalTw tw,
-                                           int q, int slot) {
-    const int n3 = lg_m / 3, rem = lg_m - 3 * n3;
+__device__ __forceinline__ void col_stages(float2 (*s_c)[kPairs], const int* cols, int lg_v, int lg_s,
+                                           GlobalTw tw, int q, int slot) {
+    const int n3 = lg_v / 3, rem = lg_v - 3 * n3;
     int sig[3], kk[3], n = 0;
-    int s0 = kLogTile + 1;
+    int s0 = lg_s + 1;
     for (int i = 0; i < n3; ++i) { sig[n] = s0; kk[n] = 3; ++n; s0 += 3; }
     if (rem) { sig[n] = s0; kk[n] = rem; ++n; }
     for (int t = 0; t < n; ++t) {
         const int i = INV ? n - 1 - t : t;
-        if (kk[i] == 3) col_pass<3, INV>(s_c, cols, lg_m, sig[i], tw, q, slot);
-        else if (kk[i] == 2) col_pass<2, INV>(s_c, cols, lg_m, sig[i], tw, q, slot);
-        else col_pass<1, INV>(s_c, cols, lg_m, sig[i], tw, q, slot);
+        if (kk[i] == 3) col_pass<3, INV>(s_c, cols, lg_v, lg_s, sig[i], tw, q, slot);
+        else if (kk[i] == 2) col_pass<2, INV>(s_c, cols, lg_v, lg_s, sig[i], tw, q, slot);
+        else col_pass<1, INV>(s_c, cols, lg_v, lg_s, sig[i], tw, q, slot);
         __syncthreads();
+    }
+}
+
+// Middle stages kLogTile + 1 .. kLogTile + A of a document with M = 2^(kMaxLogCols + A)
+// points per 512-point column (A >= 1).  With j = jhi 2^A + jlo, those stages pair
+// j's that differ in jlo only; tile t = jhi 2^A + chunk holds the 512 points
+// l = c + kTile (jhi 2^A + jlo) for the 2^(kLogTile - A) columns c of its chunk and every
+// jlo (LDS row jlo 2^(kLogTile - A) + c - c0).  The forward runs the decimation-in-time
+// stages upwards, the inverse the decimation-in-frequency stages downwards.
+template <bool INV, bool HALF>
+__global__ __launch_bounds__(kThreads, 2) void mid_kernel(const Doc* __restrict__ docs,
+                                                          const int32_t* __restrict__ tiles,
+                                                          void* __restrict__ grid, int64_t long_points,
+                                                          const float2* __restrict__ tw) {
+    __shared__ float2 s_z[kTile][kPairs];
+    const int it = tiles[blockIdx.y], pb = blockIdx.x;
+    const int q = threadIdx.x & (kPairs - 1), slot = threadIdx.x / kPairs;
+    const Doc d = load_doc(docs, it >> kItemBits);
+    const int t = it & ((1 << kItemBits) - 1);
+    const int lg_a = d.logp - kLogTile - kMaxLogCols;  // 1 .. kMaxLogMid
+    const int lg_cn = kLogTile - lg_a;                  // columns per tile
+    const int c0 = (t & ((1 << lg_a) - 1)) << lg_cn, jhi = t >> lg_a;
+    const int64_t row0 = static_cast<int64_t>(pb) * long_points + d.off + c0 +
+                         (static_cast<int64_t>(jhi) << (kLogTile + lg_a));
+    constexpr int kPer = kTile / kSlots;
+    auto flat = [&](int e) {  // LDS row e -> offset from row0: c + kTile * jlo
+        return (e & ((1 << lg_cn) - 1)) + ((e >> lg_cn) << kLogTile);
+    };
+    {
+        float2 r[kPer];
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) r[k] = grid_load<HALF>(grid, (row0 + flat(slot + kSlots * k)) * kPairs + q);
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) s_z[slot + kSlots * k][q] = r[k];
+    }
+    __syncthreads();
+    const GlobalTw gtw{tw};
+    for (int st = 0; st < lg_a; ++st) {
+        const int k = INV ? lg_a - 1 - st : st;   // stage kLogTile + 1 + k: jlo distance 2^k
+        for (int b = slot; b < kTile / 2; b += kSlots) {
+            const int cc = b & ((1 << lg_cn) - 1), jp = b >> lg_cn;
+            const int jlo = ((jp >> k) << (k + 1)) | (jp & ((1 << k) - 1));  // bit k clear
+            const int ea = (jlo << lg_cn) + cc, eb = ea + (1 << (lg_cn + k));
+            const float2 w = gtw(c0 + cc + ((jlo & ((1 << k) - 1)) << kLogTile), kLogTile + 1 + k);
+            const float2 a = s_z[ea][q], bb = s_z[eb][q];
+            if constexpr (INV) {
+                s_z[ea][q] = cadd(a, bb);
+                s_z[eb][q] = mul_conj(csub(a, bb), w);
+            } else {
+                const float2 tb = cmul(w, bb);
+                s_z[ea][q] = cadd(a, tb);
+                s_z[eb][q] = csub(a, tb);
+            }
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+        const int e = slot + kSlots * k;
+        grid_store<HALF>(grid, (row0 + flat(e)) * kPairs + q, s_z[e][q]);
     }
 }
 
@@ -512,18 +577,22 @@ __global__ __launch_bounds__(kThreads, 2) void col_kernel(
     __shared__ int s_part[kTile / 2];  // slot holding the partner column
     const int item = items[blockIdx.y], pb = blockIdx.x;
     const int q = threadIdx.x & (kPairs - 1), slot = threadIdx.x / kPairs;
-    const Doc d = load_doc(docs, item >> kMaxLogCols);
-    const int grp = item & (kMaxCols - 1);
-    const int lg_m = d.logp - kLogTile, M = 1 << lg_m, P = 1 << d.logp;
-    const int lg_g = kLogTile - 1 - lg_m;  // G = kTile / (2M) low columns
+    const Doc d = load_doc(docs, item >> kItemBits);
+    const int grp = item & ((1 << kItemBits) - 1);
+    const int lg_m0 = d.logp - kLogTile;
+    const int lg_a = lg_m0 > kMaxLogCols ? lg_m0 - kMaxLogCols : 0;  // stages of the middle pass
+    const int lg_m = lg_m0 - lg_a;        // points per column of the view (Mv)
+    const int lg_s = kLogTile + lg_a;     // the view's column stride S
+    const int S = 1 << lg_s, M = 1 << lg_m, P = 1 << d.logp;
+    const int lg_g = kLogTile - 1 - lg_m;  // G = kTile / (2 Mv) low columns
     const int G = 1 << lg_g;
     if (threadIdx.x < 2 * G) {
         const int s = threadIdx.x & (G - 1);
         const int lo = grp * G + s;
         const bool high = threadIdx.x >= G;
-        const int c = !high ? lo : (lo == 0 ? kTile / 2 : kTile - lo);
+        const int c = !high ? lo : (lo == 0 ? S / 2 : S - lo);
         s_cols[threadIdx.x] = c;
-        s_part[threadIdx.x] = (c == 0 || c == kTile / 2) ? threadIdx.x : (high ? s : G + s);
+        s_part[threadIdx.x] = (c == 0 || c == S / 2) ? threadIdx.x : (high ? s : G + s);
     }
     __syncthreads();
     const int64_t row0 = static_cast<int64_t>(pb) * long_points + d.off;
@@ -535,7 +604,7 @@ __global__ __launch_bounds__(kThreads, 2) void col_kernel(
         for (int k = 0; k < kPer; ++k) {  // e = j * 2G + slot: adjacent columns adjacent
             const int e = slot + kSlots * k;
             const int s = e & ((2 << lg_g) - 1), j = e >> lg_2g;
-            r[k] = grid_load<HALF>(grid, (row0 + s_cols[s] + static_cast<int64_t>(kTile) * j) * kPairs + q);
+            r[k] = grid_load<HALF>(grid, (row0 + s_cols[s] + (static_cast<int64_t>(j) << lg_s)) * kPairs + q);
         }
 #pragma unroll
         for (int k = 0; k < kPer; ++k) {
@@ -545,12 +614,12 @@ __global__ __launch_bounds__(kThreads, 2) void col_kernel(
     }
     __syncthreads();
     const GlobalTw gtw{tw};
-    col_stages<false>(s_c, s_cols, lg_m, gtw, q, slot);
+    col_stages<false>(s_c, s_cols, lg_m, lg_s, gtw, q, slot);
     if constexpr (MODE == 1) {
         for (int e = slot; e < kTile; e += kSlots) {
             const int s = e & ((2 << lg_g) - 1), j = e >> lg_2g;
             const int c = s_cols[s];
-            const int f = c + kTile * j;
+            const int f = c + (j << lg_s);
             if (2 * f > P) continue;
             const int jn = c == 0 ? (M - j) & (M - 1) : M - 1 - j;
             spectrum_entry<SH>(spec, d.spec + (static_cast<int64_t>(pb) * (P / 2 + 1) + f) * kPairs + q,
@@ -565,7 +634,7 @@ __global__ __launch_bounds__(kThreads, 2) void col_kernel(
         const int64_t sp0 = d.spec + static_cast<int64_t>(pb) * (P / 2 + 1) * kPairs + q;
         auto product = [&](int s, int j) {
             const int c = s_cols[s];
-            const int f = c + kTile * j;
+            const int f = c + (j << lg_s);
             const int jn = c == 0 ? (M - j) & (M - 1) : M - 1 - j;
             const int rf = (s << lg_m) + j, rn = (s_part[s] << lg_m) + jn;
             float2 u, v;
@@ -579,12 +648,12 @@ __global__ __launch_bounds__(kThreads, 2) void col_kernel(
         for (int e = slot; e < kTile / 2; e += kSlots) product(e & ((2 << lg_g) - 1), e >> lg_2g);
         if (grp == 0 && slot == 0) product(0, M / 2);
         __syncthreads();
-        col_stages<true>(s_c, s_cols, lg_m, gtw, q, slot);
+        col_stages<true>(s_c, s_cols, lg_m, lg_s, gtw, q, slot);
 #pragma unroll
         for (int k = 0; k < kPer; ++k) {
             const int e = slot + kSlots * k;
             const int s = e & ((2 << lg_g) - 1), j = e >> lg_2g;
-            grid_store<HALF>(grid, (row0 + s_cols[s] + static_cast<int64_t>(kTile) * j) * kPairs + q,
+            grid_store<HALF>(grid, (row0 + s_cols[s] + (static_cast<int64_t>(j) << lg_s)) * kPairs + q,
                              s_c[(s << lg_m) + j][q]);
         }
     }
@@ -657,6 +726,19 @@ hipError_t launch_col(int mode, const Doc* docs, const int32_t* items, int n_ite
                                                decltype(sh)::value != 0>),
                                    g, dim3(kThreads), 0, stream, docs, items, grid, long_points, spec, tw);
             });
+        });
+    });
+    return hipGetLastError();
+}
+
+hipError_t launch_mid(bool inverse, const Doc* docs, const int32_t* tiles, int n_tiles, bool half,
+                      void* grid, int64_t long_points, int npb, const float2* tw, hipStream_t stream) {
+    if (n_tiles == 0) return hipSuccess;
+    const dim3 g(npb, n_tiles);
+    dispatch2(inverse, [&](auto iv) {
+        dispatch2(half, [&](auto hf) {
+            hipLaunchKernelGGL((mid_kernel<decltype(iv)::value != 0, decltype(hf)::value != 0>), g,
+                               dim3(kThreads), 0, stream, docs, tiles, grid, long_points, tw);
         });
     });
     return hipGetLastError();

@@ -39,6 +39,11 @@ hipError_t launch_col(int mode, const Doc* docs, const int32_t* items, int n_ite
                       void* grid, int64_t long_points, int npb, bool spec_half, void* spec,
                       const float2* tw, hipStream_t stream);
 
+// Long documents of more than 2^kMaxLogCols points per 512-point column: the middle
+// stages (forward, or the inverse's, in place) on every middle-pass tile.
+hipError_t launch_mid(bool inverse, const Doc* docs, const int32_t* tiles, int n_tiles, bool half,
+                      void* grid, int64_t long_points, int npb, const float2* tw, hipStream_t stream);
+
 // Long documents: the last kLogTile inverse stages of every tile, into y.
 hipError_t launch_back(const Doc* docs, const int32_t* tile_doc, int n_tiles, bool half,
                        const void* grid, int64_t long_points, int npb, int out_dtype, void* out,

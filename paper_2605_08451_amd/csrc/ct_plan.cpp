@@ -40,10 +40,15 @@ void pack(std::vector<Doc> docs, const int64_t* class_spec, Layout* out) {
     }
     // column items: M = P / kTile per document (each holds kTile points of every
     // pair lane), document by document, so that the items reading adjacent columns
-    // of one document are dispatched together
+    // of one document are dispatched together; documents with more than 2^kMaxLogCols
+    // points per column also get M middle-pass tiles
+    out->mid_tiles.clear();
     for (int i = 0; i < out->n_long; ++i) {
-        const int M = 1 << (docs[i].logp - kLogTile);
-        for (int g = 0; g < M; ++g) out->col_items.push_back((i << kMaxLogCols) | g);
+        const int lg_m = docs[i].logp - kLogTile;
+        const int M = 1 << lg_m;
+        for (int g = 0; g < M; ++g) out->col_items.push_back((i << kItemBits) | g);
+        if (lg_m > kMaxLogCols)
+            for (int t = 0; t < M; ++t) out->mid_tiles.push_back((i << kItemBits) | t);
     }
     out->short_tile_docs.clear();
     const int64_t n_short_tiles = (out->points - out->long_points) / kTile;

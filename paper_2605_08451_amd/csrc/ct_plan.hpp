@@ -17,7 +17,9 @@ namespace rubiconv::ct {
 constexpr int kLogTile = 9;
 constexpr int kTile = 1 << kLogTile;          // points one workgroup transforms in LDS
 constexpr int kMaxLogCols = 6;                // column pass: up to 64 points per column
-constexpr int kMaxLogP = kLogTile + kMaxLogCols;  // largest transform, 2^15 points
+constexpr int kMaxLogMid = 4;                 // middle pass: up to 4 stages before the column pass
+constexpr int kMaxLogP = kLogTile + kMaxLogMid + kMaxLogCols;  // largest transform, 2^19 points
+constexpr int kItemBits = kMaxLogMid + kMaxLogCols;  // work-item index inside a document
 constexpr int kPairs = 16;                    // channel pairs per block (32 channels)
 
 // One transformed array of the flat layout: a document, or a filter size class.
@@ -38,7 +40,8 @@ struct Layout {
     int64_t points = 0;                   // all points, the short region rounded up to a tile
     std::vector<int32_t> long_tile_doc;   // tile of the long region -> its document
     std::vector<int32_t> short_tile_docs; // tile of the short region -> first and end document
-    std::vector<int32_t> col_items;       // column work item -> document << kMaxLogCols | group
+    std::vector<int32_t> col_items;       // column work item -> document << kItemBits | group
+    std::vector<int32_t> mid_tiles;       // middle-pass tile -> document << kItemBits | tile
 };
 
 struct CtHostPlan {

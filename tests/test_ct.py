@@ -24,7 +24,7 @@ def _say(*a):
 
 
 # ------------------------------------------------------------------ host: plan tables
-@pytest.mark.parametrize("i", [0, 1, 2, 3])
+@pytest.mark.parametrize("i", [0, 1, 2, 3, 4])
 def test_doc_table_matches_oracle(i):
     cu = wl.config_cu_seqlens(i)
     D, L, dt = wl.CONFIG_SHAPES[i]
@@ -53,15 +53,16 @@ def test_plan_errors():
         rc.CTPlan(np.array([[0, 5, 4]], dtype=np.int32), N=4, D=2, L=4, x_dtype="f32")
     assert e.value.status == 2
     with pytest.raises(rc.RubiconvError) as e:
-        rc.CTPlan(np.array([[0, 16385]], dtype=np.int32), N=16385, D=2, L=16385, x_dtype="f32")
-    assert e.value.status == 3                               # needs 2^16 points
-    p = rc.CTPlan(np.array([[0, 16384]], dtype=np.int32), N=16384, D=2, L=16384, x_dtype="f32")
-    assert p.doc_table()[0, 4] == 32768
+        rc.CTPlan(np.array([[0, 262145]], dtype=np.int32), N=262145, D=2, L=262145, x_dtype="f32")
+    assert e.value.status == 3                               # needs 2^20 points
+    p = rc.CTPlan(np.array([[0, 262144]], dtype=np.int32), N=262144, D=2, L=262144, x_dtype="f32")
+    assert p.doc_table()[0, 4] == 524288
+    p = rc.CTPlan(np.array([[0, 16385]], dtype=np.int32), N=16385, D=2, L=16385, x_dtype="f32")
+    assert p.doc_table()[0, 4] == 65536
     p = rc.CTPlan(np.array([[0, 20000]], dtype=np.int32), N=20000, D=2, L=12000, x_dtype="f32")
     assert p.doc_table()[0, 4] == 32768                      # 20000 + 12000 - 1 <= 2^15
-    with pytest.raises(rc.RubiconvError) as e:
-        rc.CTPlan(wl.config_cu_seqlens(4), N=262144, D=256, L=262144, x_dtype="bf16")
-    assert e.value.status == 3
+    p = rc.CTPlan(wl.config_cu_seqlens(4), N=262144, D=256, L=262144, x_dtype="bf16")
+    assert p.doc_table()[:, 4].max() == 524288
 
 
 # ------------------------------------------------------------------ GPU parity
@@ -110,6 +111,43 @@ def test_ct_full_size_sampled(device):
     ref = oracle.conv_at(W.x, W.filters, W.cu_seqlens, btd, threads=ORACLE_THREADS)
     got = y[btd[:, 0], btd[:, 1], btd[:, 2]]
     err = np.linalg.norm(got - ref) / np.linalg.norm(ref)
+    assert err <= TOL[W.x_dtype], err
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_ct_long_documents(device, dtype):
+    """Documents of 2^16 to 2^19 transform points (the middle pass between the tile
+    and the column pass), with filters as long as the row and short ones."""
+    N = 262144
+    rows = [[N], [70000, 30000, 16385, N - 116385]]
+    for L in (N, 5000):
+        W = wl.make_case(rows, D=4 if dtype == "f32" else 32, L=L, x_dtype=dtype, seed=L)
+        P = sorted(set(int(v) for v in rc.CTPlan(W.cu_seqlens, N=N, D=W.D, L=L,
+                                                  x_dtype=dtype).doc_table()[:, 4]))
+        _say(f"[ct] long documents {dtype} L={L}: sizes {P}")
+        assert max(P) >= 65536
+        y = run_ct(W, device)
+        assert_parity(y, reference(W, "fft"), W.cu_seqlens, dtype, f"long {dtype} L={L}")
+
+
+@pytest.mark.gpu
+def test_ct_long_context_sampled(device):
+    """The long-context workload (documents up to 2^19 transform points) at full size,
+    sampled entries against the defining sum."""
+    W = wl.make_config(4)
+    _say("[ct] config 4 sampled")
+    y = run_ct(W, device)
+    rng = np.random.default_rng(104)
+    n = 3000
+    btd = np.stack([np.zeros(n, dtype=np.int64), rng.integers(0, W.N, n), rng.integers(0, W.D, n)], 1)
+    extra = [(0, s, rng.integers(W.D)) for s0, s1 in zip(W.cu_seqlens[0][:-1], W.cu_seqlens[0][1:])
+             if s1 > s0 for s in (s0, s1 - 1)]
+    btd = np.concatenate([btd, np.array(extra, dtype=np.int64)])
+    ref = oracle.conv_at(W.x, W.filters, W.cu_seqlens, btd, threads=ORACLE_THREADS)
+    got = y[btd[:, 0], btd[:, 1], btd[:, 2]]
+    err = np.linalg.norm(got - ref) / np.linalg.norm(ref)
+    _say(f"[ct] config 4 sampled error {err:.2e}")
     assert err <= TOL[W.x_dtype], err
 
 
