@@ -1052,35 +1052,35 @@ __device__ __forceinline__ float pow2_scale(float a, int target) {
     return ldexpf(1.0f, max(-126, min(127, target - e)));
 }
 
-// One workgroup per 8 channel pairs (16 channels): thread t sums the tiles t / 16,
-// t / 16 + 16, ... of channel t % 16 (16 channels x 4 bytes: 64-byte rows), then the 16
-// partial sums of each channel are added in a fixed order.
+// One workgroup per 2 channel pairs (4 channels): thread t sums the tiles t / 4,
+// t / 4 + 64, ... of channel t % 4 (four independent sums in flight), then the 64 partial
+// sums of each channel are added in a fixed order.
 __global__ __launch_bounds__(256) void filter_scale_kernel(const float* __restrict__ partials,
                                                            int ntiles, int D, int npairs,
                                                            float2* __restrict__ pair_scale) {
-    __shared__ float part[16][17];
-    const int c = threadIdx.x & 15, r = threadIdx.x >> 4;
-    const int d = blockIdx.x * 16 + c;
+    __shared__ float part[64][5];
+    const int c = threadIdx.x & 3, r = threadIdx.x >> 2;
+    const int d = blockIdx.x * 4 + c;
     float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
     if (d < D) {
         int t = r;
-        for (; t + 48 < ntiles; t += 64) {  // four independent loads in flight
+        for (; t + 192 < ntiles; t += 256) {
             a0 += partials[static_cast<int64_t>(t) * D + d];
-            a1 += partials[static_cast<int64_t>(t + 16) * D + d];
-            a2 += partials[static_cast<int64_t>(t + 32) * D + d];
-            a3 += partials[static_cast<int64_t>(t + 48) * D + d];
+            a1 += partials[static_cast<int64_t>(t + 64) * D + d];
+            a2 += partials[static_cast<int64_t>(t + 128) * D + d];
+            a3 += partials[static_cast<int64_t>(t + 192) * D + d];
         }
-        for (; t < ntiles; t += 16) a0 += partials[static_cast<int64_t>(t) * D + d];
+        for (; t < ntiles; t += 64) a0 += partials[static_cast<int64_t>(t) * D + d];
     }
     part[r][c] = (a0 + a1) + (a2 + a3);
     __syncthreads();
-    if (threadIdx.x < 8) {
-        const int q = blockIdx.x * 8 + threadIdx.x;
+    if (threadIdx.x < 2) {
+        const int q = blockIdx.x * 2 + threadIdx.x;
         float g = 0.0f;
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
             float a = 0.0f;
-            for (int rr = 0; rr < 16; ++rr) a += part[rr][2 * threadIdx.x + k];
+            for (int rr = 0; rr < 64; ++rr) a += part[rr][2 * threadIdx.x + k];
             g = fmaxf(g, a);
         }
         if (q < npairs) {
@@ -1090,50 +1090,55 @@ __global__ __launch_bounds__(256) void filter_scale_kernel(const float* __restri
     }
 }
 
-// |v| as the bits of a non-negative float, for bf16 pairs (dtype 1) or fp32 words
-__device__ __forceinline__ uint32_t abs_bits_max(uint32_t w, int dtype, uint32_t m) {
-    if (dtype == 1) {
+// |v| as the bits of a non-negative float, for bf16 pairs (DT 1) or fp32 words
+template <int DT>
+__device__ __forceinline__ uint32_t abs_bits_max(uint32_t w, uint32_t m) {
+    if constexpr (DT == 1) {
         m = max(m, w & 0x7fff0000u);
         return max(m, (w << 16) & 0x7fff0000u);
+    } else {
+        return max(m, w & 0x7fffffffu);
     }
-    return max(m, w & 0x7fffffffu);
 }
 
 // Stage 1: workgroup g reduces a grid-strided share of the words; one partial per group.
-// Each thread keeps four 16-byte loads in flight per round.
+// Each thread keeps kAmaxUnroll 16-byte loads in flight per round.
+constexpr int kAmaxUnroll = 8;
+template <int DT>
 __global__ __launch_bounds__(256) void amax_partial_kernel(const uint32_t* __restrict__ in, int64_t nwords,
-                                                           int dtype, uint32_t* __restrict__ parts) {
+                                                           uint32_t* __restrict__ parts) {
     __shared__ uint32_t red[4];
-    uint32_t m = 0;
-    constexpr int kUnroll = 4;
+    uint32_t m0 = 0, m1 = 0;
     const int64_t stride = static_cast<int64_t>(gridDim.x) * 256 * 4;  // words per round-robin step
-    const bool vec = (reinterpret_cast<uintptr_t>(in) & 15) == 0;
     int64_t i = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
-    if (vec) {
-        for (; i + (kUnroll - 1) * stride + 3 < nwords; i += kUnroll * stride) {
-            uint4 w[kUnroll];
+    if ((reinterpret_cast<uintptr_t>(in) & 15) == 0) {
+        for (; i + (kAmaxUnroll - 1) * stride + 3 < nwords; i += kAmaxUnroll * stride) {
+            typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+            u32x4 w[kAmaxUnroll];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) w[u] = *reinterpret_cast<const uint4*>(in + i + u * stride);
+            for (int u = 0; u < kAmaxUnroll; ++u)
+                w[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(in + i + u * stride));
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                m = abs_bits_max(w[u].x, dtype, m);
-                m = abs_bits_max(w[u].y, dtype, m);
-                m = abs_bits_max(w[u].z, dtype, m);
-                m = abs_bits_max(w[u].w, dtype, m);
+            for (int u = 0; u < kAmaxUnroll; ++u) {
+                m0 = abs_bits_max<DT>(w[u].x, m0);
+                m1 = abs_bits_max<DT>(w[u].y, m1);
+                m0 = abs_bits_max<DT>(w[u].z, m0);
+                m1 = abs_bits_max<DT>(w[u].w, m1);
             }
         }
         for (; i + 3 < nwords; i += stride) {
             const uint4 w = *reinterpret_cast<const uint4*>(in + i);
-            m = abs_bits_max(w.x, dtype, m);
-            m = abs_bits_max(w.y, dtype, m);
-            m = abs_bits_max(w.z, dtype, m);
-            m = abs_bits_max(w.w, dtype, m);
+            m0 = abs_bits_max<DT>(w.x, m0);
+            m1 = abs_bits_max<DT>(w.y, m1);
+            m0 = abs_bits_max<DT>(w.z, m0);
+            m1 = abs_bits_max<DT>(w.w, m1);
         }
-        for (; i < nwords; ++i) m = abs_bits_max(in[i], dtype, m);  // the last partial group
+        for (; i < nwords; ++i) m0 = abs_bits_max<DT>(in[i], m0);  // the last partial group
     } else {
         for (; i < nwords; i += stride)
-            for (int k = 0; k < 4 && i + k < nwords; ++k) m = abs_bits_max(in[i + k], dtype, m);
+            for (int k = 0; k < 4 && i + k < nwords; ++k) m0 = abs_bits_max<DT>(in[i + k], m0);
     }
+    uint32_t m = max(m0, m1);
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), o)));
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
@@ -1166,7 +1171,7 @@ __global__ __launch_bounds__(256) void amax_finish_kernel(const uint32_t* __rest
 hipError_t launch_filter_scale(const float* partials, int ntiles, int D, int npairs,
                                float2* pair_scale, hipStream_t stream) {
     if (npairs <= 0) return hipSuccess;
-    hipLaunchKernelGGL(filter_scale_kernel, dim3((npairs + 7) / 8), dim3(256), 0, stream,
+    hipLaunchKernelGGL(filter_scale_kernel, dim3((npairs + 1) / 2), dim3(256), 0, stream,
                        partials, ntiles, D, npairs, pair_scale);
     return hipGetLastError();
 }
@@ -1193,7 +1198,10 @@ hipError_t launch_prescale(int dtype, const void* in, int64_t n, float extra, co
     }
     const int64_t groups = (nwords + 1023) / 1024;
     const int nparts = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(kAmaxParts, groups)));
-    hipLaunchKernelGGL(amax_partial_kernel, dim3(nparts), dim3(256), 0, stream, words, nwords, dtype, work);
+    if (dtype == 1)
+        hipLaunchKernelGGL(amax_partial_kernel<1>, dim3(nparts), dim3(256), 0, stream, words, nwords, work);
+    else
+        hipLaunchKernelGGL(amax_partial_kernel<0>, dim3(nparts), dim3(256), 0, stream, words, nwords, work);
     hipLaunchKernelGGL(amax_finish_kernel, dim3(1), dim3(256), 0, stream, work, nparts, head, tail, extra,
                        prev, out);
     return hipGetLastError();
