@@ -17,18 +17,16 @@ __device__ __forceinline__ uint32_t h2_bits(float re, float im) {  // round to n
     return __builtin_bit_cast(uint32_t, __float22half2_rn(make_float2(re, im)));
 }
 
-// bf16 of f rounded to nearest even (NaN stays a quiet NaN), in the low 16 bits.
+// bf16 of f rounded to nearest even, in the low 16 bits (v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t bf16_rne_bits(float f) {
-    const uint32_t u = __float_as_uint(f);
-    const uint32_t r = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-    return (u & 0x7fffffffu) > 0x7f800000u ? ((u >> 16) | 0x40u) : r;
+    return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
 }
 
-// (bf16(lo), bf16(hi)) rounded to nearest even, in integer arithmetic.  The packed
-// conversion instruction gave wrong results here when its operands came straight
-// from matrix-core products, so every bf16 output goes through this form.
+// (bf16(lo), bf16(hi)) rounded to nearest even: one v_cvt_pk_bf16_f32.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t bf2_bits(float lo, float hi) {
-    return bf16_rne_bits(lo) | (bf16_rne_bits(hi) << 16);
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{lo, hi}), bf16x2_t));
 }
 
 // a * b
