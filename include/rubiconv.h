@@ -38,6 +38,24 @@
  *     the call remains ordered on the caller's stream (and capturable).
  *   - Every call returns a status; nothing is thrown across the ABI.  Argument
  *     errors are detected on the host before anything is enqueued.
+ *
+ * Value range of bf16 inputs.  bf16 x runs on complex fp16 grids (fp16 spectra,
+ * twiddle and separation products; fp32 accumulation in the matrix products), whose
+ * range (6e-8 .. 65504) is far narrower than bf16's.  Two exact power-of-two scales
+ * keep the grids inside it, and are undone in fp32 before the output is rounded:
+ *   - rubiconv_filter_spectrum scales each channel pair's taps so that the larger
+ *     of the two channels' sums of |k| (a bound on every spectrum value) is 2^8;
+ *   - rubiconv_packed_conv scales x by 2^(3 - e), 2^e the power of two at or above
+ *     the largest |x| of the call (one extra read of x), and the gradient calls
+ *     scale dy (and x) the same way.
+ * Within that, results meet the 2e-2 relative L2 bar for finite bf16 inputs whose
+ * outputs are finite in bf16, except for a document whose values lie far below the
+ * call's largest |x| (the x scale is one per call): below about 1e-6 of it its grid
+ * values fall into fp16's subnormal range and lose relative precision.  Setting RUBICONV_PRESCALE=0 in the environment when a plan is
+ * created drops the forward's x scale: x is then taken as it is, which keeps the
+ * range the tests cover (a constant 5 plus unit noise under an all-ones filter, whose
+ * outputs reach 8e4, and rms(x) from 1e-4 to 300); coherent inputs of a few tens and
+ * more can then overflow a grid.  fp32 inputs run on fp32 grids and have no such limit.
  */
 #ifndef RUBICONV_H_
 #define RUBICONV_H_

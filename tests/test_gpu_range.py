@@ -58,6 +58,14 @@ def _case_inputs(case, B, N):
     elif case == "dc5_tiny_filter":      # the all-ones case with every tap 1e-6
         x = 5.0 + rng.standard_normal((B, N, D), dtype=np.float32)
         k = np.full((D, N), 1e-6, dtype=np.float32)
+    elif case == "mixed_1e-4":          # documents alternately at 1 and 1e-4 (one scale per call)
+        x = rng.standard_normal((B, N, D), dtype=np.float32)
+        cu = wl.config_cu_seqlens(2)
+        for b in range(B):
+            for i in range(cu.shape[1] - 1):
+                if i % 2:
+                    x[b, cu[b, i]:cu[b, i + 1]] *= 1e-4
+        k = wl.decaying_filters(rng, D, N)
     else:
         scale = {"wide_300": 300.0, "small_1e-4": 1e-4, "tiny_1e-6": 1e-6, "huge_1e4": 1e4}[case]
         x = scale * rng.standard_normal((B, N, D), dtype=np.float32)
@@ -66,7 +74,7 @@ def _case_inputs(case, B, N):
 
 
 @pytest.mark.parametrize("case", ["dc5_all_ones", "dc5_tiny_filter", "wide_300", "small_1e-4",
-                                  "tiny_1e-6", "huge_1e4"])
+                                  "tiny_1e-6", "huge_1e4", "mixed_1e-4"])
 def test_forward_range(device, case):
     B, N = _shape()
     W = _workload(*_case_inputs(case, B, N))
@@ -79,8 +87,9 @@ def test_forward_range(device, case):
 
 @pytest.mark.parametrize("case", ["dc5_all_ones", "wide_300", "small_1e-4"])
 def test_forward_range_without_prescale(device, monkeypatch, case):
-    """RUBICONV_PRESCALE=0 (x taken as it is): the range the forward then keeps, largest
-    coherent |x| of about 20 and rms(x) down to about 1e-4, still meets the bar."""
+    """RUBICONV_PRESCALE=0 (x taken as it is): the range the forward then keeps (a
+    constant 5 plus unit noise under an all-ones filter, rms(x) from 1e-4 to 300) still
+    meets the bar."""
     monkeypatch.setenv("RUBICONV_PRESCALE", "0")
     B, N = _shape()
     W = _workload(*_case_inputs(case, B, N))
