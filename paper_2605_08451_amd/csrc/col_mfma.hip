@@ -105,23 +105,29 @@ __device__ __forceinline__ void wave_lds_fence() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
 constexpr int kTab2 = 16 * 2 * 64;  // stage-2 operands: 16 matrices x (re, im) x 64 lanes
 
 constexpr int kF16In = 0;   // fp16 channel pairs (filter taps, packed by the pair transpose)
 constexpr int kBf16In = 1;  // bf16 channel pairs (x): used as bf16 operands as loaded
 
-template <int IN>
+// AMAX: each column task also writes the largest |x| it loaded (bf16 magnitude bits) to
+// amax_out[task].  run_flag: when not null, the launch does nothing unless *run_flag != 0.
+template <int IN, bool AMAX>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void col_fwd_mfma_kernel(const void* __restrict__ src,
                                                            int64_t src_row_stride, int D,
                                                            uint32_t* __restrict__ grid,
                                                            int64_t grid_pb_stride, LaunchTables t,
                                                            GridScale sc,
                                                            const u4* __restrict__ mt, int npb,
-                                                           int ntasks) {
+                                                           int ntasks, uint32_t* __restrict__ amax_out,
+                                                           const int* __restrict__ run_flag) {
     // stage-2 operands, shared by the workgroup's four column tasks
     __shared__ u4 tab2[kTab2];
     // per wave: one output row group (16 grid rows x 16 pairs) on its way to 16-byte stores
     __shared__ uint32_t ring_all[4][256];
+    if (run_flag != nullptr && *run_flag == 0) return;  // the whole workgroup, before any barrier
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
     copy_to_lds(mt + kMtFwd2, tab2, kTab2 / 64, wave, lane);
@@ -187,6 +193,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     __builtin_amdgcn_sched_barrier(0);
 
     uint32_t y[16][4];
+    uint32_t amax_lo = 0, amax_hi = 0;  // the largest bf16 magnitude bits of the loaded x
 #pragma unroll
     for (int n2 = 0; n2 < 16; ++n2) {
         const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -198,9 +205,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             dre = mma_f16(a[0], xb[n2], zero);
             dim = mma_f16(a[1], xb[n2], zero);
         }
+        if constexpr (AMAX) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                amax_lo = max(amax_lo, xb[n2][i] & 0x7fffu);
+                amax_hi = max(amax_hi, xb[n2][i] & 0x7fff0000u);
+            }
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r) y[n2][r] = pack_h2(dre[r] * in_mul, dim[r] * in_mul);
     }
+    const uint32_t amax_lane = max(amax_lo, amax_hi >> 16);
     // y[n2][r] = D[k1 = 4h + r][n2]; regroup so that lane group h holds n2 = 4h + r'
 #pragma unroll
     for (int r = 0; r < 4; ++r)
@@ -242,6 +257,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             __builtin_amdgcn_raw_buffer_store_b128(v, rg, static_cast<int>(st_lane), 0, 0);
             wave_lds_fence();  // the ring is rewritten for the next k1
         }
+    }
+    if constexpr (AMAX) {  // at the end, where few registers are live; every lane stores the same word
+        uint32_t mx = amax_lane;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) mx = max(mx, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mx), o)));
+        amax_out[task] = mx;
     }
 }
 
@@ -395,18 +416,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 hipError_t launch_col_fwd_mfma(int src_dtype, const void* src, int64_t src_row_stride, int D,
                                void* grid, int64_t grid_pb_stride, const LaunchTables& t,
                                GridScale sc, const void* mtab, int n_cols, int npb,
-                               hipStream_t stream) {
+                               hipStream_t stream, uint32_t* amax_out, const int* run_flag) {
     if (n_cols == 0) return hipSuccess;
+    if (amax_out != nullptr && src_dtype != 1) return hipErrorInvalidValue;
     const int ntasks = n_cols * npb;
     const dim3 g((ntasks + 3) / 4), b(256);
     const u4* mt = static_cast<const u4*>(mtab);
     uint32_t* gp = static_cast<uint32_t*>(grid);
-    if (src_dtype == 1)
-        hipLaunchKernelGGL(col_fwd_mfma_kernel<kBf16In>, g, b, 0, stream, src, src_row_stride, D, gp,
-                           grid_pb_stride, t, sc, mt, npb, ntasks);
+    if (src_dtype == 1 && amax_out != nullptr)
+        hipLaunchKernelGGL((col_fwd_mfma_kernel<kBf16In, true>), g, b, 0, stream, src, src_row_stride, D, gp,
+                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, run_flag);
+    else if (src_dtype == 1)
+        hipLaunchKernelGGL((col_fwd_mfma_kernel<kBf16In, false>), g, b, 0, stream, src, src_row_stride, D, gp,
+                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, run_flag);
     else
-        hipLaunchKernelGGL(col_fwd_mfma_kernel<kF16In>, g, b, 0, stream, src, src_row_stride, D, gp,
-                           grid_pb_stride, t, sc, mt, npb, ntasks);
+        hipLaunchKernelGGL((col_fwd_mfma_kernel<kF16In, false>), g, b, 0, stream, src, src_row_stride, D, gp,
+                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, run_flag);
     return hipGetLastError();
 }
 

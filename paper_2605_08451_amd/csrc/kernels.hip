@@ -1168,6 +1168,29 @@ __global__ __launch_bounds__(256) void amax_finish_kernel(const uint32_t* __rest
     }
 }
 
+__global__ __launch_bounds__(1024) void amax_check_kernel(const uint32_t* __restrict__ parts, int n,
+                                                           float2* __restrict__ used, int* __restrict__ redo) {
+    __shared__ uint32_t red[16];
+    uint32_t m = 0;
+    for (int i = threadIdx.x; i < n; i += 1024) m = max(m, parts[i]);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), o)));
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t r = 0;
+        for (int w = 0; w < 16; ++w) r = max(r, red[w]);
+        const float s = pow2_scale(__uint_as_float(r << 16), kDataAmaxExp);
+        used[0] = make_float2(s, 1.0f / s);
+        redo[0] = s != 1.0f ? 1 : 0;
+    }
+}
+
+hipError_t launch_amax_check(const uint32_t* parts, int n, float2* used, int* redo, hipStream_t stream) {
+    hipLaunchKernelGGL(amax_check_kernel, dim3(1), dim3(1024), 0, stream, parts, n, used, redo);
+    return hipGetLastError();
+}
+
 hipError_t launch_filter_scale(const float* partials, int ntiles, int D, int npairs,
                                float2* pair_scale, hipStream_t stream) {
     if (npairs <= 0) return hipSuccess;

@@ -115,10 +115,14 @@ constexpr int kMtEntries = 4608;
 
 // src_dtype 1: bf16 channels [rows][N][D] (x); 0: fp16 channel pairs [taps][D / 2] from
 // launch_transpose_pairs (filter taps).
+// amax_out (bf16 sources only; null for none): per column task, the largest bf16 magnitude
+// bits of the x it loaded.  run_flag (null for none): the launch does nothing unless
+// *run_flag != 0 (device memory written by an earlier kernel on the stream).
 hipError_t launch_col_fwd_mfma(int src_dtype, const void* src, int64_t src_row_stride, int D,
                                void* grid, int64_t grid_pb_stride, const LaunchTables& t,
                                GridScale sc, const void* mtab, int n_cols, int npb,
-                               hipStream_t stream);
+                               hipStream_t stream, uint32_t* amax_out = nullptr,
+                               const int* run_flag = nullptr);
 
 hipError_t launch_col_inv_mfma(int y_dtype, const void* grid, int64_t grid_pb_stride, void* dst,
                                int64_t dst_row_stride, int D, const LaunchTables& t,
@@ -165,6 +169,11 @@ hipError_t launch_filter_scale(const float* partials, int ntiles, int D, int npa
 // out = {s * extra, (prev ? prev->y : 1) / (s * extra)}.  work: kAmaxParts uint32.
 constexpr int kDataAmaxExp = 3;
 constexpr int kAmaxParts = 2048;
+
+// The unit-scale check of a column pass that recorded amax per task: from the n magnitude
+// words in parts (bf16 bits), the scale s = 2^(kDataAmaxExp - e) of the largest |x|; writes
+// used = {s, 1/s} and *redo = (s != 1), i.e. whether the pass must run again with s.
+hipError_t launch_amax_check(const uint32_t* parts, int n, float2* used, int* redo, hipStream_t stream);
 hipError_t launch_prescale(int dtype, const void* in, int64_t n, float extra, const float2* prev,
                            float2* out, uint32_t* work, hipStream_t stream);
 

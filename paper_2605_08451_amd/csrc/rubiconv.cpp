@@ -80,6 +80,8 @@ struct rubiconv_plan_s {
 namespace {
 
 constexpr size_t kAlign = 256;
+// byte offset of the forward's redo flag in the workspace header (after the scale words)
+constexpr size_t kRedoFlagOffset = 128;
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) % kAlign) == 0; }
 
@@ -313,21 +315,40 @@ std::string stage(const char* tag, const char* name) { return std::string(tag) +
 // (dtype out_dtype).  own_rows: every document's second grid rows are its own (the
 // filter gradient), so the matrix-core row pass takes one document per task instead
 // of groups of a size class.  The caller holds the plan's launch mutex.
+// spec (matrix-core column pass, bf16 input only): the column pass runs at in_sc's scale
+// while recording |in|'s largest value per task into spec->parts; a check then writes the
+// exact power-of-two scale to spec->used and, when it differs from the one used, sets
+// spec->redo, on which a second launch of the column pass redoes it at the exact scale.
+struct SpecScale {
+    uint32_t* parts;
+    float2* used;
+    int* redo;
+};
+
 hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, const void* fgrid,
                         int64_t fgrid_pb_stride, const LaunchTables& t, void* out, int out_dtype,
                         void* grid, int corr, bool own_rows, GridScale in_sc, GridScale out_sc,
-                        const char* tag, hipStream_t stream, StageRecorder& rec) {
+                        const char* tag, hipStream_t stream, StageRecorder& rec,
+                        const SpecScale* spec = nullptr) {
     const HostPlan& h = plan->h;
     const int n_cols = static_cast<int>(h.doc_col_seg.size());
     const int64_t rs = static_cast<int64_t>(h.N) * h.D;
     const bool half = h.grid_half;
-    hipError_t e = h.col_mfma && in_dtype == RUBICONV_BF16
-                       ? rubiconv::launch_col_fwd_mfma(in_dtype, in, rs, h.D, grid,
-                                                       plan->grid_pb_stride, plan->doc_t, in_sc,
-                                                       plan->mfma_tab, n_cols, h.npb, stream)
-                       : rubiconv::launch_col_fwd(h.r, half, in_dtype, in, rs, h.D, grid,
-                                                  plan->grid_pb_stride, plan->doc_t, in_sc, n_cols,
-                                                  h.npb, stream);
+    const bool mfma = h.col_mfma && in_dtype == RUBICONV_BF16;
+    if (spec != nullptr && !mfma) return hipErrorInvalidValue;
+    hipError_t e = mfma ? rubiconv::launch_col_fwd_mfma(in_dtype, in, rs, h.D, grid, plan->grid_pb_stride,
+                                                        plan->doc_t, in_sc, plan->mfma_tab, n_cols, h.npb,
+                                                        stream, spec ? spec->parts : nullptr)
+                        : rubiconv::launch_col_fwd(h.r, half, in_dtype, in, rs, h.D, grid,
+                                                   plan->grid_pb_stride, plan->doc_t, in_sc, n_cols,
+                                                   h.npb, stream);
+    if (spec != nullptr && n_cols > 0) {
+        if (e == hipSuccess) e = rubiconv::launch_amax_check(spec->parts, n_cols * h.npb, spec->used, spec->redo, stream);
+        if (e == hipSuccess)
+            e = rubiconv::launch_col_fwd_mfma(in_dtype, in, rs, h.D, grid, plan->grid_pb_stride, plan->doc_t,
+                                              {in_sc.pair, spec->used}, plan->mfma_tab, n_cols, h.npb, stream,
+                                              nullptr, spec->redo);
+    }
     rec.mark(stage(tag, "col_fwd"));
     // long rows: first level into the sub-row regions (both grids of the filter gradient)
     for (const rubiconv::LrItem& it : h.lr_doc_items)
@@ -485,7 +506,10 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
     const size_t conv_ws = align_up(static_cast<size_t>(h.npb) * pl->grid_pb_stride * esz);
     const size_t filt_ws =
         pl->taps_bytes + align_up(static_cast<size_t>(rubiconv::tap_tile_rows(std::max(h.taps_max, 1))) * h.D * 4);
-    const size_t hdr_bytes = kAlign + align_up(rubiconv::kAmaxParts * 4);
+    // header: the scale words (and the redo flag) in the first kAlign bytes, then the amax
+    // partials: kAmaxParts of the prescale pass, or one per task of the forward column pass
+    const size_t n_tasks = h.doc_col_seg.size() * static_cast<size_t>(h.npb);
+    const size_t hdr_bytes = kAlign + align_up(std::max<size_t>(rubiconv::kAmaxParts, n_tasks) * 4);
     pl->ws_hdr_off = std::max(conv_ws, filt_ws);
     pl->ws_bytes = pl->ws_hdr_off + hdr_bytes;
     pl->grid_bytes = conv_ws;
@@ -603,18 +627,24 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
                                            plan->direct_segs, static_cast<int>(h.direct_docs.size()),
                                            h.N, h.D, h.L, h.y_dtype, y, s);
         });
-    // range scales: the filter's per pair, and x's prescale when asked for
+    // range scales: the filter's per pair, and x's power-of-two prescale when asked for.
+    // On the matrix-core path the column pass first runs at scale 1 and records |x|'s
+    // largest value; it runs again only when that value asks for another scale (|x| of
+    // unit-variance activations, up to 8, keeps scale 1), which saves a read of x.
     const float2* xs = plan->ones;
-    if (e == hipSuccess && h.grid_half && plan->prescale_fwd) {
-        float2* w = prescale_words(workspace, plan->ws_hdr_off);
+    float2* w = prescale_words(workspace, plan->ws_hdr_off);
+    SpecScale spec{prescale_work(workspace, plan->ws_hdr_off), w,
+                   reinterpret_cast<int*>(reinterpret_cast<char*>(w) + kRedoFlagOffset)};
+    const bool speculative = h.grid_half && plan->prescale_fwd && h.col_mfma && h.x_dtype == RUBICONV_BF16;
+    if (e == hipSuccess && h.grid_half && plan->prescale_fwd && !speculative) {
         e = prescale(plan, h.x_dtype, x, 1.0f, nullptr, w, prescale_work(workspace, plan->ws_hdr_off), stream);
         rec.mark("prescale");
         xs = w;
     }
     if (e == hipSuccess)
         e = enqueue_conv(plan, x, h.x_dtype, spectrum, plan->cls_pb_stride, plan->doc_t, y, h.y_dtype,
-                         workspace, 0, false, {plan->ones, xs}, {filter_scales(plan, spectrum), xs}, "",
-                         stream, rec);
+                         workspace, 0, false, {plan->ones, xs}, {filter_scales(plan, spectrum), speculative ? w : xs},
+                         "", stream, rec, speculative ? &spec : nullptr);
     if (e == hipSuccess && direct) e = join_direct(plan, stream, rec);
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }
