@@ -121,7 +121,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                                                            int64_t grid_pb_stride, LaunchTables t,
                                                            GridScale sc,
                                                            const u4* __restrict__ mt, int npb,
-                                                           int ntasks, uint32_t* __restrict__ amax_out,
+                                                           int ntasks, uint16_t* __restrict__ amax_out,
                                                            const int* __restrict__ run_flag) {
     // stage-2 operands, shared by the workgroup's four column tasks
     __shared__ u4 tab2[kTab2];
@@ -133,136 +133,137 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     copy_to_lds(mt + kMtFwd2, tab2, kTab2 / 64, wave, lane);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();  // the only workgroup barrier
-    // wave-uniform task index: keeps the document's buffer resource in SGPRs
-    const int task = blockIdx.x * 4 + wave;
-    if (task >= ntasks) return;  // whole wave
-    const int col = task / npb, pb = task - col * npb;
-    const Seg* sg = t.segs + t.col_seg[col];
-    const int j = col - sg->col0, m = sg->m, len = sg->len;
-    const int p = lane & 15, h = lane >> 4;
-    const int ch = 2 * (pb * kPairsPerBlock + p);
-    constexpr int ES = 2;  // bytes per channel
-    uint32_t* ring = ring_all[wave];
+    // wave-uniform task index: keeps the document's buffer resource in SGPRs.  A launch
+    // with fewer workgroups than ntasks / 4 (the redo launch) loops over the tasks.
+    for (int task = blockIdx.x * 4 + wave; task < ntasks; task += static_cast<int>(gridDim.x) * 4) {
+        const int col = task / npb, pb = task - col * npb;
+        const Seg* sg = t.segs + t.col_seg[col];
+        const int j = col - sg->col0, m = sg->m, len = sg->len;
+        const int p = lane & 15, h = lane >> 4;
+        const int ch = 2 * (pb * kPairsPerBlock + p);
+        constexpr int ES = 2;  // bytes per channel
+        uint32_t* ring = ring_all[wave];
 
-    const char* doc = static_cast<const char*>(src) +
-                      (static_cast<int64_t>(sg->row) * src_row_stride +
-                       static_cast<int64_t>(sg->start) * D) * ES;
-    const int64_t doc_bytes = static_cast<int64_t>(len) * D * ES;
+        const char* doc = static_cast<const char*>(src) +
+                          (static_cast<int64_t>(sg->row) * src_row_stride +
+                           static_cast<int64_t>(sg->start) * D) * ES;
+        const int64_t doc_bytes = static_cast<int64_t>(len) * D * ES;
 
-    // stage 1: one MFMA tile per n2 (bf16: hi and lo matrix halves accumulate).
-    // Token t = m (16 n1 + n2) + j with n1 = 4i + h (operand slot 4h + i; the
-    // matrix tables use the same interleaving): a lane part and a wave-uniform part.
-    // All loads are issued before the first MFMA so that the wave waits once.
-    u4 xb[16];
-    {
-        uint32_t lane_off[4];
+        // stage 1: one MFMA tile per n2 (bf16: hi and lo matrix halves accumulate).
+        // Token t = m (16 n1 + n2) + j with n1 = 4i + h (operand slot 4h + i; the
+        // matrix tables use the same interleaving): a lane part and a wave-uniform part.
+        // All loads are issued before the first MFMA so that the wave waits once.
+        u4 xb[16];
+        {
+            uint32_t lane_off[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            lane_off[i] = (static_cast<uint32_t>(m) * 16u * (4 * i + h) * D + ch) * ES;
+            for (int i = 0; i < 4; ++i)
+                lane_off[i] = (static_cast<uint32_t>(m) * 16u * (4 * i + h) * D + ch) * ES;
+#pragma unroll
+            for (int n2 = 0; n2 < 16; ++n2) {
+                const __amdgpu_buffer_rsrc_t rs =
+                    sub_buffer(doc, doc_bytes, static_cast<int64_t>(m * n2 + j) * D * ES);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int off = static_cast<int>(lane_off[i]);
+                    xb[n2][i] = __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
+                }
+            }
+        }
+        // per-document twiddle w_P^(u j) = w_P^(k1 j) * w_P^(16 k2 j), u = k1 + 16 k2: the first
+        // factor is wave-uniform, the second has four values per lane (k2 = 4 r2 + h)
+        const __amdgpu_buffer_rsrc_t rt = doc_buffer(t.tw + sg->twf_off, static_cast<uint32_t>(sg->P) * 8);
+        uint32_t tw_lane[4];  // complex fp16
+#pragma unroll
+        for (int r2 = 0; r2 < 4; ++r2) {
+            const auto w = __builtin_amdgcn_raw_buffer_load_b64(
+                rt, static_cast<int>(16u * (4 * r2 + h) * j * 8), 0, 0);
+            tw_lane[r2] = h2_bits(__uint_as_float(w[0]), __uint_as_float(w[1]));
+        }
+        u4 a[4];
+        if constexpr (IN == kBf16In) {
+#pragma unroll
+            for (int o = 0; o < 4; ++o) a[o] = mt[kMtFwd1Bf16 + o * 64 + lane];
+        } else {
+#pragma unroll
+            for (int o = 0; o < 2; ++o) a[o] = mt[kMtFwd1F16 + o * 64 + lane];
+        }
+        // range scale of this lane's pair, applied to the fp32 products before fp16 rounding
+        const float in_mul = sc.pair[pb * kPairsPerBlock + p].x * sc.glob->x;
+        __builtin_amdgcn_sched_barrier(0);
+
+        uint32_t y[16][4];
+        uint32_t amax_lo = 0, amax_hi = 0;  // the largest bf16 magnitude bits of the loaded x
 #pragma unroll
         for (int n2 = 0; n2 < 16; ++n2) {
-            const __amdgpu_buffer_rsrc_t rs =
-                sub_buffer(doc, doc_bytes, static_cast<int64_t>(m * n2 + j) * D * ES);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int off = static_cast<int>(lane_off[i]);
-                xb[n2][i] = __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
-            }
-        }
-    }
-    // per-document twiddle w_P^(u j) = w_P^(k1 j) * w_P^(16 k2 j), u = k1 + 16 k2: the first
-    // factor is wave-uniform, the second has four values per lane (k2 = 4 r2 + h)
-    const __amdgpu_buffer_rsrc_t rt = doc_buffer(t.tw + sg->twf_off, static_cast<uint32_t>(sg->P) * 8);
-    uint32_t tw_lane[4];  // complex fp16
-#pragma unroll
-    for (int r2 = 0; r2 < 4; ++r2) {
-        const auto w = __builtin_amdgcn_raw_buffer_load_b64(
-            rt, static_cast<int>(16u * (4 * r2 + h) * j * 8), 0, 0);
-        tw_lane[r2] = h2_bits(__uint_as_float(w[0]), __uint_as_float(w[1]));
-    }
-    u4 a[4];
-    if constexpr (IN == kBf16In) {
-#pragma unroll
-        for (int o = 0; o < 4; ++o) a[o] = mt[kMtFwd1Bf16 + o * 64 + lane];
-    } else {
-#pragma unroll
-        for (int o = 0; o < 2; ++o) a[o] = mt[kMtFwd1F16 + o * 64 + lane];
-    }
-    // range scale of this lane's pair, applied to the fp32 products before fp16 rounding
-    const float in_mul = sc.pair[pb * kPairsPerBlock + p].x * sc.glob->x;
-    __builtin_amdgcn_sched_barrier(0);
-
-    uint32_t y[16][4];
-    uint32_t amax_lo = 0, amax_hi = 0;  // the largest bf16 magnitude bits of the loaded x
-#pragma unroll
-    for (int n2 = 0; n2 < 16; ++n2) {
-        const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
-        f4 dre, dim;
-        if constexpr (IN == kBf16In) {
-            dre = mma_bf16(a[1], xb[n2], mma_bf16(a[0], xb[n2], zero));
-            dim = mma_bf16(a[3], xb[n2], mma_bf16(a[2], xb[n2], zero));
-        } else {
-            dre = mma_f16(a[0], xb[n2], zero);
-            dim = mma_f16(a[1], xb[n2], zero);
-        }
-        if constexpr (AMAX) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                amax_lo = max(amax_lo, xb[n2][i] & 0x7fffu);
-                amax_hi = max(amax_hi, xb[n2][i] & 0x7fff0000u);
-            }
-        }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) y[n2][r] = pack_h2(dre[r] * in_mul, dim[r] * in_mul);
-    }
-    const uint32_t amax_lane = max(amax_lo, amax_hi >> 16);
-    // y[n2][r] = D[k1 = 4h + r][n2]; regroup so that lane group h holds n2 = 4h + r'
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-#pragma unroll
-        for (int rp = 0; rp < 4; ++rp)
-            lanegroup_transpose(y[rp][r], y[4 + rp][r], y[8 + rp][r], y[12 + rp][r]);
-
-    // stage 2 per k1 = 4g + r, then the per-document twiddle and the fp16 store
-    const float2* twf = t.tw + sg->twf_off;
-    const uint32_t* gdoc = grid + pb * grid_pb_stride + sg->grid_off * kPairsPerBlock;
-    const int64_t grid_bytes = static_cast<int64_t>(sg->P) * kPairsPerBlock * 4;
-    const uint32_t g_lane = (static_cast<uint32_t>(j) * kPairsPerBlock + p) * 4;
-    // 16-byte stores: lane l writes pairs 4 (l % 4) .. + 3 of grid row u = k1 + 16 (l / 4)
-    const uint32_t st_lane = (static_cast<uint32_t>(16 * (lane >> 2)) * m + j) * (kPairsPerBlock * 4) +
-                             (lane & 3) * 16;
-    (void)g_lane;
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int k1 = 4 * g + r;
-            const u4 b = {y[4 * g][r], y[4 * g + 1][r], y[4 * g + 2][r], y[4 * g + 3][r]};
-            const u4 are = tab2[(2 * k1) * 64 + lane];
-            const u4 aim = tab2[(2 * k1 + 1) * 64 + lane];
             const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
-            const f4 dre = mma_f16(are, b, zero);
-            const f4 dim = mma_f16(aim, b, zero);
-            // both table factors carry 1/sqrt(N1): undo one (x 16, exact)
-            const float2 tkf = cscale(twf[k1 * j], 16.0f);  // wave-uniform
-            const uint32_t tk = h2_bits(tkf.x, tkf.y);
-            // register r2 of lane (p, h) is grid row k1 + 16 (4 r2 + h), pair p
+            f4 dre, dim;
+            if constexpr (IN == kBf16In) {
+                dre = mma_bf16(a[1], xb[n2], mma_bf16(a[0], xb[n2], zero));
+                dim = mma_bf16(a[3], xb[n2], mma_bf16(a[2], xb[n2], zero));
+            } else {
+                dre = mma_f16(a[0], xb[n2], zero);
+                dim = mma_f16(a[1], xb[n2], zero);
+            }
+            if constexpr (AMAX) {
 #pragma unroll
-            for (int r2 = 0; r2 < 4; ++r2)
-                ring[(4 * r2 + h) * 16 + p] = cmul_h2(cmul_h2(h2_bits(dre[r2], dim[r2]), tk), tw_lane[r2]);
-            wave_lds_fence();
-            const u4 v = *reinterpret_cast<const u4*>(ring + lane * 4);
-            const __amdgpu_buffer_rsrc_t rg =
-                sub_buffer(gdoc, grid_bytes, static_cast<int64_t>(k1) * m * (kPairsPerBlock * 4));
-            __builtin_amdgcn_raw_buffer_store_b128(v, rg, static_cast<int>(st_lane), 0, 0);
-            wave_lds_fence();  // the ring is rewritten for the next k1
+                for (int i = 0; i < 4; ++i) {
+                    amax_lo = max(amax_lo, xb[n2][i] & 0x7fffu);
+                    amax_hi = max(amax_hi, xb[n2][i] & 0x7fff0000u);
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) y[n2][r] = pack_h2(dre[r] * in_mul, dim[r] * in_mul);
         }
-    }
-    if constexpr (AMAX) {  // at the end, where few registers are live; every lane stores the same word
-        uint32_t mx = amax_lane;
+        const uint32_t amax_lane = max(amax_lo, amax_hi >> 16);
+        // y[n2][r] = D[k1 = 4h + r][n2]; regroup so that lane group h holds n2 = 4h + r'
 #pragma unroll
-        for (int o = 32; o > 0; o >>= 1) mx = max(mx, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mx), o)));
-        amax_out[task] = mx;
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int rp = 0; rp < 4; ++rp)
+                lanegroup_transpose(y[rp][r], y[4 + rp][r], y[8 + rp][r], y[12 + rp][r]);
+
+        // stage 2 per k1 = 4g + r, then the per-document twiddle and the fp16 store
+        const float2* twf = t.tw + sg->twf_off;
+        const uint32_t* gdoc = grid + pb * grid_pb_stride + sg->grid_off * kPairsPerBlock;
+        const int64_t grid_bytes = static_cast<int64_t>(sg->P) * kPairsPerBlock * 4;
+        const uint32_t g_lane = (static_cast<uint32_t>(j) * kPairsPerBlock + p) * 4;
+        // 16-byte stores: lane l writes pairs 4 (l % 4) .. + 3 of grid row u = k1 + 16 (l / 4)
+        const uint32_t st_lane = (static_cast<uint32_t>(16 * (lane >> 2)) * m + j) * (kPairsPerBlock * 4) +
+                                 (lane & 3) * 16;
+        (void)g_lane;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int k1 = 4 * g + r;
+                const u4 b = {y[4 * g][r], y[4 * g + 1][r], y[4 * g + 2][r], y[4 * g + 3][r]};
+                const u4 are = tab2[(2 * k1) * 64 + lane];
+                const u4 aim = tab2[(2 * k1 + 1) * 64 + lane];
+                const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+                const f4 dre = mma_f16(are, b, zero);
+                const f4 dim = mma_f16(aim, b, zero);
+                // both table factors carry 1/sqrt(N1): undo one (x 16, exact)
+                const float2 tkf = cscale(twf[k1 * j], 16.0f);  // wave-uniform
+                const uint32_t tk = h2_bits(tkf.x, tkf.y);
+                // register r2 of lane (p, h) is grid row k1 + 16 (4 r2 + h), pair p
+#pragma unroll
+                for (int r2 = 0; r2 < 4; ++r2)
+                    ring[(4 * r2 + h) * 16 + p] = cmul_h2(cmul_h2(h2_bits(dre[r2], dim[r2]), tk), tw_lane[r2]);
+                wave_lds_fence();
+                const u4 v = *reinterpret_cast<const u4*>(ring + lane * 4);
+                const __amdgpu_buffer_rsrc_t rg =
+                    sub_buffer(gdoc, grid_bytes, static_cast<int64_t>(k1) * m * (kPairsPerBlock * 4));
+                __builtin_amdgcn_raw_buffer_store_b128(v, rg, static_cast<int>(st_lane), 0, 0);
+                wave_lds_fence();  // the ring is rewritten for the next k1
+            }
+        }
+        if constexpr (AMAX) {  // at the end, where few registers are live; every lane stores the same word
+            uint32_t mx = amax_lane;
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) mx = max(mx, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mx), o)));
+            amax_out[task] = static_cast<uint16_t>(mx);
+        }
     }
 }
 
@@ -416,11 +417,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 hipError_t launch_col_fwd_mfma(int src_dtype, const void* src, int64_t src_row_stride, int D,
                                void* grid, int64_t grid_pb_stride, const LaunchTables& t,
                                GridScale sc, const void* mtab, int n_cols, int npb,
-                               hipStream_t stream, uint32_t* amax_out, const int* run_flag) {
+                               hipStream_t stream, uint16_t* amax_out, const int* run_flag) {
     if (n_cols == 0) return hipSuccess;
     if (amax_out != nullptr && src_dtype != 1) return hipErrorInvalidValue;
     const int ntasks = n_cols * npb;
-    const dim3 g((ntasks + 3) / 4), b(256);
+    // a conditional launch (run_flag) mostly does nothing: 1024 workgroups (four per CU)
+    // that loop over the tasks start and leave faster than one workgroup per four tasks
+    const int wgs = (ntasks + 3) / 4;
+    const dim3 g(run_flag != nullptr ? std::min(wgs, 1024) : wgs), b(256);
     const u4* mt = static_cast<const u4*>(mtab);
     uint32_t* gp = static_cast<uint32_t*>(grid);
     if (src_dtype == 1 && amax_out != nullptr)

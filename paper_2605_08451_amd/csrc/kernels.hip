@@ -1168,11 +1168,31 @@ __global__ __launch_bounds__(256) void amax_finish_kernel(const uint32_t* __rest
     }
 }
 
-__global__ __launch_bounds__(1024) void amax_check_kernel(const uint32_t* __restrict__ parts, int n,
+__global__ __launch_bounds__(1024) void amax_check_kernel(const uint16_t* __restrict__ parts, int n,
                                                            float2* __restrict__ used, int* __restrict__ redo) {
     __shared__ uint32_t red[16];
     uint32_t m = 0;
-    for (int i = threadIdx.x; i < n; i += 1024) m = max(m, parts[i]);
+    // eight magnitudes per 16-byte load (parts is 256-byte aligned), four loads in flight
+    for (int base = threadIdx.x * 8; base < n; base += 4 * 1024 * 8) {
+        uint4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = base + u * 1024 * 8;
+            if (i + 8 <= n) {
+                v[u] = *reinterpret_cast<const uint4*>(parts + i);
+            } else {
+                uint32_t w[4] = {0u, 0u, 0u, 0u};
+                for (int k = i; k < n && k < i + 8; ++k) w[(k - i) >> 1] |= static_cast<uint32_t>(parts[k]) << (16 * ((k - i) & 1));
+                v[u] = make_uint4(w[0], w[1], w[2], w[3]);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const uint32_t q[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+            for (int c = 0; c < 4; ++c) m = max(m, max(q[c] & 0xffffu, q[c] >> 16));
+        }
+    }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), o)));
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
@@ -1186,7 +1206,7 @@ __global__ __launch_bounds__(1024) void amax_check_kernel(const uint32_t* __rest
     }
 }
 
-hipError_t launch_amax_check(const uint32_t* parts, int n, float2* used, int* redo, hipStream_t stream) {
+hipError_t launch_amax_check(const uint16_t* parts, int n, float2* used, int* redo, hipStream_t stream) {
     hipLaunchKernelGGL(amax_check_kernel, dim3(1), dim3(1024), 0, stream, parts, n, used, redo);
     return hipGetLastError();
 }

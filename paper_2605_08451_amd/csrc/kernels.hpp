@@ -121,7 +121,7 @@ constexpr int kMtEntries = 4608;
 hipError_t launch_col_fwd_mfma(int src_dtype, const void* src, int64_t src_row_stride, int D,
                                void* grid, int64_t grid_pb_stride, const LaunchTables& t,
                                GridScale sc, const void* mtab, int n_cols, int npb,
-                               hipStream_t stream, uint32_t* amax_out = nullptr,
+                               hipStream_t stream, uint16_t* amax_out = nullptr,
                                const int* run_flag = nullptr);
 
 hipError_t launch_col_inv_mfma(int y_dtype, const void* grid, int64_t grid_pb_stride, void* dst,
@@ -170,10 +170,10 @@ hipError_t launch_filter_scale(const float* partials, int ntiles, int D, int npa
 constexpr int kDataAmaxExp = 3;
 constexpr int kAmaxParts = 2048;
 
-// The unit-scale check of a column pass that recorded amax per task: from the n magnitude
-// words in parts (bf16 bits), the scale s = 2^(kDataAmaxExp - e) of the largest |x|; writes
+// The unit-scale check of a column pass that recorded amax per task: from the n magnitudes
+// in parts (bf16 bits without the sign), the scale s = 2^(kDataAmaxExp - e) of the largest |x|; writes
 // used = {s, 1/s} and *redo = (s != 1), i.e. whether the pass must run again with s.
-hipError_t launch_amax_check(const uint32_t* parts, int n, float2* used, int* redo, hipStream_t stream);
+hipError_t launch_amax_check(const uint16_t* parts, int n, float2* used, int* redo, hipStream_t stream);
 hipError_t launch_prescale(int dtype, const void* in, int64_t n, float extra, const float2* prev,
                            float2* out, uint32_t* work, hipStream_t stream);
 

@@ -320,7 +320,7 @@ std::string stage(const char* tag, const char* name) { return std::string(tag) +
 // exact power-of-two scale to spec->used and, when it differs from the one used, sets
 // spec->redo, on which a second launch of the column pass redoes it at the exact scale.
 struct SpecScale {
-    uint32_t* parts;
+    uint16_t* parts;
     float2* used;
     int* redo;
 };
@@ -633,7 +633,7 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
     // unit-variance activations, up to 8, keeps scale 1), which saves a read of x.
     const float2* xs = plan->ones;
     float2* w = prescale_words(workspace, plan->ws_hdr_off);
-    SpecScale spec{prescale_work(workspace, plan->ws_hdr_off), w,
+    SpecScale spec{reinterpret_cast<uint16_t*>(prescale_work(workspace, plan->ws_hdr_off)), w,
                    reinterpret_cast<int*>(reinterpret_cast<char*>(w) + kRedoFlagOffset)};
     const bool speculative = h.grid_half && plan->prescale_fwd && h.col_mfma && h.x_dtype == RUBICONV_BF16;
     if (e == hipSuccess && h.grid_half && plan->prescale_fwd && !speculative) {
