@@ -225,6 +225,35 @@ def test_long_row_sizes_precision(device, n1, monkeypatch):
         assert d <= 5e-3, (n1, L, d)
 
 
+@pytest.mark.parametrize("family", ["lds", "batch", "partner"])
+def test_row_kernel_sizes_precision(device, family, monkeypatch):
+    """The same tight bar (5e-3 per document) for the other matrix-core row kernels on the
+    matrix-core column path (D = 32): rows of 2..32 points (row_lds_kernel), rows of at
+    most 8 points batched 16 / m documents to a block (row_batch_kernel) and rows of
+    33..128 points (row_partner_kernel), every size as its own class."""
+    monkeypatch.setenv("RUBICONV_CLASS_MERGE", "0")
+    n1 = 256
+    if family == "lds":
+        ks = (2, 3, 4, 5, 6, 8, 9, 10, 12, 15, 16, 18, 20, 24, 25, 27, 30, 32)
+        monkeypatch.setenv("RUBICONV_ROW_BATCH", "0")
+    elif family == "batch":
+        ks = (1, 2, 3, 4, 5, 6, 8, 1, 2, 4, 8)
+        monkeypatch.setenv("RUBICONV_ROW_BATCH", "8")
+    else:
+        ks = (36, 40, 45, 48, 50, 54, 60, 64, 72, 75, 80, 81, 90, 96, 100, 108, 120, 128)
+    # a 7-tap filter: P >= len + 6, so a document of n1 (k - 1) + 3 tokens takes m = k
+    lens = [n1 * (k - 1) + 3 if k > 1 else 100 + 7 * i for i, k in enumerate(ks)]
+    N = max(lens) + 1
+    rows = [[ln, N - ln] for ln in lens]
+    W = wl.make_case(rows, D=32, L=7, x_dtype="bf16", seed=len(ks))
+    y, plan = run_gpu(W, device, n1=n1)
+    ms = sorted(set(int(m) for m in plan.doc_table()[:, 4]))
+    assert all(k in ms for k in ks), (ks, ms)
+    g, d = assert_parity(y, reference(W, "fft"), W.cu_seqlens, "bf16", family)
+    print(f"[row kernels] {family}: global {g:.2e}, worst document {d:.2e}", file=sys.stderr, flush=True)
+    assert d <= 5e-3, (family, d)
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_direct_path_limits(device, monkeypatch, dtype):
     """Short documents by their defining sums (the direct path) at several length limits,
