@@ -112,8 +112,31 @@ constexpr int kTab2 = 16 * 2 * 64;  // stage-2 operands: 16 matrices x (re, im) 
 constexpr int kF16In = 0;   // fp16 channel pairs (filter taps, packed by the pair transpose)
 constexpr int kBf16In = 1;  // bf16 channel pairs (x): used as bf16 operands as loaded
 
+// The largest of n bf16 magnitudes (16-bit words, 16-byte aligned), reduced by one wave on
+// its own: every wave of the launch reads the same words and gets the same value.
+__device__ __forceinline__ uint32_t wave_amax16(const uint16_t* __restrict__ a, int n, int lane) {
+    const u4* v = reinterpret_cast<const u4*>(a);
+    const int nv = n / 8;  // whole 16-byte groups
+    uint32_t m = 0;
+    for (int base = lane; base < nv; base += 8 * 64) {
+        u4 w[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) w[u] = base + 64 * u < nv ? v[base + 64 * u] : u4{0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) m = max(m, max(w[u][c] & 0xffffu, w[u][c] >> 16));
+    }
+    for (int i = nv * 8 + lane; i < n; i += 64) m = max(m, static_cast<uint32_t>(a[i]));
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), o)));
+    return m;
+}
+
 // AMAX: each column task also writes the largest |x| it loaded (bf16 magnitude bits) to
-// amax_out[task].  run_flag: when not null, the launch does nothing unless *run_flag != 0.
+// amax_out[task].  amax_in (the redo launch): the launch first takes the range scale s from
+// the n_amax magnitudes a pass with AMAX recorded, writes {s, 1/s} to *used (workgroup 0),
+// and does nothing more unless s != 1; otherwise it runs the pass at scale s.
 template <int IN, bool AMAX>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void col_fwd_mfma_kernel(const void* __restrict__ src,
                                                            int64_t src_row_stride, int D,
@@ -122,13 +145,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                                                            GridScale sc,
                                                            const u4* __restrict__ mt, int npb,
                                                            int ntasks, uint16_t* __restrict__ amax_out,
-                                                           const int* __restrict__ run_flag) {
+                                                           const uint16_t* __restrict__ amax_in, int n_amax,
+                                                           float2* __restrict__ used) {
     // stage-2 operands, shared by the workgroup's four column tasks
     __shared__ u4 tab2[kTab2];
     // per wave: one output row group (16 grid rows x 16 pairs) on its way to 16-byte stores
     __shared__ uint32_t ring_all[4][256];
-    if (run_flag != nullptr && *run_flag == 0) return;  // the whole workgroup, before any barrier
     const int lane = threadIdx.x & 63;
+    float glob_x = 1.0f;
+    if (amax_in != nullptr) {
+        glob_x = pow2_scale(__uint_as_float(wave_amax16(amax_in, n_amax, lane) << 16), kDataAmaxExp);
+        if (blockIdx.x == 0 && threadIdx.x == 0) used[0] = make_float2(glob_x, 1.0f / glob_x);
+        if (glob_x == 1.0f) return;  // every wave of every workgroup alike, before any barrier
+    } else {
+        glob_x = sc.glob->x;
+    }
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
     copy_to_lds(mt + kMtFwd2, tab2, kTab2 / 64, wave, lane);
     __builtin_amdgcn_s_waitcnt(0);
@@ -189,7 +220,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             for (int o = 0; o < 2; ++o) a[o] = mt[kMtFwd1F16 + o * 64 + lane];
         }
         // range scale of this lane's pair, applied to the fp32 products before fp16 rounding
-        const float in_mul = sc.pair[pb * kPairsPerBlock + p].x * sc.glob->x;
+        const float in_mul = sc.pair[pb * kPairsPerBlock + p].x * glob_x;
         __builtin_amdgcn_sched_barrier(0);
 
         uint32_t y[16][4];
@@ -417,25 +448,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 hipError_t launch_col_fwd_mfma(int src_dtype, const void* src, int64_t src_row_stride, int D,
                                void* grid, int64_t grid_pb_stride, const LaunchTables& t,
                                GridScale sc, const void* mtab, int n_cols, int npb,
-                               hipStream_t stream, uint16_t* amax_out, const int* run_flag) {
+                               hipStream_t stream, uint16_t* amax_out, const uint16_t* amax_in,
+                               float2* used) {
     if (n_cols == 0) return hipSuccess;
-    if (amax_out != nullptr && src_dtype != 1) return hipErrorInvalidValue;
+    if ((amax_out != nullptr || amax_in != nullptr) && src_dtype != 1) return hipErrorInvalidValue;
+    if (amax_in != nullptr && (used == nullptr || (reinterpret_cast<uintptr_t>(amax_in) & 15) != 0))
+        return hipErrorInvalidValue;
     const int ntasks = n_cols * npb;
-    // a conditional launch (run_flag) mostly does nothing: 1024 workgroups (four per CU)
-    // that loop over the tasks start and leave faster than one workgroup per four tasks
+    // the redo launch mostly does nothing: 1024 workgroups (four per CU) that loop over the
+    // tasks start and leave faster than one workgroup per four tasks
     const int wgs = (ntasks + 3) / 4;
-    const dim3 g(run_flag != nullptr ? std::min(wgs, 1024) : wgs), b(256);
+    const dim3 g(amax_in != nullptr ? std::min(wgs, 1024) : wgs), b(256);
     const u4* mt = static_cast<const u4*>(mtab);
     uint32_t* gp = static_cast<uint32_t*>(grid);
     if (src_dtype == 1 && amax_out != nullptr)
         hipLaunchKernelGGL((col_fwd_mfma_kernel<kBf16In, true>), g, b, 0, stream, src, src_row_stride, D, gp,
-                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, run_flag);
+                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, amax_in, ntasks, used);
     else if (src_dtype == 1)
         hipLaunchKernelGGL((col_fwd_mfma_kernel<kBf16In, false>), g, b, 0, stream, src, src_row_stride, D, gp,
-                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, run_flag);
+                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, amax_in, ntasks, used);
     else
         hipLaunchKernelGGL((col_fwd_mfma_kernel<kF16In, false>), g, b, 0, stream, src, src_row_stride, D, gp,
-                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, run_flag);
+                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, amax_in, ntasks, used);
     return hipGetLastError();
 }
 

@@ -1043,14 +1043,7 @@ hipError_t launch_transpose(const float* in, int rows, int cols, int in_ld, floa
     return hipGetLastError();
 }
 
-// ---------------------------------------------------------------- range scales
-// 2^(target - e) for a finite positive value a < 2^e (frexp), else 1.
-__device__ __forceinline__ float pow2_scale(float a, int target) {
-    if (!(a > 0.0f) || !(a <= 3.0e38f)) return 1.0f;
-    int e;
-    (void)frexpf(a, &e);  // a = f 2^e, 0.5 <= f < 1
-    return ldexpf(1.0f, max(-126, min(127, target - e)));
-}
+// ---------------------------------------------------------------- range scales (pow2_scale: kernels.hpp)
 
 // One workgroup per 2 channel pairs (4 channels): thread t sums the tiles t / 4,
 // t / 4 + 64, ... of channel t % 4 (four independent sums in flight), then the 64 partial
@@ -1166,49 +1159,6 @@ __global__ __launch_bounds__(256) void amax_finish_kernel(const uint32_t* __rest
         const float s = pow2_scale(a, kDataAmaxExp) * extra;
         out[0] = make_float2(s, (prev != nullptr ? prev->y : 1.0f) / s);
     }
-}
-
-__global__ __launch_bounds__(1024) void amax_check_kernel(const uint16_t* __restrict__ parts, int n,
-                                                           float2* __restrict__ used, int* __restrict__ redo) {
-    __shared__ uint32_t red[16];
-    uint32_t m = 0;
-    // eight magnitudes per 16-byte load (parts is 256-byte aligned), four loads in flight
-    for (int base = threadIdx.x * 8; base < n; base += 4 * 1024 * 8) {
-        uint4 v[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int i = base + u * 1024 * 8;
-            if (i + 8 <= n) {
-                v[u] = *reinterpret_cast<const uint4*>(parts + i);
-            } else {
-                uint32_t w[4] = {0u, 0u, 0u, 0u};
-                for (int k = i; k < n && k < i + 8; ++k) w[(k - i) >> 1] |= static_cast<uint32_t>(parts[k]) << (16 * ((k - i) & 1));
-                v[u] = make_uint4(w[0], w[1], w[2], w[3]);
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const uint32_t q[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-#pragma unroll
-            for (int c = 0; c < 4; ++c) m = max(m, max(q[c] & 0xffffu, q[c] >> 16));
-        }
-    }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), o)));
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint32_t r = 0;
-        for (int w = 0; w < 16; ++w) r = max(r, red[w]);
-        const float s = pow2_scale(__uint_as_float(r << 16), kDataAmaxExp);
-        used[0] = make_float2(s, 1.0f / s);
-        redo[0] = s != 1.0f ? 1 : 0;
-    }
-}
-
-hipError_t launch_amax_check(const uint16_t* parts, int n, float2* used, int* redo, hipStream_t stream) {
-    hipLaunchKernelGGL(amax_check_kernel, dim3(1), dim3(1024), 0, stream, parts, n, used, redo);
-    return hipGetLastError();
 }
 
 hipError_t launch_filter_scale(const float* partials, int ntiles, int D, int npairs,

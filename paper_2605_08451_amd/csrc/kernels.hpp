@@ -116,13 +116,15 @@ constexpr int kMtEntries = 4608;
 // src_dtype 1: bf16 channels [rows][N][D] (x); 0: fp16 channel pairs [taps][D / 2] from
 // launch_transpose_pairs (filter taps).
 // amax_out (bf16 sources only; null for none): per column task, the largest bf16 magnitude
-// bits of the x it loaded.  run_flag (null for none): the launch does nothing unless
-// *run_flag != 0 (device memory written by an earlier kernel on the stream).
+// bits of the x it loaded.  amax_in (null for none; 16-byte aligned, from a launch with
+// amax_out over the same tasks): this launch redoes the pass at x's power-of-two range scale
+// s = 2^(3 - e) (2^e at or above max |x|) in place of sc.glob, writes {s, 1/s} to *used, and
+// does nothing else when s = 1 (the scale the first launch used).
 hipError_t launch_col_fwd_mfma(int src_dtype, const void* src, int64_t src_row_stride, int D,
                                void* grid, int64_t grid_pb_stride, const LaunchTables& t,
                                GridScale sc, const void* mtab, int n_cols, int npb,
                                hipStream_t stream, uint16_t* amax_out = nullptr,
-                               const int* run_flag = nullptr);
+                               const uint16_t* amax_in = nullptr, float2* used = nullptr);
 
 hipError_t launch_col_inv_mfma(int y_dtype, const void* grid, int64_t grid_pb_stride, void* dst,
                                int64_t dst_row_stride, int D, const LaunchTables& t,
@@ -170,10 +172,16 @@ hipError_t launch_filter_scale(const float* partials, int ntiles, int D, int npa
 constexpr int kDataAmaxExp = 3;
 constexpr int kAmaxParts = 2048;
 
-// The unit-scale check of a column pass that recorded amax per task: from the n magnitudes
-// in parts (bf16 bits without the sign), the scale s = 2^(kDataAmaxExp - e) of the largest |x|; writes
-// used = {s, 1/s} and *redo = (s != 1), i.e. whether the pass must run again with s.
-hipError_t launch_amax_check(const uint16_t* parts, int n, float2* used, int* redo, hipStream_t stream);
+// 2^(target - e) for a = f 2^e (0.5 <= f < 1): the power of two that brings a into
+// [2^(target-1), 2^target); 1 for a zero, negative, infinite or NaN a.
+__device__ __forceinline__ float pow2_scale(float a, int target) {
+    if (!(a > 0.0f) || !(a <= 3.0e38f)) return 1.0f;
+    int e;
+    (void)frexpf(a, &e);
+    return ldexpf(1.0f, max(-126, min(127, target - e)));
+}
+
+
 hipError_t launch_prescale(int dtype, const void* in, int64_t n, float extra, const float2* prev,
                            float2* out, uint32_t* work, hipStream_t stream);
 

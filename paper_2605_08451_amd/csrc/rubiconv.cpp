@@ -80,8 +80,6 @@ struct rubiconv_plan_s {
 namespace {
 
 constexpr size_t kAlign = 256;
-// byte offset of the forward's redo flag in the workspace header (after the scale words)
-constexpr size_t kRedoFlagOffset = 128;
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) % kAlign) == 0; }
 
@@ -315,14 +313,13 @@ std::string stage(const char* tag, const char* name) { return std::string(tag) +
 // (dtype out_dtype).  own_rows: every document's second grid rows are its own (the
 // filter gradient), so the matrix-core row pass takes one document per task instead
 // of groups of a size class.  The caller holds the plan's launch mutex.
-// spec (matrix-core column pass, bf16 input only): the column pass runs at in_sc's scale
-// while recording |in|'s largest value per task into spec->parts; a check then writes the
-// exact power-of-two scale to spec->used and, when it differs from the one used, sets
-// spec->redo, on which a second launch of the column pass redoes it at the exact scale.
+// spec (matrix-core column pass, bf16 input only): the column pass runs at scale 1 while
+// recording |in|'s largest value per task into spec->parts; a second launch takes the exact
+// power-of-two scale from them, writes it to spec->used and redoes the pass at that scale
+// only when it is not 1.
 struct SpecScale {
     uint16_t* parts;
     float2* used;
-    int* redo;
 };
 
 hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, const void* fgrid,
@@ -342,13 +339,9 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
                         : rubiconv::launch_col_fwd(h.r, half, in_dtype, in, rs, h.D, grid,
                                                    plan->grid_pb_stride, plan->doc_t, in_sc, n_cols,
                                                    h.npb, stream);
-    if (spec != nullptr && n_cols > 0) {
-        if (e == hipSuccess) e = rubiconv::launch_amax_check(spec->parts, n_cols * h.npb, spec->used, spec->redo, stream);
-        if (e == hipSuccess)
-            e = rubiconv::launch_col_fwd_mfma(in_dtype, in, rs, h.D, grid, plan->grid_pb_stride, plan->doc_t,
-                                              {in_sc.pair, spec->used}, plan->mfma_tab, n_cols, h.npb, stream,
-                                              nullptr, spec->redo);
-    }
+    if (spec != nullptr && n_cols > 0 && e == hipSuccess)
+        e = rubiconv::launch_col_fwd_mfma(in_dtype, in, rs, h.D, grid, plan->grid_pb_stride, plan->doc_t, in_sc,
+                                          plan->mfma_tab, n_cols, h.npb, stream, nullptr, spec->parts, spec->used);
     rec.mark(stage(tag, "col_fwd"));
     // long rows: first level into the sub-row regions (both grids of the filter gradient)
     for (const rubiconv::LrItem& it : h.lr_doc_items)
@@ -506,7 +499,7 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
     const size_t conv_ws = align_up(static_cast<size_t>(h.npb) * pl->grid_pb_stride * esz);
     const size_t filt_ws =
         pl->taps_bytes + align_up(static_cast<size_t>(rubiconv::tap_tile_rows(std::max(h.taps_max, 1))) * h.D * 4);
-    // header: the scale words (and the redo flag) in the first kAlign bytes, then the amax
+    // header: the scale words in the first kAlign bytes, then the amax
     // partials: kAmaxParts of the prescale pass, or one per task of the forward column pass
     const size_t n_tasks = h.doc_col_seg.size() * static_cast<size_t>(h.npb);
     const size_t hdr_bytes = kAlign + align_up(std::max<size_t>(rubiconv::kAmaxParts, n_tasks) * 4);
@@ -633,8 +626,7 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
     // unit-variance activations, up to 8, keeps scale 1), which saves a read of x.
     const float2* xs = plan->ones;
     float2* w = prescale_words(workspace, plan->ws_hdr_off);
-    SpecScale spec{reinterpret_cast<uint16_t*>(prescale_work(workspace, plan->ws_hdr_off)), w,
-                   reinterpret_cast<int*>(reinterpret_cast<char*>(w) + kRedoFlagOffset)};
+    SpecScale spec{reinterpret_cast<uint16_t*>(prescale_work(workspace, plan->ws_hdr_off)), w};
     const bool speculative = h.grid_half && plan->prescale_fwd && h.col_mfma && h.x_dtype == RUBICONV_BF16;
     if (e == hipSuccess && h.grid_half && plan->prescale_fwd && !speculative) {
         e = prescale(plan, h.x_dtype, x, 1.0f, nullptr, w, prescale_work(workspace, plan->ws_hdr_off), stream);
