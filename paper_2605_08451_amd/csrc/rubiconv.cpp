@@ -44,6 +44,13 @@ struct rubiconv_plan_s {
     const float2* ones = nullptr;           // {1, 1} per channel pair: the unit range scales
     bool device_ready = false;
     bool prescale_fwd = true;    // the forward prescales x as the gradients do dy (and x)
+    // pinned host words, written by the matrix-core column pass of each call: the range
+    // scale of x (forward) and of dy (dx) the last call found.  A call starts its column
+    // pass at that scale and redoes the pass only when its own scale differs; any value
+    // is correct, a stale one costs the redo.
+    static constexpr int kHintFwd = 0, kHintDx = 1;
+    float* scale_hint = nullptr;      // host address
+    float* scale_hint_dev = nullptr;  // the same words as kernels address them
     LaunchTables doc_t{};
     LaunchTables cls_t{};
     LaunchTables grad_t{};       // doc_t with each document's "filter" rows at its own grid rows
@@ -204,6 +211,12 @@ rubiconv_status_t upload(rubiconv_plan_s* pl, hipStream_t stream) {
             hipEventCreateWithFlags(&pl->join[k], hipEventDisableTiming) != hipSuccess)
             return RUBICONV_ERR_HIP;
     }
+    if (hipHostMalloc(reinterpret_cast<void**>(&pl->scale_hint), 2 * sizeof(float),
+                      hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess)
+        return RUBICONV_ERR_ALLOC;
+    pl->scale_hint[0] = pl->scale_hint[1] = 1.0f;
+    if (hipHostGetDevicePointer(reinterpret_cast<void**>(&pl->scale_hint_dev), pl->scale_hint, 0) != hipSuccess)
+        return RUBICONV_ERR_HIP;
     pl->device_ready = true;
     return RUBICONV_OK;
 }
@@ -320,7 +333,16 @@ std::string stage(const char* tag, const char* name) { return std::string(tag) +
 struct SpecScale {
     uint16_t* parts;
     float2* used;
+    float guess;   // the first pass's scale (a power of two)
+    float* hint;   // host-mapped word that receives the exact scale
 };
+
+// The scale a call's first column pass starts at: the last one its plan found (a power of
+// two in the range pow2_scale gives, else 1).
+float scale_guess(const rubiconv_plan_s* plan, int which) {
+    const float g = reinterpret_cast<const volatile float*>(plan->scale_hint)[which];
+    return g >= 0x1p-126f && g <= 0x1p127f ? g : 1.0f;
+}
 
 hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, const void* fgrid,
                         int64_t fgrid_pb_stride, const LaunchTables& t, void* out, int out_dtype,
@@ -335,13 +357,15 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
     if (spec != nullptr && !mfma) return hipErrorInvalidValue;
     hipError_t e = mfma ? rubiconv::launch_col_fwd_mfma(in_dtype, in, rs, h.D, grid, plan->grid_pb_stride,
                                                         plan->doc_t, in_sc, plan->mfma_tab, n_cols, h.npb,
-                                                        stream, spec ? spec->parts : nullptr)
+                                                        stream, spec ? spec->parts : nullptr, nullptr, nullptr,
+                                                        spec ? spec->guess : 1.0f)
                         : rubiconv::launch_col_fwd(h.r, half, in_dtype, in, rs, h.D, grid,
                                                    plan->grid_pb_stride, plan->doc_t, in_sc, n_cols,
                                                    h.npb, stream);
     if (spec != nullptr && n_cols > 0 && e == hipSuccess)
         e = rubiconv::launch_col_fwd_mfma(in_dtype, in, rs, h.D, grid, plan->grid_pb_stride, plan->doc_t, in_sc,
-                                          plan->mfma_tab, n_cols, h.npb, stream, nullptr, spec->parts, spec->used);
+                                          plan->mfma_tab, n_cols, h.npb, stream, nullptr, spec->parts, spec->used,
+                                          spec->guess, spec->hint);
     rec.mark(stage(tag, "col_fwd"));
     // long rows: first level into the sub-row regions (both grids of the filter gradient)
     for (const rubiconv::LrItem& it : h.lr_doc_items)
@@ -542,6 +566,7 @@ void rubiconv_plan_destroy(rubiconv_plan_t plan) {
     }
     destroy_events(plan);
     destroy_side_streams(plan);
+    if (plan->scale_hint) (void)hipHostFree(plan->scale_hint);
     if (plan->dev) (void)hipFree(plan->dev);
     delete plan;
 }
@@ -621,12 +646,13 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
                                            h.N, h.D, h.L, h.y_dtype, y, s);
         });
     // range scales: the filter's per pair, and x's power-of-two prescale when asked for.
-    // On the matrix-core path the column pass first runs at scale 1 and records |x|'s
-    // largest value; it runs again only when that value asks for another scale (|x| of
-    // unit-variance activations, up to 8, keeps scale 1), which saves a read of x.
+    // On the matrix-core path the column pass first runs at the scale the plan's last
+    // call found and records |x|'s largest value; it runs again only when that value asks
+    // for another scale, which saves a read of x whenever x's range holds from call to call.
     const float2* xs = plan->ones;
     float2* w = prescale_words(workspace, plan->ws_hdr_off);
-    SpecScale spec{reinterpret_cast<uint16_t*>(prescale_work(workspace, plan->ws_hdr_off)), w};
+    SpecScale spec{reinterpret_cast<uint16_t*>(prescale_work(workspace, plan->ws_hdr_off)), w,
+                   scale_guess(plan, rubiconv_plan_s::kHintFwd), plan->scale_hint_dev + rubiconv_plan_s::kHintFwd};
     const bool speculative = h.grid_half && plan->prescale_fwd && h.col_mfma && h.x_dtype == RUBICONV_BF16;
     if (e == hipSuccess && h.grid_half && plan->prescale_fwd && !speculative) {
         e = prescale(plan, h.x_dtype, x, 1.0f, nullptr, w, prescale_work(workspace, plan->ws_hdr_off), stream);
@@ -664,18 +690,24 @@ rubiconv_status_t rubiconv_packed_conv_dx(rubiconv_plan_t plan, const void* dy, 
                                            h.N, h.D, h.L, h.x_dtype, dx, s);
         });
     // dy is prescaled by a power of two from its largest magnitude (upstream gradients are
-    // often far below 1), the filter by its per-pair scale
+    // often far below 1), the filter by its per-pair scale.  On the matrix-core path the
+    // column pass starts at the scale of the plan's last dx call and is redone only when
+    // dy's own scale differs (as in the forward).
     const float2* ds = plan->ones;
-    if (e == hipSuccess && h.grid_half) {
-        float2* w = prescale_words(workspace, plan->ws_hdr_off) + 1;
+    float2* w = prescale_words(workspace, plan->ws_hdr_off) + 1;
+    SpecScale spec{reinterpret_cast<uint16_t*>(prescale_work(workspace, plan->ws_hdr_off)), w,
+                   scale_guess(plan, rubiconv_plan_s::kHintDx), plan->scale_hint_dev + rubiconv_plan_s::kHintDx};
+    const bool speculative = h.grid_half && h.col_mfma && h.y_dtype == RUBICONV_BF16;
+    if (e == hipSuccess && h.grid_half && !speculative) {
         e = prescale(plan, h.y_dtype, dy, 1.0f, nullptr, w, prescale_work(workspace, plan->ws_hdr_off), stream);
         rec.mark("dx_prescale");
         ds = w;
     }
     if (e == hipSuccess)
         e = enqueue_conv(plan, dy, h.y_dtype, spectrum, plan->cls_pb_stride, plan->doc_t, dx,
-                         h.x_dtype, workspace, 1, false, {plan->ones, ds}, {filter_scales(plan, spectrum), ds},
-                         "dx_", stream, rec);
+                         h.x_dtype, workspace, 1, false, {plan->ones, ds},
+                         {filter_scales(plan, spectrum), speculative ? w : ds}, "dx_", stream, rec,
+                         speculative ? &spec : nullptr);
     if (e == hipSuccess && direct) e = join_direct(plan, stream, rec);
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }

@@ -126,3 +126,78 @@ def test_gradient_range(device, scale):
     gk, wk = _check_dk(dk, oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L, threads=ORACLE_THREADS),
                        "bf16", f"dk scale {scale}")
     _say(f"[range] dy scale {scale}: dx {g:.2e} / {d:.2e}, dk {gk:.2e} / {wk:.2e}")
+
+
+@pytest.mark.parametrize("loud", ["direct", "transform"])
+def test_forward_range_direct_documents(device, monkeypatch, loud):
+    """Short documents on the direct path beside transformed ones, one group 1e3 times
+    louder than the other.  The x scale of the transforms comes from the documents the
+    column pass loads, so the direct path's values do not set it; both groups must meet
+    the bar per document."""
+    monkeypatch.setenv("RUBICONV_DIRECT_MAX", "64")
+    rng = np.random.default_rng(79)
+    N = 4096
+    short = [int(v) for v in rng.integers(1, 65, 40)]
+    rows = [short + [N - sum(short)], [1500, 30, 2566], [N]]
+    W0 = wl.make_case(rows, D=D, L=N, x_dtype="bf16", seed=79)
+    x = W0.x.astype(np.float32).copy()
+    for b, r in enumerate(W0.cu_seqlens):
+        for s0, s1 in zip(r[:-1], r[1:]):
+            is_direct = 0 < s1 - s0 <= 64
+            if is_direct == (loud == "direct"):
+                x[b, s0:s1] *= 1e3
+    bits = wl.f32_to_bf16_bits(x)
+    W = wl.Workload("range-direct", W0.B, W0.N, D, W0.L, "bf16", "bf16", W0.cu_seqlens,
+                    wl.bf16_bits_to_f32(bits).reshape(x.shape), bits, W0.filters, 0)
+    y, plan, _, _ = _forward(W, device)
+    assert plan.info()["n_direct"] > 0
+    ref = oracle.conv_direct(W.x, W.filters, W.cu_seqlens, threads=ORACLE_THREADS)
+    g, d = assert_parity(y, ref, W.cu_seqlens, "bf16", f"loud {loud}")
+    _say(f"[range] loud {loud} documents: global {g:.2e}, worst document {d:.2e}")
+
+
+def test_scale_guess_sequence(device):
+    """The matrix-core column pass starts at the range scale its plan's last call found and
+    redoes the pass when the call's own scale differs.  A sequence of calls whose x scale
+    changes (1, 100, 100, 1e-3, 1) must give, for each input, the same bits whether the
+    guess was right or wrong, and the forward must meet the bar at every step; dx likewise
+    for dy scales 1e-6, 1e-6, 1."""
+    import torch
+    import paper_2605_08451_amd as rc
+    B, N = _shape()
+    rng = np.random.default_rng(80)
+    x = rng.standard_normal((B, N, D), dtype=np.float32)
+    k = wl.decaying_filters(rng, D, N)
+    W = _workload(x, k)
+    xd, kd = to_device(W, device)
+    plan = rc.Plan(W.cu_seqlens, N=W.N, D=W.D, L=W.L, x_dtype="bf16", y_dtype="bf16")
+    ws = plan.new_workspace(device)
+    spec = rc.filter_spectrum(plan, kd, workspace=ws)
+    outs = {}
+    for sc in (1.0, 100.0, 100.0, 1e-3, 1.0, 1e-3):
+        xs = (xd.float() * sc).to(torch.bfloat16)
+        y = rc.packed_conv(plan, xs, spec, workspace=ws)
+        torch.cuda.synchronize()
+        bits = y.view(torch.int16).cpu().numpy().copy()
+        if sc in outs:
+            assert np.array_equal(outs[sc], bits), f"x scale {sc}: output depends on the guess"
+        else:
+            outs[sc] = bits
+            yv = y.float().cpu().numpy().astype(np.float64)
+            ref = oracle.conv_fft(xs.float().cpu().numpy().astype(np.float64), W.filters, W.cu_seqlens,
+                                  threads=ORACLE_THREADS)
+            assert_parity(yv, ref, W.cu_seqlens, "bf16", f"x scale {sc}")
+    douts = {}
+    for sc in (1e-6, 1e-6, 1.0, 1e-6):
+        dyv = wl.round_to_bf16(sc * rng.standard_normal((B, N, D), dtype=np.float32)) if sc not in douts else douts[sc][0]
+        dy = torch.from_numpy(wl.f32_to_bf16_bits(dyv.astype(np.float32)).view(np.int16)).view(torch.bfloat16).to(device)
+        dx = rc.packed_conv_dx(plan, dy, spec, workspace=ws)
+        torch.cuda.synchronize()
+        bits = dx.view(torch.int16).cpu().numpy().copy()
+        if sc in douts:
+            assert np.array_equal(douts[sc][1], bits), f"dy scale {sc}: dx depends on the guess"
+        else:
+            douts[sc] = (dyv, bits)
+            ref = oracle.grad_x(W.filters, dyv.astype(np.float64), W.cu_seqlens, threads=ORACLE_THREADS)
+            assert_parity(dx.float().cpu().numpy().astype(np.float64), ref, W.cu_seqlens, "bf16", f"dx {sc}")
+    _say("[range] scale guesses: outputs independent of the guess")
