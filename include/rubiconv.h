@@ -47,13 +47,13 @@
  *     of the two channels' sums of |k| (a bound on every spectrum value) is 2^8;
  *   - rubiconv_packed_conv scales x by 2^(3 - e), 2^e the power of two at or above
  *     the largest |x| of the call, and the gradient calls scale dy (and x) the same
- *     way.  On the matrix-core path (N1 = 256, D a multiple of 32) the forward and dx
- *     find that scale inside their first column pass: the pass runs at the scale the
- *     plan's previous call of the same kind found (1 for the first call), and a second
- *     column pass runs only when the call's own scale differs.  The result does not
- *     depend on that guess (bit for bit); the plan keeps the two guesses in pinned host
- *     memory that its kernels write.  Elsewhere, and in dk, the tensor is read once
- *     more for its largest magnitude.
+ *     way.  On the matrix-core path (N1 = 256, D a multiple of 32) each call finds
+ *     those scales inside its column passes: a pass runs at the scale the plan's
+ *     previous call of the same kind found (1 for the first call), and a second column
+ *     pass runs only when the call's own scale differs.  The result does not depend on
+ *     that guess (bit for bit); the plan keeps its guesses in pinned host memory that
+ *     its kernels write.  Elsewhere the tensor is read once more for its largest
+ *     magnitude.
  * Within that, results meet the 2e-2 relative L2 bar for finite bf16 inputs whose
  * outputs are finite in bf16, except for a document whose values lie far below the
  * call's largest |x| (the x scale is one per call): below about 1e-6 of it its grid

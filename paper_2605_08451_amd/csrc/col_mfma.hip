@@ -136,9 +136,9 @@ __device__ __forceinline__ uint32_t wave_amax16(const uint16_t* __restrict__ a, 
 // AMAX: each column task also writes the largest |x| it loaded (bf16 magnitude bits) to
 // amax_out[task], and the pass runs at scale first_scale in place of sc.glob.  amax_in
 // (the redo launch): the launch first takes the range scale s from the n_amax magnitudes
-// a pass with AMAX recorded, writes {s, 1/s} to *used and s to *hint (workgroup 0), and
-// does nothing more when s equals first_scale (the scale that pass used); otherwise it
-// runs the pass at scale s.
+// a pass with AMAX recorded, times extra (a power of two), writes {s, p / s} to *used
+// (p = prev->y, or 1 without prev) and s to *hint (workgroup 0), and does nothing more when
+// s equals first_scale (the scale that pass used); otherwise it runs the pass at scale s.
 template <int IN, bool AMAX>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void col_fwd_mfma_kernel(const void* __restrict__ src,
                                                            int64_t src_row_stride, int D,
@@ -149,7 +149,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
                                                            int ntasks, uint16_t* __restrict__ amax_out,
                                                            const uint16_t* __restrict__ amax_in, int n_amax,
                                                            float2* __restrict__ used, float first_scale,
-                                                           float* __restrict__ hint) {
+                                                           float* __restrict__ hint, float extra,
+                                                           const float2* __restrict__ prev) {
     // stage-2 operands, shared by the workgroup's four column tasks
     __shared__ u4 tab2[kTab2];
     // per wave: one output row group (16 grid rows x 16 pairs) on its way to 16-byte stores
@@ -157,9 +158,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     const int lane = threadIdx.x & 63;
     float glob_x = 1.0f;
     if (amax_in != nullptr) {
-        glob_x = pow2_scale(__uint_as_float(wave_amax16(amax_in, n_amax, lane) << 16), kDataAmaxExp);
+        glob_x = pow2_scale(__uint_as_float(wave_amax16(amax_in, n_amax, lane) << 16), kDataAmaxExp) * extra;
         if (blockIdx.x == 0 && threadIdx.x == 0) {
-            used[0] = make_float2(glob_x, 1.0f / glob_x);
+            used[0] = make_float2(glob_x, (prev != nullptr ? prev->y : 1.0f) / glob_x);
             if (hint != nullptr) *reinterpret_cast<volatile float*>(hint) = glob_x;
         }
         if (glob_x == first_scale) return;  // every wave of every workgroup alike, before any barrier
@@ -455,7 +456,8 @@ hipError_t launch_col_fwd_mfma(int src_dtype, const void* src, int64_t src_row_s
                                void* grid, int64_t grid_pb_stride, const LaunchTables& t,
                                GridScale sc, const void* mtab, int n_cols, int npb,
                                hipStream_t stream, uint16_t* amax_out, const uint16_t* amax_in,
-                               float2* used, float first_scale, float* hint) {
+                               float2* used, float first_scale, float* hint, float extra,
+                               const float2* prev) {
     if (n_cols == 0) return hipSuccess;
     if ((amax_out != nullptr || amax_in != nullptr) && src_dtype != 1) return hipErrorInvalidValue;
     if (amax_in != nullptr && (used == nullptr || (reinterpret_cast<uintptr_t>(amax_in) & 15) != 0))
@@ -469,13 +471,16 @@ hipError_t launch_col_fwd_mfma(int src_dtype, const void* src, int64_t src_row_s
     uint32_t* gp = static_cast<uint32_t*>(grid);
     if (src_dtype == 1 && amax_out != nullptr)
         hipLaunchKernelGGL((col_fwd_mfma_kernel<kBf16In, true>), g, b, 0, stream, src, src_row_stride, D, gp,
-                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, amax_in, ntasks, used, first_scale, hint);
+                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, amax_in, ntasks, used, first_scale, hint,
+                           extra, prev);
     else if (src_dtype == 1)
         hipLaunchKernelGGL((col_fwd_mfma_kernel<kBf16In, false>), g, b, 0, stream, src, src_row_stride, D, gp,
-                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, amax_in, ntasks, used, first_scale, hint);
+                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, amax_in, ntasks, used, first_scale, hint,
+                           extra, prev);
     else
         hipLaunchKernelGGL((col_fwd_mfma_kernel<kF16In, false>), g, b, 0, stream, src, src_row_stride, D, gp,
-                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, amax_in, ntasks, used, first_scale, hint);
+                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, amax_in, ntasks, used, first_scale, hint,
+                           extra, prev);
     return hipGetLastError();
 }
 

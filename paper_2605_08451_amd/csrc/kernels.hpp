@@ -118,15 +118,17 @@ constexpr int kMtEntries = 4608;
 // amax_out (bf16 sources only; null for none): per column task, the largest bf16 magnitude
 // bits of the x it loaded, the pass running at scale first_scale in place of sc.glob.
 // amax_in (null for none; 16-byte aligned, from a launch with amax_out over the same tasks):
-// this launch takes x's power-of-two range scale s = 2^(3 - e) (2^e at or above max |x|),
-// writes {s, 1/s} to *used and s to *hint (host-mapped, may be null), and redoes the pass at
-// s in place of sc.glob unless s equals first_scale (the scale the first launch used).
+// this launch takes x's power-of-two range scale s = 2^(3 - e) extra (2^e at or above
+// max |x|, extra a power of two), writes {s, p / s} to *used (p = prev->y, or 1 for a null
+// prev) and s to *hint (host-mapped, may be null), and redoes the pass at s in place of
+// sc.glob unless s equals first_scale (the scale the first launch used).
 hipError_t launch_col_fwd_mfma(int src_dtype, const void* src, int64_t src_row_stride, int D,
                                void* grid, int64_t grid_pb_stride, const LaunchTables& t,
                                GridScale sc, const void* mtab, int n_cols, int npb,
                                hipStream_t stream, uint16_t* amax_out = nullptr,
                                const uint16_t* amax_in = nullptr, float2* used = nullptr,
-                               float first_scale = 1.0f, float* hint = nullptr);
+                               float first_scale = 1.0f, float* hint = nullptr, float extra = 1.0f,
+                               const float2* prev = nullptr);
 
 hipError_t launch_col_inv_mfma(int y_dtype, const void* grid, int64_t grid_pb_stride, void* dst,
                                int64_t dst_row_stride, int D, const LaunchTables& t,

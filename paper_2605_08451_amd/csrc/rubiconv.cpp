@@ -48,7 +48,7 @@ struct rubiconv_plan_s {
     // scale of x (forward) and of dy (dx) the last call found.  A call starts its column
     // pass at that scale and redoes the pass only when its own scale differs; any value
     // is correct, a stale one costs the redo.
-    static constexpr int kHintFwd = 0, kHintDx = 1;
+    static constexpr int kHintFwd = 0, kHintDx = 1, kHintDkX = 2, kHintDkDy = 3, kHints = 4;
     float* scale_hint = nullptr;      // host address
     float* scale_hint_dev = nullptr;  // the same words as kernels address them
     LaunchTables doc_t{};
@@ -211,10 +211,10 @@ rubiconv_status_t upload(rubiconv_plan_s* pl, hipStream_t stream) {
             hipEventCreateWithFlags(&pl->join[k], hipEventDisableTiming) != hipSuccess)
             return RUBICONV_ERR_HIP;
     }
-    if (hipHostMalloc(reinterpret_cast<void**>(&pl->scale_hint), 2 * sizeof(float),
+    if (hipHostMalloc(reinterpret_cast<void**>(&pl->scale_hint), rubiconv_plan_s::kHints * sizeof(float),
                       hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess)
         return RUBICONV_ERR_ALLOC;
-    pl->scale_hint[0] = pl->scale_hint[1] = 1.0f;
+    for (int i = 0; i < rubiconv_plan_s::kHints; ++i) pl->scale_hint[i] = 1.0f;
     if (hipHostGetDevicePointer(reinterpret_cast<void**>(&pl->scale_hint_dev), pl->scale_hint, 0) != hipSuccess)
         return RUBICONV_ERR_HIP;
     pl->device_ready = true;
@@ -333,8 +333,10 @@ std::string stage(const char* tag, const char* name) { return std::string(tag) +
 struct SpecScale {
     uint16_t* parts;
     float2* used;
-    float guess;   // the first pass's scale (a power of two)
-    float* hint;   // host-mapped word that receives the exact scale
+    float guess;                  // the first pass's scale (a power of two)
+    float* hint;                  // host-mapped word that receives the exact scale
+    float extra = 1.0f;           // power of two the scale carries besides 2^(3 - e)
+    const float2* prev = nullptr; // a scale word whose inverse the used word's inverse carries
 };
 
 // The scale a call's first column pass starts at: the last one its plan found (a power of
@@ -365,7 +367,7 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
     if (spec != nullptr && n_cols > 0 && e == hipSuccess)
         e = rubiconv::launch_col_fwd_mfma(in_dtype, in, rs, h.D, grid, plan->grid_pb_stride, plan->doc_t, in_sc,
                                           plan->mfma_tab, n_cols, h.npb, stream, nullptr, spec->parts, spec->used,
-                                          spec->guess, spec->hint);
+                                          spec->guess, spec->hint, spec->extra, spec->prev);
     rec.mark(stage(tag, "col_fwd"));
     // long rows: first level into the sub-row regions (both grids of the filter gradient)
     for (const rubiconv::LrItem& it : h.lr_doc_items)
@@ -524,9 +526,10 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
     const size_t filt_ws =
         pl->taps_bytes + align_up(static_cast<size_t>(rubiconv::tap_tile_rows(std::max(h.taps_max, 1))) * h.D * 4);
     // header: the scale words in the first kAlign bytes, then the amax
-    // partials: kAmaxParts of the prescale pass, or one per task of the forward column pass
+    // partials: kAmaxParts of the prescale pass, or one 16-bit word per column task
     const size_t n_tasks = h.doc_col_seg.size() * static_cast<size_t>(h.npb);
-    const size_t hdr_bytes = kAlign + align_up(std::max<size_t>(rubiconv::kAmaxParts, n_tasks) * 4);
+    // (dk keeps two sets of 16-bit magnitudes there, the second 16-byte aligned)
+    const size_t hdr_bytes = kAlign + align_up(std::max<size_t>(rubiconv::kAmaxParts, n_tasks + 8) * 4);
     pl->ws_hdr_off = std::max(conv_ws, filt_ws);
     pl->ws_bytes = pl->ws_hdr_off + hdr_bytes;
     pl->grid_bytes = conv_ws;
@@ -746,26 +749,48 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
     // range: x and dy prescaled by powers of two from their largest magnitudes, and
     // together by 2^-ceil(log2 P_max) (half on each side), as a correlation sums up to P
     // products; the inverse pass undoes all of it (the dy word's second half)
+    // On the matrix-core path both column passes find their scales themselves, starting
+    // from the ones the plan's previous dk call found (as the forward does for x).
     const float2* xs = plan->ones;
     const float2* ds = plan->ones;
-    if (e == hipSuccess && h.grid_half) {
-        float2* w = prescale_words(workspace, plan->dk_hdr_off);
-        uint32_t* work = prescale_work(workspace, plan->dk_hdr_off);
-        int pmax = 1;
-        for (const Seg& d : h.docs) pmax = std::max(pmax, d.P);
-        int lg = 0;
-        while ((1 << lg) < pmax && lg < 30) ++lg;
-        e = prescale(plan, h.x_dtype, x, std::ldexp(1.0f, -(lg + 1) / 2), nullptr, w, work, stream);
+    float2* w = prescale_words(workspace, plan->dk_hdr_off);
+    uint32_t* work = prescale_work(workspace, plan->dk_hdr_off);
+    int pmax = 1;
+    for (const Seg& d : h.docs) pmax = std::max(pmax, d.P);
+    int lg = 0;
+    while ((1 << lg) < pmax && lg < 30) ++lg;
+    const float ex = std::ldexp(1.0f, -(lg + 1) / 2), ed = std::ldexp(1.0f, -(lg / 2));
+    const bool speculative = h.grid_half && h.col_mfma && h.x_dtype == RUBICONV_BF16 && h.y_dtype == RUBICONV_BF16;
+    // per-task magnitudes: x's in the first half of the partials area, dy's in the second
+    uint16_t* parts = reinterpret_cast<uint16_t*>(work);
+    const size_t n_tasks = static_cast<size_t>(n_cols) * h.npb;
+    SpecScale spec_x{parts, w, scale_guess(plan, rubiconv_plan_s::kHintDkX),
+                     plan->scale_hint_dev + rubiconv_plan_s::kHintDkX, ex, nullptr};
+    SpecScale spec_dy{parts + (n_tasks + 7) / 8 * 8, w + 1, scale_guess(plan, rubiconv_plan_s::kHintDkDy),
+                      plan->scale_hint_dev + rubiconv_plan_s::kHintDkDy, ed, w};
+    if (e == hipSuccess && h.grid_half && !speculative) {
+        e = prescale(plan, h.x_dtype, x, ex, nullptr, w, work, stream);
         if (e == hipSuccess)
-            e = prescale(plan, h.y_dtype, dy, std::ldexp(1.0f, -(lg / 2)), w, w + 1, work, stream);
+            e = prescale(plan, h.y_dtype, dy, ed, w, w + 1, work, stream);
         rec.mark("dk_prescale");
+    }
+    if (h.grid_half) {
         xs = w;
         ds = w + 1;
     }
     // x's column DFTs into the second grid, then dy's passes against it with the
     // correlation product: document i's cross-correlation of dy with x lands at its
     // own token positions (lag = offset in the document) of r
-    if (e == hipSuccess)
+    if (e == hipSuccess && speculative) {
+        e = rubiconv::launch_col_fwd_mfma(h.x_dtype, x, rs, h.D, xgrid, plan->grid_pb_stride, plan->doc_t,
+                                          {plan->ones, xs}, plan->mfma_tab, n_cols, h.npb, stream, spec_x.parts,
+                                          nullptr, nullptr, spec_x.guess);
+        if (e == hipSuccess && n_cols > 0)
+            e = rubiconv::launch_col_fwd_mfma(h.x_dtype, x, rs, h.D, xgrid, plan->grid_pb_stride, plan->doc_t,
+                                              {plan->ones, xs}, plan->mfma_tab, n_cols, h.npb, stream, nullptr,
+                                              spec_x.parts, spec_x.used, spec_x.guess, spec_x.hint, spec_x.extra,
+                                              spec_x.prev);
+    } else if (e == hipSuccess) {
         e = h.col_mfma && h.x_dtype == RUBICONV_BF16
                        ? rubiconv::launch_col_fwd_mfma(h.x_dtype, x, rs, h.D, xgrid,
                                                        plan->grid_pb_stride, plan->doc_t,
@@ -774,6 +799,7 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
                        : rubiconv::launch_col_fwd(h.r, h.grid_half, h.x_dtype, x, rs, h.D, xgrid,
                                                   plan->grid_pb_stride, plan->doc_t, {plan->ones, xs},
                                                   n_cols, h.npb, stream);
+    }
     for (const rubiconv::LrItem& it : h.lr_doc_items)
         if (e == hipSuccess)
             e = rubiconv::launch_lr_step(false, xgrid, plan->grid_pb_stride, it, plan->doc_t.tw, h.n1,
@@ -782,7 +808,7 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
     if (e == hipSuccess)
         e = enqueue_conv(plan, dy, h.y_dtype, xgrid, plan->grid_pb_stride, plan->grad_t, r,
                          RUBICONV_F32, workspace, 1, true, {plan->ones, ds}, {plan->ones, ds}, "dk_",
-                         stream, rec);
+                         stream, rec, speculative ? &spec_dy : nullptr);
     if (e == hipSuccess && direct) e = join_direct(plan, stream, rec);
     if (e == hipSuccess)
         e = rubiconv::launch_lag_sum(r, plan->all_segs, static_cast<int>(h.all_docs.size()), h.N, h.D,

@@ -200,4 +200,19 @@ def test_scale_guess_sequence(device):
             douts[sc] = (dyv, bits)
             ref = oracle.grad_x(W.filters, dyv.astype(np.float64), W.cu_seqlens, threads=ORACLE_THREADS)
             assert_parity(dx.float().cpu().numpy().astype(np.float64), ref, W.cu_seqlens, "bf16", f"dx {sc}")
+    # dk: both column passes guess (x's and dy's scales); a repeated call must match
+    from tests.test_gpu_grad import _check_dk
+    dkb = {}
+    for sc in (1e-6, 1e-6, 1.0, 1e-6):
+        dyv = douts[sc][0]
+        dy = torch.from_numpy(wl.f32_to_bf16_bits(dyv.astype(np.float32)).view(np.int16)).view(torch.bfloat16).to(device)
+        dk = rc.packed_conv_dk(plan, xd, dy)
+        torch.cuda.synchronize()
+        v = dk.cpu().numpy().copy()
+        if sc in dkb:
+            assert np.array_equal(dkb[sc], v), f"dy scale {sc}: dk depends on the guess"
+        else:
+            dkb[sc] = v
+            _check_dk(v.astype(np.float64), oracle.grad_k(W.x, dyv.astype(np.float64), W.cu_seqlens, W.L,
+                                                          threads=ORACLE_THREADS), "bf16", f"dk {sc}")
     _say("[range] scale guesses: outputs independent of the guess")
