@@ -71,7 +71,7 @@ struct rubiconv_plan_s {
     // The row pass runs its size classes (independent launches) on side streams
     // forked from and joined back into the caller's stream with events; the mutex
     // keeps one call's record/wait sequence from interleaving with another's.
-    static constexpr int kSideStreams = 4;
+    static constexpr int kSideStreams = 2;
     hipStream_t side[kSideStreams] = {};
     hipEvent_t fork = nullptr;
     hipEvent_t direct_done = nullptr;  // the direct path's launch on its side stream
