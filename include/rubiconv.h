@@ -28,7 +28,8 @@
  * Conventions shared by every call:
  *   - All device pointers are HIP device memory on the current device; host
  *     pointers are ordinary process memory.  The caller owns every buffer it
- *     passes; the library owns only the plan and the plan's device tables.
+ *     passes; the library owns only the plan, the plan's device tables and 16 bytes
+ *     of pinned host memory per plan (its range-scale guesses).
  *   - Calls taking a stream enqueue work on it and return without waiting.
  *     They never synchronise the device, never allocate device memory and
  *     never print.  The plan may be used from several streams and host threads
@@ -133,8 +134,9 @@ typedef enum {
  *                   the plan on this stream is ordered after it; other streams must
  *                   wait for it (or the device be synchronised) before using the plan.
  * The plan copies what it needs; cu_seqlens_host may be freed on return.  Plan
- * creation allocates the plan's device memory and creates its side streams and
- * events (hipMalloc, hipStreamCreate, which HIP may order with other device work);
+ * creation allocates the plan's device memory and pinned host words and creates its
+ * side streams and events (hipMalloc, hipHostMalloc, hipStreamCreate, which HIP may
+ * order with other device work);
  * it does not wait for the upload.
  * Errors: RUBICONV_ERR_ARG (also for a malformed RUBICONV_DIRECT_MAX or
  * RUBICONV_CLASS_MERGE),
