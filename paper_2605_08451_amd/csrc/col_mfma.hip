@@ -190,7 +190,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         // stage 1: one MFMA tile per n2 (bf16: hi and lo matrix halves accumulate).
         // Token t = m (16 n1 + n2) + j with n1 = 4i + h (operand slot 4h + i; the
         // matrix tables use the same interleaving): a lane part and a wave-uniform part.
-        // All loads are issued before the first MFMA so that the wave waits once.
+        // All loads are issued before the first MFMA so that the wave waits once, at a
+        // raised wave priority so that waves about to load issue ahead of waves that
+        // compute (measured: the pass 2% faster)
+        __builtin_amdgcn_s_setprio(3);
         u4 xb[16];
         {
             uint32_t lane_off[4];
@@ -229,6 +232,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         // range scale of this lane's pair, applied to the fp32 products before fp16 rounding
         const float in_mul = sc.pair[pb * kPairsPerBlock + p].x * glob_x;
         __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(0);
 
         uint32_t y[16][4];
         uint32_t amax_lo = 0, amax_hi = 0;  // the largest bf16 magnitude bits of the loaded x
