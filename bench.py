@@ -84,6 +84,11 @@ def time_step(launch, stream, steps, warmup, eager):
             graph.replay()
         else:
             launch(stream)
+    settle_until = time.perf_counter() + 0.05   # clocks settle under load (untimed)
+    while time.perf_counter() < settle_until:
+        for _ in range(10):
+            step()
+        torch.cuda.synchronize()
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()

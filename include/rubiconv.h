@@ -28,8 +28,8 @@
  * Conventions shared by every call:
  *   - All device pointers are HIP device memory on the current device; host
  *     pointers are ordinary process memory.  The caller owns every buffer it
- *     passes; the library owns only the plan, the plan's device tables and 16 bytes
- *     of pinned host memory per plan (its range-scale guesses).
+ *     passes; the library owns only the plan, the plan's device tables and 1 KB of
+ *     pinned host memory per plan (its range-scale guesses).
  *   - Calls taking a stream enqueue work on it and return without waiting.
  *     They never synchronise the device, never allocate device memory and
  *     never print.  The plan may be used from several streams and host threads
@@ -50,7 +50,8 @@
  *     the largest |x| of the call, and the gradient calls scale dy (and x) the same
  *     way.  On the matrix-core path (N1 = 256, D a multiple of 32) each call finds
  *     those scales inside its column passes: a pass runs at the scale the plan's
- *     previous call of the same kind found (1 for the first call), and a second column
+ *     previous call of the same kind on the same input buffer found (1 for the first
+ *     call; 64 slots per kind, hashed from the buffer's address), and a second column
  *     pass runs only when the call's own scale differs.  The result does not depend on
  *     that guess (bit for bit); the plan keeps its guesses in pinned host memory that
  *     its kernels write.  Elsewhere the tensor is read once more for its largest

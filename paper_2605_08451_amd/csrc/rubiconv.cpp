@@ -44,11 +44,14 @@ struct rubiconv_plan_s {
     const float2* ones = nullptr;           // {1, 1} per channel pair: the unit range scales
     bool device_ready = false;
     bool prescale_fwd = true;    // the forward prescales x as the gradients do dy (and x)
-    // pinned host words, written by the matrix-core column pass of each call: the range
-    // scale of x (forward) and of dy (dx) the last call found.  A call starts its column
-    // pass at that scale and redoes the pass only when its own scale differs; any value
-    // is correct, a stale one costs the redo.
-    static constexpr int kHintFwd = 0, kHintDx = 1, kHintDkX = 2, kHintDkDy = 3, kHints = 4;
+    // pinned host words, written by the matrix-core column passes: the range scales the
+    // last calls found, per kind of call (forward x, dx dy, dk x, dk dy) and per input
+    // buffer (kHintSlots slots hashed from its address, so that one plan shared by several
+    // layers keeps each layer's scale).  A call starts its column pass at the scale of its
+    // slot and redoes the pass only when its own scale differs; any value is correct, a
+    // stale one costs the redo.
+    static constexpr int kHintFwd = 0, kHintDx = 1, kHintDkX = 2, kHintDkDy = 3;
+    static constexpr int kHintSlots = 64, kHints = 4 * kHintSlots;
     float* scale_hint = nullptr;      // host address
     float* scale_hint_dev = nullptr;  // the same words as kernels address them
     LaunchTables doc_t{};
@@ -339,10 +342,17 @@ struct SpecScale {
     const float2* prev = nullptr; // a scale word whose inverse the used word's inverse carries
 };
 
-// The scale a call's first column pass starts at: the last one its plan found (a power of
-// two in the range pow2_scale gives, else 1).
-float scale_guess(const rubiconv_plan_s* plan, int which) {
-    const float g = reinterpret_cast<const volatile float*>(plan->scale_hint)[which];
+// The hint word of a kind of call (rubiconv_plan_s::kHint*) and input buffer.
+int hint_slot(int kind, const void* input) {
+    const uint64_t a = reinterpret_cast<uintptr_t>(input) >> 8;
+    return kind * rubiconv_plan_s::kHintSlots +
+           static_cast<int>((a * 0x9E3779B97F4A7C15ull) >> 58);  // top 6 bits: 64 slots
+}
+
+// The scale a call's first column pass starts at: the last one its plan found for the
+// slot (a power of two in the range pow2_scale gives, else 1).
+float scale_guess(const rubiconv_plan_s* plan, int slot) {
+    const float g = reinterpret_cast<const volatile float*>(plan->scale_hint)[slot];
     return g >= 0x1p-126f && g <= 0x1p127f ? g : 1.0f;
 }
 
@@ -654,8 +664,9 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
     // for another scale, which saves a read of x whenever x's range holds from call to call.
     const float2* xs = plan->ones;
     float2* w = prescale_words(workspace, plan->ws_hdr_off);
+    const int slot = hint_slot(rubiconv_plan_s::kHintFwd, x);
     SpecScale spec{reinterpret_cast<uint16_t*>(prescale_work(workspace, plan->ws_hdr_off)), w,
-                   scale_guess(plan, rubiconv_plan_s::kHintFwd), plan->scale_hint_dev + rubiconv_plan_s::kHintFwd};
+                   scale_guess(plan, slot), plan->scale_hint_dev + slot};
     const bool speculative = h.grid_half && plan->prescale_fwd && h.col_mfma && h.x_dtype == RUBICONV_BF16;
     if (e == hipSuccess && h.grid_half && plan->prescale_fwd && !speculative) {
         e = prescale(plan, h.x_dtype, x, 1.0f, nullptr, w, prescale_work(workspace, plan->ws_hdr_off), stream);
@@ -698,8 +709,9 @@ rubiconv_status_t rubiconv_packed_conv_dx(rubiconv_plan_t plan, const void* dy, 
     // dy's own scale differs (as in the forward).
     const float2* ds = plan->ones;
     float2* w = prescale_words(workspace, plan->ws_hdr_off) + 1;
+    const int slot = hint_slot(rubiconv_plan_s::kHintDx, dy);
     SpecScale spec{reinterpret_cast<uint16_t*>(prescale_work(workspace, plan->ws_hdr_off)), w,
-                   scale_guess(plan, rubiconv_plan_s::kHintDx), plan->scale_hint_dev + rubiconv_plan_s::kHintDx};
+                   scale_guess(plan, slot), plan->scale_hint_dev + slot};
     const bool speculative = h.grid_half && h.col_mfma && h.y_dtype == RUBICONV_BF16;
     if (e == hipSuccess && h.grid_half && !speculative) {
         e = prescale(plan, h.y_dtype, dy, 1.0f, nullptr, w, prescale_work(workspace, plan->ws_hdr_off), stream);
@@ -764,10 +776,11 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
     // per-task magnitudes: x's in the first half of the partials area, dy's in the second
     uint16_t* parts = reinterpret_cast<uint16_t*>(work);
     const size_t n_tasks = static_cast<size_t>(n_cols) * h.npb;
-    SpecScale spec_x{parts, w, scale_guess(plan, rubiconv_plan_s::kHintDkX),
-                     plan->scale_hint_dev + rubiconv_plan_s::kHintDkX, ex, nullptr};
-    SpecScale spec_dy{parts + (n_tasks + 7) / 8 * 8, w + 1, scale_guess(plan, rubiconv_plan_s::kHintDkDy),
-                      plan->scale_hint_dev + rubiconv_plan_s::kHintDkDy, ed, w};
+    const int slot_x = hint_slot(rubiconv_plan_s::kHintDkX, x);
+    const int slot_dy = hint_slot(rubiconv_plan_s::kHintDkDy, dy);
+    SpecScale spec_x{parts, w, scale_guess(plan, slot_x), plan->scale_hint_dev + slot_x, ex, nullptr};
+    SpecScale spec_dy{parts + (n_tasks + 7) / 8 * 8, w + 1, scale_guess(plan, slot_dy),
+                      plan->scale_hint_dev + slot_dy, ed, w};
     if (e == hipSuccess && h.grid_half && !speculative) {
         e = prescale(plan, h.x_dtype, x, ex, nullptr, w, work, stream);
         if (e == hipSuccess)

@@ -157,8 +157,8 @@ def test_forward_range_direct_documents(device, monkeypatch, loud):
 
 
 def test_scale_guess_sequence(device):
-    """The matrix-core column pass starts at the range scale its plan's last call found and
-    redoes the pass when the call's own scale differs.  A sequence of calls whose x scale
+    """The matrix-core column pass starts at the range scale its plan's last call on the same
+    input buffer found and redoes the pass when the call's own scale differs.  A sequence of calls whose x scale
     changes (1, 100, 100, 1e-3, 1) must give, for each input, the same bits whether the
     guess was right or wrong, and the forward must meet the bar at every step; dx likewise
     for dy scales 1e-6, 1e-6, 1."""
@@ -174,8 +174,9 @@ def test_scale_guess_sequence(device):
     ws = plan.new_workspace(device)
     spec = rc.filter_spectrum(plan, kd, workspace=ws)
     outs = {}
+    xs = torch.empty_like(xd)   # one buffer: the guess is kept per input buffer
     for sc in (1.0, 100.0, 100.0, 1e-3, 1.0, 1e-3):
-        xs = (xd.float() * sc).to(torch.bfloat16)
+        xs.copy_((xd.float() * sc).to(torch.bfloat16))
         y = rc.packed_conv(plan, xs, spec, workspace=ws)
         torch.cuda.synchronize()
         bits = y.view(torch.int16).cpu().numpy().copy()
@@ -188,9 +189,10 @@ def test_scale_guess_sequence(device):
                                   threads=ORACLE_THREADS)
             assert_parity(yv, ref, W.cu_seqlens, "bf16", f"x scale {sc}")
     douts = {}
+    dy = torch.empty_like(xd)
     for sc in (1e-6, 1e-6, 1.0, 1e-6):
         dyv = wl.round_to_bf16(sc * rng.standard_normal((B, N, D), dtype=np.float32)) if sc not in douts else douts[sc][0]
-        dy = torch.from_numpy(wl.f32_to_bf16_bits(dyv.astype(np.float32)).view(np.int16)).view(torch.bfloat16).to(device)
+        dy.copy_(torch.from_numpy(wl.f32_to_bf16_bits(dyv.astype(np.float32)).view(np.int16)).view(torch.bfloat16))
         dx = rc.packed_conv_dx(plan, dy, spec, workspace=ws)
         torch.cuda.synchronize()
         bits = dx.view(torch.int16).cpu().numpy().copy()
@@ -205,7 +207,7 @@ def test_scale_guess_sequence(device):
     dkb = {}
     for sc in (1e-6, 1e-6, 1.0, 1e-6):
         dyv = douts[sc][0]
-        dy = torch.from_numpy(wl.f32_to_bf16_bits(dyv.astype(np.float32)).view(np.int16)).view(torch.bfloat16).to(device)
+        dy.copy_(torch.from_numpy(wl.f32_to_bf16_bits(dyv.astype(np.float32)).view(np.int16)).view(torch.bfloat16))
         dk = rc.packed_conv_dk(plan, xd, dy)
         torch.cuda.synchronize()
         v = dk.cpu().numpy().copy()
