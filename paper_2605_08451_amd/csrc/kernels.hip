@@ -1047,11 +1047,12 @@ hipError_t launch_transpose(const float* in, int rows, int cols, int in_ld, floa
 
 // One workgroup per 2 channel pairs (4 channels): thread t sums the tiles t / 4,
 // t / 4 + 64, ... of channel t % 4 (four independent sums in flight), then the 64 partial
-// sums of each channel are added in a fixed order.
+// sums of each channel are added in a fixed order (within each wave by shuffles, then the
+// four waves).
 __global__ __launch_bounds__(256) void filter_scale_kernel(const float* __restrict__ partials,
                                                            int ntiles, int D, int npairs,
                                                            float2* __restrict__ pair_scale) {
-    __shared__ float part[64][5];
+    __shared__ float part[4][4];
     const int c = threadIdx.x & 3, r = threadIdx.x >> 2;
     const int d = blockIdx.x * 4 + c;
     float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
@@ -1065,16 +1066,19 @@ __global__ __launch_bounds__(256) void filter_scale_kernel(const float* __restri
         }
         for (; t < ntiles; t += 64) a0 += partials[static_cast<int64_t>(t) * D + d];
     }
-    part[r][c] = (a0 + a1) + (a2 + a3);
+    // the 16 partial sums of each channel in a wave (lanes c, c + 4, ...), then the four waves
+    float a = (a0 + a1) + (a2 + a3);
+#pragma unroll
+    for (int o = 4; o < 64; o <<= 1) a += __shfl_xor(a, o);
+    if ((threadIdx.x & 63) < 4) part[threadIdx.x >> 6][c] = a;
     __syncthreads();
     if (threadIdx.x < 2) {
         const int q = blockIdx.x * 2 + threadIdx.x;
         float g = 0.0f;
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
-            float a = 0.0f;
-            for (int rr = 0; rr < 64; ++rr) a += part[rr][2 * threadIdx.x + k];
-            g = fmaxf(g, a);
+            const int cc = 2 * threadIdx.x + k;
+            g = fmaxf(g, (part[0][cc] + part[1][cc]) + (part[2][cc] + part[3][cc]));
         }
         if (q < npairs) {
             const float sc = pow2_scale(g, kFilterGainExp);
