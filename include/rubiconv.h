@@ -88,7 +88,7 @@ typedef enum {
     RUBICONV_OK = 0,
     RUBICONV_ERR_ARG = 1,         /* null pointer, non-positive size, unknown dtype */
     RUBICONV_ERR_SEQLENS = 2,     /* cu_seqlens row not 0 = c0 <= c1 <= ... <= c_max_docs = N */
-    RUBICONV_ERR_UNSUPPORTED = 3, /* valid request this build does not implement */
+    RUBICONV_ERR_UNSUPPORTED = 3, /* valid request the library does not implement */
     RUBICONV_ERR_ALLOC = 4,       /* host or device allocation for the plan failed */
     RUBICONV_ERR_HIP = 5          /* a HIP call or kernel launch failed */
 } rubiconv_status_t;
