@@ -12,7 +12,7 @@ import pytest
 import oracle
 import workloads as wl
 from tests.common import (ORACLE_THREADS, TOL, assert_parity, parity_report, reference,
-                          run_gpu)
+                          run_gpu, to_device)
 
 pytestmark = pytest.mark.gpu
 
@@ -279,3 +279,37 @@ def test_direct_path_limits(device, monkeypatch, dtype):
         assert_parity(dx, oracle.grad_x(W.filters, dyv, W.cu_seqlens), W.cu_seqlens, dtype,
                       f"dx limit {limit}")
         tg._check_dk(dk, oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L), dtype, f"limit {limit}")
+
+
+def test_plan_and_calls_on_a_side_stream(device):
+    """A plan made on a side stream and used there at once (its tables' upload is
+    enqueued on that stream, not waited for), with the spectrum, workspace and outputs
+    allocated by the binding for that stream: the outputs equal those of the calling
+    stream bit for bit, for the forward and both gradients."""
+    import torch
+    import paper_2605_08451_amd as rc
+    W = wl.make_case([[700, 300, 24], [1024]], D=64, L=1024, x_dtype="bf16", seed=91)
+    x, k = to_device(W, device)
+    rng = np.random.default_rng(92)
+    dy = torch.from_numpy(wl.f32_to_bf16_bits(rng.standard_normal(x.shape, dtype=np.float32))
+                          .view(np.int16)).view(torch.bfloat16).to(device)
+
+    def run(stream):
+        plan = rc.Plan(W.cu_seqlens, N=W.N, D=W.D, L=W.L, x_dtype="bf16", y_dtype="bf16", stream=stream)
+        spec = rc.filter_spectrum(plan, k, stream=stream)
+        y = rc.packed_conv(plan, x, spec, stream=stream)
+        dx = rc.packed_conv_dx(plan, dy, spec, stream=stream)
+        dk = rc.packed_conv_dk(plan, x, dy, stream=stream)
+        return plan, y, dx, dk
+
+    torch.cuda.synchronize(device)
+    ref = run(None)
+    torch.cuda.synchronize(device)
+    side = torch.cuda.Stream(device)
+    got = run(side)
+    side.synchronize()
+    for name, a, b in zip(("y", "dx", "dk"), ref[1:], got[1:]):
+        assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a,
+                           b.view(torch.int16) if b.dtype == torch.bfloat16 else b), name
+    yv = got[1].float().cpu().numpy().astype(np.float64)
+    assert_parity(yv, reference(W), W.cu_seqlens, "bf16", "side stream")
