@@ -139,10 +139,12 @@ typedef enum {
  * side streams and events (hipMalloc, hipHostMalloc, hipStreamCreate, which HIP may
  * order with other device work);
  * it does not wait for the upload.
- * Errors: RUBICONV_ERR_ARG (also for a malformed RUBICONV_DIRECT_MAX or
- * RUBICONV_CLASS_MERGE),
- * RUBICONV_ERR_SEQLENS, RUBICONV_ERR_UNSUPPORTED (n1 not supported, or a document
- * so long that its row DFT would exceed the largest supported size),
+ * Errors: RUBICONV_ERR_ARG (also for a malformed RUBICONV_DIRECT_MAX,
+ * RUBICONV_CLASS_MERGE or RUBICONV_PRESCALE),
+ * RUBICONV_ERR_SEQLENS, RUBICONV_ERR_UNSUPPORTED (n1 not supported, a document
+ * so long that its row DFT would exceed the largest supported size, or a shape whose
+ * kernels would need buffer offsets of 32 bits or more: a document's or size
+ * class's P * D * 4 bytes above 2^30, or a pair block's grid at 2^31 bytes or more),
  * RUBICONV_ERR_ALLOC, RUBICONV_ERR_HIP.
  */
 rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L, int max_docs,
