@@ -130,6 +130,11 @@ typedef enum {
  * row kernels as short rows (Algorithm 1's four-step factorisation applied to
  * the row DFT); RUBICONV_LONG_ROWS = 0 (read when the plan is made) keeps such rows
  * whole in the generic row kernel instead.
+ * A row size m_i is the smallest 2^a 3^b 5^c number of a fixed list (above it, any
+ * 2^a 3^b 5^c number) whose N1 m_i holds the causal padding.  RUBICONV_EXACT_ROWS = 1
+ * (read when the plan is made) gives rows of at most 128 points on the matrix cores
+ * (bf16 inputs) the smallest integer m_i instead, as Algorithm 1 allows: the same
+ * exact result on fewer grid points.
  *   stream          HIP stream the upload of the plan's device tables is enqueued on
  *                   (hipMemcpyAsync from a host copy the plan keeps): work that uses
  *                   the plan on this stream is ordered after it; other streams must

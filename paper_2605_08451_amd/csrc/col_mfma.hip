@@ -133,8 +133,9 @@ __device__ __forceinline__ uint32_t wave_amax16(const uint16_t* __restrict__ a, 
     return m;
 }
 
-// AMAX: each column task also writes the largest |x| it loaded (bf16 magnitude bits) to
-// amax_out[task], and the pass runs at scale first_scale in place of sc.glob.  amax_in
+// AMAX: the pass runs at scale first_scale in place of sc.glob, and each workgroup also
+// writes the largest |x| its tasks loaded (bf16 magnitude bits) to amax_out[blockIdx.x]
+// (launched with one workgroup per four tasks).  amax_in
 // (the redo launch): the launch first takes the range scale s from the n_amax magnitudes
 // a pass with AMAX recorded, times extra (a power of two), writes {s, p / s} to *used
 // (p = prev->y, or 1 without prev) and s to *hint (workgroup 0), and does nothing more when
@@ -170,7 +171,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
     copy_to_lds(mt + kMtFwd2, tab2, kTab2 / 64, wave, lane);
     __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();  // the only workgroup barrier
+    __syncthreads();  // the only workgroup barrier (AMAX: and the one after the tasks)
+    uint32_t wave_amax = 0;  // AMAX: the largest magnitude bits of the wave's tasks
     // wave-uniform task index: keeps the document's buffer resource in SGPRs.  A launch
     // with fewer workgroups than ntasks / 4 (the redo launch) loops over the tasks.
     for (int task = blockIdx.x * 4 + wave; task < ntasks; task += static_cast<int>(gridDim.x) * 4) {
@@ -304,8 +306,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
             uint32_t mx = amax_lane;
 #pragma unroll
             for (int o = 32; o > 0; o >>= 1) mx = max(mx, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mx), o)));
-            amax_out[task] = static_cast<uint16_t>(mx);
+            wave_amax = max(wave_amax, mx);
         }
+    }
+    if constexpr (AMAX) {  // one word per workgroup, so that the redo launch reduces a quarter as many
+        __shared__ uint32_t wg_amax[4];
+        wg_amax[wave] = wave_amax;  // every lane the same value
+        __syncthreads();
+        if (wave == 0)
+            amax_out[blockIdx.x] =
+                static_cast<uint16_t>(max(max(wg_amax[0], wg_amax[1]), max(wg_amax[2], wg_amax[3])));
     }
 }
 
@@ -464,26 +474,28 @@ hipError_t launch_col_fwd_mfma(int src_dtype, const void* src, int64_t src_row_s
                                const float2* prev) {
     if (n_cols == 0) return hipSuccess;
     if ((amax_out != nullptr || amax_in != nullptr) && src_dtype != 1) return hipErrorInvalidValue;
+    if (amax_out != nullptr && amax_in != nullptr) return hipErrorInvalidValue;
     if (amax_in != nullptr && (used == nullptr || (reinterpret_cast<uintptr_t>(amax_in) & 15) != 0))
         return hipErrorInvalidValue;
     const int ntasks = n_cols * npb;
     // the redo launch mostly does nothing: 1024 workgroups (four per CU) that loop over the
-    // tasks start and leave faster than one workgroup per four tasks
+    // tasks start and leave faster than one workgroup per four tasks.  Its magnitudes are
+    // those of the first launch, one per workgroup of that launch (wgs)
     const int wgs = (ntasks + 3) / 4;
     const dim3 g(amax_in != nullptr ? std::min(wgs, 1024) : wgs), b(256);
     const u4* mt = static_cast<const u4*>(mtab);
     uint32_t* gp = static_cast<uint32_t*>(grid);
     if (src_dtype == 1 && amax_out != nullptr)
         hipLaunchKernelGGL((col_fwd_mfma_kernel<kBf16In, true>), g, b, 0, stream, src, src_row_stride, D, gp,
-                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, amax_in, ntasks, used, first_scale, hint,
+                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, amax_in, wgs, used, first_scale, hint,
                            extra, prev);
     else if (src_dtype == 1)
         hipLaunchKernelGGL((col_fwd_mfma_kernel<kBf16In, false>), g, b, 0, stream, src, src_row_stride, D, gp,
-                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, amax_in, ntasks, used, first_scale, hint,
+                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, amax_in, wgs, used, first_scale, hint,
                            extra, prev);
     else
         hipLaunchKernelGGL((col_fwd_mfma_kernel<kF16In, false>), g, b, 0, stream, src, src_row_stride, D, gp,
-                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, amax_in, ntasks, used, first_scale, hint,
+                           grid_pb_stride, t, sc, mt, npb, ntasks, amax_out, amax_in, wgs, used, first_scale, hint,
                            extra, prev);
     return hipGetLastError();
 }

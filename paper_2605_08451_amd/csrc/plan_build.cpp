@@ -4,7 +4,11 @@
 // asks for a transform of at least L_i + min(L_i, L) - 1 points that N1
 // divides.  The row DFT size m_i is the smallest size of row_sizes.hpp's list
 // (longer rows: the smallest 2^a 3^b 5^c number) with
-// N1 * m_i >= L_i + min(L_i, L) - 1: any such size gives the same exact
+// N1 * m_i >= L_i + min(L_i, L) - 1.  With RUBICONV_EXACT_ROWS = 1, rows of at most
+// 16 * kMaxDenseBlocks points on complex fp16 grids (the matrix-core row kernels, whose
+// dense blocks apply an m-point DFT of any m) take the smallest integer m_i instead:
+// fewer grid points, but as many 16-point blocks per row, and measured no faster.
+// Any such size gives the same exact
 // convolution on [0, L_i) because the circular wrap of the padded product lands
 // only on positions >= L_i.  Documents with equal m_i share a size class and
 // one filter spectrum; that spectrum keeps Lh = min(L, floor((P + 1) / 2)) taps,
@@ -389,7 +393,10 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
     p.grid_half = x_dtype == 1;  // bf16 inputs: complex fp16 grids and spectra
     p.npb = ((D + 1) / 2 + kPairsPerBlock - 1) / kPairsPerBlock;
 
-    // documents and their row DFT sizes
+    // documents and their row DFT sizes (RUBICONV_EXACT_ROWS = 1: matrix-core rows at their
+    // own size)
+    const char* exact_env = std::getenv("RUBICONV_EXACT_ROWS");
+    const bool exact_rows = p.grid_half && exact_env && exact_env[0] == '1';
     std::map<int, int> class_of_m;
     for (int b = 0; b < B; ++b) {
         const int32_t* c = cu + static_cast<int64_t>(b) * (max_docs + 1);
@@ -410,8 +417,10 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
             if (mmin > kMaxM) return BuildError::kUnsupported;
             // column passes address a document with 32-bit buffer offsets
             if (static_cast<int64_t>(n1) * mmin * D * 4 > (int64_t(1) << 30)) return BuildError::kUnsupported;
-            // listed sizes have register-resident row kernels; longer rows are 5-smooth
-            int m = fast_row_size(static_cast<int>(mmin));
+            // matrix-core rows take their own size; listed sizes have register-resident
+            // row kernels; longer rows are 5-smooth
+            int m = exact_rows && mmin <= 16 * kMaxDenseBlocks ? static_cast<int>(mmin)
+                                                                 : fast_row_size(static_cast<int>(mmin));
             if (m == 0) m = smooth_ceil(static_cast<int>(mmin));
             if (m > kMaxM) return BuildError::kUnsupported;
             Seg s{};

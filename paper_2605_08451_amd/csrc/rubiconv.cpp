@@ -329,10 +329,10 @@ std::string stage(const char* tag, const char* name) { return std::string(tag) +
 // (dtype out_dtype).  own_rows: every document's second grid rows are its own (the
 // filter gradient), so the matrix-core row pass takes one document per task instead
 // of groups of a size class.  The caller holds the plan's launch mutex.
-// spec (matrix-core column pass, bf16 input only): the column pass runs at scale 1 while
-// recording |in|'s largest value per task into spec->parts; a second launch takes the exact
-// power-of-two scale from them, writes it to spec->used and redoes the pass at that scale
-// only when it is not 1.
+// spec (matrix-core column pass, bf16 input only): the column pass runs at the guessed scale
+// while recording |in|'s largest value per workgroup (four tasks) into spec->parts; a second
+// launch takes the exact power-of-two scale from them, writes it to spec->used and redoes
+// the pass at that scale only when it differs from the guess.
 struct SpecScale {
     uint16_t* parts;
     float2* used;
@@ -536,7 +536,8 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
     const size_t filt_ws =
         pl->taps_bytes + align_up(static_cast<size_t>(rubiconv::tap_tile_rows(std::max(h.taps_max, 1))) * h.D * 4);
     // header: the scale words in the first kAlign bytes, then the amax
-    // partials: kAmaxParts of the prescale pass, or one 16-bit word per column task
+    // partials: kAmaxParts of the prescale pass, or one 16-bit word per workgroup of the
+    // first forward column pass (four column tasks)
     const size_t n_tasks = h.doc_col_seg.size() * static_cast<size_t>(h.npb);
     // (dk keeps two sets of 16-bit magnitudes there, the second 16-byte aligned)
     const size_t hdr_bytes = kAlign + align_up(std::max<size_t>(rubiconv::kAmaxParts, n_tasks + 8) * 4);

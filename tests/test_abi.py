@@ -2,8 +2,9 @@
 
 The document table must match the oracle's segment derivation exactly, and every
 transform size must satisfy the causal padding rule of Algorithm 1
-(P_i >= L_i + min(L_i, L) - 1, N1 divides P_i) with m_i the smallest 2^a 3^b 5^c
-size that does.
+(P_i >= L_i + min(L_i, L) - 1, N1 divides P_i) with m_i the smallest listed (then
+2^a 3^b 5^c) size that does, or with RUBICONV_EXACT_ROWS = 1 the smallest integer for
+rows on the matrix cores (bf16 inputs, m_i <= 128).
 """
 import ctypes
 import os
@@ -58,6 +59,22 @@ def listed_row_sizes():
     return sorted(m for m, _, _ in sizes)
 
 
+#: rows of at most this many points take the matrix-core row kernels on complex fp16
+#: grids (bf16 inputs), whose dense blocks apply a DFT of any size
+DENSE_MAX_M = 128
+
+
+def own_row_size(minimal_m, dtype, exact=False):
+    """The row size the plan gives a document whose causal padding needs minimal_m grid
+    columns, before class merging."""
+    listed = listed_row_sizes()
+    if exact and dtype == "bf16" and minimal_m <= DENSE_MAX_M:
+        return minimal_m
+    if minimal_m <= listed[-1]:
+        return min(s for s in listed if s >= minimal_m)
+    return next(c for c in range(minimal_m, 4 * minimal_m) if _smooth(c))
+
+
 def _smooth(n):
     for p in (2, 3, 5):
         while n % p == 0:
@@ -65,10 +82,12 @@ def _smooth(n):
     return n == 1
 
 
+@pytest.mark.parametrize("exact", [False, True])
 @pytest.mark.parametrize("i", range(5))
 @pytest.mark.parametrize("n1", [0, 64])
-def test_doc_table_matches_oracle_segments(i, n1, monkeypatch):
+def test_doc_table_matches_oracle_segments(i, n1, exact, monkeypatch):
     monkeypatch.setenv("RUBICONV_CLASS_MERGE", "0")
+    monkeypatch.setenv("RUBICONV_EXACT_ROWS", "1" if exact else "0")
     cu = wl.config_cu_seqlens(i)
     D, L, dt = wl.CONFIG_SHAPES[i]
     N = int(cu[0, -1])
@@ -92,6 +111,9 @@ def test_doc_table_matches_oracle_segments(i, n1, monkeypatch):
     assert np.all(P >= refP), "transform shorter than the causal padding rule allows"
     listed = listed_row_sizes()
     for mi, minimal in zip(m, refP // k):
+        if exact and dt == "bf16" and minimal <= DENSE_MAX_M:   # matrix-core rows: the size itself
+            assert mi == minimal, (mi, minimal)
+            continue
         assert _smooth(int(mi))
         if minimal <= listed[-1]:   # the smallest listed size that is large enough
             assert mi == min(s for s in listed if s >= minimal), (mi, minimal)
@@ -103,18 +125,10 @@ def test_doc_table_matches_oracle_segments(i, n1, monkeypatch):
     assert info["n_classes"] == len(set(m.tolist()))
 
 
-def _own_sizes(plan_table, k):
-    """Each transform document's own row size (no class merging): the smallest listed
-    size (else 2^a 3^b 5^c number) whose N1 m reaches the causal padding."""
-    listed = listed_row_sizes()
-    out = []
-    for minimal in plan_table:
-        mm = -(-int(minimal) // k)
-        if mm <= listed[-1]:
-            out.append(min(s for s in listed if s >= mm))
-        else:
-            out.append(next(c for c in range(mm, 4 * mm) if _smooth(c)))
-    return out
+def _own_sizes(plan_table, k, dtype, exact=False):
+    """Each transform document's own row size (no class merging) for the minimal padded
+    lengths of the oracle's table."""
+    return [own_row_size(-(-int(minimal) // k), dtype, exact) for minimal in plan_table]
 
 
 #: bytes per grid point and channel pair (in grid elements) of a document and of a
@@ -126,13 +140,32 @@ def _cost(ms):
     return DOC_POINT * sum(ms) + CLASS_POINT * sum(set(ms))
 
 
+def _brute_force_best_cost(own):
+    """The least cost over every choice of classes (each a subset of the documents' own
+    sizes that holds the largest one; a document takes the smallest class that fits)."""
+    sizes = np.array(sorted(set(own)), dtype=np.int64)
+    k = len(sizes)
+    counts = np.array([own.count(int(v)) for v in sizes], dtype=np.int64)
+    masks = np.arange(1 << (k - 1), dtype=np.int64)
+    chosen = ((masks[:, None] >> np.arange(k - 1)) & 1).astype(bool)
+    chosen = np.concatenate([chosen, np.ones((len(masks), 1), dtype=bool)], axis=1)
+    # the class serving size i: the first chosen size at or after i
+    idx = np.where(chosen, np.arange(k), k)
+    serve = np.minimum.accumulate(idx[:, ::-1], axis=1)[:, ::-1]
+    served = sizes[serve]
+    cost = DOC_POINT * (served * counts).sum(axis=1) + CLASS_POINT * (chosen * sizes).sum(axis=1)
+    return int(cost.min())
+
+
+@pytest.mark.parametrize("exact", [False, True])
 @pytest.mark.parametrize("i", range(5))
-def test_class_merging(i):
+def test_class_merging(i, exact, monkeypatch):
     """With class merging (the default) every document keeps the segment of the oracle's
     table, a transform at least as long as the causal padding asks, and a row size that
     is some document's own size; the merged sizes cost no more than the unmerged ones, and
-    no other choice of classes costs less (every subset of the sizes, brute force)."""
-    import itertools
+    no other choice of classes costs less (every subset of the sizes, brute force).  Both
+    with listed sizes everywhere and with the matrix-core rows at their own sizes."""
+    monkeypatch.setenv("RUBICONV_EXACT_ROWS", "1" if exact else "0")
     cu = wl.config_cu_seqlens(i)
     D, L, dt = wl.CONFIG_SHAPES[i]
     N = int(cu[0, -1])
@@ -141,19 +174,12 @@ def test_class_merging(i):
     np.testing.assert_array_equal(t[:, :4], ref[:, :4])
     tr = t[:, 5] > 0
     m = [int(v) for v in t[tr, 4]]
-    own = _own_sizes(ref[tr, 4], 256)
+    own = _own_sizes(ref[tr, 4], 256, dt, exact)
     assert all(mi >= oi and mi in own for mi, oi in zip(m, own)), (m, own)
     assert np.all(t[tr, 5] >= ref[tr, 4])
     assert _cost(m) <= _cost(own)
-    sizes = sorted(set(own))
-    if len(sizes) <= 16:
-        best = None
-        for r in range(len(sizes)):
-            for sub in itertools.combinations(sizes[:-1], r):
-                cls = sorted(sub) + [sizes[-1]]
-                c = _cost([min(s for s in cls if s >= o) for o in own])
-                best = c if best is None else min(best, c)
-        assert _cost(m) == best
+    if len(set(own)) <= 20:
+        assert _cost(m) == _brute_force_best_cost(own)
 
 
 def test_class_merging_switch(monkeypatch):
@@ -166,7 +192,7 @@ def test_class_merging_switch(monkeypatch):
     merged = rc.Plan(cu, N=N, D=D, L=L, x_dtype=dt).info()["n_classes"]
     monkeypatch.setenv("RUBICONV_CLASS_MERGE", "0")
     t = rc.Plan(cu, N=N, D=D, L=L, x_dtype=dt).doc_table()
-    assert [int(v) for v in t[:, 4]] == _own_sizes(ref[:, 4], 256)
+    assert [int(v) for v in t[:, 4]] == _own_sizes(ref[:, 4], 256, dt)
     assert merged < len(set(t[:, 4].tolist()))
     monkeypatch.setenv("RUBICONV_CLASS_MERGE", "2")
     with pytest.raises(rc.RubiconvError) as e:

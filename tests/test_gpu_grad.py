@@ -131,6 +131,31 @@ def test_gradients_matrix_core_rows(device, D):
               f"D={D}")
 
 
+def test_gradients_unlisted_row_sizes(device, monkeypatch):
+    """Row sizes outside the 2^a 3^b 5^c list (primes and others), which the matrix-core
+    row kernels take as they are (RUBICONV_EXACT_ROWS = 1), for the forward, dx and dk:
+    every size its own class, a 7-tap filter so that a document of 256 (k - 1) + 3
+    tokens takes m = k."""
+    import paper_2605_08451_amd as rc
+    monkeypatch.setenv("RUBICONV_CLASS_MERGE", "0")
+    monkeypatch.setenv("RUBICONV_EXACT_ROWS", "1")
+    ks = (7, 11, 13, 23, 31, 37, 53, 67, 89, 101, 127)
+    lens = [256 * (k - 1) + 3 for k in ks]
+    N = max(lens) + 1
+    rows = [[ln, N - ln] for ln in lens]
+    W = wl.make_case(rows, D=32, L=7, x_dtype="bf16", seed=17)
+    dyv, dx, dk, plan = _run(W, device, seed=18)
+    ms = sorted(set(int(m) for m in plan.doc_table()[:, 4]))
+    assert all(k in ms for k in ks), (ks, ms)
+    x, k = to_device(W, device)
+    y = rc.conv(x, k, W.cu_seqlens).float().cpu().numpy().astype(np.float64)
+    assert_parity(y, oracle.conv_direct(W.x, W.filters, W.cu_seqlens, threads=ORACLE_THREADS),
+                  W.cu_seqlens, "bf16", "forward")
+    assert_parity(dx, oracle.grad_x(W.filters, dyv, W.cu_seqlens, threads=ORACLE_THREADS),
+                  W.cu_seqlens, "bf16", "dx")
+    _check_dk(dk, oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L, threads=ORACLE_THREADS), "bf16", "dk")
+
+
 def test_dx_leakage(device):
     """An impulse of dy in one document leaves dx of every other document below 1e-6 of
     its peak; impulses at the first and last token of a row."""

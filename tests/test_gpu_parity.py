@@ -230,17 +230,22 @@ def test_row_kernel_sizes_precision(device, family, monkeypatch):
     """The same tight bar (5e-3 per document) for the other matrix-core row kernels on the
     matrix-core column path (D = 32): rows of 2..32 points (row_lds_kernel), rows of at
     most 8 points batched 16 / m documents to a block (row_batch_kernel) and rows of
-    33..128 points (row_partner_kernel), every size as its own class."""
+    33..128 points (row_partner_kernel), every size as its own class: 2^a 3^b 5^c sizes
+    and, with rows at their own sizes (RUBICONV_EXACT_ROWS = 1), the others (primes among
+    them), which these kernels take as they are."""
     monkeypatch.setenv("RUBICONV_CLASS_MERGE", "0")
+    monkeypatch.setenv("RUBICONV_EXACT_ROWS", "1")
     n1 = 256
     if family == "lds":
-        ks = (2, 3, 4, 5, 6, 8, 9, 10, 12, 15, 16, 18, 20, 24, 25, 27, 30, 32)
+        ks = (2, 3, 4, 5, 6, 8, 9, 10, 12, 15, 16, 18, 20, 24, 25, 27, 30, 32,
+              7, 11, 13, 14, 17, 19, 21, 22, 23, 26, 28, 29, 31)
         monkeypatch.setenv("RUBICONV_ROW_BATCH", "0")
     elif family == "batch":
-        ks = (1, 2, 3, 4, 5, 6, 8, 1, 2, 4, 8)
+        ks = (1, 2, 3, 4, 5, 6, 8, 1, 2, 4, 8, 7, 7, 3)
         monkeypatch.setenv("RUBICONV_ROW_BATCH", "8")
     else:
-        ks = (36, 40, 45, 48, 50, 54, 60, 64, 72, 75, 80, 81, 90, 96, 100, 108, 120, 128)
+        ks = (36, 40, 45, 48, 50, 54, 60, 64, 72, 75, 80, 81, 90, 96, 100, 108, 120, 128,
+              33, 37, 41, 44, 47, 53, 59, 61, 67, 71, 77, 83, 89, 97, 101, 109, 113, 127)
     # a 7-tap filter: P >= len + 6, so a document of n1 (k - 1) + 3 tokens takes m = k
     lens = [n1 * (k - 1) + 3 if k > 1 else 100 + 7 * i for i, k in enumerate(ks)]
     N = max(lens) + 1
