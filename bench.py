@@ -65,6 +65,15 @@ def parse():
     return ap.parse_args()
 
 
+def progress(msg):
+    """One line per phase on stderr, so that a run that stops names where it was."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+# calls timed stage by stage with the library's HIP events (each call holds up to 64)
+PROFILE_CALLS = 20
+
+
 def time_step(launch, stream, steps, warmup, eager):
     """Milliseconds per call of launch(stream): a captured HIP graph replayed steps times
     (or eager launches), bracketed by events on the timing stream."""
@@ -122,10 +131,14 @@ def backward_measurement(rc, plan, W, x, k, spec, ws, stream, args):
 
     def launch_dk(s):
         rc.packed_conv_dk(plan, x, dy, dk=dk, workspace=dk_ws, stream=s)
+    progress("dx step")
     dx_ms = time_step(launch_dx, stream, args.steps, args.warmup, args.eager)
+    progress("dk step")
     dk_ms = time_step(launch_dk, stream, args.steps, args.warmup, args.eager)
-    plan.profile_start(2 * args.steps)
-    for _ in range(args.steps):
+    progress("gradient stages")
+    calls = min(args.steps, PROFILE_CALLS)
+    plan.profile_start(2 * calls)
+    for _ in range(calls):
         launch_dx(stream)
         launch_dk(stream)
     kt = plan.profile_read()
@@ -143,7 +156,7 @@ def backward_measurement(rc, plan, W, x, k, spec, ws, stream, args):
            "unit": "Mtokens*channels/s",
            "dx_hbm_roofline_frac_step": round(dx_min / (dx_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
            "dk_hbm_roofline_frac_step": round(dk_min / (dk_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-           "stages_us": {n: round(1e3 * tot / args.steps, 1) for n, (c, tot) in kt.items()}}
+           "stages_us": {n: round(1e3 * tot / calls, 1) for n, (c, tot) in kt.items()}}
     del dk_ws, dx, dk, dy
     return out
 
@@ -482,6 +495,7 @@ def configs_measurement(args, copy_gbps, cpu):
     stream = torch.cuda.current_stream(dev)
     out, cpu_out, threads = {}, {}, None
     for i in range(5):
+        progress(f"workload {wl.CONFIG_NAMES[i]}")
         W = wl.make_config(i)
         if W.x_dtype == "bf16":
             x = torch.from_numpy(W.x_bits.view(np.int16)).view(torch.bfloat16).to(dev)
@@ -544,6 +558,7 @@ def main():
         sweep(args)
         return
     dev = torch.device("cuda:0")
+    progress(f"step of {wl.CONFIG_NAMES[args.config]}")
     W = wl.make_config(args.config)
     if W.x_dtype == "bf16":
         x = torch.from_numpy(W.x_bits.view(np.int16)).view(torch.bfloat16).to(dev)
@@ -605,16 +620,18 @@ def main():
 
     # stage durations: HIP events the library records on the stream each stage runs on
     # (a stage that forks to side streams is timed from before its fork to after its join)
-    plan.profile_start(2 * args.steps)
-    for _ in range(args.steps):
+    progress("stages")
+    calls = min(args.steps, PROFILE_CALLS)
+    plan.profile_start(2 * calls)
+    for _ in range(calls):
         launch(stream)
     kt = plan.profile_read()
     plan.profile_start(0)
     kb = kernel_bytes(info, W, plan)
-    stages = {n: {"launches_per_step": c / args.steps, "avg_us": 1e3 * tot / c,
-                  "us_per_step": 1e3 * tot / args.steps,
-                  "compulsory_bytes_per_launch": round(kb[n] * args.steps / c) if n in kb else None,
-                  "compulsory_GBps": (kb[n] * args.steps / c) / (tot / c * 1e-3) / 1e9 if n in kb else None}
+    stages = {n: {"launches_per_step": c / calls, "avg_us": 1e3 * tot / c,
+                  "us_per_step": 1e3 * tot / calls,
+                  "compulsory_bytes_per_launch": round(kb[n] * calls / c) if n in kb else None,
+                  "compulsory_GBps": (kb[n] * calls / c) / (tot / c * 1e-3) / 1e9 if n in kb else None}
               for n, (c, tot) in kt.items()}
     # the dominant stage: the longest one of a step
     dom = max(stages, key=lambda n: stages[n]["us_per_step"])
@@ -660,14 +677,18 @@ def main():
     del graph
     cpu_cfg, threads = {}, None
     if not args.no_configs:
+        progress("every workload")
         out["configs"], cpu_cfg, threads = configs_measurement(args, copy_gbps, not args.no_cpu_baseline)
     if not args.no_backward:
         out["backward"] = backward_measurement(rc, plan, W, x, k, spec, ws, stream, args)
     if not args.no_ct:
+        progress("Cooley-Tukey variant")
         out["cooley_tukey"] = ct_measurement(rc, W, x, k, y, stream, ms, args)
     if args.layers > 0:
+        progress("stacked layers")
         out["stacked"] = stacked_measurement(rc, plan, W, x, stream, plan_ms, args)
     if not args.no_cpu_baseline:
+        progress("cpu baseline")
         model, ncpu = cpu_info()
         key = f"c{args.config}"
         if key not in cpu_cfg:

@@ -244,6 +244,12 @@ rubiconv_status_t rubiconv_packed_conv_noalloc(rubiconv_plan_t plan, const void*
  * product is dy's spectrum times the conjugate of x's spectrum on the
  * document's own grid, the inverse leaves the document's cross-correlation at
  * lags 0..len-1, and the documents' correlations are summed per channel and lag.
+ * The inverse transforms are linear and the same for all documents of one size
+ * class, so on the matrix-core row pass (bf16 inputs, rows of at most 128 points)
+ * the products of up to eight documents of a class are added first, longest
+ * document first, and transformed back once, onto the longest one's positions:
+ * the class's transform size keeps the causal padding of its longest document,
+ * so no document's correlation wraps onto a lag below that document's length.
  */
 
 /*
@@ -275,7 +281,8 @@ size_t rubiconv_dk_workspace_bytes(rubiconv_plan_t plan);
  *   workspace  device buffer of rubiconv_dk_workspace_bytes(plan), 256-byte
  *              aligned; dk must not overlap it.
  *   stream     HIP stream the work is enqueued on.
- * The sum over documents runs in a fixed order (longest document first, ties in
+ * The sums over documents run in a fixed order (within a size class's group and
+ * then over the groups' and other documents' correlations, longest first, ties in
  * table order), so results are deterministic.
  * Errors: RUBICONV_ERR_ARG, RUBICONV_ERR_UNSUPPORTED (a plan of 2^31 grid points
  * or more), RUBICONV_ERR_HIP.

@@ -78,6 +78,9 @@ hipError_t launch_row_fast(int m, bool half, void* grid, int64_t grid_pb_stride,
 // size class and whose second-grid rows are those of the group's first document.
 // Every document has ceil(m / 16) == nb (1 <= nb <= kMaxDenseBlocks); tabs = the
 // plan's dense operand tables, addressed through Seg::dense_off.
+// sum: every document of a group brings its own second-grid rows, the products of
+// the group's documents are added, and the one inverse transform of the sum is written
+// over the first document's rows (the others are left as they were).
 // 16-byte entries of one class's tables for the rows of 3 to 8 blocks: per direction
 // nb * nb real operands of 64 lanes, then 16 nb complex fp16 twiddles w^(-j) and
 // 16 nb complex fp32 twiddles w^j (w = exp(-2 pi i / m)), padded to whole 1 KB chunks.
@@ -86,7 +89,7 @@ constexpr int partner_tab_u4(int nb) { return (2 * nb * nb * 64 + 12 * nb + 63) 
 hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const void* fgrid,
                             int64_t fgrid_pb_stride, const Seg* segs, const int32_t* docs,
                             const int32_t* groups, int ngroups, const void* tabs, int n1, int npb,
-                            int corr, hipStream_t stream);
+                            int corr, hipStream_t stream, bool sum = false);
 
 // Long rows (fp16 grids): the first level of the row DFT of one document or class grid
 // (LrItem) for its n1 grid rows and npb pair blocks, into its sub-row region, or the

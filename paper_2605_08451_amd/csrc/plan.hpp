@@ -33,6 +33,10 @@ constexpr int kDocPointCost = 10;
 constexpr int kClassPointCost = 3;
 // Documents of one size class that share a row task of the matrix-core row pass
 constexpr int kMaxGroupDocs = 4;
+// Filter gradient: documents of one size class whose correlation products the
+// matrix-core row pass adds before its one inverse transform (fp16 sums: the bound on
+// one document's product leaves room for far more)
+constexpr int kMaxSumDocs = 8;
 // Rows of at most this many points are batched 16 / m to a matrix-core block, when
 // they hold at least 1 / kBatchMinShare of the grid (measured: +2.5% on a batch of
 // mostly 1-8-point rows, -1% when three such documents sit among long ones)

@@ -586,14 +586,28 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
             class_groups(nb, false);
             p.dense_grp_n[nb] = static_cast<int32_t>(p.dense_groups.size() / 2) - p.dense_grp0[nb];
         }
+        // filter gradient: each class's documents longest first (ties in document order),
+        // in near-equal groups of at most kMaxSumDocs
         for (int nb = 1; nb <= kMaxDenseBlocks; ++nb) {
-            p.dense_dgrp0[nb] = static_cast<int32_t>(p.dense_groups.size() / 2);
-            for (int k = 0; k < p.dense_count[nb]; ++k) {
-                if (p.docs[p.dense_docs[p.dense_list0[nb] + k]].m <= batch_m) continue;
-                p.dense_groups.push_back(p.dense_list0[nb] + k);
-                p.dense_groups.push_back(1);
+            p.dense_sgrp0[nb] = static_cast<int32_t>(p.dense_sgroups.size() / 2);
+            for (const Seg& c : p.classes) {
+                if (c.m > 16 * kMaxDenseBlocks || (c.m + 15) / 16 != nb || c.nlist == 0) continue;
+                std::vector<int32_t> mem(p.class_docs.begin() + c.list0, p.class_docs.begin() + c.list0 + c.nlist);
+                std::stable_sort(mem.begin(), mem.end(),
+                                 [&](int32_t a, int32_t b) { return p.docs[a].len > p.docs[b].len; });
+                const int n = static_cast<int>(mem.size()), ng = (n + kMaxSumDocs - 1) / kMaxSumDocs;
+                for (int g = 0, first = 0; g < ng; ++g) {
+                    const int cnt = n / ng + (g < n % ng ? 1 : 0);
+                    p.dense_sgroups.push_back(static_cast<int32_t>(p.dense_sdocs.size()));
+                    p.dense_sgroups.push_back(cnt);
+                    for (int q = 0; q < cnt; ++q) {
+                        p.dense_sdocs.push_back(mem[first + q]);
+                        p.dense_swork[nb] += p.docs[mem[first + q]].m;
+                    }
+                    first += cnt;
+                }
             }
-            p.dense_dgrp_n[nb] = static_cast<int32_t>(p.dense_groups.size() / 2) - p.dense_dgrp0[nb];
+            p.dense_sgrp_n[nb] = static_cast<int32_t>(p.dense_sgroups.size() / 2) - p.dense_sgrp0[nb];
         }
         p.dense_bgrp0 = static_cast<int32_t>(p.dense_groups.size() / 2);
         class_groups(1, true);
@@ -668,6 +682,30 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
     if ((p.grid_points + p.grid_points_lr) * pb_point_bytes >= (int64_t(1) << 31) ||
         (p.class_points + p.class_points_lr) * pb_point_bytes >= (int64_t(1) << 31))
         return BuildError::kUnsupported;
+    // filter gradient outputs: every document but the sum groups' followers
+    {
+        std::vector<char> follower(p.docs.size(), 0);
+        for (size_t g = 0; g + 1 < p.dense_sgroups.size(); g += 2)
+            for (int q = 1; q < p.dense_sgroups[g + 1]; ++q) follower[p.dense_sdocs[p.dense_sgroups[g] + q]] = 1;
+        int32_t col = 0;
+        for (size_t i = 0, k = 0; i < p.all_docs.size(); ++i) {
+            if (p.all_docs[i].P == 0) {  // a direct document: its sums go straight to the lag sum
+                p.dk_sum_segs.push_back(p.all_docs[i]);
+                continue;
+            }
+            const size_t d = k++;
+            if (follower[d]) continue;
+            Seg s = p.docs[d];
+            s.spec_off = static_cast<int32_t>(s.grid_off);  // second rows: its own x grid
+            s.col0 = col;
+            p.dk_col_seg.insert(p.dk_col_seg.end(), s.m, static_cast<int32_t>(p.dk_segs.size()));
+            col += s.m;
+            p.dk_segs.push_back(s);
+            p.dk_sum_segs.push_back(s);
+        }
+        std::stable_sort(p.dk_sum_segs.begin(), p.dk_sum_segs.end(),
+                         [](const Seg& a, const Seg& b) { return a.len > b.len; });
+    }
     *out = std::move(p);
     return BuildError::kOk;
 }

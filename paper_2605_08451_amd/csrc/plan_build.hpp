@@ -44,13 +44,27 @@ struct HostPlan {
     int32_t dense_count[kMaxDenseBlocks + 1] = {};  // documents with block count nb
     // row-task groups, pairs (first entry in dense_docs, documents): the documents of
     // one size class, at most kMaxGroupDocs per group, share one load and transform of
-    // the class's filter rows; the one-document groups serve the filter gradient, whose
-    // second operand is each document's own grid
+    // the class's filter rows
     std::vector<int32_t> dense_groups;
     int32_t dense_grp0[kMaxDenseBlocks + 1] = {};   // class groups of block count nb (pair index)
     int32_t dense_grp_n[kMaxDenseBlocks + 1] = {};
-    int32_t dense_dgrp0[kMaxDenseBlocks + 1] = {};  // one-document groups of block count nb
-    int32_t dense_dgrp_n[kMaxDenseBlocks + 1] = {};
+    // filter gradient (each document's second operand its own grid): sum groups, pairs
+    // (first entry in dense_sdocs, documents), of at most kMaxSumDocs documents of one
+    // size class, longest first; the row pass adds their correlation products and writes
+    // the inverse of the sum over the first document's rows
+    std::vector<int32_t> dense_sdocs;
+    std::vector<int32_t> dense_sgroups;
+    int32_t dense_sgrp0[kMaxDenseBlocks + 1] = {};  // sum groups of block count nb (pair index)
+    int32_t dense_sgrp_n[kMaxDenseBlocks + 1] = {};
+    double dense_swork[kMaxDenseBlocks + 1] = {};   // their summed row sizes
+    // filter gradient outputs: the documents whose rows hold correlations after the row
+    // pass (sum-group leaders and every document outside the sum groups), as copies of
+    // their segments with the second rows their own and columns renumbered (dk_segs,
+    // dk_col_seg: the inverse column pass), and with the direct documents, longest first
+    // (ties in table order), for the lag sum (dk_sum_segs)
+    std::vector<Seg> dk_segs;
+    std::vector<int32_t> dk_col_seg;
+    std::vector<Seg> dk_sum_segs;
     // rows of at most kMaxBatchM points: class groups of the batched kernel, which puts
     // 16 / m documents side by side in one block (for the filter gradient as well, as it
     // takes each document's second rows from that document)

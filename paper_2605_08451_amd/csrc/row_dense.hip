@@ -87,6 +87,11 @@ __device__ __forceinline__ uint32_t pk_add_neg_hi(uint32_t a, uint32_t b) {  // 
     asm("v_pk_add_f16 %0, %1, %2 neg_hi:[0,1]" : "=v"(r) : "v"(a), "v"(b));
     return r;
 }
+__device__ __forceinline__ uint32_t pk_add(uint32_t a, uint32_t b) {  // a + b
+    uint32_t r;
+    asm("v_pk_add_f16 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
 __device__ __forceinline__ uint32_t pk_add_neg_lo(uint32_t a, uint32_t b) {  // (a.x - b.x, a.y + b.y)
     uint32_t r;
     asm("v_pk_add_f16 %0, %1, %2 neg_lo:[0,1]" : "=v"(r) : "v"(a), "v"(b));
@@ -166,7 +171,7 @@ __device__ __forceinline__ void lds_copy16(__amdgpu_buffer_rsrc_t rs, int voffse
                                              voffset, 0, 0, 0);
 }
 
-template <int NB>
+template <int NB, bool SUM>
 __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __restrict__ grid,
                                                                int64_t grid_pb_stride,
                                                                const uint32_t* __restrict__ fgrid,
@@ -281,6 +286,127 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
         wave_lds_fence();
     };
 
+    // separated products of one document against its second rows' spectra fa (own) and
+    // fl (partner values): W(f) of row u into wu, W(-f) of row ub into the exchange row
+    auto products = [&](const uint32_t(*fa)[4], const uint32_t(*fl)[4], const uint32_t(*au)[4],
+                        uint32_t(*wu)[4]) {
+#pragma unroll
+        for (int kb = 0; kb < NB; ++kb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int slot = rbase - 16 * kb - r;  // >= -15: inside the zeroed front slots
+                const uint32_t b = xlds[16 * slot];
+                const uint32_t a = au[kb][r];
+                // correlation: the filter spectrum read at -f (its conjugate for real taps)
+                const uint32_t A = corr ? fl[kb][r] : fa[kb][r];
+                const uint32_t bf = corr ? fa[kb][r] : fl[kb][r];
+                const uint32_t e1 = pk_add_conj(a, b);
+                const uint32_t e2 = pk_swap_add_conj(a, b);
+                const uint32_t U = pk_add_neg_hi(e1, e2);
+                const uint32_t V = pk_add_neg_lo(e1, e2);
+                wu[kb][r] = w_pos(A, bf, U, V);
+                xlds[16 * slot] = w_neg(A, bf, U, V);
+            }
+        if (shift && h == 0) xlds[-16] = xlds[16 * (m - 1)];
+        wave_lds_fence();
+    };
+    // inverse DFT of rows u (from wu) and ub (from wb) into LDS rows 0 and 1 as
+    // [row][point][16 pairs], then 16-byte stores to the rows of rs
+    auto inverse_store = [&](const uint32_t(*wu)[4], const u4* wb, const RowBuffers& rs) {
+        uint32_t* out = stage;
+#pragma unroll
+        for (int kb = 0; kb < NB; ++kb) {
+            f4 acc[2][2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int jb = 0; jb < NB; ++jb) {
+                const u4 are = inv[((kb * NB + jb) * 2) * 64 + lane];
+                const u4 aim = inv[((kb * NB + jb) * 2 + 1) * 64 + lane];
+                const u4 win = {wu[jb][0], wu[jb][1], wu[jb][2], wu[jb][3]};
+                acc[0][0] = mma(are, win, acc[0][0]);
+                acc[0][1] = mma(aim, win, acc[0][1]);
+                acc[1][0] = mma(are, wb[jb], acc[1][0]);
+                acc[1][1] = mma(aim, wb[jb], acc[1][1]);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {  // output register r: time point 16 kb + 4 r + h
+                const int e = (16 * kb + 4 * r + h) * 16 + p;
+                out[e] = pack_h2(acc[0][0][r], acc[0][1][r]);
+                out[S * 16 + e] = pack_h2(acc[1][0][r], acc[1][1][r]);
+            }
+        }
+        wave_lds_fence();
+#pragma unroll
+        for (int jb = 0; jb < NB; ++jb) {
+            const int off = jb * 1024 + lane * 16;
+            const u4 vu = *reinterpret_cast<const u4*>(out + jb * 256 + lane * 4);
+            const u4 vb = *reinterpret_cast<const u4*>(out + S * 16 + jb * 256 + lane * 4);
+            __builtin_amdgcn_raw_buffer_store_b128(vu, rs.du, off, 0, 2);
+            __builtin_amdgcn_raw_buffer_store_b128(vb, rs.db, off, 0, 2);
+        }
+    };
+
+    if constexpr (SUM) {
+        // every document brings its own second rows: both spectra per document, the
+        // products added up (packed fp16), one inverse for the group into its first
+        // document's rows (rb)
+        uint32_t su[NB][4];
+        u4 sb[NB];
+        for (int k = 0;;) {
+            uint32_t fa[NB][4], fl[NB][4];
+            forward(in.fu, in.fb, fa, flds);
+#pragma unroll
+            for (int kb = 0; kb < NB; ++kb)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) fl[kb][r] = flds[16 * (rbase - 16 * kb - r)];
+            wave_lds_fence();  // the second exchange row is free from here on
+            uint32_t au[NB][4], wu[NB][4];
+            forward(in.xu, in.xb, au, xlds);
+            products(fa, fl, au, wu);
+#pragma unroll
+            for (int jb = 0; jb < NB; ++jb)
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const uint32_t wbv = xlds[16 * (16 * jb + 4 * h + t - shift)];
+                    su[jb][t] = k == 0 ? wu[jb][t] : pk_add(su[jb][t], wu[jb][t]);
+                    sb[jb][t] = k == 0 ? wbv : pk_add(sb[jb][t], wbv);
+                }
+            wave_lds_fence();  // the staging area is free for the next document's rows
+            if (++k == grp.y) break;
+            const RowBuffers rk = row_buffers(grid, grid_pb_stride, fgrid, fgrid_pb_stride,
+                                              segs + docs[grp.x + k], pb, u, ub);
+#pragma unroll
+            for (int jb = 0; jb < NB; ++jb) {
+                const int off = jb * 1024 + lane * 16;
+                lds_copy16(rk.fu, off, stage + 0 * S * 16 + jb * 256);
+                lds_copy16(rk.fb, off, stage + 1 * S * 16 + jb * 256);
+                lds_copy16(rk.du, off, stage + 2 * S * 16 + jb * 256);
+                lds_copy16(rk.db, off, stage + 3 * S * 16 + jb * 256);
+            }
+            __builtin_amdgcn_s_waitcnt(0);  // the copies have landed in LDS
+            if (pad) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    *reinterpret_cast<u4*>(stage + r * S * 16 + (NB - 1) * 256 + lane * 4) = u4{0u, 0u, 0u, 0u};
+            }
+            wave_lds_fence();
+#pragma unroll
+            for (int jb = 0; jb < NB; ++jb)
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const int e = (16 * jb + 4 * t + h) * 16 + p;
+                    in.fu[jb][t] = stage[0 * S * 16 + e];
+                    in.fb[jb][t] = stage[1 * S * 16 + e];
+                    in.xu[jb][t] = stage[2 * S * 16 + e];
+                    in.xb[jb][t] = stage[3 * S * 16 + e];
+                }
+            wave_lds_fence();
+        }
+        inverse_store(su, sb, rb);
+        return;
+    }
+
     // the filter rows, once per group: own spectrum in registers, and the partner
     // values at the slots the product reads gathered from the exchange row
     uint32_t fa[NB][4], fl[NB][4];
@@ -317,25 +443,7 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
         forward(in.xu, in.xb, au, xlds);
 
         uint32_t wu[NB][4];
-#pragma unroll
-        for (int kb = 0; kb < NB; ++kb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int slot = rbase - 16 * kb - r;  // >= -15: inside the zeroed front slots
-                const uint32_t b = xlds[16 * slot];
-                const uint32_t a = au[kb][r];
-                // correlation: the filter spectrum read at -f (its conjugate for real taps)
-                const uint32_t A = corr ? fl[kb][r] : fa[kb][r];
-                const uint32_t bf = corr ? fa[kb][r] : fl[kb][r];
-                const uint32_t e1 = pk_add_conj(a, b);
-                const uint32_t e2 = pk_swap_add_conj(a, b);
-                const uint32_t U = pk_add_neg_hi(e1, e2);
-                const uint32_t V = pk_add_neg_lo(e1, e2);
-                wu[kb][r] = w_pos(A, bf, U, V);
-                xlds[16 * slot] = w_neg(A, bf, U, V);
-            }
-        if (shift && h == 0) xlds[-16] = xlds[16 * (m - 1)];
-        wave_lds_fence();
+        products(fa, fl, au, wu);
 
         u4 wb[NB];
 #pragma unroll
@@ -344,40 +452,7 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
             for (int t = 0; t < 4; ++t) wb[jb][t] = xlds[16 * (16 * jb + 4 * h + t - shift)];
         wave_lds_fence();
 
-        // inverse DFT of both rows into LDS rows 0 and 1 as [row][point][16 pairs],
-        // then 16-byte stores
-        uint32_t* out = stage;
-#pragma unroll
-        for (int kb = 0; kb < NB; ++kb) {
-            f4 acc[2][2];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-            for (int jb = 0; jb < NB; ++jb) {
-                const u4 are = inv[((kb * NB + jb) * 2) * 64 + lane];
-                const u4 aim = inv[((kb * NB + jb) * 2 + 1) * 64 + lane];
-                const u4 win = {wu[jb][0], wu[jb][1], wu[jb][2], wu[jb][3]};
-                acc[0][0] = mma(are, win, acc[0][0]);
-                acc[0][1] = mma(aim, win, acc[0][1]);
-                acc[1][0] = mma(are, wb[jb], acc[1][0]);
-                acc[1][1] = mma(aim, wb[jb], acc[1][1]);
-            }
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {  // output register r: time point 16 kb + 4 r + h
-                const int e = (16 * kb + 4 * r + h) * 16 + p;
-                out[e] = pack_h2(acc[0][0][r], acc[0][1][r]);
-                out[S * 16 + e] = pack_h2(acc[1][0][r], acc[1][1][r]);
-            }
-        }
-        wave_lds_fence();
-#pragma unroll
-        for (int jb = 0; jb < NB; ++jb) {
-            const int off = jb * 1024 + lane * 16;
-            const u4 vu = *reinterpret_cast<const u4*>(out + jb * 256 + lane * 4);
-            const u4 vb = *reinterpret_cast<const u4*>(out + S * 16 + jb * 256 + lane * 4);
-            __builtin_amdgcn_raw_buffer_store_b128(vu, rb.du, off, 0, 2);
-            __builtin_amdgcn_raw_buffer_store_b128(vb, rb.db, off, 0, 2);
-        }
+        inverse_store(wu, wb, rb);
         if (++k == grp.y) break;
 
         // the next document's rows: the copies were issued before this document's 2 NB
@@ -427,8 +502,17 @@ __device__ __forceinline__ uint32_t mul_neg_i(uint32_t a) {
 __device__ __forceinline__ u4 mul_neg_i4(u4 a) {
     return u4{mul_neg_i(a[0]), mul_neg_i(a[1]), mul_neg_i(a[2]), mul_neg_i(a[3])};
 }
+// The operand that gives the imaginary output part from the input itself: an entry v
+// held as (Re v, -Im v) becomes (Im v, Re v), so that the product with z sums
+// Im v Re z + Re v Im z = Im(v z), as the operand itself does against -i z
+__device__ __forceinline__ uint32_t imag_operand(uint32_t a) {
+    return __builtin_amdgcn_alignbit(a, a, 16) ^ 0x00008000u;
+}
+__device__ __forceinline__ u4 imag_operand4(u4 a) {
+    return u4{imag_operand(a[0]), imag_operand(a[1]), imag_operand(a[2]), imag_operand(a[3])};
+}
 
-template <int NB>
+template <int NB, bool SUM>
 __global__ __launch_bounds__(64 * kPartnerWaves) __attribute__((amdgpu_waves_per_eu(kPartnerMinWaves<NB>, 8)))
 void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
                         const uint32_t* __restrict__ fgrid, int64_t fgrid_pb_stride,
@@ -523,41 +607,31 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
         __builtin_amdgcn_sched_barrier(0);
     };
 
-    // the filter rows, once per group
-    uint32_t fa[NB][4], fp[NB][4];
-    forward(fu, fb, fa, fp, lane);
-
     const u4* inv = tab + kFrag;
-    for (int k = 0;;) {
-        if (!kPrefetch || k > 0) load_rows(rb.du, rb.db, xu, xb);
-        int lk = lane;
-        asm volatile("" : "+v"(lk));
-        uint32_t au[NB][4], ap[NB][4];
-        forward(xu, xb, au, ap, lk);
-
-        // separated products: W(f) for row u, W(-f) for row ub at the slot of f
-        uint32_t wu[NB][4], wp[NB][4];
+    // separated products of one block of four frequencies: W(f) for row u into wu, W(-f)
+    // for row ub at the slot of f into wp (as conj(G), the inverse's input)
+    auto products_block = [&](const uint32_t* fa, const uint32_t* fp, const uint32_t* au,
+                              const uint32_t* ap, uint32_t* wu, uint32_t* wp) {
 #pragma unroll
-        for (int kb = 0; kb < NB; ++kb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const uint32_t a = au[kb][r], b = ap[kb][r];
-                // correlation: the filter spectrum read at -f (its conjugate for real taps)
-                const uint32_t A = corr ? fp[kb][r] : fa[kb][r];
-                const uint32_t Bf = corr ? fa[kb][r] : fp[kb][r];
-                const uint32_t e1 = pk_add_conj(a, b);       // s
-                const uint32_t e2 = pk_swap_add_conj(a, b);  // (Im d, Re d)
-                const uint32_t U = pk_add_neg_hi(e1, e2);    // s - i d
-                const uint32_t V = pk_add_neg_lo(e1, e2);    // s + i d
-                wu[kb][r] = w_pos(A, Bf, U, V);
-                wp[kb][r] = w_neg(A, Bf, U, V) ^ 0x80000000u;  // conj(G), the inverse's input
-            }
-
-        // inverse DFT of row u and of row ub.  A row that is its own partner stores only
-        // the first: the second goes through a buffer resource of no bytes.  The code
-        // has no branch between the matrix products and the reads of their results, so
-        // the compiler's wait states after the products hold on every path.
-        const __amdgpu_buffer_rsrc_t rdb = self ? row_buffer(nullptr, 0) : rb.db;
+        for (int r = 0; r < 4; ++r) {
+            const uint32_t a = au[r], b = ap[r];
+            // correlation: the filter spectrum read at -f (its conjugate for real taps)
+            const uint32_t A = corr ? fp[r] : fa[r];
+            const uint32_t Bf = corr ? fa[r] : fp[r];
+            const uint32_t e1 = pk_add_conj(a, b);       // s
+            const uint32_t e2 = pk_swap_add_conj(a, b);  // (Im d, Re d)
+            const uint32_t U = pk_add_neg_hi(e1, e2);    // s - i d
+            const uint32_t V = pk_add_neg_lo(e1, e2);    // s + i d
+            wu[r] = w_pos(A, Bf, U, V);
+            wp[r] = w_neg(A, Bf, U, V) ^ 0x80000000u;  // conj(G), the inverse's input
+        }
+    };
+    // inverse DFT of row u and of row ub into the rows of rs.  A row that is its own
+    // partner stores only the first: the second goes through a buffer resource of no
+    // bytes.  The code has no branch between the matrix products and the reads of their
+    // results, so the compiler's wait states after the products hold on every path.
+    auto inverse_store = [&](const uint32_t(*wu)[4], const uint32_t(*wp)[4], const RowBuffers& rs, int lk) {
+        const __amdgpu_buffer_rsrc_t rdb = self ? row_buffer(nullptr, 0) : rs.db;
 #pragma unroll
         for (int kb = 0; kb < NB; ++kb) {
             f4 acc[4];
@@ -576,7 +650,7 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
 #pragma unroll
             for (int r = 0; r < 4; ++r) {  // output register r: time point j = 16 kb + 4 r + h
                 const int off = lane_off + (16 * kb + 4 * r) * 64;
-                __builtin_amdgcn_raw_buffer_store_b32(pack_h2(acc[0][r], acc[1][r]), rb.du, off, 0, 2);
+                __builtin_amdgcn_raw_buffer_store_b32(pack_h2(acc[0][r], acc[1][r]), rs.du, off, 0, 2);
                 // w^j conj(R + i I) with w^j = (c, s): (R c + I s, R s - I c)
                 const float2 w = tw_post[16 * kb + 4 * r + (lk >> 4)];
                 const float re = acc[2][r] * w.x + acc[3][r] * w.y;
@@ -584,6 +658,91 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
                 __builtin_amdgcn_raw_buffer_store_b32(pack_h2(re, im), rdb, off, 0, 2);
             }
         }
+    };
+
+    if constexpr (SUM) {
+        // every document brings its own second rows: both spectra per document, the
+        // products added up (packed fp16), one inverse for the group into its first
+        // document's rows.  Block kb of all four spectra is formed and multiplied before
+        // the next, so that only the loaded rows and the sums stay live across blocks.
+        const RowBuffers r0 = rb;
+        uint32_t su[NB][4], sp[NB][4];
+        for (int k = 0;;) {
+            if (!kPrefetch && k == 0) load_rows(rb.du, rb.db, xu, xb);
+            int lk = lane;
+            asm volatile("" : "+v"(lk));
+            // partner inputs conj(z(j) w^(-j)) of both row pairs (row 0: w^0 = 1)
+#pragma unroll
+            for (int jb = 0; jb < NB; ++jb)
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const uint32_t tw = tw_pre[(16 * jb + 4 * t + (lk >> 4)) & pre_mask];
+                    fb[jb][t] = cmul_h2(fb[jb][t], tw) ^ 0x80000000u;
+                    xb[jb][t] = cmul_h2(xb[jb][t], tw) ^ 0x80000000u;
+                }
+#pragma unroll
+            for (int kb = 0; kb < NB; ++kb) {
+                f4 acc[8];  // second rows: own re, im, partner re, im; then the data rows alike
+#pragma unroll
+                for (int i = 0; i < 8; ++i) acc[i] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int jb = 0; jb < NB; ++jb) {
+                    // the imaginary parts through the rotated operand: no -i copies of the
+                    // four loaded rows stay live across blocks
+                    const u4 a = tab[(kb * NB + jb) * 64 + lk];
+                    const u4 ai = imag_operand4(a);
+                    acc[0] = mma(a, fu[jb], acc[0]);
+                    acc[1] = mma(ai, fu[jb], acc[1]);
+                    acc[2] = mma(a, fb[jb], acc[2]);
+                    acc[3] = mma(ai, fb[jb], acc[3]);
+                    acc[4] = mma(a, xu[jb], acc[4]);
+                    acc[5] = mma(ai, xu[jb], acc[5]);
+                    acc[6] = mma(a, xb[jb], acc[6]);
+                    acc[7] = mma(ai, xb[jb], acc[7]);
+                }
+                uint32_t fa[1][4], fp[1][4], au[1][4], ap[1][4], wu[1][4], wp[1][4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    fa[0][r] = pack_h2(acc[0][r], acc[1][r]);
+                    fp[0][r] = pack_h2(acc[2][r], -acc[3][r]);
+                    au[0][r] = pack_h2(acc[4][r], acc[5][r]);
+                    ap[0][r] = pack_h2(acc[6][r], -acc[7][r]);
+                }
+                products_block(fa[0], fp[0], au[0], ap[0], wu[0], wp[0]);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    su[kb][r] = k == 0 ? wu[0][r] : pk_add(su[kb][r], wu[0][r]);
+                    sp[kb][r] = k == 0 ? wp[0][r] : pk_add(sp[kb][r], wp[0][r]);
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            if (++k == grp.y) break;
+            rb = row_buffers(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs + docs[grp.x + k], pb, u, ub);
+            load_rows(rb.fu, rb.fb, fu, fb);
+            load_rows(rb.du, rb.db, xu, xb);
+        }
+        int lk = lane;
+        asm volatile("" : "+v"(lk));
+        inverse_store(su, sp, r0, lk);
+        return;
+    }
+
+    // the filter rows, once per group
+    uint32_t fa[NB][4], fp[NB][4];
+    forward(fu, fb, fa, fp, lane);
+
+    for (int k = 0;;) {
+        if (!kPrefetch || k > 0) load_rows(rb.du, rb.db, xu, xb);
+        int lk = lane;
+        asm volatile("" : "+v"(lk));
+        uint32_t au[NB][4], ap[NB][4];
+        forward(xu, xb, au, ap, lk);
+
+        // separated products: W(f) for row u, W(-f) for row ub at the slot of f
+        uint32_t wu[NB][4], wp[NB][4];
+#pragma unroll
+        for (int kb = 0; kb < NB; ++kb) products_block(fa[kb], fp[kb], au[kb], ap[kb], wu[kb], wp[kb]);
+        inverse_store(wu, wp, rb, lk);
         if (++k == grp.y) break;
         rb = row_buffers(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs + docs[grp.x + k], pb, u, ub);
     }
@@ -766,24 +925,34 @@ __global__ __launch_bounds__(64 * kBatchWaves) void row_batch_kernel(uint32_t* _
 template <int NB>
 hipError_t launch_lds_nb(void* grid, int64_t gs, const void* fgrid, int64_t fs, const Seg* segs,
                          const int32_t* docs, const int32_t* groups, int ngroups, const void* tabs,
-                         int n1, int npb, int corr, hipStream_t stream) {
+                         int n1, int npb, int corr, hipStream_t stream, bool sum) {
     const int ug = (n1 / 2 + 1 + kLdsWaves - 1) / kLdsWaves;
     const dim3 g(ngroups * ug, npb), b(64 * kLdsWaves);
-    hipLaunchKernelGGL((row_lds_kernel<NB>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
-                       static_cast<const uint32_t*>(fgrid), fs, segs, docs,
-                       reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr);
+    if (sum)
+        hipLaunchKernelGGL((row_lds_kernel<NB, true>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
+                           static_cast<const uint32_t*>(fgrid), fs, segs, docs,
+                           reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr);
+    else
+        hipLaunchKernelGGL((row_lds_kernel<NB, false>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
+                           static_cast<const uint32_t*>(fgrid), fs, segs, docs,
+                           reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr);
     return hipGetLastError();
 }
 
 template <int NB>
 hipError_t launch_partner_nb(void* grid, int64_t gs, const void* fgrid, int64_t fs, const Seg* segs,
                              const int32_t* docs, const int32_t* groups, int ngroups,
-                             const void* tabs, int n1, int npb, int corr, hipStream_t stream) {
+                             const void* tabs, int n1, int npb, int corr, hipStream_t stream, bool sum) {
     const int ug = (n1 / 2 + 1 + kPartnerWaves - 1) / kPartnerWaves;
     const dim3 g(ngroups * ug, npb), b(64 * kPartnerWaves);
-    hipLaunchKernelGGL((row_partner_kernel<NB>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
-                       static_cast<const uint32_t*>(fgrid), fs, segs, docs,
-                       reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr);
+    if (sum)
+        hipLaunchKernelGGL((row_partner_kernel<NB, true>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
+                           static_cast<const uint32_t*>(fgrid), fs, segs, docs,
+                           reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr);
+    else
+        hipLaunchKernelGGL((row_partner_kernel<NB, false>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
+                           static_cast<const uint32_t*>(fgrid), fs, segs, docs,
+                           reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr);
     return hipGetLastError();
 }
 
@@ -805,9 +974,9 @@ hipError_t launch_row_batch(void* grid, int64_t grid_pb_stride, const void* fgri
 hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const void* fgrid,
                             int64_t fgrid_pb_stride, const Seg* segs, const int32_t* docs,
                             const int32_t* groups, int ngroups, const void* tabs, int n1, int npb,
-                            int corr, hipStream_t stream) {
+                            int corr, hipStream_t stream, bool sum) {
     if (ngroups == 0) return hipSuccess;
-#define RUBICONV_ARGS grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, docs, groups, ngroups, tabs, n1, npb, corr, stream
+#define RUBICONV_ARGS grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, docs, groups, ngroups, tabs, n1, npb, corr, stream, sum
     switch (nb) {
         case 1: return launch_lds_nb<1>(RUBICONV_ARGS);
         case 2: return launch_lds_nb<2>(RUBICONV_ARGS);

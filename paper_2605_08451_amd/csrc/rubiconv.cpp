@@ -37,6 +37,8 @@ struct rubiconv_plan_s {
     const void* dense_tab = nullptr; // matrix-core row pass operands (inside dev)
     const int32_t* dense_docs = nullptr;  // documents by 16-point block count (inside dev)
     const int32_t* dense_groups = nullptr;  // row-task groups of dense_docs (inside dev)
+    const int32_t* dense_sdocs = nullptr;   // filter gradient: sum-group documents (inside dev)
+    const int32_t* dense_sgroups = nullptr; //   their groups
     const Seg* lr_segs = nullptr;           // long rows: sub-row documents (inside dev)
     const Seg* lr_gsegs = nullptr;          //   the same, second rows their own (filter gradient)
     const int32_t* lr_idx = nullptr;        //   identity indices
@@ -57,8 +59,9 @@ struct rubiconv_plan_s {
     LaunchTables doc_t{};
     LaunchTables cls_t{};
     LaunchTables grad_t{};       // doc_t with each document's "filter" rows at its own grid rows
+    LaunchTables dk_t{};         // grad_t restricted to the filter gradient's output documents
+    const Seg* dk_sum_segs = nullptr;  // those and the direct documents, longest first (lag sum)
     const Seg* direct_segs = nullptr;  // documents of the direct path
-    const Seg* all_segs = nullptr;     // every document, longest first (the filter gradient's sum)
     size_t dtaps_off = 0;        // spectrum: the direct path's taps [direct_taps][D] fp32
     size_t sscale_off = 0;       // spectrum: the filter's range scales, float2 per channel pair
     size_t partials_off = 0;     // filter call's workspace: |k| sums per tap tile and channel
@@ -100,7 +103,6 @@ rubiconv_status_t upload(rubiconv_plan_s* pl, hipStream_t stream) {
     const size_t o_segs = off;       off = align_up(off + n_segs * sizeof(Seg));
     const size_t o_gsegs = off;      off = align_up(off + h.docs.size() * sizeof(Seg));
     const size_t o_dsegs = off;      off = align_up(off + h.direct_docs.size() * sizeof(Seg));
-    const size_t o_asegs = off;      off = align_up(off + h.all_docs.size() * sizeof(Seg));
     const size_t o_dcol = off;       off = align_up(off + h.doc_col_seg.size() * 4);
     const size_t o_dtask = off;      off = align_up(off + h.doc_task_seg.size() * 4);
     const size_t o_ccol = off;       off = align_up(off + h.cls_col_seg.size() * 4);
@@ -112,6 +114,11 @@ rubiconv_status_t upload(rubiconv_plan_s* pl, hipStream_t stream) {
     const size_t o_dt = off;         off = align_up(off + h.dense_tab.size() * 4);
     const size_t o_dd = off;         off = align_up(off + h.dense_docs.size() * 4);
     const size_t o_dg = off;         off = align_up(off + h.dense_groups.size() * 4);
+    const size_t o_sd = off;         off = align_up(off + h.dense_sdocs.size() * 4);
+    const size_t o_sg = off;         off = align_up(off + h.dense_sgroups.size() * 4);
+    const size_t o_ksegs = off;      off = align_up(off + h.dk_segs.size() * sizeof(Seg));
+    const size_t o_kcol = off;       off = align_up(off + h.dk_col_seg.size() * 4);
+    const size_t o_ksum = off;       off = align_up(off + h.dk_sum_segs.size() * sizeof(Seg));
     const size_t o_ls = off;         off = align_up(off + h.lr_segs.size() * sizeof(Seg));
     const size_t o_lg = off;         off = align_up(off + h.lr_gsegs.size() * sizeof(Seg));
     const size_t o_li = off;         off = align_up(off + h.lr_idx.size() * 4);
@@ -129,12 +136,6 @@ rubiconv_status_t upload(rubiconv_plan_s* pl, hipStream_t stream) {
     std::memcpy(img.data() + o_segs, segs.data(), n_segs * sizeof(Seg));
     if (!h.direct_docs.empty())
         std::memcpy(img.data() + o_dsegs, h.direct_docs.data(), h.direct_docs.size() * sizeof(Seg));
-    if (!h.all_docs.empty()) {  // longest first, ties in table order (the lag sum's order)
-        std::vector<Seg> by_len(h.all_docs);
-        std::stable_sort(by_len.begin(), by_len.end(),
-                         [](const Seg& a, const Seg& b) { return a.len > b.len; });
-        std::memcpy(img.data() + o_asegs, by_len.data(), by_len.size() * sizeof(Seg));
-    }
     {  // filter gradient: the second operand of a document's row stage is its own x grid
         std::vector<Seg> gsegs(h.docs);
         for (Seg& g : gsegs) g.spec_off = static_cast<int32_t>(g.grid_off);
@@ -152,6 +153,16 @@ rubiconv_status_t upload(rubiconv_plan_s* pl, hipStream_t stream) {
     if (!h.dense_docs.empty()) std::memcpy(img.data() + o_dd, h.dense_docs.data(), h.dense_docs.size() * 4);
     if (!h.dense_groups.empty())
         std::memcpy(img.data() + o_dg, h.dense_groups.data(), h.dense_groups.size() * 4);
+    if (!h.dense_sdocs.empty()) {
+        std::memcpy(img.data() + o_sd, h.dense_sdocs.data(), h.dense_sdocs.size() * 4);
+        std::memcpy(img.data() + o_sg, h.dense_sgroups.data(), h.dense_sgroups.size() * 4);
+    }
+    if (!h.dk_segs.empty()) {
+        std::memcpy(img.data() + o_ksegs, h.dk_segs.data(), h.dk_segs.size() * sizeof(Seg));
+        std::memcpy(img.data() + o_kcol, h.dk_col_seg.data(), h.dk_col_seg.size() * 4);
+    }
+    if (!h.dk_sum_segs.empty())
+        std::memcpy(img.data() + o_ksum, h.dk_sum_segs.data(), h.dk_sum_segs.size() * sizeof(Seg));
     {
         std::vector<float> ones(2 * n_ones, 1.0f);
         std::memcpy(img.data() + o_one, ones.data(), ones.size() * sizeof(float));
@@ -191,9 +202,12 @@ rubiconv_status_t upload(rubiconv_plan_s* pl, hipStream_t stream) {
                              reinterpret_cast<const int32_t*>(base + o_dtask), tw, twn,
                              reinterpret_cast<const int32_t*>(base + o_cdoc)};
     pl->direct_segs = reinterpret_cast<const Seg*>(base + o_dsegs);
-    pl->all_segs = reinterpret_cast<const Seg*>(base + o_asegs);
     pl->grad_t = pl->doc_t;
     pl->grad_t.segs = reinterpret_cast<const Seg*>(base + o_gsegs);
+    pl->dk_t = pl->grad_t;
+    pl->dk_t.segs = reinterpret_cast<const Seg*>(base + o_ksegs);
+    pl->dk_t.col_seg = reinterpret_cast<const int32_t*>(base + o_kcol);
+    pl->dk_sum_segs = reinterpret_cast<const Seg*>(base + o_ksum);
     pl->cls_t = LaunchTables{dsegs + h.docs.size(), reinterpret_cast<const int32_t*>(base + o_ccol),
                              nullptr, tw, twn,
                              reinterpret_cast<const int32_t*>(base + o_cid)};
@@ -201,6 +215,8 @@ rubiconv_status_t upload(rubiconv_plan_s* pl, hipStream_t stream) {
     pl->dense_tab = base + o_dt;
     pl->dense_docs = reinterpret_cast<const int32_t*>(base + o_dd);
     pl->dense_groups = reinterpret_cast<const int32_t*>(base + o_dg);
+    pl->dense_sdocs = reinterpret_cast<const int32_t*>(base + o_sd);
+    pl->dense_sgroups = reinterpret_cast<const int32_t*>(base + o_sg);
     pl->lr_segs = reinterpret_cast<const Seg*>(base + o_ls);
     pl->lr_gsegs = reinterpret_cast<const Seg*>(base + o_lg);
     pl->lr_idx = reinterpret_cast<const int32_t*>(base + o_li);
@@ -400,15 +416,16 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
         if (m > rubiconv::kMaxFastM || (h.row_dense && m <= 16 * rubiconv::kMaxDenseBlocks)) continue;
         launches.push_back({static_cast<int>(c), 0, static_cast<double>(m) * h.classes[c].nlist, false});
     }
+    // own_rows (the filter gradient): the sum groups, every matrix-core row size included
     if (h.row_dense)
         for (int nb = 1; nb <= rubiconv::kMaxDenseBlocks; ++nb) {
             if (h.dense_count[nb] == 0) continue;
             double w = 0;
             for (int k = 0; k < h.dense_count[nb]; ++k) w += h.docs[h.dense_docs[h.dense_list0[nb] + k]].m;
-            if (nb == 1) w -= h.dense_bwork;
-            if ((own_rows ? h.dense_dgrp_n[nb] : h.dense_grp_n[nb]) > 0) launches.push_back({-1, nb, w, false});
+            if (nb == 1 && !own_rows) w -= h.dense_bwork;
+            if ((own_rows ? h.dense_sgrp_n[nb] : h.dense_grp_n[nb]) > 0) launches.push_back({-1, nb, w, false});
         }
-    if (h.row_dense && h.dense_bgrp_n > 0) launches.push_back({-1, 1, h.dense_bwork, true});
+    if (h.row_dense && h.dense_bgrp_n > 0 && !own_rows) launches.push_back({-1, 1, h.dense_bwork, true});
     for (size_t k = 0; k < h.lr_launches.size(); ++k)
         launches.push_back({-1, h.lr_launches[k].nb, h.lr_launches[k].work, false, static_cast<int>(k)});
     std::sort(launches.begin(), launches.end(),
@@ -427,11 +444,15 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
             return rubiconv::launch_row_batch(grid, plan->grid_pb_stride, fgrid, fgrid_pb_stride, t.segs,
                                               plan->dense_docs, plan->dense_groups + 2 * h.dense_bgrp0,
                                               h.dense_bgrp_n, plan->dense_tab, h.n1, h.npb, corr, s);
+        if (L.nb > 0 && own_rows)
+            return rubiconv::launch_row_dense(
+                L.nb, grid, plan->grid_pb_stride, fgrid, fgrid_pb_stride, t.segs, plan->dense_sdocs,
+                plan->dense_sgroups + 2 * h.dense_sgrp0[L.nb], h.dense_sgrp_n[L.nb], plan->dense_tab, h.n1,
+                h.npb, corr, s, true);
         if (L.nb > 0)
             return rubiconv::launch_row_dense(
                 L.nb, grid, plan->grid_pb_stride, fgrid, fgrid_pb_stride, t.segs, plan->dense_docs,
-                plan->dense_groups + 2 * (own_rows ? h.dense_dgrp0[L.nb] : h.dense_grp0[L.nb]),
-                own_rows ? h.dense_dgrp_n[L.nb] : h.dense_grp_n[L.nb], plan->dense_tab, h.n1, h.npb,
+                plan->dense_groups + 2 * h.dense_grp0[L.nb], h.dense_grp_n[L.nb], plan->dense_tab, h.n1, h.npb,
                 corr, s);
         if (L.cls < 0)
             return rubiconv::launch_row_conv(h.n1, half, grid, plan->grid_pb_stride, fgrid,
@@ -467,13 +488,17 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
             e = rubiconv::launch_lr_step(true, grid, plan->grid_pb_stride, it, plan->doc_t.tw, h.n1,
                                          h.npb, stream);
     rec.mark(stage(tag, "row_conv"));
+    // the filter gradient transforms back its output documents only (the sum groups'
+    // followers have added their products to their leaders' rows)
+    const LaunchTables& inv_t = own_rows ? plan->dk_t : plan->doc_t;
+    const int inv_cols = own_rows ? static_cast<int>(h.dk_col_seg.size()) : n_cols;
     if (e == hipSuccess)
         e = h.col_mfma ? rubiconv::launch_col_inv_mfma(out_dtype, grid, plan->grid_pb_stride, out,
-                                                       rs, h.D, plan->doc_t, out_sc, plan->mfma_tab,
-                                                       n_cols, h.npb, stream)
+                                                       rs, h.D, inv_t, out_sc, plan->mfma_tab,
+                                                       inv_cols, h.npb, stream)
                        : rubiconv::launch_col_inv(h.r, half, out_dtype, grid,
-                                                  plan->grid_pb_stride, out, rs, h.D, plan->doc_t,
-                                                  out_sc, n_cols, h.npb, stream);
+                                                  plan->grid_pb_stride, out, rs, h.D, inv_t,
+                                                  out_sc, inv_cols, h.npb, stream);
     rec.mark(stage(tag, "col_inv"));
     return e;
 }
@@ -825,8 +850,8 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
                          stream, rec, speculative ? &spec_dy : nullptr);
     if (e == hipSuccess && direct) e = join_direct(plan, stream, rec);
     if (e == hipSuccess)
-        e = rubiconv::launch_lag_sum(r, plan->all_segs, static_cast<int>(h.all_docs.size()), h.N, h.D,
-                                     h.L, dk, stream);
+        e = rubiconv::launch_lag_sum(r, plan->dk_sum_segs, static_cast<int>(h.dk_sum_segs.size()), h.N,
+                                     h.D, h.L, dk, stream);
     rec.mark("dk_lag_sum");
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }

@@ -216,6 +216,31 @@ def test_class_groups(device):
     _check_dk(f64(dk), oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L, threads=ORACLE_THREADS), "bf16", "dk")
 
 
+@pytest.mark.parametrize("D", [32, 64])
+def test_filter_gradient_sum_groups(device, D):
+    """The filter gradient adds the correlation products of a size class's documents
+    (up to eight, longest first) before one inverse transform: classes whose documents
+    differ in length, with the longest neither first nor last in its row, classes of
+    more than eight documents (several groups), a class of one document, short rows
+    (8-16 points) and partner-kernel rows (33-128 points); every lag of dk against the
+    oracle, per channel."""
+    N = 12000
+    rows = [[930, 1000, 960, 880, 990, 940, 905, 870, 1000, 975, N - 9450],
+            [3000, 3100, 2950, 2900, N - 11950],
+            [430, 500, 470, 450, 500, 420, 480, 460, 440, 490, N - 4640],
+            [6000, N - 6000]]
+    W = wl.make_case(rows, D=D, L=N, x_dtype="bf16", seed=D + 3)
+    dyv, dx, dk, plan = _run(W, device, seed=D + 4)
+    t = plan.doc_table()
+    ms = [int(v) for v in t[:, 4]]
+    assert max(ms.count(m) for m in set(ms)) > 8 and max(ms) > 32, ms
+    g, worst = _check_dk(dk, oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L, threads=ORACLE_THREADS), "bf16",
+                         f"D={D}")
+    _say(f"[dk sum groups] D={D}: global {g:.2e}, worst channel {worst:.2e}")
+    assert_parity(dx, oracle.grad_x(W.filters, dyv, W.cu_seqlens, threads=ORACLE_THREADS),
+                  W.cu_seqlens, "bf16", f"dx D={D}")
+
+
 @pytest.mark.parametrize("rows", [[[200] * 10 + [48]], [[200, 200, 1648]], [[200, 1848]],
                                   [[600] * 3 + [248]], [[100] * 20 + [48]]])
 def test_batched_short_rows(device, rows, monkeypatch):
