@@ -1055,19 +1055,29 @@ __global__ __launch_bounds__(256) void filter_scale_kernel(const float* __restri
     __shared__ float part[4][4];
     const int c = threadIdx.x & 3, r = threadIdx.x >> 2;
     const int d = blockIdx.x * 4 + c;
-    float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
+    // sixteen loads in flight per lane while at least 16 rounds of tiles remain (long
+    // filters have thousands of tiles per channel), then four, then one
+    float acc[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) acc[u] = 0.0f;
     if (d < D) {
         int t = r;
-        for (; t + 192 < ntiles; t += 256) {
-            a0 += partials[static_cast<int64_t>(t) * D + d];
-            a1 += partials[static_cast<int64_t>(t + 64) * D + d];
-            a2 += partials[static_cast<int64_t>(t + 128) * D + d];
-            a3 += partials[static_cast<int64_t>(t + 192) * D + d];
+        for (; t + 15 * 64 < ntiles; t += 16 * 64) {
+#pragma unroll
+            for (int u = 0; u < 16; ++u) acc[u] += partials[static_cast<int64_t>(t + 64 * u) * D + d];
         }
-        for (; t < ntiles; t += 64) a0 += partials[static_cast<int64_t>(t) * D + d];
+        for (; t + 3 * 64 < ntiles; t += 4 * 64) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) acc[u] += partials[static_cast<int64_t>(t + 64 * u) * D + d];
+        }
+        for (; t < ntiles; t += 64) acc[0] += partials[static_cast<int64_t>(t) * D + d];
     }
+#pragma unroll
+    for (int w = 8; w > 0; w >>= 1)
+#pragma unroll
+        for (int u = 0; u < w; ++u) acc[u] += acc[u + w];
     // the 16 partial sums of each channel in a wave (lanes c, c + 4, ...), then the four waves
-    float a = (a0 + a1) + (a2 + a3);
+    float a = acc[0];
 #pragma unroll
     for (int o = 4; o < 64; o <<= 1) a += __shfl_xor(a, o);
     if ((threadIdx.x & 63) < 4) part[threadIdx.x >> 6][c] = a;
