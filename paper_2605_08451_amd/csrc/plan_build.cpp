@@ -600,10 +600,7 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
                     const int cnt = n / ng + (g < n % ng ? 1 : 0);
                     p.dense_sgroups.push_back(static_cast<int32_t>(p.dense_sdocs.size()));
                     p.dense_sgroups.push_back(cnt);
-                    for (int q = 0; q < cnt; ++q) {
-                        p.dense_sdocs.push_back(mem[first + q]);
-                        p.dense_swork[nb] += p.docs[mem[first + q]].m;
-                    }
+                    for (int q = 0; q < cnt; ++q) p.dense_sdocs.push_back(mem[first + q]);
                     first += cnt;
                 }
             }

@@ -56,7 +56,6 @@ struct HostPlan {
     std::vector<int32_t> dense_sgroups;
     int32_t dense_sgrp0[kMaxDenseBlocks + 1] = {};  // sum groups of block count nb (pair index)
     int32_t dense_sgrp_n[kMaxDenseBlocks + 1] = {};
-    double dense_swork[kMaxDenseBlocks + 1] = {};   // their summed row sizes
     // filter gradient outputs: the documents whose rows hold correlations after the row
     // pass (sum-group leaders and every document outside the sum groups), as copies of
     // their segments with the second rows their own and columns renumbered (dk_segs,
