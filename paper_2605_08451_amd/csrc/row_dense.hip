@@ -772,8 +772,13 @@ __global__ __launch_bounds__(64 * kBatchWaves) void row_batch_kernel(uint32_t* _
                                                                     int corr) {
     constexpr int kTabU4 = 4 * 64;                   // one table set: forward then inverse
     constexpr uint32_t kNone = 0xffffffffu;          // an offset outside every buffer
+    constexpr int kGroupCap = kMaxGroupDocs * 16;    // documents of a group (16 / m per block)
     __shared__ u4 tab[2 * kTabU4];                   // plain tables, then block-diagonal ones
     __shared__ uint32_t xch_all[kBatchWaves][2 * (kPad + 16) * 16];
+    // the group's grid and second-grid offsets, read once per workgroup, so that a lane
+    // finds its document's rows in LDS rather than through two dependent global loads
+    __shared__ int64_t g_off[kGroupCap];
+    __shared__ int32_t s_off[kGroupCap];
 
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
     const int lane = threadIdx.x & 63;
@@ -789,8 +794,14 @@ __global__ __launch_bounds__(64 * kBatchWaves) void row_batch_kernel(uint32_t* _
         const __amdgpu_buffer_rsrc_t rt = row_buffer(tabs + segs[docs[grp.x]].dense_off, 2 * kTabU4 * 16);
         for (int c = wave; c < 2 * kTabU4 / 64; c += kBatchWaves) lds_copy16(rt, c * 1024 + lane * 16, &tab[c * 64]);
     }
+    const int ndocs = min(grp.y, kGroupCap);  // the plan's groups hold at most kGroupCap
+    for (int i = static_cast<int>(threadIdx.x); i < ndocs; i += 64 * kBatchWaves) {
+        const Seg& sg = segs[docs[grp.x + i]];
+        g_off[i] = sg.grid_off;
+        s_off[i] = sg.spec_off;
+    }
     __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();  // tables visible to every wave; the only workgroup barrier
+    __syncthreads();  // tables and offsets visible to every wave; the only workgroup barrier
     if (!active) return;
 
     const int ub = u == 0 ? 0 : n1 - u;  // n1 need not be a power of two (sub-row documents)
@@ -845,8 +856,8 @@ __global__ __launch_bounds__(64 * kBatchWaves) void row_batch_kernel(uint32_t* _
         pslot[r] = q < R ? (2 * q + 1) * m - 1 - v : -kPad;
     }
 
-    for (int k0 = 0; k0 < grp.y; k0 += R) {
-        const int nr = min(R, grp.y - k0);  // documents in this block
+    for (int k0 = 0; k0 < ndocs; k0 += R) {
+        const int nr = min(R, ndocs - k0);  // documents in this block
         // register t holds time slot 4 t + h: point j of document q
         uint32_t o_du[4], o_db[4], o_fu[4], o_fb[4];
 #pragma unroll
@@ -854,12 +865,12 @@ __global__ __launch_bounds__(64 * kBatchWaves) void row_batch_kernel(uint32_t* _
             const int v = 4 * t + h, q = v / m, j = v - q * m;
             o_du[t] = o_db[t] = o_fu[t] = o_fb[t] = kNone;
             if (q < nr) {
-                const Seg& sg = segs[docs[grp.x + k0 + q]];
+                const int64_t goff = g_off[k0 + q], soff = s_off[k0 + q];
                 const uint32_t pbyte = static_cast<uint32_t>(p) * 4;
-                o_du[t] = static_cast<uint32_t>((sg.grid_off + static_cast<int64_t>(u) * m + j) * 64) + pbyte;
-                o_db[t] = static_cast<uint32_t>((sg.grid_off + static_cast<int64_t>(ub) * m + j) * 64) + pbyte;
-                o_fu[t] = static_cast<uint32_t>((static_cast<int64_t>(sg.spec_off) + static_cast<int64_t>(u) * m + j) * 64) + pbyte;
-                o_fb[t] = static_cast<uint32_t>((static_cast<int64_t>(sg.spec_off) + static_cast<int64_t>(ub) * m + j) * 64) + pbyte;
+                o_du[t] = static_cast<uint32_t>((goff + static_cast<int64_t>(u) * m + j) * 64) + pbyte;
+                o_db[t] = static_cast<uint32_t>((goff + static_cast<int64_t>(ub) * m + j) * 64) + pbyte;
+                o_fu[t] = static_cast<uint32_t>((soff + static_cast<int64_t>(u) * m + j) * 64) + pbyte;
+                o_fb[t] = static_cast<uint32_t>((soff + static_cast<int64_t>(ub) * m + j) * 64) + pbyte;
             }
         }
         u4 fu, fb, xu, xb;
