@@ -81,10 +81,12 @@ hipError_t launch_row_fast(int m, bool half, void* grid, int64_t grid_pb_stride,
 // sum: every document of a group brings its own second-grid rows, the products of
 // the group's documents are added, and the one inverse transform of the sum is written
 // over the first document's rows (the others are left as they were).
-// 16-byte entries of one class's tables for the rows of 3 to 8 blocks: per direction
-// nb * nb real operands of 64 lanes, then 16 nb complex fp16 twiddles w^(-j) and
-// 16 nb complex fp32 twiddles w^j (w = exp(-2 pi i / m)), padded to whole 1 KB chunks.
-constexpr int partner_tab_u4(int nb) { return (2 * nb * nb * 64 + 12 * nb + 63) / 64 * 64; }
+// 16-byte entries of one class's tables for the rows of 3 to 8 blocks: nb * nb real
+// operands of 64 lanes (the forward transform; the inverse takes their conjugates),
+// then 16 nb complex fp16 twiddles w^(-j), 16 nb complex fp32 twiddles kappa w^j
+// (w = exp(-2 pi i / m)) and kappa (fp32; the inverse's scale over the forward's),
+// padded to whole 1 KB chunks.
+constexpr int partner_tab_u4(int nb) { return (nb * nb * 64 + 12 * nb + 1 + 63) / 64 * 64; }
 
 hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const void* fgrid,
                             int64_t fgrid_pb_stride, const Seg* segs, const int32_t* docs,

@@ -233,44 +233,44 @@ void make_partner_tables(int m, int n1, std::vector<uint32_t>* out) {
     const int nb = (m + 15) / 16, S = 16 * nb;
     const double fwd_scale = 1.0 / std::sqrt(static_cast<double>(m));
     const double inv_scale = std::sqrt(static_cast<double>(n1)) / 4.0;
+    // the inverse operands are kappa times the conjugates of the forward ones
+    const double kappa = inv_scale / fwd_scale;
     const std::vector<std::complex<double>> z = unit_circle(m);  // exp(-2 pi i e / m)
     const size_t start = out->size();
     // one real operand per 16 x 16 block: lane (row, q) holds entries (row, 4 q + c) as
     // (Re, -Im) pairs, c = 0..3; the imaginary output part comes from the same operand
-    // applied to -i times the input
-    auto push_re = [out](auto entry) {
-        for (int lane = 0; lane < 64; ++lane)
-            for (int c = 0; c < 4; ++c) {
-                const std::complex<double> v = entry(lane % 16, 4 * (lane / 16) + c);
-                out->push_back(to_f16_bits(v.real()) |
-                               (static_cast<uint32_t>(to_f16_bits(-v.imag())) << 16));
-            }
-    };
-    for (int dir = 0; dir < 2; ++dir)
-        for (int kb = 0; kb < nb; ++kb)
-            for (int jb = 0; jb < nb; ++jb)
-                push_re([=](int row, int n) {
-                    const int k = dir == 0 ? 16 * kb + row : 16 * jb + n;              // frequency
-                    const int j = dir == 0 ? 16 * jb + interleave(n) : 16 * kb + interleave(row);  // time
-                    if (k >= m || j >= m) return std::complex<double>(0.0, 0.0);
-                    const std::complex<double> w = z[(static_cast<int64_t>(k) * j) % m];
-                    return dir == 0 ? w * fwd_scale : std::conj(w) * inv_scale;
-                });
-    // partner-row twiddles: exp(+2 pi i j / m) as complex fp16, then exp(-2 pi i j / m)
-    // as complex fp32, for time points j < S (zero past m)
+    // applied to -i times the input.  Frequencies are interleaved like the time points,
+    // so that block (kb, jb) is symmetric in its two axes and its conjugate is block
+    // (kb, jb) of the inverse transform
+    for (int kb = 0; kb < nb; ++kb)
+        for (int jb = 0; jb < nb; ++jb)
+            for (int lane = 0; lane < 64; ++lane)
+                for (int c = 0; c < 4; ++c) {
+                    const int k = 16 * kb + interleave(lane % 16);            // frequency
+                    const int j = 16 * jb + interleave(4 * (lane / 16) + c);  // time
+                    std::complex<double> v(0.0, 0.0);
+                    if (k < m && j < m) v = z[(static_cast<int64_t>(k) * j) % m] * fwd_scale;
+                    out->push_back(to_f16_bits(v.real()) |
+                                   (static_cast<uint32_t>(to_f16_bits(-v.imag())) << 16));
+                }
+    // partner-row twiddles: exp(+2 pi i j / m) as complex fp16, then kappa exp(-2 pi i j / m)
+    // as complex fp32, for time points j < S (zero past m), then kappa itself (fp32)
     for (int j = 0; j < S; ++j) {
         const std::complex<double> w = j < m ? std::conj(z[j]) : std::complex<double>(0.0, 0.0);
         out->push_back(to_f16_bits(w.real()) | (static_cast<uint32_t>(to_f16_bits(w.imag())) << 16));
     }
+    auto push_f32 = [out](double v) {
+        const float f = static_cast<float>(v);
+        uint32_t b;
+        std::memcpy(&b, &f, 4);
+        out->push_back(b);
+    };
     for (int j = 0; j < S; ++j) {
-        const std::complex<double> w = j < m ? z[j] : std::complex<double>(0.0, 0.0);
-        const float re = static_cast<float>(w.real()), im = static_cast<float>(w.imag());
-        uint32_t b[2];
-        std::memcpy(&b[0], &re, 4);
-        std::memcpy(&b[1], &im, 4);
-        out->push_back(b[0]);
-        out->push_back(b[1]);
+        const std::complex<double> w = j < m ? z[j] * kappa : std::complex<double>(0.0, 0.0);
+        push_f32(w.real());
+        push_f32(w.imag());
     }
+    push_f32(kappa);
     // whole 1 KB chunks, as the kernel copies them
     while ((out->size() - start) % 256) out->push_back(0u);
 }

@@ -476,32 +476,36 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
 // Rows of 33..128 points (3 to 8 blocks).  Their operand tables are too large to
 // stream from the vector cache for every row, and the two LDS exchange rows of the
 // short-row kernels would leave room for few waves beside the tables.  So this
-// kernel keeps one real operand per block and direction in LDS and produces the
-// partner row's spectra directly in the order the separated product needs them:
-//   - the imaginary output part is the same operand applied to -i times the input
-//     (A_re = [Re | -Im] against (Im x, -Re x) gives Im(a x)), halving the tables;
+// kernel keeps one real operand per block in LDS and produces the partner row's
+// spectra directly in the order the separated product needs them:
+//   - the imaginary output part comes from the same operand, its halves swapped and
+//     one negated (A_re = [Re | -Im] becomes [Im | Re]), halving the tables;
+//   - frequencies are interleaved in the slots like the time points, so that each
+//     block of the DFT matrix is symmetric and the inverse transform, kappa times the
+//     conjugate of the forward one, runs on the same operands: half the tables again;
 //   - with w = exp(-2 pi i / m) and T the forward table, row ub's spectrum at the
 //     partner column of v is Z(m - 1 - v) = conj(T conj(z(j) w^(-j)))(v) for u > 0,
 //     and Z((m - v) mod m) = conj(T conj(z))(v) for row 0, so it lands in the
 //     registers of frequency v of row u;
 //   - W(-f) of row ub then sits at the slot of v, frequency m - 1 - v, and the row's
-//     inverse is y(j) = w^j conj(T_inv conj(G))(j) with G(v) = W(m - 1 - v).
+//     inverse is y(j) = w^j conj(T_inv conj(G))(j) = kappa w^j (T G)(j) with
+//     G(v) = W(m - 1 - v).
 // The products and inverses need no lane exchange, so the only LDS is the tables
 // and the kernel runs as many waves as its registers allow.  Rows 0 and N1/2 are
 // their own partners: their partner spectra come from their own data and only the
 // row itself is transformed back and stored.
 constexpr int kPartnerWaves = 4;  // rows u of one document per workgroup
 
-template <int NB>
-constexpr int kPartnerMinWaves = NB <= 2 ? 4 : NB <= 4 ? 3 : NB <= 6 ? 2 : 1;
+// waves per SIMD the registers must allow (the summing variant keeps four loaded rows
+// live across its blocks), and at most: rows of 5 or 6 blocks keep their filter spectra,
+// a block of both data spectra and the products live at once (164-198 registers), and
+// left free to aim at the occupancy their LDS would allow, the compiler's schedule
+// spills instead
+template <int NB, bool SUM>
+constexpr int kPartnerMinWaves = NB <= (SUM ? 2 : 3) ? 4 : NB <= 4 ? 3 : NB <= 6 ? 2 : 1;
+template <int NB, bool SUM>
+constexpr int kPartnerMaxWaves = (!SUM && NB >= 5 && NB <= 6) ? 2 : 8;
 
-// -i a = (Im a, -Re a)
-__device__ __forceinline__ uint32_t mul_neg_i(uint32_t a) {
-    return __builtin_amdgcn_alignbit(a, a, 16) ^ 0x80000000u;
-}
-__device__ __forceinline__ u4 mul_neg_i4(u4 a) {
-    return u4{mul_neg_i(a[0]), mul_neg_i(a[1]), mul_neg_i(a[2]), mul_neg_i(a[3])};
-}
 // The operand that gives the imaginary output part from the input itself: an entry v
 // held as (Re v, -Im v) becomes (Im v, Re v), so that the product with z sums
 // Im v Re z + Re v Im z = Im(v z), as the operand itself does against -i z
@@ -513,14 +517,14 @@ __device__ __forceinline__ u4 imag_operand4(u4 a) {
 }
 
 template <int NB, bool SUM>
-__global__ __launch_bounds__(64 * kPartnerWaves) __attribute__((amdgpu_waves_per_eu(kPartnerMinWaves<NB>, 8)))
+__global__ __launch_bounds__(64 * kPartnerWaves) __attribute__((amdgpu_waves_per_eu(kPartnerMinWaves<NB, SUM>, kPartnerMaxWaves<NB, SUM>)))
 void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
                         const uint32_t* __restrict__ fgrid, int64_t fgrid_pb_stride,
                         const Seg* __restrict__ segs, const int32_t* __restrict__ docs,
                         const int2* __restrict__ groups, const u4* __restrict__ tabs, int n1,
                         int corr) {
     constexpr int S = 16 * NB;
-    constexpr int kFrag = NB * NB * 64;            // u4 per direction
+    constexpr int kFrag = NB * NB * 64;            // u4 of DFT operands
     constexpr int kTab = partner_tab_u4(NB);
     constexpr bool kPrefetch = NB <= 4;            // first data rows loaded with the filter rows
     __shared__ u4 tab[kTab];
@@ -566,8 +570,9 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
     __syncthreads();  // tables visible to every wave; the only workgroup barrier
     if (!active) return;
 
-    const uint32_t* tw_pre = reinterpret_cast<const uint32_t*>(tab + 2 * kFrag);  // w^(-j), fp16
-    const float2* tw_post = reinterpret_cast<const float2*>(tab + 2 * kFrag + S / 4);  // w^j
+    const uint32_t* tw_pre = reinterpret_cast<const uint32_t*>(tab + kFrag);  // w^(-j), fp16
+    const float2* tw_post = reinterpret_cast<const float2*>(tab + kFrag + S / 4);  // kappa w^j
+    const float kappa = reinterpret_cast<const float*>(tab + kFrag + 3 * S / 4)[0];
     // rows u > 0 pair v with m - 1 - v and take the twiddle, row 0 pairs v with (m - v) mod m
     const int pre_mask = u != 0 ? -1 : 0;
 
@@ -593,10 +598,11 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
 #pragma unroll
             for (int jb = 0; jb < NB; ++jb) {
                 const u4 a = tab[(kb * NB + jb) * 64 + lk];
+                const u4 ai = imag_operand4(a);
                 acc[0] = mma(a, in_u[jb], acc[0]);
-                acc[1] = mma(a, mul_neg_i4(in_u[jb]), acc[1]);
+                acc[1] = mma(ai, in_u[jb], acc[1]);
                 acc[2] = mma(a, in_b[jb], acc[2]);
-                acc[3] = mma(a, mul_neg_i4(in_b[jb]), acc[3]);
+                acc[3] = mma(ai, in_b[jb], acc[3]);
             }
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
@@ -607,9 +613,8 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
         __builtin_amdgcn_sched_barrier(0);
     };
 
-    const u4* inv = tab + kFrag;
-    // separated products of one block of four frequencies: W(f) for row u into wu, W(-f)
-    // for row ub at the slot of f into wp (as conj(G), the inverse's input)
+    // separated products of one block of four frequencies: conj W(f) for row u into wu,
+    // W(-f) for row ub at the slot of f into wp (G, see inverse_store)
     auto products_block = [&](const uint32_t* fa, const uint32_t* fp, const uint32_t* au,
                               const uint32_t* ap, uint32_t* wu, uint32_t* wp) {
 #pragma unroll
@@ -622,15 +627,57 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
             const uint32_t e2 = pk_swap_add_conj(a, b);  // (Im d, Re d)
             const uint32_t U = pk_add_neg_hi(e1, e2);    // s - i d
             const uint32_t V = pk_add_neg_lo(e1, e2);    // s + i d
-            wu[r] = w_pos(A, Bf, U, V);
-            wp[r] = w_neg(A, Bf, U, V) ^ 0x80000000u;  // conj(G), the inverse's input
+            wu[r] = w_pos(A, Bf, U, V) ^ 0x80000000u;
+            wp[r] = w_neg(A, Bf, U, V);
         }
     };
-    // inverse DFT of row u and of row ub into the rows of rs.  A row that is its own
-    // partner stores only the first: the second goes through a buffer resource of no
-    // bytes.  The code has no branch between the matrix products and the reads of their
-    // results, so the compiler's wait states after the products hold on every path.
+    // forward DFT of the data rows u and ub, block by block, each block's products
+    // with the filter spectra fa / fp formed before the next block
+    auto forward_products = [&](const u4* in_u, u4* in_b, const uint32_t(*fa)[4], const uint32_t(*fp)[4],
+                                uint32_t(*wu)[4], uint32_t(*wp)[4], int lk) {
+#pragma unroll
+        for (int jb = 0; jb < NB; ++jb)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const uint32_t tw = tw_pre[(16 * jb + 4 * t + (lk >> 4)) & pre_mask];
+                in_b[jb][t] = cmul_h2(in_b[jb][t], tw) ^ 0x80000000u;
+            }
+#pragma unroll
+        for (int kb = 0; kb < NB; ++kb) {
+            f4 acc[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[i] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int jb = 0; jb < NB; ++jb) {
+                const u4 a = tab[(kb * NB + jb) * 64 + lk];
+                const u4 ai = imag_operand4(a);
+                acc[0] = mma(a, in_u[jb], acc[0]);
+                acc[1] = mma(ai, in_u[jb], acc[1]);
+                acc[2] = mma(a, in_b[jb], acc[2]);
+                acc[3] = mma(ai, in_b[jb], acc[3]);
+            }
+            uint32_t au[4], ap[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                au[r] = pack_h2(acc[0][r], acc[1][r]);
+                ap[r] = pack_h2(acc[2][r], -acc[3][r]);
+            }
+            products_block(fa[kb], fp[kb], au, ap, wu[kb], wp[kb]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    // inverse DFT of row u and of row ub into the rows of rs, through the forward
+    // operands: the inverse matrix is kappa conj(T), so row u's output is
+    // kappa conj(T conj W) (wu holds conj W) and row ub's is kappa w^j (T G)(j), the
+    // partner form of the forward section above.  A row that is its own partner stores
+    // only the first: the second goes through a buffer resource of no bytes.  The code
+    // has no branch between the matrix products and the reads of their results, so the
+    // compiler's wait states after the products hold on every path.
     auto inverse_store = [&](const uint32_t(*wu)[4], const uint32_t(*wp)[4], const RowBuffers& rs, int lk) {
+        // the operands are those of the forward transform: the lane index passes through
+        // an empty asm statement again so that the compiler does not keep the forward
+        // fragments live for reuse here
+        asm volatile("" : "+v"(lk));
         const __amdgpu_buffer_rsrc_t rdb = self ? row_buffer(nullptr, 0) : rs.db;
 #pragma unroll
         for (int kb = 0; kb < NB; ++kb) {
@@ -639,22 +686,24 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
             for (int i = 0; i < 4; ++i) acc[i] = f4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
             for (int jb = 0; jb < NB; ++jb) {
-                const u4 a = inv[(kb * NB + jb) * 64 + lk];
+                const u4 a = tab[(kb * NB + jb) * 64 + lk];
+                const u4 ai = imag_operand4(a);
                 const u4 bu = {wu[jb][0], wu[jb][1], wu[jb][2], wu[jb][3]};
                 const u4 bp = {wp[jb][0], wp[jb][1], wp[jb][2], wp[jb][3]};
                 acc[0] = mma(a, bu, acc[0]);
-                acc[1] = mma(a, mul_neg_i4(bu), acc[1]);
+                acc[1] = mma(ai, bu, acc[1]);
                 acc[2] = mma(a, bp, acc[2]);
-                acc[3] = mma(a, mul_neg_i4(bp), acc[3]);
+                acc[3] = mma(ai, bp, acc[3]);
             }
 #pragma unroll
             for (int r = 0; r < 4; ++r) {  // output register r: time point j = 16 kb + 4 r + h
                 const int off = lane_off + (16 * kb + 4 * r) * 64;
-                __builtin_amdgcn_raw_buffer_store_b32(pack_h2(acc[0][r], acc[1][r]), rs.du, off, 0, 2);
-                // w^j conj(R + i I) with w^j = (c, s): (R c + I s, R s - I c)
+                __builtin_amdgcn_raw_buffer_store_b32(pack_h2(kappa * acc[0][r], -kappa * acc[1][r]), rs.du,
+                                                      off, 0, 2);
+                // kappa w^j (R + i I) with kappa w^j = (c, s): (R c - I s, R s + I c)
                 const float2 w = tw_post[16 * kb + 4 * r + (lk >> 4)];
-                const float re = acc[2][r] * w.x + acc[3][r] * w.y;
-                const float im = acc[2][r] * w.y - acc[3][r] * w.x;
+                const float re = acc[2][r] * w.x - acc[3][r] * w.y;
+                const float im = acc[2][r] * w.y + acc[3][r] * w.x;
                 __builtin_amdgcn_raw_buffer_store_b32(pack_h2(re, im), rdb, off, 0, 2);
             }
         }
@@ -735,13 +784,11 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
         if (!kPrefetch || k > 0) load_rows(rb.du, rb.db, xu, xb);
         int lk = lane;
         asm volatile("" : "+v"(lk));
-        uint32_t au[NB][4], ap[NB][4];
-        forward(xu, xb, au, ap, lk);
-
-        // separated products: W(f) for row u, W(-f) for row ub at the slot of f
+        // the data rows' spectra block by block, each block's separated products formed
+        // at once (conj W(f) for row u, W(-f) for row ub at the slot of f), so that only
+        // one block of the two spectra is live
         uint32_t wu[NB][4], wp[NB][4];
-#pragma unroll
-        for (int kb = 0; kb < NB; ++kb) products_block(fa[kb], fp[kb], au[kb], ap[kb], wu[kb], wp[kb]);
+        forward_products(xu, xb, fa, fp, wu, wp, lk);
         inverse_store(wu, wp, rb, lk);
         if (++k == grp.y) break;
         rb = row_buffers(grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs + docs[grp.x + k], pb, u, ub);
