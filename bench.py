@@ -113,7 +113,8 @@ def time_step(launch, stream, steps, warmup, eager):
 def backward_measurement(rc, plan, W, x, k, spec, ws, stream, args):
     """The two gradient calls on the same batch: dx (rubiconv_packed_conv_dx) and dk
     (rubiconv_packed_conv_dk) for a seeded upstream gradient of y's shape and dtype, each
-    timed as its own step, with per-kernel event times of the same calls."""
+    timed as its own step, with per-kernel event times of the same calls; then both in
+    one call (rubiconv_packed_conv_backward) as a step of its own."""
     import torch
     import workloads as wl
     dev = x.device
@@ -135,12 +136,17 @@ def backward_measurement(rc, plan, W, x, k, spec, ws, stream, args):
     dx_ms = time_step(launch_dx, stream, args.steps, args.warmup, args.eager)
     progress("dk step")
     dk_ms = time_step(launch_dk, stream, args.steps, args.warmup, args.eager)
+    def launch_bwd(s):
+        rc.packed_conv_backward(plan, x, dy, spec, dx=dx, dk=dk, workspace=dk_ws, stream=s)
+    progress("fused backward step")
+    bwd_ms = time_step(launch_bwd, stream, args.steps, args.warmup, args.eager)
     progress("gradient stages")
     calls = min(args.steps, PROFILE_CALLS)
-    plan.profile_start(2 * calls)
+    plan.profile_start(3 * calls)
     for _ in range(calls):
         launch_dx(stream)
         launch_dk(stream)
+        launch_bwd(stream)
     kt = plan.profile_read()
     plan.profile_start(0)
     tok_ch = W.B * W.N * W.D
@@ -150,9 +156,10 @@ def backward_measurement(rc, plan, W, x, k, spec, ws, stream, args):
     # and writes dx; dk reads x and dy and writes dk (D L 4)
     dx_min = tok_ch * (sx + sy) + W.D * W.L * 8
     dk_min = tok_ch * (sx + sy) + W.D * W.L * 4
-    out = {"dx_ms": round(dx_ms, 4), "dk_ms": round(dk_ms, 4),
+    out = {"dx_ms": round(dx_ms, 4), "dk_ms": round(dk_ms, 4), "backward_ms": round(bwd_ms, 4),
            "dx_value": round(tok_ch / (dx_ms * 1e-3) / 1e6, 1),
            "dk_value": round(tok_ch / (dk_ms * 1e-3) / 1e6, 1),
+           "backward_value": round(tok_ch / (bwd_ms * 1e-3) / 1e6, 1),
            "unit": "Mtokens*channels/s",
            "dx_hbm_roofline_frac_step": round(dx_min / (dx_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
            "dk_hbm_roofline_frac_step": round(dk_min / (dk_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),

@@ -267,8 +267,9 @@ rubiconv_status_t rubiconv_packed_conv_noalloc(rubiconv_plan_t plan, const void*
 rubiconv_status_t rubiconv_packed_conv_dx(rubiconv_plan_t plan, const void* dy, const void* spectrum,
                                           void* dx, void* workspace, hipStream_t stream);
 
-/* Bytes of device scratch rubiconv_packed_conv_dk needs: two document grids and
- * a float32 [B][N][D] buffer.  0 for a null plan. */
+/* Bytes of device scratch rubiconv_packed_conv_dk and rubiconv_packed_conv_backward
+ * need: two document grids and a float32 [B][N][D] buffer (at least
+ * rubiconv_workspace_bytes).  0 for a null plan. */
 size_t rubiconv_dk_workspace_bytes(rubiconv_plan_t plan);
 
 /*
@@ -289,6 +290,29 @@ size_t rubiconv_dk_workspace_bytes(rubiconv_plan_t plan);
  */
 rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, const void* dy,
                                           float* dk, void* workspace, hipStream_t stream);
+
+/*
+ * dx and dk of one backward pass in one call: the same results as
+ * rubiconv_packed_conv_dx followed by rubiconv_packed_conv_dk, with dy's column
+ * DFTs (Algorithm 1's first transform step) computed once for both.  dk's row
+ * stage writes its class sums over x's grid in the workspace, so dy's grid stays
+ * for dx's correlation with the filter (the same products as for dx alone).
+ * Taken when every transform document runs on the matrix-core passes (bf16 x and
+ * dy, rows of at most 128 points, no split rows); otherwise the two calls run in
+ * sequence.  dx is bit-identical to rubiconv_packed_conv_dx's; dk's products are
+ * formed from dy's grid at dx's range scale times the filter gradient's split
+ * (exact powers of two), so it can differ from rubiconv_packed_conv_dk's in the
+ * last bits of fp16 rounding.
+ *
+ *   x, dy, spectrum, dx, dk as for the two calls above; dx and dk must not
+ *              overlap each other, the inputs or workspace.
+ *   workspace  device buffer of rubiconv_dk_workspace_bytes(plan), 256-byte aligned.
+ *   stream     HIP stream the work is enqueued on.
+ * Errors: RUBICONV_ERR_ARG, RUBICONV_ERR_UNSUPPORTED (as for dk), RUBICONV_ERR_HIP.
+ */
+rubiconv_status_t rubiconv_packed_conv_backward(rubiconv_plan_t plan, const void* x, const void* dy,
+                                                const void* spectrum, void* dx, float* dk, void* workspace,
+                                                hipStream_t stream);
 
 /* Summary of a plan (host call, no device work). */
 typedef struct {

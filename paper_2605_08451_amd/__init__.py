@@ -40,7 +40,7 @@ _STATUS = {0: "ok", 1: "invalid argument", 2: "invalid cu_seqlens", 3: "unsuppor
 EXPORTED_SYMBOLS = ("rubiconv_plan", "rubiconv_plan_destroy", "rubiconv_spectrum_bytes",
                     "rubiconv_workspace_bytes", "rubiconv_filter_spectrum", "rubiconv_packed_conv",
                     "rubiconv_packed_conv_dx", "rubiconv_dk_workspace_bytes", "rubiconv_packed_conv_dk",
-                    "rubiconv_packed_conv_noalloc",
+                    "rubiconv_packed_conv_backward", "rubiconv_packed_conv_noalloc",
                     "rubiconv_plan_info", "rubiconv_plan_doc_table", "rubiconv_profile_start",
                     "rubiconv_profile_read", "rubiconv_status_string",
                     "rubiconv_ct_plan", "rubiconv_ct_plan_destroy", "rubiconv_ct_spectrum_bytes",
@@ -102,6 +102,8 @@ def load_library():
     lib.rubiconv_dk_workspace_bytes.restype = sz
     lib.rubiconv_packed_conv_dk.argtypes = [vp, vp, vp, vp, vp, vp]
     lib.rubiconv_packed_conv_dk.restype = c_int
+    lib.rubiconv_packed_conv_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.rubiconv_packed_conv_backward.restype = c_int
     lib.rubiconv_plan_info.argtypes = [vp, ctypes.POINTER(_PlanInfo)]
     lib.rubiconv_plan_info.restype = c_int
     lib.rubiconv_plan_doc_table.argtypes = [vp, i32p, c_int, ctypes.POINTER(c_int)]
@@ -400,6 +402,37 @@ def packed_conv_dk(plan: Plan, x: torch.Tensor, dy: torch.Tensor,
                                                  _stream_handle(dev, stream)),
                "rubiconv_packed_conv_dk")
     return dk
+
+
+def packed_conv_backward(plan: Plan, x: torch.Tensor, dy: torch.Tensor, spectrum: torch.Tensor,
+                         dx: Optional[torch.Tensor] = None, dk: Optional[torch.Tensor] = None,
+                         workspace: Optional[torch.Tensor] = None, stream=None):
+    """(dx, dk) of one backward pass in one call (``rubiconv_packed_conv_backward``): the
+    results of :func:`packed_conv_dx` and :func:`packed_conv_dk`, dy's column pass shared."""
+    _check_btd(x, plan, plan.x_dtype, "x")
+    _check_btd(dy, plan, plan.y_dtype, "dy")
+    dev = x.device
+    with _on_stream(stream):
+        if dx is None:
+            dx = torch.empty((plan.B, plan.N, plan.D), dtype=_torch_dtype(plan.x_dtype), device=dev)
+        if dk is None:
+            dk = torch.empty((plan.D, plan.L), dtype=torch.float32, device=dev)
+        if workspace is None:
+            workspace = plan.new_dk_workspace(dev)
+    _check_btd(dx, plan, plan.x_dtype, "dx")
+    _cuda_contig(dk, "dk")
+    if tuple(dk.shape) != (plan.D, plan.L) or dk.dtype != torch.float32:
+        raise ValueError(f"dk must be float32 [{plan.D}, {plan.L}]")
+    if workspace.numel() * workspace.element_size() < plan.dk_workspace_bytes:
+        raise ValueError("workspace buffer too small")
+    if spectrum.numel() * spectrum.element_size() < plan.spectrum_bytes:
+        raise ValueError("spectrum buffer too small")
+    with torch.cuda.device(dev):
+        _check(plan._lib.rubiconv_packed_conv_backward(plan.handle, x.data_ptr(), dy.data_ptr(),
+                                                       spectrum.data_ptr(), dx.data_ptr(), dk.data_ptr(),
+                                                       workspace.data_ptr(), _stream_handle(dev, stream)),
+               "rubiconv_packed_conv_backward")
+    return dx, dk
 
 
 def conv(x: torch.Tensor, filters: torch.Tensor, cu_seqlens, y_dtype=None, n1: int = 0):

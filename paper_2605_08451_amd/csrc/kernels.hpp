@@ -80,7 +80,10 @@ hipError_t launch_row_fast(int m, bool half, void* grid, int64_t grid_pb_stride,
 // plan's dense operand tables, addressed through Seg::dense_off.
 // sum: every document of a group brings its own second-grid rows, the products of
 // the group's documents are added, and the one inverse transform of the sum is written
-// over the first document's rows (the others are left as they were).
+// over the first document's rows (the others are left as they were); with sum, dscale
+// (a power of two) multiplies the data rows' spectra before they are rounded to fp16,
+// and out2 writes the inverse over the first document's second-grid rows instead, which
+// leaves the grid itself as it was (both: 1 and false without sum).
 // 16-byte entries of one class's tables for the rows of 3 to 8 blocks: nb * nb real
 // operands of 64 lanes (the forward transform; the inverse takes their conjugates),
 // then 16 nb complex fp16 twiddles w^(-j), 16 nb complex fp32 twiddles kappa w^j
@@ -91,7 +94,8 @@ constexpr int partner_tab_u4(int nb) { return (nb * nb * 64 + 12 * nb + 1 + 63) 
 hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const void* fgrid,
                             int64_t fgrid_pb_stride, const Seg* segs, const int32_t* docs,
                             const int32_t* groups, int ngroups, const void* tabs, int n1, int npb,
-                            int corr, hipStream_t stream, bool sum = false);
+                            int corr, hipStream_t stream, bool sum = false, float dscale = 1.0f,
+                            bool out2 = false);
 
 // Long rows (fp16 grids): the first level of the row DFT of one document or class grid
 // (LrItem) for its n1 grid rows and npb pair blocks, into its sub-row region, or the

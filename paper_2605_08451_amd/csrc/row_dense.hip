@@ -180,7 +180,7 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
                                                                const int32_t* __restrict__ docs,
                                                                const int2* __restrict__ groups,
                                                                const u4* __restrict__ tabs, int n1,
-                                                               int corr) {
+                                                               int corr, float dscale, int out2) {
     constexpr int S = 16 * NB;                     // points per row, padded to whole blocks
     constexpr int kTabU4 = 4 * NB * NB * 64;       // forward then inverse fragments
     constexpr int kStage = 4 * S * 16;             // u32 per wave: four rows [point][16 pairs]
@@ -256,7 +256,7 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
     // forward DFT of rows u and ub: own[kb][r] = frequency 16 kb + 4 h + r of row u;
     // row ub's spectrum to the exchange row dst (slot 16 kb + 4 h + r - shift), and
     // its frequency 0 returned for row 0's wrap
-    auto forward = [&](const u4* in_u, const u4* in_b, uint32_t(*own)[4], uint32_t* dst) {
+    auto forward = [&](const u4* in_u, const u4* in_b, uint32_t(*own)[4], uint32_t* dst, float sc) {
 #pragma unroll
         for (int i = 0; i < kPad / 4; ++i) dst[16 * (4 * i + h - kPad)] = 0u;
         uint32_t keep = 0u;
@@ -276,8 +276,8 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
             }
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                own[kb][r] = pack_h2(acc[0][0][r], acc[0][1][r]);
-                const uint32_t bv = pack_h2(acc[1][0][r], acc[1][1][r]);
+                own[kb][r] = pack_h2(sc * acc[0][0][r], sc * acc[0][1][r]);
+                const uint32_t bv = pack_h2(sc * acc[1][0][r], sc * acc[1][1][r]);
                 dst[16 * (16 * kb + 4 * h + r - shift)] = bv;
                 if (kb == 0 && r == 0) keep = bv;
             }
@@ -348,21 +348,21 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
     };
 
     if constexpr (SUM) {
-        // every document brings its own second rows: both spectra per document, the
-        // products added up (packed fp16), one inverse for the group into its first
-        // document's rows (rb)
+        // every document brings its own second rows: both spectra per document (the data
+        // rows' times dscale), the products added up (packed fp16), one inverse for the
+        // group into its first document's rows (rb; with out2, its second rows)
         uint32_t su[NB][4];
         u4 sb[NB];
         for (int k = 0;;) {
             uint32_t fa[NB][4], fl[NB][4];
-            forward(in.fu, in.fb, fa, flds);
+            forward(in.fu, in.fb, fa, flds, 1.0f);
 #pragma unroll
             for (int kb = 0; kb < NB; ++kb)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) fl[kb][r] = flds[16 * (rbase - 16 * kb - r)];
             wave_lds_fence();  // the second exchange row is free from here on
             uint32_t au[NB][4], wu[NB][4];
-            forward(in.xu, in.xb, au, xlds);
+            forward(in.xu, in.xb, au, xlds, dscale);
             products(fa, fl, au, wu);
 #pragma unroll
             for (int jb = 0; jb < NB; ++jb)
@@ -403,14 +403,14 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
                 }
             wave_lds_fence();
         }
-        inverse_store(su, sb, rb);
+        inverse_store(su, sb, out2 ? RowBuffers{rb.fu, rb.fb, rb.fu, rb.fb} : rb);
         return;
     }
 
     // the filter rows, once per group: own spectrum in registers, and the partner
     // values at the slots the product reads gathered from the exchange row
     uint32_t fa[NB][4], fl[NB][4];
-    forward(in.fu, in.fb, fa, flds);
+    forward(in.fu, in.fb, fa, flds, 1.0f);
 #pragma unroll
     for (int kb = 0; kb < NB; ++kb)
 #pragma unroll
@@ -440,7 +440,7 @@ __global__ __launch_bounds__(64 * kLdsWaves) void row_lds_kernel(uint32_t* __res
             __builtin_amdgcn_sched_barrier(0);  // the copies stay ahead of this document's stores
         }
         uint32_t au[NB][4];
-        forward(in.xu, in.xb, au, xlds);
+        forward(in.xu, in.xb, au, xlds, 1.0f);
 
         uint32_t wu[NB][4];
         products(fa, fl, au, wu);
@@ -522,7 +522,7 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
                         const uint32_t* __restrict__ fgrid, int64_t fgrid_pb_stride,
                         const Seg* __restrict__ segs, const int32_t* __restrict__ docs,
                         const int2* __restrict__ groups, const u4* __restrict__ tabs, int n1,
-                        int corr) {
+                        int corr, float dscale, int out2) {
     constexpr int S = 16 * NB;
     constexpr int kFrag = NB * NB * 64;            // u4 of DFT operands
     constexpr int kTab = partner_tab_u4(NB);
@@ -710,10 +710,11 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
     };
 
     if constexpr (SUM) {
-        // every document brings its own second rows: both spectra per document, the
-        // products added up (packed fp16), one inverse for the group into its first
-        // document's rows.  Block kb of all four spectra is formed and multiplied before
-        // the next, so that only the loaded rows and the sums stay live across blocks.
+        // every document brings its own second rows: both spectra per document (the data
+        // rows' times dscale), the products added up (packed fp16), one inverse for the
+        // group into its first document's rows (with out2, its second rows).  Block kb of
+        // all four spectra is formed and multiplied before the next, so that only the
+        // loaded rows and the sums stay live across blocks.
         const RowBuffers r0 = rb;
         uint32_t su[NB][4], sp[NB][4];
         for (int k = 0;;) {
@@ -754,8 +755,8 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
                 for (int r = 0; r < 4; ++r) {
                     fa[0][r] = pack_h2(acc[0][r], acc[1][r]);
                     fp[0][r] = pack_h2(acc[2][r], -acc[3][r]);
-                    au[0][r] = pack_h2(acc[4][r], acc[5][r]);
-                    ap[0][r] = pack_h2(acc[6][r], -acc[7][r]);
+                    au[0][r] = pack_h2(dscale * acc[4][r], dscale * acc[5][r]);
+                    ap[0][r] = pack_h2(dscale * acc[6][r], -dscale * acc[7][r]);
                 }
                 products_block(fa[0], fp[0], au[0], ap[0], wu[0], wp[0]);
 #pragma unroll
@@ -772,7 +773,7 @@ void row_partner_kernel(uint32_t* __restrict__ grid, int64_t grid_pb_stride,
         }
         int lk = lane;
         asm volatile("" : "+v"(lk));
-        inverse_store(su, sp, r0, lk);
+        inverse_store(su, sp, out2 ? RowBuffers{r0.fu, r0.fb, r0.fu, r0.fb} : r0, lk);
         return;
     }
 
@@ -983,34 +984,40 @@ __global__ __launch_bounds__(64 * kBatchWaves) void row_batch_kernel(uint32_t* _
 template <int NB>
 hipError_t launch_lds_nb(void* grid, int64_t gs, const void* fgrid, int64_t fs, const Seg* segs,
                          const int32_t* docs, const int32_t* groups, int ngroups, const void* tabs,
-                         int n1, int npb, int corr, hipStream_t stream, bool sum) {
+                         int n1, int npb, int corr, hipStream_t stream, bool sum, float dscale,
+                         bool out2) {
     const int ug = (n1 / 2 + 1 + kLdsWaves - 1) / kLdsWaves;
     const dim3 g(ngroups * ug, npb), b(64 * kLdsWaves);
     if (sum)
         hipLaunchKernelGGL((row_lds_kernel<NB, true>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
                            static_cast<const uint32_t*>(fgrid), fs, segs, docs,
-                           reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr);
+                           reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr,
+                           dscale, out2 ? 1 : 0);
     else
         hipLaunchKernelGGL((row_lds_kernel<NB, false>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
                            static_cast<const uint32_t*>(fgrid), fs, segs, docs,
-                           reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr);
+                           reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr,
+                           dscale, out2 ? 1 : 0);
     return hipGetLastError();
 }
 
 template <int NB>
 hipError_t launch_partner_nb(void* grid, int64_t gs, const void* fgrid, int64_t fs, const Seg* segs,
                              const int32_t* docs, const int32_t* groups, int ngroups,
-                             const void* tabs, int n1, int npb, int corr, hipStream_t stream, bool sum) {
+                             const void* tabs, int n1, int npb, int corr, hipStream_t stream, bool sum,
+                             float dscale, bool out2) {
     const int ug = (n1 / 2 + 1 + kPartnerWaves - 1) / kPartnerWaves;
     const dim3 g(ngroups * ug, npb), b(64 * kPartnerWaves);
     if (sum)
         hipLaunchKernelGGL((row_partner_kernel<NB, true>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
                            static_cast<const uint32_t*>(fgrid), fs, segs, docs,
-                           reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr);
+                           reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr,
+                           dscale, out2 ? 1 : 0);
     else
         hipLaunchKernelGGL((row_partner_kernel<NB, false>), g, b, 0, stream, static_cast<uint32_t*>(grid), gs,
                            static_cast<const uint32_t*>(fgrid), fs, segs, docs,
-                           reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr);
+                           reinterpret_cast<const int2*>(groups), static_cast<const u4*>(tabs), n1, corr,
+                           dscale, out2 ? 1 : 0);
     return hipGetLastError();
 }
 
@@ -1032,9 +1039,10 @@ hipError_t launch_row_batch(void* grid, int64_t grid_pb_stride, const void* fgri
 hipError_t launch_row_dense(int nb, void* grid, int64_t grid_pb_stride, const void* fgrid,
                             int64_t fgrid_pb_stride, const Seg* segs, const int32_t* docs,
                             const int32_t* groups, int ngroups, const void* tabs, int n1, int npb,
-                            int corr, hipStream_t stream, bool sum) {
+                            int corr, hipStream_t stream, bool sum, float dscale, bool out2) {
     if (ngroups == 0) return hipSuccess;
-#define RUBICONV_ARGS grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, docs, groups, ngroups, tabs, n1, npb, corr, stream, sum
+    if (!sum && (dscale != 1.0f || out2)) return hipErrorInvalidValue;
+#define RUBICONV_ARGS grid, grid_pb_stride, fgrid, fgrid_pb_stride, segs, docs, groups, ngroups, tabs, n1, npb, corr, stream, sum, dscale, out2
     switch (nb) {
         case 1: return launch_lds_nb<1>(RUBICONV_ARGS);
         case 2: return launch_lds_nb<2>(RUBICONV_ARGS);

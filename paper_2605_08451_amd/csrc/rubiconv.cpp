@@ -44,6 +44,7 @@ struct rubiconv_plan_s {
     const int32_t* lr_idx = nullptr;        //   identity indices
     const int32_t* lr_groups = nullptr;     //   groups of the sub-row launches
     const float2* ones = nullptr;           // {1, 1} per channel pair: the unit range scales
+    const float2* dk_unscale = nullptr;     // {ed, 1 / ed} per channel pair (dk_split)
     bool device_ready = false;
     bool prescale_fwd = true;    // the forward prescales x as the gradients do dy (and x)
     // pinned host words, written by the matrix-core column passes: the range scales the
@@ -96,6 +97,17 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) % kAlign) == 0; }
 
+// The filter gradient's range split: x and dy carry ex and ed, together
+// 2^-ceil(log2 P_max), as a correlation sums up to P products.
+void dk_split(const HostPlan& h, float* ex, float* ed) {
+    int pmax = 1;
+    for (const Seg& d : h.docs) pmax = std::max(pmax, d.P);
+    int lg = 0;
+    while ((1 << lg) < pmax && lg < 30) ++lg;
+    *ex = std::ldexp(1.0f, -(lg + 1) / 2);
+    *ed = std::ldexp(1.0f, -(lg / 2));
+}
+
 rubiconv_status_t upload(rubiconv_plan_s* pl, hipStream_t stream) {
     const HostPlan& h = pl->h;
     const size_t n_segs = h.docs.size() + h.classes.size();
@@ -125,6 +137,7 @@ rubiconv_status_t upload(rubiconv_plan_s* pl, hipStream_t stream) {
     const size_t o_lq = off;         off = align_up(off + h.lr_groups.size() * 4);
     const size_t n_ones = static_cast<size_t>(std::max(h.npb, 1)) * kPairsPerBlock;
     const size_t o_one = off;        off = align_up(off + n_ones * sizeof(float2));
+    const size_t o_dku = off;        off = align_up(off + n_ones * sizeof(float2));
     const size_t total = off;
 
     // the host image stays with the plan: the copy below is stream-ordered and may still
@@ -166,6 +179,10 @@ rubiconv_status_t upload(rubiconv_plan_s* pl, hipStream_t stream) {
     {
         std::vector<float> ones(2 * n_ones, 1.0f);
         std::memcpy(img.data() + o_one, ones.data(), ones.size() * sizeof(float));
+        float ex, ed;
+        dk_split(h, &ex, &ed);
+        std::vector<float2> dku(n_ones, make_float2(ed, 1.0f / ed));
+        std::memcpy(img.data() + o_dku, dku.data(), dku.size() * sizeof(float2));
     }
     if (!h.lr_segs.empty()) {
         std::memcpy(img.data() + o_ls, h.lr_segs.data(), h.lr_segs.size() * sizeof(Seg));
@@ -222,6 +239,7 @@ rubiconv_status_t upload(rubiconv_plan_s* pl, hipStream_t stream) {
     pl->lr_idx = reinterpret_cast<const int32_t*>(base + o_li);
     pl->lr_groups = reinterpret_cast<const int32_t*>(base + o_lq);
     pl->ones = reinterpret_cast<const float2*>(base + o_one);
+    pl->dk_unscale = reinterpret_cast<const float2*>(base + o_dku);
     // the fork and join events only order this device's streams: no system-scope fence
     // (the kernels' own release and acquire make their data visible across the device),
     // which spares a cache writeback and invalidation at every fork and join
@@ -376,11 +394,10 @@ float scale_guess(const rubiconv_plan_s* plan, int slot) {
     return g >= 0x1p-126f && g <= 0x1p127f ? g : 1.0f;
 }
 
-hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, const void* fgrid,
-                        int64_t fgrid_pb_stride, const LaunchTables& t, void* out, int out_dtype,
-                        void* grid, int corr, bool own_rows, GridScale in_sc, GridScale out_sc,
-                        const char* tag, hipStream_t stream, StageRecorder& rec,
-                        const SpecScale* spec = nullptr) {
+// The forward column pass of `in` into `grid` (and the long rows' first level); with
+// spec, at a guessed scale, then the redo launch (SpecScale).
+hipError_t enqueue_col_fwd(rubiconv_plan_s* plan, const void* in, int in_dtype, void* grid, GridScale in_sc,
+                           hipStream_t stream, const SpecScale* spec) {
     const HostPlan& h = plan->h;
     const int n_cols = static_cast<int>(h.doc_col_seg.size());
     const int64_t rs = static_cast<int64_t>(h.N) * h.D;
@@ -398,12 +415,23 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
         e = rubiconv::launch_col_fwd_mfma(in_dtype, in, rs, h.D, grid, plan->grid_pb_stride, plan->doc_t, in_sc,
                                           plan->mfma_tab, n_cols, h.npb, stream, nullptr, spec->parts, spec->used,
                                           spec->guess, spec->hint, spec->extra, spec->prev);
-    rec.mark(stage(tag, "col_fwd"));
     // long rows: first level into the sub-row regions (both grids of the filter gradient)
     for (const rubiconv::LrItem& it : h.lr_doc_items)
         if (e == hipSuccess)
             e = rubiconv::launch_lr_step(false, grid, plan->grid_pb_stride, it, plan->doc_t.tw, h.n1,
                                          h.npb, stream);
+    return e;
+}
+
+// The row stage on `grid` against the second grid `fgrid` (a filter spectrum, or x's grid
+// for the filter gradient: own_rows, the sum groups), then the long rows' inverse first
+// level.  dscale and out2 apply to the sum groups (launch_row_dense).
+hipError_t enqueue_rows(rubiconv_plan_s* plan, const void* fgrid, int64_t fgrid_pb_stride, const LaunchTables& t,
+                        void* grid, int corr, bool own_rows, hipStream_t stream, float dscale = 1.0f,
+                        bool out2 = false) {
+    const HostPlan& h = plan->h;
+    const bool half = h.grid_half;
+    hipError_t e = hipSuccess;
     // row pass: the generic kernel (long rows) and one launch per listed size
     // class, spread over the side streams (largest work first, least-loaded stream)
     struct Launch {
@@ -452,7 +480,7 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
             return rubiconv::launch_row_dense(
                 L.nb, grid, plan->grid_pb_stride, fgrid, fgrid_pb_stride, t.segs, plan->dense_sdocs,
                 plan->dense_sgroups + 2 * h.dense_sgrp0[L.nb], h.dense_sgrp_n[L.nb], plan->dense_tab, h.n1,
-                h.npb, corr, s, true);
+                h.npb, corr, s, true, dscale, out2);
         if (L.nb > 0)
             return rubiconv::launch_row_dense(
                 L.nb, grid, plan->grid_pb_stride, fgrid, fgrid_pb_stride, t.segs, plan->dense_docs,
@@ -491,20 +519,48 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
         if (e == hipSuccess)
             e = rubiconv::launch_lr_step(true, grid, plan->grid_pb_stride, it, plan->doc_t.tw, h.n1,
                                          h.npb, stream);
-    rec.mark(stage(tag, "row_conv"));
-    // the filter gradient transforms back its output documents only (the sum groups'
-    // followers have added their products to their leaders' rows)
+    return e;
+}
+
+// The inverse column pass of `grid` into `out`.  own_rows (the filter gradient): its output
+// documents only, the sum groups' followers having added their products to their
+// leaders' rows.
+hipError_t enqueue_col_inv(rubiconv_plan_s* plan, const void* grid, void* out, int out_dtype, bool own_rows,
+                           GridScale out_sc, hipStream_t stream) {
+    const HostPlan& h = plan->h;
+    const int64_t rs = static_cast<int64_t>(h.N) * h.D;
     const LaunchTables& inv_t = own_rows ? plan->dk_t : plan->doc_t;
-    const int inv_cols = own_rows ? static_cast<int>(h.dk_col_seg.size()) : n_cols;
-    if (e == hipSuccess)
-        e = h.col_mfma ? rubiconv::launch_col_inv_mfma(out_dtype, grid, plan->grid_pb_stride, out,
-                                                       rs, h.D, inv_t, out_sc, plan->mfma_tab,
-                                                       inv_cols, h.npb, stream)
-                       : rubiconv::launch_col_inv(h.r, half, out_dtype, grid,
-                                                  plan->grid_pb_stride, out, rs, h.D, inv_t,
-                                                  out_sc, inv_cols, h.npb, stream);
+    const int inv_cols = own_rows ? static_cast<int>(h.dk_col_seg.size()) : static_cast<int>(h.doc_col_seg.size());
+    return h.col_mfma ? rubiconv::launch_col_inv_mfma(out_dtype, grid, plan->grid_pb_stride, out, rs, h.D, inv_t,
+                                                      out_sc, plan->mfma_tab, inv_cols, h.npb, stream)
+                      : rubiconv::launch_col_inv(h.r, h.grid_half, out_dtype, grid, plan->grid_pb_stride, out, rs,
+                                                 h.D, inv_t, out_sc, inv_cols, h.npb, stream);
+}
+
+hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, const void* fgrid,
+                        int64_t fgrid_pb_stride, const LaunchTables& t, void* out, int out_dtype,
+                        void* grid, int corr, bool own_rows, GridScale in_sc, GridScale out_sc,
+                        const char* tag, hipStream_t stream, StageRecorder& rec,
+                        const SpecScale* spec = nullptr) {
+    hipError_t e = enqueue_col_fwd(plan, in, in_dtype, grid, in_sc, stream, spec);
+    rec.mark(stage(tag, "col_fwd"));
+    if (e == hipSuccess) e = enqueue_rows(plan, fgrid, fgrid_pb_stride, t, grid, corr, own_rows, stream);
+    rec.mark(stage(tag, "row_conv"));
+    if (e == hipSuccess) e = enqueue_col_inv(plan, grid, out, out_dtype, own_rows, out_sc, stream);
     rec.mark(stage(tag, "col_inv"));
     return e;
+}
+
+// The fused backward shares dy's column pass between dx and dk when every transform
+// document takes the matrix-core passes on bf16 x and dy: no long rows and no VALU row
+// launches, so that the filter gradient's row stage is the sum groups alone.
+bool backward_fusable(const HostPlan& h) {
+    if (!(h.grid_half && h.col_mfma && h.row_dense && h.x_dtype == RUBICONV_BF16 && h.y_dtype == RUBICONV_BF16))
+        return false;
+    if (!h.lr_doc_items.empty() || !h.doc_task_seg.empty()) return false;
+    for (const Seg& c : h.classes)
+        if (c.m > 16 * rubiconv::kMaxDenseBlocks) return false;
+    return true;
 }
 
 }  // namespace
@@ -574,7 +630,8 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
     pl->ws_bytes = pl->ws_hdr_off + hdr_bytes;
     pl->grid_bytes = conv_ws;
     pl->dk_hdr_off = 2 * conv_ws + align_up(static_cast<size_t>(h.B) * h.N * h.D * 4);
-    pl->dk_ws_bytes = pl->dk_hdr_off + hdr_bytes;
+    // (at least the convolution's: the fused backward may run dx and dk in sequence in it)
+    pl->dk_ws_bytes = std::max(pl->dk_hdr_off + hdr_bytes, pl->ws_bytes);
     pl->spec_bytes = std::max(pl->spec_bytes, kAlign);
     // RUBICONV_PRESCALE = 0: the forward takes x as it is, without the power-of-two
     // scale from its largest magnitude (which costs one extra read of x); the gradients
@@ -797,11 +854,8 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
     const float2* ds = plan->ones;
     float2* w = prescale_words(workspace, plan->dk_hdr_off);
     uint32_t* work = prescale_work(workspace, plan->dk_hdr_off);
-    int pmax = 1;
-    for (const Seg& d : h.docs) pmax = std::max(pmax, d.P);
-    int lg = 0;
-    while ((1 << lg) < pmax && lg < 30) ++lg;
-    const float ex = std::ldexp(1.0f, -(lg + 1) / 2), ed = std::ldexp(1.0f, -(lg / 2));
+    float ex, ed;
+    dk_split(h, &ex, &ed);
     const bool speculative = h.grid_half && h.col_mfma && h.x_dtype == RUBICONV_BF16 && h.y_dtype == RUBICONV_BF16;
     // per-task magnitudes: x's in the first half of the partials area, dy's in the second
     uint16_t* parts = reinterpret_cast<uint16_t*>(work);
@@ -857,6 +911,88 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
         e = rubiconv::launch_lag_sum(r, plan->dk_sum_segs, static_cast<int>(h.dk_sum_segs.size()), h.N,
                                      h.D, h.L, dk, stream);
     rec.mark("dk_lag_sum");
+    return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
+}
+
+
+rubiconv_status_t rubiconv_packed_conv_backward(rubiconv_plan_t plan, const void* x, const void* dy,
+                                                const void* spectrum, void* dx, float* dk, void* workspace,
+                                                hipStream_t stream) {
+    if (!plan || !x || !dy || !spectrum || !dx || !dk || !workspace) return RUBICONV_ERR_ARG;
+    if (!aligned(spectrum) || !aligned(workspace)) return RUBICONV_ERR_ARG;
+    const HostPlan& h = plan->h;
+    const size_t xsz = h.x_dtype == RUBICONV_F32 ? 4 : 2;
+    const size_t ysz = h.y_dtype == RUBICONV_F32 ? 4 : 2;
+    if (reinterpret_cast<uintptr_t>(x) % xsz || reinterpret_cast<uintptr_t>(dy) % ysz ||
+        reinterpret_cast<uintptr_t>(dx) % xsz || reinterpret_cast<uintptr_t>(dk) % 4)
+        return RUBICONV_ERR_ARG;
+    if (!plan->device_ready) return RUBICONV_ERR_HIP;
+    if (!backward_fusable(h)) {
+        rubiconv_status_t st = rubiconv_packed_conv_dx(plan, dy, spectrum, dx, workspace, stream);
+        if (st == RUBICONV_OK) st = rubiconv_packed_conv_dk(plan, x, dy, dk, workspace, stream);
+        return st;
+    }
+    // the x grid doubles as the "filter" grid: its offsets must fit the 32-bit field
+    if (h.grid_points + h.grid_points_lr > INT32_MAX) return RUBICONV_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(plan->launch_mu);
+    StageRecorder rec(plan, stream);
+    char* ws = static_cast<char*>(workspace);
+    void* dygrid = ws;
+    void* xgrid = ws + plan->grid_bytes;
+    float* r = reinterpret_cast<float*>(ws + 2 * plan->grid_bytes);
+    const int n_cols = static_cast<int>(h.doc_col_seg.size());
+    hipError_t e = hipSuccess;
+    // direct documents: dx's and dk's sums, one after the other beside the transforms
+    const bool direct = !h.direct_docs.empty();
+    if (direct)
+        e = fork_direct(plan, stream, rec, "bwd_direct", [&](hipStream_t s) {
+            hipError_t de = rubiconv::launch_direct(1, h.direct_max, h.y_dtype, dy, 0, nullptr,
+                                                    direct_taps(plan, spectrum), plan->direct_segs,
+                                                    static_cast<int>(h.direct_docs.size()), h.N, h.D, h.L,
+                                                    h.x_dtype, dx, s);
+            if (de == hipSuccess)
+                de = rubiconv::launch_direct(2, h.direct_max, h.y_dtype, dy, h.x_dtype, x, nullptr,
+                                             plan->direct_segs, static_cast<int>(h.direct_docs.size()), h.N,
+                                             h.D, h.L, 0, r, s);
+            return de;
+        });
+    // range: dy's grid carries dx's scale s_dy (its magnitude alone); x's carries s_x ex
+    // (as in dk), and the sum-group kernels multiply dy's spectra by ed before the
+    // products, so that dk's products sit where dk's own passes put them.  dy's word is
+    // {s_dy, 1 / s_dy} (dx's inverse); x's inverse factor also carries 1 / s_dy, and the
+    // per-pair words 1 / ed: dk's inverse undoes all of it.
+    float ex, ed;
+    dk_split(h, &ex, &ed);
+    float2* w = prescale_words(workspace, plan->dk_hdr_off);
+    uint16_t* parts = reinterpret_cast<uint16_t*>(prescale_work(workspace, plan->dk_hdr_off));
+    const size_t n_tasks = static_cast<size_t>(n_cols) * h.npb;
+    const int slot_dy = hint_slot(rubiconv_plan_s::kHintDx, dy);
+    const int slot_x = hint_slot(rubiconv_plan_s::kHintDkX, x);
+    const SpecScale spec_dy{parts + (n_tasks + 7) / 8 * 8, w + 1, scale_guess(plan, slot_dy),
+                            plan->scale_hint_dev + slot_dy, 1.0f, nullptr};
+    const SpecScale spec_x{parts, w, scale_guess(plan, slot_x), plan->scale_hint_dev + slot_x, ex, w + 1};
+    if (e == hipSuccess) e = enqueue_col_fwd(plan, dy, h.y_dtype, dygrid, {plan->ones, w + 1}, stream, &spec_dy);
+    rec.mark("bwd_col_fwd_dy");
+    if (e == hipSuccess) e = enqueue_col_fwd(plan, x, h.x_dtype, xgrid, {plan->ones, w}, stream, &spec_x);
+    rec.mark("bwd_col_fwd_x");
+    // dk: the sum groups against x's grid, their sums written over x's grid (dy's stays)
+    if (e == hipSuccess)
+        e = enqueue_rows(plan, xgrid, plan->grid_pb_stride, plan->grad_t, dygrid, 1, true, stream, ed, true);
+    rec.mark("bwd_dk_row_conv");
+    if (e == hipSuccess) e = enqueue_col_inv(plan, xgrid, r, RUBICONV_F32, true, {plan->dk_unscale, w}, stream);
+    rec.mark("bwd_dk_col_inv");
+    if (e == hipSuccess && direct) e = join_direct(plan, stream, rec);
+    if (e == hipSuccess)
+        e = rubiconv::launch_lag_sum(r, plan->dk_sum_segs, static_cast<int>(h.dk_sum_segs.size()), h.N,
+                                     h.D, h.L, dk, stream);
+    rec.mark("bwd_dk_lag_sum");
+    // dx: the correlation with the filter on dy's grid, in place
+    if (e == hipSuccess)
+        e = enqueue_rows(plan, spectrum, plan->cls_pb_stride, plan->doc_t, dygrid, 1, false, stream);
+    rec.mark("bwd_dx_row_conv");
+    if (e == hipSuccess)
+        e = enqueue_col_inv(plan, dygrid, dx, h.x_dtype, false, {filter_scales(plan, spectrum), w + 1}, stream);
+    rec.mark("bwd_dx_col_inv");
     return e == hipSuccess ? RUBICONV_OK : RUBICONV_ERR_HIP;
 }
 

@@ -261,6 +261,12 @@ def test_null_arguments_rejected_before_any_device_work():
     assert lib.rubiconv_plan(None, 1, 8, 2, 3, 1, None, 0, 0, 0, None) == 1
     assert lib.rubiconv_spectrum_bytes(None) == 0 and lib.rubiconv_workspace_bytes(None) == 0
     assert lib.rubiconv_status_string(2) == b"invalid cu_seqlens"
+    fake = 1 << 20   # never dereferenced: the calls return before launching
+    assert lib.rubiconv_packed_conv_backward(None, fake, fake, fake, fake, fake, fake, None) == 1
+    assert lib.rubiconv_packed_conv_backward(plan.handle, fake, fake, fake, None, fake, fake, None) == 1
+    assert lib.rubiconv_packed_conv_backward(plan.handle, fake, fake, fake, fake, fake, fake + 4, None) == 1
+    # the fused backward may run dx and dk in sequence in the dk workspace
+    assert plan.dk_workspace_bytes >= plan.workspace_bytes
     lib.rubiconv_plan_destroy(None)
 
 
@@ -294,6 +300,7 @@ def test_stream_calls_without_device_report_hip_error():
     fake = 1 << 20   # never dereferenced: the call returns before launching
     assert lib.rubiconv_packed_conv(plan.handle, fake, fake, fake, fake, None) == 5
     assert lib.rubiconv_filter_spectrum(plan.handle, fake, fake, fake, None) == 5
+    assert lib.rubiconv_packed_conv_backward(plan.handle, fake, fake, fake, fake, fake, fake, None) == 5
 
 
 def test_buffer_sizes_cover_the_layouts():

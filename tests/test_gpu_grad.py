@@ -320,3 +320,71 @@ def test_generic_long_rows(device, monkeypatch, dtype):
     bsd = np.stack([rng.integers(0, W.B, n), rng.integers(0, W.N, n), rng.integers(0, W.D, n)], 1)
     ref = oracle.grad_x_at(W.filters, dyv, W.cu_seqlens, bsd, threads=ORACLE_THREADS)
     assert rel_l2(dx[bsd[:, 0], bsd[:, 1], bsd[:, 2]], ref) <= TOL[dtype]
+
+
+def _fused_and_separate(W, device, seed):
+    """dx and dk from rubiconv_packed_conv_backward and from the two separate calls on one
+    plan and the same inputs (float64 arrays), and the plan."""
+    import torch
+    import paper_2605_08451_amd as rc
+    x, k = to_device(W, device)
+    dyv, dy = _dy(W, seed)
+    dy = dy.to(device)
+    plan = rc.Plan(W.cu_seqlens, N=W.N, D=W.D, L=W.L, x_dtype=W.x_dtype, y_dtype=W.y_dtype)
+    ws = plan.new_dk_workspace(device)
+    spec = rc.filter_spectrum(plan, k, workspace=ws)
+    dx_s = rc.packed_conv_dx(plan, dy, spec, workspace=ws)
+    dk_s = rc.packed_conv_dk(plan, x, dy, workspace=ws)
+    dx_f, dk_f = rc.packed_conv_backward(plan, x, dy, spec, workspace=ws)
+    torch.cuda.synchronize(device)
+    same_dx = bool(torch.equal(dx_s, dx_f))
+    out = [t.float().cpu().numpy().astype(np.float64) for t in (dx_s, dk_s, dx_f, dk_f)]
+    return dyv, same_dx, out, plan
+
+
+FUSED_CASES = {
+    # every document on the matrix-core row kernels: the fused path
+    "mid-length": dict(config=2),
+    "sum-groups": dict(rows=[[930, 1000, 960, 880, 990, 940, 905, 870, 1000, 975, 12000 - 9450],
+                             [3000, 3100, 2950, 2900, 12000 - 11950], [6000, 6000]], N=12000, D=32),
+    "direct": dict(rows=[[40] * 30 + [2800], [17, 63, 5, 1, 64] * 8 + [4000 - 1200]], N=4000, D=32,
+                   direct=64),
+    # the two calls in sequence: fp32 grids, and rows of 129-256 points on the VALU kernels
+    "fp32": dict(config=0),
+    "valu-rows": dict(rows=[[20000, 4000]], N=24000, D=32),
+}
+
+
+@pytest.mark.parametrize("case", list(FUSED_CASES))
+def test_fused_backward(device, monkeypatch, case):
+    """rubiconv_packed_conv_backward against the separate dx and dk calls: dx bit for bit,
+    dk within the bar of the oracle (every lag where the oracle is cheap, sampled at full
+    size) and close to the separate call's; on the fallback both bit for bit."""
+    spec = FUSED_CASES[case]
+    if "direct" in spec:
+        monkeypatch.setenv("RUBICONV_DIRECT_MAX", str(spec["direct"]))
+    if "config" in spec:
+        W = wl.make_config(spec["config"])
+    else:
+        W = wl.make_case(spec["rows"], D=spec["D"], L=spec["N"], x_dtype="bf16", seed=len(case))
+    _say(f"[fused backward] {case}")
+    dyv, same_dx, (dx_s, dk_s, dx_f, dk_f), plan = _fused_and_separate(W, device, seed=3 + len(case))
+    assert same_dx, f"{case}: dx differs from rubiconv_packed_conv_dx"
+    fused = W.x_dtype == "bf16" and max(int(m) for m in plan.doc_table()[:, 4]) <= 128
+    if not fused:
+        assert np.array_equal(dk_f, dk_s), f"{case}: the fallback's dk differs"
+        return
+    if "direct" in spec:
+        assert plan.info()["n_direct"] > 0
+    close = rel_l2(dk_f, dk_s)
+    if W.B * W.N * W.D <= 2_000_000:
+        g, worst = _check_dk(dk_f, oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L, threads=ORACLE_THREADS),
+                             "bf16", case)
+    else:
+        rng = np.random.default_rng(31)
+        dt = np.stack([rng.integers(0, W.D, 400), rng.integers(0, W.L, 400)], 1)
+        refk = oracle.grad_k_at(W.x, dyv, W.cu_seqlens, W.L, dt, threads=ORACLE_THREADS)
+        g = worst = rel_l2(dk_f[dt[:, 0], dt[:, 1]], refk)
+        assert g <= TOL["bf16"], f"{case}: sampled dk {g:.2e}"
+    _say(f"[fused backward] {case}: dk {g:.2e} / {worst:.2e}, against the separate call {close:.2e}")
+    assert close <= 5e-3, close

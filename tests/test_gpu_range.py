@@ -120,12 +120,19 @@ def test_gradient_range(device, scale):
     spec = rc.filter_spectrum(plan, kd, workspace=ws)
     dx = rc.packed_conv_dx(plan, dy, spec, workspace=ws).float().cpu().numpy().astype(np.float64)
     dk = rc.packed_conv_dk(plan, xd, dy).cpu().numpy().astype(np.float64)
+    # the fused backward: dy's grid at dx's scale, dk's split applied in the row stage
+    dxf, dkf = rc.packed_conv_backward(plan, xd, dy, spec)
+    dxf, dkf = dxf.float().cpu().numpy().astype(np.float64), dkf.cpu().numpy().astype(np.float64)
     assert np.isfinite(dx).all() and np.isfinite(dk).all(), scale
-    g, d = assert_parity(dx, oracle.grad_x(W.filters, dyv, W.cu_seqlens, threads=ORACLE_THREADS),
-                         W.cu_seqlens, "bf16", f"dx scale {scale}")
-    gk, wk = _check_dk(dk, oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L, threads=ORACLE_THREADS),
-                       "bf16", f"dk scale {scale}")
+    assert np.isfinite(dxf).all() and np.isfinite(dkf).all(), scale
+    refx = oracle.grad_x(W.filters, dyv, W.cu_seqlens, threads=ORACLE_THREADS)
+    refk = oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L, threads=ORACLE_THREADS)
+    g, d = assert_parity(dx, refx, W.cu_seqlens, "bf16", f"dx scale {scale}")
+    gk, wk = _check_dk(dk, refk, "bf16", f"dk scale {scale}")
     _say(f"[range] dy scale {scale}: dx {g:.2e} / {d:.2e}, dk {gk:.2e} / {wk:.2e}")
+    g, d = assert_parity(dxf, refx, W.cu_seqlens, "bf16", f"fused dx scale {scale}")
+    gk, wk = _check_dk(dkf, refk, "bf16", f"fused dk scale {scale}")
+    _say(f"[range] fused, dy scale {scale}: dx {g:.2e} / {d:.2e}, dk {gk:.2e} / {wk:.2e}")
 
 
 @pytest.mark.parametrize("loud", ["direct", "transform"])
