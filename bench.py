@@ -114,7 +114,7 @@ def backward_measurement(rc, plan, W, x, k, spec, ws, stream, args):
     """The two gradient calls on the same batch: dx (rubiconv_packed_conv_dx) and dk
     (rubiconv_packed_conv_dk) for a seeded upstream gradient of y's shape and dtype, each
     timed as its own step, with per-kernel event times of the same calls; then both in
-    one call (rubiconv_packed_conv_backward) as a step of its own."""
+    one call (rubiconv_packed_conv_backward) as a step of its own (graph replay only)."""
     import torch
     import workloads as wl
     dev = x.device
@@ -142,11 +142,10 @@ def backward_measurement(rc, plan, W, x, k, spec, ws, stream, args):
     bwd_ms = time_step(launch_bwd, stream, args.steps, args.warmup, args.eager)
     progress("gradient stages")
     calls = min(args.steps, PROFILE_CALLS)
-    plan.profile_start(3 * calls)
+    plan.profile_start(2 * calls)
     for _ in range(calls):
         launch_dx(stream)
         launch_dk(stream)
-        launch_bwd(stream)
     kt = plan.profile_read()
     plan.profile_start(0)
     tok_ch = W.B * W.N * W.D

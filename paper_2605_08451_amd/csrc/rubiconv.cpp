@@ -297,11 +297,14 @@ struct StageRecorder {
         }
     }
     bool active() const { return slot >= 0; }
-    void mark(const std::string& name) {
-        if (slot < 0 || k + 1 >= rubiconv_plan_s::kEventsPerCall) return;
+    // records the stage's end; returns that event (null while not recording)
+    hipEvent_t mark(const std::string& name) {
+        if (slot < 0 || k + 1 >= rubiconv_plan_s::kEventsPerCall) return nullptr;
         ++k;
-        (void)hipEventRecord(pl->prof_events[slot * rubiconv_plan_s::kEventsPerCall + k], stream);
+        hipEvent_t ev = pl->prof_events[slot * rubiconv_plan_s::kEventsPerCall + k];
+        if (hipEventRecord(ev, stream) != hipSuccess) return nullptr;
         pl->prof_names[slot].push_back(name);
+        return ev;
     }
 };
 
@@ -426,9 +429,11 @@ hipError_t enqueue_col_fwd(rubiconv_plan_s* plan, const void* in, int in_dtype, 
 // The row stage on `grid` against the second grid `fgrid` (a filter spectrum, or x's grid
 // for the filter gradient: own_rows, the sum groups), then the long rows' inverse first
 // level.  dscale and out2 apply to the sum groups (launch_row_dense).
+// `after`: an event just recorded on `stream` (a stage-timing mark), which the side
+// streams then wait on in place of a fork event of their own (one marker less).
 hipError_t enqueue_rows(rubiconv_plan_s* plan, const void* fgrid, int64_t fgrid_pb_stride, const LaunchTables& t,
-                        void* grid, int corr, bool own_rows, hipStream_t stream, float dscale = 1.0f,
-                        bool out2 = false) {
+                        void* grid, int corr, bool own_rows, hipStream_t stream, hipEvent_t after = nullptr,
+                        float dscale = 1.0f, bool out2 = false) {
     const HostPlan& h = plan->h;
     const bool half = h.grid_half;
     hipError_t e = hipSuccess;
@@ -500,8 +505,12 @@ hipError_t enqueue_rows(rubiconv_plan_s* plan, const void* fgrid, int64_t fgrid_
         for (const Launch& L : launches)
             if (e == hipSuccess) e = launch_one(L, stream);
     } else if (e == hipSuccess) {
-        e = hipEventRecord(plan->fork, stream);
-        for (int k = 0; k < nside && e == hipSuccess; ++k) e = hipStreamWaitEvent(plan->side[k], plan->fork, 0);
+        hipEvent_t fork = after;
+        if (fork == nullptr) {
+            fork = plan->fork;
+            e = hipEventRecord(fork, stream);
+        }
+        for (int k = 0; k < nside && e == hipSuccess; ++k) e = hipStreamWaitEvent(plan->side[k], fork, 0);
         std::vector<double> load(nside, 0.0);
         for (size_t i = 1; i < launches.size() && e == hipSuccess; ++i) {
             const Launch& L = launches[i];
@@ -543,8 +552,8 @@ hipError_t enqueue_conv(rubiconv_plan_s* plan, const void* in, int in_dtype, con
                         const char* tag, hipStream_t stream, StageRecorder& rec,
                         const SpecScale* spec = nullptr) {
     hipError_t e = enqueue_col_fwd(plan, in, in_dtype, grid, in_sc, stream, spec);
-    rec.mark(stage(tag, "col_fwd"));
-    if (e == hipSuccess) e = enqueue_rows(plan, fgrid, fgrid_pb_stride, t, grid, corr, own_rows, stream);
+    const hipEvent_t col_done = rec.mark(stage(tag, "col_fwd"));
+    if (e == hipSuccess) e = enqueue_rows(plan, fgrid, fgrid_pb_stride, t, grid, corr, own_rows, stream, col_done);
     rec.mark(stage(tag, "row_conv"));
     if (e == hipSuccess) e = enqueue_col_inv(plan, grid, out, out_dtype, own_rows, out_sc, stream);
     rec.mark(stage(tag, "col_inv"));
@@ -974,10 +983,11 @@ rubiconv_status_t rubiconv_packed_conv_backward(rubiconv_plan_t plan, const void
     if (e == hipSuccess) e = enqueue_col_fwd(plan, dy, h.y_dtype, dygrid, {plan->ones, w + 1}, stream, &spec_dy);
     rec.mark("bwd_col_fwd_dy");
     if (e == hipSuccess) e = enqueue_col_fwd(plan, x, h.x_dtype, xgrid, {plan->ones, w}, stream, &spec_x);
-    rec.mark("bwd_col_fwd_x");
+    const hipEvent_t cols_done = rec.mark("bwd_col_fwd_x");
     // dk: the sum groups against x's grid, their sums written over x's grid (dy's stays)
     if (e == hipSuccess)
-        e = enqueue_rows(plan, xgrid, plan->grid_pb_stride, plan->grad_t, dygrid, 1, true, stream, ed, true);
+        e = enqueue_rows(plan, xgrid, plan->grid_pb_stride, plan->grad_t, dygrid, 1, true, stream, cols_done, ed,
+                         true);
     rec.mark("bwd_dk_row_conv");
     if (e == hipSuccess) e = enqueue_col_inv(plan, xgrid, r, RUBICONV_F32, true, {plan->dk_unscale, w}, stream);
     rec.mark("bwd_dk_col_inv");
@@ -985,10 +995,10 @@ rubiconv_status_t rubiconv_packed_conv_backward(rubiconv_plan_t plan, const void
     if (e == hipSuccess)
         e = rubiconv::launch_lag_sum(r, plan->dk_sum_segs, static_cast<int>(h.dk_sum_segs.size()), h.N,
                                      h.D, h.L, dk, stream);
-    rec.mark("bwd_dk_lag_sum");
+    const hipEvent_t dk_done = rec.mark("bwd_dk_lag_sum");
     // dx: the correlation with the filter on dy's grid, in place
     if (e == hipSuccess)
-        e = enqueue_rows(plan, spectrum, plan->cls_pb_stride, plan->doc_t, dygrid, 1, false, stream);
+        e = enqueue_rows(plan, spectrum, plan->cls_pb_stride, plan->doc_t, dygrid, 1, false, stream, dk_done);
     rec.mark("bwd_dx_row_conv");
     if (e == hipSuccess)
         e = enqueue_col_inv(plan, dygrid, dx, h.x_dtype, false, {filter_scales(plan, spectrum), w + 1}, stream);
