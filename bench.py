@@ -70,7 +70,7 @@ def progress(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-# calls timed stage by stage with the library's HIP events (each call holds up to 64)
+# calls timed stage by stage with the library's HIP events (up to 16 per call)
 PROFILE_CALLS = 20
 
 

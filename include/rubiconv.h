@@ -344,17 +344,19 @@ rubiconv_status_t rubiconv_plan_doc_table(rubiconv_plan_t plan, int32_t* out, in
  * Stage timing (tracing; not for production loops).  After
  * rubiconv_profile_start(plan, max_calls), each of the next max_calls calls of
  * rubiconv_filter_spectrum / rubiconv_packed_conv / rubiconv_packed_conv_dx /
- * rubiconv_packed_conv_dk with this plan records a HIP
- * event on its stream before its first kernel and after every kernel, so each
- * kernel's duration is measured on the stream it runs on.  rubiconv_profile_read
- * waits for the recorded events and returns, per kernel name, the number of
- * launches and their total milliseconds (host array of cap entries; *n receives
- * the number of distinct kernels).  Profiling state belongs to the plan: use one
- * stream and one thread while it is active.  max_calls = 0 stops profiling.
+ * rubiconv_packed_conv_dk / rubiconv_packed_conv_backward with this plan records a
+ * HIP event on its stream before its first kernel and after every stage (a stage is
+ * one kernel, or the launches of the row stage across the plan's side streams up to
+ * their join), at most 16 per call.  rubiconv_profile_read waits for the recorded
+ * events and returns, per stage name, the number of calls that recorded it and
+ * their total milliseconds (host array of cap entries; *n receives the number of
+ * distinct stages).  The plan keeps the events it creates for this until it is
+ * destroyed.  Profiling state belongs to the plan: use one stream and one thread
+ * while it is active.  max_calls = 0 stops profiling.
  * Errors: RUBICONV_ERR_ARG, RUBICONV_ERR_ALLOC (event creation), RUBICONV_ERR_HIP.
  */
 typedef struct {
-    char name[32];   /* kernel name, e.g. "col_fwd" */
+    char name[32];   /* stage name, e.g. "col_fwd" */
     int launches;
     double total_ms;
 } rubiconv_kernel_time_t;

@@ -85,9 +85,11 @@ struct rubiconv_plan_s {
     hipEvent_t join[kSideStreams] = {};
     std::mutex launch_mu;
     // stage timing (rubiconv_profile_start / _read)
-    static constexpr int kEventsPerCall = 64;  // before the first kernel + after each launch
+    static constexpr int kEventsPerCall = 16;  // before the first kernel + after each stage
     int prof_max = 0, prof_used = 0;
-    std::vector<hipEvent_t> prof_events;           // prof_max * kEventsPerCall
+    // at least prof_max * kEventsPerCall events, created as profiling first needs them and
+    // kept (re-recorded by later profiling) until the plan is destroyed
+    std::vector<hipEvent_t> prof_events;
     std::vector<std::vector<std::string>> prof_names;
 };
 
@@ -1040,18 +1042,15 @@ rubiconv_status_t rubiconv_plan_doc_table(rubiconv_plan_t plan, int32_t* out, in
 
 rubiconv_status_t rubiconv_profile_start(rubiconv_plan_t plan, int max_calls) {
     if (!plan || max_calls < 0) return RUBICONV_ERR_ARG;
-    destroy_events(plan);
+    plan->prof_max = plan->prof_used = 0;
+    plan->prof_names.clear();
     if (max_calls == 0) return RUBICONV_OK;
     if (!plan->device_ready) return RUBICONV_ERR_HIP;
-    const int n = max_calls * rubiconv_plan_s::kEventsPerCall;
-    plan->prof_events.reserve(n);
-    for (int i = 0; i < n; ++i) {
+    const size_t n = static_cast<size_t>(max_calls) * rubiconv_plan_s::kEventsPerCall;
+    while (plan->prof_events.size() < n) {
         hipEvent_t ev;
         // timing only: no system-scope fence at each stage boundary
-        if (hipEventCreateWithFlags(&ev, hipEventDisableSystemFence) != hipSuccess) {
-            destroy_events(plan);
-            return RUBICONV_ERR_ALLOC;
-        }
+        if (hipEventCreateWithFlags(&ev, hipEventDisableSystemFence) != hipSuccess) return RUBICONV_ERR_ALLOC;
         plan->prof_events.push_back(ev);
     }
     plan->prof_names.assign(max_calls, {});
