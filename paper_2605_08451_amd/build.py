@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "librubiconv.so")
 BUILD = os.path.join(ROOT, "_build")
 SOURCES = ["kernels.hip", "row_fast.hip", "row_dense.hip", "col_mfma.hip", "plan_build.cpp", "rubiconv.cpp",
-           "ct_kernels.hip", "ct_plan.cpp", "ct_api.cpp", "long_rows.hip", "noalloc.hip"]
+           "ct_kernels.hip", "ct_plan.cpp", "ct_api.cpp", "long_rows.hip", "noalloc.hip", "direct_mfma.hip"]
 ARCH = "gfx950"
 
 

@@ -534,9 +534,6 @@ __global__ __launch_bounds__(256) void transpose_pairs_kernel(const float* __res
 //   kDirectXcorr: out[tau] = sum_{t = tau}^{len-1} a[t] b[t - tau], tau < min(len, L)
 //                 (the filter gradient's per-document correlation of dy with x, fp32)
 // All sums run in fp32 in ascending lag (or token) order.
-constexpr int kDirectConv = 0;
-constexpr int kDirectCorr = 1;
-constexpr int kDirectXcorr = 2;
 
 template <class T>
 __device__ __forceinline__ float load_elem(const T* p, int64_t i);

@@ -144,6 +144,21 @@ hipError_t launch_col_inv_mfma(int y_dtype, const void* grid, int64_t grid_pb_st
                                GridScale sc, const void* mtab, int n_cols, int npb,
                                hipStream_t stream);
 
+// Direct-path modes (launch_direct, launch_direct_mfma)
+constexpr int kDirectConv = 0;
+constexpr int kDirectCorr = 1;
+constexpr int kDirectXcorr = 2;
+
+// The direct path on the matrix cores (direct_mfma.hip): the same three modes for bf16 a
+// (x, or dy) and b (x, mode 2) of documents of at most kMaxDirectMfma tokens, D a multiple
+// of 32, a, b and out 16-byte aligned.  taps: [D][T] bf16 pairs (launch_split_taps), T >=
+// min(L, longest document); unused in mode 2.  Outputs: y or dx in bf16, the correlation
+// in fp32 (as launch_direct).
+hipError_t launch_direct_mfma(int mode, const void* a, const void* b, const uint32_t* taps, int T,
+                              const Seg* docs, int n_docs, int N, int D, int L, void* out, hipStream_t stream);
+// taps[d][t] = bf16(k[d][t]) | bf16(k[d][t] - bf16(k[d][t])) << 16, t < T (row stride ld of k)
+hipError_t launch_split_taps(const float* filters, int D, int T, int ld, uint32_t* taps, hipStream_t stream);
+
 // Documents computed by their defining sums (the direct path; kernels.hip):
 // mode 0 out = y from a = x, mode 1 out = dx from a = dy, mode 2 out = the
 // per-document correlation of a = dy with b = x at lags tau < min(len, L), written at

@@ -20,6 +20,12 @@ constexpr int kMaxDenseBlocks = 8;  // matrix-core row pass: m <= 16 * kMaxDense
 
 // Longest document the direct path may take (its per-output sums stay short).
 constexpr int kMaxDirect = 128;
+// Longest document the direct path takes on the matrix cores (bf16 inputs, D a multiple of
+// 32): its sums run as blocked Toeplitz products, one LDS row of this many tokens per
+// channel; it is also that path's default limit (measured: rows of 1024 tokens leave one
+// workgroup per CU and made the LM-packing workload 6% slower than the transforms, rows of
+// 512 three workgroups and 7% faster)
+constexpr int kMaxDirectMfma = 512;
 // Default: documents of at most this many tokens take the direct path, when together
 // they would hold at least 1/kDirectMinShare of the transform grid (measured: a few
 // short documents among long ones cost more on their own launch than they save).

@@ -349,7 +349,7 @@ std::vector<int> merge_size_classes(const std::vector<int>& m0, int max_merge_m)
 
 BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_docs,
                            const int32_t* cu, int x_dtype, int y_dtype, int n1, int direct_max,
-                           bool direct_by_share, bool merge_classes) {
+                           bool direct_by_share, bool merge_classes, bool direct_mfma) {
     if (!out || !cu || B < 1 || N < 1 || D < 1 || L < 1 || max_docs < 1) return BuildError::kArg;
     if (x_dtype < 0 || x_dtype > 1 || y_dtype < 0 || y_dtype > 1) return BuildError::kArg;
     if (n1 == 0) n1 = 256;
@@ -367,7 +367,9 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
             if (c[k + 1] < c[k] || c[k + 1] > N) return BuildError::kSeqlens;
     }
 
-    if (direct_max < 0 || direct_max > kMaxDirect) return BuildError::kArg;
+    // the matrix-core direct path: bf16 x and dy, channels in blocks of 32
+    direct_mfma = direct_mfma && direct_mfma_possible(x_dtype, y_dtype, D);
+    if (direct_max < 0 || direct_max > (direct_mfma ? kMaxDirectMfma : kMaxDirect)) return BuildError::kArg;
     if (direct_by_share && direct_max > 0) {
         // the direct path pays once its documents would hold a real share of the
         // transform grid (each at least one whole N1-point column grid); a handful of
@@ -448,6 +450,7 @@ BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_do
     for (const Seg& s : p.docs) class_of_m[s.m] = 0;
 
     if (!p.direct_docs.empty()) p.direct_taps = std::min(L, direct_max);
+    p.direct_mfma = direct_mfma && !p.direct_docs.empty();
     // size classes, ascending m: twiddles, spectrum offsets, filter taps
     {
         size_t tw_floats = 0;

@@ -21,6 +21,7 @@ struct HostPlan {
     // defining sums, computed directly (direct_docs: row, start, len; m = P = 0).
     int direct_max = 0;
     int direct_taps = 0;                // taps the direct path reads: min(L, direct_max)
+    bool direct_mfma = false;           // the direct path on the matrix cores (taps [D][T] as bf16 hi, lo)
     std::vector<Seg> direct_docs;
     std::vector<int32_t> direct_index;  // index of each direct document inside its row
     // every non-empty document in row order (transformed ones with their m and P,
@@ -89,6 +90,12 @@ struct HostPlan {
 // Smallest 2^a 3^b 5^c >= v (v >= 1).
 int smooth_ceil(int v);
 
+// The direct path can run on the matrix cores: bf16 x and dy (dtype 1), channels in
+// blocks of 32.
+inline bool direct_mfma_possible(int x_dtype, int y_dtype, int D) {
+    return x_dtype == 1 && y_dtype == 1 && D % 32 == 0;
+}
+
 // MFMA operand tables of the N1 = 256 matrix-core column passes (kMtEntries
 // 16-byte entries, 4 x uint32 each, in the order of kernels.hpp's kMt* offsets).
 void build_mfma_tables(std::vector<uint32_t>* out);
@@ -113,7 +120,8 @@ void build_batch_tables(int m, int n1, std::vector<uint32_t>* out);
 // that removes a filter class and saves bytes overall (merge_size_classes).
 BuildError build_host_plan(HostPlan* out, int B, int N, int D, int L, int max_docs,
                            const int32_t* cu_seqlens, int x_dtype, int y_dtype, int n1,
-                           int direct_max, bool direct_by_share, bool merge_classes);
+                           int direct_max, bool direct_by_share, bool merge_classes,
+                           bool direct_mfma = false);
 
 // Row sizes after class merging, one per entry of m0 (each a valid size for its
 // document).  Sizes u_1 < ... < u_k with document counts c_t; a class of size u_j

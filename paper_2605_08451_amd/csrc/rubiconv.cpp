@@ -12,6 +12,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <initializer_list>
 #include <mutex>
 #include <new>
 #include <string>
@@ -63,7 +64,8 @@ struct rubiconv_plan_s {
     LaunchTables dk_t{};         // grad_t restricted to the filter gradient's output documents
     const Seg* dk_sum_segs = nullptr;  // those and the direct documents, longest first (lag sum)
     const Seg* direct_segs = nullptr;  // documents of the direct path
-    size_t dtaps_off = 0;        // spectrum: the direct path's taps [direct_taps][D] fp32
+    size_t dtaps_off = 0;        // spectrum: the direct path's taps, [direct_taps][D] fp32 or (matrix
+                                 // cores) [D][direct_taps] bf16 pairs hi | lo << 16
     size_t sscale_off = 0;       // spectrum: the filter's range scales, float2 per channel pair
     size_t partials_off = 0;     // filter call's workspace: |k| sums per tap tile and channel
     size_t ws_hdr_off = 0;       // workspace: prescales of x and dy, then the amax partials
@@ -339,6 +341,28 @@ const float* direct_taps(const rubiconv_plan_s* plan, const void* spectrum) {
     return reinterpret_cast<const float*>(static_cast<const char*>(spectrum) + plan->dtaps_off);
 }
 
+// The matrix-core direct path moves 16-byte pieces of 8 channels: with it the tensors of
+// a call must be 16-byte aligned.
+bool direct_aligned(const rubiconv_plan_s* plan, std::initializer_list<const void*> ptrs) {
+    if (!plan->h.direct_mfma) return true;
+    for (const void* q : ptrs)
+        if (reinterpret_cast<uintptr_t>(q) & 15) return false;
+    return true;
+}
+
+// The direct path's sums (launch_direct's arguments): on the matrix cores when the plan
+// says so, with the taps the filter call wrote for them.
+hipError_t direct_sums(const rubiconv_plan_s* plan, int mode, int a_dtype, const void* a, int b_dtype,
+                       const void* b, const float* taps, int out_dtype, void* out, hipStream_t s) {
+    const HostPlan& h = plan->h;
+    const int n = static_cast<int>(h.direct_docs.size());
+    if (h.direct_mfma)
+        return rubiconv::launch_direct_mfma(mode, a, b, reinterpret_cast<const uint32_t*>(taps), h.direct_taps,
+                                            plan->direct_segs, n, h.N, h.D, h.L, out, s);
+    return rubiconv::launch_direct(mode, h.direct_max, a_dtype, a, b_dtype, b, taps, plan->direct_segs, n, h.N,
+                                   h.D, h.L, out_dtype, out, s);
+}
+
 // The filter's per-pair range scales inside a spectrum buffer (unit scales on fp32 grids).
 const float2* filter_scales(const rubiconv_plan_s* plan, const void* spectrum) {
     if (!plan->h.grid_half) return plan->ones;
@@ -585,14 +609,26 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
     *out = nullptr;
     rubiconv_plan_s* pl = new (std::nothrow) rubiconv_plan_s();
     if (!pl) return RUBICONV_ERR_ALLOC;
-    // RUBICONV_DIRECT_MAX (0 .. kMaxDirect) overrides the direct path's length limit
-    int direct_max = rubiconv::kDefaultDirect;
+    // The direct path runs on the matrix cores where it can (bf16 x and dy, D a multiple of
+    // 32; RUBICONV_DIRECT_MFMA = 0 keeps it on the VALU kernel), for documents of up to
+    // kMaxDirectMfma tokens, else kDefaultDirect; RUBICONV_DIRECT_MAX (0 .. kMaxDirect, or
+    // kMaxDirectMfma on the matrix cores) overrides that limit
+    bool direct_mfma = true;
+    if (const char* v = std::getenv("RUBICONV_DIRECT_MFMA")) {
+        if (std::strcmp(v, "0") != 0 && std::strcmp(v, "1") != 0) {
+            delete pl;
+            return RUBICONV_ERR_ARG;
+        }
+        direct_mfma = v[0] == '1';
+    }
+    int direct_max = direct_mfma && rubiconv::direct_mfma_possible(x_dtype, y_dtype, D) ? rubiconv::kMaxDirectMfma
+                                                                                      : rubiconv::kDefaultDirect;
     bool direct_by_share = true;  // an explicit limit applies as given
     if (const char* v = std::getenv("RUBICONV_DIRECT_MAX")) {
         direct_by_share = false;
         char* end = nullptr;
         const long n = std::strtol(v, &end, 10);
-        if (end == v || *end != '\0' || n < 0 || n > rubiconv::kMaxDirect) {
+        if (end == v || *end != '\0' || n < 0 || n > rubiconv::kMaxDirectMfma) {
             delete pl;
             return RUBICONV_ERR_ARG;
         }
@@ -609,7 +645,7 @@ rubiconv_status_t rubiconv_plan(rubiconv_plan_t* out, int B, int N, int D, int L
     }
     BuildError be = rubiconv::build_host_plan(&pl->h, B, N, D, L, max_docs, cu_seqlens_host,
                                               static_cast<int>(x_dtype), static_cast<int>(y_dtype),
-                                              n1, direct_max, direct_by_share, merge);
+                                              n1, direct_max, direct_by_share, merge, direct_mfma);
     if (be != BuildError::kOk) {
         delete pl;
         if (be == BuildError::kArg) return RUBICONV_ERR_ARG;
@@ -727,7 +763,12 @@ rubiconv_status_t rubiconv_filter_spectrum(rubiconv_plan_t plan, const float* fi
             e = rubiconv::launch_lr_step(false, spectrum, plan->cls_pb_stride, it, plan->doc_t.tw, h.n1,
                                          h.npb, stream);
     rec.mark("filter_col_fwd");
-    if (e == hipSuccess && h.direct_taps > 0) {  // the direct path's taps, [T][D] fp32
+    if (e == hipSuccess && h.direct_taps > 0 && h.direct_mfma) {  // [D][T] bf16 hi, lo
+        e = rubiconv::launch_split_taps(filters, h.D, h.direct_taps, h.L,
+                                        reinterpret_cast<uint32_t*>(static_cast<char*>(spectrum) + plan->dtaps_off),
+                                        stream);
+        rec.mark("filter_direct_taps");
+    } else if (e == hipSuccess && h.direct_taps > 0) {  // the direct path's taps, [T][D] fp32
         e = rubiconv::launch_transpose(filters, h.D, h.direct_taps, h.L,
                                        reinterpret_cast<float*>(static_cast<char*>(spectrum) + plan->dtaps_off),
                                        h.D, nullptr, stream);
@@ -742,7 +783,7 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
     if (!aligned(spectrum) || !aligned(workspace)) return RUBICONV_ERR_ARG;
     const size_t esz = plan->h.x_dtype == RUBICONV_F32 ? 4 : 2;
     const size_t ysz = plan->h.y_dtype == RUBICONV_F32 ? 4 : 2;
-    if (reinterpret_cast<uintptr_t>(x) % esz || reinterpret_cast<uintptr_t>(y) % ysz)
+    if (reinterpret_cast<uintptr_t>(x) % esz || reinterpret_cast<uintptr_t>(y) % ysz || !direct_aligned(plan, {x, y}))
         return RUBICONV_ERR_ARG;
     if (!plan->device_ready) return RUBICONV_ERR_HIP;
     std::lock_guard<std::mutex> lock(plan->launch_mu);
@@ -752,9 +793,7 @@ rubiconv_status_t rubiconv_packed_conv(rubiconv_plan_t plan, const void* x, cons
     hipError_t e = hipSuccess;
     if (direct)
         e = fork_direct(plan, stream, rec, "direct", [&](hipStream_t s) {
-            return rubiconv::launch_direct(0, h.direct_max, h.x_dtype, x, 0, nullptr, direct_taps(plan, spectrum),
-                                           plan->direct_segs, static_cast<int>(h.direct_docs.size()),
-                                           h.N, h.D, h.L, h.y_dtype, y, s);
+            return direct_sums(plan, 0, h.x_dtype, x, 0, nullptr, direct_taps(plan, spectrum), h.y_dtype, y, s);
         });
     // range scales: the filter's per pair, and x's power-of-two prescale when asked for.
     // On the matrix-core path the column pass first runs at the scale the plan's last
@@ -785,7 +824,8 @@ rubiconv_status_t rubiconv_packed_conv_dx(rubiconv_plan_t plan, const void* dy, 
     if (!aligned(spectrum) || !aligned(workspace)) return RUBICONV_ERR_ARG;
     const size_t xsz = plan->h.x_dtype == RUBICONV_F32 ? 4 : 2;
     const size_t ysz = plan->h.y_dtype == RUBICONV_F32 ? 4 : 2;
-    if (reinterpret_cast<uintptr_t>(dy) % ysz || reinterpret_cast<uintptr_t>(dx) % xsz)
+    if (reinterpret_cast<uintptr_t>(dy) % ysz || reinterpret_cast<uintptr_t>(dx) % xsz ||
+        !direct_aligned(plan, {dy, dx}))
         return RUBICONV_ERR_ARG;
     if (!plan->device_ready) return RUBICONV_ERR_HIP;
     std::lock_guard<std::mutex> lock(plan->launch_mu);
@@ -797,9 +837,7 @@ rubiconv_status_t rubiconv_packed_conv_dx(rubiconv_plan_t plan, const void* dy, 
     hipError_t e = hipSuccess;
     if (direct)
         e = fork_direct(plan, stream, rec, "dx_direct", [&](hipStream_t s) {
-            return rubiconv::launch_direct(1, h.direct_max, h.y_dtype, dy, 0, nullptr, direct_taps(plan, spectrum),
-                                           plan->direct_segs, static_cast<int>(h.direct_docs.size()),
-                                           h.N, h.D, h.L, h.x_dtype, dx, s);
+            return direct_sums(plan, 1, h.y_dtype, dy, 0, nullptr, direct_taps(plan, spectrum), h.x_dtype, dx, s);
         });
     // dy is prescaled by a power of two from its largest magnitude (upstream gradients are
     // often far below 1), the filter by its per-pair scale.  On the matrix-core path the
@@ -835,7 +873,7 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
     const size_t xsz = h.x_dtype == RUBICONV_F32 ? 4 : 2;
     const size_t ysz = h.y_dtype == RUBICONV_F32 ? 4 : 2;
     if (reinterpret_cast<uintptr_t>(x) % xsz || reinterpret_cast<uintptr_t>(dy) % ysz ||
-        reinterpret_cast<uintptr_t>(dk) % 4)
+        reinterpret_cast<uintptr_t>(dk) % 4 || !direct_aligned(plan, {x, dy}))
         return RUBICONV_ERR_ARG;
     // the x grid doubles as the "filter" grid: its offsets must fit the 32-bit field
     if (h.grid_points + h.grid_points_lr > INT32_MAX) return RUBICONV_ERR_UNSUPPORTED;
@@ -852,9 +890,7 @@ rubiconv_status_t rubiconv_packed_conv_dk(rubiconv_plan_t plan, const void* x, c
     hipError_t e = hipSuccess;
     if (direct)
         e = fork_direct(plan, stream, rec, "dk_direct", [&](hipStream_t s) {
-            return rubiconv::launch_direct(2, h.direct_max, h.y_dtype, dy, h.x_dtype, x, nullptr, plan->direct_segs,
-                                           static_cast<int>(h.direct_docs.size()), h.N, h.D, h.L, 0,
-                                           r, s);
+            return direct_sums(plan, 2, h.y_dtype, dy, h.x_dtype, x, nullptr, 0, r, s);
         });
     // range: x and dy prescaled by powers of two from their largest magnitudes, and
     // together by 2^-ceil(log2 P_max) (half on each side), as a correlation sums up to P
@@ -935,7 +971,8 @@ rubiconv_status_t rubiconv_packed_conv_backward(rubiconv_plan_t plan, const void
     const size_t xsz = h.x_dtype == RUBICONV_F32 ? 4 : 2;
     const size_t ysz = h.y_dtype == RUBICONV_F32 ? 4 : 2;
     if (reinterpret_cast<uintptr_t>(x) % xsz || reinterpret_cast<uintptr_t>(dy) % ysz ||
-        reinterpret_cast<uintptr_t>(dx) % xsz || reinterpret_cast<uintptr_t>(dk) % 4)
+        reinterpret_cast<uintptr_t>(dx) % xsz || reinterpret_cast<uintptr_t>(dk) % 4 ||
+        !direct_aligned(plan, {x, dy, dx}))
         return RUBICONV_ERR_ARG;
     if (!plan->device_ready) return RUBICONV_ERR_HIP;
     if (!backward_fusable(h)) {
@@ -957,14 +994,9 @@ rubiconv_status_t rubiconv_packed_conv_backward(rubiconv_plan_t plan, const void
     const bool direct = !h.direct_docs.empty();
     if (direct)
         e = fork_direct(plan, stream, rec, "bwd_direct", [&](hipStream_t s) {
-            hipError_t de = rubiconv::launch_direct(1, h.direct_max, h.y_dtype, dy, 0, nullptr,
-                                                    direct_taps(plan, spectrum), plan->direct_segs,
-                                                    static_cast<int>(h.direct_docs.size()), h.N, h.D, h.L,
-                                                    h.x_dtype, dx, s);
-            if (de == hipSuccess)
-                de = rubiconv::launch_direct(2, h.direct_max, h.y_dtype, dy, h.x_dtype, x, nullptr,
-                                             plan->direct_segs, static_cast<int>(h.direct_docs.size()), h.N,
-                                             h.D, h.L, 0, r, s);
+            hipError_t de = direct_sums(plan, 1, h.y_dtype, dy, 0, nullptr, direct_taps(plan, spectrum), h.x_dtype,
+                                        dx, s);
+            if (de == hipSuccess) de = direct_sums(plan, 2, h.y_dtype, dy, h.x_dtype, x, nullptr, 0, r, s);
             return de;
         });
     // range: dy's grid carries dx's scale s_dy (its magnitude alone); x's carries s_x ex

@@ -312,3 +312,25 @@ def test_buffer_sizes_cover_the_layouts():
     # workspace holds at least the complex fp32 document grid of every pair block
     assert plan.workspace_bytes >= npb * 16 * 8 * info["grid_points"]
     assert plan.workspace_bytes % 256 == 0 and plan.spectrum_bytes % 256 == 0
+
+
+def test_direct_path_defaults(monkeypatch):
+    """The direct path runs on the matrix cores for bf16 plans with whole 32-channel
+    blocks, for documents of up to 512 tokens, when together they hold at least 1/16 of
+    the transform grid: the LM-packing workload's short documents take it, the mid-length
+    workload's two short ones do not.  RUBICONV_DIRECT_MFMA = 0 returns to the VALU
+    kernel's 64-token limit, and a limit above 512 is refused."""
+    def info(i):
+        cu = wl.config_cu_seqlens(i)
+        D, L, dt = wl.CONFIG_SHAPES[i]
+        return rc.Plan(cu, N=int(cu[0, -1]), D=D, L=L, x_dtype=dt).info()
+    c1 = info(1)
+    assert c1["direct_max"] == 512 and c1["n_direct"] > 20
+    assert info(2)["n_direct"] == 0
+    monkeypatch.setenv("RUBICONV_DIRECT_MFMA", "0")
+    assert info(1)["direct_max"] in (0, 64)
+    monkeypatch.setenv("RUBICONV_DIRECT_MFMA", "1")
+    monkeypatch.setenv("RUBICONV_DIRECT_MAX", "513")
+    with pytest.raises(rc.RubiconvError) as e:
+        info(1)
+    assert e.value.status == 1

@@ -136,6 +136,7 @@ def test_gradients_unlisted_row_sizes(device, monkeypatch):
     row kernels take as they are (RUBICONV_EXACT_ROWS = 1), for the forward, dx and dk:
     every size its own class, a 7-tap filter so that a document of 256 (k - 1) + 3
     tokens takes m = k."""
+    monkeypatch.setenv("RUBICONV_DIRECT_MAX", "0")   # every document on the transform path
     import paper_2605_08451_amd as rc
     monkeypatch.setenv("RUBICONV_CLASS_MERGE", "0")
     monkeypatch.setenv("RUBICONV_EXACT_ROWS", "1")
@@ -186,11 +187,12 @@ def test_gradients_deterministic(device):
     np.testing.assert_array_equal(a[2], b[2])
 
 
-def test_class_groups(device):
+def test_class_groups(device, monkeypatch):
     """Size classes holding one to ten documents: the matrix-core row kernels take a
     class's documents in groups of at most four sharing one filter-row transform (ten
     documents: groups of 4, 3 and 3), for short rows, 17-32-point rows and the partner
     kernel; the forward, dx and dk (whose tasks keep one document each) meet the bar."""
+    monkeypatch.setenv("RUBICONV_DIRECT_MAX", "0")   # every document on the transform path
     import paper_2605_08451_amd as rc
     import torch
     N = 8192
@@ -217,13 +219,14 @@ def test_class_groups(device):
 
 
 @pytest.mark.parametrize("D", [32, 64])
-def test_filter_gradient_sum_groups(device, D):
+def test_filter_gradient_sum_groups(device, D, monkeypatch):
     """The filter gradient adds the correlation products of a size class's documents
     (up to eight, longest first) before one inverse transform: classes whose documents
     differ in length, with the longest neither first nor last in its row, classes of
     more than eight documents (several groups), a class of one document, short rows
     (8-16 points) and partner-kernel rows (33-128 points); every lag of dk against the
     oracle, per channel."""
+    monkeypatch.setenv("RUBICONV_DIRECT_MAX", "0")   # every document on the transform path
     N = 12000
     rows = [[930, 1000, 960, 880, 990, 940, 905, 870, 1000, 975, N - 9450],
             [3000, 3100, 2950, 2900, N - 11950],
@@ -248,6 +251,7 @@ def test_batched_short_rows(device, rows, monkeypatch):
     partial blocks, a class of one document, rows of one point, and row 0 (one
     document per block); forward, dx and dk.  Slots past a block's documents must
     not read stale exchange values (a non-finite one would spread over its pair)."""
+    monkeypatch.setenv("RUBICONV_DIRECT_MAX", "0")   # every document on the transform path
     import paper_2605_08451_amd as rc
     monkeypatch.setenv("RUBICONV_ROW_BATCH", "8")   # whatever share these rows hold
     W = wl.make_case(rows, D=32, L=2048, x_dtype="bf16", seed=sum(rows[0]))

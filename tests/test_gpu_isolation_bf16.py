@@ -108,6 +108,37 @@ def test_impulse_isolation_forward_and_dx(device, monkeypatch, D, L):
                 assert leak <= 1e-6 * peak, (name, b, s0, s1, t, leak, peak)
 
 
+def test_impulse_isolation_direct_path(device, monkeypatch):
+    """The same impulses with the documents of up to 512 tokens on the direct path on the
+    matrix cores (RUBICONV_DIRECT_MAX = 512): y, dx and dk stay inside their documents."""
+    monkeypatch.setenv("RUBICONV_DIRECT_MAX", "512")
+    D = 32
+    c = _Case(device, D, N, seed=11)
+    info = c.plan.info()
+    assert info["n_direct"] == sum(1 for r in ROWS for n in r if n <= 512)
+    for (b, s0, s1) in _docs(c.cu):
+        if b != 1:
+            continue
+        t = (s0 + s1) // 2
+        v = np.zeros((c.plan.B, N, D), dtype=np.float32)
+        v[b, t, :] = c.rng.standard_normal(D).astype(np.float32) + 2.0
+        inside = np.zeros(v.shape, dtype=bool)
+        inside[b, s0:s1] = True
+        for name, out in (("y", c.forward(v)), ("dx", c.dx(v))):
+            assert np.isfinite(out).all(), (name, b, s0, s1, t)
+            peak = np.abs(out[inside]).max()
+            assert peak > 0, (name, b, s0, s1, t)
+            assert np.abs(out[~inside]).max() <= 1e-6 * peak, (name, b, s0, s1, t)
+        x = np.zeros((c.plan.B, N, D), dtype=np.float32)
+        x[b, s0:s1] = c.rng.standard_normal((s1 - s0, D)).astype(np.float32)
+        dy = c.rng.standard_normal((c.plan.B, N, D)).astype(np.float32)
+        full = c.dk(x, dy)
+        dy[b, s0:s1] = 0.0
+        other = c.dk(x, dy)
+        peak = np.abs(full).max()
+        assert peak > 0 and np.abs(other).max() <= 1e-6 * peak, (b, s0, s1)
+
+
 def test_dk_isolation(device, monkeypatch):
     """x in one document only and dy in every other one: the filter gradient is exactly
     zero (no document's correlation sees another's tokens); with dy everywhere it is not."""

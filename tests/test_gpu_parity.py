@@ -12,7 +12,7 @@ import pytest
 import oracle
 import workloads as wl
 from tests.common import (ORACLE_THREADS, TOL, assert_parity, parity_report, reference,
-                          run_gpu, to_device)
+                          rel_l2, run_gpu, to_device)
 
 pytestmark = pytest.mark.gpu
 
@@ -171,9 +171,10 @@ def test_plan_reused_with_two_filters(device):
 
 @pytest.mark.parametrize("D", [32, 96])
 @pytest.mark.parametrize("y_dtype", ["bf16", "f32"])
-def test_matrix_core_column_path(device, D, y_dtype):
+def test_matrix_core_column_path(device, D, y_dtype, monkeypatch):
     """bf16 inputs with whole 32-channel blocks take the matrix-core column passes:
     documents of length 1, N1 - 1, N1, N1 + 1, whole rows, short and long filters."""
+    monkeypatch.setenv("RUBICONV_DIRECT_MAX", "0")   # every document on the transform path
     rng = np.random.default_rng(D)
     N = 3000
     rows = [[N], [1, 255, 256, 257, 1, 2230], wl.random_rows(rng, 1, N, 700, p_short=0.4)[0]]
@@ -189,6 +190,7 @@ def test_row_pass_every_block_count(device, D, monkeypatch):
     matrix-core block count (m <= 16, 17..32, ..., 113..128, at and next to the block
     edges) and the register-resident sizes above it (135, 160, 256).  A length of
     128 m needs exactly m grid columns at N1 = 256."""
+    monkeypatch.setenv("RUBICONV_DIRECT_MAX", "0")   # every document on the transform path
     rows = [[32768],
             [20480, 12288],
             [17280, 12800, 2304, 384],
@@ -233,6 +235,7 @@ def test_row_kernel_sizes_precision(device, family, monkeypatch):
     33..128 points (row_partner_kernel), every size as its own class: 2^a 3^b 5^c sizes
     and, with rows at their own sizes (RUBICONV_EXACT_ROWS = 1), the others (primes among
     them), which these kernels take as they are."""
+    monkeypatch.setenv("RUBICONV_DIRECT_MAX", "0")   # every document on the transform path
     monkeypatch.setenv("RUBICONV_CLASS_MERGE", "0")
     monkeypatch.setenv("RUBICONV_EXACT_ROWS", "1")
     n1 = 256
@@ -284,6 +287,55 @@ def test_direct_path_limits(device, monkeypatch, dtype):
         assert_parity(dx, oracle.grad_x(W.filters, dyv, W.cu_seqlens), W.cu_seqlens, dtype,
                       f"dx limit {limit}")
         tg._check_dk(dk, oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L), dtype, f"limit {limit}")
+
+
+@pytest.mark.parametrize("limit", [64, 300, 512])
+def test_direct_path_on_matrix_cores(device, monkeypatch, limit):
+    """The direct path on the matrix cores (RUBICONV_DIRECT_MFMA=1): documents up to the
+    limit by blocked Toeplitz products, whole 16-token blocks and ragged ones, one token,
+    documents longer than the filter (L = 500) and transformed documents beside them; the
+    forward, both gradients and the fused backward meet the oracle bar, and the direct
+    documents reach it with room to spare (their sums run in fp32 with the taps in two
+    bf16 parts)."""
+    import torch
+    import paper_2605_08451_amd as rc
+    import tests.test_gpu_grad as tg
+    monkeypatch.setenv("RUBICONV_DIRECT_MFMA", "1")
+    monkeypatch.setenv("RUBICONV_DIRECT_MAX", str(limit))
+    N = 4096
+    rows = [[1, 15, 16, 17, 31, 33, 100, 255, 256, 257, 700, 1024], [64, 300, 500, 501, 1000], [N]]
+    for r in rows[:2]:
+        r.append(N - sum(r))
+    W = wl.make_case(rows, D=64, L=500, x_dtype="bf16", seed=limit)
+    ref = reference(W)
+    y, plan = run_gpu(W, device)
+    info = plan.info()
+    assert info["direct_max"] == limit
+    assert info["n_direct"] == sum(1 for r in rows for n in r if 0 < n <= limit)
+    g, d = assert_parity(y, ref, W.cu_seqlens, "bf16", f"limit {limit}")
+    # the direct documents alone: fp32 sums of exact bf16 products (taps split in two)
+    worst = 0.0
+    for b, r in enumerate(rows):
+        s0 = 0
+        for n in r:
+            if 0 < n <= limit:
+                worst = max(worst, rel_l2(y[b, s0:s0 + n], ref[b, s0:s0 + n]))
+            s0 += n
+    assert worst <= 3e-3, worst  # the bf16 rounding of y alone is about 1.6e-3
+    dyv, dx, dk, _ = tg._run(W, device, seed=limit + 7)
+    refx = oracle.grad_x(W.filters, dyv, W.cu_seqlens)
+    refk = oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L)
+    assert_parity(dx, refx, W.cu_seqlens, "bf16", f"dx limit {limit}")
+    tg._check_dk(dk, refk, "bf16", f"dk limit {limit}")
+    x, k = to_device(W, device)
+    dy = torch.from_numpy(wl.f32_to_bf16_bits(dyv.astype(np.float32)).view(np.int16)).view(
+        torch.bfloat16).to(device)
+    p2 = rc.Plan(W.cu_seqlens, N=W.N, D=W.D, L=W.L, x_dtype="bf16")
+    dxf, dkf = rc.packed_conv_backward(p2, x, dy, rc.filter_spectrum(p2, k))
+    assert_parity(dxf.float().cpu().numpy().astype(np.float64), refx, W.cu_seqlens, "bf16", "fused dx")
+    tg._check_dk(dkf.cpu().numpy().astype(np.float64), refk, "bf16", "fused dk")
+    print(f"[direct mfma] limit {limit}: y {g:.2e} / {d:.2e}, direct documents {worst:.2e}",
+          file=sys.stderr, flush=True)
 
 
 def test_plan_and_calls_on_a_side_stream(device):
