@@ -109,13 +109,17 @@ typedef enum {
  *   n1              column size N1 of the grid (the paper's k): 0 picks the
  *                   default (256); otherwise 64 or 256.
  *
- * Documents of at most 64 tokens take the direct path when together they would
- * fill at least 1/16 of the transform grid: they skip the transforms, and their
- * outputs are the defining sums of the block-diagonal Toeplitz form (Section 3.2)
- * evaluated directly, which avoids padding a short document to a whole N1-point
- * column grid.  The environment variable RUBICONV_DIRECT_MAX = 0..128, read when
- * the plan is made, sets the length limit and drops the share condition (0 turns
- * the path off).
+ * Documents of at most 64 tokens (512 with bf16 x and y and D a multiple of 32)
+ * take the direct path when together they would fill at least 1/16 of the
+ * transform grid: they skip the transforms, and their outputs are the defining sums
+ * of the block-diagonal Toeplitz form (Section 3.2) evaluated directly, which avoids
+ * padding a short document to a whole N1-point column grid.  With bf16 x and y and D
+ * a multiple of 32 those sums run on the matrix cores as blocked Toeplitz products
+ * (fp32 accumulation), and every x, y, dy and dx buffer passed with the plan must be
+ * 16-byte aligned (RUBICONV_ERR_ARG otherwise); RUBICONV_DIRECT_MFMA = 0, read when the
+ * plan is made, keeps them on the 64-token VALU kernel.  RUBICONV_DIRECT_MAX = 0..128
+ * (0..512 on the matrix cores), read when the plan is made, sets the length limit and
+ * drops the share condition (0 turns the path off).
  * Documents whose smallest transform sizes differ little may share one size class:
  * a document then takes a larger transform than its own minimum (any transform
  * holding the causal padding gives the same exact result, Theorem 2.1), when that
@@ -145,7 +149,7 @@ typedef enum {
  * order with other device work);
  * it does not wait for the upload.
  * Errors: RUBICONV_ERR_ARG (also for a malformed RUBICONV_DIRECT_MAX,
- * RUBICONV_CLASS_MERGE or RUBICONV_PRESCALE),
+ * RUBICONV_DIRECT_MFMA, RUBICONV_CLASS_MERGE or RUBICONV_PRESCALE),
  * RUBICONV_ERR_SEQLENS, RUBICONV_ERR_UNSUPPORTED (n1 not supported, a document
  * so long that its row DFT would exceed the largest supported size, or a shape whose
  * kernels would need buffer offsets of 32 bits or more: a document's or size
