@@ -338,6 +338,29 @@ def test_direct_path_on_matrix_cores(device, monkeypatch, limit):
           file=sys.stderr, flush=True)
 
 
+@pytest.mark.parametrize("L,D", [(20, 96), (512, 32)])
+def test_direct_path_filter_lengths(device, monkeypatch, L, D):
+    """The direct path on the matrix cores with a filter far shorter than its documents
+    (20 taps: every document longer than the filter reads zero taps past it) and with one
+    as long as the longest direct document, over six and two 16-channel groups: the
+    forward and both gradients meet the oracle bar on every document, direct or not."""
+    import tests.test_gpu_grad as tg
+    monkeypatch.setenv("RUBICONV_DIRECT_MFMA", "1")
+    monkeypatch.setenv("RUBICONV_DIRECT_MAX", "512")
+    N = 2048
+    rows = [[1, 19, 20, 21, 48, 511, 512, 513], [200, 17, 1000]]
+    for r in rows:
+        r.append(N - sum(r))
+    W = wl.make_case(rows, D=D, L=L, x_dtype="bf16", seed=L + D)
+    ref = reference(W)
+    y, plan = run_gpu(W, device)
+    assert plan.info()["n_direct"] == sum(1 for r in rows for n in r if 0 < n <= 512)
+    assert_parity(y, ref, W.cu_seqlens, "bf16", f"L {L} D {D}")
+    dyv, dx, dk, _ = tg._run(W, device, seed=L + D + 1)
+    assert_parity(dx, oracle.grad_x(W.filters, dyv, W.cu_seqlens), W.cu_seqlens, "bf16", f"dx L {L} D {D}")
+    tg._check_dk(dk, oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L), "bf16", f"dk L {L} D {D}")
+
+
 def test_plan_and_calls_on_a_side_stream(device):
     """A plan made on a side stream and used there at once (its tables' upload is
     enqueued on that stream, not waited for), with the spectrum, workspace and outputs
