@@ -343,7 +343,8 @@ def test_direct_path_filter_lengths(device, monkeypatch, L, D):
     """The direct path on the matrix cores with a filter far shorter than its documents
     (20 taps: every document longer than the filter reads zero taps past it) and with one
     as long as the longest direct document, over six and two 16-channel groups: the
-    forward and both gradients meet the oracle bar on every document, direct or not."""
+    forward and both gradients, alone and in one call, meet the oracle bar on every
+    document, direct or not."""
     import tests.test_gpu_grad as tg
     monkeypatch.setenv("RUBICONV_DIRECT_MFMA", "1")
     monkeypatch.setenv("RUBICONV_DIRECT_MAX", "512")
@@ -358,7 +359,19 @@ def test_direct_path_filter_lengths(device, monkeypatch, L, D):
     assert_parity(y, ref, W.cu_seqlens, "bf16", f"L {L} D {D}")
     dyv, dx, dk, _ = tg._run(W, device, seed=L + D + 1)
     assert_parity(dx, oracle.grad_x(W.filters, dyv, W.cu_seqlens), W.cu_seqlens, "bf16", f"dx L {L} D {D}")
-    tg._check_dk(dk, oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L), "bf16", f"dk L {L} D {D}")
+    refk = oracle.grad_k(W.x, dyv, W.cu_seqlens, W.L)
+    tg._check_dk(dk, refk, "bf16", f"dk L {L} D {D}")
+    # both gradients in one call
+    import torch
+    import paper_2605_08451_amd as rc
+    x, k = to_device(W, device)
+    dy = torch.from_numpy(wl.f32_to_bf16_bits(dyv.astype(np.float32)).view(np.int16)).view(
+        torch.bfloat16).to(device)
+    p2 = rc.Plan(W.cu_seqlens, N=W.N, D=W.D, L=W.L, x_dtype="bf16")
+    dxf, dkf = rc.packed_conv_backward(p2, x, dy, rc.filter_spectrum(p2, k))
+    assert_parity(dxf.float().cpu().numpy().astype(np.float64), oracle.grad_x(W.filters, dyv, W.cu_seqlens),
+                  W.cu_seqlens, "bf16", f"fused dx L {L} D {D}")
+    tg._check_dk(dkf.cpu().numpy().astype(np.float64), refk, "bf16", f"fused dk L {L} D {D}")
 
 
 def test_plan_and_calls_on_a_side_stream(device):
